@@ -1,0 +1,83 @@
+"""Linear layers with bias and ReLU: the dense feature processor ("bottom"
+MLP, Section 3.3.1) and the task modules ("top" MLP with one output per
+objective, Section 3.3.3).
+
+Test infrastructure only (see the package docstring).
+
+Weights are ``[out, in]``.  Forward of one layer: ``a = h W^T + b``; a hidden
+layer stores ``rnd(max(a, 0))`` (its ReLU output at the storage precision); the
+last top layer returns the logits ``a`` unrounded.  Backward of one layer,
+given the gradient ``g`` of its output: ``dW = g^T h``, ``db = sum_b g``,
+``dh = g W``; the gradient reaching a hidden activation is masked by that
+activation being positive (ReLU) and stored as ``rnd(...)``.
+"""
+import numpy as np
+
+
+def linear(h, W, b):
+    return np.asarray(h, np.float64) @ np.asarray(W, np.float64).T + np.asarray(b, np.float64)
+
+
+def linear_grads(g, h, W):
+    """(dW, db, dh) of ``a = h W^T + b`` given ``g = dL/da``."""
+    g = np.asarray(g, np.float64)
+    h = np.asarray(h, np.float64)
+    return g.T @ h, g.sum(axis=0), g @ np.asarray(W, np.float64)
+
+
+def relu_band(h, W, b):
+    """Half-width of the band around zero inside which the sign of a
+    pre-activation is not fixed by fp32 accumulation: the worst-case error of
+    summing the ``K`` products plus the bias in any order in fp32,
+    ``K * 2^-24 * (sum_k |W_k h_k| + |b|)``."""
+    h = np.abs(np.asarray(h, np.float64))
+    K = h.shape[1]
+    return (K + 1) * 2.0 ** -24 * (h @ np.abs(np.asarray(W, np.float64)).T + np.abs(np.asarray(b, np.float64)))
+
+
+def mlp_forward(h0, layers, rnd, relu_last, overrides=None):
+    """Returns ``(hs, masks)``: the layer inputs/outputs ``[h0, h1, ..., hL]``
+    and, per layer, its ReLU decision (``None`` for a linear last layer).
+    Every layer but (optionally) the last applies ReLU and storage rounding.
+
+    ``overrides[i]``, when given, is ``(where, positive)``: at the positions in
+    ``where`` the ReLU of layer i takes the decision ``positive`` instead of
+    the sign of the float64 pre-activation.  Parity tests use it only inside
+    ``relu_band``, where either decision is a correct result of fp32
+    arithmetic."""
+    hs = [np.asarray(h0, np.float64)]
+    masks = []
+    for i, (W, b) in enumerate(layers):
+        a = linear(hs[-1], W, b)
+        last = i == len(layers) - 1
+        if relu_last or not last:
+            on = a > 0
+            if overrides is not None and overrides[i] is not None:
+                where, positive = overrides[i]
+                on = np.where(where, positive, on)
+            hs.append(rnd(np.where(on, np.maximum(a, 0.0), 0.0)))
+            masks.append(on)
+        else:
+            hs.append(a)
+            masks.append(None)
+    return hs, masks
+
+
+def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad):
+    """Backward through ``mlp_forward``.  ``g_out`` is dL/d(hs[-1]) (before the
+    last ReLU mask when ``relu_last``).  Returns (dWs, dbs, dL/dh0 or None)."""
+    L = len(layers)
+    g = np.asarray(g_out, np.float64)
+    if relu_last:
+        g = rnd(g * masks[-1])
+    dWs, dbs = [None] * L, [None] * L
+    dh0 = None
+    for i in range(L - 1, -1, -1):
+        W, _ = layers[i]
+        dW, db, dh = linear_grads(g, hs[i], W)
+        dWs[i], dbs[i] = dW, db
+        if i > 0:
+            g = rnd(dh * masks[i - 1])
+        elif need_input_grad:
+            dh0 = dh
+    return dWs, dbs, dh0
