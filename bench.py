@@ -1,0 +1,220 @@
+#!/usr/bin/env python3
+"""Benchmark of one training step of the Lattice Network's sparse-dense core
+on one MI355X.
+
+A step is one call of lattice_step on one batch: pooled lookups, bottom MLP,
+FM interaction, top MLP, masked BCE, full backward, row-coalesced embedding
+gradient and row-sparse SGD on the tables.  Default workload: B=8192, 64
+tables of 2,000,000 x 128 bf16 (Zipf 1.05 indices, Poisson(20) bags clipped to
+[1,128]), dense 64 -> 512 -> 128, FM over 65 vectors with rank 32, top
+2208 -> 1024 -> 512 -> 16, 50% masked heads, SGD lr 0.01 on the tables.
+Inputs are seeded and synthetic and resident in HBM before timing starts.
+
+Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFS = 2516.6    # MI355X dense bf16 MFMA, TFLOP/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cfg", type=int, default=3)
+    ap.add_argument("--batches", type=int, default=2, help="distinct batches cycled")
+    ap.add_argument("--cpu-sample", type=int, default=2048, help="samples in the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--uniform", action="store_true", help="uniform indices (control run)")
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def mlp_fwd_flops(dims, B):
+    return sum(2.0 * B * dims[i] * dims[i + 1] for i in range(len(dims) - 1))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the path has no multi-GPU sharding in this build)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2512_09200_amd import api
+    from paper_2512_09200_amd._abi import STAGES
+
+    cfg = synth.CONFIGS[args.cfg]
+    if args.uniform:
+        cfg = cfg.scaled(index_dist=("uniform",))
+    dev = "cuda"
+    sdt = synth.torch_dtype(cfg.dtype)
+    t0 = time.time()
+    log(f"[bench] {cfg.name}: generating {args.batches} batches")
+    batches = []
+    for i in range(args.batches):
+        b = synth.make_batch(cfg, i)
+        batches.append(dict(
+            np=b, offsets=torch.from_numpy(b["offsets"]).to(dev),
+            indices=torch.from_numpy(b["indices"]).to(dev),
+            dense=torch.from_numpy(b["dense"]).to(sdt).to(dev),
+            labels=torch.from_numpy(b["labels"]).to(dev), mask=torch.from_numpy(b["mask"]).to(dev),
+            nnz=int(b["offsets"][-1])))
+    row_base = torch.from_numpy(batches[0]["np"]["row_base"]).to(dev)
+    log(f"[bench] batches ready ({time.time() - t0:.1f}s); generating tables")
+    E = synth.make_tables(cfg, device=dev)
+    p = synth.make_dense_params(cfg)
+
+    def lin(W, b):
+        return dict(W=torch.from_numpy(W).to(sdt).to(dev), b=torch.from_numpy(b).to(dev),
+                    dW=torch.empty(W.shape, device=dev), db=torch.empty(b.shape, device=dev))
+
+    bottom = [lin(W, b) for W, b in p["bottom"]]
+    top = [lin(W, b) for W, b in p["top"]]
+    fm_W = torch.from_numpy(p["fm_W"]).to(sdt).to(dev) if "fm_W" in p else None
+    fm_dW = torch.empty(tuple(fm_W.shape), device=dev) if fm_W is not None else None
+    model = api.StepModel(tables=E, row_base=row_base, num_features=cfg.F, dense_in=cfg.dense_in,
+                          bottom=bottom, top=top, interact=cfg.interact, fm_W=fm_W, fm_dW=fm_dW,
+                          pool=cfg.pool)
+    nnz_max = max(b["nnz"] for b in batches)
+    lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False)
+    ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident ({time.time() - t0:.1f}s); workspace {lay.total_bytes / 2**30:.2f} GiB")
+
+    def step(i, events=None):
+        b = batches[i % len(batches)]
+        api.lattice_step(model, b["offsets"], b["indices"], b["dense"], b["labels"], b["mask"], ws,
+                         cfg.lr_tables, False, stage_events=events, nnz_capacity=nnz_max)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+
+    nst = len(STAGES)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(args.steps)]
+    for es in ev:          # create the underlying events before handing them to the library
+        for e in es:
+            e.record()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, ev[i])
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t_start
+    ms_per_step = 1e3 * t_total / args.steps
+    stage_ms = {s: float(np.mean([ev[i][k].elapsed_time(ev[i][k + 1]) for i in range(args.steps)]))
+                for k, s in enumerate(STAGES)}
+    log("[bench] stage ms: " + ", ".join(f"{k}={v:.3f}" for k, v in stage_ms.items()))
+
+    # ---- algorithmic work -------------------------------------------------
+    es = 2 if cfg.dtype == "bf16" else 4
+    nnz = float(np.mean([b["nnz"] for b in batches]))
+    bags = cfg.F * cfg.B
+    row_bytes = cfg.d * es
+    fwd_bytes = nnz * (row_bytes + 4) + bags * 4 + bags * cfg.d * es
+    # unique rows of the last batch used (read back outside the timed region)
+    v = api.step_views(model, ws, lay, cfg.B, cfg.T, nnz_max)
+    U = int(v["num_unique"].item())
+    bwd_bytes = nnz * (cfg.d * es + 4) + bags * 4 + (U * 2 * row_bytes if cfg.lr_tables else U * (4 * cfg.d + 4))
+    fwd_gbs = fwd_bytes / (stage_ms["embbag_fwd"] * 1e-3) / 1e9
+    bwd_gbs = bwd_bytes / (stage_ms["embbag_bwd"] * 1e-3) / 1e9
+    n = cfg.n_slots
+    flops_fwd = mlp_fwd_flops((cfg.dense_in,) + tuple(cfg.bottom), cfg.B) if cfg.has_dense else 0.0
+    flops_fwd += mlp_fwd_flops((cfg.top_in,) + tuple(cfg.top), cfg.B)
+    if cfg.interact == "fm":
+        flops_fwd += 4.0 * cfg.B * n * cfg.d * cfg.fm_rank
+    elif cfg.interact == "dot":
+        flops_fwd += 2.0 * cfg.B * cfg.n_pairs * cfg.d
+    dense_stages = ["bottom_fwd", "interact_fwd", "top_fwd", "top_bwd", "interact_bwd", "bottom_bwd"]
+    dense_ms = sum(stage_ms[s] for s in dense_stages)
+    mfma_tfs = 3.0 * flops_fwd / (dense_ms * 1e-3) / 1e12
+    samples_per_s = cfg.B / (ms_per_step * 1e-3)
+
+    roofline = {"bound": "hbm", "kernel": "embbag_fwd_kernel", "achieved": round(fwd_gbs, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(fwd_gbs / HBM_PEAK_GBS, 4),
+                "traffic": None,
+                "bytes_per_launch": int(fwd_bytes), "launch_ms": round(stage_ms["embbag_fwd"], 4)}
+
+    # ---- CPU baseline: the oracle on a bounded sample of the same workload ----
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, batches[0]["np"], p, E, args.cpu_sample)
+
+    out = {
+        "metric": "train samples/s (fwd+bwd) at 1 GPU; EmbBag HBM GB/s and interaction MFMA util",
+        "value": round(samples_per_s, 1), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
+        "data": "synthetic (seeded; Zipf/Poisson jagged batches, random-init weights)",
+        "config": {"workload": cfg.name, "global_batch": cfg.B, "features": cfg.F,
+                   "rows_per_table": cfg.rows, "dim": cfg.d,
+                   "index_dist": list(cfg.index_dist), "bag_dist": list(cfg.bag_dist),
+                   "interaction": cfg.interact, "top": list(cfg.top), "lr_tables": cfg.lr_tables,
+                   "nnz_per_step": int(nnz), "unique_rows_last_step": U, "parallelism": "single-gpu"},
+        "roofline": roofline,
+        "embbag_fwd_GBps": round(fwd_gbs, 1), "embbag_bwd_GBps": round(bwd_gbs, 1),
+        "embbag_fwd_hbm_frac": round(fwd_gbs / HBM_PEAK_GBS, 4),
+        "embbag_bwd_hbm_frac": round(bwd_gbs / HBM_PEAK_GBS, 4),
+        "interaction_mlp_TFLOPs": round(mfma_tfs, 1),
+        "interaction_mlp_mfma_frac": round(mfma_tfs / MFMA_BF16_PEAK_TFS, 4),
+        "stage_ms": {k: round(x, 4) for k, x in stage_ms.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, batch, params, E, n_samples):
+    """Times the CPU oracle (as it stands) on the first n_samples samples of
+    the batch, with the touched table rows copied to host memory."""
+    import numpy as np
+    import torch
+
+    import synth
+    from oracle import step as ostep
+
+    Bs = min(n_samples, cfg.B)
+    scfg, sub, rows = synth.sub_batch(cfg, batch, np.arange(Bs))
+    table = E[torch.from_numpy(rows).to(E.device)].float().cpu().double().numpy()
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 0) for i in threadpool_info()), default=None)
+    except Exception:
+        pass
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    t = time.perf_counter()
+    ostep.step(scfg, params, table, sub)
+    dt = time.perf_counter() - t
+    return {"value": round(Bs / dt, 3), "unit": "samples/s", "cores": threads or os.cpu_count(),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"first {Bs} of {cfg.B} samples of batch 0 (all {cfg.F} features, "
+                      f"{int(sub['offsets'][-1])} lookups, {rows.size} touched rows), fwd+bwd+SGD "
+                      "in float64 numpy", "cpu_model": cpu_model, "nproc": os.cpu_count()}
+
+
+if __name__ == "__main__":
+    main()

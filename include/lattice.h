@@ -1,0 +1,339 @@
+/*
+ * lattice.h -- C ABI of the MI355X (gfx950) training-step library for the
+ * sparse-dense core of the Lattice Network (Meta Lattice, arXiv 2512.09200).
+ *
+ * One training step of that core is: pooled embedding lookups over jagged
+ * multi-hot categorical features (Section 3.3.1), the dense-feature MLP
+ * (Section 3.3.1), the pairwise feature interaction -- dot-product Gram, the
+ * factorization-machine block, or a stack of FM blocks with linear
+ * compression, residual and LayerNorm (the DHEN/Wukong fusion block,
+ * Section 3.3.2) -- the task modules with one logit per objective
+ * (Section 3.3.3), the masked multi-objective loss (impressions train only
+ * their routed heads, Section 3.2.1), and the backward pass including the
+ * row-coalesced embedding gradient and a row-sparse SGD update of the tables.
+ *
+ * Conventions shared by every entry point
+ *  - Pointers are DEVICE pointers unless marked "host".  Every buffer is owned
+ *    by the caller; the library never allocates or frees device memory.
+ *    Scratch memory is a caller-provided workspace whose size the matching
+ *    *_workspace / lattice_step_plan call reports.
+ *  - Layouts are row-major and contiguous unless a row stride (in elements)
+ *    is given.  Weights are [out, in].
+ *  - Storage dtype: LATTICE_F32 keeps every tensor in fp32.  LATTICE_BF16
+ *    stores tables, weights, activations and activation gradients (all GEMM
+ *    operands) in bf16, rounded to nearest even from fp32 accumulators;
+ *    biases, LayerNorm gains, logits, the loss and all parameter gradients are
+ *    fp32 (mixed precision with bf16 GEMMs and fp32 normalisation,
+ *    Section 3.5.2).
+ *  - `stream` is a hipStream_t (NULL = default stream).  All work is enqueued
+ *    on it in order; nothing synchronises except lattice_validate_batch.
+ *  - Results are deterministic: identical inputs give bitwise-identical
+ *    outputs (no floating-point atomics anywhere).
+ *  - Every function returns a lattice_status; nothing aborts or prints.
+ *    Arguments are checked before anything is launched; on failure
+ *    lattice_last_error() holds a message (thread-local).  The hot path does
+ *    NOT bounds-check embedding indices: out-of-range indices give undefined
+ *    results; lattice_validate_batch checks a batch.
+ *  - B = 0 or nnz = 0 are valid and produce the mathematically defined
+ *    (zero / empty) results.
+ */
+#ifndef LATTICE_H_
+#define LATTICE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LATTICE_ABI_VERSION 1
+#define LATTICE_MAX_LAYERS 8
+
+typedef enum {
+  LATTICE_OK = 0,
+  LATTICE_ERR_INVALID_ARG = 1,  /* null pointer, negative or inconsistent size */
+  LATTICE_ERR_UNSUPPORTED = 2,  /* valid but not supported (dim, dtype, size limits) */
+  LATTICE_ERR_WORKSPACE = 3,    /* workspace too small */
+  LATTICE_ERR_BAD_INPUT = 4,    /* malformed batch (lattice_validate_batch) */
+  LATTICE_ERR_HIP = 5           /* a HIP call or kernel launch failed */
+} lattice_status;
+
+typedef enum { LATTICE_F32 = 0, LATTICE_BF16 = 1 } lattice_dtype;
+typedef enum { LATTICE_POOL_SUM = 0, LATTICE_POOL_MEAN = 1 } lattice_pool;
+typedef enum {
+  LATTICE_INTERACT_DOT = 0,    /* pairwise dot products, strict upper triangle */
+  LATTICE_INTERACT_FM = 1,     /* factorization-machine block X (X^T W) */
+  LATTICE_INTERACT_STACK = 2   /* stacked FM -> linear -> residual -> LayerNorm */
+} lattice_interact_kind;
+
+/* ------------------------------------------------------------------------ */
+/* Jagged categorical batch and embedding tables (Section 3.3.1)            */
+/* ------------------------------------------------------------------------ */
+
+/* Feature-major jagged batch: bag f*B+b holds the indices of feature f for
+ * sample b at positions offsets[f*B+b] .. offsets[f*B+b+1]-1.  Indices are
+ * table-local row ids.  An empty bag is a feature the record does not carry
+ * (zero-padded in the unified dataset, Section 3.2) and pools to zero. */
+typedef struct {
+  int32_t num_features;     /* F >= 0 */
+  int32_t batch;            /* B >= 0 */
+  const int32_t* offsets;   /* device [F*B+1], offsets[0] = 0, non-decreasing */
+  const int32_t* indices;   /* device [nnz] */
+  int64_t nnz;              /* host copy of offsets[F*B]; < 2^31 */
+} lattice_jagged;
+
+/* All tables stacked in one buffer; table f occupies global rows
+ * row_base[f] .. row_base[f+1]-1.  Embedding dimension d is uniform across
+ * features (Section 3.3.1). */
+typedef struct {
+  void* data;                /* device [total_rows, dim], dtype */
+  lattice_dtype dtype;
+  int32_t dim;               /* d: multiple of 8 (bf16) or 4 (fp32), <= 256 */
+  int64_t total_rows;        /* < 2^31 */
+  const int64_t* row_base;   /* device [F+1] */
+} lattice_tables;
+
+/* Pooled lookup: X[b, first_slot+f, :] = sum (or mean) over j in bag(f,b) of
+ * table row row_base[f] + indices[j], accumulated in fp32, stored in x_dtype.
+ * X is [B, n_slots, dim]; slots outside first_slot .. first_slot+F-1 are not
+ * touched.  Errors: INVALID_ARG (nulls, first_slot+F > n_slots), UNSUPPORTED
+ * (dim), HIP. */
+lattice_status lattice_embbag_fwd(const lattice_tables* tables, const lattice_jagged* bags,
+                                  lattice_pool pool, void* X, lattice_dtype x_dtype,
+                                  int32_t n_slots, int32_t first_slot, void* stream);
+
+/* Row-coalesced sparse gradient of the pooled lookup, deterministic
+ * (sort-by-row segmented reduction, no atomics). */
+typedef struct {
+  int32_t* unique_rows;  /* device [nnz]: global rows that occur, ascending; first *num_unique valid */
+  int32_t* seg_offsets;  /* device [nnz+1]: run start of each unique row in sorted order; [num_unique] = nnz */
+  int32_t* sorted_bags;  /* device [nnz]: bag id f*B+b of each occurrence, by (row, position) */
+  int32_t* num_unique;   /* device [1] */
+  float* grad_rows;      /* device [nnz, dim] fp32 or NULL: G[u] = sum of dX over row u's occurrences */
+} lattice_sparse_grad;
+
+size_t lattice_embbag_bwd_workspace(const lattice_tables* tables, const lattice_jagged* bags);
+
+/* G[u] = sum over occurrences j of global row unique_rows[u] of
+ * dX[b(j), first_slot+f(j), :] (divided by the bag length for mean pooling),
+ * summed in fp32 in a fixed order.  If lr != 0 the occurring rows of
+ * tables->data are updated in place: E[r] <- round(E[r] - lr * G[r]); other
+ * rows are untouched.  dX is [B, n_slots, dim] in dx_dtype.  Errors:
+ * INVALID_ARG, UNSUPPORTED (dim, total_rows >= 2^31), WORKSPACE, HIP. */
+lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_jagged* bags,
+                                  lattice_pool pool, const void* dX, lattice_dtype dx_dtype,
+                                  int32_t n_slots, int32_t first_slot,
+                                  const lattice_sparse_grad* out, float lr,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronous check of a batch against the tables: offsets[0] == 0,
+ * non-decreasing, offsets[F*B] == nnz, and 0 <= indices[j] < rows of its
+ * table.  Returns BAD_INPUT with *first_bad (host) = first bad offset
+ * position (as -1 - position) or first bad index position. */
+lattice_status lattice_validate_batch(const lattice_tables* tables, const lattice_jagged* bags,
+                                      int64_t* first_bad, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Interaction (Section 3.3.2)                                              */
+/* ------------------------------------------------------------------------ */
+
+/* One layer of the FM stack: F = X (X^T W) (rank k), H = A vec(F) reshaped
+ * to [n_out, dim] (no bias: bias-less backbone, Section 3.3.4), residual
+ * R = C X (C != NULL, a linear compression block) or R = X, output
+ * LayerNorm_gamma(H + R) per vector over dim (gain only, fp32 math). */
+typedef struct {
+  const void* W;        /* device [n_in, rank] */
+  const void* A;        /* device [n_out*dim, n_in*rank] */
+  const void* C;        /* device [n_out, n_in] or NULL (requires n_in == n_out) */
+  const float* gamma;   /* device [dim] */
+  float* dW;            /* device fp32 grads, same shapes (bwd) */
+  float* dA;
+  float* dC;
+  float* dgamma;
+} lattice_stack_layer;
+
+typedef struct {
+  lattice_interact_kind kind;
+  lattice_dtype dtype;
+  int32_t n;             /* vectors per sample entering the interaction */
+  int32_t dim;           /* d */
+  int32_t rank;          /* k (FM, STACK) */
+  int32_t emit_slot0;    /* DOT/FM: out row = [X[b,0,:], interaction] (dense vector first) */
+  const void* fm_W;      /* FM: device [n, rank] */
+  float* fm_dW;          /* FM: device [n, rank] fp32 (bwd) */
+  int32_t n_layers;      /* STACK: layers (<= LATTICE_MAX_LAYERS) */
+  int32_t stack_n;       /* STACK: vectors per layer output */
+  float ln_eps;          /* STACK: LayerNorm epsilon */
+  const lattice_stack_layer* layers;  /* host [n_layers] */
+} lattice_interact_desc;
+
+/* DOT: out[b, m(i,j)] = <X[b,i], X[b,j]> for i<j, m(i,j) row-major over the
+ * strict upper triangle.  FM: out[b] = vec_rowmajor(X_b (X_b^T W)), [n, k].
+ * STACK: out[b] = vec(X_{L+1}), [stack_n, dim].  X is [B, n, dim]; out rows
+ * have stride out_stride (elements) and start with X[b,0,:] when emit_slot0.
+ * The workspace holds what the backward needs (STACK) and must be passed
+ * unchanged to lattice_interact_bwd.  Errors: INVALID_ARG, UNSUPPORTED,
+ * WORKSPACE, HIP. */
+size_t lattice_interact_workspace(const lattice_interact_desc* desc, int32_t B);
+lattice_status lattice_interact_fwd(const lattice_interact_desc* desc, int32_t B, const void* X,
+                                    void* out, int64_t out_stride, void* ws, size_t ws_bytes,
+                                    void* stream);
+
+/* Gradient of lattice_interact_fwd: given d_out (same layout as out, storage
+ * dtype), writes dX [B, n, dim] (storage dtype; with emit_slot0 the slot-0
+ * part of d_out is added to dX[:,0,:] in fp32 before rounding) and the
+ * parameter gradients named in desc (fp32, overwritten, summed over the batch
+ * in a fixed order). */
+lattice_status lattice_interact_bwd(const lattice_interact_desc* desc, int32_t B, const void* X,
+                                    const void* d_out, int64_t d_out_stride, void* dX,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* MLPs and multi-objective heads (Sections 3.3.1, 3.3.3, 3.2.1)            */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  int32_t in_dim, out_dim;
+  const void* W;    /* device [out_dim, in_dim], storage dtype */
+  const float* b;   /* device [out_dim] or NULL */
+  float* dW;        /* device [out_dim, in_dim] fp32 (bwd, overwritten) */
+  float* db;        /* device [out_dim] fp32 or NULL (bwd, overwritten) */
+} lattice_linear;
+
+typedef struct {
+  lattice_dtype dtype;
+  int32_t n_layers;                 /* 1 .. LATTICE_MAX_LAYERS */
+  const lattice_linear* layers;     /* host [n_layers] */
+  int32_t relu_last;                /* 1: ReLU on every layer (bottom MLP);
+                                       0: last layer linear, fp32 output (heads) */
+} lattice_mlp_desc;
+
+/* Masked multi-objective BCE with logits z [B, T]: with N = max(1, sum m),
+ * loss = sum m*(max(z,0) - z*y + log1p(exp(-|z|))) / N and
+ * d_logits = m*(sigmoid(z) - y)/N, so masked heads get exactly zero. */
+typedef struct {
+  const float* labels;   /* device [B, T] */
+  const uint8_t* mask;   /* device [B, T], 0/1 */
+  float* loss;           /* device [1] */
+  float* d_logits;       /* device [B, T] fp32 */
+  void* d_logits_op;     /* device [B, T] storage dtype (backward GEMM operand) or NULL */
+} lattice_loss_desc;
+
+/* Workspace of lattice_mlp_heads_fwd and lattice_mlp_heads_bwd (the larger
+ * of the two). */
+size_t lattice_mlp_heads_workspace(const lattice_mlp_desc* desc, int32_t B);
+
+/* Forward: acts[i] (host array of device pointers) receives layer i's output
+ * [B, out_i] with row stride act_strides[i] (host array, elements): ReLU then
+ * storage rounding on hidden layers; fp32 logits on a linear last layer.  If
+ * loss != NULL the masked BCE is evaluated on the logits (which must then be
+ * contiguous, act_strides[last] == T).  `in` is [B, in_0] with row stride
+ * in_stride, storage dtype.  Errors: INVALID_ARG, WORKSPACE, HIP. */
+lattice_status lattice_mlp_heads_fwd(const lattice_mlp_desc* desc, int32_t B, const void* in,
+                                     int64_t in_stride, void* const* acts,
+                                     const int64_t* act_strides, const lattice_loss_desc* loss,
+                                     void* ws, size_t ws_bytes, void* stream);
+
+/* Backward: d_out is the gradient of the last layer's output (storage dtype;
+ * for relu_last the gradient of the post-ReLU output, masked here by
+ * acts[last] > 0).  Writes dW/db of every layer (fp32, overwritten, summed
+ * over the batch in a fixed order) and, if d_in != NULL, the input gradient
+ * [B, in_0] (stride d_in_stride, storage dtype, unmasked).  Errors:
+ * INVALID_ARG, WORKSPACE, HIP. */
+lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, const void* in,
+                                     int64_t in_stride, const void* const* acts,
+                                     const int64_t* act_strides, const void* d_out,
+                                     int64_t d_out_stride, void* d_in, int64_t d_in_stride,
+                                     void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Whole training step                                                      */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  lattice_dtype dtype;
+  lattice_pool pool;
+  lattice_tables tables;
+  int32_t num_features;        /* F */
+  int32_t dense_in;            /* dense inputs (0: no dense path, no bottom MLP) */
+  lattice_mlp_desc bottom;     /* relu_last = 1, output width = dim */
+  lattice_interact_desc interact;  /* n = F + (dense_in > 0); emit_slot0 = dense_in > 0 */
+  lattice_mlp_desc top;        /* relu_last = 0, output width = T */
+} lattice_model_desc;
+
+typedef struct {
+  lattice_jagged bags;
+  const void* dense;           /* device [B, dense_in], storage dtype */
+  const float* labels;         /* device [B, T] */
+  const uint8_t* mask;         /* device [B, T] */
+} lattice_batch_desc;
+
+/* Stages of lattice_step, in order (for optional per-stage timing). */
+typedef enum {
+  LATTICE_STAGE_EMBBAG_FWD = 0,
+  LATTICE_STAGE_BOTTOM_FWD,
+  LATTICE_STAGE_INTERACT_FWD,
+  LATTICE_STAGE_TOP_FWD,
+  LATTICE_STAGE_LOSS,
+  LATTICE_STAGE_TOP_BWD,
+  LATTICE_STAGE_INTERACT_BWD,
+  LATTICE_STAGE_BOTTOM_BWD,
+  LATTICE_STAGE_EMBBAG_BWD,
+  LATTICE_STEP_STAGES
+} lattice_step_stage;
+
+typedef struct {
+  float lr_tables;             /* row-sparse SGD step on the tables (0: none) */
+  int32_t emit_grad_rows;      /* 1: also write the [nnz, dim] fp32 row gradients */
+  int64_t nnz_capacity;        /* lookups the workspace is planned for (0: the batch's nnz);
+                                  plan and step must use the same value */
+  void* const* stage_events;   /* host array of LATTICE_STEP_STAGES+1 hipEvent_t or NULL:
+                                  [0] is recorded before the first stage and [s+1]
+                                  after stage s, on the step's stream */
+} lattice_step_opts;
+
+/* Byte offsets of every intermediate inside the step workspace (-1: absent). */
+typedef struct {
+  int64_t total_bytes;
+  int64_t X;            /* [B, n, dim] stacked vectors (dense slot 0, then features) */
+  int64_t t;            /* [B, t_stride] top-MLP input */
+  int64_t t_stride;     /* elements */
+  int64_t logits;       /* [B, T] fp32 */
+  int64_t d_logits;     /* [B, T] fp32 */
+  int64_t d_logits_op;  /* [B, T] storage dtype */
+  int64_t loss;         /* [1] fp32 */
+  int64_t d_t;          /* [B, t_stride] gradient of the top input */
+  int64_t dX;           /* [B, n, dim] gradient of the stacked vectors */
+  int64_t bottom_act[LATTICE_MAX_LAYERS];   /* [B, out_i] hidden bottom outputs (last: in X) */
+  int64_t top_act[LATTICE_MAX_LAYERS];      /* [B, out_i] hidden top outputs (last: logits) */
+  int64_t unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows;
+  int64_t scratch;      /* shared scratch of the stages */
+  int64_t scratch_bytes;
+} lattice_step_layout;
+
+/* Workspace layout for batches of B samples and at most
+ * max(nnz, opts->nnz_capacity) lookups. */
+lattice_status lattice_step_plan(const lattice_model_desc* model, int32_t B, int64_t nnz,
+                                 const lattice_step_opts* opts, lattice_step_layout* layout);
+
+/* One forward + backward step: pooled lookups, bottom MLP, interaction, top
+ * MLP, masked BCE, and the backward of all of them; parameter gradients go to
+ * the dW/db/... pointers in `model`; the row-coalesced table gradient goes to
+ * the workspace (see lattice_step_layout); with lr_tables != 0 the tables are
+ * updated in place.  ws must be lattice_step_plan(...)->total_bytes long for
+ * the same opts; the batch's nnz must not exceed opts->nnz_capacity (when
+ * set).  Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP. */
+lattice_status lattice_step(const lattice_model_desc* model, const lattice_batch_desc* batch,
+                            const lattice_step_opts* opts, void* ws, size_t ws_bytes,
+                            void* stream);
+
+/* ------------------------------------------------------------------------ */
+const char* lattice_status_string(lattice_status s);
+const char* lattice_last_error(void);
+int lattice_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LATTICE_H_ */

@@ -21,12 +21,14 @@ def sigmoid(z):
     return np.where(z >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
 
 
-def masked_bce(z, y, m):
-    """(loss, dz) in float64."""
+def masked_bce(z, y, m, normalizer=None):
+    """(loss, dz) in float64.  ``normalizer`` replaces ``max(1, sum m)`` when
+    the rows given are a subset of a larger batch whose labelled-entry count
+    defines N."""
     z = np.asarray(z, np.float64)
     y = np.asarray(y, np.float64)
     m = np.asarray(m, np.float64)
-    N = max(1.0, float(m.sum()))
+    N = max(1.0, float(m.sum())) if normalizer is None else float(normalizer)
     l = np.maximum(z, 0.0) - z * y + np.log1p(np.exp(-np.abs(z)))
     loss = float((m * l).sum() / N)
     dz = m * (sigmoid(z) - y) / N

@@ -1,4 +1,4 @@
-"""Comparison metric of the parity tests.
+"""Comparison metrics of the parity tests.
 
 Test infrastructure only (see the package docstring).
 
@@ -32,3 +32,22 @@ def max_rel_err(x, r):
     err = np.zeros_like(rr)
     err[ok] = np.abs(xx[ok] - rr[ok]) / denom[ok]
     return float(err.max())
+
+
+def max_rel_err_normwise(x, r):
+    """Largest absolute deviation relative to the largest reference magnitude,
+    ``max_i |x_i - r_i| / max_i |r_i|`` (0 for an all-zero reference that x
+    matches exactly; a non-finite value in x fails)."""
+    x = np.asarray(x, np.float64)
+    r = np.asarray(r, np.float64)
+    if x.shape != r.shape:
+        raise ValueError(f"shape mismatch {x.shape} vs {r.shape}")
+    if r.size == 0:
+        return 0.0
+    if not np.all(np.isfinite(x)):
+        return float("inf")
+    scale = np.abs(r).max()
+    diff = np.abs(x - r).max()
+    if scale == 0:
+        return 0.0 if diff == 0 else float("inf")
+    return float(diff / scale)

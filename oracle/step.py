@@ -33,9 +33,11 @@ def rounding(dtype):
     return _bf16.round_bf16 if dtype == "bf16" else _bf16.identity
 
 
-def forward(cfg, params, table, batch, overrides=None):
+def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None):
     """``overrides`` (optional) maps "bottom"/"top" to per-layer ReLU decision
-    overrides (see ``mlp.mlp_forward``)."""
+    overrides (see ``mlp.mlp_forward``); ``loss_normalizer`` (optional) is the
+    labelled-entry count of the full batch when ``batch`` holds a subset of
+    its samples."""
     rnd = rounding(cfg.dtype)
     B, F, d = int(cfg.B), int(cfg.F), int(cfg.d)
     n, s0 = cfg.n_slots, cfg.first_emb_slot
@@ -70,7 +72,7 @@ def forward(cfg, params, table, batch, overrides=None):
                          overrides=(overrides or {}).get("top"))
     c["hs_top"], c["masks_top"] = hs_top, mt
     z = hs_top[-1]
-    loss, dz = masked_bce(z, batch["labels"], batch["mask"])
+    loss, dz = masked_bce(z, batch["labels"], batch["mask"], loss_normalizer)
     c.update(logits=z, loss=loss, dz=dz, t=t)
     return c
 
@@ -113,7 +115,7 @@ def backward(cfg, params, table, batch, c, lr_tables=None):
     return g
 
 
-def step(cfg, params, table, batch, lr_tables=None, overrides=None):
-    c = forward(cfg, params, table, batch, overrides)
+def step(cfg, params, table, batch, lr_tables=None, overrides=None, loss_normalizer=None):
+    c = forward(cfg, params, table, batch, overrides, loss_normalizer)
     g = backward(cfg, params, table, batch, c, lr_tables)
     return c, g

@@ -1,0 +1,288 @@
+"""Torch-facing binding of the C ABI: the same entry-point names as
+include/lattice.h, taking torch tensors that live on the GPU.  Argument
+marshalling and buffer allocation only -- every step runs in liblattice.so.
+"""
+import ctypes
+from ctypes import byref
+
+import torch
+
+from . import _abi as A
+from ._abi import check, load
+
+_POOL = {"sum": A.POOL_SUM, "mean": A.POOL_MEAN}
+_KIND = {"dot": A.DOT, "fm": A.FM, "stack": A.STACK}
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dt(t):
+    if t.dtype == torch.bfloat16:
+        return A.BF16
+    if t.dtype == torch.float32:
+        return A.F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _row_stride(t):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a 2-D tensor with unit column stride")
+    return t.stride(0)
+
+
+def _contig(*ts):
+    for t in ts:
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensor must be contiguous")
+
+
+def _tables(table, row_base):
+    _contig(table, row_base)
+    return A.lattice_tables(data=table.data_ptr(), dtype=_dt(table), dim=table.shape[1],
+                            total_rows=table.shape[0], row_base=row_base.data_ptr())
+
+
+def _jagged(offsets, indices, F, B):
+    _contig(offsets, indices)
+    return A.lattice_jagged(num_features=F, batch=B, offsets=offsets.data_ptr(),
+                            indices=indices.data_ptr() if indices.numel() else None,
+                            nnz=indices.numel())
+
+
+# ---------------------------------------------------------------------------
+def lattice_embbag_fwd(table, row_base, offsets, indices, F, B, X, first_slot=0, pool="sum",
+                       stream=None):
+    _contig(X)
+    lib = load()
+    t, j = _tables(table, row_base), _jagged(offsets, indices, F, B)
+    check(lib.lattice_embbag_fwd(byref(t), byref(j), _POOL[pool], _p(X), _dt(X), X.shape[1],
+                                 first_slot, _stream(stream)))
+    return X
+
+
+def lattice_embbag_bwd(table, row_base, offsets, indices, F, B, dX, first_slot=0, lr=0.0,
+                       pool="sum", emit_grad_rows=True, stream=None):
+    """Returns dict(unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows); with lr != 0
+    the table is updated in place."""
+    _contig(dX)
+    lib = load()
+    t, j = _tables(table, row_base), _jagged(offsets, indices, F, B)
+    nnz = indices.numel()
+    dev = table.device
+    n = max(nnz, 1)
+    out = dict(unique_rows=torch.empty(n, dtype=torch.int32, device=dev),
+               seg_offsets=torch.empty(n + 1, dtype=torch.int32, device=dev),
+               sorted_bags=torch.empty(n, dtype=torch.int32, device=dev),
+               num_unique=torch.empty(1, dtype=torch.int32, device=dev),
+               grad_rows=torch.empty((n, table.shape[1]), dtype=torch.float32, device=dev)
+               if emit_grad_rows else None)
+    sg = A.lattice_sparse_grad(*(o.data_ptr() if o is not None else None for o in
+                                 (out["unique_rows"], out["seg_offsets"], out["sorted_bags"],
+                                  out["num_unique"], out["grad_rows"])))
+    wsb = lib.lattice_embbag_bwd_workspace(byref(t), byref(j))
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    check(lib.lattice_embbag_bwd(byref(t), byref(j), _POOL[pool], _p(dX), _dt(dX), dX.shape[1],
+                                 first_slot, byref(sg), float(lr), _p(ws), wsb, _stream(stream)))
+    return out
+
+
+def lattice_validate_batch(table, row_base, offsets, indices, F, B, stream=None):
+    """Returns (ok, first_bad)."""
+    lib = load()
+    t, j = _tables(table, row_base), _jagged(offsets, indices, F, B)
+    bad = ctypes.c_int64(0)
+    st = lib.lattice_validate_batch(byref(t), byref(j), byref(bad), _stream(stream))
+    if st == 4:
+        return False, bad.value
+    check(st)
+    return True, 0
+
+
+# ---------------------------------------------------------------------------
+def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0):
+    return A.lattice_interact_desc(kind=_KIND[kind], dtype=_dt(X), n=X.shape[1], dim=X.shape[2],
+                                   rank=(fm_W.shape[1] if fm_W is not None else rank),
+                                   emit_slot0=int(emit_slot0), fm_W=fm_W.data_ptr() if fm_W is not None else None,
+                                   fm_dW=fm_dW.data_ptr() if fm_dW is not None else None,
+                                   n_layers=0, stack_n=0, ln_eps=0.0, layers=None)
+
+
+def lattice_interact_fwd(kind, X, out, emit_slot0=False, fm_W=None, stream=None):
+    _contig(X, fm_W)
+    lib = load()
+    d = interact_desc(kind, X, emit_slot0, fm_W)
+    wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
+    check(lib.lattice_interact_fwd(byref(d), X.shape[0], _p(X), _p(out), _row_stride(out), _p(ws),
+                                   wsb, _stream(stream)))
+    return out
+
+
+def lattice_interact_bwd(kind, X, d_out, dX, emit_slot0=False, fm_W=None, fm_dW=None, stream=None):
+    _contig(X, dX, fm_W, fm_dW)
+    lib = load()
+    d = interact_desc(kind, X, emit_slot0, fm_W, fm_dW)
+    wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
+    check(lib.lattice_interact_bwd(byref(d), X.shape[0], _p(X), _p(d_out), _row_stride(d_out),
+                                   _p(dX), _p(ws), wsb, _stream(stream)))
+    return dX
+
+
+# ---------------------------------------------------------------------------
+def mlp_desc(layers, relu_last, dtype):
+    """layers: list of dicts with W, b (optional), dW, db (optional)."""
+    arr = (A.lattice_linear * len(layers))()
+    for i, L in enumerate(layers):
+        W = L["W"]
+        _contig(W)
+        arr[i] = A.lattice_linear(in_dim=W.shape[1], out_dim=W.shape[0], W=W.data_ptr(),
+                                  b=L["b"].data_ptr() if L.get("b") is not None else None,
+                                  dW=L["dW"].data_ptr() if L.get("dW") is not None else None,
+                                  db=L["db"].data_ptr() if L.get("db") is not None else None)
+    d = A.lattice_mlp_desc(dtype=dtype, n_layers=len(layers), layers=arr, relu_last=int(relu_last))
+    d._keep = arr
+    return d
+
+
+def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None):
+    """acts: list of output tensors (2-D, unit column stride); loss: optional
+    dict(labels, mask, loss, d_logits, d_logits_op)."""
+    lib = load()
+    d = mlp_desc(layers, relu_last, _dt(x))
+    n = len(layers)
+    ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
+    strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
+    ld = None
+    if loss is not None:
+        ld = A.lattice_loss_desc(labels=loss["labels"].data_ptr(), mask=loss["mask"].data_ptr(),
+                                 loss=loss["loss"].data_ptr(), d_logits=loss["d_logits"].data_ptr(),
+                                 d_logits_op=loss["d_logits_op"].data_ptr()
+                                 if loss.get("d_logits_op") is not None else None)
+    wsb = lib.lattice_mlp_heads_workspace(byref(d), x.shape[0])
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=x.device)
+    check(lib.lattice_mlp_heads_fwd(byref(d), x.shape[0], _p(x), _row_stride(x), ptrs, strides,
+                                    byref(ld) if ld is not None else None, _p(ws), wsb,
+                                    _stream(stream)))
+
+
+def lattice_mlp_heads_bwd(layers, x, acts, d_out, relu_last, d_in=None, stream=None):
+    lib = load()
+    d = mlp_desc(layers, relu_last, _dt(x))
+    n = len(layers)
+    ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
+    strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
+    wsb = lib.lattice_mlp_heads_workspace(byref(d), x.shape[0])
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=x.device)
+    check(lib.lattice_mlp_heads_bwd(byref(d), x.shape[0], _p(x), _row_stride(x), ptrs, strides,
+                                    _p(d_out), _row_stride(d_out), _p(d_in),
+                                    _row_stride(d_in) if d_in is not None else 0, _p(ws), wsb,
+                                    _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+class StepModel:
+    """Marshals a model's device tensors into a lattice_model_desc.
+
+    tables [R, d], row_base int64 [F+1]; bottom/top: lists of dicts
+    {W, b, dW, db}; fm_W / fm_dW for the FM interaction."""
+
+    def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
+                 fm_W=None, fm_dW=None, pool="sum"):
+        _contig(tables, row_base)
+        dt = _dt(tables)
+        d = tables.shape[1]
+        n = num_features + (1 if dense_in > 0 else 0)
+        self._bottom = mlp_desc(bottom, True, dt) if dense_in > 0 else A.lattice_mlp_desc(dtype=dt)
+        self._top = mlp_desc(top, False, dt)
+        idesc = A.lattice_interact_desc(kind=_KIND[interact], dtype=dt, n=n, dim=d,
+                                        rank=fm_W.shape[1] if fm_W is not None else 0,
+                                        emit_slot0=int(dense_in > 0),
+                                        fm_W=fm_W.data_ptr() if fm_W is not None else None,
+                                        fm_dW=fm_dW.data_ptr() if fm_dW is not None else None,
+                                        n_layers=0, stack_n=0, ln_eps=0.0, layers=None)
+        self.desc = A.lattice_model_desc(dtype=dt, pool=_POOL[pool], tables=_tables(tables, row_base),
+                                         num_features=num_features, dense_in=dense_in,
+                                         bottom=self._bottom, interact=idesc, top=self._top)
+        self.tensors = dict(tables=tables, row_base=row_base, bottom=bottom, top=top, fm_W=fm_W,
+                            fm_dW=fm_dW)
+        self.device = tables.device
+        self.num_features = num_features
+        self.dense_in = dense_in
+        self.n = n
+        self.d = d
+
+
+def lattice_step_plan(model, B, nnz, lr_tables=0.0, emit_grad_rows=False):
+    """Layout of a workspace for batches of B samples and up to nnz lookups;
+    pass the same nnz as nnz_capacity to lattice_step."""
+    lib = load()
+    opts = A.lattice_step_opts(lr_tables=float(lr_tables), emit_grad_rows=int(emit_grad_rows),
+                               nnz_capacity=int(nnz))
+    lay = A.lattice_step_layout()
+    check(lib.lattice_step_plan(byref(model.desc), B, nnz, byref(opts), byref(lay)))
+    return lay
+
+
+def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0,
+                 emit_grad_rows=False, stream=None, stage_events=None, nnz_capacity=0):
+    """One forward+backward step; ws is a uint8 device tensor of at least
+    lattice_step_plan(...).total_bytes.  stage_events: optional list of
+    len(STAGES)+1 torch.cuda.Event(enable_timing=True) recorded between the
+    stages on the step's stream."""
+    lib = load()
+    _contig(dense, labels, mask, ws)
+    B = labels.shape[0]
+    batch = A.lattice_batch_desc(bags=_jagged(offsets, indices, model.num_features, B),
+                                 dense=dense.data_ptr() if dense is not None and dense.numel() else None,
+                                 labels=labels.data_ptr(), mask=mask.data_ptr())
+    opts = A.lattice_step_opts(lr_tables=float(lr_tables), emit_grad_rows=int(emit_grad_rows),
+                               nnz_capacity=int(nnz_capacity or indices.numel()))
+    if stage_events is not None:
+        if len(stage_events) != len(A.STAGES) + 1:
+            raise ValueError("need len(STAGES)+1 events")
+        arr = (ctypes.c_void_p * len(stage_events))(*[e.cuda_event for e in stage_events])
+        opts.stage_events = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    check(lib.lattice_step(byref(model.desc), byref(batch), byref(opts), _p(ws), ws.numel(),
+                           _stream(stream)))
+
+
+def step_views(model, ws, layout, B, T, nnz):
+    """Torch views of the step's intermediates inside the workspace."""
+    dt = model.tensors["tables"].dtype
+    es = 2 if dt == torch.bfloat16 else 4
+
+    def view(off, shape, dtype):
+        if off < 0:
+            return None
+        n = 1
+        for s in shape:
+            n *= s
+        size = n * torch.empty((), dtype=dtype).element_size()
+        return ws[off: off + size].view(dtype).view(*shape)
+
+    n, d = model.n, model.d
+    v = dict(X=view(layout.X, (B, n, d), dt), t=view(layout.t, (B, layout.t_stride), dt),
+             logits=view(layout.logits, (B, T), torch.float32),
+             d_logits=view(layout.d_logits, (B, T), torch.float32),
+             loss=view(layout.loss, (1,), torch.float32),
+             d_t=view(layout.d_t, (B, layout.t_stride), dt), dX=view(layout.dX, (B, n, d), dt),
+             unique_rows=view(layout.unique_rows, (max(nnz, 1),), torch.int32),
+             seg_offsets=view(layout.seg_offsets, (max(nnz, 1) + 1,), torch.int32),
+             sorted_bags=view(layout.sorted_bags, (max(nnz, 1),), torch.int32),
+             num_unique=view(layout.num_unique, (1,), torch.int32),
+             grad_rows=view(layout.grad_rows, (max(nnz, 1), d), torch.float32))
+    tops = model.tensors["top"]
+    v["top_act"] = [view(layout.top_act[i], (B, tops[i]["W"].shape[0]), dt) for i in range(len(tops) - 1)]
+    bots = model.tensors["bottom"]
+    v["bottom_act"] = [view(layout.bottom_act[i], (B, bots[i]["W"].shape[0]), dt)
+                       for i in range(len(bots) - 1)] if model.dense_in > 0 else []
+    _ = es
+    return v

@@ -1,0 +1,664 @@
+// C ABI of the training-step library: argument checks, the public entry
+// points, and lattice_step, which runs the whole forward + backward on one
+// stream over a caller-provided workspace whose layout lattice_step_plan
+// reports.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+
+#include "../../include/lattice.h"
+#include "common.h"
+#include "kernels.h"
+
+namespace lat {
+static thread_local char g_err[1024] = "";
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+}  // namespace lat
+
+using namespace lat;
+
+#define FAIL(code, ...)         \
+  do {                          \
+    ::lat::set_error(__VA_ARGS__); \
+    return code;                \
+  } while (0)
+#define REQUIRE(cond, ...) \
+  do {                     \
+    if (!(cond)) FAIL(LATTICE_ERR_INVALID_ARG, __VA_ARGS__); \
+  } while (0)
+#define HIPRET(expr)                                  \
+  do {                                                \
+    hipError_t e__ = (expr);                          \
+    if (e__ != hipSuccess) return LATTICE_ERR_HIP;    \
+  } while (0)
+
+static inline DType dt_of(lattice_dtype d) { return d == LATTICE_BF16 ? DT_BF16 : DT_F32; }
+static inline size_t esize(lattice_dtype d) { return d == LATTICE_BF16 ? 2 : 4; }
+static inline hipStream_t strm(void* s) { return reinterpret_cast<hipStream_t>(s); }
+static inline size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static lattice_status check_dim(int dim, lattice_dtype dt) {
+  if (dim <= 0 || dim > 256) FAIL(LATTICE_ERR_UNSUPPORTED, "dim %d outside 1..256", dim);
+  if (dt == LATTICE_BF16 && dim % 8) FAIL(LATTICE_ERR_UNSUPPORTED, "bf16 dim %d not a multiple of 8", dim);
+  if (dt == LATTICE_F32 && dim % 4) FAIL(LATTICE_ERR_UNSUPPORTED, "fp32 dim %d not a multiple of 4", dim);
+  return LATTICE_OK;
+}
+
+static lattice_status check_tables(const lattice_tables* t, const lattice_jagged* j) {
+  REQUIRE(t && j, "null tables or bags");
+  REQUIRE(j->num_features >= 0 && j->batch >= 0 && j->nnz >= 0, "negative sizes");
+  REQUIRE(j->nnz < ((int64_t)1 << 31), "nnz must be < 2^31");
+  if (j->nnz > 0) REQUIRE(j->indices, "null indices");
+  if ((int64_t)j->num_features * j->batch > 0) REQUIRE(j->offsets && t->row_base && t->data, "null pointer in batch/tables");
+  REQUIRE(t->dtype == LATTICE_F32 || t->dtype == LATTICE_BF16, "bad table dtype");
+  if (t->total_rows >= ((int64_t)1 << 31)) FAIL(LATTICE_ERR_UNSUPPORTED, "total_rows must be < 2^31");
+  return check_dim(t->dim, t->dtype);
+}
+
+extern "C" {
+
+const char* lattice_status_string(lattice_status s) {
+  switch (s) {
+    case LATTICE_OK: return "ok";
+    case LATTICE_ERR_INVALID_ARG: return "invalid argument";
+    case LATTICE_ERR_UNSUPPORTED: return "unsupported";
+    case LATTICE_ERR_WORKSPACE: return "workspace too small";
+    case LATTICE_ERR_BAD_INPUT: return "malformed input";
+    case LATTICE_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+const char* lattice_last_error(void) { return g_err; }
+int lattice_abi_version(void) { return LATTICE_ABI_VERSION; }
+
+// ---------------------------------------------------------------------------
+lattice_status lattice_embbag_fwd(const lattice_tables* tables, const lattice_jagged* bags,
+                                  lattice_pool pool, void* X, lattice_dtype x_dtype,
+                                  int32_t n_slots, int32_t first_slot, void* stream) {
+  lattice_status st = check_tables(tables, bags);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(x_dtype == LATTICE_F32 || x_dtype == LATTICE_BF16, "bad X dtype");
+  REQUIRE(pool == LATTICE_POOL_SUM || pool == LATTICE_POOL_MEAN, "bad pool mode");
+  REQUIRE(first_slot >= 0 && first_slot + bags->num_features <= n_slots, "slots out of range");
+  if ((int64_t)bags->num_features * bags->batch == 0) return LATTICE_OK;
+  REQUIRE(X, "null X");
+  HIPRET(embbag_fwd(tables->data, dt_of(tables->dtype), tables->dim, tables->row_base,
+                    bags->offsets, bags->indices, bags->num_features, bags->batch,
+                    pool == LATTICE_POOL_MEAN, X, dt_of(x_dtype), n_slots, first_slot,
+                    strm(stream)));
+  return LATTICE_OK;
+}
+
+size_t lattice_embbag_bwd_workspace(const lattice_tables* tables, const lattice_jagged* bags) {
+  if (!tables || !bags) return 0;
+  return embbag_bwd_workspace(bags->nnz, tables->dim);
+}
+
+lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_jagged* bags,
+                                  lattice_pool pool, const void* dX, lattice_dtype dx_dtype,
+                                  int32_t n_slots, int32_t first_slot,
+                                  const lattice_sparse_grad* out, float lr, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  lattice_status st = check_tables(tables, bags);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(out && out->unique_rows && out->seg_offsets && out->sorted_bags && out->num_unique,
+          "null sparse-gradient output");
+  REQUIRE(dx_dtype == LATTICE_F32 || dx_dtype == LATTICE_BF16, "bad dX dtype");
+  REQUIRE(pool == LATTICE_POOL_SUM || pool == LATTICE_POOL_MEAN, "bad pool mode");
+  REQUIRE(first_slot >= 0 && first_slot + bags->num_features <= n_slots, "slots out of range");
+  if (bags->nnz > 0) REQUIRE(dX, "null dX");
+  const size_t need = embbag_bwd_workspace(bags->nnz, tables->dim);
+  if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+  HIPRET(embbag_bwd(tables->row_base, tables->total_rows, bags->offsets, bags->indices,
+                    bags->num_features, bags->batch, bags->nnz, pool == LATTICE_POOL_MEAN, dX,
+                    dt_of(dx_dtype), n_slots, first_slot, tables->dim, out->unique_rows,
+                    out->seg_offsets, out->sorted_bags, out->num_unique, out->grad_rows,
+                    tables->data, dt_of(tables->dtype), lr, ws, strm(stream)));
+  return LATTICE_OK;
+}
+
+__device__ unsigned long long g_validate_result[2];
+static std::mutex g_validate_mu;
+
+lattice_status lattice_validate_batch(const lattice_tables* tables, const lattice_jagged* bags,
+                                      int64_t* first_bad, void* stream) {
+  lattice_status st = check_tables(tables, bags);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(first_bad, "null first_bad");
+  *first_bad = 0;
+  if ((int64_t)bags->num_features * bags->batch == 0) return LATTICE_OK;
+  std::lock_guard<std::mutex> lock(g_validate_mu);
+  void* ptr = nullptr;
+  if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_validate_result)) != hipSuccess)
+    FAIL(LATTICE_ERR_HIP, "hipGetSymbolAddress failed");
+  HIPRET(validate_batch(tables->row_base, bags->offsets, bags->indices, bags->num_features,
+                        bags->batch, bags->nnz, (unsigned long long*)ptr, strm(stream)));
+  unsigned long long host[2];
+  if (hipMemcpyAsync(host, ptr, sizeof(host), hipMemcpyDeviceToHost, strm(stream)) != hipSuccess ||
+      hipStreamSynchronize(strm(stream)) != hipSuccess)
+    FAIL(LATTICE_ERR_HIP, "validate copy failed");
+  if (host[0] != ~0ull) {
+    *first_bad = -1 - (int64_t)host[0];
+    FAIL(LATTICE_ERR_BAD_INPUT, "malformed offsets at position %lld", (long long)host[0]);
+  }
+  if (host[1] != ~0ull) {
+    *first_bad = (int64_t)host[1];
+    FAIL(LATTICE_ERR_BAD_INPUT, "index out of range at position %lld", (long long)host[1]);
+  }
+  return LATTICE_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// interaction
+// ---------------------------------------------------------------------------
+static lattice_status check_interact(const lattice_interact_desc* d, int32_t B) {
+  REQUIRE(d, "null interaction descriptor");
+  REQUIRE(B >= 0, "negative batch");
+  REQUIRE(d->dtype == LATTICE_F32 || d->dtype == LATTICE_BF16, "bad dtype");
+  REQUIRE(d->n >= 1 && d->dim >= 1, "bad n/dim");
+  lattice_status st = check_dim(d->dim, d->dtype);
+  if (st != LATTICE_OK) return st;
+  if (d->kind == LATTICE_INTERACT_DOT) {
+    if (dot_lds_bytes(d->n, d->dim) > 160 * 1024)
+      FAIL(LATTICE_ERR_UNSUPPORTED, "DOT with n=%d, dim=%d exceeds LDS", d->n, d->dim);
+  } else if (d->kind == LATTICE_INTERACT_FM) {
+    REQUIRE(d->rank >= 1 && d->fm_W, "FM needs rank and W");
+    if (fm_lds_bytes(d->n, d->dim, d->rank) > 160 * 1024 || d->n * d->rank > 256 * 64)
+      FAIL(LATTICE_ERR_UNSUPPORTED, "FM with n=%d, dim=%d, rank=%d exceeds LDS", d->n, d->dim, d->rank);
+  } else {
+    FAIL(LATTICE_ERR_UNSUPPORTED, "interaction kind %d not supported", (int)d->kind);
+  }
+  return LATTICE_OK;
+}
+
+static int64_t interact_width(const lattice_interact_desc* d) {
+  int64_t w = d->kind == LATTICE_INTERACT_DOT ? (int64_t)d->n * (d->n - 1) / 2
+                                              : (int64_t)d->n * d->rank;
+  return w + (d->emit_slot0 ? d->dim : 0);
+}
+
+static size_t interact_ws(const lattice_interact_desc* d) {
+  return d->kind == LATTICE_INTERACT_FM ? fm_bwd_workspace(d->n, d->rank) : 0;
+}
+
+static hipError_t interact_fwd_impl(const lattice_interact_desc* d, int B, const void* X,
+                                    void* out, int64_t os, hipStream_t s) {
+  if (d->kind == LATTICE_INTERACT_DOT)
+    return dot_fwd(dt_of(d->dtype), X, B, d->n, d->dim, out, os, d->emit_slot0, s);
+  return fm_fwd(dt_of(d->dtype), X, d->fm_W, B, d->n, d->dim, d->rank, out, os, d->emit_slot0, s);
+}
+
+static hipError_t interact_bwd_impl(const lattice_interact_desc* d, int B, const void* X,
+                                    const void* dout, int64_t ds, void* dX, void* ws,
+                                    hipStream_t s) {
+  if (d->kind == LATTICE_INTERACT_DOT)
+    return dot_bwd(dt_of(d->dtype), X, B, d->n, d->dim, dout, ds, d->emit_slot0, dX, s);
+  return fm_bwd(dt_of(d->dtype), X, d->fm_W, B, d->n, d->dim, d->rank, dout, ds, d->emit_slot0,
+                nullptr, dX, dt_of(d->dtype), d->fm_dW, ws, s);
+}
+
+extern "C" {
+
+size_t lattice_interact_workspace(const lattice_interact_desc* desc, int32_t B) {
+  (void)B;
+  return desc ? interact_ws(desc) : 0;
+}
+
+lattice_status lattice_interact_fwd(const lattice_interact_desc* desc, int32_t B, const void* X,
+                                    void* out, int64_t out_stride, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  lattice_status st = check_interact(desc, B);
+  if (st != LATTICE_OK) return st;
+  if (B == 0) return LATTICE_OK;
+  REQUIRE(X && out, "null X/out");
+  REQUIRE(out_stride >= interact_width(desc), "out_stride %lld < row width %lld",
+          (long long)out_stride, (long long)interact_width(desc));
+  HIPRET(interact_fwd_impl(desc, B, X, out, out_stride, strm(stream)));
+  return LATTICE_OK;
+}
+
+lattice_status lattice_interact_bwd(const lattice_interact_desc* desc, int32_t B, const void* X,
+                                    const void* d_out, int64_t d_out_stride, void* dX, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  lattice_status st = check_interact(desc, B);
+  if (st != LATTICE_OK) return st;
+  if (desc->kind == LATTICE_INTERACT_FM) REQUIRE(desc->fm_dW, "FM backward needs fm_dW");
+  const size_t need = interact_ws(desc);
+  if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+  if (B > 0) REQUIRE(X && d_out && dX, "null X/d_out/dX");
+  REQUIRE(d_out_stride >= interact_width(desc) || B == 0, "d_out_stride too small");
+  HIPRET(interact_bwd_impl(desc, B, X, d_out, d_out_stride, dX, ws, strm(stream)));
+  return LATTICE_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// MLP + heads
+// ---------------------------------------------------------------------------
+static lattice_status check_mlp(const lattice_mlp_desc* d, int32_t B) {
+  REQUIRE(d && d->layers, "null MLP descriptor");
+  REQUIRE(B >= 0, "negative batch");
+  REQUIRE(d->n_layers >= 1 && d->n_layers <= LATTICE_MAX_LAYERS, "n_layers %d outside 1..%d",
+          d->n_layers, LATTICE_MAX_LAYERS);
+  REQUIRE(d->dtype == LATTICE_F32 || d->dtype == LATTICE_BF16, "bad dtype");
+  for (int i = 0; i < d->n_layers; ++i) {
+    const lattice_linear& L = d->layers[i];
+    REQUIRE(L.in_dim >= 1 && L.out_dim >= 1 && L.W, "layer %d: bad dims or null W", i);
+    if (i > 0) REQUIRE(L.in_dim == d->layers[i - 1].out_dim, "layer %d: in_dim mismatch", i);
+  }
+  return LATTICE_OK;
+}
+
+static size_t mlp_bwd_ws(const lattice_mlp_desc* d, int B) {
+  size_t s = 0;
+  for (int i = 0; i < d->n_layers; ++i) {
+    const lattice_linear& L = d->layers[i];
+    GemmArgs g;
+    g.dt = dt_of(d->dtype);
+    g.max_splits = 16;
+    g.M = L.out_dim; g.N = L.in_dim; g.K = B;
+    s = std::max(s, gemm_workspace(g));
+    g.M = B; g.N = L.in_dim; g.K = L.out_dim;
+    s = std::max(s, gemm_workspace(g));
+    s = std::max(s, colsum_workspace(B, L.out_dim));
+  }
+  return al256(s);
+}
+
+static size_t mlp_gbuf_elems(const lattice_mlp_desc* d, int B) {
+  int64_t w = 1;
+  for (int i = 1; i < d->n_layers; ++i) w = std::max<int64_t>(w, d->layers[i].in_dim);
+  w = std::max<int64_t>(w, d->layers[d->n_layers - 1].out_dim);
+  return (size_t)w * B;
+}
+
+static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
+                              void* const* acts, const int64_t* strides, hipStream_t s) {
+  for (int i = 0; i < d->n_layers; ++i) {
+    const lattice_linear& L = d->layers[i];
+    const bool last = i == d->n_layers - 1;
+    GemmArgs g;
+    g.dt = dt_of(d->dtype);
+    g.A = i == 0 ? in : acts[i - 1];
+    g.lda = i == 0 ? in_stride : strides[i - 1];
+    g.B = L.W; g.ldb = L.in_dim;
+    g.C = acts[i]; g.ldc = strides[i];
+    g.c_dt = (last && !d->relu_last) ? DT_F32 : dt_of(d->dtype);
+    g.M = B; g.N = L.out_dim; g.K = L.in_dim;
+    g.bias = L.b;
+    g.relu = (!last || d->relu_last) ? 1 : 0;
+    hipError_t e = gemm(g, nullptr, s);  // forward GEMMs never split K
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// g_last: gradient of the last layer's output, already ReLU-masked where needed.
+static hipError_t mlp_backward(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
+                               const void* const* acts, const int64_t* strides,
+                               const void* g_last, int64_t g_last_stride, void* d_in,
+                               int64_t d_in_stride, void* gbuf0, void* gbuf1, void* ws,
+                               hipStream_t s) {
+  const DType dt = dt_of(d->dtype);
+  const void* g = g_last;
+  int64_t gs = g_last_stride;
+  for (int i = d->n_layers - 1; i >= 0; --i) {
+    const lattice_linear& L = d->layers[i];
+    const void* in_i = i == 0 ? in : acts[i - 1];
+    const int64_t ld_in = i == 0 ? in_stride : strides[i - 1];
+    if (L.dW) {
+      GemmArgs w;
+      w.dt = dt;
+      w.A = g; w.lda = gs; w.ta = 1;
+      w.B = in_i; w.ldb = ld_in; w.tb = 1;
+      w.C = L.dW; w.ldc = L.in_dim; w.c_dt = DT_F32;
+      w.M = L.out_dim; w.N = L.in_dim; w.K = B;
+      w.max_splits = 16;
+      hipError_t e = gemm(w, ws, s);
+      if (e != hipSuccess) return e;
+    }
+    if (L.db) {
+      hipError_t e = colsum(g, dt, gs, B, L.out_dim, L.db, ws, s);
+      if (e != hipSuccess) return e;
+    }
+    if (i > 0 || d_in) {
+      void* dst = i > 0 ? ((d->n_layers - 1 - i) % 2 == 0 ? gbuf0 : gbuf1) : d_in;
+      const int64_t dst_ld = i > 0 ? L.in_dim : d_in_stride;
+      GemmArgs x;
+      x.dt = dt;
+      x.A = g; x.lda = gs;
+      x.B = L.W; x.ldb = L.in_dim; x.tb = 1;
+      x.C = dst; x.ldc = dst_ld; x.c_dt = dt;
+      x.M = B; x.N = L.in_dim; x.K = L.out_dim;
+      x.max_splits = 16;
+      if (i > 0) {
+        x.mask = acts[i - 1];
+        x.mask_dt = dt;
+        x.ldm = strides[i - 1];
+      }
+      hipError_t e = gemm(x, ws, s);
+      if (e != hipSuccess) return e;
+      g = dst;
+      gs = dst_ld;
+    }
+  }
+  return hipSuccess;
+}
+
+__global__ void relu_mask_kernel(const void* g, int64_t gs, const void* act, int64_t as, int B,
+                                 int N, int bf, void* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)B * N) return;
+  const int64_t r = i / N, c = i % N;
+  if (bf) {
+    const float a = bf2f(((const bf16_t*)act)[r * as + c]);
+    const bf16_t v = ((const bf16_t*)g)[r * gs + c];
+    ((bf16_t*)out)[i] = a > 0.f ? v : (bf16_t)0;
+  } else {
+    const float a = ((const float*)act)[r * as + c];
+    ((float*)out)[i] = a > 0.f ? ((const float*)g)[r * gs + c] : 0.f;
+  }
+}
+
+static size_t mlp_heads_ws(const lattice_mlp_desc* d, int B) {
+  const size_t g = al256(mlp_gbuf_elems(d, B) * esize(d->dtype));
+  const int T = d->layers[d->n_layers - 1].out_dim;
+  return mlp_bwd_ws(d, B) + 3 * g + al256(bce_workspace((int64_t)B * T));
+}
+
+extern "C" {
+
+size_t lattice_mlp_heads_workspace(const lattice_mlp_desc* desc, int32_t B) {
+  if (check_mlp(desc, B) != LATTICE_OK) return 0;
+  return mlp_heads_ws(desc, B);
+}
+
+lattice_status lattice_mlp_heads_fwd(const lattice_mlp_desc* desc, int32_t B, const void* in,
+                                     int64_t in_stride, void* const* acts,
+                                     const int64_t* act_strides, const lattice_loss_desc* loss,
+                                     void* ws, size_t ws_bytes, void* stream) {
+  lattice_status st = check_mlp(desc, B);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(acts && act_strides, "null acts");
+  REQUIRE(in || B == 0, "null input");
+  REQUIRE(in_stride >= desc->layers[0].in_dim, "in_stride too small");
+  for (int i = 0; i < desc->n_layers; ++i)
+    REQUIRE((acts[i] || B == 0) && act_strides[i] >= desc->layers[i].out_dim, "bad act %d", i);
+  const int T = desc->layers[desc->n_layers - 1].out_dim;
+  if (loss) {
+    REQUIRE(!desc->relu_last, "the loss needs a linear last layer");
+    REQUIRE(act_strides[desc->n_layers - 1] == T, "logits must be contiguous for the loss");
+    REQUIRE(loss->labels && loss->mask && loss->loss && loss->d_logits, "null loss buffers");
+    const size_t need = bce_workspace((int64_t)B * T);
+    if (ws_bytes < need || !ws) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+  }
+  if (B > 0) HIPRET(mlp_forward(desc, B, in, in_stride, acts, act_strides, strm(stream)));
+  if (loss)
+    HIPRET(bce((const float*)acts[desc->n_layers - 1], loss->labels, loss->mask, (int64_t)B * T,
+               loss->loss, loss->d_logits, loss->d_logits_op, dt_of(desc->dtype), ws,
+               strm(stream)));
+  return LATTICE_OK;
+}
+
+lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, const void* in,
+                                     int64_t in_stride, const void* const* acts,
+                                     const int64_t* act_strides, const void* d_out,
+                                     int64_t d_out_stride, void* d_in, int64_t d_in_stride,
+                                     void* ws, size_t ws_bytes, void* stream) {
+  lattice_status st = check_mlp(desc, B);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(acts && act_strides, "null acts");
+  const size_t need = mlp_heads_ws(desc, B);
+  if (ws_bytes < need || !ws) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+  if (B > 0) REQUIRE(in && d_out, "null in/d_out");
+  const int L = desc->n_layers;
+  const int T = desc->layers[L - 1].out_dim;
+  REQUIRE(d_out_stride >= T, "d_out_stride too small");
+  if (d_in) REQUIRE(d_in_stride >= desc->layers[0].in_dim, "d_in_stride too small");
+  char* p = (char*)ws;
+  void* gemm_ws = p; p += mlp_bwd_ws(desc, B);
+  const size_t g = al256(mlp_gbuf_elems(desc, B) * esize(desc->dtype));
+  void* gb0 = p; p += g;
+  void* gb1 = p; p += g;
+  void* masked = p;
+  const void* g_last = d_out;
+  int64_t g_ld = d_out_stride;
+  if (desc->relu_last && B > 0) {
+    relu_mask_kernel<<<cdiv((int64_t)B * T, 256), 256, 0, strm(stream)>>>(
+        d_out, d_out_stride, acts[L - 1], act_strides[L - 1], B, T, desc->dtype == LATTICE_BF16,
+        masked);
+    if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
+    g_last = masked;
+    g_ld = T;
+  }
+  HIPRET(mlp_backward(desc, B, in, in_stride, acts, act_strides, g_last, g_ld, d_in, d_in_stride,
+                      gb0, gb1, gemm_ws, strm(stream)));
+  return LATTICE_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// whole step
+// ---------------------------------------------------------------------------
+struct Plan {
+  lattice_step_layout L;
+  int n, T, t_stride;
+  size_t gbuf_top, gbuf_bot, scratch;
+  int64_t g_top[2], g_bot[2];
+};
+
+static lattice_status check_model(const lattice_model_desc* m, int B) {
+  REQUIRE(m, "null model");
+  REQUIRE(B >= 0, "negative batch");
+  REQUIRE(m->dtype == LATTICE_F32 || m->dtype == LATTICE_BF16, "bad dtype");
+  REQUIRE(m->tables.dtype == m->dtype, "table dtype must equal the model dtype");
+  lattice_status st = check_dim(m->tables.dim, m->dtype);
+  if (st != LATTICE_OK) return st;
+  const int d = m->tables.dim;
+  const int n = m->num_features + (m->dense_in > 0 ? 1 : 0);
+  REQUIRE(m->num_features >= 1, "need at least one feature");
+  if (m->dense_in > 0) {
+    st = check_mlp(&m->bottom, B);
+    if (st != LATTICE_OK) return st;
+    REQUIRE(m->bottom.relu_last == 1, "bottom MLP must apply ReLU on every layer");
+    REQUIRE(m->bottom.layers[0].in_dim == m->dense_in, "bottom input width != dense_in");
+    REQUIRE(m->bottom.layers[m->bottom.n_layers - 1].out_dim == d, "bottom output width != dim");
+    REQUIRE(m->bottom.dtype == m->dtype, "bottom dtype");
+  }
+  st = check_mlp(&m->top, B);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(m->top.relu_last == 0, "top MLP last layer must be linear");
+  REQUIRE(m->top.dtype == m->dtype, "top dtype");
+  st = check_interact(&m->interact, B);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(m->interact.n == n && m->interact.dim == d && m->interact.dtype == m->dtype,
+          "interaction shape/dtype mismatch");
+  REQUIRE(m->interact.emit_slot0 == (m->dense_in > 0 ? 1 : 0), "emit_slot0 must equal (dense_in > 0)");
+  REQUIRE(m->top.layers[0].in_dim == interact_width(&m->interact), "top input width %d != %lld",
+          m->top.layers[0].in_dim, (long long)interact_width(&m->interact));
+  return LATTICE_OK;
+}
+
+static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
+                                const lattice_step_opts* o, Plan* P) {
+  lattice_status st = check_model(m, B);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(nnz >= 0 && nnz < ((int64_t)1 << 31), "bad nnz");
+  const size_t es = esize(m->dtype);
+  const int d = m->tables.dim;
+  P->n = m->interact.n;
+  P->T = m->top.layers[m->top.n_layers - 1].out_dim;
+  P->t_stride = (int)((m->top.layers[0].in_dim + 7) / 8 * 8);
+  lattice_step_layout& L = P->L;
+  for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) L.bottom_act[i] = L.top_act[i] = -1;
+  int64_t off = 0;
+  auto take = [&](size_t bytes) { int64_t r = off; off += (int64_t)al256(bytes); return r; };
+  L.X = take((size_t)B * P->n * d * es);
+  L.t = take((size_t)B * P->t_stride * es);
+  L.t_stride = P->t_stride;
+  if (m->dense_in > 0)
+    for (int i = 0; i + 1 < m->bottom.n_layers; ++i) L.bottom_act[i] = take((size_t)B * m->bottom.layers[i].out_dim * es);
+  for (int i = 0; i + 1 < m->top.n_layers; ++i) L.top_act[i] = take((size_t)B * m->top.layers[i].out_dim * es);
+  L.logits = take((size_t)B * P->T * 4);
+  L.d_logits = take((size_t)B * P->T * 4);
+  L.d_logits_op = take((size_t)B * P->T * es);
+  L.loss = take(4);
+  L.d_t = take((size_t)B * P->t_stride * es);
+  L.dX = take((size_t)B * P->n * d * es);
+  const size_t gt = mlp_gbuf_elems(&m->top, B) * es;
+  P->g_top[0] = take(gt);
+  P->g_top[1] = take(gt);
+  if (m->dense_in > 0) {
+    const size_t gb = mlp_gbuf_elems(&m->bottom, B) * es;
+    P->g_bot[0] = take(gb);
+    P->g_bot[1] = take(gb);
+  } else {
+    P->g_bot[0] = P->g_bot[1] = -1;
+  }
+  const int64_t nn = nnz > 0 ? nnz : 1;
+  L.unique_rows = take((size_t)nn * 4);
+  L.seg_offsets = take((size_t)(nn + 1) * 4);
+  L.sorted_bags = take((size_t)nn * 4);
+  L.num_unique = take(4);
+  L.grad_rows = (o && o->emit_grad_rows) ? take((size_t)nn * d * 4) : -1;
+  size_t sc = 0;
+  sc = std::max(sc, mlp_bwd_ws(&m->top, B));
+  if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
+  sc = std::max(sc, bce_workspace((int64_t)B * P->T));
+  sc = std::max(sc, interact_ws(&m->interact));
+  sc = std::max(sc, embbag_bwd_workspace(nnz, d));
+  L.scratch = take(sc);
+  L.scratch_bytes = (int64_t)sc;
+  L.total_bytes = off;
+  return LATTICE_OK;
+}
+
+extern "C" {
+
+lattice_status lattice_step_plan(const lattice_model_desc* model, int32_t B, int64_t nnz,
+                                 const lattice_step_opts* opts, lattice_step_layout* layout) {
+  REQUIRE(layout, "null layout");
+  Plan P;
+  const int64_t cap = (opts && opts->nnz_capacity > nnz) ? opts->nnz_capacity : nnz;
+  lattice_status st = make_plan(model, B, cap, opts, &P);
+  if (st != LATTICE_OK) return st;
+  *layout = P.L;
+  return LATTICE_OK;
+}
+
+lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_desc* batch,
+                            const lattice_step_opts* opts, void* ws, size_t ws_bytes,
+                            void* stream) {
+  REQUIRE(m && batch && opts, "null model/batch/opts");
+  const int B = batch->bags.batch;
+  REQUIRE(batch->bags.num_features == m->num_features, "batch features != model features");
+  REQUIRE(opts->nnz_capacity == 0 || batch->bags.nnz <= opts->nnz_capacity,
+          "batch nnz %lld exceeds nnz_capacity %lld", (long long)batch->bags.nnz,
+          (long long)opts->nnz_capacity);
+  Plan P;
+  const int64_t cap = opts->nnz_capacity > 0 ? opts->nnz_capacity : batch->bags.nnz;
+  lattice_status st = make_plan(m, B, cap, opts, &P);
+  if (st != LATTICE_OK) return st;
+  st = check_tables(&m->tables, &batch->bags);
+  if (st != LATTICE_OK) return st;
+  if (ws_bytes < (size_t)P.L.total_bytes || !ws)
+    FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %lld", ws_bytes, (long long)P.L.total_bytes);
+  REQUIRE(batch->labels && batch->mask, "null labels/mask");
+  if (m->dense_in > 0) REQUIRE(batch->dense || B == 0, "null dense input");
+  if (B == 0) return LATTICE_OK;
+
+  hipStream_t s = strm(stream);
+  auto mark = [&](int i) -> hipError_t {
+    return opts->stage_events ? hipEventRecord((hipEvent_t)opts->stage_events[i], s) : hipSuccess;
+  };
+  char* base = (char*)ws;
+  auto at = [&](int64_t o) -> void* { return o < 0 ? nullptr : base + o; };
+  const lattice_step_layout& L = P.L;
+  const DType dt = dt_of(m->dtype);
+  const int d = m->tables.dim, n = P.n, T = P.T;
+  const int s0 = m->dense_in > 0 ? 1 : 0;
+  void* X = at(L.X);
+  void* t = at(L.t);
+  void* scratch = at(L.scratch);
+
+  HIPRET(mark(0));
+  // 1. pooled lookups -> embedding slots of X
+  HIPRET(embbag_fwd(m->tables.data, dt, d, m->tables.row_base, batch->bags.offsets,
+                    batch->bags.indices, m->num_features, B, m->pool == LATTICE_POOL_MEAN, X, dt,
+                    n, s0, s));
+  HIPRET(mark(1));
+  // 2. bottom MLP -> slot 0 of X
+  void* bacts[LATTICE_MAX_LAYERS];
+  int64_t bstr[LATTICE_MAX_LAYERS];
+  if (m->dense_in > 0) {
+    const int nb = m->bottom.n_layers;
+    for (int i = 0; i + 1 < nb; ++i) {
+      bacts[i] = at(L.bottom_act[i]);
+      bstr[i] = m->bottom.layers[i].out_dim;
+    }
+    bacts[nb - 1] = X;
+    bstr[nb - 1] = (int64_t)n * d;
+    HIPRET(mlp_forward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, s));
+  }
+  HIPRET(mark(2));
+  // 3. interaction -> top input t = [X[:,0,:], interaction]
+  HIPRET(interact_fwd_impl(&m->interact, B, X, t, P.t_stride, s));
+  HIPRET(mark(3));
+  // 4. top MLP -> logits; 5. masked BCE
+  const int nt = m->top.n_layers;
+  void* tacts[LATTICE_MAX_LAYERS];
+  int64_t tstr[LATTICE_MAX_LAYERS];
+  for (int i = 0; i + 1 < nt; ++i) {
+    tacts[i] = at(L.top_act[i]);
+    tstr[i] = m->top.layers[i].out_dim;
+  }
+  tacts[nt - 1] = at(L.logits);
+  tstr[nt - 1] = T;
+  HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, s));
+  HIPRET(mark(4));
+  HIPRET(bce((const float*)at(L.logits), batch->labels, batch->mask, (int64_t)B * T,
+             (float*)at(L.loss), (float*)at(L.d_logits), at(L.d_logits_op), dt, scratch, s));
+  HIPRET(mark(5));
+  // 6. top backward -> d_t
+  HIPRET(mlp_backward(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, at(L.d_t),
+                      P.t_stride, at(P.g_top[0]), at(P.g_top[1]), scratch, s));
+  HIPRET(mark(6));
+  // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
+  void* dX = at(L.dX);
+  HIPRET(interact_bwd_impl(&m->interact, B, X, at(L.d_t), P.t_stride, dX, scratch, s));
+  HIPRET(mark(7));
+  // 8. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
+  if (m->dense_in > 0) {
+    void* masked = at(P.g_bot[1]);
+    relu_mask_kernel<<<cdiv((int64_t)B * d, 256), 256, 0, s>>>(dX, (int64_t)n * d, X,
+                                                               (int64_t)n * d, B, d,
+                                                               dt == DT_BF16, masked);
+    if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
+    // g buffers: masked lives in g_bot[1]; the first hidden gradient goes to g_bot[0]
+    HIPRET(mlp_backward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, masked, d,
+                        nullptr, 0, at(P.g_bot[0]), at(P.g_top[0]), scratch, s));
+  }
+  HIPRET(mark(8));
+  // 9. row-coalesced embedding gradient (+ row-sparse SGD)
+  HIPRET(embbag_bwd(m->tables.row_base, m->tables.total_rows, batch->bags.offsets,
+                    batch->bags.indices, m->num_features, B, batch->bags.nnz,
+                    m->pool == LATTICE_POOL_MEAN, dX, dt, n, s0, d, (int*)at(L.unique_rows),
+                    (int*)at(L.seg_offsets), (int*)at(L.sorted_bags), (int*)at(L.num_unique),
+                    (float*)at(L.grad_rows), m->tables.data, dt, opts->lr_tables, scratch, s));
+  HIPRET(mark(9));
+  return LATTICE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,68 @@
+// Internal launchers (namespace lat).  Every launcher enqueues on the given
+// stream and returns the first HIP error (with lat::set_error detail).
+#pragma once
+#include "common.h"
+
+namespace lat {
+
+// sort.hip
+size_t scan_workspace(int64_t n);
+hipError_t exclusive_scan(const int* in, int* out, int64_t n, int* tmp, hipStream_t s);
+hipError_t exclusive_scan_inplace_small(int* a, int n, hipStream_t s);
+size_t radix_sort_workspace(int64_t n);
+hipError_t radix_sort_pairs(int* keys, int* vals, int64_t n, int64_t max_key, int* keys_out,
+                            int* vals_out, void* ws, hipStream_t s);
+
+// embbag.hip
+hipError_t embbag_fwd(const void* E, DType edt, int dim, const int64_t* row_base,
+                      const int32_t* offsets, const int32_t* indices, int F, int B, int mean,
+                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s);
+size_t embbag_bwd_workspace(int64_t nnz, int dim);
+hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t* offsets,
+                      const int32_t* indices, int F, int B, int64_t nnz, int mean,
+                      const void* dX, DType dxt, int n_slots, int first_slot, int dim,
+                      int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
+                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s);
+hipError_t validate_batch(const int64_t* row_base, const int32_t* offsets,
+                          const int32_t* indices, int F, int B, int64_t nnz,
+                          unsigned long long* dev_result, hipStream_t s);
+
+// gemm.hip
+struct GemmArgs {
+  DType dt = DT_BF16;          // operand dtype
+  const void* A = nullptr; int64_t lda = 0; int ta = 0;
+  const void* B = nullptr; int64_t ldb = 0; int tb = 0;
+  void* C = nullptr; int64_t ldc = 0; DType c_dt = DT_F32;
+  int M = 0, N = 0, K = 0;
+  const float* bias = nullptr;
+  int relu = 0;
+  const void* mask = nullptr; DType mask_dt = DT_BF16; int64_t ldm = 0;
+  int max_splits = 1;          // split-K only when the caller provides gemm_workspace()
+};
+int gemm_splits(const GemmArgs& g);
+size_t gemm_workspace(const GemmArgs& g);
+hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t s);
+size_t colsum_workspace(int M, int N);
+hipError_t colsum(const void* G, DType dt, int64_t ld, int M, int N, float* out, void* ws,
+                  hipStream_t s);
+
+// interact.hip
+size_t dot_lds_bytes(int n, int d);
+size_t fm_lds_bytes(int n, int d, int k);
+hipError_t dot_fwd(DType dt, const void* X, int B, int n, int d, void* out, int64_t ostride,
+                   int emit0, hipStream_t s);
+hipError_t dot_bwd(DType dt, const void* X, int B, int n, int d, const void* dout,
+                   int64_t dstride, int emit0, void* dX, hipStream_t s);
+hipError_t fm_fwd(DType dt, const void* X, const void* W, int B, int n, int d, int k, void* out,
+                  int64_t ostride, int emit0, hipStream_t s);
+size_t fm_bwd_workspace(int n, int k);
+hipError_t fm_bwd(DType dt, const void* X, const void* W, int B, int n, int d, int k,
+                  const void* dout, int64_t dstride, int emit0, const float* addend,
+                  void* dX, DType dxt, float* dW, void* ws, hipStream_t s);
+
+// loss.hip
+size_t bce_workspace(int64_t n);
+hipError_t bce(const float* z, const float* y, const uint8_t* m, int64_t n, float* loss, float* dz,
+               void* dz_op, DType op_dt, void* ws, hipStream_t s);
+
+}  // namespace lat

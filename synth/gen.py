@@ -266,3 +266,33 @@ def randn(shape, seed: int, stream: int = 0, scale: float = 1.0, dtype: str = "f
     if dtype == "bf16":
         x = to_storage(x, "bf16").float().numpy()
     return x
+
+
+def sub_batch(cfg: Config, batch: Dict[str, np.ndarray], samples):
+    """The batch restricted to ``samples`` (all features, feature-major), with
+    the table rows it touches renumbered compactly.  Returns
+    ``(sub_cfg, sub, global_rows)``: ``global_rows[i]`` is the global table row
+    behind compact row ``i``, so the caller gathers the compact table as
+    ``E[global_rows]``.  Pure index plumbing."""
+    samples = np.asarray(samples, dtype=np.int64)
+    B, F = cfg.B, cfg.F
+    off = batch["offsets"].astype(np.int64)
+    lens, idx_parts, rows_parts, base = [], [], [], [0]
+    for f in range(F):
+        bags = f * B + samples
+        lo, hi = off[bags], off[bags + 1]
+        idx = np.concatenate([batch["indices"][a:b] for a, b in zip(lo, hi)]).astype(np.int64) \
+            if samples.size else np.zeros(0, np.int64)
+        rb = int(batch["row_base"][f])
+        uniq, inv = np.unique(idx, return_inverse=True)
+        rows_parts.append(rb + uniq)
+        idx_parts.append(inv.astype(np.int32))
+        lens.append(hi - lo)
+        base.append(base[-1] + uniq.size)
+    lens = np.concatenate(lens)
+    sub = dict(offsets=np.concatenate([[0], np.cumsum(lens)]).astype(np.int32),
+               indices=np.concatenate(idx_parts).astype(np.int32),
+               row_base=np.array(base, dtype=np.int64),
+               dense=batch["dense"][samples], labels=batch["labels"][samples],
+               mask=batch["mask"][samples], domain=batch["domain"][samples])
+    return cfg.scaled(B=int(samples.size)), sub, np.concatenate(rows_parts)

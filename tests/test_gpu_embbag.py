@@ -1,0 +1,144 @@
+"""Parity of the pooled lookup and its deterministic sparse gradient against
+the oracle (bookkeeping bit-exact; values to the workload's tolerance)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import embbag as oe
+from oracle.step import rounding
+from tests._util import DEV, Workload, assert_close, tol
+
+CASES = {
+    "cfg1": synth.CFG1,
+    "cfg1-mean": synth.CFG1.scaled(pool="mean"),
+    "cfg2-small": synth.small(synth.CFG2, B=256, rows=3000),
+    "cfg4-small-empty-bags": synth.small(synth.CFG4, B=192, rows=1500),
+    "cfg3-small": synth.small(synth.CFG3, B=64, rows=20000),
+}
+
+
+def _X(w, fill):
+    c = w.cfg
+    return torch.full((c.B, c.n_slots, c.d), fill, dtype=synth.torch_dtype(c.dtype), device=DEV)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(CASES))
+def test_embbag_fwd(name):
+    from paper_2512_09200_amd import api
+    cfg = CASES[name]
+    print(f"[embbag_fwd] {name} B={cfg.B} F={cfg.F} d={cfg.d} {cfg.dtype}", flush=True)
+    w = Workload(cfg)
+    X = _X(w, float("nan"))
+    api.lattice_embbag_fwd(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B, X,
+                           cfg.first_emb_slot, cfg.pool)
+    torch.cuda.synchronize()
+    ref = rounding(cfg.dtype)(oe.pool_forward(w.table_np(), w.batch["row_base"], w.batch["offsets"],
+                                              w.batch["indices"], cfg.F, cfg.B, cfg.pool))
+    assert_close("X", X[:, cfg.first_emb_slot:], ref, tol(cfg))
+    if cfg.first_emb_slot:
+        assert torch.isnan(X[:, 0].float()).all(), "slot 0 must not be touched"
+    empty = np.diff(w.batch["offsets"]).reshape(cfg.F, cfg.B) == 0
+    if empty.any():
+        got = X[:, cfg.first_emb_slot:].float().cpu().numpy().transpose(1, 0, 2)
+        assert np.all(got[empty] == 0), "empty bags must pool to exact zeros"
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("lr", [0.0, 0.5])
+def test_embbag_bwd(name, lr):
+    from paper_2512_09200_amd import api
+    cfg = CASES[name]
+    print(f"[embbag_bwd] {name} lr={lr}", flush=True)
+    w = Workload(cfg)
+    rnd = rounding(cfg.dtype)
+    dX_np = synth.randn((cfg.B, cfg.n_slots, cfg.d), seed=cfg.seed, stream=1, scale=1e-2,
+                        dtype=cfg.dtype)
+    dX = torch.from_numpy(dX_np).to(synth.torch_dtype(cfg.dtype)).to(DEV)
+    E0 = w.table_np()
+    out = api.lattice_embbag_bwd(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B, dX,
+                                 cfg.first_emb_slot, lr=lr, pool=cfg.pool)
+    torch.cuda.synchronize()
+    b = w.batch
+    bk = oe.bookkeeping(b["row_base"], b["offsets"], b["indices"], cfg.F, cfg.B)
+    uniq, G = oe.pool_backward(dX_np[:, cfg.first_emb_slot:], b["row_base"], b["offsets"],
+                               b["indices"], cfg.F, cfg.B, cfg.pool)
+    U = int(out["num_unique"].item())
+    assert U == uniq.size
+    np.testing.assert_array_equal(out["unique_rows"][:U].cpu().numpy(), bk["unique_rows"])
+    seg = np.append(bk["seg_offsets"], w.nnz)
+    np.testing.assert_array_equal(out["seg_offsets"][:U + 1].cpu().numpy(), seg)
+    np.testing.assert_array_equal(out["sorted_bags"][:w.nnz].cpu().numpy(), bk["sorted_bags"])
+    assert_close("grad_rows", out["grad_rows"][:U], G, tol(cfg))
+    E1 = w.table_np()
+    if lr:
+        assert_close("updated_rows", E1[uniq], oe.sgd_rows(E0[uniq], G, lr, rnd), tol(cfg))
+        untouched = np.ones(E0.shape[0], bool)
+        untouched[uniq] = False
+        assert np.array_equal(E1[untouched], E0[untouched]), "untouched rows changed"
+    else:
+        assert np.array_equal(E1, E0)
+
+
+@pytest.mark.gpu
+def test_embbag_bwd_hot_row_spanning_many_chunks():
+    """One row hit 5000 times in a bag plus singles: a run spanning ~80 chunks."""
+    from paper_2512_09200_amd import api
+    cfg = synth.Config(name="hot", B=4, F=2, rows=1000, d=64, dtype="bf16", index_dist=("uniform",),
+                       bag_dist=("uniform", 1, 1), dense_in=0, bottom=(), interact="dot", top=(1,))
+    lens = np.array([5000, 1, 3, 0, 7, 2, 0, 1])
+    offsets = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    idx = np.concatenate([np.full(5000, 17), [3], [17, 17, 999], [5, 6, 17, 17, 0, 999, 998], [1, 1], [17]]).astype(np.int32)
+    row_base = np.array([0, 1000, 2000])
+    E = torch.randn((2000, 64), device=DEV).mul_(0.01).to(torch.bfloat16)
+    dX_np = synth.randn((4, 2, 64), seed=5, stream=2, dtype="bf16")
+    dX = torch.from_numpy(dX_np).to(torch.bfloat16).to(DEV)
+    E0 = E.float().cpu().double().numpy()
+    out = api.lattice_embbag_bwd(E, torch.from_numpy(row_base).to(DEV), torch.from_numpy(offsets).to(DEV),
+                                 torch.from_numpy(idx).to(DEV), 2, 4, dX, 0, lr=0.25)
+    torch.cuda.synchronize()
+    bk = oe.bookkeeping(row_base, offsets, idx, 2, 4)
+    uniq, G = oe.pool_backward(dX_np, row_base, offsets, idx, 2, 4)
+    U = int(out["num_unique"].item())
+    np.testing.assert_array_equal(out["unique_rows"][:U].cpu().numpy(), bk["unique_rows"])
+    np.testing.assert_array_equal(out["sorted_bags"][:idx.size].cpu().numpy(), bk["sorted_bags"])
+    assert_close("grad_rows", out["grad_rows"][:U], G, 2e-2)
+    E1 = E.float().cpu().double().numpy()
+    from oracle.bf16 import round_bf16
+    assert_close("updated_rows", E1[uniq], oe.sgd_rows(E0[uniq], G, 0.25, round_bf16), 2e-2)
+
+
+@pytest.mark.gpu
+def test_embbag_bwd_is_deterministic():
+    from paper_2512_09200_amd import api
+    cfg = CASES["cfg2-small"]
+    w = Workload(cfg)
+    dX = torch.from_numpy(synth.randn((cfg.B, cfg.n_slots, cfg.d), seed=9, dtype=cfg.dtype)).to(
+        torch.bfloat16).to(DEV)
+    r1 = api.lattice_embbag_bwd(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B, dX, 1)
+    r2 = api.lattice_embbag_bwd(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B, dX, 1)
+    torch.cuda.synchronize()
+    U = int(r1["num_unique"].item())
+    assert U == int(r2["num_unique"].item())
+    # only the first num_unique entries (num_unique+1 offsets) are defined
+    for k, n in (("unique_rows", U), ("seg_offsets", U + 1), ("sorted_bags", w.nnz), ("grad_rows", U)):
+        assert torch.equal(r1[k][:n], r2[k][:n]), k
+
+
+@pytest.mark.gpu
+def test_validate_batch():
+    from paper_2512_09200_amd import api
+    cfg = CASES["cfg2-small"]
+    w = Workload(cfg)
+    ok, _ = api.lattice_validate_batch(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B)
+    assert ok
+    bad = w.indices.clone()
+    bad[123] = cfg.rows          # one past the end of its table
+    ok, pos = api.lattice_validate_batch(w.E, w.row_base, w.offsets, bad, cfg.F, cfg.B)
+    assert not ok and pos == 123
+    off = w.offsets.clone()
+    off[10] = off[11] + 1        # non-monotone
+    ok, pos = api.lattice_validate_batch(w.E, w.row_base, off, w.indices, cfg.F, cfg.B)
+    assert not ok and pos < 0

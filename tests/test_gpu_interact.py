@@ -1,0 +1,67 @@
+"""Parity of the DOT and FM interaction kernels (forward and backward)
+against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import interact as oi
+from oracle.step import rounding
+from tests._util import DEV, assert_close, to_dev
+
+CASES = {
+    # name: (kind, dtype, B, n, d, k, emit0, zero_slots)
+    "dot-f32-cfg1": ("dot", "f32", 128, 9, 32, 0, True, False),
+    "dot-bf16-cfg2": ("dot", "bf16", 300, 27, 64, 0, True, False),
+    "dot-bf16-cfg4-absent": ("dot", "bf16", 96, 97, 128, 0, True, True),
+    "fm-bf16-cfg3": ("fm", "bf16", 200, 65, 128, 32, True, False),
+    "fm-f32-small": ("fm", "f32", 50, 10, 32, 16, False, False),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(CASES))
+def test_interact_fwd_bwd(name):
+    from paper_2512_09200_amd import api
+    kind, dt, B, n, d, k, emit0, zero_slots = CASES[name]
+    print(f"[interact] {name}", flush=True)
+    rnd = rounding(dt)
+    sdt = synth.torch_dtype(dt)
+    t = 1e-5 if dt == "f32" else 2e-2
+    X = synth.randn((B, n, d), seed=21, scale=0.05, dtype=dt)
+    if zero_slots:
+        r = np.random.default_rng(5)
+        X[r.random((B, n)) < 0.58] = 0.0
+    Xd = to_dev(X, sdt)
+    W = synth.randn((n, k), seed=22, scale=1 / np.sqrt(n), dtype=dt) if kind == "fm" else None
+    Wd = to_dev(W, sdt) if W is not None else None
+    width = (n * (n - 1) // 2 if kind == "dot" else n * k)
+    off = d if emit0 else 0
+    stride = (off + width + 7) // 8 * 8
+    out = torch.full((B, stride), 7.0, dtype=sdt, device=DEV)
+    api.lattice_interact_fwd(kind, Xd, out, emit_slot0=emit0, fm_W=Wd)
+    torch.cuda.synchronize()
+    if kind == "dot":
+        ref = oi.dot_forward(X, rnd)
+    else:
+        O, P = oi.fm_forward(X, W, rnd)
+        ref = O.reshape(B, -1)
+    assert_close("out", out[:, off:off + width], ref, t)
+    if emit0:
+        assert torch.equal(out[:, :d], Xd[:, 0]), "slot 0 copy"
+    assert (out[:, off + width:].float() == 7.0).all(), "padding columns touched"
+    # backward
+    G = synth.randn((B, stride), seed=23, scale=1e-3, dtype=dt)
+    Gd = to_dev(G, sdt)
+    dX = torch.zeros((B, n, d), dtype=sdt, device=DEV)
+    dW = torch.zeros((n, k), device=DEV) if kind == "fm" else None
+    api.lattice_interact_bwd(kind, Xd, Gd, dX, emit_slot0=emit0, fm_W=Wd, fm_dW=dW)
+    torch.cuda.synchronize()
+    if kind == "dot":
+        dref = oi.dot_backward(G[:, off:off + width], X)
+    else:
+        dref, dWref = oi.fm_backward(G[:, off:off + width].reshape(B, n, k), X, W, P, rnd)
+        assert_close("fm_dW", dW, dWref, t)
+    if emit0:
+        dref[:, 0] += G[:, :d]
+    assert_close("dX", dX, rnd(dref), t)

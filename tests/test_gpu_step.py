@@ -1,0 +1,109 @@
+"""End-to-end parity of lattice_step (forward + backward + sparse gradient
++ row-sparse SGD) against the oracle on seeded workloads with the structure of
+each configuration."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import embbag as oe
+from oracle import step as ostep
+from tests._util import DEV, Workload, assert_close, assert_close_composed, relu_overrides, tol
+
+CASES = {
+    "cfg1": (synth.CFG1, 0.0),
+    "cfg2-small": (synth.small(synth.CFG2, B=256, rows=3000), 0.0),
+    "cfg3-small": (synth.small(synth.CFG3, B=128, rows=6000), 0.01),
+    "cfg3-small-big-lr": (synth.small(synth.CFG3, B=96, rows=6000), 1000.0),
+    "cfg4-small": (synth.small(synth.CFG4, B=256, rows=2000), 0.0),
+}
+SPARE = {"cfg2-small": 12345}   # workspace planned with more lookups than the batch has
+
+
+def gpu_relu_io(cfg, w, v):
+    """Per-layer GPU inputs and outputs of the ReLU layers (see relu_overrides)."""
+    bout = v["bottom_act"] + ([v["X"][:, 0]] if cfg.has_dense else [])
+    bin_ = ([w.dense] + v["bottom_act"]) if cfg.has_dense else []
+    tout = v["top_act"]
+    tin = [v["t"][:, :cfg.top_in]] + v["top_act"]
+    return dict(bottom=bin_, top=tin), dict(bottom=bout, top=tout)
+
+
+def run_step(w, lr, emit=True, spare=0):
+    """One step; the workspace is planned for nnz + spare lookups."""
+    from paper_2512_09200_amd import api
+    cfg = w.cfg
+    model = w.step_model()
+    lay = api.lattice_step_plan(model, cfg.B, w.nnz + spare, lr, emit)
+    ws = torch.zeros(lay.total_bytes, dtype=torch.uint8, device=DEV)
+    api.lattice_step(model, w.offsets, w.indices, w.dense, w.labels, w.mask, ws, lr, emit,
+                     nnz_capacity=w.nnz + spare)
+    torch.cuda.synchronize()
+    return model, api.step_views(model, ws, lay, cfg.B, cfg.T, w.nnz), ws
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(CASES))
+def test_step_matches_oracle(name):
+    cfg, lr = CASES[name]
+    print(f"[step] {name} B={cfg.B} F={cfg.F} rows={cfg.rows} lr={lr}", flush=True)
+    w = Workload(cfg)
+    E0 = w.table_np()
+    _, v, _ = run_step(w, lr, spare=SPARE.get(name, 0))
+    t = tol(cfg)
+    s0 = cfg.first_emb_slot
+    ov, nband, nflip = relu_overrides(cfg, w.params, E0, w.batch, *gpu_relu_io(cfg, w, v))
+    print(f"  ReLU decisions in the ambiguity band: {nband}, taken the other way: {nflip}", flush=True)
+    c, g = ostep.step(cfg, w.params, E0, w.batch, lr_tables=lr, overrides=ov)
+    # the pooled lookups are one stage: compared element-wise
+    assert_close("X[emb]", v["X"][:, s0:], c["X"][:, s0:], t)
+    for name_, got_, ref_ in [("X", v["X"], c["X"]), ("t", v["t"][:, :cfg.top_in], c["t"]),
+                              ("logits", v["logits"], c["logits"]),
+                              ("loss", v["loss"], np.array([c["loss"]])),
+                              ("d_logits", v["d_logits"], c["dz"]),
+                              ("d_t", v["d_t"][:, :cfg.top_in], g["d_top_in"])]:
+        assert_close_composed(name_, got_, ref_, t)
+    for i in range(len(w.top)):
+        assert_close_composed(f"top{i}.dW", w.top[i]["dW"], g["top_dW"][i], t, strict_bound=0.5)
+        assert_close_composed(f"top{i}.db", w.top[i]["db"], g["top_db"][i], t)
+    for i in range(len(w.bottom)):
+        assert_close_composed(f"bottom{i}.dW", w.bottom[i]["dW"], g["bottom_dW"][i], t, strict_bound=0.5)
+        assert_close_composed(f"bottom{i}.db", w.bottom[i]["db"], g["bottom_db"][i], t)
+    if cfg.interact == "fm":
+        assert_close_composed("fm.dW", w.fm_dW, g["fm_dW"], t)
+    assert_close_composed("dX_emb", v["dX"][:, s0:], g["dX_emb"], t)
+    bk = g["bookkeeping"]
+    U = int(v["num_unique"].item())
+    assert U == bk["unique_rows"].size
+    np.testing.assert_array_equal(v["unique_rows"][:U].cpu().numpy(), bk["unique_rows"])
+    np.testing.assert_array_equal(v["seg_offsets"][:U + 1].cpu().numpy(), np.append(bk["seg_offsets"], w.nnz))
+    np.testing.assert_array_equal(v["sorted_bags"][:w.nnz].cpu().numpy(), bk["sorted_bags"])
+    assert_close_composed("grad_rows", v["grad_rows"][:U], g["grad_rows"], t)
+    E1 = w.table_np()
+    if lr:
+        uniq = g["unique_rows"]
+        assert_close_composed("updated_rows", E1[uniq], g["updated_rows"], t)
+        keep = np.ones(E0.shape[0], bool)
+        keep[uniq] = False
+        assert np.array_equal(E1[keep], E0[keep])
+    else:
+        assert np.array_equal(E1, E0)
+
+
+@pytest.mark.gpu
+def test_step_is_deterministic():
+    cfg = synth.small(synth.CFG3, B=128, rows=6000)
+    w = Workload(cfg)
+    _, v1, ws1 = run_step(w, 0.0)
+    g1 = [L["dW"].clone() for L in w.top + w.bottom] + [w.fm_dW.clone()]
+    _, v2, ws2 = run_step(w, 0.0)
+    g2 = [L["dW"].clone() for L in w.top + w.bottom] + [w.fm_dW.clone()]
+    U = int(v1["num_unique"].item())
+    assert U == int(v2["num_unique"].item())
+    for k in ("X", "t", "logits", "loss", "dX", "sorted_bags"):
+        assert torch.equal(v1[k], v2[k]), k
+    for k in ("unique_rows", "grad_rows"):
+        assert torch.equal(v1[k][:U], v2[k][:U]), k
+    assert torch.equal(v1["seg_offsets"][:U + 1], v2["seg_offsets"][:U + 1])
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
