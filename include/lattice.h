@@ -89,7 +89,7 @@ typedef struct {
 typedef struct {
   void* data;                /* device [total_rows, dim], dtype */
   lattice_dtype dtype;
-  int32_t dim;               /* d: multiple of 8 (bf16) or 4 (fp32), <= 256 */
+  int32_t dim;               /* d: multiple of 8, <= 256 */
   int64_t total_rows;        /* < 2^31 */
   const int64_t* row_base;   /* device [F+1] */
 } lattice_tables;
@@ -308,6 +308,7 @@ typedef struct {
   int64_t bottom_act[LATTICE_MAX_LAYERS];   /* [B, out_i] hidden bottom outputs (last: in X) */
   int64_t top_act[LATTICE_MAX_LAYERS];      /* [B, out_i] hidden top outputs (last: logits) */
   int64_t unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows;
+  int64_t keys, vals;   /* [nnz] int32: sort keys (global row) and bag ids, built by the forward */
   int64_t scratch;      /* shared scratch of the stages */
   int64_t scratch_bytes;
 } lattice_step_layout;

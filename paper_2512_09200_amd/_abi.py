@@ -87,7 +87,8 @@ class lattice_step_layout(Structure):
                  ("loss", c_int64), ("d_t", c_int64), ("dX", c_int64),
                  ("bottom_act", c_int64 * MAX_LAYERS), ("top_act", c_int64 * MAX_LAYERS)]
                 + [(k, c_int64) for k in ("unique_rows", "seg_offsets", "sorted_bags",
-                                          "num_unique", "grad_rows", "scratch", "scratch_bytes")])
+                                          "num_unique", "grad_rows", "keys", "vals", "scratch",
+                                          "scratch_bytes")])
 
 
 # (name, restype, argtypes)

@@ -45,8 +45,8 @@ static inline size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static lattice_status check_dim(int dim, lattice_dtype dt) {
   if (dim <= 0 || dim > 256) FAIL(LATTICE_ERR_UNSUPPORTED, "dim %d outside 1..256", dim);
-  if (dt == LATTICE_BF16 && dim % 8) FAIL(LATTICE_ERR_UNSUPPORTED, "bf16 dim %d not a multiple of 8", dim);
-  if (dt == LATTICE_F32 && dim % 4) FAIL(LATTICE_ERR_UNSUPPORTED, "fp32 dim %d not a multiple of 4", dim);
+  if (dim % 8) FAIL(LATTICE_ERR_UNSUPPORTED, "dim %d not a multiple of 8", dim);
+  (void)dt;
   return LATTICE_OK;
 }
 
@@ -185,14 +185,24 @@ static int64_t interact_width(const lattice_interact_desc* d) {
   return w + (d->emit_slot0 ? d->dim : 0);
 }
 
+// The MFMA path reads and writes rows with 4-byte accesses: row strides must
+// keep every row 16-byte aligned.
+static bool fm_uses_mfma(const lattice_interact_desc* d, int64_t stride = 8) {
+  return d->dtype == LATTICE_BF16 && fm_mfma_supported(d->n, d->dim, d->rank) && stride % 8 == 0;
+}
+
 static size_t interact_ws(const lattice_interact_desc* d) {
-  return d->kind == LATTICE_INTERACT_FM ? fm_bwd_workspace(d->n, d->rank) : 0;
+  if (d->kind != LATTICE_INTERACT_FM) return 0;
+  return std::max(fm_mfma_bwd_workspace(d->n, d->rank), fm_bwd_workspace(d->n, d->rank));
 }
 
 static hipError_t interact_fwd_impl(const lattice_interact_desc* d, int B, const void* X,
                                     void* out, int64_t os, hipStream_t s) {
   if (d->kind == LATTICE_INTERACT_DOT)
     return dot_fwd(dt_of(d->dtype), X, B, d->n, d->dim, out, os, d->emit_slot0, s);
+  if (fm_uses_mfma(d, os))
+    return fm_mfma(true, X, d->fm_W, B, d->n, d->dim, d->rank, out, os, d->emit_slot0, nullptr, 0,
+                   nullptr, nullptr, nullptr, nullptr, nullptr, s);
   return fm_fwd(dt_of(d->dtype), X, d->fm_W, B, d->n, d->dim, d->rank, out, os, d->emit_slot0, s);
 }
 
@@ -201,6 +211,9 @@ static hipError_t interact_bwd_impl(const lattice_interact_desc* d, int B, const
                                     hipStream_t s) {
   if (d->kind == LATTICE_INTERACT_DOT)
     return dot_bwd(dt_of(d->dtype), X, B, d->n, d->dim, dout, ds, d->emit_slot0, dX, s);
+  if (fm_uses_mfma(d, ds))
+    return fm_mfma(false, X, d->fm_W, B, d->n, d->dim, d->rank, nullptr, 0, d->emit_slot0, dout, ds,
+                   nullptr, dX, nullptr, d->fm_dW, ws, s);
   return fm_bwd(dt_of(d->dtype), X, d->fm_W, B, d->n, d->dim, d->rank, dout, ds, d->emit_slot0,
                 nullptr, dX, dt_of(d->dtype), d->fm_dW, ws, s);
 }
@@ -533,6 +546,8 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   L.sorted_bags = take((size_t)nn * 4);
   L.num_unique = take(4);
   L.grad_rows = (o && o->emit_grad_rows) ? take((size_t)nn * d * 4) : -1;
+  L.keys = take((size_t)nn * 4);
+  L.vals = take((size_t)nn * 4);
   size_t sc = 0;
   sc = std::max(sc, mlp_bwd_ws(&m->top, B));
   if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
@@ -597,7 +612,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   // 1. pooled lookups -> embedding slots of X
   HIPRET(embbag_fwd(m->tables.data, dt, d, m->tables.row_base, batch->bags.offsets,
                     batch->bags.indices, m->num_features, B, m->pool == LATTICE_POOL_MEAN, X, dt,
-                    n, s0, s));
+                    n, s0, s, (int*)at(L.keys), (int*)at(L.vals)));
   HIPRET(mark(1));
   // 2. bottom MLP -> slot 0 of X
   void* bacts[LATTICE_MAX_LAYERS];
@@ -656,7 +671,8 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                     batch->bags.indices, m->num_features, B, batch->bags.nnz,
                     m->pool == LATTICE_POOL_MEAN, dX, dt, n, s0, d, (int*)at(L.unique_rows),
                     (int*)at(L.seg_offsets), (int*)at(L.sorted_bags), (int*)at(L.num_unique),
-                    (float*)at(L.grad_rows), m->tables.data, dt, opts->lr_tables, scratch, s));
+                    (float*)at(L.grad_rows), m->tables.data, dt, opts->lr_tables, scratch, s,
+                    (const int*)at(L.keys), (const int*)at(L.vals)));
   HIPRET(mark(9));
   return LATTICE_OK;
 }

@@ -33,7 +33,8 @@ template <typename TT, typename XT, int LP>
 __global__ __launch_bounds__(256) void embbag_fwd_kernel(
     const TT* __restrict__ E, const int64_t* __restrict__ row_base,
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ indices, int F, int B,
-    int dim, int mean, XT* __restrict__ X, int n_slots, int first_slot) {
+    int dim, int mean, XT* __restrict__ X, int n_slots, int first_slot, int* __restrict__ keys,
+    int* __restrict__ vals) {
   constexpr int VE = 16 / sizeof(TT);  // table elements per 16-byte lane chunk
   constexpr int G = 64 / LP;           // row groups per wave
   constexpr int U = (16 / G) > 0 ? (16 / G) : 1;  // loads in flight per group
@@ -46,6 +47,13 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
   const int start = offsets[bag], end = offsets[bag + 1];
   const TT* Ef = E + row_base[f] * (int64_t)dim + sub * VE;
 
+  if (keys) {  // sort keys of the backward (global row) and values (bag id), coalesced
+    const int rb = (int)row_base[f];
+    for (int q = start + lane; q < end; q += 64) {
+      keys[q] = rb + indices[q];
+      vals[q] = (int)bag;
+    }
+  }
   float acc[VE];
 #pragma unroll
   for (int i = 0; i < VE; ++i) acc[i] = 0.f;
@@ -95,14 +103,15 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
 template <typename TT, typename XT>
 static hipError_t embbag_fwd_t(const void* E, int dim, const int64_t* row_base,
                                const int32_t* offsets, const int32_t* indices, int F, int B,
-                               int mean, void* X, int n_slots, int first_slot, hipStream_t s) {
+                               int mean, void* X, int n_slots, int first_slot, int* keys,
+                               int* vals, hipStream_t s) {
   const int64_t bags = (int64_t)F * B;
   if (bags == 0) return hipSuccess;
   const int lanes = (int)((dim * sizeof(TT) + 15) / 16);
   const int grid = cdiv(bags, 4);
 #define LAT_FWD(LPV)                                                                       \
   embbag_fwd_kernel<TT, XT, LPV><<<grid, 256, 0, s>>>(                                    \
-      (const TT*)E, row_base, offsets, indices, F, B, dim, mean, (XT*)X, n_slots, first_slot)
+      (const TT*)E, row_base, offsets, indices, F, B, dim, mean, (XT*)X, n_slots, first_slot, keys, vals)
   if (lanes <= 1) LAT_FWD(1);
   else if (lanes <= 2) LAT_FWD(2);
   else if (lanes <= 4) LAT_FWD(4);
@@ -117,14 +126,15 @@ static hipError_t embbag_fwd_t(const void* E, int dim, const int64_t* row_base,
 
 hipError_t embbag_fwd(const void* E, DType edt, int dim, const int64_t* row_base,
                       const int32_t* offsets, const int32_t* indices, int F, int B, int mean,
-                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s) {
+                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s, int* keys,
+                      int* vals) {
   if (edt == DT_BF16 && xdt == DT_BF16)
-    return embbag_fwd_t<bf16_t, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
+    return embbag_fwd_t<bf16_t, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
   if (edt == DT_BF16 && xdt == DT_F32)
-    return embbag_fwd_t<bf16_t, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
+    return embbag_fwd_t<bf16_t, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
   if (edt == DT_F32 && xdt == DT_F32)
-    return embbag_fwd_t<float, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
-  return embbag_fwd_t<float, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
+    return embbag_fwd_t<float, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
+  return embbag_fwd_t<float, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -244,6 +254,14 @@ __device__ inline void finalize_row(int u, int row, float g, int a, int dim, flo
   }
 }
 
+// One block per chunk of CHUNK consecutive sorted occurrences.
+//  1. wave 0: keys and bags of the chunk; run boundaries by ballot; the
+//     pieces (maximal runs inside the chunk) with their end position, segment
+//     id and kind (complete run, or cut by the chunk start / end)
+//  2. all threads: gather the chunk's dX rows into LDS (fp32) and, at the same
+//     time, load the table rows of the complete runs that the SGD updates
+//  3. work items (piece, 8 columns): sum the piece's rows in position order
+//     and write the row gradient / apply the SGD / store the partial
 template <typename DT, typename ET>
 __global__ __launch_bounds__(256) void chunk_reduce_kernel(
     const int* __restrict__ skeys, const int* __restrict__ sbags, int n,
@@ -251,33 +269,77 @@ __global__ __launch_bounds__(256) void chunk_reduce_kernel(
     const int32_t* __restrict__ offsets, int mean, const int* __restrict__ chunk_uid,
     float* __restrict__ part, int* __restrict__ part_uid, int* __restrict__ span_list,
     int* __restrict__ span_count, float* __restrict__ grad_rows, ET* __restrict__ E, float lr) {
-  extern __shared__ float rows[];  // [CHUNK][dim]
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  DT* rows = reinterpret_cast<DT*>(smem_raw);  // [CHUNK][dim], the gathered dX rows as stored
   __shared__ int k_s[CHUNK];
   __shared__ int b_s[CHUNK];
   __shared__ float sc_s[CHUNK];
+  __shared__ int pend_s[CHUNK];    // end position of piece i
+  __shared__ int pkind_s[CHUNK];   // 1: complete run, 2: cut at chunk start (slot 0), 3: cut at end only (slot 1)
+  __shared__ int pu_s[CHUNK];      // segment id of piece i
+  __shared__ int npieces_s;
   const int c = blockIdx.x;
   const int64_t p0 = (int64_t)c * CHUNK;
   const int cnt = (int)((n - p0) < CHUNK ? (n - p0) : CHUNK);
   const int tid = threadIdx.x;
-  if (tid < cnt) {
-    k_s[tid] = skeys[p0 + tid];
-    const int bag = sbags[p0 + tid];
-    b_s[tid] = bag;
-    float sc = 1.f;
-    if (mean) {
-      const int len = offsets[bag + 1] - offsets[bag];
-      sc = 1.f / (float)len;
+  if (tid < CHUNK) {
+    const int key = tid < cnt ? skeys[p0 + tid] : -1;
+    const int prev = p0 > 0 ? skeys[p0 - 1] : -1;
+    const int next = (p0 + cnt < n) ? skeys[p0 + cnt] : -1;
+    const int key_prev = __shfl_up(key, 1, 64);
+    const bool starts = tid < cnt && tid > 0 && key != key_prev;
+    const uint64_t smask = __ballot(starts);
+    const uint64_t le = (tid == 63) ? ~0ull : ((2ull << tid) - 1);
+    const int u = chunk_uid[c] + __popcll(smask & le);
+    const int key_next = __shfl_down(key, 1, 64);
+    const bool ends = tid < cnt && (tid == cnt - 1 || key_next != key);
+    const uint64_t emask = __ballot(ends);
+    const bool starts_before = p0 > 0 && prev == __shfl(key, 0, 64);
+    const bool touch_start = (smask & le) == 0 && starts_before;
+    const bool touch_end = (tid == cnt - 1) && next == key;
+    if (tid < cnt) {
+      k_s[tid] = key;
+      const int bag = sbags[p0 + tid];
+      b_s[tid] = bag;
+      sc_s[tid] = mean ? 1.f / (float)(offsets[bag + 1] - offsets[bag]) : 1.f;
     }
-    sc_s[tid] = sc;
+    if (ends) {
+      const int i = __popcll(emask & (le >> 1));  // pieces ending before tid
+      pend_s[i] = tid;
+      pkind_s[i] = (!touch_start && !touch_end) ? 1 : (touch_start ? 2 : 3);
+      pu_s[i] = u;
+    }
+    if (tid == 0) npieces_s = __popcll(emask);
+    if (ends && tid == cnt - 1) {
+      part_uid[c] = touch_end ? u : -1;
+      if (touch_end && !touch_start) span_list[atomicAdd(span_count, 1)] = c;
+    }
   }
-  const int prev_key = p0 > 0 ? skeys[p0 - 1] : -1;
-  const int next_key = (p0 + cnt < n) ? skeys[p0 + cnt] : -1;
   __syncthreads();
 
-  // gather all rows of the chunk (16-byte vectors, 4 loads in flight per thread)
   constexpr int VE = 16 / sizeof(DT);
   const int vpr = dim / VE;
   const int total = cnt * vpr;
+  const int np = npieces_s;
+  const int ipr = dim / 8;          // work items per piece (8 columns each)
+  const int items = np * ipr;
+  // table rows of this thread's complete pieces: loads in flight with the gather
+  constexpr int EV = 8 * sizeof(ET) / 16;  // 16-byte vectors per 8 columns
+  u32x4 ev[4][EV];
+  if (E) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int it = tid + q * 256;
+      if (it < items) {
+        const int i = it / ipr, a = (it - i * ipr) * 8;
+        if (pkind_s[i] == 1) {
+          const ET* e = E + (int64_t)k_s[pend_s[i]] * dim + a;
+#pragma unroll
+          for (int h = 0; h < EV; ++h) ev[q][h] = ldg16(e + h * (16 / sizeof(ET)));
+        }
+      }
+    }
+  }
   for (int v0 = tid; v0 < total; v0 += 256 * 4) {
     u32x4 buf[4];
 #pragma unroll
@@ -295,86 +357,106 @@ __global__ __launch_bounds__(256) void chunk_reduce_kernel(
       const int v = v0 + q * 256;
       if (v < total) {
         const int r = v / vpr, col = (v % vpr) * VE;
-        float t[VE];
-        Vec16<DT>::unpack(buf[q], t);
-        if (mean) {
-#pragma unroll
-          for (int i = 0; i < VE; ++i) t[i] = t[i] * sc_s[r];
-        }
-#pragma unroll
-        for (int i = 0; i < VE; ++i) rows[r * dim + col + i] = t[i];
+        *reinterpret_cast<u32x4*>(rows + r * dim + col) = buf[q];
       }
     }
   }
   __syncthreads();
 
-  const bool starts_before = p0 > 0 && prev_key == k_s[0];
-  for (int a = tid; a < dim; a += 256) {
-    if (a == 0) part_uid[c] = -1;
-    float acc = 0.f;
-    int u = chunk_uid[c];
-    int first = 0;
-    for (int p = 0; p < cnt; ++p) {
-      acc += rows[p * dim + a];
-      const bool piece_end = (p == cnt - 1) || (k_s[p + 1] != k_s[p]);
-      if (piece_end) {
-        const bool touch_start = first == 0 && starts_before;
-        const bool touch_end = (p == cnt - 1) && next_key == k_s[p];
-        if (!touch_start && !touch_end) {
-          finalize_row<ET>(u, k_s[p], acc, a, dim, grad_rows, E, lr);
-        } else if (touch_start) {
-          part[((int64_t)c * 2 + 0) * dim + a] = acc;
-          if (touch_end && a == 0) part_uid[c] = u;
-        } else {
-          part[((int64_t)c * 2 + 1) * dim + a] = acc;
-          if (a == 0) {
-            part_uid[c] = u;
-            span_list[atomicAdd(span_count, 1)] = c;  // first chunk of a spanning run
+  // items beyond the first 1024 (dim > 128) load their table rows in place
+  for (int base = 0; base < items; base += 1024) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int it = base + tid + q * 256;
+      if (it >= items) continue;
+      const int i = it / ipr, a = (it - i * ipr) * 8;
+      const int pe = pend_s[i], ps = i == 0 ? 0 : pend_s[i - 1] + 1;
+      const int kind = pkind_s[i];
+      if (base > 0 && E && kind == 1) {
+        const ET* e = E + (int64_t)k_s[pe] * dim + a;
+#pragma unroll
+        for (int h = 0; h < EV; ++h) ev[q][h] = ldg16(e + h * (16 / sizeof(ET)));
+      }
+      float g[8];
+#pragma unroll
+      for (int h = 0; h < 8; ++h) g[h] = 0.f;
+      for (int p = ps; p <= pe; ++p) {
+        float x[8];
+#pragma unroll
+        for (int h = 0; h < 8; h += VE)
+          Vec16<DT>::unpack(*reinterpret_cast<const u32x4*>(rows + p * dim + a + h), x + h);
+        const float scl = sc_s[p];
+#pragma unroll
+        for (int h = 0; h < 8; ++h) g[h] += mean ? x[h] * scl : x[h];
+      }
+      if (kind == 1) {
+        if (grad_rows) {
+          float* gr = grad_rows + (int64_t)pu_s[i] * dim + a;
+          stg16(gr, u32x4{__float_as_uint(g[0]), __float_as_uint(g[1]), __float_as_uint(g[2]), __float_as_uint(g[3])});
+          stg16(gr + 4, u32x4{__float_as_uint(g[4]), __float_as_uint(g[5]), __float_as_uint(g[6]), __float_as_uint(g[7])});
+        }
+        if (E) {
+          constexpr int PV = 16 / sizeof(ET);
+          ET* e = E + (int64_t)k_s[pe] * dim + a;
+#pragma unroll
+          for (int h = 0; h < EV; ++h) {
+            float x[PV];
+            Vec16<ET>::unpack(ev[q][h], x);
+#pragma unroll
+            for (int t = 0; t < PV; ++t) x[t] = x[t] - lr * g[h * PV + t];
+            stg16(e + h * PV, Vec16<ET>::pack(x));
           }
         }
-        acc = 0.f;
-        first = p + 1;
-        ++u;
+      } else {
+        float* pp = part + ((int64_t)c * 2 + (kind - 2)) * dim + a;
+        stg16(pp, u32x4{__float_as_uint(g[0]), __float_as_uint(g[1]), __float_as_uint(g[2]), __float_as_uint(g[3])});
+        stg16(pp + 4, u32x4{__float_as_uint(g[4]), __float_as_uint(g[5]), __float_as_uint(g[6]), __float_as_uint(g[7])});
       }
     }
   }
 }
 
-// One block per spanning run (persistent grid): sums the run's partials in
-// chunk order; column a is split over J = blockDim/dim interleaved subsets
-// that are combined in a fixed order.
+// One wave per spanning run (persistent grid of 4-wave blocks): the run's
+// partials are summed in chunk order; lane l owns columns 2l, 2l+1.
 template <typename ET>
-__global__ __launch_bounds__(1024) void chunk_fixup_kernel(
+__global__ __launch_bounds__(256) void chunk_fixup_kernel(
     const int* __restrict__ span_list, const int* __restrict__ span_count,
     const int* __restrict__ part_uid, const int* __restrict__ seg_offsets,
     const int* __restrict__ unique_rows, const float* __restrict__ part, int dim,
     float* __restrict__ grad_rows, ET* __restrict__ E, float lr) {
-  __shared__ float red[1024];
   const int nspan = *span_count;
-  const int J = blockDim.x / dim;
-  const int a = threadIdx.x % dim, j = threadIdx.x / dim;
-  for (int i = blockIdx.x; i < nspan; i += gridDim.x) {
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6), nwaves = gridDim.x * 4;
+  for (int i = wave; i < nspan; i += nwaves) {
     const int c0 = span_list[i];
     const int u = part_uid[c0];
     const int end = seg_offsets[u + 1];
     const int ce = (end - 1) / CHUNK;
     const int Q = ce - c0 + 1;  // pieces: slot 1 of c0, slot 0 of c0+1..ce
-    float acc = 0.f;
-    if (j < J) {
-#pragma unroll 4
-      for (int q = j; q < Q; q += J) {
-        const int64_t slot = (q == 0) ? ((int64_t)c0 * 2 + 1) : ((int64_t)(c0 + q) * 2 + 0);
-        acc += part[slot * dim + a];
+    for (int a = 2 * lane; a < dim; a += 128) {
+      float s0 = 0.f, s1 = 0.f;
+      int q = 0;
+      for (; q + 8 <= Q; q += 8) {
+        float2 v[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int qq = q + t;
+          const int64_t slot = (qq == 0) ? ((int64_t)c0 * 2 + 1) : ((int64_t)(c0 + qq) * 2);
+          v[t] = *reinterpret_cast<const float2*>(part + slot * dim + a);
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) { s0 += v[t].x; s1 += v[t].y; }
       }
-      red[j * dim + a] = acc;
+      for (; q < Q; ++q) {
+        const int64_t slot = (q == 0) ? ((int64_t)c0 * 2 + 1) : ((int64_t)(c0 + q) * 2);
+        const float2 v = *reinterpret_cast<const float2*>(part + slot * dim + a);
+        s0 += v.x;
+        s1 += v.y;
+      }
+      const int row = unique_rows[u];
+      finalize_row<ET>(u, row, s0, a, dim, grad_rows, E, lr);
+      finalize_row<ET>(u, row, s1, a + 1, dim, grad_rows, E, lr);
     }
-    __syncthreads();
-    if (j == 0) {
-      float s = 0.f;
-      for (int jj = 0; jj < J; ++jj) s += red[jj * dim + a];
-      finalize_row<ET>(u, unique_rows[u], s, a, dim, grad_rows, E, lr);
-    }
-    __syncthreads();
   }
 }
 
@@ -411,7 +493,7 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
   const int chunks = cdiv(n, CHUNK);
   zero_int_kernel<<<1, 64, 0, s>>>(span_count, 1);
   LAT_LAUNCH_CHECK();
-  const size_t lds = (size_t)CHUNK * dim * sizeof(float);
+  const size_t lds = (size_t)CHUNK * dim * sizeof(DT);
   if (lds > 48 * 1024)
     LAT_HIP_CHECK(hipFuncSetAttribute((const void*)chunk_reduce_kernel<DT, ET>,
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
@@ -419,9 +501,8 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
       skeys, sbags, n, (const DT*)dX, B, n_slots, first_slot, dim, offsets, mean, chunk_uid,
       part, part_uid, span_list, span_count, grad_rows, (ET*)E, lr);
   LAT_LAUNCH_CHECK();
-  const int fix_threads = dim >= 1024 ? dim : (1024 / dim) * dim;
-  const int fix_grid = chunks < 1024 ? chunks : 1024;
-  chunk_fixup_kernel<ET><<<fix_grid, fix_threads, 0, s>>>(span_list, span_count, part_uid,
+  const int fix_grid = chunks < 2048 ? chunks : 2048;
+  chunk_fixup_kernel<ET><<<fix_grid, 256, 0, s>>>(span_list, span_count, part_uid,
                                                          seg_offsets, unique_rows, part, dim,
                                                          grad_rows, (ET*)E, lr);
   LAT_LAUNCH_CHECK();
@@ -432,7 +513,8 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t
                       const int32_t* indices, int F, int B, int64_t nnz, int mean,
                       const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
-                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s) {
+                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
+                      const int* keys_in, const int* vals_in) {
   if (nnz == 0) {
     set_empty_kernel<<<1, 1, 0, s>>>(num_unique, seg_offsets);
     LAT_LAUNCH_CHECK();
@@ -454,8 +536,13 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t
   float* part = (float*)take((size_t)chunks * 2 * dim * 4);
 
   const int64_t bags = (int64_t)F * B;
-  embbag_keys_kernel<<<cdiv(bags, 4), 256, 0, s>>>(row_base, offsets, indices, F, B, keys, vals);
-  LAT_LAUNCH_CHECK();
+  if (keys_in && vals_in) {
+    keys = const_cast<int*>(keys_in);  // read-only from here on
+    vals = const_cast<int*>(vals_in);
+  } else {
+    embbag_keys_kernel<<<cdiv(bags, 4), 256, 0, s>>>(row_base, offsets, indices, F, B, keys, vals);
+    LAT_LAUNCH_CHECK();
+  }
   hipError_t e = radix_sort_pairs(keys, vals, n, total_rows - 1, skeys, sorted_bags, sort_ws, s);
   if (e != hipSuccess) return e;
   const int tiles = cdiv(n, SEG_TILE);

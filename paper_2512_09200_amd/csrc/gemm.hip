@@ -349,17 +349,48 @@ hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t st) {
 }
 
 // --- deterministic column sums: out[n] = sum_m G[m*ld + n] (bias gradients) ---
+// Block: 64 columns as 8 groups of 8, 32 row lanes, CS_ROWS rows; partial sums
+// combined in a fixed order in LDS, then over row chunks in a second kernel.
 constexpr int CS_ROWS = 256;
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ G, int64_t ldG,
-                                                             int M, int N,
+                                                             int M, int N, int vec,
                                                              float* __restrict__ part) {
-  const int col = blockIdx.x * 256 + threadIdx.x;
-  if (col >= N) return;
+  constexpr int VE = 16 / sizeof(T);
+  __shared__ float red[32][65];
+  const int cg = threadIdx.x & 7, rl = threadIdx.x >> 3;
+  const int col0 = blockIdx.x * 64 + cg * 8;
   const int r0 = blockIdx.y * CS_ROWS, r1 = min(M, r0 + CS_ROWS);
-  float s = 0.f;
-  for (int r = r0; r < r1; ++r) s += ld(G + (int64_t)r * ldG + col);
-  part[(int64_t)blockIdx.y * N + col] = s;
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  if (vec && col0 + 8 <= N) {
+#pragma unroll 4
+    for (int r = r0 + rl; r < r1; r += 32) {
+      const T* g = G + (int64_t)r * ldG + col0;
+#pragma unroll
+      for (int h = 0; h < 8; h += VE) {
+        float t[VE];
+        Vec16<T>::unpack(ldg16(g + h), t);
+#pragma unroll
+        for (int i = 0; i < VE; ++i) acc[h + i] += t[i];
+      }
+    }
+  } else {
+    for (int r = r0 + rl; r < r1; r += 32)
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (col0 + i < N) acc[i] += ld(G + (int64_t)r * ldG + col0 + i);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) red[rl][cg * 8 + i] = acc[i];
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int col = blockIdx.x * 64 + threadIdx.x;
+    float s = 0.f;
+    for (int i = 0; i < 32; ++i) s += red[i][threadIdx.x];
+    if (col < N) part[(int64_t)blockIdx.y * N + col] = s;
+  }
 }
 __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ part,
                                                            int chunks, int N,
@@ -378,16 +409,18 @@ hipError_t colsum(const void* G, DType dt, int64_t ld, int M, int N, float* out,
   if (N == 0) return hipSuccess;
   const int chunks = cdiv(M > 0 ? M : 1, CS_ROWS);
   float* part = (float*)ws;
-  dim3 grid(cdiv(N, 256), chunks);
   if (M == 0) {
     colsum_final_kernel<<<cdiv(N, 256), 256, 0, st>>>(part, 0, N, out);
     LAT_LAUNCH_CHECK();
     return hipSuccess;
   }
+  dim3 grid(cdiv(N, 64), chunks);
+  const int ve = dt == DT_BF16 ? 8 : 4;
+  const int vec = (ld % ve == 0) && (((uintptr_t)G & 15) == 0);
   if (dt == DT_BF16)
-    colsum_partial_kernel<bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)G, ld, M, N, part);
+    colsum_partial_kernel<bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)G, ld, M, N, vec, part);
   else
-    colsum_partial_kernel<float><<<grid, 256, 0, st>>>((const float*)G, ld, M, N, part);
+    colsum_partial_kernel<float><<<grid, 256, 0, st>>>((const float*)G, ld, M, N, vec, part);
   LAT_LAUNCH_CHECK();
   colsum_final_kernel<<<cdiv(N, 256), 256, 0, st>>>(part, chunks, N, out);
   LAT_LAUNCH_CHECK();

@@ -14,15 +14,19 @@ hipError_t radix_sort_pairs(int* keys, int* vals, int64_t n, int64_t max_key, in
                             int* vals_out, void* ws, hipStream_t s);
 
 // embbag.hip
+// keys/vals (optional): also write the backward's sort keys (global row) and
+// values (bag id) per position, so the backward can skip building them.
 hipError_t embbag_fwd(const void* E, DType edt, int dim, const int64_t* row_base,
                       const int32_t* offsets, const int32_t* indices, int F, int B, int mean,
-                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s);
+                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s,
+                      int* keys = nullptr, int* vals = nullptr);
 size_t embbag_bwd_workspace(int64_t nnz, int dim);
 hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t* offsets,
                       const int32_t* indices, int F, int B, int64_t nnz, int mean,
                       const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
-                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s);
+                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
+                      const int* keys_in = nullptr, const int* vals_in = nullptr);
 hipError_t validate_batch(const int64_t* row_base, const int32_t* offsets,
                           const int32_t* indices, int F, int B, int64_t nnz,
                           unsigned long long* dev_result, hipStream_t s);
@@ -59,6 +63,14 @@ size_t fm_bwd_workspace(int n, int k);
 hipError_t fm_bwd(DType dt, const void* X, const void* W, int B, int n, int d, int k,
                   const void* dout, int64_t dstride, int emit0, const float* addend,
                   void* dX, DType dxt, float* dW, void* ws, hipStream_t s);
+
+// fm_mfma.hip (bf16 MFMA path of the FM block)
+bool fm_mfma_supported(int n, int d, int k);
+size_t fm_mfma_bwd_workspace(int n, int k);
+hipError_t fm_mfma(bool fwd, const void* X, const void* W, int B, int n, int d, int k, void* out,
+                   int64_t ostride, int emit0, const void* dout, int64_t dstride,
+                   const float* addend, void* dX, float* dX_f32, float* dW, void* ws,
+                   hipStream_t s);
 
 // loss.hip
 size_t bce_workspace(int64_t n);

@@ -22,6 +22,7 @@ constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int SCAN_THREADS = 256;
 constexpr int SCAN_ITEMS = 16;
 constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;  // 4096
+static_assert(SORT_THREADS == RADIX, "one thread per digit in the scatter's tile scan");
 
 // ---------------------------------------------------------------------------
 // device-wide exclusive scan of int32 (counts fit int32: totals < 2^31)
@@ -144,13 +145,17 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_kernel(
   constexpr int NW = SORT_THREADS / 64;
   constexpr int CHUNK = SORT_TILE / NW;  // 1024 consecutive items per wave
   constexpr int ROUNDS = CHUNK / 64;     // 16
-  __shared__ int wcnt[NW][RADIX];
-  __shared__ int wbase[NW][RADIX];
+  __shared__ int wcnt[NW][RADIX];        // per-wave digit counts, then per-wave bases in the tile
+  __shared__ int dstart[RADIX];          // first tile position of each digit
+  __shared__ int scan_tmp[SORT_THREADS / 64];
+  __shared__ int lkeys[SORT_TILE];
+  __shared__ int lvals[SORT_TILE];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < NW * RADIX; i += SORT_THREADS) (&wcnt[0][0])[i] = 0;
   __syncthreads();
 
-  const int64_t cbase = (int64_t)blockIdx.x * SORT_TILE + (int64_t)w * CHUNK;
+  const int64_t tbase = (int64_t)blockIdx.x * SORT_TILE;
+  const int64_t cbase = tbase + (int64_t)w * CHUNK;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int key[ROUNDS], val[ROUNDS], rank[ROUNDS];
 #pragma unroll
@@ -160,6 +165,7 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_kernel(
     key[r] = valid ? keys_in[k] : 0;
     val[r] = valid ? vals_in[k] : 0;
   }
+  // stable rank of each item among the wave's items with the same digit
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
     int64_t k = cbase + (int64_t)r * 64 + lane;
@@ -181,23 +187,42 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_kernel(
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS) {
-    int run = offsets[(int64_t)d * tiles + blockIdx.x];
+  // tile-level digit starts (exclusive scan over digits) and per-wave bases
+  {
+    const int d = threadIdx.x;  // SORT_THREADS == RADIX
+    int tot = 0;
+    for (int i = 0; i < NW; ++i) tot += wcnt[i][d];
+    int all;
+    const int st = block_exclusive_scan(tot, scan_tmp, &all);
+    dstart[d] = st;
+    int run = st;
     for (int i = 0; i < NW; ++i) {
-      wbase[i][d] = run;
-      run += wcnt[i][d];
+      const int c = wcnt[i][d];
+      wcnt[i][d] = run;
+      run += c;
     }
   }
   __syncthreads();
+  // the tile in stable digit order in LDS
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
     int64_t k = cbase + (int64_t)r * 64 + lane;
     if (k < n) {
       uint32_t d = ((uint32_t)key[r] >> shift) & (RADIX - 1);
-      int pos = wbase[w][d] + rank[r];
-      keys_out[pos] = key[r];
-      vals_out[pos] = val[r];
+      const int pos = wcnt[w][d] + rank[r];
+      lkeys[pos] = key[r];
+      lvals[pos] = val[r];
     }
+  }
+  __syncthreads();
+  // consecutive threads write consecutive positions of each digit's run
+  const int tn = (int)((n - tbase) < SORT_TILE ? (n - tbase) : SORT_TILE);
+  for (int i = threadIdx.x; i < tn; i += SORT_THREADS) {
+    const int kk = lkeys[i];
+    const uint32_t d = ((uint32_t)kk >> shift) & (RADIX - 1);
+    const int pos = offsets[(int64_t)d * tiles + blockIdx.x] + (i - dstart[d]);
+    keys_out[pos] = kk;
+    vals_out[pos] = lvals[i];
   }
 }
 

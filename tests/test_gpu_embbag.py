@@ -15,6 +15,7 @@ CASES = {
     "cfg2-small": synth.small(synth.CFG2, B=256, rows=3000),
     "cfg4-small-empty-bags": synth.small(synth.CFG4, B=192, rows=1500),
     "cfg3-small": synth.small(synth.CFG3, B=64, rows=20000),
+    "d256-bf16-mean": synth.small(synth.CFG2, B=96, rows=800, F=5, d=256, pool="mean"),
 }
 
 

@@ -14,7 +14,11 @@ CASES = {
     "dot-f32-cfg1": ("dot", "f32", 128, 9, 32, 0, True, False),
     "dot-bf16-cfg2": ("dot", "bf16", 300, 27, 64, 0, True, False),
     "dot-bf16-cfg4-absent": ("dot", "bf16", 96, 97, 128, 0, True, True),
-    "fm-bf16-cfg3": ("fm", "bf16", 200, 65, 128, 32, True, False),
+    "fm-bf16-cfg3": ("fm", "bf16", 200, 65, 128, 32, True, False),      # MFMA path
+    "fm-bf16-cfg3-many": ("fm", "bf16", 700, 65, 128, 32, True, False), # > 1 sample per block
+    "fm-bf16-n30-d64-k32": ("fm", "bf16", 37, 30, 64, 32, False, False),  # MFMA, other tiles
+    "fm-bf16-n29-d128-k64": ("fm", "bf16", 41, 29, 128, 64, True, False),
+    "fm-bf16-valu": ("fm", "bf16", 33, 10, 32, 16, False, False),       # VALU path (d=32)
     "fm-f32-small": ("fm", "f32", 50, 10, 32, 16, False, False),
 }
 
