@@ -88,9 +88,20 @@ def main():
     top = [lin(W, b) for W, b in p["top"]]
     fm_W = torch.from_numpy(p["fm_W"]).to(sdt).to(dev) if "fm_W" in p else None
     fm_dW = torch.empty(tuple(fm_W.shape), device=dev) if fm_W is not None else None
+    stack = None
+    if "stack" in p:
+        stack = []
+        for lay in p["stack"]:
+            d = {k: torch.from_numpy(lay[k]).to(sdt).to(dev) for k in ("W", "A")}
+            d["gamma"] = torch.from_numpy(lay["gamma"]).to(dev)
+            d["C"] = torch.from_numpy(lay["C"]).to(sdt).to(dev) if lay["C"] is not None else None
+            for k in ("W", "A", "gamma", "C"):
+                if d[k] is not None:
+                    d["d" + k] = torch.empty(tuple(d[k].shape), device=dev)
+            stack.append(d)
     model = api.StepModel(tables=E, row_base=row_base, num_features=cfg.F, dense_in=cfg.dense_in,
                           bottom=bottom, top=top, interact=cfg.interact, fm_W=fm_W, fm_dW=fm_dW,
-                          pool=cfg.pool)
+                          pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps)
     nnz_max = max(b["nnz"] for b in batches)
     lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False)
     ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
@@ -142,6 +153,14 @@ def main():
         flops_fwd += 4.0 * cfg.B * n * cfg.d * cfg.fm_rank
     elif cfg.interact == "dot":
         flops_fwd += 2.0 * cfg.B * cfg.n_pairs * cfg.d
+    elif cfg.interact == "stack":
+        nl = n
+        for l in range(cfg.stack_layers):
+            flops_fwd += 4.0 * cfg.B * nl * cfg.d * cfg.fm_rank                      # FM block
+            flops_fwd += 2.0 * cfg.B * (nl * cfg.fm_rank) * (cfg.stack_n * cfg.d)    # compression
+            if l == 0 and nl != cfg.stack_n:
+                flops_fwd += 2.0 * cfg.B * cfg.stack_n * nl * cfg.d                  # residual C X
+            nl = cfg.stack_n
     dense_stages = ["bottom_fwd", "interact_fwd", "top_fwd", "top_bwd", "interact_bwd", "bottom_bwd"]
     dense_ms = sum(stage_ms[s] for s in dense_stages)
     mfma_tfs = 3.0 * flops_fwd / (dense_ms * 1e-3) / 1e12

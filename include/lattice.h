@@ -258,7 +258,7 @@ typedef struct {
   int32_t num_features;        /* F */
   int32_t dense_in;            /* dense inputs (0: no dense path, no bottom MLP) */
   lattice_mlp_desc bottom;     /* relu_last = 1, output width = dim */
-  lattice_interact_desc interact;  /* n = F + (dense_in > 0); emit_slot0 = dense_in > 0 */
+  lattice_interact_desc interact;  /* n = F + (dense_in > 0); emit_slot0 = dense_in > 0 (DOT/FM) */
   lattice_mlp_desc top;        /* relu_last = 0, output width = T */
 } lattice_model_desc;
 
@@ -309,6 +309,7 @@ typedef struct {
   int64_t top_act[LATTICE_MAX_LAYERS];      /* [B, out_i] hidden top outputs (last: logits) */
   int64_t unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows;
   int64_t keys, vals;   /* [nnz] int32: sort keys (global row) and bag ids, built by the forward */
+  int64_t interact;     /* interaction workspace (saved state from forward to backward) */
   int64_t scratch;      /* shared scratch of the stages */
   int64_t scratch_bytes;
 } lattice_step_layout;

@@ -106,33 +106,58 @@ def lattice_validate_batch(table, row_base, offsets, indices, F, B, stream=None)
 
 
 # ---------------------------------------------------------------------------
-def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0):
-    return A.lattice_interact_desc(kind=_KIND[kind], dtype=_dt(X), n=X.shape[1], dim=X.shape[2],
-                                   rank=(fm_W.shape[1] if fm_W is not None else rank),
-                                   emit_slot0=int(emit_slot0), fm_W=fm_W.data_ptr() if fm_W is not None else None,
-                                   fm_dW=fm_dW.data_ptr() if fm_dW is not None else None,
-                                   n_layers=0, stack_n=0, ln_eps=0.0, layers=None)
+def _ptr(t):
+    return t.data_ptr() if t is not None else None
 
 
-def lattice_interact_fwd(kind, X, out, emit_slot0=False, fm_W=None, stream=None):
+def stack_layers(layers):
+    """layers: list of dicts W, A, C (or None), gamma, dW, dA, dC, dgamma (device tensors)."""
+    arr = (A.lattice_stack_layer * len(layers))()
+    for i, L in enumerate(layers):
+        _contig(*(L.get(k) for k in ("W", "A", "C", "gamma")))
+        arr[i] = A.lattice_stack_layer(*(_ptr(L.get(k)) for k in
+                                         ("W", "A", "C", "gamma", "dW", "dA", "dC", "dgamma")))
+    return arr
+
+
+def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0, stack=None, stack_n=0,
+                  ln_eps=1e-5):
+    """stack: list of layer dicts (see stack_layers) for kind "stack"."""
+    arr = stack_layers(stack) if stack else None
+    if stack:
+        rank = stack[0]["W"].shape[1]
+    d = A.lattice_interact_desc(kind=_KIND[kind], dtype=_dt(X), n=X.shape[1], dim=X.shape[2],
+                                rank=(fm_W.shape[1] if fm_W is not None else rank),
+                                emit_slot0=int(emit_slot0), fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
+                                n_layers=len(stack) if stack else 0, stack_n=stack_n,
+                                ln_eps=ln_eps, layers=arr)
+    d._keep = arr
+    return d
+
+
+def lattice_interact_fwd(kind, X, out, emit_slot0=False, fm_W=None, stream=None, stack=None,
+                         stack_n=0, ln_eps=1e-5):
+    """Returns the workspace (saved state), which lattice_interact_bwd needs."""
     _contig(X, fm_W)
     lib = load()
-    d = interact_desc(kind, X, emit_slot0, fm_W)
+    d = interact_desc(kind, X, emit_slot0, fm_W, stack=stack, stack_n=stack_n, ln_eps=ln_eps)
     wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
     check(lib.lattice_interact_fwd(byref(d), X.shape[0], _p(X), _p(out), _row_stride(out), _p(ws),
                                    wsb, _stream(stream)))
-    return out
+    return ws
 
 
-def lattice_interact_bwd(kind, X, d_out, dX, emit_slot0=False, fm_W=None, fm_dW=None, stream=None):
+def lattice_interact_bwd(kind, X, d_out, dX, emit_slot0=False, fm_W=None, fm_dW=None, stream=None,
+                         stack=None, stack_n=0, ln_eps=1e-5, ws=None):
     _contig(X, dX, fm_W, fm_dW)
     lib = load()
-    d = interact_desc(kind, X, emit_slot0, fm_W, fm_dW)
+    d = interact_desc(kind, X, emit_slot0, fm_W, fm_dW, stack=stack, stack_n=stack_n, ln_eps=ln_eps)
     wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
-    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
+    if ws is None:
+        ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
     check(lib.lattice_interact_bwd(byref(d), X.shape[0], _p(X), _p(d_out), _row_stride(d_out),
-                                   _p(dX), _p(ws), wsb, _stream(stream)))
+                                   _p(dX), _p(ws), ws.numel(), _stream(stream)))
     return dX
 
 
@@ -195,24 +220,25 @@ class StepModel:
     {W, b, dW, db}; fm_W / fm_dW for the FM interaction."""
 
     def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
-                 fm_W=None, fm_dW=None, pool="sum"):
+                 fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5):
         _contig(tables, row_base)
         dt = _dt(tables)
         d = tables.shape[1]
         n = num_features + (1 if dense_in > 0 else 0)
         self._bottom = mlp_desc(bottom, True, dt) if dense_in > 0 else A.lattice_mlp_desc(dtype=dt)
         self._top = mlp_desc(top, False, dt)
-        idesc = A.lattice_interact_desc(kind=_KIND[interact], dtype=dt, n=n, dim=d,
-                                        rank=fm_W.shape[1] if fm_W is not None else 0,
-                                        emit_slot0=int(dense_in > 0),
-                                        fm_W=fm_W.data_ptr() if fm_W is not None else None,
-                                        fm_dW=fm_dW.data_ptr() if fm_dW is not None else None,
-                                        n_layers=0, stack_n=0, ln_eps=0.0, layers=None)
+        self._stack = stack_layers(stack) if stack else None
+        rank = fm_W.shape[1] if fm_W is not None else (stack[0]["W"].shape[1] if stack else 0)
+        idesc = A.lattice_interact_desc(kind=_KIND[interact], dtype=dt, n=n, dim=d, rank=rank,
+                                        emit_slot0=int(dense_in > 0 and interact != "stack"),
+                                        fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
+                                        n_layers=len(stack) if stack else 0, stack_n=stack_n,
+                                        ln_eps=ln_eps, layers=self._stack)
         self.desc = A.lattice_model_desc(dtype=dt, pool=_POOL[pool], tables=_tables(tables, row_base),
                                          num_features=num_features, dense_in=dense_in,
                                          bottom=self._bottom, interact=idesc, top=self._top)
         self.tensors = dict(tables=tables, row_base=row_base, bottom=bottom, top=top, fm_W=fm_W,
-                            fm_dW=fm_dW)
+                            fm_dW=fm_dW, stack=stack)
         self.device = tables.device
         self.num_features = num_features
         self.dense_in = dense_in

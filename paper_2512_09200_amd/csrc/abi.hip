@@ -159,6 +159,25 @@ lattice_status lattice_validate_batch(const lattice_tables* tables, const lattic
 // ---------------------------------------------------------------------------
 // interaction
 // ---------------------------------------------------------------------------
+static StackShape stack_shape(const lattice_interact_desc* d) {
+  StackShape sh;
+  sh.L = d->n_layers;
+  sh.n0 = d->n;
+  sh.nv = d->stack_n;
+  sh.d = d->dim;
+  sh.k = d->rank;
+  sh.has_C0 = (d->layers && d->n_layers > 0 && d->layers[0].C) ? 1 : 0;
+  sh.eps = d->ln_eps;
+  return sh;
+}
+
+static void stack_layers(const lattice_interact_desc* d, StackLayer* out) {
+  for (int l = 0; l < d->n_layers; ++l) {
+    const lattice_stack_layer& L = d->layers[l];
+    out[l] = StackLayer{L.W, L.A, L.C, L.gamma, L.dW, L.dA, L.dC, L.dgamma};
+  }
+}
+
 static lattice_status check_interact(const lattice_interact_desc* d, int32_t B) {
   REQUIRE(d, "null interaction descriptor");
   REQUIRE(B >= 0, "negative batch");
@@ -173,6 +192,21 @@ static lattice_status check_interact(const lattice_interact_desc* d, int32_t B) 
     REQUIRE(d->rank >= 1 && d->fm_W, "FM needs rank and W");
     if (fm_lds_bytes(d->n, d->dim, d->rank) > 160 * 1024 || d->n * d->rank > 256 * 64)
       FAIL(LATTICE_ERR_UNSUPPORTED, "FM with n=%d, dim=%d, rank=%d exceeds LDS", d->n, d->dim, d->rank);
+  } else if (d->kind == LATTICE_INTERACT_STACK) {
+    if (d->dtype != LATTICE_BF16) FAIL(LATTICE_ERR_UNSUPPORTED, "STACK runs in bf16 only");
+    REQUIRE(d->n_layers >= 1 && d->n_layers <= LATTICE_MAX_LAYERS && d->layers, "STACK needs 1..%d layers",
+            LATTICE_MAX_LAYERS);
+    REQUIRE(d->rank >= 1 && d->stack_n >= 1 && d->ln_eps > 0.f, "STACK needs rank, stack_n, ln_eps > 0");
+    REQUIRE(!d->emit_slot0, "STACK does not emit slot 0");
+    for (int l = 0; l < d->n_layers; ++l) {
+      const lattice_stack_layer& L = d->layers[l];
+      REQUIRE(L.W && L.A && L.gamma, "STACK layer %d: null W/A/gamma", l);
+      if (l == 0 && d->n != d->stack_n) REQUIRE(L.C, "STACK layer 0 needs C when n != stack_n");
+      if (l > 0) REQUIRE(!L.C, "STACK layer %d: only layer 0 may have C", l);
+    }
+    if (!stack_supported(stack_shape(d)))
+      FAIL(LATTICE_ERR_UNSUPPORTED, "STACK shape n=%d stack_n=%d dim=%d rank=%d not supported", d->n,
+           d->stack_n, d->dim, d->rank);
   } else {
     FAIL(LATTICE_ERR_UNSUPPORTED, "interaction kind %d not supported", (int)d->kind);
   }
@@ -180,6 +214,7 @@ static lattice_status check_interact(const lattice_interact_desc* d, int32_t B) 
 }
 
 static int64_t interact_width(const lattice_interact_desc* d) {
+  if (d->kind == LATTICE_INTERACT_STACK) return (int64_t)d->stack_n * d->dim;
   int64_t w = d->kind == LATTICE_INTERACT_DOT ? (int64_t)d->n * (d->n - 1) / 2
                                               : (int64_t)d->n * d->rank;
   return w + (d->emit_slot0 ? d->dim : 0);
@@ -191,13 +226,19 @@ static bool fm_uses_mfma(const lattice_interact_desc* d, int64_t stride = 8) {
   return d->dtype == LATTICE_BF16 && fm_mfma_supported(d->n, d->dim, d->rank) && stride % 8 == 0;
 }
 
-static size_t interact_ws(const lattice_interact_desc* d) {
+static size_t interact_ws(const lattice_interact_desc* d, int B) {
+  if (d->kind == LATTICE_INTERACT_STACK) return stack_plan(stack_shape(d), B).total_bytes;
   if (d->kind != LATTICE_INTERACT_FM) return 0;
   return std::max(fm_mfma_bwd_workspace(d->n, d->rank), fm_bwd_workspace(d->n, d->rank));
 }
 
 static hipError_t interact_fwd_impl(const lattice_interact_desc* d, int B, const void* X,
-                                    void* out, int64_t os, hipStream_t s) {
+                                    void* out, int64_t os, void* ws, hipStream_t s) {
+  if (d->kind == LATTICE_INTERACT_STACK) {
+    StackLayer Ls[LATTICE_MAX_LAYERS];
+    stack_layers(d, Ls);
+    return stack_fwd(stack_shape(d), Ls, B, X, out, os, ws, s);
+  }
   if (d->kind == LATTICE_INTERACT_DOT)
     return dot_fwd(dt_of(d->dtype), X, B, d->n, d->dim, out, os, d->emit_slot0, s);
   if (fm_uses_mfma(d, os))
@@ -209,6 +250,11 @@ static hipError_t interact_fwd_impl(const lattice_interact_desc* d, int B, const
 static hipError_t interact_bwd_impl(const lattice_interact_desc* d, int B, const void* X,
                                     const void* dout, int64_t ds, void* dX, void* ws,
                                     hipStream_t s) {
+  if (d->kind == LATTICE_INTERACT_STACK) {
+    StackLayer Ls[LATTICE_MAX_LAYERS];
+    stack_layers(d, Ls);
+    return stack_bwd(stack_shape(d), Ls, B, X, dout, ds, dX, ws, s);
+  }
   if (d->kind == LATTICE_INTERACT_DOT)
     return dot_bwd(dt_of(d->dtype), X, B, d->n, d->dim, dout, ds, d->emit_slot0, dX, s);
   if (fm_uses_mfma(d, ds))
@@ -221,22 +267,21 @@ static hipError_t interact_bwd_impl(const lattice_interact_desc* d, int B, const
 extern "C" {
 
 size_t lattice_interact_workspace(const lattice_interact_desc* desc, int32_t B) {
-  (void)B;
-  return desc ? interact_ws(desc) : 0;
+  return (desc && check_interact(desc, B) == LATTICE_OK) ? interact_ws(desc, B) : 0;
 }
 
 lattice_status lattice_interact_fwd(const lattice_interact_desc* desc, int32_t B, const void* X,
                                     void* out, int64_t out_stride, void* ws, size_t ws_bytes,
                                     void* stream) {
-  (void)ws;
-  (void)ws_bytes;
   lattice_status st = check_interact(desc, B);
   if (st != LATTICE_OK) return st;
   if (B == 0) return LATTICE_OK;
   REQUIRE(X && out, "null X/out");
   REQUIRE(out_stride >= interact_width(desc), "out_stride %lld < row width %lld",
           (long long)out_stride, (long long)interact_width(desc));
-  HIPRET(interact_fwd_impl(desc, B, X, out, out_stride, strm(stream)));
+  const size_t need = desc->kind == LATTICE_INTERACT_STACK ? interact_ws(desc, B) : 0;
+  if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+  HIPRET(interact_fwd_impl(desc, B, X, out, out_stride, ws, strm(stream)));
   return LATTICE_OK;
 }
 
@@ -246,7 +291,12 @@ lattice_status lattice_interact_bwd(const lattice_interact_desc* desc, int32_t B
   lattice_status st = check_interact(desc, B);
   if (st != LATTICE_OK) return st;
   if (desc->kind == LATTICE_INTERACT_FM) REQUIRE(desc->fm_dW, "FM backward needs fm_dW");
-  const size_t need = interact_ws(desc);
+  if (desc->kind == LATTICE_INTERACT_STACK)
+    for (int l = 0; l < desc->n_layers; ++l) {
+      const lattice_stack_layer& L = desc->layers[l];
+      REQUIRE(L.dW && L.dA && L.dgamma && (!L.C || L.dC), "STACK layer %d: null gradient buffer", l);
+    }
+  const size_t need = interact_ws(desc, B);
   if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
   if (B > 0) REQUIRE(X && d_out && dX, "null X/d_out/dX");
   REQUIRE(d_out_stride >= interact_width(desc) || B == 0, "d_out_stride too small");
@@ -498,7 +548,8 @@ static lattice_status check_model(const lattice_model_desc* m, int B) {
   if (st != LATTICE_OK) return st;
   REQUIRE(m->interact.n == n && m->interact.dim == d && m->interact.dtype == m->dtype,
           "interaction shape/dtype mismatch");
-  REQUIRE(m->interact.emit_slot0 == (m->dense_in > 0 ? 1 : 0), "emit_slot0 must equal (dense_in > 0)");
+  const int want_emit = (m->dense_in > 0 && m->interact.kind != LATTICE_INTERACT_STACK) ? 1 : 0;
+  REQUIRE(m->interact.emit_slot0 == want_emit, "emit_slot0 must be %d", want_emit);
   REQUIRE(m->top.layers[0].in_dim == interact_width(&m->interact), "top input width %d != %lld",
           m->top.layers[0].in_dim, (long long)interact_width(&m->interact));
   return LATTICE_OK;
@@ -552,7 +603,7 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   sc = std::max(sc, mlp_bwd_ws(&m->top, B));
   if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
   sc = std::max(sc, bce_workspace((int64_t)B * P->T));
-  sc = std::max(sc, interact_ws(&m->interact));
+  L.interact = take(interact_ws(&m->interact, B));
   sc = std::max(sc, embbag_bwd_workspace(nnz, d));
   L.scratch = take(sc);
   L.scratch_bytes = (int64_t)sc;
@@ -629,7 +680,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   }
   HIPRET(mark(2));
   // 3. interaction -> top input t = [X[:,0,:], interaction]
-  HIPRET(interact_fwd_impl(&m->interact, B, X, t, P.t_stride, s));
+  HIPRET(interact_fwd_impl(&m->interact, B, X, t, P.t_stride, at(L.interact), s));
   HIPRET(mark(3));
   // 4. top MLP -> logits; 5. masked BCE
   const int nt = m->top.n_layers;
@@ -652,7 +703,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   HIPRET(mark(6));
   // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
   void* dX = at(L.dX);
-  HIPRET(interact_bwd_impl(&m->interact, B, X, at(L.d_t), P.t_stride, dX, scratch, s));
+  HIPRET(interact_bwd_impl(&m->interact, B, X, at(L.d_t), P.t_stride, dX, at(L.interact), s));
   HIPRET(mark(7));
   // 8. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
   if (m->dense_in > 0) {

@@ -30,117 +30,139 @@ struct Epi {
   int relu;
   const void* mask;     // activation whose sign gates the output, or null
   DType mask_dt;
-  int64_t ldm;
+  int64_t ldm, s_mask;
+  const float* addend;  // + addend[m*ld_add + n] (fp32) or null
+  int64_t ld_add, s_add;
+  int accumulate;       // + the existing (fp32) C
 };
 
 template <typename CT>
-__device__ inline void epi_store(CT* C, int64_t ldc, int row, int col, float v, const Epi& e) {
+__device__ inline void epi_store(CT* C, int64_t ldc, int row, int col, float v, const Epi& e,
+                                 int64_t bz) {
   if (e.bias) v += e.bias[col];
+  if (e.addend) v += e.addend[bz * e.s_add + (int64_t)row * e.ld_add + col];
+  if (e.accumulate) v += ld(C + (int64_t)row * ldc + col);
   if (e.relu) v = v > 0.f ? v : 0.f;
   if (e.mask) {
-    float g = e.mask_dt == DT_BF16 ? bf2f(((const bf16_t*)e.mask)[(int64_t)row * e.ldm + col])
-                                   : ((const float*)e.mask)[(int64_t)row * e.ldm + col];
+    const int64_t mi = bz * e.s_mask + (int64_t)row * e.ldm + col;
+    float g = e.mask_dt == DT_BF16 ? bf2f(((const bf16_t*)e.mask)[mi]) : ((const float*)e.mask)[mi];
     v = g > 0.f ? v : 0.f;
   }
   st(C + (int64_t)row * ldc + col, v);
 }
 
+// An operand: element (r, k) of A(m,k) / B(n,k).  K-contiguous: p[r*ld + koff(k)];
+// MN-contiguous: p[koff(k)*... + r] with koff(k) counted in rows of length ld.
+// K segmentation splits k into (k / kseg, k % kseg): the segment index moves by
+// ks elements (batched sums over samples as one contraction).
+struct Opnd {
+  const bf16_t* p;
+  int64_t ld;
+  int kseg;     // 0: no segmentation
+  int64_t ks;
+};
+template <bool MN>
+__device__ inline int64_t koff(const Opnd& o, int k) {
+  if (o.kseg == 0) return MN ? (int64_t)k * o.ld : (int64_t)k;
+  const int q = k / o.kseg, r = k - q * o.kseg;
+  return (int64_t)q * o.ks + (MN ? (int64_t)r * o.ld : (int64_t)r);
+}
+
 // --- operand tile loaders: fill S[rows][GLD] (k contiguous) for rows r0.., k k0.. ---
 // K-contiguous, 16-byte vectors: 128 rows x 32 k = 4 vectors per row, 2 per thread.
-__device__ inline void load_k_vec(const bf16_t* __restrict__ P, int64_t ld, int rows_total,
-                                  int K, int r0, int k0, u32x4 (&reg)[2]) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int v = threadIdx.x + i * 256;
-    const int r = v >> 2, kc = (v & 3) * 8;
-    const int gr = r0 + r, gk = k0 + kc;
-    if (gr < rows_total && gk < K) reg[i] = ldg16(P + (int64_t)gr * ld + gk);
-    else reg[i] = u32x4{0, 0, 0, 0};
-  }
-}
-__device__ inline void store_k_vec(bf16_t* S, const u32x4 (&reg)[2]) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int v = threadIdx.x + i * 256;
-    const int r = v >> 2, kc = (v & 3) * 8;
-    *reinterpret_cast<u32x4*>(S + r * GLD + kc) = reg[i];
-  }
-}
-// M-contiguous: thread owns rows (2p, 2p+1) and 8 consecutive k (wave w -> k 8w..8w+7).
-__device__ inline void load_m_vec(const bf16_t* __restrict__ P, int64_t ld, int rows_total,
-                                  int K, int r0, int k0, uint32_t (&reg)[8]) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int gr = r0 + 2 * lane;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int gk = k0 + w * 8 + i;
-    if (gk < K && gr < rows_total) reg[i] = *reinterpret_cast<const uint32_t*>(P + (int64_t)gk * ld + gr);
-    else reg[i] = 0u;
-  }
-}
-__device__ inline void store_m_vec(bf16_t* S, const uint32_t (&reg)[8]) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  u32x4 lo, hi;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    // reg[k] = (row 2p at k) | (row 2p+1 at k) << 16
-    lo[i] = __builtin_amdgcn_perm(reg[2 * i + 1], reg[2 * i], 0x05040100u);  // low halves
-    hi[i] = __builtin_amdgcn_perm(reg[2 * i + 1], reg[2 * i], 0x07060302u);  // high halves
-  }
-  *reinterpret_cast<u32x4*>(S + (2 * lane) * GLD + w * 8) = lo;
-  *reinterpret_cast<u32x4*>(S + (2 * lane + 1) * GLD + w * 8) = hi;
-}
-// Generic element loader (any alignment / transposition).
-template <bool T>
-__device__ inline void load_elem(const bf16_t* __restrict__ P, int64_t ld, int rows_total, int K,
-                                 int r0, int k0, bf16_t (&reg)[16]) {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int e = threadIdx.x + i * 256;
-    const int r = e >> 5, kk = e & 31;
-    const int gr = r0 + r, gk = k0 + kk;
-    bf16_t v = 0;
-    if (gr < rows_total && gk < K) v = T ? P[(int64_t)gk * ld + gr] : P[(int64_t)gr * ld + gk];
-    reg[i] = v;
-  }
-}
-__device__ inline void store_elem(bf16_t* S, const bf16_t (&reg)[16]) {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int e = threadIdx.x + i * 256;
-    S[(e >> 5) * GLD + (e & 31)] = reg[i];
-  }
-}
-
-template <bool T, bool VEC> struct Loader;
-template <> struct Loader<false, true> {
+struct LoadK {
   u32x4 r[2];
-  __device__ void load(const bf16_t* P, int64_t ld, int R, int K, int r0, int k0) { load_k_vec(P, ld, R, K, r0, k0, r); }
-  __device__ void store(bf16_t* S) { store_k_vec(S, r); }
+  __device__ void load(const Opnd& o, int R, int K, int r0, int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int v = threadIdx.x + i * 256;
+      const int rr = v >> 2, kc = (v & 3) * 8;
+      const int gr = r0 + rr, gk = k0 + kc;
+      if (gr < R && gk < K) r[i] = ldg16(o.p + (int64_t)gr * o.ld + koff<false>(o, gk));
+      else r[i] = u32x4{0, 0, 0, 0};
+    }
+  }
+  __device__ void store(bf16_t* S) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int v = threadIdx.x + i * 256;
+      *reinterpret_cast<u32x4*>(S + (v >> 2) * GLD + (v & 3) * 8) = r[i];
+    }
+  }
 };
-template <> struct Loader<true, true> {
+// MN-contiguous: thread owns rows (2p, 2p+1) and 8 consecutive k (wave w -> k 8w..8w+7),
+// read as 4-byte row pairs (coalesced across the wave) and transposed in registers.
+struct LoadMN {
   uint32_t r[8];
-  __device__ void load(const bf16_t* P, int64_t ld, int R, int K, int r0, int k0) { load_m_vec(P, ld, R, K, r0, k0, r); }
-  __device__ void store(bf16_t* S) { store_m_vec(S, r); }
+  __device__ void load(const Opnd& o, int R, int K, int r0, int k0) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int gr = r0 + 2 * lane;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int gk = k0 + w * 8 + i;
+      if (gk < K && gr < R) r[i] = *reinterpret_cast<const uint32_t*>(o.p + koff<true>(o, gk) + gr);
+      else r[i] = 0u;
+    }
+  }
+  __device__ void store(bf16_t* S) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    u32x4 lo, hi;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      // r[k] = (row 2p at k) | (row 2p+1 at k) << 16
+      lo[i] = __builtin_amdgcn_perm(r[2 * i + 1], r[2 * i], 0x05040100u);  // low halves
+      hi[i] = __builtin_amdgcn_perm(r[2 * i + 1], r[2 * i], 0x07060302u);  // high halves
+    }
+    *reinterpret_cast<u32x4*>(S + (2 * lane) * GLD + w * 8) = lo;
+    *reinterpret_cast<u32x4*>(S + (2 * lane + 1) * GLD + w * 8) = hi;
+  }
 };
-template <bool T> struct Loader<T, false> {
+// Generic element loader (any alignment / transposition).
+template <bool MN>
+struct LoadElem {
   bf16_t r[16];
-  __device__ void load(const bf16_t* P, int64_t ld, int R, int K, int r0, int k0) { load_elem<T>(P, ld, R, K, r0, k0, r); }
-  __device__ void store(bf16_t* S) { store_elem(S, r); }
+  __device__ void load(const Opnd& o, int R, int K, int r0, int k0) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int e = threadIdx.x + i * 256;
+      const int rr = e >> 5, kk = e & 31;
+      const int gr = r0 + rr, gk = k0 + kk;
+      bf16_t v = 0;
+      if (gr < R && gk < K) v = MN ? o.p[koff<true>(o, gk) + gr] : o.p[(int64_t)gr * o.ld + koff<false>(o, gk)];
+      r[i] = v;
+    }
+  }
+  __device__ void store(bf16_t* S) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int e = threadIdx.x + i * 256;
+      S[(e >> 5) * GLD + (e & 31)] = r[i];
+    }
+  }
 };
+template <bool MN, bool VEC> struct LoaderSel;
+template <> struct LoaderSel<false, true> { using T = LoadK; };
+template <> struct LoaderSel<true, true> { using T = LoadMN; };
+template <bool MN> struct LoaderSel<MN, false> { using T = LoadElem<MN>; };
 
+// blockIdx.z: split index (split-K) or batch index (batched; never both)
 template <bool TA, bool TB, bool VA, bool VB, typename CT>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
-    const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ Bm, int64_t ldb,
-    CT* __restrict__ C, int64_t ldc, int M, int N, int K, int k_per_split,
-    float* __restrict__ partial, Epi epi) {
+    Opnd A, Opnd Bm, CT* __restrict__ C, int64_t ldc, int M, int N, int K, int k_per_split,
+    float* __restrict__ partial, Epi epi, int64_t sA, int64_t sB, int64_t sC, int batched) {
   __shared__ __attribute__((aligned(16))) bf16_t As[2][GBM * GLD];
   __shared__ __attribute__((aligned(16))) bf16_t Bs[2][GBN * GLD];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w >> 1, wn = w & 1;
   const int m0 = blockIdx.y * GBM, n0 = blockIdx.x * GBN;
-  const int kbeg = blockIdx.z * k_per_split;
-  const int kend = min(K, kbeg + k_per_split);
+  const int64_t bz = batched ? blockIdx.z : 0;
+  if (batched) {
+    A.p += bz * sA;
+    Bm.p += bz * sB;
+    C += bz * sC;
+  }
+  const int kbeg = batched ? 0 : blockIdx.z * k_per_split;
+  const int kend = batched ? K : min(K, kbeg + k_per_split);
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -150,12 +172,12 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  Loader<TA, VA> la;
-  Loader<TB, VB> lb;
+  typename LoaderSel<TA, VA>::T la;
+  typename LoaderSel<TB, VB>::T lb;
   const int ktiles = (kend - kbeg + GBK - 1) / GBK;
   if (ktiles > 0) {
-    la.load(A, lda, M, kend, m0, kbeg);
-    lb.load(Bm, ldb, N, kend, n0, kbeg);
+    la.load(A, M, kend, m0, kbeg);
+    lb.load(Bm, N, kend, n0, kbeg);
     la.store(As[0]);
     lb.store(Bs[0]);
   }
@@ -165,8 +187,8 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     const int cur = kt & 1;
     const bool more = kt + 1 < ktiles;
     if (more) {
-      la.load(A, lda, M, kend, m0, kbeg + (kt + 1) * GBK);
-      lb.load(Bm, ldb, N, kend, n0, kbeg + (kt + 1) * GBK);
+      la.load(A, M, kend, m0, kbeg + (kt + 1) * GBK);
+      lb.load(Bm, N, kend, n0, kbeg + (kt + 1) * GBK);
     }
     const bf16_t* as = As[cur] + (wm * 64 + frow) * GLD + fk;
     const bf16_t* bs = Bs[cur] + (wn * 64 + frow) * GLD + fk;
@@ -200,7 +222,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
         const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         if (row < M && col < N) {
           if (partial) partial[((int64_t)blockIdx.z * M + row) * N + col] = acc[i][j][r];
-          else epi_store<CT>(C, ldc, row, col, acc[i][j][r], epi);
+          else epi_store<CT>(C, ldc, row, col, acc[i][j][r], epi, bz);
         }
       }
     }
@@ -217,7 +239,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   const int row = (int)(i / N), col = (int)(i % N);
   float s = 0.f;
   for (int z = 0; z < splits; ++z) s += partial[(int64_t)z * M * N + i];
-  epi_store<CT>(C, ldc, row, col, s, epi);
+  epi_store<CT>(C, ldc, row, col, s, epi, 0);
 }
 
 // --- fp32 VALU GEMM (fp32 workloads): 64x64 tile, 4x4 per thread, any layout ---
@@ -261,25 +283,30 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int row = m0 + ty * 4 + i, col = n0 + tx * 4 + j;
-      if (row < M && col < N) epi_store<CT>(C, ldc, row, col, acc[i][j], epi);
+      if (row < M && col < N) epi_store<CT>(C, ldc, row, col, acc[i][j], epi, 0);
     }
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 static bool aligned4(const void* p) { return ((uintptr_t)p & 3) == 0; }
 
-size_t gemm_workspace(const GemmArgs& g) {
-  int splits = gemm_splits(g);
-  return splits > 1 ? (size_t)splits * g.M * g.N * sizeof(float) : 0;
-}
-
 int gemm_splits(const GemmArgs& g) {
-  if (g.dt != DT_BF16) return 1;
+  if (g.dt != DT_BF16 || g.batch > 1) return 1;
   const int tiles = cdiv(g.M, GBM) * cdiv(g.N, GBN);
   int s = 1;
   // fill the 256 compute units at least twice over when K is long enough
   while (tiles * s < 512 && g.K / (s * 2) >= 512 && s * 2 <= g.max_splits) s *= 2;
   return s;
+}
+
+size_t gemm_workspace(const GemmArgs& g) {
+  int splits = gemm_splits(g);
+  return splits > 1 ? (size_t)splits * g.M * g.N * sizeof(float) : 0;
+}
+
+static Epi make_epi(const GemmArgs& g) {
+  return Epi{g.bias, g.relu, g.mask, g.mask_dt, g.ldm, g.s_mask, g.addend, g.ld_add, g.s_add,
+             g.accumulate};
 }
 
 template <bool TA, bool TB, bool VA, bool VB>
@@ -291,17 +318,18 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
   }
   int kps = (g.K + splits - 1) / splits;
   kps = ((kps + GBK - 1) / GBK) * GBK;
-  dim3 grid(cdiv(g.N, GBN), cdiv(g.M, GBM), splits);
-  Epi epi{g.bias, g.relu, g.mask, g.mask_dt, g.ldm};
+  const int batched = g.batch > 1 ? 1 : 0;
+  dim3 grid(cdiv(g.N, GBN), cdiv(g.M, GBM), batched ? g.batch : splits);
+  Epi epi = make_epi(g);
+  Opnd a{(const bf16_t*)g.A, g.lda, g.kseg, g.ksA};
+  Opnd b{(const bf16_t*)g.B, g.ldb, g.kseg, g.ksB};
   float* partial = splits > 1 ? ws : nullptr;
   if (g.c_dt == DT_BF16)
     gemm_bf16_kernel<TA, TB, VA, VB, bf16_t><<<grid, 256, 0, st>>>(
-        (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K,
-        kps, partial, epi);
+        a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA, g.sB, g.sC, batched);
   else
     gemm_bf16_kernel<TA, TB, VA, VB, float><<<grid, 256, 0, st>>>(
-        (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, (float*)g.C, g.ldc, g.M, g.N, g.K,
-        kps, partial, epi);
+        a, b, (float*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA, g.sB, g.sC, batched);
   LAT_LAUNCH_CHECK();
   if (splits > 1) {
     const int64_t n = (int64_t)g.M * g.N;
@@ -316,11 +344,15 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
 
 template <bool TA, bool TB>
 static hipError_t gemm_bf16_dispatch(const GemmArgs& g, float* ws, hipStream_t st) {
-  // 16-byte K-vectors need k-aligned rows; M-pairs need even rows and 4-byte alignment
-  const bool va = TA ? (g.lda % 2 == 0 && aligned4(g.A) && g.M % 2 == 0)
-                     : (g.lda % 8 == 0 && aligned16(g.A) && g.K % 8 == 0);
-  const bool vb = TB ? (g.ldb % 2 == 0 && aligned4(g.B) && g.N % 2 == 0)
-                     : (g.ldb % 8 == 0 && aligned16(g.B) && g.K % 8 == 0);
+  // 16-byte K-vectors need 8-aligned rows (and segments); M-pairs need even rows
+  // and 4-byte alignment.  Batch strides must keep the same alignment.
+  const bool seg_ok = g.kseg == 0 || (g.kseg % 8 == 0 && g.ksA % 8 == 0 && g.ksB % 8 == 0);
+  const bool va = TA ? (g.lda % 2 == 0 && aligned4(g.A) && g.M % 2 == 0 && g.sA % 2 == 0 &&
+                        (g.kseg == 0 || g.ksA % 2 == 0))
+                     : (g.lda % 8 == 0 && aligned16(g.A) && g.K % 8 == 0 && g.sA % 8 == 0 && seg_ok);
+  const bool vb = TB ? (g.ldb % 2 == 0 && aligned4(g.B) && g.N % 2 == 0 && g.sB % 2 == 0 &&
+                        (g.kseg == 0 || g.ksB % 2 == 0))
+                     : (g.ldb % 8 == 0 && aligned16(g.B) && g.K % 8 == 0 && g.sB % 8 == 0 && seg_ok);
   if (va && vb) return gemm_bf16_launch<TA, TB, true, true>(g, ws, st);
   if (va) return gemm_bf16_launch<TA, TB, true, false>(g, ws, st);
   if (vb) return gemm_bf16_launch<TA, TB, false, true>(g, ws, st);
@@ -328,7 +360,11 @@ static hipError_t gemm_bf16_dispatch(const GemmArgs& g, float* ws, hipStream_t s
 }
 
 hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t st) {
-  if (g.M == 0 || g.N == 0) return hipSuccess;
+  if (g.M == 0 || g.N == 0 || g.batch == 0) return hipSuccess;
+  if (g.accumulate && g.c_dt != DT_F32) {
+    set_error("accumulating GEMM needs an fp32 output");
+    return hipErrorInvalidValue;
+  }
   if (g.dt == DT_BF16) {
     float* w = (float*)ws;
     if (!g.ta && !g.tb) return gemm_bf16_dispatch<false, false>(g, w, st);
@@ -336,8 +372,12 @@ hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t st) {
     if (g.ta && !g.tb) return gemm_bf16_dispatch<true, false>(g, w, st);
     return gemm_bf16_dispatch<true, true>(g, w, st);
   }
+  if (g.batch > 1 || g.kseg) {
+    set_error("fp32 GEMM: batching / K segmentation not supported");
+    return hipErrorInvalidValue;
+  }
   dim3 grid(cdiv(g.N, 64), cdiv(g.M, 64));
-  Epi epi{g.bias, g.relu, g.mask, g.mask_dt, g.ldm};
+  Epi epi = make_epi(g);
   if (g.c_dt == DT_F32)
     gemm_f32_kernel<float><<<grid, 256, 0, st>>>((const float*)g.A, g.lda, g.ta, (const float*)g.B,
                                                  g.ldb, g.tb, (float*)g.C, g.ldc, g.M, g.N, g.K, epi);

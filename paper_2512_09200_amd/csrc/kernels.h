@@ -40,8 +40,14 @@ struct GemmArgs {
   int M = 0, N = 0, K = 0;
   const float* bias = nullptr;
   int relu = 0;
-  const void* mask = nullptr; DType mask_dt = DT_BF16; int64_t ldm = 0;
+  const void* mask = nullptr; DType mask_dt = DT_BF16; int64_t ldm = 0, s_mask = 0;
+  const float* addend = nullptr; int64_t ld_add = 0, s_add = 0;  // epilogue + addend[m][n]
+  int accumulate = 0;          // epilogue + existing C (fp32 C only)
   int max_splits = 1;          // split-K only when the caller provides gemm_workspace()
+  int batch = 1;               // batched: blockIdx.z = batch index; strides in elements
+  int64_t sA = 0, sB = 0, sC = 0;
+  int kseg = 0;                // K segmentation: k -> (k / kseg) * ks + k % kseg (0: none)
+  int64_t ksA = 0, ksB = 0;
 };
 int gemm_splits(const GemmArgs& g);
 size_t gemm_workspace(const GemmArgs& g);
@@ -71,6 +77,31 @@ hipError_t fm_mfma(bool fwd, const void* X, const void* W, int B, int n, int d, 
                    int64_t ostride, int emit0, const void* dout, int64_t dstride,
                    const float* addend, void* dX, float* dX_f32, float* dW, void* ws,
                    hipStream_t s);
+
+// stack.hip (stacked FM -> linear -> residual -> LayerNorm interaction)
+struct StackShape {
+  int L, n0, nv, d, k;  // layers, input vectors, vectors per layer output, dim, FM rank
+  int has_C0;           // layer 0 uses a compression residual C [nv, n0]
+  float eps;
+};
+struct StackLayer {
+  const void* W;        // [n, k] bf16
+  const void* A;        // [nv*d, n*k] bf16
+  const void* C;        // [nv, n0] bf16 (layer 0) or null
+  const float* gamma;   // [d]
+  float* dW; float* dA; float* dC; float* dgamma;
+};
+struct StackPlan {       // byte offsets inside the interaction workspace
+  size_t P[8], F[8], H[8], mean[8], rstd[8], Xn[8], R0, state_bytes;
+  size_t du, duR, dF, dP, dXf, dgp, gemm_ws, total_bytes;
+};
+bool stack_supported(const StackShape& sh);
+StackPlan stack_plan(const StackShape& sh, int B);
+hipError_t stack_fwd(const StackShape& sh, const StackLayer* Ls, int B, const void* X, void* out,
+                     int64_t out_stride, void* state, hipStream_t s);
+hipError_t stack_bwd(const StackShape& sh, const StackLayer* Ls, int B, const void* X,
+                     const void* d_out, int64_t d_out_stride, void* dX, void* state,
+                     hipStream_t s);
 
 // loss.hip
 size_t bce_workspace(int64_t n);

@@ -47,6 +47,20 @@ def to_dev(x, dtype=None):
     return t.to(DEV)
 
 
+def stack_dev(layers, sdt):
+    """Stack parameters (numpy, from synth) on the device with zeroed gradients."""
+    out = []
+    for lay in layers:
+        def z(x):
+            return torch.zeros(x.shape, dtype=torch.float32, device=DEV)
+        d = dict(W=to_dev(lay["W"], sdt), A=to_dev(lay["A"], sdt), gamma=to_dev(lay["gamma"]),
+                 C=to_dev(lay["C"], sdt) if lay["C"] is not None else None)
+        d.update(dW=z(lay["W"]), dA=z(lay["A"]), dgamma=z(lay["gamma"]),
+                 dC=z(lay["C"]) if lay["C"] is not None else None)
+        out.append(d)
+    return out
+
+
 class Workload:
     """Seeded inputs of a config on the GPU, plus the same values for the oracle."""
 
@@ -75,6 +89,7 @@ class Workload:
         self.fm_W = to_dev(self.params["fm_W"], sdt) if "fm_W" in self.params else None
         self.fm_dW = torch.zeros(self.fm_W.shape, dtype=torch.float32, device=DEV) \
             if self.fm_W is not None else None
+        self.stack = stack_dev(self.params["stack"], sdt) if "stack" in self.params else None
 
     def table_np(self):
         return self.E.float().cpu().double().numpy()
@@ -84,7 +99,8 @@ class Workload:
         c = self.cfg
         return api.StepModel(tables=self.E, row_base=self.row_base, num_features=c.F,
                              dense_in=c.dense_in, bottom=self.bottom, top=self.top,
-                             interact=c.interact, fm_W=self.fm_W, fm_dW=self.fm_dW, pool=c.pool)
+                             interact=c.interact, fm_W=self.fm_W, fm_dW=self.fm_dW, pool=c.pool,
+                             stack=self.stack, stack_n=c.stack_n, ln_eps=c.ln_eps)
 
 
 def relu_overrides(cfg, params, table, batch, gpu_in, gpu_out, max_iter=4):

@@ -69,3 +69,45 @@ def test_interact_fwd_bwd(name):
     if emit0:
         dref[:, 0] += G[:, :d]
     assert_close("dX", dX, rnd(dref), t)
+
+
+STACK_CASES = {
+    # name: (B, n0, stack_n, d, rank, layers)
+    "stack-C-d64": (96, 24, 8, 64, 16, 3),     # compression residual on layer 1
+    "stack-id-d128": (40, 16, 16, 128, 32, 2),  # identity residual throughout
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(STACK_CASES))
+def test_stack_fwd_bwd(name):
+    from paper_2512_09200_amd import api
+    from tests._util import assert_close_composed, stack_dev
+    B, n0, nv, d, k, L = STACK_CASES[name]
+    print(f"[stack] {name}", flush=True)
+    cfg = synth.CFG5.scaled(B=B, F=n0, d=d, stack_n=nv, fm_rank=k, stack_layers=L,
+                            top=(16, 4), seed=77)
+    params = synth.make_dense_params(cfg)
+    layers = params["stack"]
+    rnd = rounding("bf16")
+    X = synth.randn((B, n0, d), seed=31, scale=0.05, dtype="bf16")
+    Xd = to_dev(X, torch.bfloat16)
+    dev_layers = stack_dev(layers, torch.bfloat16)
+    out = torch.zeros((B, nv * d), dtype=torch.bfloat16, device=DEV)
+    ws = api.lattice_interact_fwd("stack", Xd, out, stack=dev_layers, stack_n=nv, ln_eps=cfg.ln_eps)
+    torch.cuda.synchronize()
+    XL, caches = oi.stack_forward(X, layers, nv, d, rnd, cfg.ln_eps)
+    assert_close_composed("X_L", out, XL.reshape(B, -1), 2e-2)
+    G = synth.randn((B, nv * d), seed=32, scale=1e-3, dtype="bf16")
+    dX = torch.zeros((B, n0, d), dtype=torch.bfloat16, device=DEV)
+    api.lattice_interact_bwd("stack", Xd, to_dev(G, torch.bfloat16), dX, stack=dev_layers,
+                             stack_n=nv, ln_eps=cfg.ln_eps, ws=ws)
+    torch.cuda.synchronize()
+    dX1, grads = oi.stack_backward(G.reshape(B, nv, d), layers, caches, rnd)
+    assert_close_composed("dX", dX, rnd(dX1), 2e-2)
+    for l, (gl, dl) in enumerate(zip(grads, dev_layers)):
+        assert_close_composed(f"layer{l}.dW", dl["dW"], gl["dW"], 2e-2, strict_bound=0.5)
+        assert_close_composed(f"layer{l}.dA", dl["dA"], gl["dA"], 2e-2, strict_bound=0.5)
+        assert_close_composed(f"layer{l}.dgamma", dl["dgamma"], gl["dgamma"], 2e-2)
+        if "dC" in gl:
+            assert_close_composed(f"layer{l}.dC", dl["dC"], gl["dC"], 2e-2, strict_bound=0.5)

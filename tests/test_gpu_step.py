@@ -16,6 +16,10 @@ CASES = {
     "cfg3-small": (synth.small(synth.CFG3, B=128, rows=6000), 0.01),
     "cfg3-small-big-lr": (synth.small(synth.CFG3, B=96, rows=6000), 1000.0),
     "cfg4-small": (synth.small(synth.CFG4, B=256, rows=2000), 0.0),
+    "cfg5-small-d64": (synth.CFG5.scaled(B=64, F=24, rows=1500, d=64, stack_n=8, fm_rank=16,
+                                         top=(128, 32, 8)), 0.0),
+    "cfg5-small-d128": (synth.CFG5.scaled(B=48, F=32, rows=1000, stack_n=16, fm_rank=32,
+                                          top=(256, 64, 16)), 0.0),
 }
 SPARE = {"cfg2-small": 12345}   # workspace planned with more lookups than the batch has
 
@@ -71,7 +75,16 @@ def test_step_matches_oracle(name):
         assert_close_composed(f"bottom{i}.db", w.bottom[i]["db"], g["bottom_db"][i], t)
     if cfg.interact == "fm":
         assert_close_composed("fm.dW", w.fm_dW, g["fm_dW"], t)
-    assert_close_composed("dX_emb", v["dX"][:, s0:], g["dX_emb"], t)
+    if cfg.interact == "stack":
+        for l, (gl, dl) in enumerate(zip(g["stack"], w.stack)):
+            for key in ("dW", "dA", "dgamma", "dC"):
+                if key in gl:
+                    assert_close_composed(f"stack{l}.{key}", dl[key], gl[key], t,
+                                          strict_bound=0.5 if key != "dgamma" else None)
+    # through the stacked layers the embedding-slot gradient passes three
+    # LayerNorm backwards (mean subtraction) and nine contractions
+    assert_close_composed("dX_emb", v["dX"][:, s0:], g["dX_emb"], t,
+                          strict_bound=0.1 if cfg.interact == "stack" else None)
     bk = g["bookkeeping"]
     U = int(v["num_unique"].item())
     assert U == bk["unique_rows"].size
