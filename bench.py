@@ -30,11 +30,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cfg", type=int, default=3)
+    ap.add_argument("--workload", default="large-emb-fm",
+                    help="one of: tiny-dot-f32, mid-dot-bf16, large-emb-fm, multidomain-dot, deep-stack")
     ap.add_argument("--batches", type=int, default=2, help="distinct batches cycled")
     ap.add_argument("--cpu-sample", type=int, default=2048, help="samples in the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--uniform", action="store_true", help="uniform indices (control run)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="after the timed steps, stream 1 GiB through a plain elementwise kernel "
+                         "(torch.neg, 1 GiB read + 1 GiB written) as a counter calibration point")
     return ap.parse_args()
 
 
@@ -59,7 +63,10 @@ def main():
     from paper_2512_09200_amd import api
     from paper_2512_09200_amd._abi import STAGES
 
-    cfg = synth.CONFIGS[args.cfg]
+    if args.workload not in synth.WORKLOADS:
+        print(f"unknown workload {args.workload!r}; choose from {sorted(synth.WORKLOADS)}", file=sys.stderr)
+        sys.exit(2)
+    cfg = synth.WORKLOADS[args.workload]
     if args.uniform:
         cfg = cfg.scaled(index_dist=("uniform",))
     dev = "cuda"
@@ -166,10 +173,20 @@ def main():
     mfma_tfs = 3.0 * flops_fwd / (dense_ms * 1e-3) / 1e12
     samples_per_s = cfg.B / (ms_per_step * 1e-3)
 
+    traffic = counted_traffic(cfg.name, "embbag_fwd_kernel")
     roofline = {"bound": "hbm", "kernel": "embbag_fwd_kernel", "achieved": round(fwd_gbs, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(fwd_gbs / HBM_PEAK_GBS, 4),
-                "traffic": None,
+                "traffic": traffic,
                 "bytes_per_launch": int(fwd_bytes), "launch_ms": round(stage_ms["embbag_fwd"], 4)}
+
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload ----
     cpu = None
@@ -197,6 +214,35 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def source_digest(files):
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counted_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    counter summary (FETCH_SIZE + WRITE_SIZE, each scaled by the reading of a
+    copy kernel of known size), or None when there is none or the kernel's
+    sources have changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt")
+    try:
+        kv = {}
+        for line in open(path):
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        files = kv["sources"].split()
+        if source_digest(files) != kv["sources_sha256"]:
+            return None
+        return int(kv["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(cfg, batch, params, E, n_samples):

@@ -94,40 +94,40 @@ class Config:
 SEED_BASE = 2512092000
 
 
-CFG1 = Config(
-    name="cfg1-tiny-f32", B=128, F=8, rows=4096, d=32, dtype="f32",
+TINY = Config(
+    name="tiny-dot-f32", B=128, F=8, rows=4096, d=32, dtype="f32",
     index_dist=("uniform",), bag_dist=("uniform", 1, 8),
     dense_in=13, bottom=(64, 32), interact="dot", top=(64, 4),
     label_p=("fixed", 0.3), mask=("none",), seed=SEED_BASE + 1)
 
-CFG2 = Config(
-    name="cfg2-mid-bf16", B=2048, F=26, rows=100_000, d=64, dtype="bf16",
+MID = Config(
+    name="mid-dot-bf16", B=2048, F=26, rows=100_000, d=64, dtype="bf16",
     index_dist=("zipf", 1.1), bag_dist=("poisson", 10.0, 1, 64),
     dense_in=13, bottom=(256, 64), interact="dot", top=(512, 256, 8),
     label_p=("uniform", 0.01, 0.3), mask=("iid", 0.5), seed=SEED_BASE + 2)
 
-CFG3 = Config(
-    name="cfg3-large-emb-fm", B=8192, F=64, rows=2_000_000, d=128, dtype="bf16",
+LARGE_FM = Config(
+    name="large-emb-fm", B=8192, F=64, rows=2_000_000, d=128, dtype="bf16",
     index_dist=("zipf", 1.05), bag_dist=("poisson", 20.0, 1, 128),
     dense_in=64, bottom=(512, 128), interact="fm", fm_rank=32,
     top=(1024, 512, 16), label_p=("uniform", 0.01, 0.3), mask=("iid", 0.5),
     lr_tables=0.01, seed=SEED_BASE + 3)
 
-CFG4 = Config(
-    name="cfg4-multidomain", B=8192, F=96, rows=1_000_000, d=128, dtype="bf16",
+MULTIDOMAIN = Config(
+    name="multidomain-dot", B=8192, F=96, rows=1_000_000, d=128, dtype="bf16",
     index_dist=("zipf", 1.1), bag_dist=("poisson", 15.0, 1, 128),
     dense_in=64, bottom=(512, 128), interact="dot", top=(1024, 512, 32),
     label_p=("uniform", 0.01, 0.3), mask=("domain",),
     domains=((0.4, 0.3, 0.2, 0.1), 40, 8), seed=SEED_BASE + 4)
 
-CFG5 = Config(
-    name="cfg5-deep-stack", B=16384, F=256, rows=500_000, d=128, dtype="bf16",
+DEEP_STACK = Config(
+    name="deep-stack", B=16384, F=256, rows=500_000, d=128, dtype="bf16",
     index_dist=("zipf", 1.05), bag_dist=("poisson", 8.0, 1, 64),
     dense_in=0, bottom=(), interact="stack", fm_rank=64, stack_layers=3,
     stack_n=64, top=(2048, 512, 64), label_p=("uniform", 0.01, 0.3),
     mask=("iid", 0.5), seed=SEED_BASE + 5)
 
-CONFIGS = {1: CFG1, 2: CFG2, 3: CFG3, 4: CFG4, 5: CFG5}
+WORKLOADS = {c.name: c for c in (TINY, MID, LARGE_FM, MULTIDOMAIN, DEEP_STACK)}
 
 
 def small(cfg: Config, B: int, rows: int, **kw) -> Config:

@@ -10,12 +10,12 @@ from oracle.step import rounding
 from tests._util import DEV, Workload, assert_close, tol
 
 CASES = {
-    "cfg1": synth.CFG1,
-    "cfg1-mean": synth.CFG1.scaled(pool="mean"),
-    "cfg2-small": synth.small(synth.CFG2, B=256, rows=3000),
-    "cfg4-small-empty-bags": synth.small(synth.CFG4, B=192, rows=1500),
-    "cfg3-small": synth.small(synth.CFG3, B=64, rows=20000),
-    "d256-bf16-mean": synth.small(synth.CFG2, B=96, rows=800, F=5, d=256, pool="mean"),
+    "tiny": synth.TINY,
+    "tiny-mean": synth.TINY.scaled(pool="mean"),
+    "mid-small": synth.small(synth.MID, B=256, rows=3000),
+    "multidomain-small-empty-bags": synth.small(synth.MULTIDOMAIN, B=192, rows=1500),
+    "large-fm-small": synth.small(synth.LARGE_FM, B=64, rows=20000),
+    "d256-bf16-mean": synth.small(synth.MID, B=96, rows=800, F=5, d=256, pool="mean"),
 }
 
 
@@ -114,7 +114,7 @@ def test_embbag_bwd_hot_row_spanning_many_chunks():
 @pytest.mark.gpu
 def test_embbag_bwd_is_deterministic():
     from paper_2512_09200_amd import api
-    cfg = CASES["cfg2-small"]
+    cfg = CASES["mid-small"]
     w = Workload(cfg)
     dX = torch.from_numpy(synth.randn((cfg.B, cfg.n_slots, cfg.d), seed=9, dtype=cfg.dtype)).to(
         torch.bfloat16).to(DEV)
@@ -131,7 +131,7 @@ def test_embbag_bwd_is_deterministic():
 @pytest.mark.gpu
 def test_validate_batch():
     from paper_2512_09200_amd import api
-    cfg = CASES["cfg2-small"]
+    cfg = CASES["mid-small"]
     w = Workload(cfg)
     ok, _ = api.lattice_validate_batch(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B)
     assert ok

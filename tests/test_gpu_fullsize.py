@@ -12,7 +12,7 @@ from oracle import embbag as oe
 from oracle.bf16 import round_bf16
 from tests._util import DEV, assert_close
 
-CFG = synth.CFG3
+CFG = synth.LARGE_FM
 
 
 @pytest.fixture(scope="module")

@@ -11,11 +11,11 @@ from tests._util import DEV, assert_close, to_dev
 
 CASES = {
     # name: (kind, dtype, B, n, d, k, emit0, zero_slots)
-    "dot-f32-cfg1": ("dot", "f32", 128, 9, 32, 0, True, False),
-    "dot-bf16-cfg2": ("dot", "bf16", 300, 27, 64, 0, True, False),
-    "dot-bf16-cfg4-absent": ("dot", "bf16", 96, 97, 128, 0, True, True),
-    "fm-bf16-cfg3": ("fm", "bf16", 200, 65, 128, 32, True, False),      # MFMA path
-    "fm-bf16-cfg3-many": ("fm", "bf16", 700, 65, 128, 32, True, False), # > 1 sample per block
+    "dot-f32-tiny": ("dot", "f32", 128, 9, 32, 0, True, False),
+    "dot-bf16-n27": ("dot", "bf16", 300, 27, 64, 0, True, False),
+    "dot-bf16-n97-absent": ("dot", "bf16", 96, 97, 128, 0, True, True),
+    "fm-bf16-n65": ("fm", "bf16", 200, 65, 128, 32, True, False),      # MFMA path
+    "fm-bf16-n65-many": ("fm", "bf16", 700, 65, 128, 32, True, False), # > 1 sample per block
     "fm-bf16-n30-d64-k32": ("fm", "bf16", 37, 30, 64, 32, False, False),  # MFMA, other tiles
     "fm-bf16-n29-d128-k64": ("fm", "bf16", 41, 29, 128, 64, True, False),
     "fm-bf16-valu": ("fm", "bf16", 33, 10, 32, 16, False, False),       # VALU path (d=32)
@@ -85,7 +85,7 @@ def test_stack_fwd_bwd(name):
     from tests._util import assert_close_composed, stack_dev
     B, n0, nv, d, k, L = STACK_CASES[name]
     print(f"[stack] {name}", flush=True)
-    cfg = synth.CFG5.scaled(B=B, F=n0, d=d, stack_n=nv, fm_rank=k, stack_layers=L,
+    cfg = synth.DEEP_STACK.scaled(B=B, F=n0, d=d, stack_n=nv, fm_rank=k, stack_layers=L,
                             top=(16, 4), seed=77)
     params = synth.make_dense_params(cfg)
     layers = params["stack"]

@@ -11,17 +11,17 @@ from oracle import step as ostep
 from tests._util import DEV, Workload, assert_close, assert_close_composed, relu_overrides, tol
 
 CASES = {
-    "cfg1": (synth.CFG1, 0.0),
-    "cfg2-small": (synth.small(synth.CFG2, B=256, rows=3000), 0.0),
-    "cfg3-small": (synth.small(synth.CFG3, B=128, rows=6000), 0.01),
-    "cfg3-small-big-lr": (synth.small(synth.CFG3, B=96, rows=6000), 1000.0),
-    "cfg4-small": (synth.small(synth.CFG4, B=256, rows=2000), 0.0),
-    "cfg5-small-d64": (synth.CFG5.scaled(B=64, F=24, rows=1500, d=64, stack_n=8, fm_rank=16,
+    "tiny": (synth.TINY, 0.0),
+    "mid-small": (synth.small(synth.MID, B=256, rows=3000), 0.0),
+    "large-fm-small": (synth.small(synth.LARGE_FM, B=128, rows=6000), 0.01),
+    "large-fm-small-big-lr": (synth.small(synth.LARGE_FM, B=96, rows=6000), 1000.0),
+    "multidomain-small": (synth.small(synth.MULTIDOMAIN, B=256, rows=2000), 0.0),
+    "deep-stack-small-d64": (synth.DEEP_STACK.scaled(B=64, F=24, rows=1500, d=64, stack_n=8, fm_rank=16,
                                          top=(128, 32, 8)), 0.0),
-    "cfg5-small-d128": (synth.CFG5.scaled(B=48, F=32, rows=1000, stack_n=16, fm_rank=32,
+    "deep-stack-small-d128": (synth.DEEP_STACK.scaled(B=48, F=32, rows=1000, stack_n=16, fm_rank=32,
                                           top=(256, 64, 16)), 0.0),
 }
-SPARE = {"cfg2-small": 12345}   # workspace planned with more lookups than the batch has
+SPARE = {"mid-small": 12345}   # workspace planned with more lookups than the batch has
 
 
 def gpu_relu_io(cfg, w, v):
@@ -105,7 +105,7 @@ def test_step_matches_oracle(name):
 
 @pytest.mark.gpu
 def test_step_is_deterministic():
-    cfg = synth.small(synth.CFG3, B=128, rows=6000)
+    cfg = synth.small(synth.LARGE_FM, B=128, rows=6000)
     w = Workload(cfg)
     _, v1, ws1 = run_step(w, 0.0)
     g1 = [L["dW"].clone() for L in w.top + w.bottom] + [w.fm_dW.clone()]

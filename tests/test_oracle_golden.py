@@ -43,7 +43,7 @@ def test_worked_example():
 
 def test_bf16_storage_mode_stays_close_to_float64_mode():
     # the storage points only perturb values at the bf16 rounding level
-    cfg16 = synth.small(synth.CFG2, B=64, rows=500)
+    cfg16 = synth.small(synth.MID, B=64, rows=500)
     cfg64 = cfg16.scaled(dtype="f32")
     batch = synth.make_batch(cfg16)
     params = synth.make_dense_params(cfg16)              # bf16-valued weights for both modes
