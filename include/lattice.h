@@ -120,7 +120,8 @@ size_t lattice_embbag_bwd_workspace(const lattice_tables* tables, const lattice_
  * summed in fp32 in a fixed order.  If lr != 0 the occurring rows of
  * tables->data are updated in place: E[r] <- round(E[r] - lr * G[r]); other
  * rows are untouched.  dX is [B, n_slots, dim] in dx_dtype.  Errors:
- * INVALID_ARG, UNSUPPORTED (dim, total_rows >= 2^31), WORKSPACE, HIP. */
+ * INVALID_ARG, UNSUPPORTED (dim, total_rows >= 2^31, dX larger than 4 GiB),
+ * WORKSPACE, HIP. */
 lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_jagged* bags,
                                   lattice_pool pool, const void* dX, lattice_dtype dx_dtype,
                                   int32_t n_slots, int32_t first_slot,
@@ -325,7 +326,8 @@ lattice_status lattice_step_plan(const lattice_model_desc* model, int32_t B, int
  * the workspace (see lattice_step_layout); with lr_tables != 0 the tables are
  * updated in place.  ws must be lattice_step_plan(...)->total_bytes long for
  * the same opts; the batch's nnz must not exceed opts->nnz_capacity (when
- * set).  Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP. */
+ * set).  Errors: INVALID_ARG, UNSUPPORTED (also: stacked vectors X larger
+ * than 4 GiB), WORKSPACE, HIP. */
 lattice_status lattice_step(const lattice_model_desc* model, const lattice_batch_desc* batch,
                             const lattice_step_opts* opts, void* ws, size_t ws_bytes,
                             void* stream);

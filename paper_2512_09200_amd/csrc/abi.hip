@@ -113,6 +113,8 @@ lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_ja
   REQUIRE(pool == LATTICE_POOL_SUM || pool == LATTICE_POOL_MEAN, "bad pool mode");
   REQUIRE(first_slot >= 0 && first_slot + bags->num_features <= n_slots, "slots out of range");
   if (bags->nnz > 0) REQUIRE(dX, "null dX");
+  if ((int64_t)bags->batch * n_slots * tables->dim * (int64_t)esize(dx_dtype) > (int64_t)UINT32_MAX)
+    FAIL(LATTICE_ERR_UNSUPPORTED, "dX larger than 4 GiB");
   const size_t need = embbag_bwd_workspace(bags->nnz, tables->dim);
   if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
   HIPRET(embbag_bwd(tables->row_base, tables->total_rows, bags->offsets, bags->indices,
@@ -552,6 +554,9 @@ static lattice_status check_model(const lattice_model_desc* m, int B) {
   REQUIRE(m->interact.emit_slot0 == want_emit, "emit_slot0 must be %d", want_emit);
   REQUIRE(m->top.layers[0].in_dim == interact_width(&m->interact), "top input width %d != %lld",
           m->top.layers[0].in_dim, (long long)interact_width(&m->interact));
+  if ((int64_t)B * n * d * (int64_t)esize(m->dtype) > (int64_t)UINT32_MAX)
+    FAIL(LATTICE_ERR_UNSUPPORTED, "stacked vectors of %lld bytes exceed 4 GiB",
+         (long long)B * n * d * (int64_t)esize(m->dtype));
   return LATTICE_OK;
 }
 

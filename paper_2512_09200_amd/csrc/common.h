@@ -93,6 +93,18 @@ __device__ inline void stg16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*
 
 inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
+// MI355X has 8 XCDs, each with its own L2; consecutive workgroup ids are
+// dealt to the XCDs round-robin.  xcd_block() renumbers the linear block id
+// so that each XCD walks one contiguous share of [0, nblocks): work items
+// that are neighbours in the renumbered order share one L2.  A bijection on
+// [0, nblocks).
+constexpr int NUM_XCD = 8;
+__device__ inline int xcd_block(int bid, int nblocks) {
+  const int x = bid % NUM_XCD, i = bid / NUM_XCD;
+  const int q = nblocks / NUM_XCD, r = nblocks % NUM_XCD;
+  return x * q + (x < r ? x : r) + i;
+}
+
 }  // namespace lat
 
 // Host-side error plumbing shared by the launchers.

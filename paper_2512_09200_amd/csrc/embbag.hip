@@ -13,14 +13,15 @@
 //   keys     : key = row_base[f] + index, value = bag id, per position
 //   sort     : stable LSD radix sort by key (ties keep position order)
 //   segments : run boundaries -> unique rows ascending, run offsets, and the
-//              segment id at each chunk start
-//   chunks   : the sorted occurrences are cut into fixed chunks of 64; one
-//              block per chunk gathers its 64 dX rows into LDS (all loads in
-//              flight at once), then each thread walks one column in order.
-//              Runs that end inside the chunk are final (written to G and/or
-//              applied as SGD); runs cut by a chunk boundary leave a partial
-//   fixup    : each run that spans chunks sums its partials in chunk order
-// Work per block is uniform whatever the Zipf skew of the rows.
+//              run id before every 256-position range
+//   reduce   : one wave per range of 256 sorted occurrences; dX rows are
+//              gathered into registers chunk by chunk and summed by an
+//              in-register segmented scan in a fixed order, with the running
+//              sum carried from chunk to chunk.  Runs that start and end in
+//              the range are final (written to G and/or applied as SGD); a
+//              run cut by a range boundary leaves a partial sum
+//   fixup    : each run that crosses ranges sums its partials in range order
+// Work per wave is uniform whatever the Zipf skew of the rows.
 #include "common.h"
 #include "kernels.h"
 
@@ -39,12 +40,16 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
   constexpr int G = 64 / LP;           // row groups per wave
   constexpr int U = (16 / G) > 0 ? (16 / G) : 1;  // loads in flight per group
   const int lane = threadIdx.x & 63;
-  const int64_t bag = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  // each XCD pools a contiguous span of bags (whole tables): a table's hot
+  // rows are cached in one L2 instead of in all of them
+  // (the bag and its bounds are made scalar explicitly: uniform loop control)
+  const int64_t bag = __builtin_amdgcn_readfirstlane(xcd_block(blockIdx.x, gridDim.x) * 4 + (threadIdx.x >> 6));
   if (bag >= (int64_t)F * B) return;
   const int f = (int)(bag / B), b = (int)(bag % B);
   const int g = lane / LP, sub = lane % LP;
   const bool active = sub * VE < dim;
-  const int start = offsets[bag], end = offsets[bag + 1];
+  const int start = __builtin_amdgcn_readfirstlane(offsets[bag]);
+  const int end = __builtin_amdgcn_readfirstlane(offsets[bag + 1]);
   const TT* Ef = E + row_base[f] * (int64_t)dim + sub * VE;
 
   if (keys) {  // sort keys of the backward (global row) and values (bag id), coalesced
@@ -163,7 +168,9 @@ __global__ __launch_bounds__(256) void embbag_keys_kernel(const int64_t* __restr
 constexpr int SEG_THREADS = 256;
 constexpr int SEG_ITEMS = 16;
 constexpr int SEG_TILE = SEG_THREADS * SEG_ITEMS;
-constexpr int CHUNK = 64;  // occurrences per reduction chunk
+// Sorted occurrences per wave in the segmented reduction.  Partial sums only
+// arise where a run crosses a multiple of RANGE.
+constexpr int RANGE = 256;
 
 __device__ inline int seg_flag(const int* k, int64_t i) { return (i == 0 || k[i] != k[i - 1]) ? 1 : 0; }
 
@@ -202,37 +209,47 @@ __global__ __launch_bounds__(SEG_THREADS) void seg_count_kernel(const int* __res
   if (threadIdx.x == 0) tile_counts[blockIdx.x] = tot;
 }
 
+// Run starts of one tile, visited as SEG_ITEMS consecutive 256-position
+// stripes (coalesced); a stripe's starts are ranked by wave ballots.  Writes
+// the unique rows and run offsets, num_unique, and for every RANGE-aligned
+// position k the id of the run holding position k-1 (-1 at k = 0).
 __global__ __launch_bounds__(SEG_THREADS) void seg_write_kernel(
     const int* __restrict__ keys, int n, const int* __restrict__ tile_base,
     int* __restrict__ unique_rows, int* __restrict__ seg_offsets, int* __restrict__ num_unique,
-    int* __restrict__ chunk_uid) {
-  __shared__ int lds[SEG_THREADS / 64];
-  const int64_t base = (int64_t)blockIdx.x * SEG_TILE + (int64_t)threadIdx.x * SEG_ITEMS;
-  int fl[SEG_ITEMS];
-  int c = 0;
-#pragma unroll
+    int* __restrict__ range_ubefore) {
+  __shared__ int wsum[SEG_THREADS / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  int run = tile_base[blockIdx.x];
+  const int64_t base = (int64_t)blockIdx.x * SEG_TILE;
   for (int i = 0; i < SEG_ITEMS; ++i) {
-    fl[i] = (base + i < n) ? seg_flag(keys, base + i) : 0;
-    c += fl[i];
-  }
-  int tot;
-  int run = block_sum_scan(c, lds, &tot) + tile_base[blockIdx.x];
+    const int64_t k = base + (int64_t)i * SEG_THREADS + threadIdx.x;
+    const bool in = k < n;
+    const int key = in ? keys[k] : 0;
+    const int fl = in && (k == 0 || key != keys[k - 1]) ? 1 : 0;
+    const uint64_t m = __ballot(fl);
+    if (lane == 0) wsum[w] = __popcll(m);
+    __syncthreads();
+    int off = 0, tot = 0;
 #pragma unroll
-  for (int i = 0; i < SEG_ITEMS; ++i) {
-    const int64_t k = base + i;
-    if (k < n) {
-      run += fl[i];
-      const int u = run - 1;  // segment id of position k
-      if (fl[i]) {
-        unique_rows[u] = keys[k];
+    for (int q = 0; q < SEG_THREADS / 64; ++q) {
+      off += q < w ? wsum[q] : 0;
+      tot += wsum[q];
+    }
+    __syncthreads();
+    if (in) {
+      const int u = run + off + __popcll(m & lt) + fl - 1;  // run id of position k
+      if (fl) {
+        unique_rows[u] = key;
         seg_offsets[u] = (int)k;
       }
-      if (k % CHUNK == 0) chunk_uid[k / CHUNK] = u;
+      if (k % RANGE == 0) range_ubefore[k / RANGE] = u - fl;
       if (k == n - 1) {
         num_unique[0] = u + 1;
         seg_offsets[u + 1] = n;
       }
     }
+    run += tot;
   }
 }
 
@@ -242,220 +259,301 @@ __global__ void set_empty_kernel(int* num_unique, int* seg_offsets) {
 }
 
 // ---------------------------------------------------------------------------
-// backward: chunked segmented reduction (+ fused SGD)
+// backward: segmented reduction over the sorted occurrences (+ fused SGD)
 // ---------------------------------------------------------------------------
-template <typename ET>
-__device__ inline void finalize_row(int u, int row, float g, int a, int dim, float* grad_rows,
-                                    ET* E, float lr) {
-  if (grad_rows) grad_rows[(int64_t)u * dim + a] = g;
-  if (E) {
-    ET* e = E + (int64_t)row * dim + a;
-    st(e, ld(e) - lr * g);
+// N consecutive elements of T held by one lane, as raw 32-bit words.
+template <typename T, int N>
+struct Frag {
+  static constexpr int NB = N * (int)sizeof(T);
+  static constexpr int W = NB >= 4 ? NB / 4 : 1;
+  uint32_t w[W];
+  __device__ inline void load(const T* p) {
+    if constexpr (NB == 2) {
+      w[0] = *reinterpret_cast<const uint16_t*>(p);
+    } else if constexpr (NB == 4) {
+      w[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else if constexpr (NB == 8) {
+      const uint2 v = *reinterpret_cast<const uint2*>(p);
+      w[0] = v.x;
+      w[1] = v.y;
+    } else {
+#pragma unroll
+      for (int q = 0; q < W / 4; ++q) {
+        const u32x4 v = ldg16(reinterpret_cast<const uint32_t*>(p) + 4 * q);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[4 * q + t] = v[t];
+      }
+    }
   }
-}
+  // element i as fp32
+  __device__ inline float get(int i) const {
+    if constexpr (sizeof(T) == 2)
+      return __uint_as_float((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16));
+    else
+      return __uint_as_float(w[i]);
+  }
+  // stores v[0..N) rounded to T
+  __device__ static inline void store(T* p, const float* v) {
+    uint32_t o[W];
+    if constexpr (sizeof(T) == 2) {
+      if constexpr (N == 1) {
+        *reinterpret_cast<uint16_t*>(p) = f2bf(v[0]);
+        return;
+      } else {
+#pragma unroll
+        for (int t = 0; t < W; ++t) o[t] = pack_bf2(v[2 * t], v[2 * t + 1]);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < W; ++t) o[t] = __float_as_uint(v[t]);
+    }
+    if constexpr (NB == 4) {
+      *reinterpret_cast<uint32_t*>(p) = o[0];
+    } else if constexpr (NB == 8) {
+      *reinterpret_cast<uint2*>(p) = uint2{o[0], o[1]};
+    } else if constexpr (NB >= 16) {
+#pragma unroll
+      for (int q = 0; q < W / 4; ++q)
+        stg16(reinterpret_cast<uint32_t*>(p) + 4 * q, u32x4{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]});
+    }
+  }
+};
 
-// One block per chunk of CHUNK consecutive sorted occurrences.
-//  1. wave 0: keys and bags of the chunk; run boundaries by ballot; the
-//     pieces (maximal runs inside the chunk) with their end position, segment
-//     id and kind (complete run, or cut by the chunk start / end)
-//  2. all threads: gather the chunk's dX rows into LDS (fp32) and, at the same
-//     time, load the table rows of the complete runs that the SGD updates
-//  3. work items (piece, 8 columns): sum the piece's rows in position order
-//     and write the row gradient / apply the SGD / store the partial
-template <typename DT, typename ET>
-__global__ __launch_bounds__(256) void chunk_reduce_kernel(
+// One wave per RANGE consecutive sorted occurrences.  The wave walks the
+// occurrences one dX row per step: lane l holds bytes [l*BPL, (l+1)*BPL) of
+// the row, so run starts and ends are the same for every lane and the
+// segmented sum is a single running fp32 accumulator per column, reset at
+// each run start and added to in position order (uniform branches, no
+// cross-lane arithmetic).  Per chunk of 64 occurrences:
+//   1. keys and bag ids (one per lane, prefetched a chunk ahead); run starts
+//      and ends by comparing neighbouring keys (ballots)
+//   2. in groups of S occurrences: the S dX rows, and the table rows of the
+//      runs that end there and started inside this range, all loads in
+//      flight together; then the S steps of the running sum
+//   3. at each run end: a complete run writes its row gradient and/or applies
+//      the SGD update; the run cut by the range start (no start inside the
+//      range) goes to partial slot 0, the run cut by the range end to slot 1
+// No floating-point atomics; every sum is taken in position order.
+// FULL: the row is exactly 64*BPL bytes (every lane active, no predication).
+template <typename DT, typename ET, int BPL, bool MEAN, bool FULL>
+struct SegWave {
+  static constexpr int EPL = BPL / (int)sizeof(DT);       // columns per lane
+  static constexpr int S = BPL == 4 ? 32 : (BPL == 8 ? 16 : 8);  // rows in flight
+  // per-wave state (wave-uniform scalars and this lane's accumulators)
+  float acc[EPL];
+  bool started;
+  int u_before;
+
+  // One group of S occurrences starting at chunk row s0 (s0 + S <= cnt when
+  // CHECK is false).  xoff: per-lane byte offset of the occurrence's dX row;
+  // key: per-lane global row.
+  template <bool CHECK>
+  __device__ inline void group(int s0, int cnt, uint64_t smask, uint64_t cmask, uint64_t pmask,
+                               int xoff, int key, float scl, const char* dXb, ET* E,
+                               float* grad_rows, float* part, int wave, int dim, int lane_b,
+                               int col, bool active, float lr) {
+    Frag<DT, EPL> xf[S];
+    Frag<ET, EPL> ef[S];
+    const int lane_e = col * (int)sizeof(ET);
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      const int r = s0 + i;
+      if (CHECK && r >= cnt) break;
+      const char* rowp = dXb + (uint32_t)__builtin_amdgcn_readlane(xoff, r);
+      if (FULL || active) xf[i].load(reinterpret_cast<const DT*>(rowp + lane_b));
+      if (E && ((cmask >> r) & 1)) {
+        const char* erow = reinterpret_cast<const char*>(E) +
+                           (int64_t)__builtin_amdgcn_readlane(key, r) * dim * (int64_t)sizeof(ET);
+        if (FULL || active) ef[i].load(reinterpret_cast<const ET*>(erow + lane_e));
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      const int r = s0 + i;
+      if (CHECK && r >= cnt) break;
+      float sc = 1.f;
+      if (MEAN) sc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scl), r));
+      const bool st = (smask >> r) & 1;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const float v = MEAN ? xf[i].get(e) * sc : xf[i].get(e);
+        acc[e] = st ? v : acc[e] + v;
+      }
+      if ((pmask >> r) & 1) {
+        const uint64_t le = (r == 63) ? ~0ull : ((2ull << r) - 1);
+        if ((cmask >> r) & 1) {
+          if (grad_rows && (FULL || active))
+            Frag<float, EPL>::store(grad_rows + (int64_t)(u_before + __popcll(smask & le)) * dim + col, acc);
+          if (E) {
+            float upd[EPL];
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) upd[e] = ef[i].get(e) - lr * acc[e];
+            ET* erow = E + (int64_t)__builtin_amdgcn_readlane(key, r) * dim;
+            if (FULL || active) Frag<ET, EPL>::store(erow + col, upd);
+          }
+        } else {
+          const bool has_start = started || (smask & le);
+          if (FULL || active)
+            Frag<float, EPL>::store(part + ((int64_t)wave * 2 + (has_start ? 1 : 0)) * dim + col, acc);
+        }
+      }
+    }
+  }
+};
+
+template <typename DT, typename ET, int BPL, bool MEAN, bool FULL>
+__global__ __launch_bounds__(256) void seg_reduce_kernel(
     const int* __restrict__ skeys, const int* __restrict__ sbags, int n,
     const DT* __restrict__ dX, int B, int n_slots, int first_slot, int dim,
-    const int32_t* __restrict__ offsets, int mean, const int* __restrict__ chunk_uid,
+    const int32_t* __restrict__ offsets, const int* __restrict__ range_ubefore,
     float* __restrict__ part, int* __restrict__ part_uid, int* __restrict__ span_list,
     int* __restrict__ span_count, float* __restrict__ grad_rows, ET* __restrict__ E, float lr) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-  DT* rows = reinterpret_cast<DT*>(smem_raw);  // [CHUNK][dim], the gathered dX rows as stored
-  __shared__ int k_s[CHUNK];
-  __shared__ int b_s[CHUNK];
-  __shared__ float sc_s[CHUNK];
-  __shared__ int pend_s[CHUNK];    // end position of piece i
-  __shared__ int pkind_s[CHUNK];   // 1: complete run, 2: cut at chunk start (slot 0), 3: cut at end only (slot 1)
-  __shared__ int pu_s[CHUNK];      // segment id of piece i
-  __shared__ int npieces_s;
-  const int c = blockIdx.x;
-  const int64_t p0 = (int64_t)c * CHUNK;
-  const int cnt = (int)((n - p0) < CHUNK ? (n - p0) : CHUNK);
-  const int tid = threadIdx.x;
-  if (tid < CHUNK) {
-    const int key = tid < cnt ? skeys[p0 + tid] : -1;
-    const int prev = p0 > 0 ? skeys[p0 - 1] : -1;
-    const int next = (p0 + cnt < n) ? skeys[p0 + cnt] : -1;
-    const int key_prev = __shfl_up(key, 1, 64);
-    const bool starts = tid < cnt && tid > 0 && key != key_prev;
-    const uint64_t smask = __ballot(starts);
-    const uint64_t le = (tid == 63) ? ~0ull : ((2ull << tid) - 1);
-    const int u = chunk_uid[c] + __popcll(smask & le);
-    const int key_next = __shfl_down(key, 1, 64);
-    const bool ends = tid < cnt && (tid == cnt - 1 || key_next != key);
-    const uint64_t emask = __ballot(ends);
-    const bool starts_before = p0 > 0 && prev == __shfl(key, 0, 64);
-    const bool touch_start = (smask & le) == 0 && starts_before;
-    const bool touch_end = (tid == cnt - 1) && next == key;
-    if (tid < cnt) {
-      k_s[tid] = key;
-      const int bag = sbags[p0 + tid];
-      b_s[tid] = bag;
-      sc_s[tid] = mean ? 1.f / (float)(offsets[bag + 1] - offsets[bag]) : 1.f;
-    }
-    if (ends) {
-      const int i = __popcll(emask & (le >> 1));  // pieces ending before tid
-      pend_s[i] = tid;
-      pkind_s[i] = (!touch_start && !touch_end) ? 1 : (touch_start ? 2 : 3);
-      pu_s[i] = u;
-    }
-    if (tid == 0) npieces_s = __popcll(emask);
-    if (ends && tid == cnt - 1) {
-      part_uid[c] = touch_end ? u : -1;
-      if (touch_end && !touch_start) span_list[atomicAdd(span_count, 1)] = c;
-    }
-  }
-  __syncthreads();
+  using W = SegWave<DT, ET, BPL, MEAN, FULL>;
+  constexpr int EPL = W::EPL, S = W::S;
+  const int lane = threadIdx.x & 63;
+  // Each XCD takes a contiguous span of ranges, so the dX rows of one table's
+  // occurrences stay in that XCD's L2 while it works through them.  Wave-
+  // uniform values are made scalar explicitly: all control flow below is
+  // uniform branching.
+  const int wave = __builtin_amdgcn_readfirstlane(xcd_block(blockIdx.x, gridDim.x) * 4 + (threadIdx.x >> 6));
+  const int r0 = wave * RANGE;
+  if (r0 >= n) return;
+  const int rend = n - r0 < RANGE ? n : r0 + RANGE;
+  const int col = lane * EPL;
+  const bool active = col < dim;
+  const int lane_b = lane * BPL;
+  const int row_bytes = dim * (int)sizeof(DT);
+  const char* dXb = reinterpret_cast<const char*>(dX);
 
-  constexpr int VE = 16 / sizeof(DT);
-  const int vpr = dim / VE;
-  const int total = cnt * vpr;
-  const int np = npieces_s;
-  const int ipr = dim / 8;          // work items per piece (8 columns each)
-  const int items = np * ipr;
-  // table rows of this thread's complete pieces: loads in flight with the gather
-  constexpr int EV = 8 * sizeof(ET) / 16;  // 16-byte vectors per 8 columns
-  u32x4 ev[4][EV];
-  if (E) {
+  W w;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int it = tid + q * 256;
-      if (it < items) {
-        const int i = it / ipr, a = (it - i * ipr) * 8;
-        if (pkind_s[i] == 1) {
-          const ET* e = E + (int64_t)k_s[pend_s[i]] * dim + a;
-#pragma unroll
-          for (int h = 0; h < EV; ++h) ev[q][h] = ldg16(e + h * (16 / sizeof(ET)));
-        }
-      }
-    }
-  }
-  for (int v0 = tid; v0 < total; v0 += 256 * 4) {
-    u32x4 buf[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int v = v0 + q * 256;
-      if (v < total) {
-        const int r = v / vpr, col = (v % vpr) * VE;
-        const int bag = b_s[r];
-        const int f = bag / B, b = bag % B;
-        buf[q] = ldg16(dX + ((int64_t)b * n_slots + first_slot + f) * dim + col);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int v = v0 + q * 256;
-      if (v < total) {
-        const int r = v / vpr, col = (v % vpr) * VE;
-        *reinterpret_cast<u32x4*>(rows + r * dim + col) = buf[q];
-      }
-    }
-  }
-  __syncthreads();
+  for (int e = 0; e < EPL; ++e) w.acc[e] = 0.f;
+  w.started = false;                                       // a run started at or after r0
+  w.u_before = __builtin_amdgcn_readfirstlane(range_ubefore[wave]);  // run id before the chunk
+  int prev_key = r0 > 0 ? __builtin_amdgcn_readfirstlane(skeys[r0 - 1]) : -1;
+  int last_nxt = -1;
 
-  // items beyond the first 1024 (dim > 128) load their table rows in place
-  for (int base = 0; base < items; base += 1024) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int it = base + tid + q * 256;
-      if (it >= items) continue;
-      const int i = it / ipr, a = (it - i * ipr) * 8;
-      const int pe = pend_s[i], ps = i == 0 ? 0 : pend_s[i - 1] + 1;
-      const int kind = pkind_s[i];
-      if (base > 0 && E && kind == 1) {
-        const ET* e = E + (int64_t)k_s[pe] * dim + a;
-#pragma unroll
-        for (int h = 0; h < EV; ++h) ev[q][h] = ldg16(e + h * (16 / sizeof(ET)));
-      }
-      float g[8];
-#pragma unroll
-      for (int h = 0; h < 8; ++h) g[h] = 0.f;
-      for (int p = ps; p <= pe; ++p) {
-        float x[8];
-#pragma unroll
-        for (int h = 0; h < 8; h += VE)
-          Vec16<DT>::unpack(*reinterpret_cast<const u32x4*>(rows + p * dim + a + h), x + h);
-        const float scl = sc_s[p];
-#pragma unroll
-        for (int h = 0; h < 8; ++h) g[h] += mean ? x[h] * scl : x[h];
-      }
-      if (kind == 1) {
-        if (grad_rows) {
-          float* gr = grad_rows + (int64_t)pu_s[i] * dim + a;
-          stg16(gr, u32x4{__float_as_uint(g[0]), __float_as_uint(g[1]), __float_as_uint(g[2]), __float_as_uint(g[3])});
-          stg16(gr + 4, u32x4{__float_as_uint(g[4]), __float_as_uint(g[5]), __float_as_uint(g[6]), __float_as_uint(g[7])});
-        }
-        if (E) {
-          constexpr int PV = 16 / sizeof(ET);
-          ET* e = E + (int64_t)k_s[pe] * dim + a;
-#pragma unroll
-          for (int h = 0; h < EV; ++h) {
-            float x[PV];
-            Vec16<ET>::unpack(ev[q][h], x);
-#pragma unroll
-            for (int t = 0; t < PV; ++t) x[t] = x[t] - lr * g[h * PV + t];
-            stg16(e + h * PV, Vec16<ET>::pack(x));
-          }
-        }
-      } else {
-        float* pp = part + ((int64_t)c * 2 + (kind - 2)) * dim + a;
-        stg16(pp, u32x4{__float_as_uint(g[0]), __float_as_uint(g[1]), __float_as_uint(g[2]), __float_as_uint(g[3])});
-        stg16(pp + 4, u32x4{__float_as_uint(g[4]), __float_as_uint(g[5]), __float_as_uint(g[6]), __float_as_uint(g[7])});
-      }
+  int p0 = r0;
+  int key = -1, bag = 0, nxt;
+  {
+    const int cnt = rend - p0 < 64 ? rend - p0 : 64;
+    if (lane < cnt) {
+      key = skeys[p0 + lane];
+      bag = sbags[p0 + lane];
     }
+    nxt = p0 + cnt < n ? __builtin_amdgcn_readfirstlane(skeys[p0 + cnt]) : -1;
+  }
+  while (p0 < rend) {
+    const int cnt = rend - p0 < 64 ? rend - p0 : 64;
+    const bool valid = lane < cnt;
+    const int q0 = p0 + cnt;
+    int nkey = -1, nbag = 0, nnxt = -1;
+    if (q0 < rend) {
+      const int ncnt = rend - q0 < 64 ? rend - q0 : 64;
+      if (lane < ncnt) {
+        nkey = skeys[q0 + lane];
+        nbag = sbags[q0 + lane];
+      }
+      nnxt = q0 + ncnt < n ? __builtin_amdgcn_readfirstlane(skeys[q0 + ncnt]) : -1;
+    }
+    int kp = __shfl_up(key, 1, 64);
+    if (lane == 0) kp = prev_key;
+    int kn = __shfl_down(key, 1, 64);
+    if (lane == cnt - 1) kn = nxt;
+    const uint64_t smask = __ballot(valid && key != kp);   // run starts
+    const uint64_t emask = __ballot(valid && key != kn);   // run ends
+    // runs ending here are complete if a start lies at or before them in the range
+    const uint64_t ge_first = smask ? ~((smask & (~smask + 1)) - 1) : 0ull;
+    const uint64_t cmask = emask & (w.started ? ~0ull : ge_first);
+    const uint64_t pmask = emask | (q0 == rend ? (1ull << (cnt - 1)) : 0ull);  // piece ends
+    int xoff = 0;
+    float scl = 1.f;
+    if (valid) {
+      const int f = bag / B, b = bag - f * B;
+      xoff = (int)((uint32_t)(b * n_slots + first_slot + f) * (uint32_t)row_bytes);  // < 2^32 (host check)
+      if (MEAN) scl = 1.f / (float)(offsets[bag + 1] - offsets[bag]);
+    }
+    int s0 = 0;
+    for (; s0 + S <= cnt; s0 += S)
+      w.template group<false>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, E, grad_rows,
+                              part, wave, dim, lane_b, col, active, lr);
+    if (s0 < cnt)
+      w.template group<true>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, E, grad_rows,
+                             part, wave, dim, lane_b, col, active, lr);
+    w.started = w.started || smask != 0;
+    prev_key = __builtin_amdgcn_readlane(key, cnt - 1);
+    w.u_before += __popcll(smask);
+    last_nxt = nxt;
+    key = nkey;
+    bag = nbag;
+    nxt = nnxt;
+    p0 = q0;
+  }
+  if (lane == 0) {
+    const bool touch_end = rend < n && last_nxt == prev_key;
+    part_uid[wave] = touch_end ? w.u_before : -1;
+    if (touch_end && w.started) span_list[atomicAdd(span_count, 1)] = wave;
   }
 }
 
-// One wave per spanning run (persistent grid of 4-wave blocks): the run's
-// partials are summed in chunk order; lane l owns columns 2l, 2l+1.
+// One wave per run that crosses a range boundary: its partial sums (slot 1 of
+// the range where it starts, slot 0 of every later range it reaches) are
+// added in range order by S interleaved streams of dim/4 lanes each, then the
+// streams are combined in stream order; the total goes to the row gradient
+// and/or the SGD update.
 template <typename ET>
-__global__ __launch_bounds__(256) void chunk_fixup_kernel(
+__global__ __launch_bounds__(256) void seg_fixup_kernel(
     const int* __restrict__ span_list, const int* __restrict__ span_count,
     const int* __restrict__ part_uid, const int* __restrict__ seg_offsets,
     const int* __restrict__ unique_rows, const float* __restrict__ part, int dim,
     float* __restrict__ grad_rows, ET* __restrict__ E, float lr) {
   const int nspan = *span_count;
   const int lane = threadIdx.x & 63;
+  const int CL = dim / 4;  // 4-column groups (dim % 8 == 0, dim <= 256)
+  const int S = 64 / CL;   // streams
+  const int cq = lane % CL, s = lane / CL;
+  const bool act = s < S;
   const int wave = blockIdx.x * 4 + (threadIdx.x >> 6), nwaves = gridDim.x * 4;
   for (int i = wave; i < nspan; i += nwaves) {
     const int c0 = span_list[i];
     const int u = part_uid[c0];
     const int end = seg_offsets[u + 1];
-    const int ce = (end - 1) / CHUNK;
-    const int Q = ce - c0 + 1;  // pieces: slot 1 of c0, slot 0 of c0+1..ce
-    for (int a = 2 * lane; a < dim; a += 128) {
-      float s0 = 0.f, s1 = 0.f;
-      int q = 0;
-      for (; q + 8 <= Q; q += 8) {
-        float2 v[8];
+    const int Q = (end - 1) / RANGE - c0 + 1;
+    f32x4 a = {0.f, 0.f, 0.f, 0.f};
+    if (act) {
+      int q = s;
+      for (; q + 3 * S < Q; q += 4 * S) {
+        f32x4 v[4];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          const int qq = q + t;
-          const int64_t slot = (qq == 0) ? ((int64_t)c0 * 2 + 1) : ((int64_t)(c0 + qq) * 2);
-          v[t] = *reinterpret_cast<const float2*>(part + slot * dim + a);
+        for (int t = 0; t < 4; ++t) {
+          const int qq = q + t * S;
+          const int64_t slot = qq == 0 ? (int64_t)c0 * 2 + 1 : (int64_t)(c0 + qq) * 2;
+          v[t] = *reinterpret_cast<const f32x4*>(part + slot * dim + cq * 4);
         }
 #pragma unroll
-        for (int t = 0; t < 8; ++t) { s0 += v[t].x; s1 += v[t].y; }
+        for (int t = 0; t < 4; ++t) a += v[t];
       }
-      for (; q < Q; ++q) {
-        const int64_t slot = (q == 0) ? ((int64_t)c0 * 2 + 1) : ((int64_t)(c0 + q) * 2);
-        const float2 v = *reinterpret_cast<const float2*>(part + slot * dim + a);
-        s0 += v.x;
-        s1 += v.y;
+      for (; q < Q; q += S) {
+        const int64_t slot = q == 0 ? (int64_t)c0 * 2 + 1 : (int64_t)(c0 + q) * 2;
+        a += *reinterpret_cast<const f32x4*>(part + slot * dim + cq * 4);
       }
+    }
+    f32x4 t4 = {0.f, 0.f, 0.f, 0.f};
+    for (int ss = 0; ss < S; ++ss) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) t4[e] += __shfl(a[e], ss * CL + cq, 64);
+    }
+    if (s == 0) {
       const int row = unique_rows[u];
-      finalize_row<ET>(u, row, s0, a, dim, grad_rows, E, lr);
-      finalize_row<ET>(u, row, s1, a + 1, dim, grad_rows, E, lr);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = cq * 4 + e;
+        if (grad_rows) grad_rows[(int64_t)u * dim + c] = t4[e];
+        if (E) {
+          ET* p = E + (int64_t)row * dim + c;
+          st(p, ld(p) - lr * t4[e]);
+        }
+      }
     }
   }
 }
@@ -469,42 +567,48 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t embbag_bwd_workspace(int64_t nnz, int dim) {
   const int64_t n = nnz > 0 ? nnz : 1;
-  const int64_t chunks = cdiv(n, CHUNK);
+  const int64_t ranges = cdiv(n, RANGE);
   size_t s = 0;
-  s += 2 * align256((size_t)n * 4);                 // keys, vals (unsorted)
-  s += align256((size_t)n * 4);                     // sorted keys
+  s += 2 * align256((size_t)n * 4);                    // keys, vals (unsorted)
+  s += align256((size_t)n * 4);                        // sorted keys
   s += align256(radix_sort_workspace(n));
   s += align256((size_t)(cdiv(n, SEG_TILE) + 1) * 4);  // segment tile counts
-  s += align256((size_t)chunks * 4);                // chunk_uid
-  s += align256((size_t)chunks * 4);                // part_uid
-  s += align256((size_t)chunks * 4);                // span_list
-  s += align256(4);                                 // span_count
-  s += align256((size_t)chunks * 2 * dim * 4);      // partial rows
+  s += 3 * align256((size_t)ranges * 4);               // range_ubefore, part_uid, span_list
+  s += align256(4);                                    // span_count
+  s += align256((size_t)ranges * 2 * dim * 4);         // partial sums
   return s;
 }
 
 template <typename DT, typename ET>
 static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, const void* dX,
                                     int B, int n_slots, int first_slot, int dim,
-                                    const int32_t* offsets, int mean, const int* chunk_uid,
+                                    const int32_t* offsets, int mean, const int* range_ubefore,
                                     float* part, int* part_uid, int* span_list, int* span_count,
                                     const int* seg_offsets, const int* unique_rows,
                                     float* grad_rows, void* E, float lr, hipStream_t s) {
-  const int chunks = cdiv(n, CHUNK);
+  const int ranges = cdiv(n, RANGE);
   zero_int_kernel<<<1, 64, 0, s>>>(span_count, 1);
   LAT_LAUNCH_CHECK();
-  const size_t lds = (size_t)CHUNK * dim * sizeof(DT);
-  if (lds > 48 * 1024)
-    LAT_HIP_CHECK(hipFuncSetAttribute((const void*)chunk_reduce_kernel<DT, ET>,
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-  chunk_reduce_kernel<DT, ET><<<chunks, 256, lds, s>>>(
-      skeys, sbags, n, (const DT*)dX, B, n_slots, first_slot, dim, offsets, mean, chunk_uid,
-      part, part_uid, span_list, span_count, grad_rows, (ET*)E, lr);
+  const int row_bytes = dim * (int)sizeof(DT);
+  const int grid = cdiv(ranges, 4);
+#define LAT_SEG(BPLV, MV, FV)                                                               \
+  seg_reduce_kernel<DT, ET, BPLV, MV, FV><<<grid, 256, 0, s>>>(                            \
+      skeys, sbags, n, (const DT*)dX, B, n_slots, first_slot, dim, offsets, range_ubefore, \
+      part, part_uid, span_list, span_count, grad_rows, (ET*)E, lr)
+  if (row_bytes == 256) {
+    if (mean) LAT_SEG(4, true, true); else LAT_SEG(4, false, true);
+  } else if (row_bytes < 256) {
+    if (mean) LAT_SEG(4, true, false); else LAT_SEG(4, false, false);
+  } else if (row_bytes <= 512) {
+    if (mean) LAT_SEG(8, true, false); else LAT_SEG(8, false, false);
+  } else {
+    if (mean) LAT_SEG(16, true, false); else LAT_SEG(16, false, false);
+  }
+#undef LAT_SEG
   LAT_LAUNCH_CHECK();
-  const int fix_grid = chunks < 2048 ? chunks : 2048;
-  chunk_fixup_kernel<ET><<<fix_grid, 256, 0, s>>>(span_list, span_count, part_uid,
-                                                         seg_offsets, unique_rows, part, dim,
-                                                         grad_rows, (ET*)E, lr);
+  const int fix_grid = grid < 2048 ? grid : 2048;
+  seg_fixup_kernel<ET><<<fix_grid, 256, 0, s>>>(span_list, span_count, part_uid, seg_offsets,
+                                                unique_rows, part, dim, grad_rows, (ET*)E, lr);
   LAT_LAUNCH_CHECK();
   return hipSuccess;
 }
@@ -521,7 +625,12 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t
     return hipSuccess;
   }
   const int n = (int)nnz;
-  const int64_t chunks = cdiv(n, CHUNK);
+  const int64_t ranges = cdiv(n, RANGE);
+  if ((int64_t)B * n_slots * dim * (dxt == DT_BF16 ? 2 : 4) > (int64_t)UINT32_MAX) {
+    set_error("dX of %lld bytes: the sparse gradient addresses dX with 32-bit offsets",
+              (long long)B * n_slots * dim * (dxt == DT_BF16 ? 2 : 4));
+    return hipErrorInvalidValue;
+  }
   char* p = static_cast<char*>(ws);
   auto take = [&](size_t bytes) { char* q = p; p += align256(bytes); return q; };
   int* keys = (int*)take((size_t)n * 4);
@@ -529,11 +638,11 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t
   int* skeys = (int*)take((size_t)n * 4);
   void* sort_ws = take(radix_sort_workspace(n));
   int* tile_counts = (int*)take((size_t)(cdiv(n, SEG_TILE) + 1) * 4);
-  int* chunk_uid = (int*)take((size_t)chunks * 4);
-  int* part_uid = (int*)take((size_t)chunks * 4);
-  int* span_list = (int*)take((size_t)chunks * 4);
+  int* range_ubefore = (int*)take((size_t)ranges * 4);
+  int* part_uid = (int*)take((size_t)ranges * 4);
+  int* span_list = (int*)take((size_t)ranges * 4);
   int* span_count = (int*)take(4);
-  float* part = (float*)take((size_t)chunks * 2 * dim * 4);
+  float* part = (float*)take((size_t)ranges * 2 * dim * 4);
 
   const int64_t bags = (int64_t)F * B;
   if (keys_in && vals_in) {
@@ -551,12 +660,12 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t
   e = exclusive_scan_inplace_small(tile_counts, tiles, s);
   if (e != hipSuccess) return e;
   seg_write_kernel<<<tiles, SEG_THREADS, 0, s>>>(skeys, n, tile_counts, unique_rows, seg_offsets,
-                                                 num_unique, chunk_uid);
+                                                 num_unique, range_ubefore);
   LAT_LAUNCH_CHECK();
   void* Eupd = lr != 0.f ? E : nullptr;
 #define LAT_RED(DTT, ETT)                                                                     \
   return embbag_bwd_reduce<DTT, ETT>(skeys, sorted_bags, n, dX, B, n_slots, first_slot, dim,   \
-                                     offsets, mean, chunk_uid, part, part_uid, span_list,      \
+                                     offsets, mean, range_ubefore, part, part_uid, span_list,  \
                                      span_count, seg_offsets, unique_rows, grad_rows, Eupd, lr, s)
   if (dxt == DT_BF16 && et == DT_BF16) LAT_RED(bf16_t, bf16_t);
   if (dxt == DT_BF16 && et == DT_F32) LAT_RED(bf16_t, float);

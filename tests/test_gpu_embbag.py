@@ -143,3 +143,74 @@ def test_validate_batch():
     off[10] = off[11] + 1        # non-monotone
     ok, pos = api.lattice_validate_batch(w.E, w.row_base, off, w.indices, cfg.F, cfg.B)
     assert not ok and pos < 0
+
+
+def _structured_bags(rng, F, B, rows):
+    """Bags whose sorted occurrence list has runs of lengths around the
+    256-occurrence reduction ranges: runs of exactly 256 and 257, a run of
+    255 + 1, a run of 1000, then a mix of singles and short runs."""
+    runs = [256, 257, 255, 1, 1000, 3, 512, 1, 1, 2, 64, 65, 300]
+    idx_per_feature = [[] for _ in range(F)]
+    r = 0
+    for L in runs:
+        f = r % F
+        idx_per_feature[f].extend([(17 * r + 5) % rows] * L)
+        r += 1
+    for f in range(F):
+        idx_per_feature[f].extend(rng.integers(0, rows, size=int(rng.integers(50, 400))).tolist())
+        rng.shuffle(idx_per_feature[f])
+    offsets = [0]
+    indices = []
+    for f in range(F):
+        ids = idx_per_feature[f]
+        cuts = np.sort(rng.integers(0, len(ids) + 1, size=B - 1))
+        cuts = np.concatenate([[0], cuts, [len(ids)]])
+        for b in range(B):
+            indices.extend(ids[cuts[b]:cuts[b + 1]])
+            offsets.append(len(indices))
+    return np.array(offsets, np.int32), np.array(indices, np.int32)
+
+
+LANE_LAYOUTS = [(8, "bf16", "sum"), (16, "bf16", "mean"), (24, "bf16", "sum"), (32, "bf16", "sum"),
+                (40, "f32", "sum"), (128, "bf16", "mean"), (256, "f32", "sum"), (256, "bf16", "sum")]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("d,dtype,pool", LANE_LAYOUTS, ids=[f"d{d}-{t}-{p}" for d, t, p in LANE_LAYOUTS])
+@pytest.mark.parametrize("lr", [0.0, 0.25])
+def test_embbag_bwd_range_boundaries(d, dtype, pool, lr):
+    """Runs that end exactly at, one before and one after the 256-occurrence
+    reduction ranges, plus long runs crossing several, at every lane layout of
+    the reduction (16-byte lanes per row from 1 to 64, and widths that are not
+    a power of two)."""
+    from paper_2512_09200_amd import api
+    print(f"[embbag_bwd_ranges] d={d} {dtype} {pool} lr={lr}", flush=True)
+    F, B, rows = 3, 37, 700
+    rng = np.random.default_rng(20251209 + d)
+    offsets, idx = _structured_bags(rng, F, B, rows)
+    row_base = np.arange(F + 1, dtype=np.int64) * rows
+    sdt = synth.torch_dtype(dtype)
+    E = torch.from_numpy(synth.randn((F * rows, d), seed=d, stream=3, scale=0.1, dtype=dtype)).to(sdt).to(DEV)
+    dX_np = synth.randn((B, F + 1, d), seed=d, stream=4, dtype=dtype)
+    dX = torch.from_numpy(dX_np).to(sdt).to(DEV)
+    E0 = E.float().cpu().double().numpy()
+    out = api.lattice_embbag_bwd(E, torch.from_numpy(row_base).to(DEV), torch.from_numpy(offsets).to(DEV),
+                                 torch.from_numpy(idx).to(DEV), F, B, dX, 1, lr=lr, pool=pool)
+    torch.cuda.synchronize()
+    bk = oe.bookkeeping(row_base, offsets, idx, F, B)
+    uniq, G = oe.pool_backward(dX_np[:, 1:], row_base, offsets, idx, F, B, pool)
+    U = int(out["num_unique"].item())
+    assert U == uniq.size
+    np.testing.assert_array_equal(out["unique_rows"][:U].cpu().numpy(), bk["unique_rows"])
+    np.testing.assert_array_equal(out["seg_offsets"][:U + 1].cpu().numpy(), np.append(bk["seg_offsets"], idx.size))
+    np.testing.assert_array_equal(out["sorted_bags"][:idx.size].cpu().numpy(), bk["sorted_bags"])
+    t = 1e-5 if dtype == "f32" else 2e-2
+    assert_close("grad_rows", out["grad_rows"][:U], G, t)
+    E1 = E.float().cpu().double().numpy()
+    if lr:
+        assert_close("updated_rows", E1[uniq], oe.sgd_rows(E0[uniq], G, lr, rounding(dtype)), t)
+        untouched = np.ones(E0.shape[0], bool)
+        untouched[uniq] = False
+        assert np.array_equal(E1[untouched], E0[untouched]), "untouched rows changed"
+    else:
+        assert np.array_equal(E1, E0)
