@@ -2,12 +2,10 @@
 // deterministic row-coalesced gradient with an optional fused row-sparse SGD
 // update.
 //
-// Forward: one wavefront per bag.  A table row is split into 16-byte lane
-// chunks (a 256-byte bf16 row of d=128 is 16 lanes); the wave's 64 lanes form
-// G = 64/LP groups that each take every G-th entry of the bag, and every group
-// issues U row loads before using any of them, so each wave keeps G*U rows in
-// flight.  The groups' fp32 partial sums are combined with a fixed butterfly
-// (deterministic), and the first group writes the pooled row.
+// Forward: one wavefront per 16 consecutive bags, walking their lookups one
+// table row per step (each lane holds a 4..16-byte slice of the row), with
+// the rows of 8..32 lookups in flight at once; each bag is summed in position
+// order in fp32 and stored when it ends.
 //
 // Backward (no floating-point atomics):
 //   keys     : key = row_base[f] + index, value = bag id, per position
@@ -27,80 +25,185 @@
 
 namespace lat {
 
-// ---------------------------------------------------------------------------
-// forward
-// ---------------------------------------------------------------------------
-template <typename TT, typename XT, int LP>
-__global__ __launch_bounds__(256) void embbag_fwd_kernel(
-    const TT* __restrict__ E, const int64_t* __restrict__ row_base,
-    const int32_t* __restrict__ offsets, const int32_t* __restrict__ indices, int F, int B,
-    int dim, int mean, XT* __restrict__ X, int n_slots, int first_slot, int* __restrict__ keys,
-    int* __restrict__ vals) {
-  constexpr int VE = 16 / sizeof(TT);  // table elements per 16-byte lane chunk
-  constexpr int G = 64 / LP;           // row groups per wave
-  constexpr int U = (16 / G) > 0 ? (16 / G) : 1;  // loads in flight per group
-  const int lane = threadIdx.x & 63;
-  // each XCD pools a contiguous span of bags (whole tables): a table's hot
-  // rows are cached in one L2 instead of in all of them
-  // (the bag and its bounds are made scalar explicitly: uniform loop control)
-  const int64_t bag = __builtin_amdgcn_readfirstlane(xcd_block(blockIdx.x, gridDim.x) * 4 + (threadIdx.x >> 6));
-  if (bag >= (int64_t)F * B) return;
-  const int f = (int)(bag / B), b = (int)(bag % B);
-  const int g = lane / LP, sub = lane % LP;
-  const bool active = sub * VE < dim;
-  const int start = __builtin_amdgcn_readfirstlane(offsets[bag]);
-  const int end = __builtin_amdgcn_readfirstlane(offsets[bag + 1]);
-  const TT* Ef = E + row_base[f] * (int64_t)dim + sub * VE;
-
-  if (keys) {  // sort keys of the backward (global row) and values (bag id), coalesced
-    const int rb = (int)row_base[f];
-    for (int q = start + lane; q < end; q += 64) {
-      keys[q] = rb + indices[q];
-      vals[q] = (int)bag;
-    }
-  }
-  float acc[VE];
+// N consecutive elements of T held by one lane, as raw 32-bit words.
+template <typename T, int N>
+struct Frag {
+  static constexpr int NB = N * (int)sizeof(T);
+  static constexpr int W = NB >= 4 ? NB / 4 : 1;
+  uint32_t w[W];
+  __device__ inline void load(const T* p) {
+    if constexpr (NB == 2) {
+      w[0] = *reinterpret_cast<const uint16_t*>(p);
+    } else if constexpr (NB == 4) {
+      w[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else if constexpr (NB == 8) {
+      const uint2 v = *reinterpret_cast<const uint2*>(p);
+      w[0] = v.x;
+      w[1] = v.y;
+    } else {
 #pragma unroll
-  for (int i = 0; i < VE; ++i) acc[i] = 0.f;
-
-  for (int p = start + g; p < end; p += G * U) {
-    int idx[U];
-    u32x4 v[U];
+      for (int q = 0; q < W / 4; ++q) {
+        const u32x4 v = ldg16(reinterpret_cast<const uint32_t*>(p) + 4 * q);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int q = p + u * G;
-      idx[u] = (q < end) ? indices[q] : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (idx[u] >= 0 && active) v[u] = ldg16(Ef + (int64_t)idx[u] * dim);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (idx[u] >= 0 && active) {
-        float t[VE];
-        Vec16<TT>::unpack(v[u], t);
-#pragma unroll
-        for (int i = 0; i < VE; ++i) acc[i] += t[i];
+        for (int t = 0; t < 4; ++t) w[4 * q + t] = v[t];
       }
     }
   }
-#pragma unroll
-  for (int o = LP; o < 64; o <<= 1) {
-#pragma unroll
-    for (int i = 0; i < VE; ++i) acc[i] += __shfl_xor(acc[i], o, 64);
+  // element i as fp32
+  __device__ inline float get(int i) const {
+    if constexpr (sizeof(T) == 2)
+      return __uint_as_float((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16));
+    else
+      return __uint_as_float(w[i]);
   }
-  if (g == 0 && active) {
-    if (mean && end > start) {
-      const float len = (float)(end - start);
+  // stores v[0..N) rounded to T
+  __device__ static inline void store(T* p, const float* v) {
+    uint32_t o[W];
+    if constexpr (sizeof(T) == 2) {
+      if constexpr (N == 1) {
+        *reinterpret_cast<uint16_t*>(p) = f2bf(v[0]);
+        return;
+      } else {
 #pragma unroll
-      for (int i = 0; i < VE; ++i) acc[i] = acc[i] / len;
-    }
-    XT* out = X + ((int64_t)b * n_slots + first_slot + f) * dim + sub * VE;
-    if constexpr (sizeof(XT) == sizeof(TT)) {
-      stg16(out, Vec16<XT>::pack(acc));
+        for (int t = 0; t < W; ++t) o[t] = pack_bf2(v[2 * t], v[2 * t + 1]);
+      }
     } else {
 #pragma unroll
-      for (int i = 0; i < VE; ++i) st(out + i, acc[i]);
+      for (int t = 0; t < W; ++t) o[t] = __float_as_uint(v[t]);
+    }
+    if constexpr (NB == 4) {
+      *reinterpret_cast<uint32_t*>(p) = o[0];
+    } else if constexpr (NB == 8) {
+      *reinterpret_cast<uint2*>(p) = uint2{o[0], o[1]};
+    } else if constexpr (NB >= 16) {
+#pragma unroll
+      for (int q = 0; q < W / 4; ++q)
+        stg16(reinterpret_cast<uint32_t*>(p) + 4 * q, u32x4{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]});
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// forward
+// ---------------------------------------------------------------------------
+constexpr int FWD_BAGS = 16;  // bags per wave in the forward
+
+// S consecutive lookups of a chunk starting at chunk row s0 (all inside the
+// chunk when CHECK is false): their table rows are loaded together, then
+// added to the running sum in order; a bag end stores and resets the sum.
+template <typename TT, typename XT, int EPL, int S, bool MEAN, bool FULL, bool CHECK>
+__device__ inline void fwd_group(int s0, int cnt, uint64_t emask, int grow, int xrow, float inv_len,
+                                 const char* Eb, int64_t row_bytes, int lane_b, XT* X, int dim,
+                                 int col, bool active, float* acc) {
+  Frag<TT, EPL> xf[S];
+#pragma unroll
+  for (int i = 0; i < S; ++i) {
+    const int r = s0 + i;
+    if (CHECK && r >= cnt) break;
+    const char* rowp = Eb + (int64_t)__builtin_amdgcn_readlane(grow, r) * row_bytes;
+    if (FULL || active) xf[i].load(reinterpret_cast<const TT*>(rowp + lane_b));
+  }
+#pragma unroll
+  for (int i = 0; i < S; ++i) {
+    const int r = s0 + i;
+    if (CHECK && r >= cnt) break;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[e] += xf[i].get(e);
+    if ((emask >> r) & 1) {
+      if (MEAN) {
+        const float il = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(inv_len), r));
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] *= il;
+      }
+      XT* out = X + (int64_t)__builtin_amdgcn_readlane(xrow, r) * dim + col;
+      if (FULL || active) Frag<XT, EPL>::store(out, acc);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+    }
+  }
+}
+
+// One wave per FWD_BAGS consecutive bags (feature-major, so a wave's bags are
+// consecutive samples of one or two features).  The wave walks their lookups
+// in position order one table row per step: lane l holds bytes
+// [l*BPL, (l+1)*BPL) of the row, so bag ends are the same for every lane and
+// the pooled sum is one fp32 accumulator per column, stored and reset at each
+// bag end.  Per chunk of 64 positions: indices (one per lane), their bags, the
+// global rows and the destination slots; then in groups of S positions the S
+// table rows are loaded together and summed in order.  Empty bags are written
+// as zeros.  With keys != NULL the backward's sort keys (global row) and
+// values (bag id) are written per position as well.
+template <typename TT, typename XT, int BPL, bool MEAN, bool FULL>
+__global__ __launch_bounds__(256) void embbag_fwd_kernel(
+    const TT* __restrict__ E, const int64_t* __restrict__ row_base,
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ indices, int F, int B,
+    int dim, XT* __restrict__ X, int n_slots, int first_slot, int* __restrict__ keys,
+    int* __restrict__ vals) {
+  constexpr int EPL = BPL / (int)sizeof(TT);
+  constexpr int S = BPL == 4 ? 32 : (BPL == 8 ? 16 : 8);
+  const int lane = threadIdx.x & 63;
+  // Each XCD pools a contiguous span of bags (whole tables), so a table's hot
+  // rows are cached in one L2.  Wave-uniform values are scalar: uniform
+  // control flow throughout.
+  const int wave = __builtin_amdgcn_readfirstlane(xcd_block(blockIdx.x, gridDim.x) * 4 + (threadIdx.x >> 6));
+  const int nbags = F * B;
+  const int b0 = wave * FWD_BAGS;
+  if (b0 >= nbags) return;
+  const int nb = nbags - b0 < FWD_BAGS ? nbags - b0 : FWD_BAGS;
+  // lane k <= nb holds offsets[b0 + k]
+  const int offv = lane <= nb ? offsets[b0 + lane] : 0;
+  const int p_begin = __builtin_amdgcn_readlane(offv, 0);
+  const int p_end = __builtin_amdgcn_readlane(offv, nb);
+  const int col = lane * EPL;
+  const bool active = col < dim;
+  const int lane_b = lane * BPL;
+  const int64_t row_bytes = (int64_t)dim * (int64_t)sizeof(TT);
+  const char* Eb = reinterpret_cast<const char*>(E);
+
+  float acc[EPL];
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+  for (int p0 = p_begin; p0 < p_end; p0 += 64) {
+    const int cnt = p_end - p0 < 64 ? p_end - p0 : 64;
+    const int p = p0 + lane;
+    const bool valid = lane < cnt;
+    // bag (index k within the wave's bags) of this lane's position
+    int k = 0;
+    for (int q = 1; q < nb; ++q) k += p >= __builtin_amdgcn_readlane(offv, q) ? 1 : 0;
+    // (shuffles stay outside divergent code: a shuffle from a lane that is
+    // switched off reads nothing)
+    const int next_off = __shfl(offv, k + 1, 64);
+    const int this_off = __shfl(offv, k, 64);
+    const uint64_t emask = __ballot(valid && p + 1 == next_off);  // last position of its bag
+    const int bag = b0 + k;
+    const int f = bag / B, b = bag - f * B;
+    int grow = 0, xrow = 0;
+    float inv_len = 1.f;
+    if (valid) {
+      grow = (int)(row_base[f] + indices[p]);
+      xrow = b * n_slots + first_slot + f;
+      if (MEAN) inv_len = 1.f / (float)(next_off - this_off);
+      if (keys) {
+        keys[p] = grow;
+        vals[p] = bag;
+      }
+    }
+    int s0 = 0;
+    for (; s0 + S <= cnt; s0 += S)
+      fwd_group<TT, XT, EPL, S, MEAN, FULL, false>(s0, cnt, emask, grow, xrow, inv_len, Eb, row_bytes,
+                                                    lane_b, X, dim, col, active, acc);
+    if (s0 < cnt)
+      fwd_group<TT, XT, EPL, S, MEAN, FULL, true>(s0, cnt, emask, grow, xrow, inv_len, Eb, row_bytes,
+                                                   lane_b, X, dim, col, active, acc);
+  }
+  // empty bags pool to zero
+  for (int q = 0; q < nb; ++q) {
+    if (__builtin_amdgcn_readlane(offv, q) == __builtin_amdgcn_readlane(offv, q + 1)) {
+      const int bag = b0 + q, f = bag / B, b = bag - f * B;
+      float z[EPL];
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) z[e] = 0.f;
+      if (FULL || active) Frag<XT, EPL>::store(X + ((int64_t)b * n_slots + first_slot + f) * dim + col, z);
     }
   }
 }
@@ -112,18 +215,20 @@ static hipError_t embbag_fwd_t(const void* E, int dim, const int64_t* row_base,
                                int* vals, hipStream_t s) {
   const int64_t bags = (int64_t)F * B;
   if (bags == 0) return hipSuccess;
-  const int lanes = (int)((dim * sizeof(TT) + 15) / 16);
-  const int grid = cdiv(bags, 4);
-#define LAT_FWD(LPV)                                                                       \
-  embbag_fwd_kernel<TT, XT, LPV><<<grid, 256, 0, s>>>(                                    \
-      (const TT*)E, row_base, offsets, indices, F, B, dim, mean, (XT*)X, n_slots, first_slot, keys, vals)
-  if (lanes <= 1) LAT_FWD(1);
-  else if (lanes <= 2) LAT_FWD(2);
-  else if (lanes <= 4) LAT_FWD(4);
-  else if (lanes <= 8) LAT_FWD(8);
-  else if (lanes <= 16) LAT_FWD(16);
-  else if (lanes <= 32) LAT_FWD(32);
-  else LAT_FWD(64);
+  const int row_bytes = dim * (int)sizeof(TT);
+  const int grid = cdiv(cdiv(bags, FWD_BAGS), 4);
+#define LAT_FWD(BPLV, MV, FV)                                                              \
+  embbag_fwd_kernel<TT, XT, BPLV, MV, FV><<<grid, 256, 0, s>>>(                           \
+      (const TT*)E, row_base, offsets, indices, F, B, dim, (XT*)X, n_slots, first_slot, keys, vals)
+  if (row_bytes == 256) {
+    if (mean) LAT_FWD(4, true, true); else LAT_FWD(4, false, true);
+  } else if (row_bytes < 256) {
+    if (mean) LAT_FWD(4, true, false); else LAT_FWD(4, false, false);
+  } else if (row_bytes <= 512) {
+    if (mean) LAT_FWD(8, true, false); else LAT_FWD(8, false, false);
+  } else {
+    if (mean) LAT_FWD(16, true, false); else LAT_FWD(16, false, false);
+  }
 #undef LAT_FWD
   LAT_LAUNCH_CHECK();
   return hipSuccess;
@@ -261,64 +366,6 @@ __global__ void set_empty_kernel(int* num_unique, int* seg_offsets) {
 // ---------------------------------------------------------------------------
 // backward: segmented reduction over the sorted occurrences (+ fused SGD)
 // ---------------------------------------------------------------------------
-// N consecutive elements of T held by one lane, as raw 32-bit words.
-template <typename T, int N>
-struct Frag {
-  static constexpr int NB = N * (int)sizeof(T);
-  static constexpr int W = NB >= 4 ? NB / 4 : 1;
-  uint32_t w[W];
-  __device__ inline void load(const T* p) {
-    if constexpr (NB == 2) {
-      w[0] = *reinterpret_cast<const uint16_t*>(p);
-    } else if constexpr (NB == 4) {
-      w[0] = *reinterpret_cast<const uint32_t*>(p);
-    } else if constexpr (NB == 8) {
-      const uint2 v = *reinterpret_cast<const uint2*>(p);
-      w[0] = v.x;
-      w[1] = v.y;
-    } else {
-#pragma unroll
-      for (int q = 0; q < W / 4; ++q) {
-        const u32x4 v = ldg16(reinterpret_cast<const uint32_t*>(p) + 4 * q);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) w[4 * q + t] = v[t];
-      }
-    }
-  }
-  // element i as fp32
-  __device__ inline float get(int i) const {
-    if constexpr (sizeof(T) == 2)
-      return __uint_as_float((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16));
-    else
-      return __uint_as_float(w[i]);
-  }
-  // stores v[0..N) rounded to T
-  __device__ static inline void store(T* p, const float* v) {
-    uint32_t o[W];
-    if constexpr (sizeof(T) == 2) {
-      if constexpr (N == 1) {
-        *reinterpret_cast<uint16_t*>(p) = f2bf(v[0]);
-        return;
-      } else {
-#pragma unroll
-        for (int t = 0; t < W; ++t) o[t] = pack_bf2(v[2 * t], v[2 * t + 1]);
-      }
-    } else {
-#pragma unroll
-      for (int t = 0; t < W; ++t) o[t] = __float_as_uint(v[t]);
-    }
-    if constexpr (NB == 4) {
-      *reinterpret_cast<uint32_t*>(p) = o[0];
-    } else if constexpr (NB == 8) {
-      *reinterpret_cast<uint2*>(p) = uint2{o[0], o[1]};
-    } else if constexpr (NB >= 16) {
-#pragma unroll
-      for (int q = 0; q < W / 4; ++q)
-        stg16(reinterpret_cast<uint32_t*>(p) + 4 * q, u32x4{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]});
-    }
-  }
-};
-
 // One wave per RANGE consecutive sorted occurrences.  The wave walks the
 // occurrences one dX row per step: lane l holds bytes [l*BPL, (l+1)*BPL) of
 // the row, so run starts and ends are the same for every lane and the
