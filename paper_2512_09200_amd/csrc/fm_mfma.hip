@@ -3,16 +3,18 @@
 // d in {64, 128}, rank k in {32, 64}.
 //
 // Each block of 8 waves loops over samples.  A sample's X [n, d] is read once
-// with coalesced 4-byte loads (8 rows x 2 columns per thread), transposed in
-// registers, and staged in LDS twice -- row-major X[j][a] and transposed
-// X^T[a][j] -- so every MFMA operand is read as k-contiguous 16-byte
-// fragments.  Storage rounding matches the rest of the step: P = X^T W and
+// with coalesced 4-byte loads (8 rows x 2 columns per thread) into registers
+// one sample ahead (the next sample's loads are in flight while the current
+// one is computed), transposed in registers, and staged in LDS twice --
+// row-major X[j][a] and transposed X^T[a][j] -- so every MFMA operand is read
+// as k-contiguous 16-byte fragments.  Storage rounding matches the rest of the step: P = X^T W and
 // dP = X^T G are rounded to bf16 before use, O and dX are stored in bf16.
 //   forward : P = X^T W (contraction over j), O = X P (over a)
-//   backward: P, dP share the X^T fragments; dX = [G | W] [P | dP]^T is one
-//             contraction over 2k; dW += X dP accumulates in the waves'
-//             registers across the block's samples (fixed order), and the
-//             per-block partials are summed in block order afterwards.
+//   backward: P, dP and dP^T (= G^T X, the dW operand) share the staged
+//             fragments; dX = [G | W] [P | dP]^T is one contraction over 2k;
+//             dW += X dP accumulates in the waves' registers across the
+//             block's samples (fixed order), and the per-block partials are
+//             summed in block order afterwards.
 #include "common.h"
 #include "kernels.h"
 
@@ -43,29 +45,45 @@ __device__ inline int frag_row(int r) { return 8 * (r >> 2) + 4 * ((threadIdx.x 
 // Stage a [rows][cols] bf16 matrix (row stride gld, rows >= nrows read as 0)
 // into LDS twice: R[j][c] (stride ldr) and T[c][j] (stride ldt).  Items are
 // (group of 8 rows, pair of columns); RP = padded row count (multiple of 8).
-template <int RP, int COLS>
-__device__ inline void stage_both(const bf16_t* __restrict__ g, int64_t gld, int nrows,
-                                  bf16_t* R, int ldr, bf16_t* T, int ldt) {
-  constexpr int ITEMS = (RP / 8) * (COLS / 2);
-  for (int it = threadIdx.x; it < ITEMS; it += blockDim.x) {
-    const int grp = it / (COLS / 2), pr = it % (COLS / 2);
-    const int j0 = grp * 8, c = pr * 2;
-    uint32_t v[8];
+// load() fetches this thread's items into registers (so the next sample can
+// be in flight while the current one is computed), store() writes them.
+template <int RP, int COLS, int THREADS>
+struct Stager {
+  static constexpr int ITEMS = (RP / 8) * (COLS / 2);
+  static constexpr int PER = (ITEMS + THREADS - 1) / THREADS;
+  uint32_t v[PER][8];
+  __device__ inline void load(const bf16_t* __restrict__ g, int64_t gld, int nrows) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      v[i] = (j0 + i < nrows) ? *reinterpret_cast<const uint32_t*>(g + (int64_t)(j0 + i) * gld + c) : 0u;
+    for (int q = 0; q < PER; ++q) {
+      const int it = threadIdx.x + q * THREADS;
+      if (it < ITEMS) {
+        const int j0 = (it / (COLS / 2)) * 8, c = (it % (COLS / 2)) * 2;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint32_t*>(R + (j0 + i) * ldr + c) = v[i];
-    u32x4 lo, hi;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      lo[i] = __builtin_amdgcn_perm(v[2 * i + 1], v[2 * i], 0x05040100u);
-      hi[i] = __builtin_amdgcn_perm(v[2 * i + 1], v[2 * i], 0x07060302u);
+        for (int i = 0; i < 8; ++i)
+          v[q][i] = (j0 + i < nrows) ? *reinterpret_cast<const uint32_t*>(g + (int64_t)(j0 + i) * gld + c) : 0u;
+      }
     }
-    *reinterpret_cast<u32x4*>(T + c * ldt + j0) = lo;
-    *reinterpret_cast<u32x4*>(T + (c + 1) * ldt + j0) = hi;
   }
-}
+  __device__ inline void store(bf16_t* R, int ldr, bf16_t* T, int ldt) const {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int it = threadIdx.x + q * THREADS;
+      if (it < ITEMS) {
+        const int j0 = (it / (COLS / 2)) * 8, c = (it % (COLS / 2)) * 2;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) *reinterpret_cast<uint32_t*>(R + (j0 + i) * ldr + c) = v[q][i];
+        u32x4 lo, hi;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          lo[i] = __builtin_amdgcn_perm(v[q][2 * i + 1], v[q][2 * i], 0x05040100u);
+          hi[i] = __builtin_amdgcn_perm(v[q][2 * i + 1], v[q][2 * i], 0x07060302u);
+        }
+        *reinterpret_cast<u32x4*>(T + c * ldt + j0) = lo;
+        *reinterpret_cast<u32x4*>(T + (c + 1) * ldt + j0) = hi;
+      }
+    }
+  }
+};
 
 template <int NP, int D, int K>
 __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restrict__ X,
@@ -79,12 +97,19 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
   __shared__ __attribute__((aligned(16))) bf16_t WR[NP * LR];
   __shared__ __attribute__((aligned(16))) bf16_t WT[K * LT];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  stage_both<NP, K>(W, K, n, WR, LR, WT, LT);
+  {
+    Stager<NP, K, 512> sw;
+    sw.load(W, K, n);
+    sw.store(WR, LR, WT, LT);
+  }
   const int off = emit0 ? D : 0;
+  Stager<NP, D, 512> sx;
+  if (blockIdx.x < B) sx.load(X + (int64_t)blockIdx.x * n * D, D, n);
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
-    const bf16_t* Xb = X + (int64_t)b * n * D;
-    stage_both<NP, D>(Xb, D, n, Xs, LX, XT, LT);
+    sx.store(Xs, LX, XT, LT);
     __syncthreads();
+    // the next sample's X is in flight while this one is computed
+    if (b + (int)gridDim.x < B) sx.load(X + (int64_t)(b + gridDim.x) * n * D, D, n);
     // P[a][c] = sum_j X^T[a][j] W^T[c][j]; tile (ta, tc) per wave
     constexpr int PT_TILES = (D / 32) * (K / 32);
     for (int t = w; t < PT_TILES; t += 8) {
@@ -125,44 +150,61 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
     const bf16_t* __restrict__ dout, int64_t dstride, int emit0, const float* __restrict__ addend,
     bf16_t* __restrict__ dX, float* __restrict__ dX_f32, float* __restrict__ dw_part) {
   constexpr int LX = D + 8, LT = NP + 8, LG = 2 * K + 8, LPD = 2 * K + 8, LDT = D + 8;
-  constexpr int XT_SIZE = (D * LT > K * LDT) ? D * LT : K * LDT;
   __shared__ __attribute__((aligned(16))) bf16_t Xs[NP * LX];
-  __shared__ __attribute__((aligned(16))) bf16_t XT[XT_SIZE];   // later dP^T [K][LDT]
+  __shared__ __attribute__((aligned(16))) bf16_t XT[D * LT];
+  __shared__ __attribute__((aligned(16))) bf16_t PT_[K * LDT];  // dP^T [K][LDT]
   __shared__ __attribute__((aligned(16))) bf16_t GW[NP * LG];   // [j][ G (K) | W (K) ]
   __shared__ __attribute__((aligned(16))) bf16_t GT[K * LT];
   __shared__ __attribute__((aligned(16))) bf16_t WT[K * LT];
   __shared__ __attribute__((aligned(16))) bf16_t PD[D * LPD];   // [a][ P (K) | dP (K) ]
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  stage_both<NP, K>(W, K, n, GW + K, LG, WT, LT);
+  {
+    Stager<NP, K, 512> sw;
+    sw.load(W, K, n);
+    sw.store(GW + K, LG, WT, LT);
+  }
   constexpr int DW_TILES = (NP / 32) * (K / 32);
   f32x16 dw[(DW_TILES + 7) / 8];
 #pragma unroll
   for (int i = 0; i < (DW_TILES + 7) / 8; ++i) zero16(dw[i]);
   const int off = emit0 ? D : 0;
+  Stager<NP, D, 512> sx;
+  Stager<NP, K, 512> sg;
+  if (blockIdx.x < B) {
+    sx.load(X + (int64_t)blockIdx.x * n * D, D, n);
+    sg.load(dout + (int64_t)blockIdx.x * dstride + off, K, n);
+  }
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
-    const bf16_t* Xb = X + (int64_t)b * n * D;
     const bf16_t* gb = dout + (int64_t)b * dstride;
-    stage_both<NP, D>(Xb, D, n, Xs, LX, XT, LT);
-    stage_both<NP, K>(gb + off, K, n, GW, LG, GT, LT);
+    sx.store(Xs, LX, XT, LT);
+    sg.store(GW, LG, GT, LT);
     __syncthreads();
-    // P = X^T W and dP = X^T G, both rounded to bf16, into PD
+    // the next sample's X and G are in flight while this one is computed
+    if (b + (int)gridDim.x < B) {
+      sx.load(X + (int64_t)(b + gridDim.x) * n * D, D, n);
+      sg.load(dout + (int64_t)(b + gridDim.x) * dstride + off, K, n);
+    }
+    // P = X^T W and dP = X^T G into PD[a][P | dP], and dP^T[c][a] = G^T X
+    // into DT (the dW operand), all rounded to bf16
     constexpr int P_TILES = (D / 32) * (K / 32);
-    for (int t = w; t < 2 * P_TILES; t += 8) {
+    bf16_t* DT = PT_;
+    for (int t = w; t < 3 * P_TILES; t += 8) {
       const int which = t / P_TILES, tt = t % P_TILES;
-      const int ta = tt / (K / 32), tc = tt % (K / 32);
       f32x16 acc;
       zero16(acc);
-      mfma_tile<NP>(acc, XT + ta * 32 * LT, LT, (which ? GT : WT) + tc * 32 * LT, LT);
-      const int c = tc * 32 + (lane & 31) + which * K;
+      if (which < 2) {
+        const int ta = tt / (K / 32), tc = tt % (K / 32);
+        mfma_tile<NP>(acc, XT + ta * 32 * LT, LT, (which ? GT : WT) + tc * 32 * LT, LT);
+        const int c = tc * 32 + (lane & 31) + which * K;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) PD[(ta * 32 + frag_row(r)) * LPD + c] = f2bf(acc[r]);
-    }
-    __syncthreads();
-    // dP^T into the X^T buffer
-    bf16_t* DT = XT;
-    for (int e = threadIdx.x; e < K * D; e += blockDim.x) {
-      const int c = e / D, a = e % D;
-      DT[c * LDT + a] = PD[a * LPD + K + c];
+        for (int r = 0; r < 16; ++r) PD[(ta * 32 + frag_row(r)) * LPD + c] = f2bf(acc[r]);
+      } else {
+        const int tc = tt / (D / 32), ta = tt % (D / 32);
+        mfma_tile<NP>(acc, GT + tc * 32 * LT, LT, XT + ta * 32 * LT, LT);
+        const int a = ta * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) DT[(tc * 32 + frag_row(r)) * LDT + a] = f2bf(acc[r]);
+      }
     }
     __syncthreads();
     // dX[j][a] = sum_kk GW[j][kk] PD[a][kk]  (+ addend, + slot-0 gradient)

@@ -5,25 +5,34 @@
 // weight-gradient (dY^T X) products all map onto one kernel family without
 // materialised transposes.
 //
-// bf16 path (gfx950 MFMA): block tile 128x128, K step 32, 256 threads as a
+// bf16 path (gfx950 MFMA): block tile 128x128, K step 64, 256 threads as a
 // 2x2 grid of waves each owning a 64x64 sub-tile = 2x2 fragments of
 // v_mfma_f32_32x32x16_bf16.  Operands are staged through LDS in [row][k]
-// layout (k contiguous, rows padded to 40 elements so 16-byte fragment reads
-// of 16 lanes hit 64 distinct banks).  A K-contiguous operand is copied with
-// 16-byte loads; an M-contiguous operand is read as 2-element pairs along M
-// (coalesced across the wave) and transposed in registers before the LDS
-// write.  Global loads of step k+1 overlap the MFMAs of step k (double
-// buffer).  Split-K writes fp32 partials that a second kernel sums in a fixed
-// order, so results are deterministic.
+// layout (k contiguous, rows padded to 72 elements).  A K-contiguous operand
+// is copied with 16-byte loads; an M-contiguous operand is read with 16-byte
+// loads along M (8 rows x 4 k per thread) and transposed in registers before
+// the LDS write.  Global loads run two K steps ahead of the MFMAs (two
+// register stages, two LDS stages).  Tiles are numbered so that each XCD works
+// through whole row panels of A (one L2 keeps the panel while the XCD sweeps
+// the columns).  The finished tile is staged through LDS as fp32 so that the
+// epilogue reads and writes rows with 16-byte vectors.  Split-K writes fp32
+// partials that a second kernel sums in a fixed order, so results are
+// deterministic.
 //
-// Epilogue: + bias[n], ReLU, or multiply by (mask[m, n] > 0) (the ReLU
-// derivative read from a stored activation), then round to the output dtype.
+// Epilogue: + bias[n], + addend[m, n], + C (accumulate), ReLU, or multiply by
+// (mask[m, n] > 0) (the ReLU derivative read from a stored activation), then
+// round to the output dtype.
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace lat {
 
-constexpr int GBM = 128, GBN = 128, GBK = 32, GPAD = 8, GLD = GBK + GPAD;
+constexpr int GBM = 128, GBN = 128, GBK = 64, GPAD = 8, GLD = GBK + GPAD;
+constexpr int CLD = GBN + 4;  // fp32 row stride of the staged C tile
+constexpr size_t GEMM_LDS = (size_t)2 * (GBM + GBN) * GLD * sizeof(uint16_t);  // 73,728 B
+static_assert((size_t)GBM * CLD * sizeof(float) <= GEMM_LDS, "C staging must fit the operand stages");
 
 struct Epi {
   const float* bias;    // [N] or null
@@ -51,6 +60,59 @@ __device__ inline void epi_store(CT* C, int64_t ldc, int row, int col, float v, 
   st(C + (int64_t)row * ldc + col, v);
 }
 
+__device__ inline void ld8f(const float* p, float* v) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[i] = a[i];
+    v[4 + i] = b[i];
+  }
+}
+
+// Epilogue of 8 consecutive columns of one row with 16-byte vectors (the
+// caller guarantees alignment and col + 8 <= N).
+template <typename CT>
+__device__ inline void epi_store8(CT* C, int64_t ldc, int row, int col, float* v, const Epi& e,
+                                  int64_t bz) {
+  float t[8];
+  if (e.bias) {
+    ld8f(e.bias + col, t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += t[i];
+  }
+  if (e.addend) {
+    ld8f(e.addend + bz * e.s_add + (int64_t)row * e.ld_add + col, t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += t[i];
+  }
+  CT* c = C + (int64_t)row * ldc + col;
+  if (e.accumulate) {  // fp32 C only
+    ld8f(reinterpret_cast<const float*>(c), t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += t[i];
+  }
+  if (e.relu) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = v[i] > 0.f ? v[i] : 0.f;
+  }
+  if (e.mask) {
+    const int64_t mi = bz * e.s_mask + (int64_t)row * e.ldm + col;
+    if (e.mask_dt == DT_BF16) {
+      Vec16<bf16_t>::unpack(ldg16(reinterpret_cast<const bf16_t*>(e.mask) + mi), t);
+    } else {
+      ld8f(reinterpret_cast<const float*>(e.mask) + mi, t);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = t[i] > 0.f ? v[i] : 0.f;
+  }
+  if constexpr (sizeof(CT) == 2) {
+    stg16(c, Vec16<bf16_t>::pack(v));
+  } else {
+    stg16(c, Vec16<float>::pack(v));
+    stg16(c + 4, Vec16<float>::pack(v + 4));
+  }
+}
+
 // An operand: element (r, k) of A(m,k) / B(n,k).  K-contiguous: p[r*ld + koff(k)];
 // MN-contiguous: p[koff(k)*... + r] with koff(k) counted in rows of length ld.
 // K segmentation splits k into (k / kseg, k % kseg): the segment index moves by
@@ -69,74 +131,77 @@ __device__ inline int64_t koff(const Opnd& o, int k) {
 }
 
 // --- operand tile loaders: fill S[rows][GLD] (k contiguous) for rows r0.., k k0.. ---
-// K-contiguous, 16-byte vectors: 128 rows x 32 k = 4 vectors per row, 2 per thread.
+// K-contiguous, 16-byte vectors: 128 rows x 64 k = 8 vectors per row, 4 per thread.
 struct LoadK {
-  u32x4 r[2];
-  __device__ void load(const Opnd& o, int R, int K, int r0, int k0) {
+  u32x4 r[4];
+  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 4; ++i) {
       const int v = threadIdx.x + i * 256;
-      const int rr = v >> 2, kc = (v & 3) * 8;
+      const int rr = v >> 3, kc = (v & 7) * 8;
       const int gr = r0 + rr, gk = k0 + kc;
       if (gr < R && gk < K) r[i] = ldg16(o.p + (int64_t)gr * o.ld + koff<false>(o, gk));
       else r[i] = u32x4{0, 0, 0, 0};
     }
   }
-  __device__ void store(bf16_t* S) {
+  __device__ inline void store(bf16_t* S) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 4; ++i) {
       const int v = threadIdx.x + i * 256;
-      *reinterpret_cast<u32x4*>(S + (v >> 2) * GLD + (v & 3) * 8) = r[i];
+      *reinterpret_cast<u32x4*>(S + (v >> 3) * GLD + (v & 7) * 8) = r[i];
     }
   }
 };
-// MN-contiguous: thread owns rows (2p, 2p+1) and 8 consecutive k (wave w -> k 8w..8w+7),
-// read as 4-byte row pairs (coalesced across the wave) and transposed in registers.
+// MN-contiguous, 16-byte vectors along M: a thread holds 8 consecutive rows x
+// 4 consecutive k (four 16-byte loads), transposed in registers to 4-k pieces
+// per row (8-byte LDS writes).  Wave w, lane l: row group mg = 4w + l/16,
+// k group kg = l%16, so one load instruction reads 64 contiguous bytes of
+// each of 16 k-rows, and the 16 lanes of a group write one row's 128 bytes.
 struct LoadMN {
-  uint32_t r[8];
-  __device__ void load(const Opnd& o, int R, int K, int r0, int k0) {
+  u32x4 r[4];
+  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int gr = r0 + 2 * lane;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int gk = k0 + w * 8 + i;
-      if (gk < K && gr < R) r[i] = *reinterpret_cast<const uint32_t*>(o.p + koff<true>(o, gk) + gr);
-      else r[i] = 0u;
-    }
-  }
-  __device__ void store(bf16_t* S) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    u32x4 lo, hi;
+    const int gr = r0 + (4 * w + (lane >> 4)) * 8, kb = k0 + (lane & 15) * 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      // r[k] = (row 2p at k) | (row 2p+1 at k) << 16
-      lo[i] = __builtin_amdgcn_perm(r[2 * i + 1], r[2 * i], 0x05040100u);  // low halves
-      hi[i] = __builtin_amdgcn_perm(r[2 * i + 1], r[2 * i], 0x07060302u);  // high halves
+      const int gk = kb + i;
+      if (gk < K && gr < R) r[i] = ldg16(o.p + koff<true>(o, gk) + gr);
+      else r[i] = u32x4{0, 0, 0, 0};
     }
-    *reinterpret_cast<u32x4*>(S + (2 * lane) * GLD + w * 8) = lo;
-    *reinterpret_cast<u32x4*>(S + (2 * lane + 1) * GLD + w * 8) = hi;
+  }
+  __device__ inline void store(bf16_t* S) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    bf16_t* s = S + ((4 * w + (lane >> 4)) * 8) * GLD + (lane & 15) * 4;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      // row j of the group: (k0, k1, k2, k3) = half (j & 1) of word j/2 of r[0..3]
+      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+      const uint32_t lo = __builtin_amdgcn_perm(r[1][j >> 1], r[0][j >> 1], sel);
+      const uint32_t hi = __builtin_amdgcn_perm(r[3][j >> 1], r[2][j >> 1], sel);
+      *reinterpret_cast<uint2*>(s + j * GLD) = uint2{lo, hi};
+    }
   }
 };
 // Generic element loader (any alignment / transposition).
 template <bool MN>
 struct LoadElem {
-  bf16_t r[16];
-  __device__ void load(const Opnd& o, int R, int K, int r0, int k0) {
+  bf16_t r[32];
+  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < 32; ++i) {
       const int e = threadIdx.x + i * 256;
-      const int rr = e >> 5, kk = e & 31;
+      const int rr = e >> 6, kk = e & 63;
       const int gr = r0 + rr, gk = k0 + kk;
       bf16_t v = 0;
       if (gr < R && gk < K) v = MN ? o.p[koff<true>(o, gk) + gr] : o.p[(int64_t)gr * o.ld + koff<false>(o, gk)];
       r[i] = v;
     }
   }
-  __device__ void store(bf16_t* S) {
+  __device__ inline void store(bf16_t* S) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < 32; ++i) {
       const int e = threadIdx.x + i * 256;
-      S[(e >> 5) * GLD + (e & 31)] = r[i];
+      S[(e >> 6) * GLD + (e & 63)] = r[i];
     }
   }
 };
@@ -145,16 +210,43 @@ template <> struct LoaderSel<false, true> { using T = LoadK; };
 template <> struct LoaderSel<true, true> { using T = LoadMN; };
 template <bool MN> struct LoaderSel<MN, false> { using T = LoadElem<MN>; };
 
-// blockIdx.z: split index (split-K) or batch index (batched; never both)
+// 64 k of MFMAs on the staged tiles: each wave 2x2 fragments of 32x32.
+__device__ inline void mma_k64(const bf16_t* As, const bf16_t* Bs, int wm, int wn, int lane,
+                               f32x16 (&acc)[2][2]) {
+  const int frow = lane & 31, fk = (lane >> 5) * 8;
+  const bf16_t* as = As + (wm * 64 + frow) * GLD + fk;
+  const bf16_t* bs = Bs + (wn * 64 + frow) * GLD + fk;
+#pragma unroll
+  for (int ks = 0; ks < GBK; ks += 16) {
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(as + ks);
+    const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(as + 32 * GLD + ks);
+    const bf16x8 b0 = *reinterpret_cast<const bf16x8*>(bs + ks);
+    const bf16x8 b1 = *reinterpret_cast<const bf16x8*>(bs + 32 * GLD + ks);
+    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
+    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
+    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
+    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+  }
+}
+
+// grid: x = M tiles * N tiles (renumbered per XCD), z = split index (split-K)
+// or batch index (batched; never both).  vec: 16-byte epilogue vectors allowed.
 template <bool TA, bool TB, bool VA, bool VB, typename CT>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     Opnd A, Opnd Bm, CT* __restrict__ C, int64_t ldc, int M, int N, int K, int k_per_split,
-    float* __restrict__ partial, Epi epi, int64_t sA, int64_t sB, int64_t sC, int batched) {
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][GBM * GLD];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][GBN * GLD];
+    float* __restrict__ partial, Epi epi, int64_t sA, int64_t sB, int64_t sC, int batched, int vec) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char gemm_smem[];
+  bf16_t* As[2];
+  bf16_t* Bs[2];
+  As[0] = reinterpret_cast<bf16_t*>(gemm_smem);
+  Bs[0] = As[0] + GBM * GLD;
+  As[1] = Bs[0] + GBN * GLD;
+  Bs[1] = As[1] + GBM * GLD;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w >> 1, wn = w & 1;
-  const int m0 = blockIdx.y * GBM, n0 = blockIdx.x * GBN;
+  const int tiles_n = (N + GBN - 1) / GBN;
+  const int tile = xcd_block(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * GBM, n0 = (tile % tiles_n) * GBN;
   const int64_t bz = batched ? blockIdx.z : 0;
   if (batched) {
     A.p += bz * sA;
@@ -172,59 +264,88 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  typename LoaderSel<TA, VA>::T la;
-  typename LoaderSel<TB, VB>::T lb;
-  const int ktiles = (kend - kbeg + GBK - 1) / GBK;
+  typename LoaderSel<TA, VA>::T la0, la1;
+  typename LoaderSel<TB, VB>::T lb0, lb1;
+  const int ktiles = kend > kbeg ? (kend - kbeg + GBK - 1) / GBK : 0;
   if (ktiles > 0) {
-    la.load(A, M, kend, m0, kbeg);
-    lb.load(Bm, N, kend, n0, kbeg);
-    la.store(As[0]);
-    lb.store(Bs[0]);
+    la0.load(A, M, kend, m0, kbeg);
+    lb0.load(Bm, N, kend, n0, kbeg);
+  }
+  if (ktiles > 1) {
+    la1.load(A, M, kend, m0, kbeg + GBK);
+    lb1.load(Bm, N, kend, n0, kbeg + GBK);
+  }
+  if (ktiles > 0) {
+    la0.store(As[0]);
+    lb0.store(Bs[0]);
   }
   __syncthreads();
-  const int frow = lane & 31, fk = (lane >> 5) * 8;
-  for (int kt = 0; kt < ktiles; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < ktiles;
-    if (more) {
-      la.load(A, M, kend, m0, kbeg + (kt + 1) * GBK);
-      lb.load(Bm, N, kend, n0, kbeg + (kt + 1) * GBK);
+  // Two register stages and two LDS stages: while the MFMAs consume LDS stage
+  // s, the registers of the other stage receive the tile two steps ahead.
+  for (int kt = 0; kt < ktiles; kt += 2) {
+    if (kt + 2 < ktiles) {
+      la0.load(A, M, kend, m0, kbeg + (kt + 2) * GBK);
+      lb0.load(Bm, N, kend, n0, kbeg + (kt + 2) * GBK);
     }
-    const bf16_t* as = As[cur] + (wm * 64 + frow) * GLD + fk;
-    const bf16_t* bs = Bs[cur] + (wn * 64 + frow) * GLD + fk;
-#pragma unroll
-    for (int ks = 0; ks < GBK; ks += 16) {
-      bf16x8 a0 = *reinterpret_cast<const bf16x8*>(as + ks);
-      bf16x8 a1 = *reinterpret_cast<const bf16x8*>(as + 32 * GLD + ks);
-      bf16x8 b0 = *reinterpret_cast<const bf16x8*>(bs + ks);
-      bf16x8 b1 = *reinterpret_cast<const bf16x8*>(bs + 32 * GLD + ks);
-      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+    mma_k64(As[0], Bs[0], wm, wn, lane, acc);
+    if (kt + 1 < ktiles) {
+      la1.store(As[1]);
+      lb1.store(Bs[1]);
     }
-    if (more) {
-      la.store(As[cur ^ 1]);
-      lb.store(Bs[cur ^ 1]);
+    __syncthreads();
+    if (kt + 1 >= ktiles) break;
+    if (kt + 3 < ktiles) {
+      la1.load(A, M, kend, m0, kbeg + (kt + 3) * GBK);
+      lb1.load(Bm, N, kend, n0, kbeg + (kt + 3) * GBK);
+    }
+    mma_k64(As[1], Bs[1], wm, wn, lane, acc);
+    if (kt + 2 < ktiles) {
+      la0.store(As[0]);
+      lb0.store(Bs[0]);
     }
     __syncthreads();
   }
 
-  // D[i][j] of a 32x32 fragment: lane holds column (lane & 31), rows
-  // 8*(r/4) + 4*(lane/32) + r%4 for r = 0..15.
+  // Stage the fp32 tile in LDS.  D[i][j] of a 32x32 fragment: lane holds
+  // column (lane & 31), rows 8*(r/4) + 4*(lane/32) + r%4 for r = 0..15.
+  float* Cs = reinterpret_cast<float*>(gemm_smem);
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+      const int cl = wn * 64 + j * 32 + (lane & 31);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < M && col < N) {
-          if (partial) partial[((int64_t)blockIdx.z * M + row) * N + col] = acc[i][j][r];
-          else epi_store<CT>(C, ldc, row, col, acc[i][j][r], epi, bz);
-        }
+        const int rl = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        Cs[rl * CLD + cl] = acc[i][j][r];
       }
+    }
+  __syncthreads();
+  // Rows of the tile, 8 columns per thread.
+#pragma unroll
+  for (int q = 0; q < (GBM * GBN / 8) / 256; ++q) {
+    const int chunk = threadIdx.x + q * 256;
+    const int rl = chunk / (GBN / 8), cl = (chunk % (GBN / 8)) * 8;
+    const int row = m0 + rl, col = n0 + cl;
+    if (row >= M || col >= N) continue;
+    float v[8];
+    ld8f(Cs + rl * CLD + cl, v);
+    if (partial) {
+      float* pp = partial + ((int64_t)blockIdx.z * M + row) * N + col;
+      if ((N & 3) == 0 && col + 8 <= N) {
+        stg16(pp, Vec16<float>::pack(v));
+        stg16(pp + 4, Vec16<float>::pack(v + 4));
+      } else {
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (col + t < N) pp[t] = v[t];
+      }
+    } else if (vec && col + 8 <= N) {
+      epi_store8<CT>(C, ldc, row, col, v, epi, bz);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+        if (col + t < N) epi_store<CT>(C, ldc, row, col + t, v[t], epi, bz);
     }
   }
 }
@@ -288,7 +409,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
-static bool aligned4(const void* p) { return ((uintptr_t)p & 3) == 0; }
 
 int gemm_splits(const GemmArgs& g) {
   if (g.dt != DT_BF16 || g.batch > 1) return 1;
@@ -309,6 +429,23 @@ static Epi make_epi(const GemmArgs& g) {
              g.accumulate};
 }
 
+static bool a16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// 16-byte epilogue vectors: every row of C and of the epilogue operands
+// (bias, addend, mask) starts 16-byte aligned.
+static int epi_vec_ok(const GemmArgs& g) {
+  const int64_t ce = g.c_dt == DT_BF16 ? 8 : 4;
+  if (!a16(g.C) || g.ldc % ce || g.sC % ce) return 0;
+  if (g.accumulate && (g.ldc % 4)) return 0;
+  if (g.bias && !a16(g.bias)) return 0;
+  if (g.addend && (!a16(g.addend) || g.ld_add % 4 || g.s_add % 4)) return 0;
+  if (g.mask) {
+    const int64_t me = g.mask_dt == DT_BF16 ? 8 : 4;
+    if (!a16(g.mask) || g.ldm % me || g.s_mask % me) return 0;
+  }
+  return 1;
+}
+
 template <bool TA, bool TB, bool VA, bool VB>
 static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st) {
   const int splits = gemm_splits(g);
@@ -319,17 +456,29 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
   int kps = (g.K + splits - 1) / splits;
   kps = ((kps + GBK - 1) / GBK) * GBK;
   const int batched = g.batch > 1 ? 1 : 0;
-  dim3 grid(cdiv(g.N, GBN), cdiv(g.M, GBM), batched ? g.batch : splits);
+  dim3 grid(cdiv(g.N, GBN) * cdiv(g.M, GBM), 1, batched ? g.batch : splits);
   Epi epi = make_epi(g);
   Opnd a{(const bf16_t*)g.A, g.lda, g.kseg, g.ksA};
   Opnd b{(const bf16_t*)g.B, g.ldb, g.kseg, g.ksB};
   float* partial = splits > 1 ? ws : nullptr;
-  if (g.c_dt == DT_BF16)
-    gemm_bf16_kernel<TA, TB, VA, VB, bf16_t><<<grid, 256, 0, st>>>(
-        a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA, g.sB, g.sC, batched);
-  else
-    gemm_bf16_kernel<TA, TB, VA, VB, float><<<grid, 256, 0, st>>>(
-        a, b, (float*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA, g.sB, g.sC, batched);
+  const int vec = epi_vec_ok(g);
+  // The kernels use 72 KiB of dynamic LDS (above the 64 KiB default limit).
+  static std::once_flag once_bf, once_f;
+  if (g.c_dt == DT_BF16) {
+    auto k = gemm_bf16_kernel<TA, TB, VA, VB, bf16_t>;
+    std::call_once(once_bf, [&] {
+      (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
+    });
+    k<<<grid, 256, GEMM_LDS, st>>>(a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA,
+                                   g.sB, g.sC, batched, vec);
+  } else {
+    auto k = gemm_bf16_kernel<TA, TB, VA, VB, float>;
+    std::call_once(once_f, [&] {
+      (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
+    });
+    k<<<grid, 256, GEMM_LDS, st>>>(a, b, (float*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA,
+                                   g.sB, g.sC, batched, vec);
+  }
   LAT_LAUNCH_CHECK();
   if (splits > 1) {
     const int64_t n = (int64_t)g.M * g.N;
@@ -344,14 +493,14 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
 
 template <bool TA, bool TB>
 static hipError_t gemm_bf16_dispatch(const GemmArgs& g, float* ws, hipStream_t st) {
-  // 16-byte K-vectors need 8-aligned rows (and segments); M-pairs need even rows
-  // and 4-byte alignment.  Batch strides must keep the same alignment.
+  // 16-byte vectors (along K, or along M/N for a transposed operand) need
+  // 8-element-aligned rows, segments and batch strides.
   const bool seg_ok = g.kseg == 0 || (g.kseg % 8 == 0 && g.ksA % 8 == 0 && g.ksB % 8 == 0);
-  const bool va = TA ? (g.lda % 2 == 0 && aligned4(g.A) && g.M % 2 == 0 && g.sA % 2 == 0 &&
-                        (g.kseg == 0 || g.ksA % 2 == 0))
+  const bool va = TA ? (g.lda % 8 == 0 && aligned16(g.A) && g.M % 8 == 0 && g.sA % 8 == 0 &&
+                        (g.kseg == 0 || g.ksA % 8 == 0))
                      : (g.lda % 8 == 0 && aligned16(g.A) && g.K % 8 == 0 && g.sA % 8 == 0 && seg_ok);
-  const bool vb = TB ? (g.ldb % 2 == 0 && aligned4(g.B) && g.N % 2 == 0 && g.sB % 2 == 0 &&
-                        (g.kseg == 0 || g.ksB % 2 == 0))
+  const bool vb = TB ? (g.ldb % 8 == 0 && aligned16(g.B) && g.N % 8 == 0 && g.sB % 8 == 0 &&
+                        (g.kseg == 0 || g.ksB % 8 == 0))
                      : (g.ldb % 8 == 0 && aligned16(g.B) && g.K % 8 == 0 && g.sB % 8 == 0 && seg_ok);
   if (va && vb) return gemm_bf16_launch<TA, TB, true, true>(g, ws, st);
   if (va) return gemm_bf16_launch<TA, TB, true, false>(g, ws, st);
