@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 1
+#define LATTICE_ABI_VERSION 2
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -84,14 +84,19 @@ typedef struct {
 } lattice_jagged;
 
 /* All tables stacked in one buffer; table f occupies global rows
- * row_base[f] .. row_base[f+1]-1.  Embedding dimension d is uniform across
- * features (Section 3.3.1). */
+ * row_base[f] .. row_base[f+1]-1 (row_base non-decreasing).  Embedding
+ * dimension d is uniform across features (Section 3.3.1). */
 typedef struct {
   void* data;                /* device [total_rows, dim], dtype */
   lattice_dtype dtype;
   int32_t dim;               /* d: multiple of 8, <= 256 */
   int64_t total_rows;        /* < 2^31 */
   const int64_t* row_base;   /* device [F+1] */
+  int64_t max_rows;          /* rows of the largest table, or 0 (unknown: total_rows
+                                is used).  The backward sorts each feature's lookups
+                                by their row within its table, so its cost grows with
+                                the bits of this bound.  Must be >= every table's rows
+                                (lattice_validate_batch checks it). */
 } lattice_tables;
 
 /* Pooled lookup: X[b, first_slot+f, :] = sum (or mean) over j in bag(f,b) of
@@ -129,9 +134,11 @@ lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_ja
                                   void* ws, size_t ws_bytes, void* stream);
 
 /* Synchronous check of a batch against the tables: offsets[0] == 0,
- * non-decreasing, offsets[F*B] == nnz, and 0 <= indices[j] < rows of its
- * table.  Returns BAD_INPUT with *first_bad (host) = first bad offset
- * position (as -1 - position) or first bad index position. */
+ * non-decreasing, offsets[F*B] == nnz, 0 <= indices[j] < rows of its
+ * table, and (if max_rows != 0) no table has more than max_rows rows.
+ * Returns BAD_INPUT with *first_bad (host) = first bad offset position (as
+ * -1 - position), first bad index position, or -1 - (F*B + 1 + f) for a
+ * table f larger than max_rows. */
 lattice_status lattice_validate_batch(const lattice_tables* tables, const lattice_jagged* bags,
                                       int64_t* first_bad, void* stream);
 

@@ -26,7 +26,7 @@ class lattice_jagged(Structure):
 
 class lattice_tables(Structure):
     _fields_ = [("data", c_void_p), ("dtype", c_int), ("dim", c_int32), ("total_rows", c_int64),
-                ("row_base", c_void_p)]
+                ("row_base", c_void_p), ("max_rows", c_int64)]
 
 
 class lattice_sparse_grad(Structure):

@@ -43,10 +43,20 @@ def _contig(*ts):
             raise ValueError("tensor must be contiguous")
 
 
-def _tables(table, row_base):
+def table_max_rows(row_base):
+    """Rows of the largest table (one device-to-host copy of row_base)."""
+    rb = row_base.cpu()
+    return int((rb[1:] - rb[:-1]).max()) if rb.numel() > 1 else 0
+
+
+def _tables(table, row_base, max_rows=None):
+    """max_rows None: derived from row_base (a synchronising copy); 0: unknown."""
     _contig(table, row_base)
+    if max_rows is None:
+        max_rows = table_max_rows(row_base)
     return A.lattice_tables(data=table.data_ptr(), dtype=_dt(table), dim=table.shape[1],
-                            total_rows=table.shape[0], row_base=row_base.data_ptr())
+                            total_rows=table.shape[0], row_base=row_base.data_ptr(),
+                            max_rows=int(max_rows))
 
 
 def _jagged(offsets, indices, F, B):
@@ -61,19 +71,19 @@ def lattice_embbag_fwd(table, row_base, offsets, indices, F, B, X, first_slot=0,
                        stream=None):
     _contig(X)
     lib = load()
-    t, j = _tables(table, row_base), _jagged(offsets, indices, F, B)
+    t, j = _tables(table, row_base, 0), _jagged(offsets, indices, F, B)
     check(lib.lattice_embbag_fwd(byref(t), byref(j), _POOL[pool], _p(X), _dt(X), X.shape[1],
                                  first_slot, _stream(stream)))
     return X
 
 
 def lattice_embbag_bwd(table, row_base, offsets, indices, F, B, dX, first_slot=0, lr=0.0,
-                       pool="sum", emit_grad_rows=True, stream=None):
+                       pool="sum", emit_grad_rows=True, stream=None, max_rows=None):
     """Returns dict(unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows); with lr != 0
-    the table is updated in place."""
+    the table is updated in place.  max_rows: rows of the largest table (None: from row_base)."""
     _contig(dX)
     lib = load()
-    t, j = _tables(table, row_base), _jagged(offsets, indices, F, B)
+    t, j = _tables(table, row_base, max_rows), _jagged(offsets, indices, F, B)
     nnz = indices.numel()
     dev = table.device
     n = max(nnz, 1)
@@ -93,10 +103,10 @@ def lattice_embbag_bwd(table, row_base, offsets, indices, F, B, dX, first_slot=0
     return out
 
 
-def lattice_validate_batch(table, row_base, offsets, indices, F, B, stream=None):
+def lattice_validate_batch(table, row_base, offsets, indices, F, B, stream=None, max_rows=None):
     """Returns (ok, first_bad)."""
     lib = load()
-    t, j = _tables(table, row_base), _jagged(offsets, indices, F, B)
+    t, j = _tables(table, row_base, max_rows), _jagged(offsets, indices, F, B)
     bad = ctypes.c_int64(0)
     st = lib.lattice_validate_batch(byref(t), byref(j), byref(bad), _stream(stream))
     if st == 4:
@@ -217,10 +227,12 @@ class StepModel:
     """Marshals a model's device tensors into a lattice_model_desc.
 
     tables [R, d], row_base int64 [F+1]; bottom/top: lists of dicts
-    {W, b, dW, db}; fm_W / fm_dW for the FM interaction."""
+    {W, b, dW, db}; fm_W / fm_dW for the FM interaction; max_rows: rows of the
+    largest table (None: read from row_base once, here)."""
 
     def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
-                 fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5):
+                 fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5,
+                 max_rows=None):
         _contig(tables, row_base)
         dt = _dt(tables)
         d = tables.shape[1]
@@ -234,7 +246,8 @@ class StepModel:
                                         fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
                                         n_layers=len(stack) if stack else 0, stack_n=stack_n,
                                         ln_eps=ln_eps, layers=self._stack)
-        self.desc = A.lattice_model_desc(dtype=dt, pool=_POOL[pool], tables=_tables(tables, row_base),
+        self.desc = A.lattice_model_desc(dtype=dt, pool=_POOL[pool],
+                                         tables=_tables(tables, row_base, max_rows),
                                          num_features=num_features, dense_in=dense_in,
                                          bottom=self._bottom, interact=idesc, top=self._top)
         self.tensors = dict(tables=tables, row_base=row_base, bottom=bottom, top=top, fm_W=fm_W,

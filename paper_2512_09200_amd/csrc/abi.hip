@@ -50,6 +50,11 @@ static lattice_status check_dim(int dim, lattice_dtype dt) {
   return LATTICE_OK;
 }
 
+// rows of the largest table (max_rows when given, else the total row count)
+static int64_t local_rows_bound(const lattice_tables* t) {
+  return t->max_rows > 0 ? t->max_rows : t->total_rows;
+}
+
 static lattice_status check_tables(const lattice_tables* t, const lattice_jagged* j) {
   REQUIRE(t && j, "null tables or bags");
   REQUIRE(j->num_features >= 0 && j->batch >= 0 && j->nnz >= 0, "negative sizes");
@@ -58,6 +63,7 @@ static lattice_status check_tables(const lattice_tables* t, const lattice_jagged
   if ((int64_t)j->num_features * j->batch > 0) REQUIRE(j->offsets && t->row_base && t->data, "null pointer in batch/tables");
   REQUIRE(t->dtype == LATTICE_F32 || t->dtype == LATTICE_BF16, "bad table dtype");
   if (t->total_rows >= ((int64_t)1 << 31)) FAIL(LATTICE_ERR_UNSUPPORTED, "total_rows must be < 2^31");
+  REQUIRE(t->max_rows >= 0 && t->max_rows <= t->total_rows, "max_rows outside 0 .. total_rows");
   return check_dim(t->dim, t->dtype);
 }
 
@@ -97,7 +103,7 @@ lattice_status lattice_embbag_fwd(const lattice_tables* tables, const lattice_ja
 
 size_t lattice_embbag_bwd_workspace(const lattice_tables* tables, const lattice_jagged* bags) {
   if (!tables || !bags) return 0;
-  return embbag_bwd_workspace(bags->nnz, tables->dim);
+  return embbag_bwd_workspace(bags->nnz, tables->dim, bags->num_features);
 }
 
 lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_jagged* bags,
@@ -115,9 +121,9 @@ lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_ja
   if (bags->nnz > 0) REQUIRE(dX, "null dX");
   if ((int64_t)bags->batch * n_slots * tables->dim * (int64_t)esize(dx_dtype) > (int64_t)UINT32_MAX)
     FAIL(LATTICE_ERR_UNSUPPORTED, "dX larger than 4 GiB");
-  const size_t need = embbag_bwd_workspace(bags->nnz, tables->dim);
+  const size_t need = embbag_bwd_workspace(bags->nnz, tables->dim, bags->num_features);
   if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
-  HIPRET(embbag_bwd(tables->row_base, tables->total_rows, bags->offsets, bags->indices,
+  HIPRET(embbag_bwd(tables->row_base, local_rows_bound(tables), bags->offsets, bags->indices,
                     bags->num_features, bags->batch, bags->nnz, pool == LATTICE_POOL_MEAN, dX,
                     dt_of(dx_dtype), n_slots, first_slot, tables->dim, out->unique_rows,
                     out->seg_offsets, out->sorted_bags, out->num_unique, out->grad_rows,
@@ -140,13 +146,17 @@ lattice_status lattice_validate_batch(const lattice_tables* tables, const lattic
   if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_validate_result)) != hipSuccess)
     FAIL(LATTICE_ERR_HIP, "hipGetSymbolAddress failed");
   HIPRET(validate_batch(tables->row_base, bags->offsets, bags->indices, bags->num_features,
-                        bags->batch, bags->nnz, (unsigned long long*)ptr, strm(stream)));
+                        bags->batch, bags->nnz, tables->max_rows, (unsigned long long*)ptr,
+                        strm(stream)));
   unsigned long long host[2];
   if (hipMemcpyAsync(host, ptr, sizeof(host), hipMemcpyDeviceToHost, strm(stream)) != hipSuccess ||
       hipStreamSynchronize(strm(stream)) != hipSuccess)
     FAIL(LATTICE_ERR_HIP, "validate copy failed");
   if (host[0] != ~0ull) {
     *first_bad = -1 - (int64_t)host[0];
+    const int64_t nbags = (int64_t)bags->num_features * bags->batch;
+    if ((int64_t)host[0] > nbags)
+      FAIL(LATTICE_ERR_BAD_INPUT, "table %lld has more than max_rows rows", (long long)host[0] - nbags - 1);
     FAIL(LATTICE_ERR_BAD_INPUT, "malformed offsets at position %lld", (long long)host[0]);
   }
   if (host[1] != ~0ull) {
@@ -609,7 +619,7 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
   sc = std::max(sc, bce_workspace((int64_t)B * P->T));
   L.interact = take(interact_ws(&m->interact, B));
-  sc = std::max(sc, embbag_bwd_workspace(nnz, d));
+  sc = std::max(sc, embbag_bwd_workspace(nnz, d, m->num_features));
   L.scratch = take(sc);
   L.scratch_bytes = (int64_t)sc;
   L.total_bytes = off;
@@ -723,7 +733,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   }
   HIPRET(mark(8));
   // 9. row-coalesced embedding gradient (+ row-sparse SGD)
-  HIPRET(embbag_bwd(m->tables.row_base, m->tables.total_rows, batch->bags.offsets,
+  HIPRET(embbag_bwd(m->tables.row_base, local_rows_bound(&m->tables), batch->bags.offsets,
                     batch->bags.indices, m->num_features, B, batch->bags.nnz,
                     m->pool == LATTICE_POOL_MEAN, dX, dt, n, s0, d, (int*)at(L.unique_rows),
                     (int*)at(L.seg_offsets), (int*)at(L.sorted_bags), (int*)at(L.num_unique),

@@ -9,7 +9,10 @@
 //
 // Backward (no floating-point atomics):
 //   keys     : key = row_base[f] + index, value = bag id, per position
-//   sort     : stable LSD radix sort by key (ties keep position order)
+//   sort     : stable LSD radix sort by key (ties keep position order); the
+//              positions are grouped by feature, so each feature's segment is
+//              sorted by its local row and only the largest table's row bits
+//              need digit passes
 //   segments : run boundaries -> unique rows ascending, run offsets, and the
 //              run id before every 256-position range
 //   reduce   : one wave per range of 256 sorted occurrences; dX rows are
@@ -612,13 +615,13 @@ __global__ void zero_int_kernel(int* p, int n) {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-size_t embbag_bwd_workspace(int64_t nnz, int dim) {
+size_t embbag_bwd_workspace(int64_t nnz, int dim, int F) {
   const int64_t n = nnz > 0 ? nnz : 1;
   const int64_t ranges = cdiv(n, RANGE);
   size_t s = 0;
   s += 2 * align256((size_t)n * 4);                    // keys, vals (unsorted)
   s += align256((size_t)n * 4);                        // sorted keys
-  s += align256(radix_sort_workspace(n));
+  s += align256(radix_sort_segments_workspace(n, F));
   s += align256((size_t)(cdiv(n, SEG_TILE) + 1) * 4);  // segment tile counts
   s += 3 * align256((size_t)ranges * 4);               // range_ubefore, part_uid, span_list
   s += align256(4);                                    // span_count
@@ -660,7 +663,7 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
   return hipSuccess;
 }
 
-hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t* offsets,
+hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
                       const int32_t* indices, int F, int B, int64_t nnz, int mean,
                       const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
@@ -683,7 +686,7 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t
   int* keys = (int*)take((size_t)n * 4);
   int* vals = (int*)take((size_t)n * 4);
   int* skeys = (int*)take((size_t)n * 4);
-  void* sort_ws = take(radix_sort_workspace(n));
+  void* sort_ws = take(radix_sort_segments_workspace(n, F));
   int* tile_counts = (int*)take((size_t)(cdiv(n, SEG_TILE) + 1) * 4);
   int* range_ubefore = (int*)take((size_t)ranges * 4);
   int* part_uid = (int*)take((size_t)ranges * 4);
@@ -699,7 +702,8 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t
     embbag_keys_kernel<<<cdiv(bags, 4), 256, 0, s>>>(row_base, offsets, indices, F, B, keys, vals);
     LAT_LAUNCH_CHECK();
   }
-  hipError_t e = radix_sort_pairs(keys, vals, n, total_rows - 1, skeys, sorted_bags, sort_ws, s);
+  hipError_t e = radix_sort_segments(keys, vals, n, offsets, F, B, row_base, max_local_rows, skeys,
+                                     sorted_bags, sort_ws, s);
   if (e != hipSuccess) return e;
   const int tiles = cdiv(n, SEG_TILE);
   seg_count_kernel<<<tiles, SEG_THREADS, 0, s>>>(skeys, n, tile_counts);
@@ -732,10 +736,12 @@ __global__ void validate_init_kernel(unsigned long long* r) {
 __global__ __launch_bounds__(256) void validate_kernel(const int64_t* __restrict__ row_base,
                                                        const int32_t* __restrict__ offsets,
                                                        const int32_t* __restrict__ indices, int F,
-                                                       int B, int64_t nnz,
+                                                       int B, int64_t nnz, int64_t max_rows,
                                                        unsigned long long* __restrict__ bad) {
   const int64_t bags = (int64_t)F * B;
   const int64_t bag = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (max_rows > 0 && bag < F && row_base[bag + 1] - row_base[bag] > max_rows)
+    atomicMin(&bad[0], (unsigned long long)(bags + 1 + bag));
   if (bag == 0 && offsets[0] != 0) atomicMin(&bad[0], 0ull);
   if (bag == 0 && offsets[bags] != nnz) atomicMin(&bad[0], (unsigned long long)bags);
   if (bag >= bags) return;
@@ -756,13 +762,14 @@ __global__ __launch_bounds__(256) void validate_kernel(const int64_t* __restrict
 }
 
 hipError_t validate_batch(const int64_t* row_base, const int32_t* offsets,
-                          const int32_t* indices, int F, int B, int64_t nnz,
+                          const int32_t* indices, int F, int B, int64_t nnz, int64_t max_rows,
                           unsigned long long* dev_result, hipStream_t s) {
   validate_init_kernel<<<1, 1, 0, s>>>(dev_result);
   LAT_LAUNCH_CHECK();
   const int64_t bags = (int64_t)F * B;
-  validate_kernel<<<cdiv(bags + 1, 256), 256, 0, s>>>(row_base, offsets, indices, F, B, nnz,
-                                                       dev_result);
+  const int64_t threads = (bags + 1 > F ? bags + 1 : F);
+  validate_kernel<<<cdiv(threads, 256), 256, 0, s>>>(row_base, offsets, indices, F, B, nnz,
+                                                     max_rows, dev_result);
   LAT_LAUNCH_CHECK();
   return hipSuccess;
 }

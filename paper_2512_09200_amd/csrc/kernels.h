@@ -9,9 +9,12 @@ namespace lat {
 size_t scan_workspace(int64_t n);
 hipError_t exclusive_scan(const int* in, int* out, int64_t n, int* tmp, hipStream_t s);
 hipError_t exclusive_scan_inplace_small(int* a, int n, hipStream_t s);
-size_t radix_sort_workspace(int64_t n);
-hipError_t radix_sort_pairs(int* keys, int* vals, int64_t n, int64_t max_key, int* keys_out,
-                            int* vals_out, void* ws, hipStream_t s);
+// Sort of a jagged batch's (global row, bag) pairs whose positions are grouped
+// by feature: each feature segment is sorted by its local row (< max_local_rows).
+size_t radix_sort_segments_workspace(int64_t n, int F);
+hipError_t radix_sort_segments(int* keys, int* vals, int64_t n, const int32_t* offsets, int F,
+                               int B, const int64_t* row_base, int64_t max_local_rows,
+                               int* keys_out, int* vals_out, void* ws, hipStream_t s);
 
 // embbag.hip
 // keys/vals (optional): also write the backward's sort keys (global row) and
@@ -20,15 +23,16 @@ hipError_t embbag_fwd(const void* E, DType edt, int dim, const int64_t* row_base
                       const int32_t* offsets, const int32_t* indices, int F, int B, int mean,
                       void* X, DType xdt, int n_slots, int first_slot, hipStream_t s,
                       int* keys = nullptr, int* vals = nullptr);
-size_t embbag_bwd_workspace(int64_t nnz, int dim);
-hipError_t embbag_bwd(const int64_t* row_base, int64_t total_rows, const int32_t* offsets,
+size_t embbag_bwd_workspace(int64_t nnz, int dim, int F);
+// max_local_rows: rows of the largest table (bounds every local index)
+hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
                       const int32_t* indices, int F, int B, int64_t nnz, int mean,
                       const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
                       float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
                       const int* keys_in = nullptr, const int* vals_in = nullptr);
 hipError_t validate_batch(const int64_t* row_base, const int32_t* offsets,
-                          const int32_t* indices, int F, int B, int64_t nnz,
+                          const int32_t* indices, int F, int B, int64_t nnz, int64_t max_rows,
                           unsigned long long* dev_result, hipStream_t s);
 
 // gemm.hip

@@ -2,9 +2,9 @@
 // exclusive scan, used by the deterministic embedding backward to group the
 // occurrences of each table row.
 //
-// Sort pass (8-bit digit):
-//   hist    : per tile of 4096 items, digit histogram in LDS -> counts[d][tile]
-//   scan    : exclusive scan of counts (digit-major) -> global bucket offsets
+// Sort pass (digit of up to 8 bits):
+//   hist    : per tile of 4096 items, digit histogram in LDS -> counts
+//   scan    : exclusive scan of the counts -> global bucket offsets
 //   scatter : each wave ranks its contiguous 1024-item chunk with ballots
 //             (items with equal digits keep their order), waves are ordered
 //             within the tile, tiles within the bucket: a stable pass.
@@ -123,25 +123,88 @@ hipError_t exclusive_scan(const int* in, int* out, int64_t n, int* tmp, hipStrea
 // ---------------------------------------------------------------------------
 // radix sort
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(SORT_THREADS) void radix_hist_kernel(const int* __restrict__ keys, int n,
-                                                                   int shift, int tiles,
-                                                                   int* __restrict__ counts) {
-  __shared__ int hist[RADIX];
-  for (int i = threadIdx.x; i < RADIX; i += SORT_THREADS) hist[i] = 0;
-  __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * SORT_TILE;
-#pragma unroll
-  for (int i = 0; i < SORT_ITEMS; ++i) {
-    int64_t k = base + (int64_t)i * SORT_THREADS + threadIdx.x;
-    if (k < n) atomicAdd(&hist[((uint32_t)keys[k] >> shift) & (RADIX - 1)], 1);
-  }
-  __syncthreads();
-  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS) counts[(int64_t)d * tiles + blockIdx.x] = hist[d];
+static int key_bits(int64_t max_key) {
+  int b = 0;
+  while (b < 31 && ((int64_t)1 << b) <= max_key) ++b;
+  return b;
 }
 
-__global__ __launch_bounds__(SORT_THREADS) void radix_scatter_kernel(
-    const int* __restrict__ keys_in, const int* __restrict__ vals_in, int n, int shift, int tiles,
-    const int* __restrict__ offsets, int* __restrict__ keys_out, int* __restrict__ vals_out) {
+// ---------------------------------------------------------------------------
+// segmented radix sort (positions grouped by feature)
+// ---------------------------------------------------------------------------
+// The occurrences of a jagged batch are feature-major, so segment f (positions
+// offsets[f*B] .. offsets[(f+1)*B]) holds all keys of table f, and those keys
+// lie in [row_base[f], row_base[f] + rows_f).  Sorting every segment by its
+// local row (key - row_base[f]) is therefore a sort by global key, and needs
+// only as many digit passes as the largest table has row bits.  Tiles never
+// straddle segments; a pass scatters each tile inside its own segment, with
+// bucket offsets from one device-wide scan of the counts laid out as
+// [segment][digit][tile of the segment].
+
+__global__ __launch_bounds__(256) void seg_ntiles_kernel(const int32_t* __restrict__ offsets, int F,
+                                                         int B, int* __restrict__ tile_base) {
+  const int f = blockIdx.x * 256 + threadIdx.x;
+  if (f > F) return;
+  tile_base[f] = f < F ? (offsets[(int64_t)(f + 1) * B] - offsets[(int64_t)f * B] + SORT_TILE - 1) / SORT_TILE : 0;
+}
+
+// tile -> segment map: block f fills its segment's tiles
+__global__ __launch_bounds__(256) void seg_tilemap_kernel(const int* __restrict__ tile_base,
+                                                          int* __restrict__ tile_seg) {
+  const int f = blockIdx.x;
+  for (int t = tile_base[f] + threadIdx.x; t < tile_base[f + 1]; t += 256) tile_seg[t] = f;
+}
+
+struct SegTile {
+  int f, lt, nt, base, cnt, cb;  // segment, tile within it, its tile count, first position, items, count base
+  int64_t key0;                  // row_base[f]
+};
+
+__device__ inline bool seg_tile(const int* tile_base, const int* tile_seg, const int32_t* offsets,
+                                const int64_t* row_base, int F, int B, int radix, SegTile& t) {
+  const int tix = blockIdx.x;
+  if (tix >= tile_base[F]) return false;
+  t.f = tile_seg[tix];
+  const int tb = tile_base[t.f];
+  t.lt = tix - tb;
+  t.nt = tile_base[t.f + 1] - tb;
+  const int s0 = offsets[(int64_t)t.f * B], s1 = offsets[(int64_t)(t.f + 1) * B];
+  t.base = s0 + t.lt * SORT_TILE;
+  t.cnt = s1 - t.base < SORT_TILE ? s1 - t.base : SORT_TILE;
+  t.cb = tb * radix;
+  t.key0 = row_base[t.f];
+  return true;
+}
+
+__global__ __launch_bounds__(SORT_THREADS) void radix_hist_seg_kernel(
+    const int* __restrict__ keys, const int32_t* __restrict__ offsets, const int64_t* __restrict__ row_base,
+    int F, int B, const int* __restrict__ tile_base, const int* __restrict__ tile_seg, int shift,
+    int dbits, int* __restrict__ counts) {
+  __shared__ int hist[RADIX];
+  const int radix = 1 << dbits;
+  SegTile t;
+  if (!seg_tile(tile_base, tile_seg, offsets, row_base, F, B, radix, t)) {
+    // blocks past the last tile clear the unused tail of the counts
+    for (int d = threadIdx.x; d < radix; d += SORT_THREADS) counts[(int64_t)blockIdx.x * radix + d] = 0;
+    return;
+  }
+  for (int i = threadIdx.x; i < radix; i += SORT_THREADS) hist[i] = 0;
+  __syncthreads();
+  const int key0 = (int)t.key0;
+#pragma unroll
+  for (int i = 0; i < SORT_ITEMS; ++i) {
+    const int k = i * SORT_THREADS + threadIdx.x;
+    if (k < t.cnt) atomicAdd(&hist[((uint32_t)(keys[t.base + k] - key0) >> shift) & (radix - 1)], 1);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < radix; d += SORT_THREADS) counts[t.cb + (int64_t)d * t.nt + t.lt] = hist[d];
+}
+
+__global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
+    const int* __restrict__ keys_in, const int* __restrict__ vals_in, const int32_t* __restrict__ offsets,
+    const int64_t* __restrict__ row_base, int F, int B, const int* __restrict__ tile_base,
+    const int* __restrict__ tile_seg, int shift, int dbits, const int* __restrict__ coffs,
+    int* __restrict__ keys_out, int* __restrict__ vals_out) {
   constexpr int NW = SORT_THREADS / 64;
   constexpr int CHUNK = SORT_TILE / NW;  // 1024 consecutive items per wave
   constexpr int ROUNDS = CHUNK / 64;     // 16
@@ -150,36 +213,37 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_kernel(
   __shared__ int scan_tmp[SORT_THREADS / 64];
   __shared__ int lkeys[SORT_TILE];
   __shared__ int lvals[SORT_TILE];
+  const int radix = 1 << dbits;
+  SegTile t;
+  if (!seg_tile(tile_base, tile_seg, offsets, row_base, F, B, radix, t)) return;
+  const int key0 = (int)t.key0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < NW * RADIX; i += SORT_THREADS) (&wcnt[0][0])[i] = 0;
   __syncthreads();
-
-  const int64_t tbase = (int64_t)blockIdx.x * SORT_TILE;
-  const int64_t cbase = tbase + (int64_t)w * CHUNK;
+  const int cbase = w * CHUNK;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int key[ROUNDS], val[ROUNDS], rank[ROUNDS];
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
-    int64_t k = cbase + (int64_t)r * 64 + lane;
-    bool valid = k < n;
-    key[r] = valid ? keys_in[k] : 0;
-    val[r] = valid ? vals_in[k] : 0;
+    const int k = cbase + r * 64 + lane;
+    const bool valid = k < t.cnt;
+    key[r] = valid ? keys_in[t.base + k] : 0;
+    val[r] = valid ? vals_in[t.base + k] : 0;
   }
   // stable rank of each item among the wave's items with the same digit
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
-    int64_t k = cbase + (int64_t)r * 64 + lane;
-    bool valid = k < n;
-    uint32_t d = ((uint32_t)key[r] >> shift) & (RADIX - 1);
+    const int k = cbase + r * 64 + lane;
+    const bool valid = k < t.cnt;
+    const uint32_t d = ((uint32_t)(key[r] - key0) >> shift) & (radix - 1);
     uint64_t peers = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < RADIX_BITS; ++b) {
-      uint64_t m = __ballot((d >> b) & 1u);
+    for (int b = 0; b < dbits; ++b) {
+      const uint64_t m = __ballot((d >> b) & 1u);
       peers &= ((d >> b) & 1u) ? m : ~m;
     }
-    int before = __popcll(peers & lt_mask);
-    int cnt = __popcll(peers);
-    int base = valid ? wcnt[w][d] : 0;
+    const int before = __popcll(peers & lt_mask);
+    const int cnt = __popcll(peers);
+    const int base = valid ? wcnt[w][d] : 0;
     rank[r] = base + before;
     __builtin_amdgcn_wave_barrier();
     if (valid && before == 0) wcnt[w][d] = base + cnt;
@@ -189,26 +253,27 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_kernel(
   __syncthreads();
   // tile-level digit starts (exclusive scan over digits) and per-wave bases
   {
-    const int d = threadIdx.x;  // SORT_THREADS == RADIX
+    const int d = threadIdx.x;  // SORT_THREADS == RADIX >= radix
     int tot = 0;
-    for (int i = 0; i < NW; ++i) tot += wcnt[i][d];
+    if (d < radix)
+      for (int i = 0; i < NW; ++i) tot += wcnt[i][d];
     int all;
     const int st = block_exclusive_scan(tot, scan_tmp, &all);
     dstart[d] = st;
     int run = st;
-    for (int i = 0; i < NW; ++i) {
-      const int c = wcnt[i][d];
-      wcnt[i][d] = run;
-      run += c;
-    }
+    if (d < radix)
+      for (int i = 0; i < NW; ++i) {
+        const int c = wcnt[i][d];
+        wcnt[i][d] = run;
+        run += c;
+      }
   }
   __syncthreads();
-  // the tile in stable digit order in LDS
 #pragma unroll
   for (int r = 0; r < ROUNDS; ++r) {
-    int64_t k = cbase + (int64_t)r * 64 + lane;
-    if (k < n) {
-      uint32_t d = ((uint32_t)key[r] >> shift) & (RADIX - 1);
+    const int k = cbase + r * 64 + lane;
+    if (k < t.cnt) {
+      const uint32_t d = ((uint32_t)(key[r] - key0) >> shift) & (radix - 1);
       const int pos = wcnt[w][d] + rank[r];
       lkeys[pos] = key[r];
       lvals[pos] = val[r];
@@ -216,61 +281,67 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_kernel(
   }
   __syncthreads();
   // consecutive threads write consecutive positions of each digit's run
-  const int tn = (int)((n - tbase) < SORT_TILE ? (n - tbase) : SORT_TILE);
-  for (int i = threadIdx.x; i < tn; i += SORT_THREADS) {
+  for (int i = threadIdx.x; i < t.cnt; i += SORT_THREADS) {
     const int kk = lkeys[i];
-    const uint32_t d = ((uint32_t)kk >> shift) & (RADIX - 1);
-    const int pos = offsets[(int64_t)d * tiles + blockIdx.x] + (i - dstart[d]);
+    const uint32_t d = ((uint32_t)(kk - key0) >> shift) & (radix - 1);
+    const int pos = coffs[t.cb + (int64_t)d * t.nt + t.lt] + (i - dstart[d]);
     keys_out[pos] = kk;
     vals_out[pos] = lvals[i];
   }
 }
 
-static int key_bits(int64_t max_key) {
-  int b = 0;
-  while (b < 31 && ((int64_t)1 << b) <= max_key) ++b;
-  return b;
+static int seg_sort_tiles_max(int64_t n, int F) { return cdiv(n, SORT_TILE) + F; }
+
+size_t radix_sort_segments_workspace(int64_t n, int F) {
+  const int64_t tmax = seg_sort_tiles_max(n > 0 ? n : 1, F);
+  const size_t c = (size_t)RADIX * tmax;
+  return 2 * (size_t)(n > 0 ? n : 1) * sizeof(int)  // ping-pong keys/vals
+         + 2 * c * sizeof(int)                        // counts + offsets
+         + scan_workspace((int64_t)c)
+         + (size_t)(F + 1 + tmax) * sizeof(int) + 1024;  // tile_base, tile_seg
 }
 
-size_t radix_sort_workspace(int64_t n) {
-  const int tiles = cdiv(n, SORT_TILE);
-  size_t c = (size_t)RADIX * tiles;
-  return 2 * (size_t)n * sizeof(int)            // ping-pong keys/vals (second buffer pair)
-         + 2 * c * sizeof(int)                  // counts + offsets
-         + scan_workspace((int64_t)c) + 256;
-}
-
-// Sorts (keys, vals) of length n with keys in [0, max_key].  keys/vals are
-// clobbered; the sorted result is written to keys_out / vals_out.
-hipError_t radix_sort_pairs(int* keys, int* vals, int64_t n, int64_t max_key, int* keys_out,
-                            int* vals_out, void* ws, hipStream_t s) {
+hipError_t radix_sort_segments(int* keys, int* vals, int64_t n, const int32_t* offsets, int F,
+                               int B, const int64_t* row_base, int64_t max_local_rows,
+                               int* keys_out, int* vals_out, void* ws, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int tiles = cdiv(n, SORT_TILE);
-  const size_t c = (size_t)RADIX * tiles;
+  const int tmax = seg_sort_tiles_max(n, F);
+  const size_t c = (size_t)RADIX * tmax;
   char* p = static_cast<char*>(ws);
   int* kb = reinterpret_cast<int*>(p); p += (size_t)n * sizeof(int);
   int* vb = reinterpret_cast<int*>(p); p += (size_t)n * sizeof(int);
   int* counts = reinterpret_cast<int*>(p); p += c * sizeof(int);
   int* offs = reinterpret_cast<int*>(p); p += c * sizeof(int);
-  int* tmp = reinterpret_cast<int*>(p);
+  int* tmp = reinterpret_cast<int*>(p); p += scan_workspace((int64_t)c);
+  int* tile_base = reinterpret_cast<int*>(p); p += (size_t)(F + 1) * sizeof(int);
+  int* tile_seg = reinterpret_cast<int*>(p);
 
-  const int bits = key_bits(max_key);
+  seg_ntiles_kernel<<<cdiv(F + 1, 256), 256, 0, s>>>(offsets, F, B, tile_base);
+  LAT_LAUNCH_CHECK();
+  hipError_t e = exclusive_scan_inplace_small(tile_base, F + 1, s);
+  if (e != hipSuccess) return e;
+  seg_tilemap_kernel<<<F, 256, 0, s>>>(tile_base, tile_seg);
+  LAT_LAUNCH_CHECK();
+
+  const int bits = key_bits(max_local_rows > 0 ? max_local_rows - 1 : 0);
   const int passes = bits == 0 ? 1 : (bits + RADIX_BITS - 1) / RADIX_BITS;
-  // ping-pong so that the final pass lands in keys_out / vals_out
+  const int dbits = bits == 0 ? 1 : (bits + passes - 1) / passes;
+  const int radix = 1 << dbits;
   int* src_k = keys; int* src_v = vals;
   for (int pass = 0; pass < passes; ++pass) {
     const bool last = pass == passes - 1;
-    // passes remaining after this one decide the buffer so the last is *_out
     const int remaining = passes - 1 - pass;
     int* dst_k = last ? keys_out : ((remaining % 2 == 1) ? kb : keys_out);
     int* dst_v = last ? vals_out : ((remaining % 2 == 1) ? vb : vals_out);
-    const int shift = pass * RADIX_BITS;
-    radix_hist_kernel<<<tiles, SORT_THREADS, 0, s>>>(src_k, (int)n, shift, tiles, counts);
+    const int shift = pass * dbits;
+    radix_hist_seg_kernel<<<tmax, SORT_THREADS, 0, s>>>(src_k, offsets, row_base, F, B, tile_base,
+                                                         tile_seg, shift, dbits, counts);
     LAT_LAUNCH_CHECK();
-    hipError_t e = exclusive_scan(counts, offs, (int64_t)c, tmp, s);
+    e = exclusive_scan(counts, offs, (int64_t)radix * tmax, tmp, s);
     if (e != hipSuccess) return e;
-    radix_scatter_kernel<<<tiles, SORT_THREADS, 0, s>>>(src_k, src_v, (int)n, shift, tiles, offs,
-                                                        dst_k, dst_v);
+    radix_scatter_seg_kernel<<<tmax, SORT_THREADS, 0, s>>>(src_k, src_v, offsets, row_base, F, B,
+                                                            tile_base, tile_seg, shift, dbits, offs,
+                                                            dst_k, dst_v);
     LAT_LAUNCH_CHECK();
     src_k = dst_k; src_v = dst_v;
   }

@@ -54,7 +54,8 @@ def test_exports_are_c_symbols():
 
 def test_host_queries_without_gpu(lib):
     lib.lattice_abi_version.restype = ctypes.c_int
-    assert lib.lattice_abi_version() == 1
+    version = int(re.search(r"#define LATTICE_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
+    assert lib.lattice_abi_version() == version
     lib.lattice_status_string.restype = ctypes.c_char_p
     lib.lattice_status_string.argtypes = [ctypes.c_int]
     msgs = {code: lib.lattice_status_string(code).decode() for code in _abi.STATUS}

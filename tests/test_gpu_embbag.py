@@ -143,6 +143,29 @@ def test_validate_batch():
     off[10] = off[11] + 1        # non-monotone
     ok, pos = api.lattice_validate_batch(w.E, w.row_base, off, w.indices, cfg.F, cfg.B)
     assert not ok and pos < 0
+    # a row bound smaller than the tables
+    ok, pos = api.lattice_validate_batch(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B,
+                                         max_rows=cfg.rows - 1)
+    assert not ok and pos == -1 - (cfg.F * cfg.B + 1)
+
+
+@pytest.mark.gpu
+def test_embbag_bwd_row_bound_only_changes_passes():
+    """The backward sorts each feature by its local row with as many digit
+    passes as max_rows needs; with max_rows unknown (0) it uses the total row
+    count (more passes).  Both must give identical results."""
+    from paper_2512_09200_amd import api
+    cfg = CASES["large-fm-small"]
+    w = Workload(cfg)
+    dX = torch.from_numpy(synth.randn((cfg.B, cfg.n_slots, cfg.d), seed=11, dtype=cfg.dtype)).to(
+        torch.bfloat16).to(DEV)
+    r1 = api.lattice_embbag_bwd(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B, dX, 1, max_rows=0)
+    r2 = api.lattice_embbag_bwd(w.E, w.row_base, w.offsets, w.indices, cfg.F, cfg.B, dX, 1)
+    torch.cuda.synchronize()
+    U = int(r1["num_unique"].item())
+    assert U == int(r2["num_unique"].item())
+    for k, n in (("unique_rows", U), ("seg_offsets", U + 1), ("sorted_bags", w.nnz), ("grad_rows", U)):
+        assert torch.equal(r1[k][:n], r2[k][:n]), k
 
 
 def _structured_bags(rng, F, B, rows):
