@@ -287,7 +287,10 @@ typedef enum {
   LATTICE_STAGE_TOP_BWD,
   LATTICE_STAGE_INTERACT_BWD,
   LATTICE_STAGE_BOTTOM_BWD,
-  LATTICE_STAGE_EMBBAG_BWD,
+  LATTICE_STAGE_EMBBAG_SORT,     /* sparse gradient: sort of (row, bag) pairs */
+  LATTICE_STAGE_EMBBAG_RUNS,     /* sparse gradient: unique rows and run offsets */
+  LATTICE_STAGE_EMBBAG_REDUCE,   /* sparse gradient: segmented reduction (+ SGD) */
+  LATTICE_STAGE_EMBBAG_FIXUP,    /* sparse gradient: runs crossing reduction ranges */
   LATTICE_STEP_STAGES
 } lattice_step_stage;
 

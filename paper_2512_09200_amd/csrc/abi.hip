@@ -738,8 +738,9 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                     m->pool == LATTICE_POOL_MEAN, dX, dt, n, s0, d, (int*)at(L.unique_rows),
                     (int*)at(L.seg_offsets), (int*)at(L.sorted_bags), (int*)at(L.num_unique),
                     (float*)at(L.grad_rows), m->tables.data, dt, opts->lr_tables, scratch, s,
-                    (const int*)at(L.keys), (const int*)at(L.vals)));
-  HIPRET(mark(9));
+                    (const int*)at(L.keys), (const int*)at(L.vals),
+                    opts->stage_events ? opts->stage_events + 9 : nullptr));
+  HIPRET(mark(LATTICE_STEP_STAGES));
   return LATTICE_OK;
 }
 

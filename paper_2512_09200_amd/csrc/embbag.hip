@@ -635,10 +635,9 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
                                     const int32_t* offsets, int mean, const int* range_ubefore,
                                     float* part, int* part_uid, int* span_list, int* span_count,
                                     const int* seg_offsets, const int* unique_rows,
-                                    float* grad_rows, void* E, float lr, hipStream_t s) {
+                                    float* grad_rows, void* E, float lr, hipStream_t s,
+                                    hipEvent_t ev_reduced) {
   const int ranges = cdiv(n, RANGE);
-  zero_int_kernel<<<1, 64, 0, s>>>(span_count, 1);
-  LAT_LAUNCH_CHECK();
   const int row_bytes = dim * (int)sizeof(DT);
   const int grid = cdiv(ranges, 4);
 #define LAT_SEG(BPLV, MV, FV)                                                               \
@@ -656,6 +655,7 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
   }
 #undef LAT_SEG
   LAT_LAUNCH_CHECK();
+  if (ev_reduced) LAT_HIP_CHECK(hipEventRecord(ev_reduced, s));
   const int fix_grid = grid < 2048 ? grid : 2048;
   seg_fixup_kernel<ET><<<fix_grid, 256, 0, s>>>(span_list, span_count, part_uid, seg_offsets,
                                                 unique_rows, part, dim, grad_rows, (ET*)E, lr);
@@ -668,10 +668,14 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int
                       const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
                       float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
-                      const int* keys_in, const int* vals_in) {
+                      const int* keys_in, const int* vals_in, void* const* sub_events) {
+  auto record = [&](int i) -> hipError_t {
+    return sub_events ? hipEventRecord((hipEvent_t)sub_events[i], s) : hipSuccess;
+  };
   if (nnz == 0) {
     set_empty_kernel<<<1, 1, 0, s>>>(num_unique, seg_offsets);
     LAT_LAUNCH_CHECK();
+    for (int i = 0; i < 3; ++i) LAT_HIP_CHECK(record(i));
     return hipSuccess;
   }
   const int n = (int)nnz;
@@ -705,7 +709,10 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int
   hipError_t e = radix_sort_segments(keys, vals, n, offsets, F, B, row_base, max_local_rows, skeys,
                                      sorted_bags, sort_ws, s);
   if (e != hipSuccess) return e;
+  LAT_HIP_CHECK(record(0));
   const int tiles = cdiv(n, SEG_TILE);
+  zero_int_kernel<<<1, 64, 0, s>>>(span_count, 1);
+  LAT_LAUNCH_CHECK();
   seg_count_kernel<<<tiles, SEG_THREADS, 0, s>>>(skeys, n, tile_counts);
   LAT_LAUNCH_CHECK();
   e = exclusive_scan_inplace_small(tile_counts, tiles, s);
@@ -713,11 +720,14 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int
   seg_write_kernel<<<tiles, SEG_THREADS, 0, s>>>(skeys, n, tile_counts, unique_rows, seg_offsets,
                                                  num_unique, range_ubefore);
   LAT_LAUNCH_CHECK();
+  LAT_HIP_CHECK(record(1));
   void* Eupd = lr != 0.f ? E : nullptr;
+  hipEvent_t ev_reduced = sub_events ? (hipEvent_t)sub_events[2] : nullptr;
 #define LAT_RED(DTT, ETT)                                                                     \
   return embbag_bwd_reduce<DTT, ETT>(skeys, sorted_bags, n, dX, B, n_slots, first_slot, dim,   \
                                      offsets, mean, range_ubefore, part, part_uid, span_list,  \
-                                     span_count, seg_offsets, unique_rows, grad_rows, Eupd, lr, s)
+                                     span_count, seg_offsets, unique_rows, grad_rows, Eupd, lr, s, \
+                                     ev_reduced)
   if (dxt == DT_BF16 && et == DT_BF16) LAT_RED(bf16_t, bf16_t);
   if (dxt == DT_BF16 && et == DT_F32) LAT_RED(bf16_t, float);
   if (dxt == DT_F32 && et == DT_BF16) LAT_RED(float, bf16_t);

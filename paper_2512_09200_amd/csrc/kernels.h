@@ -30,7 +30,8 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int
                       const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
                       float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
-                      const int* keys_in = nullptr, const int* vals_in = nullptr);
+                      const int* keys_in = nullptr, const int* vals_in = nullptr,
+                      void* const* sub_events = nullptr);  // 3 hipEvent_t: after sort, runs, reduce
 hipError_t validate_batch(const int64_t* row_base, const int32_t* offsets,
                           const int32_t* indices, int F, int B, int64_t nnz, int64_t max_rows,
                           unsigned long long* dev_result, hipStream_t s);
