@@ -51,9 +51,14 @@ def run_step(w, lr, emit=True, spare=0):
 def test_step_matches_oracle(name):
     cfg, lr = CASES[name]
     print(f"[step] {name} B={cfg.B} F={cfg.F} rows={cfg.rows} lr={lr}", flush=True)
+    check_step(cfg, lr, spare=SPARE.get(name, 0))
+
+
+def check_step(cfg, lr, spare=0):
+    """Whole-batch comparison of one lattice_step with the oracle."""
     w = Workload(cfg)
     E0 = w.table_np()
-    _, v, _ = run_step(w, lr, spare=SPARE.get(name, 0))
+    _, v, _ = run_step(w, lr, spare=spare)
     t = tol(cfg)
     s0 = cfg.first_emb_slot
     ov, nband, nflip = relu_overrides(cfg, w.params, E0, w.batch, *gpu_relu_io(cfg, w, v))
