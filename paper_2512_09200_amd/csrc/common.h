@@ -25,18 +25,28 @@ __host__ __device__ inline float bf2f(bf16_t h) {
   return v.f;
 }
 
-// fp32 -> bf16, round to nearest even; NaN stays NaN.
+// fp32 -> bf16, round to nearest even; NaN stays NaN.  On the GPU this is the
+// hardware conversion (v_cvt_pk_bf16_f32 on gfx950); the host keeps the
+// bit-level rounding.
 __host__ __device__ inline bf16_t f2bf(float f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_bit_cast(bf16_t, (__bf16)f);
+#else
   union { uint32_t u; float f; } v;
   v.f = f;
   uint32_t u = v.u;
   if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
   u += 0x7fffu + ((u >> 16) & 1u);
   return (bf16_t)(u >> 16);
+#endif
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// two fp32 -> two bf16 in one 32-bit word (a in the low half), one instruction
 __device__ inline uint32_t pack_bf2(float a, float b) {
-  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
 
 template <typename T> struct Elt;
@@ -99,6 +109,9 @@ inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 // that are neighbours in the renumbered order share one L2.  A bijection on
 // [0, nblocks).
 constexpr int NUM_XCD = 8;
+
+// Word 3 of a raw (untyped, unswizzled) buffer resource on gfx9-family GPUs.
+constexpr int BUF_RSRC_WORD3 = 0x00020000;
 __device__ inline int xcd_block(int bid, int nblocks) {
   const int x = bid % NUM_XCD, i = bid / NUM_XCD;
   const int q = nblocks / NUM_XCD, r = nblocks % NUM_XCD;

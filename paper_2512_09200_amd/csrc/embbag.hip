@@ -52,12 +52,30 @@ struct Frag {
       }
     }
   }
+  // streaming (non-temporal) access: data touched once, kept out of the caches' way
+  __device__ inline void load_nt(const T* p) {
+    if constexpr (NB == 4) {
+      w[0] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
+    } else {
+      load(p);
+    }
+  }
   // element i as fp32
   __device__ inline float get(int i) const {
     if constexpr (sizeof(T) == 2)
       return __uint_as_float((i & 1) ? (w[i >> 1] & 0xffff0000u) : (w[i >> 1] << 16));
     else
       return __uint_as_float(w[i]);
+  }
+  // stores v[0..N) rounded to T, non-temporal where the width allows
+  __device__ static inline void store_nt(T* p, const float* v) {
+    if constexpr (NB == 4 && sizeof(T) == 2) {
+      __builtin_nontemporal_store(pack_bf2(v[0], v[1]), reinterpret_cast<uint32_t*>(p));
+    } else if constexpr (NB == 4) {
+      __builtin_nontemporal_store(__float_as_uint(v[0]), reinterpret_cast<uint32_t*>(p));
+    } else {
+      store(p, v);
+    }
   }
   // stores v[0..N) rounded to T
   __device__ static inline void store(T* p, const float* v) {
@@ -99,11 +117,13 @@ __device__ inline void fwd_group(int s0, int cnt, uint64_t emask, int grow, int 
                                  const char* Eb, int64_t row_bytes, int lane_b, XT* X, int dim,
                                  int col, bool active, float* acc) {
   Frag<TT, EPL> xf[S];
+  const uint64_t em = emask >> s0;  // the group's bag ends at positions 0 .. S-1
 #pragma unroll
   for (int i = 0; i < S; ++i) {
     const int r = s0 + i;
     if (CHECK && r >= cnt) break;
-    const char* rowp = Eb + (int64_t)__builtin_amdgcn_readlane(grow, r) * row_bytes;
+    const int gr = __builtin_amdgcn_readlane(grow, r);
+    const char* rowp = Eb + (FULL ? ((int64_t)gr << 8) : (int64_t)gr * row_bytes);
     if (FULL || active) xf[i].load(reinterpret_cast<const TT*>(rowp + lane_b));
   }
 #pragma unroll
@@ -112,7 +132,7 @@ __device__ inline void fwd_group(int s0, int cnt, uint64_t emask, int grow, int 
     if (CHECK && r >= cnt) break;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[e] += xf[i].get(e);
-    if ((emask >> r) & 1) {
+    if ((em >> i) & 1) {
       if (MEAN) {
         const float il = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(inv_len), r));
 #pragma unroll
@@ -399,22 +419,31 @@ struct SegWave {
   // key: per-lane global row.
   template <bool CHECK>
   __device__ inline void group(int s0, int cnt, uint64_t smask, uint64_t cmask, uint64_t pmask,
-                               int xoff, int key, float scl, const char* dXb, ET* E,
-                               float* grad_rows, float* part, int wave, int dim, int lane_b,
-                               int col, bool active, float lr) {
+                               int xoff, int key, float scl, const char* dXb,
+                               __amdgpu_buffer_rsrc_t dXr, ET* E, float* grad_rows, float* part,
+                               int wave, int dim, int lane_b, int col, bool active, float lr) {
     Frag<DT, EPL> xf[S];
     Frag<ET, EPL> ef[S];
     const int lane_e = col * (int)sizeof(ET);
+    // the group's run bits at positions 0 .. S-1 (constant-position tests below)
+    const uint64_t sm = smask >> s0, cm = cmask >> s0, pm = pmask >> s0;
 #pragma unroll
     for (int i = 0; i < S; ++i) {
       const int r = s0 + i;
       if (CHECK && r >= cnt) break;
-      const char* rowp = dXb + (uint32_t)__builtin_amdgcn_readlane(xoff, r);
-      if (FULL || active) xf[i].load(reinterpret_cast<const DT*>(rowp + lane_b));
-      if (E && ((cmask >> r) & 1)) {
+      const int xr = __builtin_amdgcn_readlane(xoff, r);
+      if constexpr (FULL) {
+        // 256-byte rows: one dword per lane, scalar row offset (buffer load)
+        xf[i].w[0] = __builtin_amdgcn_raw_buffer_load_b32(dXr, lane_b, xr, 0);
+      } else {
+        if (active) xf[i].load(reinterpret_cast<const DT*>(dXb + (uint32_t)xr + lane_b));
+      }
+      if (E && ((cm >> i) & 1)) {
+        const int kr = __builtin_amdgcn_readlane(key, r);
         const char* erow = reinterpret_cast<const char*>(E) +
-                           (int64_t)__builtin_amdgcn_readlane(key, r) * dim * (int64_t)sizeof(ET);
-        if (FULL || active) ef[i].load(reinterpret_cast<const ET*>(erow + lane_e));
+                           (FULL ? ((int64_t)kr << 8) : (int64_t)kr * dim * (int64_t)sizeof(ET));
+        // each occurring table row is read and written exactly once: streamed
+        if (FULL || active) ef[i].load_nt(reinterpret_cast<const ET*>(erow + lane_e));
       }
     }
 #pragma unroll
@@ -423,23 +452,27 @@ struct SegWave {
       if (CHECK && r >= cnt) break;
       float sc = 1.f;
       if (MEAN) sc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scl), r));
-      const bool st = (smask >> r) & 1;
+      // running sum, restarted at a run start: acc * keep + v with keep = 0 or 1
+      // (exact for finite values in both cases)
+      const float keep = ((sm >> i) & 1) ? 0.f : 1.f;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
         const float v = MEAN ? xf[i].get(e) * sc : xf[i].get(e);
-        acc[e] = st ? v : acc[e] + v;
+        acc[e] = __builtin_fmaf(acc[e], keep, v);
       }
-      if ((pmask >> r) & 1) {
+      if ((pm >> i) & 1) {
         const uint64_t le = (r == 63) ? ~0ull : ((2ull << r) - 1);
-        if ((cmask >> r) & 1) {
+        if ((cm >> i) & 1) {
           if (grad_rows && (FULL || active))
             Frag<float, EPL>::store(grad_rows + (int64_t)(u_before + __popcll(smask & le)) * dim + col, acc);
           if (E) {
             float upd[EPL];
 #pragma unroll
             for (int e = 0; e < EPL; ++e) upd[e] = ef[i].get(e) - lr * acc[e];
-            ET* erow = E + (int64_t)__builtin_amdgcn_readlane(key, r) * dim;
-            if (FULL || active) Frag<ET, EPL>::store(erow + col, upd);
+            const int kr = __builtin_amdgcn_readlane(key, r);
+            ET* erow = FULL ? reinterpret_cast<ET*>(reinterpret_cast<char*>(E) + ((int64_t)kr << 8))
+                            : E + (int64_t)kr * dim;
+            if (FULL || active) Frag<ET, EPL>::store_nt(erow + col, upd);
           }
         } else {
           const bool has_start = started || (smask & le);
@@ -474,6 +507,12 @@ __global__ __launch_bounds__(256) void seg_reduce_kernel(
   const int lane_b = lane * BPL;
   const int row_bytes = dim * (int)sizeof(DT);
   const char* dXb = reinterpret_cast<const char*>(dX);
+  // dX as a buffer of B*n_slots*dim elements (< 4 GiB, checked by the launcher)
+  const __amdgpu_buffer_rsrc_t dXr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<DT*>(dX), (short)0,
+      (int)(uint32_t)((uint64_t)B * n_slots * dim * sizeof(DT) < 0xffffffffull
+                          ? (uint64_t)B * n_slots * dim * sizeof(DT) : 0xffffffffull),
+      BUF_RSRC_WORD3);
 
   W w;
 #pragma unroll
@@ -525,10 +564,10 @@ __global__ __launch_bounds__(256) void seg_reduce_kernel(
     }
     int s0 = 0;
     for (; s0 + S <= cnt; s0 += S)
-      w.template group<false>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, E, grad_rows,
+      w.template group<false>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, dXr, E, grad_rows,
                               part, wave, dim, lane_b, col, active, lr);
     if (s0 < cnt)
-      w.template group<true>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, E, grad_rows,
+      w.template group<true>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, dXr, E, grad_rows,
                              part, wave, dim, lane_b, col, active, lr);
     w.started = w.started || smask != 0;
     prev_key = __builtin_amdgcn_readlane(key, cnt - 1);

@@ -215,16 +215,18 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
       zero16(acc);
       mfma_tile<2 * K>(acc, GW + tj * 32 * LG, LG, PD + ta * 32 * LPD, LPD);
       const int a = ta * 32 + (lane & 31);
+      const int64_t sbase = (int64_t)b * n * D;  // this sample's [n, D] block
+      const float g0 = (emit0 && tj == 0) ? bf2f(gb[a]) : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = tj * 32 + frag_row(r);
         if (j < n) {
           float v = acc[r];
-          const int64_t idx = ((int64_t)b * n + j) * D + a;
-          if (addend) v += addend[idx];
-          if (emit0 && j == 0) v += bf2f(gb[a]);
-          if (dX_f32) dX_f32[idx] = v;
-          else dX[idx] = f2bf(v);
+          const int e = j * D + a;
+          if (addend) v += addend[sbase + e];
+          if (j == 0) v += g0;
+          if (dX_f32) dX_f32[sbase + e] = v;
+          else dX[sbase + e] = f2bf(v);
         }
       }
     }
