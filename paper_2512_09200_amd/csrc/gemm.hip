@@ -134,13 +134,14 @@ __device__ inline int64_t koff(const Opnd& o, int k) {
 // K-contiguous, 16-byte vectors: 128 rows x 64 k = 8 vectors per row, 4 per thread.
 struct LoadK {
   u32x4 r[4];
-  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0) {
+  // edge: the tile may reach past R rows or K columns (uniform per block and step)
+  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool edge) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int v = threadIdx.x + i * 256;
       const int rr = v >> 3, kc = (v & 7) * 8;
       const int gr = r0 + rr, gk = k0 + kc;
-      if (gr < R && gk < K) r[i] = ldg16(o.p + (int64_t)gr * o.ld + koff<false>(o, gk));
+      if (!edge || (gr < R && gk < K)) r[i] = ldg16(o.p + (int64_t)gr * o.ld + koff<false>(o, gk));
       else r[i] = u32x4{0, 0, 0, 0};
     }
   }
@@ -159,13 +160,13 @@ struct LoadK {
 // each of 16 k-rows, and the 16 lanes of a group write one row's 128 bytes.
 struct LoadMN {
   u32x4 r[4];
-  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0) {
+  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool edge) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int gr = r0 + (4 * w + (lane >> 4)) * 8, kb = k0 + (lane & 15) * 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int gk = kb + i;
-      if (gk < K && gr < R) r[i] = ldg16(o.p + koff<true>(o, gk) + gr);
+      if (!edge || (gk < K && gr < R)) r[i] = ldg16(o.p + koff<true>(o, gk) + gr);
       else r[i] = u32x4{0, 0, 0, 0};
     }
   }
@@ -186,7 +187,7 @@ struct LoadMN {
 template <bool MN>
 struct LoadElem {
   bf16_t r[32];
-  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0) {
+  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool /*edge*/) {
 #pragma unroll
     for (int i = 0; i < 32; ++i) {
       const int e = threadIdx.x + i * 256;
@@ -267,14 +268,16 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   typename LoaderSel<TA, VA>::T la0, la1;
   typename LoaderSel<TB, VB>::T lb0, lb1;
   const int ktiles = kend > kbeg ? (kend - kbeg + GBK - 1) / GBK : 0;
-  if (ktiles > 0) {
-    la0.load(A, M, kend, m0, kbeg);
-    lb0.load(Bm, N, kend, n0, kbeg);
-  }
-  if (ktiles > 1) {
-    la1.load(A, M, kend, m0, kbeg + GBK);
-    lb1.load(Bm, N, kend, n0, kbeg + GBK);
-  }
+  // tiles reaching past the matrix edge take the checked loads (uniform)
+  const bool edge_m = m0 + GBM > M, edge_n = n0 + GBN > N;
+  auto load = [&](auto& la, auto& lb, int kt) {
+    const int k0 = kbeg + kt * GBK;
+    const bool edge_k = k0 + GBK > kend;
+    la.load(A, M, kend, m0, k0, edge_m || edge_k);
+    lb.load(Bm, N, kend, n0, k0, edge_n || edge_k);
+  };
+  if (ktiles > 0) load(la0, lb0, 0);
+  if (ktiles > 1) load(la1, lb1, 1);
   if (ktiles > 0) {
     la0.store(As[0]);
     lb0.store(Bs[0]);
@@ -282,27 +285,25 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   __syncthreads();
   // Two register stages and two LDS stages: while the MFMAs consume LDS stage
   // s, the registers of the other stage receive the tile two steps ahead.
-  for (int kt = 0; kt < ktiles; kt += 2) {
-    if (kt + 2 < ktiles) {
-      la0.load(A, M, kend, m0, kbeg + (kt + 2) * GBK);
-      lb0.load(Bm, N, kend, n0, kbeg + (kt + 2) * GBK);
-    }
+  // The loop body is two steps with no early exit (so the accumulators keep
+  // their registers); an odd last step follows the loop.
+  int kt = 0;
+  for (; kt + 2 <= ktiles; kt += 2) {
+    if (kt + 2 < ktiles) load(la0, lb0, kt + 2);
     mma_k64(As[0], Bs[0], wm, wn, lane, acc);
-    if (kt + 1 < ktiles) {
-      la1.store(As[1]);
-      lb1.store(Bs[1]);
-    }
+    la1.store(As[1]);
+    lb1.store(Bs[1]);
     __syncthreads();
-    if (kt + 1 >= ktiles) break;
-    if (kt + 3 < ktiles) {
-      la1.load(A, M, kend, m0, kbeg + (kt + 3) * GBK);
-      lb1.load(Bm, N, kend, n0, kbeg + (kt + 3) * GBK);
-    }
+    if (kt + 3 < ktiles) load(la1, lb1, kt + 3);
     mma_k64(As[1], Bs[1], wm, wn, lane, acc);
     if (kt + 2 < ktiles) {
       la0.store(As[0]);
       lb0.store(Bs[0]);
     }
+    __syncthreads();
+  }
+  if (kt < ktiles) {
+    mma_k64(As[0], Bs[0], wm, wn, lane, acc);
     __syncthreads();
   }
 
