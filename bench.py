@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--cpu-sample", type=int, default=2048, help="samples in the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--uniform", action="store_true", help="uniform indices (control run)")
+    ap.add_argument("--single-stream", action="store_true",
+                    help="run the sparse gradient's sort on the step's stream (no overlap)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, stream 1 GiB through a plain elementwise kernel "
                          "(torch.neg, 1 GiB read + 1 GiB written) as a counter calibration point")
@@ -119,7 +121,8 @@ def main():
     def step(i, events=None):
         b = batches[i % len(batches)]
         api.lattice_step(model, b["offsets"], b["indices"], b["dense"], b["labels"], b["mask"], ws,
-                         cfg.lr_tables, False, stage_events=events, nnz_capacity=nnz_max)
+                         cfg.lr_tables, False, stage_events=events, nnz_capacity=nnz_max,
+                         single_stream=args.single_stream)
 
     for i in range(args.warmup):
         step(i)
@@ -127,7 +130,8 @@ def main():
     log("[bench] warmup done")
 
     nst = len(STAGES)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(args.steps)]
+    # begin / end event of every stage, recorded on the stream that runs it
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nst)] for _ in range(args.steps)]
     for es in ev:          # create the underlying events before handing them to the library
         for e in es:
             e.record()
@@ -138,7 +142,8 @@ def main():
     torch.cuda.synchronize()
     t_total = time.perf_counter() - t_start
     ms_per_step = 1e3 * t_total / args.steps
-    stage_ms = {s: float(np.mean([ev[i][k].elapsed_time(ev[i][k + 1]) for i in range(args.steps)]))
+    stage_ms = {s: float(np.mean([ev[i][2 * k].elapsed_time(ev[i][2 * k + 1])
+                                  for i in range(args.steps)]))
                 for k, s in enumerate(STAGES)}
     log("[bench] stage ms: " + ", ".join(f"{k}={v:.3f}" for k, v in stage_ms.items()))
 
@@ -216,7 +221,8 @@ def main():
                    "rows_per_table": cfg.rows, "dim": cfg.d,
                    "index_dist": list(cfg.index_dist), "bag_dist": list(cfg.bag_dist),
                    "interaction": cfg.interact, "top": list(cfg.top), "lr_tables": cfg.lr_tables,
-                   "nnz_per_step": int(nnz), "unique_rows_last_step": U, "parallelism": "single-gpu"},
+                   "nnz_per_step": int(nnz), "unique_rows_last_step": U, "parallelism": "single-gpu",
+                   "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,
         "gather_roofline": gather_roofline,
         "embbag_fwd_GBps": round(fwd_gbs, 1), "embbag_bwd_GBps": round(bwd_gbs, 1),

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 2
+#define LATTICE_ABI_VERSION 3
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -294,14 +294,28 @@ typedef enum {
   LATTICE_STEP_STAGES
 } lattice_step_stage;
 
+/* Streams.  The sort and run bookkeeping of the sparse gradient need only
+ * the batch, so by default lattice_step runs them on a library-owned side
+ * stream of the caller's device (non-blocking, default priority, one per
+ * device, created on first use and kept until the process ends), forked from
+ * the caller's stream after the pooled lookups and joined back before the
+ * segmented reduction; they overlap the dense forward and backward.  All
+ * work is still ordered after the caller's prior work on `stream`, and the
+ * call's work is complete when `stream` reaches the end of it, as with a
+ * single stream.  Concurrent calls (any threads) share the side stream and
+ * serialise their sparse stages on it.  single_stream = 1 keeps every stage
+ * on the caller's stream; results are identical either way. */
 typedef struct {
   float lr_tables;             /* row-sparse SGD step on the tables (0: none) */
   int32_t emit_grad_rows;      /* 1: also write the [nnz, dim] fp32 row gradients */
   int64_t nnz_capacity;        /* lookups the workspace is planned for (0: the batch's nnz);
                                   plan and step must use the same value */
-  void* const* stage_events;   /* host array of LATTICE_STEP_STAGES+1 hipEvent_t or NULL:
-                                  [0] is recorded before the first stage and [s+1]
-                                  after stage s, on the step's stream */
+  void* const* stage_events;   /* host array of 2*LATTICE_STEP_STAGES hipEvent_t or NULL:
+                                  [2s] is recorded when stage s begins and [2s+1] when
+                                  it ends, on the stream that runs the stage (the side
+                                  stream for EMBBAG_SORT and EMBBAG_RUNS unless
+                                  single_stream) */
+  int32_t single_stream;       /* 1: no side stream (see above) */
 } lattice_step_opts;
 
 /* Byte offsets of every intermediate inside the step workspace (-1: absent). */
@@ -321,8 +335,10 @@ typedef struct {
   int64_t unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows;
   int64_t keys, vals;   /* [nnz] int32: sort keys (global row) and bag ids, built by the forward */
   int64_t interact;     /* interaction workspace (saved state from forward to backward) */
-  int64_t scratch;      /* shared scratch of the stages */
+  int64_t scratch;      /* scratch shared by the dense stages */
   int64_t scratch_bytes;
+  int64_t sparse;       /* scratch of the sparse gradient (sort, runs, reduction) */
+  int64_t sparse_bytes;
 } lattice_step_layout;
 
 /* Workspace layout for batches of B samples and at most

@@ -74,7 +74,7 @@ class lattice_batch_desc(Structure):
 
 class lattice_step_opts(Structure):
     _fields_ = [("lr_tables", c_float), ("emit_grad_rows", c_int32), ("nnz_capacity", c_int64),
-                ("stage_events", POINTER(c_void_p))]
+                ("stage_events", POINTER(c_void_p)), ("single_stream", c_int32)]
 
 
 STAGES = ["embbag_fwd", "bottom_fwd", "interact_fwd", "top_fwd", "loss", "top_bwd",
@@ -89,7 +89,7 @@ class lattice_step_layout(Structure):
                  ("bottom_act", c_int64 * MAX_LAYERS), ("top_act", c_int64 * MAX_LAYERS)]
                 + [(k, c_int64) for k in ("unique_rows", "seg_offsets", "sorted_bags",
                                           "num_unique", "grad_rows", "keys", "vals", "interact", "scratch",
-                                          "scratch_bytes")])
+                                          "scratch_bytes", "sparse", "sparse_bytes")])
 
 
 # (name, restype, argtypes)

@@ -271,11 +271,14 @@ def lattice_step_plan(model, B, nnz, lr_tables=0.0, emit_grad_rows=False):
 
 
 def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0,
-                 emit_grad_rows=False, stream=None, stage_events=None, nnz_capacity=0):
+                 emit_grad_rows=False, stream=None, stage_events=None, nnz_capacity=0,
+                 single_stream=False):
     """One forward+backward step; ws is a uint8 device tensor of at least
     lattice_step_plan(...).total_bytes.  stage_events: optional list of
-    len(STAGES)+1 torch.cuda.Event(enable_timing=True) recorded between the
-    stages on the step's stream."""
+    2*len(STAGES) torch.cuda.Event(enable_timing=True): [2s] and [2s+1] are
+    recorded when stage s begins and ends, on the stream that runs it.
+    single_stream: keep the sparse gradient's sort on the step's stream
+    instead of the library's side stream."""
     lib = load()
     _contig(dense, labels, mask, ws)
     B = labels.shape[0]
@@ -283,10 +286,11 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
                                  dense=dense.data_ptr() if dense is not None and dense.numel() else None,
                                  labels=labels.data_ptr(), mask=mask.data_ptr())
     opts = A.lattice_step_opts(lr_tables=float(lr_tables), emit_grad_rows=int(emit_grad_rows),
-                               nnz_capacity=int(nnz_capacity or indices.numel()))
+                               nnz_capacity=int(nnz_capacity or indices.numel()),
+                               single_stream=int(bool(single_stream)))
     if stage_events is not None:
-        if len(stage_events) != len(A.STAGES) + 1:
-            raise ValueError("need len(STAGES)+1 events")
+        if len(stage_events) != 2 * len(A.STAGES):
+            raise ValueError("need 2*len(STAGES) events")
         arr = (ctypes.c_void_p * len(stage_events))(*[e.cuda_event for e in stage_events])
         opts.stage_events = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
     check(lib.lattice_step(byref(model.desc), byref(batch), byref(opts), _p(ws), ws.numel(),

@@ -619,12 +619,53 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
   sc = std::max(sc, bce_workspace((int64_t)B * P->T));
   L.interact = take(interact_ws(&m->interact, B));
-  sc = std::max(sc, embbag_bwd_workspace(nnz, d, m->num_features));
   L.scratch = take(sc);
   L.scratch_bytes = (int64_t)sc;
+  // the sparse gradient's scratch is its own: its first half may run on the
+  // side stream while the dense stages use `scratch`
+  const size_t sp = embbag_bwd_workspace(nnz, d, m->num_features);
+  L.sparse = take(sp);
+  L.sparse_bytes = (int64_t)sp;
   L.total_bytes = off;
   return LATTICE_OK;
 }
+
+// Side stream of each device for the sparse gradient's sort and run
+// bookkeeping, with its fork / join events.  Created on first use, kept until
+// the process ends; g_side_mu serialises every use.
+namespace {
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_side_mu;
+SideStream g_side[kMaxDevices];
+
+// Requires g_side_mu held.
+lattice_status side_stream_of(hipStream_t main, SideStream** out) {
+  hipDevice_t dev = 0;
+  if (hipStreamGetDevice(main, &dev) != hipSuccess)
+    FAIL(LATTICE_ERR_HIP, "hipStreamGetDevice failed");
+  REQUIRE(dev >= 0 && dev < kMaxDevices, "device %d out of range", (int)dev);
+  SideStream& ss = g_side[dev];
+  if (!ss.s) {
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipGetDevice failed");
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipSetDevice failed");
+    hipError_t e = hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming);
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess) {
+      ss = SideStream{};  // handles of a failed set-up stay unused
+      FAIL(LATTICE_ERR_HIP, "side stream set-up failed: %s", hipGetErrorString(e));
+    }
+  }
+  *out = &ss;
+  return LATTICE_OK;
+}
+}  // namespace
 
 extern "C" {
 
@@ -661,8 +702,13 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   if (B == 0) return LATTICE_OK;
 
   hipStream_t s = strm(stream);
-  auto mark = [&](int i) -> hipError_t {
-    return opts->stage_events ? hipEventRecord((hipEvent_t)opts->stage_events[i], s) : hipSuccess;
+  void* const* ev = opts->stage_events;
+  auto stage_ev = [&](int i) -> void* const* { return ev ? ev + 2 * i : nullptr; };
+  auto begin = [&](int i) -> hipError_t {
+    return ev ? hipEventRecord((hipEvent_t)ev[2 * i], s) : hipSuccess;
+  };
+  auto end = [&](int i) -> hipError_t {
+    return ev ? hipEventRecord((hipEvent_t)ev[2 * i + 1], s) : hipSuccess;
   };
   char* base = (char*)ws;
   auto at = [&](int64_t o) -> void* { return o < 0 ? nullptr : base + o; };
@@ -673,14 +719,40 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   void* X = at(L.X);
   void* t = at(L.t);
   void* scratch = at(L.scratch);
+  void* sparse = at(L.sparse);
+  const int64_t nnz = batch->bags.nnz;
+  // first half of the sparse gradient: sort of the forward's (row, bag)
+  // pairs, unique rows and run offsets (stages EMBBAG_SORT and EMBBAG_RUNS)
+  auto sparse_sort = [&](hipStream_t on) -> hipError_t {
+    return embbag_bwd_sort(m->tables.row_base, local_rows_bound(&m->tables), batch->bags.offsets,
+                           batch->bags.indices, m->num_features, B, nnz, d,
+                           (int*)at(L.unique_rows), (int*)at(L.seg_offsets),
+                           (int*)at(L.sorted_bags), (int*)at(L.num_unique), sparse, on,
+                           (const int*)at(L.keys), (const int*)at(L.vals),
+                           stage_ev(LATTICE_STAGE_EMBBAG_SORT));
+  };
 
-  HIPRET(mark(0));
   // 1. pooled lookups -> embedding slots of X
+  HIPRET(begin(LATTICE_STAGE_EMBBAG_FWD));
   HIPRET(embbag_fwd(m->tables.data, dt, d, m->tables.row_base, batch->bags.offsets,
                     batch->bags.indices, m->num_features, B, m->pool == LATTICE_POOL_MEAN, X, dt,
                     n, s0, s, (int*)at(L.keys), (int*)at(L.vals)));
-  HIPRET(mark(1));
+  HIPRET(end(LATTICE_STAGE_EMBBAG_FWD));
+  // fork: the sort and run bookkeeping go to the side stream, overlapping
+  // the dense stages; the lock is held until the join is enqueued
+  std::unique_lock<std::mutex> lock(g_side_mu, std::defer_lock);
+  SideStream* side = nullptr;
+  if (!opts->single_stream) {
+    lock.lock();
+    st = side_stream_of(s, &side);
+    if (st != LATTICE_OK) return st;
+    HIPRET(hipEventRecord(side->fork, s));
+    HIPRET(hipStreamWaitEvent(side->s, side->fork, 0));
+    HIPRET(sparse_sort(side->s));
+    HIPRET(hipEventRecord(side->join, side->s));
+  }
   // 2. bottom MLP -> slot 0 of X
+  HIPRET(begin(LATTICE_STAGE_BOTTOM_FWD));
   void* bacts[LATTICE_MAX_LAYERS];
   int64_t bstr[LATTICE_MAX_LAYERS];
   if (m->dense_in > 0) {
@@ -693,11 +765,13 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     bstr[nb - 1] = (int64_t)n * d;
     HIPRET(mlp_forward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, s));
   }
-  HIPRET(mark(2));
+  HIPRET(end(LATTICE_STAGE_BOTTOM_FWD));
   // 3. interaction -> top input t = [X[:,0,:], interaction]
+  HIPRET(begin(LATTICE_STAGE_INTERACT_FWD));
   HIPRET(interact_fwd_impl(&m->interact, B, X, t, P.t_stride, at(L.interact), s));
-  HIPRET(mark(3));
+  HIPRET(end(LATTICE_STAGE_INTERACT_FWD));
   // 4. top MLP -> logits; 5. masked BCE
+  HIPRET(begin(LATTICE_STAGE_TOP_FWD));
   const int nt = m->top.n_layers;
   void* tacts[LATTICE_MAX_LAYERS];
   int64_t tstr[LATTICE_MAX_LAYERS];
@@ -708,19 +782,23 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   tacts[nt - 1] = at(L.logits);
   tstr[nt - 1] = T;
   HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, s));
-  HIPRET(mark(4));
+  HIPRET(end(LATTICE_STAGE_TOP_FWD));
+  HIPRET(begin(LATTICE_STAGE_LOSS));
   HIPRET(bce((const float*)at(L.logits), batch->labels, batch->mask, (int64_t)B * T,
              (float*)at(L.loss), (float*)at(L.d_logits), at(L.d_logits_op), dt, scratch, s));
-  HIPRET(mark(5));
+  HIPRET(end(LATTICE_STAGE_LOSS));
   // 6. top backward -> d_t
+  HIPRET(begin(LATTICE_STAGE_TOP_BWD));
   HIPRET(mlp_backward(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, at(L.d_t),
                       P.t_stride, at(P.g_top[0]), at(P.g_top[1]), scratch, s));
-  HIPRET(mark(6));
+  HIPRET(end(LATTICE_STAGE_TOP_BWD));
   // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
+  HIPRET(begin(LATTICE_STAGE_INTERACT_BWD));
   void* dX = at(L.dX);
   HIPRET(interact_bwd_impl(&m->interact, B, X, at(L.d_t), P.t_stride, dX, at(L.interact), s));
-  HIPRET(mark(7));
+  HIPRET(end(LATTICE_STAGE_INTERACT_BWD));
   // 8. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
+  HIPRET(begin(LATTICE_STAGE_BOTTOM_BWD));
   if (m->dense_in > 0) {
     void* masked = at(P.g_bot[1]);
     relu_mask_kernel<<<cdiv((int64_t)B * d, 256), 256, 0, s>>>(dX, (int64_t)n * d, X,
@@ -731,16 +809,19 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     HIPRET(mlp_backward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, masked, d,
                         nullptr, 0, at(P.g_bot[0]), at(P.g_top[0]), scratch, s));
   }
-  HIPRET(mark(8));
-  // 9. row-coalesced embedding gradient (+ row-sparse SGD)
-  HIPRET(embbag_bwd(m->tables.row_base, local_rows_bound(&m->tables), batch->bags.offsets,
-                    batch->bags.indices, m->num_features, B, batch->bags.nnz,
-                    m->pool == LATTICE_POOL_MEAN, dX, dt, n, s0, d, (int*)at(L.unique_rows),
-                    (int*)at(L.seg_offsets), (int*)at(L.sorted_bags), (int*)at(L.num_unique),
-                    (float*)at(L.grad_rows), m->tables.data, dt, opts->lr_tables, scratch, s,
-                    (const int*)at(L.keys), (const int*)at(L.vals),
-                    opts->stage_events ? opts->stage_events + 9 : nullptr));
-  HIPRET(mark(LATTICE_STEP_STAGES));
+  HIPRET(end(LATTICE_STAGE_BOTTOM_BWD));
+  // 9. row-coalesced embedding gradient (+ row-sparse SGD): join, then reduce
+  if (side) {
+    HIPRET(hipStreamWaitEvent(s, side->join, 0));
+    lock.unlock();
+  } else {
+    HIPRET(sparse_sort(s));
+  }
+  HIPRET(embbag_bwd_apply(batch->bags.offsets, m->num_features, B, nnz,
+                          m->pool == LATTICE_POOL_MEAN, dX, dt, n, s0, d,
+                          (const int*)at(L.unique_rows), (const int*)at(L.seg_offsets),
+                          (const int*)at(L.sorted_bags), (float*)at(L.grad_rows), m->tables.data,
+                          dt, opts->lr_tables, sparse, s, stage_ev(LATTICE_STAGE_EMBBAG_REDUCE)));
   return LATTICE_OK;
 }
 

@@ -675,8 +675,13 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
                                     float* part, int* part_uid, int* span_list, int* span_count,
                                     const int* seg_offsets, const int* unique_rows,
                                     float* grad_rows, void* E, float lr, hipStream_t s,
-                                    hipEvent_t ev_reduced) {
+                                    void* const* ev) {
+  // ev (optional): 4 events, begin / end of the reduction and of the fixup
+  auto record = [&](int i) -> hipError_t {
+    return ev ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
+  };
   const int ranges = cdiv(n, RANGE);
+  LAT_HIP_CHECK(record(0));
   const int row_bytes = dim * (int)sizeof(DT);
   const int grid = cdiv(ranges, 4);
 #define LAT_SEG(BPLV, MV, FV)                                                               \
@@ -694,49 +699,64 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
   }
 #undef LAT_SEG
   LAT_LAUNCH_CHECK();
-  if (ev_reduced) LAT_HIP_CHECK(hipEventRecord(ev_reduced, s));
+  LAT_HIP_CHECK(record(1));
+  LAT_HIP_CHECK(record(2));
   const int fix_grid = grid < 2048 ? grid : 2048;
   seg_fixup_kernel<ET><<<fix_grid, 256, 0, s>>>(span_list, span_count, part_uid, seg_offsets,
                                                 unique_rows, part, dim, grad_rows, (ET*)E, lr);
   LAT_LAUNCH_CHECK();
+  LAT_HIP_CHECK(record(3));
   return hipSuccess;
 }
 
-hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
-                      const int32_t* indices, int F, int B, int64_t nnz, int mean,
-                      const void* dX, DType dxt, int n_slots, int first_slot, int dim,
-                      int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
-                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
-                      const int* keys_in, const int* vals_in, void* const* sub_events) {
+// The sparse gradient's workspace, shared by its two phases.
+struct EmbBwdWs {
+  int *keys, *vals, *skeys;
+  void* sort_ws;
+  int *tile_counts, *range_ubefore, *part_uid, *span_list, *span_count;
+  float* part;
+};
+static EmbBwdWs emb_bwd_ws(void* ws, int64_t nnz, int dim, int F) {
+  const int64_t n = nnz > 0 ? nnz : 1;
+  const int64_t ranges = cdiv(n, RANGE);
+  char* p = static_cast<char*>(ws);
+  auto take = [&](size_t bytes) { char* q = p; p += align256(bytes); return q; };
+  EmbBwdWs w;
+  w.keys = (int*)take((size_t)n * 4);
+  w.vals = (int*)take((size_t)n * 4);
+  w.skeys = (int*)take((size_t)n * 4);
+  w.sort_ws = take(radix_sort_segments_workspace(n, F));
+  w.tile_counts = (int*)take((size_t)(cdiv(n, SEG_TILE) + 1) * 4);
+  w.range_ubefore = (int*)take((size_t)ranges * 4);
+  w.part_uid = (int*)take((size_t)ranges * 4);
+  w.span_list = (int*)take((size_t)ranges * 4);
+  w.span_count = (int*)take(4);
+  w.part = (float*)take((size_t)ranges * 2 * dim * 4);
+  return w;
+}
+
+hipError_t embbag_bwd_sort(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
+                           const int32_t* indices, int F, int B, int64_t nnz, int dim,
+                           int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
+                           void* ws, hipStream_t s, const int* keys_in, const int* vals_in,
+                           void* const* ev) {
+  // ev (optional): 4 events, begin / end of the sort and of the run bookkeeping
   auto record = [&](int i) -> hipError_t {
-    return sub_events ? hipEventRecord((hipEvent_t)sub_events[i], s) : hipSuccess;
+    return ev ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
   };
+  LAT_HIP_CHECK(record(0));
   if (nnz == 0) {
+    LAT_HIP_CHECK(record(1));
+    LAT_HIP_CHECK(record(2));
     set_empty_kernel<<<1, 1, 0, s>>>(num_unique, seg_offsets);
     LAT_LAUNCH_CHECK();
-    for (int i = 0; i < 3; ++i) LAT_HIP_CHECK(record(i));
+    LAT_HIP_CHECK(record(3));
     return hipSuccess;
   }
   const int n = (int)nnz;
-  const int64_t ranges = cdiv(n, RANGE);
-  if ((int64_t)B * n_slots * dim * (dxt == DT_BF16 ? 2 : 4) > (int64_t)UINT32_MAX) {
-    set_error("dX of %lld bytes: the sparse gradient addresses dX with 32-bit offsets",
-              (long long)B * n_slots * dim * (dxt == DT_BF16 ? 2 : 4));
-    return hipErrorInvalidValue;
-  }
-  char* p = static_cast<char*>(ws);
-  auto take = [&](size_t bytes) { char* q = p; p += align256(bytes); return q; };
-  int* keys = (int*)take((size_t)n * 4);
-  int* vals = (int*)take((size_t)n * 4);
-  int* skeys = (int*)take((size_t)n * 4);
-  void* sort_ws = take(radix_sort_segments_workspace(n, F));
-  int* tile_counts = (int*)take((size_t)(cdiv(n, SEG_TILE) + 1) * 4);
-  int* range_ubefore = (int*)take((size_t)ranges * 4);
-  int* part_uid = (int*)take((size_t)ranges * 4);
-  int* span_list = (int*)take((size_t)ranges * 4);
-  int* span_count = (int*)take(4);
-  float* part = (float*)take((size_t)ranges * 2 * dim * 4);
-
+  EmbBwdWs w = emb_bwd_ws(ws, nnz, dim, F);
+  int* keys = w.keys;
+  int* vals = w.vals;
   const int64_t bags = (int64_t)F * B;
   if (keys_in && vals_in) {
     keys = const_cast<int*>(keys_in);  // read-only from here on
@@ -745,33 +765,66 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int
     embbag_keys_kernel<<<cdiv(bags, 4), 256, 0, s>>>(row_base, offsets, indices, F, B, keys, vals);
     LAT_LAUNCH_CHECK();
   }
-  hipError_t e = radix_sort_segments(keys, vals, n, offsets, F, B, row_base, max_local_rows, skeys,
-                                     sorted_bags, sort_ws, s);
+  hipError_t e = radix_sort_segments(keys, vals, n, offsets, F, B, row_base, max_local_rows,
+                                     w.skeys, sorted_bags, w.sort_ws, s);
   if (e != hipSuccess) return e;
-  LAT_HIP_CHECK(record(0));
-  const int tiles = cdiv(n, SEG_TILE);
-  zero_int_kernel<<<1, 64, 0, s>>>(span_count, 1);
-  LAT_LAUNCH_CHECK();
-  seg_count_kernel<<<tiles, SEG_THREADS, 0, s>>>(skeys, n, tile_counts);
-  LAT_LAUNCH_CHECK();
-  e = exclusive_scan_inplace_small(tile_counts, tiles, s);
-  if (e != hipSuccess) return e;
-  seg_write_kernel<<<tiles, SEG_THREADS, 0, s>>>(skeys, n, tile_counts, unique_rows, seg_offsets,
-                                                 num_unique, range_ubefore);
-  LAT_LAUNCH_CHECK();
   LAT_HIP_CHECK(record(1));
+  LAT_HIP_CHECK(record(2));
+  const int tiles = cdiv(n, SEG_TILE);
+  zero_int_kernel<<<1, 64, 0, s>>>(w.span_count, 1);
+  LAT_LAUNCH_CHECK();
+  seg_count_kernel<<<tiles, SEG_THREADS, 0, s>>>(w.skeys, n, w.tile_counts);
+  LAT_LAUNCH_CHECK();
+  e = exclusive_scan_inplace_small(w.tile_counts, tiles, s);
+  if (e != hipSuccess) return e;
+  seg_write_kernel<<<tiles, SEG_THREADS, 0, s>>>(w.skeys, n, w.tile_counts, unique_rows,
+                                                 seg_offsets, num_unique, w.range_ubefore);
+  LAT_LAUNCH_CHECK();
+  LAT_HIP_CHECK(record(3));
+  return hipSuccess;
+}
+
+hipError_t embbag_bwd_apply(const int32_t* offsets, int F, int B, int64_t nnz, int mean,
+                            const void* dX, DType dxt, int n_slots, int first_slot, int dim,
+                            const int* unique_rows, const int* seg_offsets, const int* sorted_bags,
+                            float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
+                            void* const* ev) {
+  if (nnz == 0) {
+    if (ev)
+      for (int i = 0; i < 4; ++i) LAT_HIP_CHECK(hipEventRecord((hipEvent_t)ev[i], s));
+    return hipSuccess;
+  }
+  const int n = (int)nnz;
+  if ((int64_t)B * n_slots * dim * (dxt == DT_BF16 ? 2 : 4) > (int64_t)UINT32_MAX) {
+    set_error("dX of %lld bytes: the sparse gradient addresses dX with 32-bit offsets",
+              (long long)B * n_slots * dim * (dxt == DT_BF16 ? 2 : 4));
+    return hipErrorInvalidValue;
+  }
+  EmbBwdWs w = emb_bwd_ws(ws, nnz, dim, F);
   void* Eupd = lr != 0.f ? E : nullptr;
-  hipEvent_t ev_reduced = sub_events ? (hipEvent_t)sub_events[2] : nullptr;
-#define LAT_RED(DTT, ETT)                                                                     \
-  return embbag_bwd_reduce<DTT, ETT>(skeys, sorted_bags, n, dX, B, n_slots, first_slot, dim,   \
-                                     offsets, mean, range_ubefore, part, part_uid, span_list,  \
-                                     span_count, seg_offsets, unique_rows, grad_rows, Eupd, lr, s, \
-                                     ev_reduced)
+#define LAT_RED(DTT, ETT)                                                                       \
+  return embbag_bwd_reduce<DTT, ETT>(w.skeys, sorted_bags, n, dX, B, n_slots, first_slot, dim,   \
+                                     offsets, mean, w.range_ubefore, w.part, w.part_uid,          \
+                                     w.span_list, w.span_count, seg_offsets, unique_rows,         \
+                                     grad_rows, Eupd, lr, s, ev)
   if (dxt == DT_BF16 && et == DT_BF16) LAT_RED(bf16_t, bf16_t);
   if (dxt == DT_BF16 && et == DT_F32) LAT_RED(bf16_t, float);
   if (dxt == DT_F32 && et == DT_BF16) LAT_RED(float, bf16_t);
   LAT_RED(float, float);
 #undef LAT_RED
+}
+
+hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
+                      const int32_t* indices, int F, int B, int64_t nnz, int mean,
+                      const void* dX, DType dxt, int n_slots, int first_slot, int dim,
+                      int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
+                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s) {
+  hipError_t e = embbag_bwd_sort(row_base, max_local_rows, offsets, indices, F, B, nnz, dim,
+                                 unique_rows, seg_offsets, sorted_bags, num_unique, ws, s,
+                                 nullptr, nullptr, nullptr);
+  if (e != hipSuccess) return e;
+  return embbag_bwd_apply(offsets, F, B, nnz, mean, dX, dxt, n_slots, first_slot, dim, unique_rows,
+                          seg_offsets, sorted_bags, grad_rows, E, et, lr, ws, s, nullptr);
 }
 
 // ---------------------------------------------------------------------------

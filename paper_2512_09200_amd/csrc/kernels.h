@@ -24,14 +24,26 @@ hipError_t embbag_fwd(const void* E, DType edt, int dim, const int64_t* row_base
                       void* X, DType xdt, int n_slots, int first_slot, hipStream_t s,
                       int* keys = nullptr, int* vals = nullptr);
 size_t embbag_bwd_workspace(int64_t nnz, int dim, int F);
-// max_local_rows: rows of the largest table (bounds every local index)
+// max_local_rows: rows of the largest table (bounds every local index).
+// The sparse gradient in two phases over one workspace: embbag_bwd_sort needs
+// only the batch (or the forward's keys/vals) -- sort, unique rows, run
+// offsets; embbag_bwd_apply needs dX -- segmented reduction and SGD.
+// ev (optional): 4 events each, begin/end of the phase's two parts.
+hipError_t embbag_bwd_sort(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
+                           const int32_t* indices, int F, int B, int64_t nnz, int dim,
+                           int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
+                           void* ws, hipStream_t s, const int* keys_in, const int* vals_in,
+                           void* const* ev);
+hipError_t embbag_bwd_apply(const int32_t* offsets, int F, int B, int64_t nnz, int mean,
+                            const void* dX, DType dxt, int n_slots, int first_slot, int dim,
+                            const int* unique_rows, const int* seg_offsets, const int* sorted_bags,
+                            float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
+                            void* const* ev);
 hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
                       const int32_t* indices, int F, int B, int64_t nnz, int mean,
                       const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
-                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s,
-                      const int* keys_in = nullptr, const int* vals_in = nullptr,
-                      void* const* sub_events = nullptr);  // 3 hipEvent_t: after sort, runs, reduce
+                      float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s);
 hipError_t validate_batch(const int64_t* row_base, const int32_t* offsets,
                           const int32_t* indices, int F, int B, int64_t nnz, int64_t max_rows,
                           unsigned long long* dev_result, hipStream_t s);

@@ -61,3 +61,29 @@ def test_host_queries_without_gpu(lib):
     msgs = {code: lib.lattice_status_string(code).decode() for code in _abi.STATUS}
     assert all(msgs.values()) and len(set(msgs.values())) == len(msgs), msgs
     assert "unknown" in lib.lattice_status_string(99).decode()
+
+
+def test_binding_structs_match_the_header(tmp_path):
+    """Every ctypes structure of the binding has the size and field offsets
+    of the C struct of the same name, as a C compiler lays it out."""
+    structs = [getattr(_abi, n) for n in dir(_abi)
+               if n.startswith("lattice_") and isinstance(getattr(_abi, n), type)
+               and issubclass(getattr(_abi, n), ctypes.Structure)]
+    assert structs
+    lines = ['#include <stddef.h>', '#include <stdio.h>', f'#include "{HEADER}"', "int main(void) {"]
+    expect = []
+    for S in structs:
+        lines.append(f'  printf("%zu\\n", sizeof({S.__name__}));')
+        expect.append((S.__name__, "sizeof", ctypes.sizeof(S)))
+        for f in S._fields_:
+            lines.append(f'  printf("%zu\\n", offsetof({S.__name__}, {f[0]}));')
+            expect.append((S.__name__, f[0], getattr(S, f[0]).offset))
+    lines.append("  return 0;\n}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-o", str(exe), str(src)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    bad = [(s, f, want, g) for (s, f, want), g in zip(expect, got) if want != g]
+    assert len(got) == len(expect) and not bad, bad

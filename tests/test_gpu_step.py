@@ -33,7 +33,7 @@ def gpu_relu_io(cfg, w, v):
     return dict(bottom=bin_, top=tin), dict(bottom=bout, top=tout)
 
 
-def run_step(w, lr, emit=True, spare=0):
+def run_step(w, lr, emit=True, spare=0, **kw):
     """One step; the workspace is planned for nnz + spare lookups."""
     from paper_2512_09200_amd import api
     cfg = w.cfg
@@ -41,7 +41,7 @@ def run_step(w, lr, emit=True, spare=0):
     lay = api.lattice_step_plan(model, cfg.B, w.nnz + spare, lr, emit)
     ws = torch.zeros(lay.total_bytes, dtype=torch.uint8, device=DEV)
     api.lattice_step(model, w.offsets, w.indices, w.dense, w.labels, w.mask, ws, lr, emit,
-                     nnz_capacity=w.nnz + spare)
+                     nnz_capacity=w.nnz + spare, **kw)
     torch.cuda.synchronize()
     return model, api.step_views(model, ws, lay, cfg.B, cfg.T, w.nnz), ws
 
@@ -125,3 +125,48 @@ def test_step_is_deterministic():
     assert torch.equal(v1["seg_offsets"][:U + 1], v2["seg_offsets"][:U + 1])
     for a, b in zip(g1, g2):
         assert torch.equal(a, b)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", ["large-fm-small", "mid-small"])
+def test_step_side_stream_matches_single_stream(name):
+    """The sparse gradient's sort and run bookkeeping on the library's side
+    stream (the default) and on the step's own stream give bit-identical
+    results, SGD updates included; the begin / end events of every stage are
+    recorded in order of their stage's stream."""
+    from paper_2512_09200_amd._abi import STAGES
+    cfg, lr = CASES[name]
+    lr = lr or 0.05
+    w = Workload(cfg)
+    E0 = w.E.clone()
+    stream = torch.cuda.Stream()   # a non-default caller stream
+    events = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(STAGES))]
+    for e in events:                # create the events before handing them over
+        e.record()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        _, v1, _ = run_step(w, lr, stream=stream, stage_events=events)
+    g1 = [L["dW"].clone() for L in w.top + w.bottom] + [w.fm_dW.clone() if w.fm_dW is not None else None]
+    E1 = w.E.clone()
+    w.E.copy_(E0)
+    _, v2, _ = run_step(w, lr, single_stream=True)
+    g2 = [L["dW"].clone() for L in w.top + w.bottom] + [w.fm_dW.clone() if w.fm_dW is not None else None]
+    U = int(v1["num_unique"].item())
+    assert U == int(v2["num_unique"].item())
+    for k in ("X", "t", "logits", "loss", "dX", "sorted_bags"):
+        assert torch.equal(v1[k], v2[k]), k
+    for k in ("unique_rows", "grad_rows"):
+        assert torch.equal(v1[k][:U], v2[k][:U]), k
+    assert torch.equal(v1["seg_offsets"][:U + 1], v2["seg_offsets"][:U + 1])
+    for a, b in zip(g1, g2):
+        assert (a is None and b is None) or torch.equal(a, b)
+    assert torch.equal(E1, w.E)
+    assert not torch.equal(E1, E0)
+    ms = [events[2 * k].elapsed_time(events[2 * k + 1]) for k in range(len(STAGES))]
+    assert all(x >= 0 for x in ms), dict(zip(STAGES, ms))
+    # the dense stages follow one another on the caller's stream; the
+    # reduction starts after both the dense backward and the run bookkeeping
+    i = {s: k for k, s in enumerate(STAGES)}
+    assert events[2 * i["bottom_bwd"] + 1].elapsed_time(events[2 * i["embbag_reduce"]]) >= 0
+    assert events[2 * i["embbag_runs"] + 1].elapsed_time(events[2 * i["embbag_reduce"]]) >= 0
+    assert events[2 * i["embbag_fwd"] + 1].elapsed_time(events[2 * i["embbag_sort"]]) >= 0
