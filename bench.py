@@ -182,7 +182,8 @@ def main():
             if l == 0 and nl != cfg.stack_n:
                 flops_fwd += 2.0 * cfg.B * cfg.stack_n * nl * cfg.d                  # residual C X
             nl = cfg.stack_n
-    dense_stages = ["bottom_fwd", "interact_fwd", "top_fwd", "top_bwd", "interact_bwd", "bottom_bwd"]
+    dense_stages = ["bottom_fwd", "interact_fwd", "top_fwd", "top_bwd", "interact_bwd", "top_wgrad",
+                    "bottom_bwd"]
     dense_ms = sum(stage_ms[s] for s in dense_stages)
     mfma_tfs = 3.0 * flops_fwd / (dense_ms * 1e-3) / 1e12
     samples_per_s = cfg.B / (ms_per_step * 1e-3)

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 3
+#define LATTICE_ABI_VERSION 4
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -284,8 +284,9 @@ typedef enum {
   LATTICE_STAGE_INTERACT_FWD,
   LATTICE_STAGE_TOP_FWD,
   LATTICE_STAGE_LOSS,
-  LATTICE_STAGE_TOP_BWD,
+  LATTICE_STAGE_TOP_BWD,         /* gradient chain of the top MLP down to its input */
   LATTICE_STAGE_INTERACT_BWD,
+  LATTICE_STAGE_TOP_WGRAD,       /* weight and bias gradients of the top MLP */
   LATTICE_STAGE_BOTTOM_BWD,
   LATTICE_STAGE_EMBBAG_SORT,     /* sparse gradient: sort of (row, bag) pairs */
   LATTICE_STAGE_EMBBAG_RUNS,     /* sparse gradient: unique rows and run offsets */
@@ -295,11 +296,14 @@ typedef enum {
 } lattice_step_stage;
 
 /* Streams.  The sort and run bookkeeping of the sparse gradient need only
- * the batch, so by default lattice_step runs them on a library-owned side
- * stream of the caller's device (non-blocking, default priority, one per
- * device, created on first use and kept until the process ends), forked from
- * the caller's stream after the pooled lookups and joined back before the
- * segmented reduction; they overlap the dense forward and backward.  All
+ * the batch, and the dense weight gradients (top MLP weights, bottom MLP
+ * backward) are not needed by the sparse gradient, so by default lattice_step
+ * runs them on a library-owned side stream of the caller's device
+ * (non-blocking, default priority, one per device, created on first use and
+ * kept until the process ends): the sort is forked from the caller's stream
+ * after the pooled lookups and overlaps the dense forward and backward; the
+ * weight gradients are forked after the interaction backward and overlap the
+ * segmented reduction, which waits for the sort.  All
  * work is still ordered after the caller's prior work on `stream`, and the
  * call's work is complete when `stream` reaches the end of it, as with a
  * single stream.  Concurrent calls (any threads) share the side stream and
@@ -313,8 +317,8 @@ typedef struct {
   void* const* stage_events;   /* host array of 2*LATTICE_STEP_STAGES hipEvent_t or NULL:
                                   [2s] is recorded when stage s begins and [2s+1] when
                                   it ends, on the stream that runs the stage (the side
-                                  stream for EMBBAG_SORT and EMBBAG_RUNS unless
-                                  single_stream) */
+                                  stream for EMBBAG_SORT, EMBBAG_RUNS, TOP_WGRAD and
+                                  BOTTOM_BWD unless single_stream) */
   int32_t single_stream;       /* 1: no side stream (see above) */
 } lattice_step_opts;
 

@@ -78,7 +78,7 @@ class lattice_step_opts(Structure):
 
 
 STAGES = ["embbag_fwd", "bottom_fwd", "interact_fwd", "top_fwd", "loss", "top_bwd",
-          "interact_bwd", "bottom_bwd", "embbag_sort", "embbag_runs", "embbag_reduce",
+          "interact_bwd", "top_wgrad", "bottom_bwd", "embbag_sort", "embbag_runs", "embbag_reduce",
           "embbag_fixup"]
 
 

@@ -379,54 +379,110 @@ static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, 
   return hipSuccess;
 }
 
+// Weight and bias gradients of layer i: dW = gᵀ · in (fp32), db = Σ_b g.
+static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const void* g,
+                                  int64_t gs, const void* in_i, int64_t ld_in, void* ws,
+                                  hipStream_t s) {
+  const lattice_linear& L = d->layers[i];
+  const DType dt = dt_of(d->dtype);
+  if (L.dW) {
+    GemmArgs w;
+    w.dt = dt;
+    w.A = g; w.lda = gs; w.ta = 1;
+    w.B = in_i; w.ldb = ld_in; w.tb = 1;
+    w.C = L.dW; w.ldc = L.in_dim; w.c_dt = DT_F32;
+    w.M = L.out_dim; w.N = L.in_dim; w.K = B;
+    w.max_splits = 16;
+    hipError_t e = gemm(w, ws, s);
+    if (e != hipSuccess) return e;
+  }
+  if (L.db) return colsum(g, dt, gs, B, L.out_dim, L.db, ws, s);
+  return hipSuccess;
+}
+
+// Input gradient of layer i: dst = (g · W) ⊙ [mask > 0] (mask: the layer's
+// input activation, i.e. the previous layer's ReLU output; null: no mask).
+static hipError_t mlp_layer_dgrad(const lattice_mlp_desc* d, int i, int B, const void* g,
+                                  int64_t gs, void* dst, int64_t dst_ld, const void* mask,
+                                  int64_t ldm, void* ws, hipStream_t s) {
+  const lattice_linear& L = d->layers[i];
+  GemmArgs x;
+  x.dt = dt_of(d->dtype);
+  x.A = g; x.lda = gs;
+  x.B = L.W; x.ldb = L.in_dim; x.tb = 1;
+  x.C = dst; x.ldc = dst_ld; x.c_dt = x.dt;
+  x.M = B; x.N = L.in_dim; x.K = L.out_dim;
+  x.max_splits = 16;
+  if (mask) {
+    x.mask = mask;
+    x.mask_dt = x.dt;
+    x.ldm = ldm;
+  }
+  return gemm(x, ws, s);
+}
+
 // g_last: gradient of the last layer's output, already ReLU-masked where needed.
+// Layer by layer (weights, then input gradient); hidden gradients alternate
+// between gbuf0 and gbuf1.
 static hipError_t mlp_backward(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
                                const void* const* acts, const int64_t* strides,
                                const void* g_last, int64_t g_last_stride, void* d_in,
                                int64_t d_in_stride, void* gbuf0, void* gbuf1, void* ws,
                                hipStream_t s) {
-  const DType dt = dt_of(d->dtype);
   const void* g = g_last;
   int64_t gs = g_last_stride;
   for (int i = d->n_layers - 1; i >= 0; --i) {
     const lattice_linear& L = d->layers[i];
     const void* in_i = i == 0 ? in : acts[i - 1];
     const int64_t ld_in = i == 0 ? in_stride : strides[i - 1];
-    if (L.dW) {
-      GemmArgs w;
-      w.dt = dt;
-      w.A = g; w.lda = gs; w.ta = 1;
-      w.B = in_i; w.ldb = ld_in; w.tb = 1;
-      w.C = L.dW; w.ldc = L.in_dim; w.c_dt = DT_F32;
-      w.M = L.out_dim; w.N = L.in_dim; w.K = B;
-      w.max_splits = 16;
-      hipError_t e = gemm(w, ws, s);
-      if (e != hipSuccess) return e;
-    }
-    if (L.db) {
-      hipError_t e = colsum(g, dt, gs, B, L.out_dim, L.db, ws, s);
-      if (e != hipSuccess) return e;
-    }
+    hipError_t e = mlp_layer_wgrad(d, i, B, g, gs, in_i, ld_in, ws, s);
+    if (e != hipSuccess) return e;
     if (i > 0 || d_in) {
       void* dst = i > 0 ? ((d->n_layers - 1 - i) % 2 == 0 ? gbuf0 : gbuf1) : d_in;
       const int64_t dst_ld = i > 0 ? L.in_dim : d_in_stride;
-      GemmArgs x;
-      x.dt = dt;
-      x.A = g; x.lda = gs;
-      x.B = L.W; x.ldb = L.in_dim; x.tb = 1;
-      x.C = dst; x.ldc = dst_ld; x.c_dt = dt;
-      x.M = B; x.N = L.in_dim; x.K = L.out_dim;
-      x.max_splits = 16;
-      if (i > 0) {
-        x.mask = acts[i - 1];
-        x.mask_dt = dt;
-        x.ldm = strides[i - 1];
-      }
-      hipError_t e = gemm(x, ws, s);
+      e = mlp_layer_dgrad(d, i, B, g, gs, dst, dst_ld, i > 0 ? acts[i - 1] : nullptr,
+                          i > 0 ? strides[i - 1] : 0, ws, s);
       if (e != hipSuccess) return e;
       g = dst;
       gs = dst_ld;
     }
+  }
+  return hipSuccess;
+}
+
+// The gradient chain alone: hidden gradients into gl[i] (gradient of layer
+// i's output, [B, out_i], i < n-1) and the input gradient into d_in (if any).
+static hipError_t mlp_backward_data(const lattice_mlp_desc* d, int B, const void* const* acts,
+                                    const int64_t* strides, const void* g_last,
+                                    int64_t g_last_stride, void* d_in, int64_t d_in_stride,
+                                    void* const* gl, void* ws, hipStream_t s) {
+  const void* g = g_last;
+  int64_t gs = g_last_stride;
+  for (int i = d->n_layers - 1; i >= 0; --i) {
+    if (i == 0 && !d_in) break;
+    void* dst = i > 0 ? gl[i - 1] : d_in;
+    const int64_t dst_ld = i > 0 ? d->layers[i].in_dim : d_in_stride;
+    hipError_t e = mlp_layer_dgrad(d, i, B, g, gs, dst, dst_ld, i > 0 ? acts[i - 1] : nullptr,
+                                   i > 0 ? strides[i - 1] : 0, ws, s);
+    if (e != hipSuccess) return e;
+    g = dst;
+    gs = dst_ld;
+  }
+  return hipSuccess;
+}
+
+// Weight and bias gradients of every layer from the stored chain.
+static hipError_t mlp_backward_weights(const lattice_mlp_desc* d, int B, const void* in,
+                                       int64_t in_stride, const void* const* acts,
+                                       const int64_t* strides, const void* g_last,
+                                       int64_t g_last_stride, void* const* gl, void* ws,
+                                       hipStream_t s) {
+  for (int i = d->n_layers - 1; i >= 0; --i) {
+    const void* g = i == d->n_layers - 1 ? g_last : gl[i];
+    const int64_t gs = i == d->n_layers - 1 ? g_last_stride : d->layers[i].out_dim;
+    hipError_t e = mlp_layer_wgrad(d, i, B, g, gs, i == 0 ? in : acts[i - 1],
+                                   i == 0 ? in_stride : strides[i - 1], ws, s);
+    if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
@@ -531,7 +587,9 @@ struct Plan {
   lattice_step_layout L;
   int n, T, t_stride;
   size_t gbuf_top, gbuf_bot, scratch;
-  int64_t g_top[2], g_bot[2];
+  // per hidden layer i: gradient of its output [B, out_i]; g_masked: the
+  // ReLU-masked gradient of the bottom MLP's output [B, dim]
+  int64_t g_top[LATTICE_MAX_LAYERS], g_bot[LATTICE_MAX_LAYERS], g_masked;
 };
 
 static lattice_status check_model(const lattice_model_desc* m, int B) {
@@ -596,15 +654,13 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   L.loss = take(4);
   L.d_t = take((size_t)B * P->t_stride * es);
   L.dX = take((size_t)B * P->n * d * es);
-  const size_t gt = mlp_gbuf_elems(&m->top, B) * es;
-  P->g_top[0] = take(gt);
-  P->g_top[1] = take(gt);
+  for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) P->g_top[i] = P->g_bot[i] = -1;
+  for (int i = 0; i + 1 < m->top.n_layers; ++i) P->g_top[i] = take((size_t)B * m->top.layers[i].out_dim * es);
+  P->g_masked = -1;
   if (m->dense_in > 0) {
-    const size_t gb = mlp_gbuf_elems(&m->bottom, B) * es;
-    P->g_bot[0] = take(gb);
-    P->g_bot[1] = take(gb);
-  } else {
-    P->g_bot[0] = P->g_bot[1] = -1;
+    for (int i = 0; i + 1 < m->bottom.n_layers; ++i)
+      P->g_bot[i] = take((size_t)B * m->bottom.layers[i].out_dim * es);
+    P->g_masked = take((size_t)B * d * es);
   }
   const int64_t nn = nnz > 0 ? nnz : 1;
   L.unique_rows = take((size_t)nn * 4);
@@ -636,7 +692,9 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
 namespace {
 struct SideStream {
   hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  // fork after the pooled lookups and after the interaction backward; join
+  // after the sort and run bookkeeping and after the dense weight gradients
+  hipEvent_t fork_fwd = nullptr, fork_bwd = nullptr, sorted = nullptr, done = nullptr;
 };
 constexpr int kMaxDevices = 64;
 std::mutex g_side_mu;
@@ -654,8 +712,8 @@ lattice_status side_stream_of(hipStream_t main, SideStream** out) {
     if (hipGetDevice(&cur) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipGetDevice failed");
     if (cur != dev && hipSetDevice(dev) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipSetDevice failed");
     hipError_t e = hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming);
+    for (hipEvent_t* ev : {&ss.fork_fwd, &ss.fork_bwd, &ss.sorted, &ss.done})
+      if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
     if (cur != dev) (void)hipSetDevice(cur);
     if (e != hipSuccess) {
       ss = SideStream{};  // handles of a failed set-up stay unused
@@ -746,10 +804,10 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     lock.lock();
     st = side_stream_of(s, &side);
     if (st != LATTICE_OK) return st;
-    HIPRET(hipEventRecord(side->fork, s));
-    HIPRET(hipStreamWaitEvent(side->s, side->fork, 0));
+    HIPRET(hipEventRecord(side->fork_fwd, s));
+    HIPRET(hipStreamWaitEvent(side->s, side->fork_fwd, 0));
     HIPRET(sparse_sort(side->s));
-    HIPRET(hipEventRecord(side->join, side->s));
+    HIPRET(hipEventRecord(side->sorted, side->s));
   }
   // 2. bottom MLP -> slot 0 of X
   HIPRET(begin(LATTICE_STAGE_BOTTOM_FWD));
@@ -787,33 +845,56 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   HIPRET(bce((const float*)at(L.logits), batch->labels, batch->mask, (int64_t)B * T,
              (float*)at(L.loss), (float*)at(L.d_logits), at(L.d_logits_op), dt, scratch, s));
   HIPRET(end(LATTICE_STAGE_LOSS));
-  // 6. top backward -> d_t
+  // 6. top backward, gradient chain only -> d_t (weight gradients: 8.)
+  void* gtop[LATTICE_MAX_LAYERS];
+  for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) gtop[i] = at(P.g_top[i]);
   HIPRET(begin(LATTICE_STAGE_TOP_BWD));
-  HIPRET(mlp_backward(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, at(L.d_t),
-                      P.t_stride, at(P.g_top[0]), at(P.g_top[1]), scratch, s));
+  HIPRET(mlp_backward_data(&m->top, B, tacts, tstr, at(L.d_logits_op), T, at(L.d_t), P.t_stride,
+                           gtop, scratch, s));
   HIPRET(end(LATTICE_STAGE_TOP_BWD));
   // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
   HIPRET(begin(LATTICE_STAGE_INTERACT_BWD));
   void* dX = at(L.dX);
   HIPRET(interact_bwd_impl(&m->interact, B, X, at(L.d_t), P.t_stride, dX, at(L.interact), s));
   HIPRET(end(LATTICE_STAGE_INTERACT_BWD));
-  // 8. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
-  HIPRET(begin(LATTICE_STAGE_BOTTOM_BWD));
-  if (m->dense_in > 0) {
-    void* masked = at(P.g_bot[1]);
-    relu_mask_kernel<<<cdiv((int64_t)B * d, 256), 256, 0, s>>>(dX, (int64_t)n * d, X,
-                                                               (int64_t)n * d, B, d,
-                                                               dt == DT_BF16, masked);
-    if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
-    // g buffers: masked lives in g_bot[1]; the first hidden gradient goes to g_bot[0]
-    HIPRET(mlp_backward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, masked, d,
-                        nullptr, 0, at(P.g_bot[0]), at(P.g_top[0]), scratch, s));
-  }
-  HIPRET(end(LATTICE_STAGE_BOTTOM_BWD));
-  // 9. row-coalesced embedding gradient (+ row-sparse SGD): join, then reduce
+  // 8. weight gradients of the top MLP and the bottom backward need nothing
+  // the sparse gradient writes: on the side stream they overlap the
+  // segmented reduction
+  hipStream_t ws_stream = s;
   if (side) {
-    HIPRET(hipStreamWaitEvent(s, side->join, 0));
-    lock.unlock();
+    HIPRET(hipEventRecord(side->fork_bwd, s));
+    HIPRET(hipStreamWaitEvent(side->s, side->fork_bwd, 0));
+    ws_stream = side->s;
+  }
+  auto wbegin = [&](int i) -> hipError_t {
+    return ev ? hipEventRecord((hipEvent_t)ev[2 * i], ws_stream) : hipSuccess;
+  };
+  auto wend = [&](int i) -> hipError_t {
+    return ev ? hipEventRecord((hipEvent_t)ev[2 * i + 1], ws_stream) : hipSuccess;
+  };
+  HIPRET(wbegin(LATTICE_STAGE_TOP_WGRAD));
+  HIPRET(mlp_backward_weights(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, gtop,
+                              scratch, ws_stream));
+  HIPRET(wend(LATTICE_STAGE_TOP_WGRAD));
+  // 9. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
+  HIPRET(wbegin(LATTICE_STAGE_BOTTOM_BWD));
+  if (m->dense_in > 0) {
+    void* masked = at(P.g_masked);
+    relu_mask_kernel<<<cdiv((int64_t)B * d, 256), 256, 0, ws_stream>>>(
+        dX, (int64_t)n * d, X, (int64_t)n * d, B, d, dt == DT_BF16, masked);
+    if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
+    void* gbot[LATTICE_MAX_LAYERS];
+    for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) gbot[i] = at(P.g_bot[i]);
+    HIPRET(mlp_backward_data(&m->bottom, B, bacts, bstr, masked, d, nullptr, 0, gbot, scratch,
+                             ws_stream));
+    HIPRET(mlp_backward_weights(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, masked, d,
+                                gbot, scratch, ws_stream));
+  }
+  HIPRET(wend(LATTICE_STAGE_BOTTOM_BWD));
+  // 10. row-coalesced embedding gradient (+ row-sparse SGD) once the sort is done
+  if (side) {
+    HIPRET(hipEventRecord(side->done, side->s));
+    HIPRET(hipStreamWaitEvent(s, side->sorted, 0));
   } else {
     HIPRET(sparse_sort(s));
   }
@@ -822,6 +903,11 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                           (const int*)at(L.unique_rows), (const int*)at(L.seg_offsets),
                           (const int*)at(L.sorted_bags), (float*)at(L.grad_rows), m->tables.data,
                           dt, opts->lr_tables, sparse, s, stage_ev(LATTICE_STAGE_EMBBAG_REDUCE)));
+  // join: the caller's stream passes this point after all of the step's work
+  if (side) {
+    HIPRET(hipStreamWaitEvent(s, side->done, 0));
+    lock.unlock();
+  }
   return LATTICE_OK;
 }
 

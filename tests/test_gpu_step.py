@@ -164,9 +164,15 @@ def test_step_side_stream_matches_single_stream(name):
     assert not torch.equal(E1, E0)
     ms = [events[2 * k].elapsed_time(events[2 * k + 1]) for k in range(len(STAGES))]
     assert all(x >= 0 for x in ms), dict(zip(STAGES, ms))
-    # the dense stages follow one another on the caller's stream; the
-    # reduction starts after both the dense backward and the run bookkeeping
+    # ordering: the sort after the pooled lookups; the reduction after the
+    # interaction backward (dX) and the run bookkeeping; the weight gradients
+    # after the interaction backward
     i = {s: k for k, s in enumerate(STAGES)}
-    assert events[2 * i["bottom_bwd"] + 1].elapsed_time(events[2 * i["embbag_reduce"]]) >= 0
-    assert events[2 * i["embbag_runs"] + 1].elapsed_time(events[2 * i["embbag_reduce"]]) >= 0
-    assert events[2 * i["embbag_fwd"] + 1].elapsed_time(events[2 * i["embbag_sort"]]) >= 0
+
+    def before(a, b):   # stage a ends before stage b begins
+        return events[2 * i[a] + 1].elapsed_time(events[2 * i[b]]) >= 0
+    assert before("embbag_fwd", "embbag_sort")
+    assert before("interact_bwd", "embbag_reduce")
+    assert before("embbag_runs", "embbag_reduce")
+    assert before("interact_bwd", "top_wgrad")
+    assert before("top_wgrad", "bottom_bwd")
