@@ -118,11 +118,11 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs resident ({time.time() - t0:.1f}s); workspace {lay.total_bytes / 2**30:.2f} GiB")
 
-    def step(i, events=None):
+    def step(i, events=None, single_stream=args.single_stream):
         b = batches[i % len(batches)]
         api.lattice_step(model, b["offsets"], b["indices"], b["dense"], b["labels"], b["mask"], ws,
                          cfg.lr_tables, False, stage_events=events, nnz_capacity=nnz_max,
-                         single_stream=args.single_stream)
+                         single_stream=single_stream)
 
     for i in range(args.warmup):
         step(i)
@@ -130,22 +130,42 @@ def main():
     log("[bench] warmup done")
 
     nst = len(STAGES)
-    # begin / end event of every stage, recorded on the stream that runs it
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nst)] for _ in range(args.steps)]
-    for es in ev:          # create the underlying events before handing them to the library
-        for e in es:
-            e.record()
-    torch.cuda.synchronize()
+
+    def make_events(n):
+        # begin / end event of every stage, recorded on the stream that runs it
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nst)] for _ in range(n)]
+        for es in ev:      # create the underlying events before handing them to the library
+            for e in es:
+                e.record()
+        torch.cuda.synchronize()
+        return ev
+
+    def stage_times(ev):
+        return {s: float(np.mean([e[2 * k].elapsed_time(e[2 * k + 1]) for e in ev]))
+                for k, s in enumerate(STAGES)}
+
+    ev = make_events(args.steps)
     t_start = time.perf_counter()
     for i in range(args.steps):
         step(args.warmup + i, ev[i])
     torch.cuda.synchronize()
     t_total = time.perf_counter() - t_start
     ms_per_step = 1e3 * t_total / args.steps
-    stage_ms = {s: float(np.mean([ev[i][2 * k].elapsed_time(ev[i][2 * k + 1])
-                                  for i in range(args.steps)]))
-                for k, s in enumerate(STAGES)}
+    stage_ms = stage_times(ev)
     log("[bench] stage ms: " + ", ".join(f"{k}={v:.3f}" for k, v in stage_ms.items()))
+    # Per-stage attribution without overlap: stages sharing the GPU with the
+    # side stream's work run slower than alone, so the kernels' own rates
+    # (GB/s, MFMA fraction) come from further steps on one stream, after the
+    # timed region.
+    if args.single_stream:
+        iso_ms = stage_ms
+    else:
+        ev_iso = make_events(args.steps)
+        for i in range(args.steps):
+            step(args.warmup + args.steps + i, ev_iso[i], single_stream=True)
+        torch.cuda.synchronize()
+        iso_ms = stage_times(ev_iso)
+        log("[bench] stage ms, one stream: " + ", ".join(f"{k}={v:.3f}" for k, v in iso_ms.items()))
 
     # ---- algorithmic work -------------------------------------------------
     es = 2 if cfg.dtype == "bf16" else 4
@@ -163,7 +183,7 @@ def main():
     # whole sparse-gradient stage (sort and bookkeeping are implementation overhead)
     bwd_bytes = nnz * (cfg.d * es + 4) + bags * 4 + (U * 2 * row_bytes if cfg.lr_tables else U * (4 * cfg.d + 4))
     bwd_stages = ["embbag_sort", "embbag_runs", "embbag_reduce", "embbag_fixup"]
-    bwd_ms = sum(stage_ms[s] for s in bwd_stages)
+    bwd_ms = sum(iso_ms[s] for s in bwd_stages)
     fwd_gbs = fwd_bytes / (stage_ms["embbag_fwd"] * 1e-3) / 1e9
     red_gbs = red_bytes / (stage_ms["embbag_reduce"] * 1e-3) / 1e9
     bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
@@ -184,7 +204,7 @@ def main():
             nl = cfg.stack_n
     dense_stages = ["bottom_fwd", "interact_fwd", "top_fwd", "top_bwd", "interact_bwd", "top_wgrad",
                     "bottom_bwd"]
-    dense_ms = sum(stage_ms[s] for s in dense_stages)
+    dense_ms = sum(iso_ms[s] for s in dense_stages)
     mfma_tfs = 3.0 * flops_fwd / (dense_ms * 1e-3) / 1e12
     samples_per_s = cfg.B / (ms_per_step * 1e-3)
 
@@ -233,6 +253,7 @@ def main():
         "interaction_mlp_TFLOPs": round(mfma_tfs, 1),
         "interaction_mlp_mfma_frac": round(mfma_tfs / MFMA_BF16_PEAK_TFS, 4),
         "stage_ms": {k: round(x, 4) for k, x in stage_ms.items()},
+        "stage_ms_one_stream": {k: round(x, 4) for k, x in iso_ms.items()},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

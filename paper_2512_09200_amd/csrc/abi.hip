@@ -385,6 +385,7 @@ static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const
                                   hipStream_t s) {
   const lattice_linear& L = d->layers[i];
   const DType dt = dt_of(d->dtype);
+  bool db_done = false;
   if (L.dW) {
     GemmArgs w;
     w.dt = dt;
@@ -393,10 +394,15 @@ static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const
     w.C = L.dW; w.ldc = L.in_dim; w.c_dt = DT_F32;
     w.M = L.out_dim; w.N = L.in_dim; w.K = B;
     w.max_splits = 16;
+    // bf16: db is the row sum of A = gᵀ, taken by the same GEMM
+    if (dt == DT_BF16 && L.db) {
+      w.rowsum = L.db;
+      db_done = true;
+    }
     hipError_t e = gemm(w, ws, s);
     if (e != hipSuccess) return e;
   }
-  if (L.db) return colsum(g, dt, gs, B, L.out_dim, L.db, ws, s);
+  if (L.db && !db_done) return colsum(g, dt, gs, B, L.out_dim, L.db, ws, s);
   return hipSuccess;
 }
 

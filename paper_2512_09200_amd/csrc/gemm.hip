@@ -232,10 +232,14 @@ __device__ inline void mma_k64(const bf16_t* As, const bf16_t* Bs, int wm, int w
 
 // grid: x = M tiles * N tiles (renumbered per XCD), z = split index (split-K)
 // or batch index (batched; never both).  vec: 16-byte epilogue vectors allowed.
+// rowsum (optional, not batched): rowsum[m] = sum over k of A[m][k], added in
+// k order by the blocks of the first N tile from their LDS A tiles; with
+// split-K each split's sum goes to rs_partial[split][m].
 template <bool TA, bool TB, bool VA, bool VB, typename CT>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     Opnd A, Opnd Bm, CT* __restrict__ C, int64_t ldc, int M, int N, int K, int k_per_split,
-    float* __restrict__ partial, Epi epi, int64_t sA, int64_t sB, int64_t sC, int batched, int vec) {
+    float* __restrict__ partial, Epi epi, int64_t sA, int64_t sB, int64_t sC, int batched, int vec,
+    float* __restrict__ rowsum, float* __restrict__ rs_partial) {
   extern __shared__ __attribute__((aligned(16))) unsigned char gemm_smem[];
   bf16_t* As[2];
   bf16_t* Bs[2];
@@ -276,6 +280,23 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     la.load(A, M, kend, m0, k0, edge_m || edge_k);
     lb.load(Bm, N, kend, n0, k0, edge_n || edge_k);
   };
+  // row sums of A: thread t adds 32 k of row t/2 of each LDS A tile
+  const bool rs_on = rowsum != nullptr && n0 == 0;
+  float rs = 0.f;
+  auto rowsum_step = [&](const bf16_t* as) {
+    if (rs_on) {
+      const bf16_t* p = as + (threadIdx.x >> 1) * GLD + (threadIdx.x & 1) * 32;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const u32x4 x = *reinterpret_cast<const u32x4*>(p + v * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          rs += __uint_as_float(x[e] << 16);
+          rs += __uint_as_float(x[e] & 0xffff0000u);
+        }
+      }
+    }
+  };
   if (ktiles > 0) load(la0, lb0, 0);
   if (ktiles > 1) load(la1, lb1, 1);
   if (ktiles > 0) {
@@ -291,11 +312,13 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   for (; kt + 2 <= ktiles; kt += 2) {
     if (kt + 2 < ktiles) load(la0, lb0, kt + 2);
     mma_k64(As[0], Bs[0], wm, wn, lane, acc);
+    rowsum_step(As[0]);
     la1.store(As[1]);
     lb1.store(Bs[1]);
     __syncthreads();
     if (kt + 3 < ktiles) load(la1, lb1, kt + 3);
     mma_k64(As[1], Bs[1], wm, wn, lane, acc);
+    rowsum_step(As[1]);
     if (kt + 2 < ktiles) {
       la0.store(As[0]);
       lb0.store(Bs[0]);
@@ -304,7 +327,16 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   }
   if (kt < ktiles) {
     mma_k64(As[0], Bs[0], wm, wn, lane, acc);
+    rowsum_step(As[0]);
     __syncthreads();
+  }
+  if (rs_on) {
+    rs += __shfl_xor(rs, 1, 64);  // the two halves of the row, in a fixed order
+    const int row = m0 + (threadIdx.x >> 1);
+    if ((threadIdx.x & 1) == 0 && row < M) {
+      if (rs_partial) rs_partial[(int64_t)blockIdx.z * M + row] = rs;
+      else rowsum[row] = rs;
+    }
   }
 
   // Stage the fp32 tile in LDS.  D[i][j] of a 32x32 fragment: lane holds
@@ -355,8 +387,14 @@ template <typename CT>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial,
                                                             int splits, int M, int N,
                                                             CT* __restrict__ C, int64_t ldc,
-                                                            Epi epi) {
+                                                            Epi epi, const float* __restrict__ rs_partial,
+                                                            float* __restrict__ rowsum) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (rowsum && i < M) {
+    float r = 0.f;
+    for (int z = 0; z < splits; ++z) r += rs_partial[(int64_t)z * M + i];
+    rowsum[i] = r;
+  }
   if (i >= (int64_t)M * N) return;
   const int row = (int)(i / N), col = (int)(i % N);
   float s = 0.f;
@@ -420,9 +458,10 @@ int gemm_splits(const GemmArgs& g) {
   return s;
 }
 
+// split-K partial tiles [splits][M][N], then the row-sum partials [splits][M]
 size_t gemm_workspace(const GemmArgs& g) {
   int splits = gemm_splits(g);
-  return splits > 1 ? (size_t)splits * g.M * g.N * sizeof(float) : 0;
+  return splits > 1 ? (size_t)splits * ((size_t)g.M * g.N + g.M) * sizeof(float) : 0;
 }
 
 static Epi make_epi(const GemmArgs& g) {
@@ -462,6 +501,7 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
   Opnd a{(const bf16_t*)g.A, g.lda, g.kseg, g.ksA};
   Opnd b{(const bf16_t*)g.B, g.ldb, g.kseg, g.ksB};
   float* partial = splits > 1 ? ws : nullptr;
+  float* rs_partial = (splits > 1 && g.rowsum) ? ws + (size_t)splits * g.M * g.N : nullptr;
   const int vec = epi_vec_ok(g);
   // The kernels use 72 KiB of dynamic LDS (above the 64 KiB default limit).
   static std::once_flag once_bf, once_f;
@@ -471,22 +511,24 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
     });
     k<<<grid, 256, GEMM_LDS, st>>>(a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA,
-                                   g.sB, g.sC, batched, vec);
+                                   g.sB, g.sC, batched, vec, g.rowsum, rs_partial);
   } else {
     auto k = gemm_bf16_kernel<TA, TB, VA, VB, float>;
     std::call_once(once_f, [&] {
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
     });
     k<<<grid, 256, GEMM_LDS, st>>>(a, b, (float*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA,
-                                   g.sB, g.sC, batched, vec);
+                                   g.sB, g.sC, batched, vec, g.rowsum, rs_partial);
   }
   LAT_LAUNCH_CHECK();
   if (splits > 1) {
     const int64_t n = (int64_t)g.M * g.N;
     if (g.c_dt == DT_BF16)
-      splitk_reduce_kernel<bf16_t><<<cdiv(n, 256), 256, 0, st>>>(ws, splits, g.M, g.N, (bf16_t*)g.C, g.ldc, epi);
+      splitk_reduce_kernel<bf16_t><<<cdiv(n, 256), 256, 0, st>>>(ws, splits, g.M, g.N, (bf16_t*)g.C,
+                                                                  g.ldc, epi, rs_partial, g.rowsum);
     else
-      splitk_reduce_kernel<float><<<cdiv(n, 256), 256, 0, st>>>(ws, splits, g.M, g.N, (float*)g.C, g.ldc, epi);
+      splitk_reduce_kernel<float><<<cdiv(n, 256), 256, 0, st>>>(ws, splits, g.M, g.N, (float*)g.C,
+                                                                 g.ldc, epi, rs_partial, g.rowsum);
     LAT_LAUNCH_CHECK();
   }
   return hipSuccess;
@@ -513,6 +555,10 @@ hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t st) {
   if (g.M == 0 || g.N == 0 || g.batch == 0) return hipSuccess;
   if (g.accumulate && g.c_dt != DT_F32) {
     set_error("accumulating GEMM needs an fp32 output");
+    return hipErrorInvalidValue;
+  }
+  if (g.rowsum && (g.dt != DT_BF16 || g.batch > 1)) {
+    set_error("GEMM row sums: bf16 and not batched only");
     return hipErrorInvalidValue;
   }
   if (g.dt == DT_BF16) {

@@ -65,6 +65,7 @@ struct GemmArgs {
   int64_t sA = 0, sB = 0, sC = 0;
   int kseg = 0;                // K segmentation: k -> (k / kseg) * ks + k % kseg (0: none)
   int64_t ksA = 0, ksB = 0;
+  float* rowsum = nullptr;     // bf16, not batched: rowsum[m] = sum_k A[m][k] (fp32, k order)
 };
 int gemm_splits(const GemmArgs& g);
 size_t gemm_workspace(const GemmArgs& g);

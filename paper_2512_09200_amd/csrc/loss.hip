@@ -12,7 +12,9 @@
 namespace lat {
 
 constexpr int BCE_THREADS = 256;
-constexpr int BCE_TILE = 4096;
+// two logits per thread: the passes are latency-bound (one exp/log1p chain
+// per element), so many small blocks beat few long ones
+constexpr int BCE_TILE = 512;
 
 __device__ inline float block_sum_f(float v, float* lds) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;

@@ -209,7 +209,7 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   constexpr int CHUNK = SORT_TILE / NW;  // 1024 consecutive items per wave
   constexpr int ROUNDS = CHUNK / 64;     // 16
   __shared__ int wcnt[NW][RADIX];        // per-wave digit counts, then per-wave bases in the tile
-  __shared__ int dstart[RADIX];          // first tile position of each digit
+  __shared__ int dbase[RADIX];           // output position of tile position 0 of each digit
   __shared__ int scan_tmp[SORT_THREADS / 64];
   __shared__ int lkeys[SORT_TILE];
   __shared__ int lvals[SORT_TILE];
@@ -259,7 +259,7 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
       for (int i = 0; i < NW; ++i) tot += wcnt[i][d];
     int all;
     const int st = block_exclusive_scan(tot, scan_tmp, &all);
-    dstart[d] = st;
+    if (d < radix) dbase[d] = coffs[t.cb + (int64_t)d * t.nt + t.lt] - st;
     int run = st;
     if (d < radix)
       for (int i = 0; i < NW; ++i) {
@@ -284,7 +284,7 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   for (int i = threadIdx.x; i < t.cnt; i += SORT_THREADS) {
     const int kk = lkeys[i];
     const uint32_t d = ((uint32_t)(kk - key0) >> shift) & (radix - 1);
-    const int pos = coffs[t.cb + (int64_t)d * t.nt + t.lt] + (i - dstart[d]);
+    const int pos = dbase[d] + i;
     keys_out[pos] = kk;
     vals_out[pos] = lvals[i];
   }
