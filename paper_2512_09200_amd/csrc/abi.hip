@@ -238,6 +238,12 @@ static bool fm_uses_mfma(const lattice_interact_desc* d, int64_t stride = 8) {
   return d->dtype == LATTICE_BF16 && fm_mfma_supported(d->n, d->dim, d->rank) && stride % 8 == 0;
 }
 
+// DOT on MFMA: bf16, n <= 128, d in {64, 128}, X rows read with 4-byte loads
+static bool dot_uses_mfma(const lattice_interact_desc* d, const void* X) {
+  return d->dtype == LATTICE_BF16 && dot_mfma_supported(d->n, d->dim) &&
+         ((uintptr_t)X & 3) == 0;
+}
+
 static size_t interact_ws(const lattice_interact_desc* d, int B) {
   if (d->kind == LATTICE_INTERACT_STACK) return stack_plan(stack_shape(d), B).total_bytes;
   if (d->kind != LATTICE_INTERACT_FM) return 0;
@@ -251,8 +257,11 @@ static hipError_t interact_fwd_impl(const lattice_interact_desc* d, int B, const
     stack_layers(d, Ls);
     return stack_fwd(stack_shape(d), Ls, B, X, out, os, ws, s);
   }
-  if (d->kind == LATTICE_INTERACT_DOT)
+  if (d->kind == LATTICE_INTERACT_DOT) {
+    if (dot_uses_mfma(d, X))
+      return dot_mfma(true, X, B, d->n, d->dim, out, os, d->emit_slot0, nullptr, 0, nullptr, s);
     return dot_fwd(dt_of(d->dtype), X, B, d->n, d->dim, out, os, d->emit_slot0, s);
+  }
   if (fm_uses_mfma(d, os))
     return fm_mfma(true, X, d->fm_W, B, d->n, d->dim, d->rank, out, os, d->emit_slot0, nullptr, 0,
                    nullptr, nullptr, nullptr, nullptr, nullptr, s);
@@ -267,8 +276,11 @@ static hipError_t interact_bwd_impl(const lattice_interact_desc* d, int B, const
     stack_layers(d, Ls);
     return stack_bwd(stack_shape(d), Ls, B, X, dout, ds, dX, ws, s);
   }
-  if (d->kind == LATTICE_INTERACT_DOT)
+  if (d->kind == LATTICE_INTERACT_DOT) {
+    if (dot_uses_mfma(d, X))
+      return dot_mfma(false, X, B, d->n, d->dim, nullptr, 0, d->emit_slot0, dout, ds, dX, s);
     return dot_bwd(dt_of(d->dtype), X, B, d->n, d->dim, dout, ds, d->emit_slot0, dX, s);
+  }
   if (fm_uses_mfma(d, ds))
     return fm_mfma(false, X, d->fm_W, B, d->n, d->dim, d->rank, nullptr, 0, d->emit_slot0, dout, ds,
                    nullptr, dX, nullptr, d->fm_dW, ws, s);

@@ -141,8 +141,17 @@ struct LoadK {
       const int v = threadIdx.x + i * 256;
       const int rr = v >> 3, kc = (v & 7) * 8;
       const int gr = r0 + rr, gk = k0 + kc;
-      if (!edge || (gr < R && gk < K)) r[i] = ldg16(o.p + (int64_t)gr * o.ld + koff<false>(o, gk));
-      else r[i] = u32x4{0, 0, 0, 0};
+      if (!edge || (gr < R && gk < K)) {
+        r[i] = ldg16(o.p + (int64_t)gr * o.ld + koff<false>(o, gk));
+        // a vector reaching past K (rows padded to 8 elements): zero the tail
+        if (edge && gk + 8 > K) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (gk + e >= K) r[i][e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+        }
+      } else {
+        r[i] = u32x4{0, 0, 0, 0};
+      }
     }
   }
   __device__ inline void store(bf16_t* S) {
@@ -183,26 +192,50 @@ struct LoadMN {
     }
   }
 };
-// Generic element loader (any alignment / transposition).
+// Generic element loader (any alignment / transposition).  Consecutive lanes
+// take consecutive elements in memory: along k for a K-contiguous operand,
+// along the rows for an MN-contiguous one.  It holds no tile in registers:
+// load() records the tile and store() reads it from memory straight into LDS
+// (2-byte loads would otherwise pin 32 registers per stage).
 template <bool MN>
 struct LoadElem {
-  bf16_t r[32];
-  __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool /*edge*/) {
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const int e = threadIdx.x + i * 256;
-      const int rr = e >> 6, kk = e & 63;
-      const int gr = r0 + rr, gk = k0 + kk;
-      bf16_t v = 0;
-      if (gr < R && gk < K) v = MN ? o.p[koff<true>(o, gk) + gr] : o.p[(int64_t)gr * o.ld + koff<false>(o, gk)];
-      r[i] = v;
+  const Opnd* o;
+  int R, K, r0, k0;
+  __device__ static inline void at(int e, int& rr, int& kk) {
+    if (MN) {
+      rr = e & (GBM - 1);
+      kk = e / GBM;
+    } else {
+      rr = e >> 6;
+      kk = e & 63;
     }
   }
+  __device__ inline void load(const Opnd& o_, int R_, int K_, int r0_, int k0_, bool /*edge*/) {
+    o = &o_;
+    R = R_;
+    K = K_;
+    r0 = r0_;
+    k0 = k0_;
+  }
   __device__ inline void store(bf16_t* S) {
+    // all 32 loads in flight at once (two elements per register), then the writes
+    uint32_t r[16];
 #pragma unroll
     for (int i = 0; i < 32; ++i) {
-      const int e = threadIdx.x + i * 256;
-      S[(e >> 6) * GLD + (e & 63)] = r[i];
+      int rr, kk;
+      at(threadIdx.x + i * 256, rr, kk);
+      const int gr = r0 + rr, gk = k0 + kk;
+      uint32_t v = 0;
+      if (gr < R && gk < K)
+        v = MN ? o->p[koff<true>(*o, gk) + gr] : o->p[(int64_t)gr * o->ld + koff<false>(*o, gk)];
+      if (i & 1) r[i >> 1] |= v << 16;
+      else r[i >> 1] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      int rr, kk;
+      at(threadIdx.x + i * 256, rr, kk);
+      S[rr * GLD + kk] = (bf16_t)((i & 1) ? (r[i >> 1] >> 16) : (r[i >> 1] & 0xffffu));
     }
   }
 };
@@ -538,13 +571,17 @@ template <bool TA, bool TB>
 static hipError_t gemm_bf16_dispatch(const GemmArgs& g, float* ws, hipStream_t st) {
   // 16-byte vectors (along K, or along M/N for a transposed operand) need
   // 8-element-aligned rows, segments and batch strides.
+  // A length not a multiple of 8 is fine when the rows are padded to one: the
+  // last vector then stays inside its row (the K-contiguous loader zeroes the
+  // elements past K; rows past M or N only feed discarded outputs).
   const bool seg_ok = g.kseg == 0 || (g.kseg % 8 == 0 && g.ksA % 8 == 0 && g.ksB % 8 == 0);
-  const bool va = TA ? (g.lda % 8 == 0 && aligned16(g.A) && g.M % 8 == 0 && g.sA % 8 == 0 &&
+  auto fits = [&](int len, int64_t ld) { return len % 8 == 0 || (g.kseg == 0 && ld >= (len + 7) / 8 * 8); };
+  const bool va = TA ? (g.lda % 8 == 0 && aligned16(g.A) && fits(g.M, g.lda) && g.sA % 8 == 0 &&
                         (g.kseg == 0 || g.ksA % 8 == 0))
-                     : (g.lda % 8 == 0 && aligned16(g.A) && g.K % 8 == 0 && g.sA % 8 == 0 && seg_ok);
-  const bool vb = TB ? (g.ldb % 8 == 0 && aligned16(g.B) && g.N % 8 == 0 && g.sB % 8 == 0 &&
+                     : (g.lda % 8 == 0 && aligned16(g.A) && fits(g.K, g.lda) && g.sA % 8 == 0 && seg_ok);
+  const bool vb = TB ? (g.ldb % 8 == 0 && aligned16(g.B) && fits(g.N, g.ldb) && g.sB % 8 == 0 &&
                         (g.kseg == 0 || g.ksB % 8 == 0))
-                     : (g.ldb % 8 == 0 && aligned16(g.B) && g.K % 8 == 0 && g.sB % 8 == 0 && seg_ok);
+                     : (g.ldb % 8 == 0 && aligned16(g.B) && fits(g.K, g.ldb) && g.sB % 8 == 0 && seg_ok);
   if (va && vb) return gemm_bf16_launch<TA, TB, true, true>(g, ws, st);
   if (va) return gemm_bf16_launch<TA, TB, true, false>(g, ws, st);
   if (vb) return gemm_bf16_launch<TA, TB, false, true>(g, ws, st);

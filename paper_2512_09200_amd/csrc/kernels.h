@@ -96,6 +96,11 @@ hipError_t fm_mfma(bool fwd, const void* X, const void* W, int B, int n, int d, 
                    const float* addend, void* dX, float* dX_f32, float* dW, void* ws,
                    hipStream_t s);
 
+// dot_mfma.hip (bf16 MFMA path of the DOT interaction)
+bool dot_mfma_supported(int n, int d);
+hipError_t dot_mfma(bool fwd, const void* X, int B, int n, int d, void* out, int64_t ostride,
+                    int emit0, const void* dout, int64_t dstride, void* dX, hipStream_t s);
+
 // stack.hip (stacked FM -> linear -> residual -> LayerNorm interaction)
 struct StackShape {
   int L, n0, nv, d, k;  // layers, input vectors, vectors per layer output, dim, FM rank

@@ -14,6 +14,13 @@ CASES = {
     "dot-f32-tiny": ("dot", "f32", 128, 9, 32, 0, True, False),
     "dot-bf16-n27": ("dot", "bf16", 300, 27, 64, 0, True, False),
     "dot-bf16-n97-absent": ("dot", "bf16", 96, 97, 128, 0, True, True),
+    # MFMA path (bf16, n <= 128, d in {64, 128}): tile edges, no pairs, many samples per block
+    "dot-bf16-n1": ("dot", "bf16", 40, 1, 64, 0, True, False),
+    "dot-bf16-n2-d128": ("dot", "bf16", 40, 2, 128, 0, False, False),
+    "dot-bf16-n32-d64": ("dot", "bf16", 70, 32, 64, 0, True, False),
+    "dot-bf16-n33-d128": ("dot", "bf16", 70, 33, 128, 0, False, False),
+    "dot-bf16-n64-d128": ("dot", "bf16", 50, 64, 128, 0, True, False),
+    "dot-bf16-n128-d64-many": ("dot", "bf16", 1100, 128, 64, 0, True, False),
     "fm-bf16-n65": ("fm", "bf16", 200, 65, 128, 32, True, False),      # MFMA path
     "fm-bf16-n65-many": ("fm", "bf16", 700, 65, 128, 32, True, False), # > 1 sample per block
     "fm-bf16-n30-d64-k32": ("fm", "bf16", 37, 30, 64, 32, False, False),  # MFMA, other tiles
@@ -26,9 +33,23 @@ CASES = {
 @pytest.mark.gpu
 @pytest.mark.parametrize("name", list(CASES))
 def test_interact_fwd_bwd(name):
-    from paper_2512_09200_amd import api
-    kind, dt, B, n, d, k, emit0, zero_slots = CASES[name]
     print(f"[interact] {name}", flush=True)
+    check_interact(*CASES[name])
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("pad", [1, 3])
+def test_dot_unaligned_row_stride(pad):
+    """Output / gradient rows whose stride is not a multiple of 8 elements
+    (the packed pairs then start off 16-byte alignment)."""
+    print(f"[interact] dot n=97 d=128, row stride padded by {pad}", flush=True)
+    check_interact("dot", "bf16", 33, 97, 128, 0, True, False, pad=pad)
+
+
+def check_interact(kind, dt, B, n, d, k, emit0, zero_slots, pad=0):
+    """Forward and backward of one interaction against the oracle; output
+    rows of stride `stride + pad` (a column slice of a wider buffer)."""
+    from paper_2512_09200_amd import api
     rnd = rounding(dt)
     sdt = synth.torch_dtype(dt)
     t = 1e-5 if dt == "f32" else 2e-2
@@ -42,7 +63,7 @@ def test_interact_fwd_bwd(name):
     width = (n * (n - 1) // 2 if kind == "dot" else n * k)
     off = d if emit0 else 0
     stride = (off + width + 7) // 8 * 8
-    out = torch.full((B, stride), 7.0, dtype=sdt, device=DEV)
+    out = torch.full((B, stride + pad), 7.0, dtype=sdt, device=DEV)[:, :stride]
     api.lattice_interact_fwd(kind, Xd, out, emit_slot0=emit0, fm_W=Wd)
     torch.cuda.synchronize()
     if kind == "dot":
@@ -56,7 +77,8 @@ def test_interact_fwd_bwd(name):
     assert (out[:, off + width:].float() == 7.0).all(), "padding columns touched"
     # backward
     G = synth.randn((B, stride), seed=23, scale=1e-3, dtype=dt)
-    Gd = to_dev(G, sdt)
+    Gd = torch.zeros((B, stride + pad), dtype=sdt, device=DEV)[:, :stride]
+    Gd.copy_(to_dev(G, sdt))
     dX = torch.zeros((B, n, d), dtype=sdt, device=DEV)
     dW = torch.zeros((n, k), device=DEV) if kind == "fm" else None
     api.lattice_interact_bwd(kind, Xd, Gd, dX, emit_slot0=emit0, fm_W=Wd, fm_dW=dW)

@@ -19,7 +19,12 @@ SHAPES = {
     "f32-heads": ("f32", 128, (68, 64, 4), False),
     "f32-bottom": ("f32", 129, (13, 64, 32), True),
     "bf16-deep-k": ("bf16", 512, (2208, 1024, 16), False),
+    # input rows padded to 8 elements (NaN in the padding): vector loads of
+    # the last partial vector must not let the padding into the contraction
+    "bf16-padded-in-415": ("bf16", 300, (415, 512, 256, 8), False),
+    "bf16-padded-in-13": ("bf16", 260, (13, 256, 64), True),
 }
+PADDED = {"bf16-padded-in-415", "bf16-padded-in-13"}
 
 
 def _layers(dt, dims, seed):
@@ -46,6 +51,11 @@ def test_mlp_fwd_bwd(name):
     L = [dict(W=to_dev(W, sdt), b=to_dev(b), dW=torch.zeros(W.shape, device=DEV),
               db=torch.zeros(b.shape, device=DEV)) for W, b in layers]
     xd = to_dev(x, sdt)
+    if name in PADDED:
+        ld = (dims[0] + 7) // 8 * 8
+        buf = torch.full((B, ld), float("nan"), dtype=sdt, device=DEV)
+        buf[:, :dims[0]] = xd
+        xd = buf[:, :dims[0]]
     acts = [torch.empty((B, dims[i + 1]), dtype=(torch.float32 if (i == len(layers) - 1 and not relu_last) else sdt),
                         device=DEV) for i in range(len(layers))]
     loss = None
