@@ -131,14 +131,17 @@ __device__ inline int64_t koff(const Opnd& o, int k) {
 }
 
 // --- operand tile loaders: fill S[rows][GLD] (k contiguous) for rows r0.., k k0.. ---
-// K-contiguous, 16-byte vectors: 128 rows x 64 k = 8 vectors per row, 4 per thread.
+// K-contiguous, 16-byte vectors: ROWS rows x 64 k = 8 vectors per row,
+// ROWS / 32 per thread.
+template <int ROWS = GBM, int THREADS = 256>
 struct LoadK {
-  u32x4 r[4];
+  static constexpr int NV = ROWS * 8 / THREADS;
+  u32x4 r[NV];
   // edge: the tile may reach past R rows or K columns (uniform per block and step)
   __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool edge) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int v = threadIdx.x + i * 256;
+    for (int i = 0; i < NV; ++i) {
+      const int v = threadIdx.x + i * THREADS;
       const int rr = v >> 3, kc = (v & 7) * 8;
       const int gr = r0 + rr, gk = k0 + kc;
       if (!edge || (gr < R && gk < K)) {
@@ -156,8 +159,8 @@ struct LoadK {
   }
   __device__ inline void store(bf16_t* S) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int v = threadIdx.x + i * 256;
+    for (int i = 0; i < NV; ++i) {
+      const int v = threadIdx.x + i * THREADS;
       *reinterpret_cast<u32x4*>(S + (v >> 3) * GLD + (v & 7) * 8) = r[i];
     }
   }
@@ -167,28 +170,38 @@ struct LoadK {
 // per row (8-byte LDS writes).  Wave w, lane l: row group mg = 4w + l/16,
 // k group kg = l%16, so one load instruction reads 64 contiguous bytes of
 // each of 16 k-rows, and the 16 lanes of a group write one row's 128 bytes.
+// In general item it = thread + q * THREADS is row group it / 16, k group
+// it % 16 (ROWS / 8 row groups x 16 k groups).
+template <int ROWS = GBM, int THREADS = 256>
 struct LoadMN {
-  u32x4 r[4];
+  static constexpr int NI = ROWS * 2 / THREADS;
+  u32x4 r[NI][4];
   __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool edge) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int gr = r0 + (4 * w + (lane >> 4)) * 8, kb = k0 + (lane & 15) * 4;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int gk = kb + i;
-      if (!edge || (gk < K && gr < R)) r[i] = ldg16(o.p + koff<true>(o, gk) + gr);
-      else r[i] = u32x4{0, 0, 0, 0};
+    for (int q = 0; q < NI; ++q) {
+      const int it = threadIdx.x + q * THREADS;
+      const int gr = r0 + (it >> 4) * 8, kb = k0 + (it & 15) * 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int gk = kb + i;
+        if (!edge || (gk < K && gr < R)) r[q][i] = ldg16(o.p + koff<true>(o, gk) + gr);
+        else r[q][i] = u32x4{0, 0, 0, 0};
+      }
     }
   }
   __device__ inline void store(bf16_t* S) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    bf16_t* s = S + ((4 * w + (lane >> 4)) * 8) * GLD + (lane & 15) * 4;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      // row j of the group: (k0, k1, k2, k3) = half (j & 1) of word j/2 of r[0..3]
-      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-      const uint32_t lo = __builtin_amdgcn_perm(r[1][j >> 1], r[0][j >> 1], sel);
-      const uint32_t hi = __builtin_amdgcn_perm(r[3][j >> 1], r[2][j >> 1], sel);
-      *reinterpret_cast<uint2*>(s + j * GLD) = uint2{lo, hi};
+    for (int q = 0; q < NI; ++q) {
+      const int it = threadIdx.x + q * THREADS;
+      bf16_t* s = S + ((it >> 4) * 8) * GLD + (it & 15) * 4;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        // row j of the group: (k0, k1, k2, k3) = half (j & 1) of word j/2 of r[q][0..3]
+        const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t lo = __builtin_amdgcn_perm(r[q][1][j >> 1], r[q][0][j >> 1], sel);
+        const uint32_t hi = __builtin_amdgcn_perm(r[q][3][j >> 1], r[q][2][j >> 1], sel);
+        *reinterpret_cast<uint2*>(s + j * GLD) = uint2{lo, hi};
+      }
     }
   }
 };
@@ -240,8 +253,8 @@ struct LoadElem {
   }
 };
 template <bool MN, bool VEC> struct LoaderSel;
-template <> struct LoaderSel<false, true> { using T = LoadK; };
-template <> struct LoaderSel<true, true> { using T = LoadMN; };
+template <> struct LoaderSel<false, true> { using T = LoadK<>; };
+template <> struct LoaderSel<true, true> { using T = LoadMN<>; };
 template <bool MN> struct LoaderSel<MN, false> { using T = LoadElem<MN>; };
 
 // 64 k of MFMAs on the staged tiles: each wave 2x2 fragments of 32x32.
@@ -435,6 +448,174 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   epi_store<CT>(C, ldc, row, col, s, epi, 0);
 }
 
+// --- large products: block tile 256x256, 4 waves of 128x128 (4x4 fragments) ---
+// Twice the MFMA work per byte read from LDS of the 128x128 kernel (whose
+// 64x64 wave tiles keep the LDS port as busy as the matrix cores), for
+// products with enough 256x256 tiles to fill the chip.  Same staging (two
+// register and two LDS stages, 16-byte vector loaders only), same epilogue;
+// the fp32 tile is staged through LDS in two halves of 128 rows.  No split-K
+// and no batching.
+constexpr int BBM = 256, BBN = 256, BCLD = BBN + 4;
+constexpr size_t GEMM_BIG_LDS = (size_t)2 * (BBM + BBN) * GLD * sizeof(uint16_t);  // 147,456 B
+static_assert((size_t)(BBM / 2) * BCLD * sizeof(float) <= GEMM_BIG_LDS, "C staging must fit");
+
+// NW waves as 2 (M) x NW/2 (N): each wave 128 x 1024/NW, 4 x FN fragments
+template <bool MN, int THREADS> struct BigLoader;
+template <int THREADS> struct BigLoader<false, THREADS> { using T = LoadK<BBM, THREADS>; };
+template <int THREADS> struct BigLoader<true, THREADS> { using T = LoadMN<BBM, THREADS>; };
+
+template <int FN>
+__device__ inline void mma_big_k64(const bf16_t* As, const bf16_t* Bs, int wm, int wn, int lane,
+                                   f32x16 (&acc)[4][FN]) {
+  const int frow = lane & 31, fk = (lane >> 5) * 8;
+  const bf16_t* as = As + (wm * 128 + frow) * GLD + fk;
+  const bf16_t* bs = Bs + (wn * FN * 32 + frow) * GLD + fk;
+#pragma unroll
+  for (int ks = 0; ks < GBK; ks += 16) {
+    bf16x8 a[4], b[FN];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8*>(as + i * 32 * GLD + ks);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) b[j] = *reinterpret_cast<const bf16x8*>(bs + j * 32 * GLD + ks);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  }
+}
+
+template <bool TA, bool TB, typename CT, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, CT* __restrict__ C,
+                                                              int64_t ldc, int M, int N, int K,
+                                                              Epi epi, int vec,
+                                                              float* __restrict__ rowsum) {
+  constexpr int THREADS = NW * 64;
+  constexpr int FN = 8 / NW * 2;  // fragments along N per wave: 4 (4 waves) or 2 (8 waves)
+  extern __shared__ __attribute__((aligned(16))) unsigned char gemm_smem[];
+  bf16_t* As[2];
+  bf16_t* Bs[2];
+  As[0] = reinterpret_cast<bf16_t*>(gemm_smem);
+  Bs[0] = As[0] + BBM * GLD;
+  As[1] = Bs[0] + BBN * GLD;
+  Bs[1] = As[1] + BBM * GLD;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w / (NW / 2), wn = w % (NW / 2);
+  const int tiles_n = (N + BBN - 1) / BBN;
+  const int tile = xcd_block(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * BBM, n0 = (tile % tiles_n) * BBN;
+
+  f32x16 acc[4][FN];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  typename BigLoader<TA, THREADS>::T la0, la1;
+  typename BigLoader<TB, THREADS>::T lb0, lb1;
+  const int ktiles = (K + GBK - 1) / GBK;
+  const bool edge_m = m0 + BBM > M, edge_n = n0 + BBN > N;
+  auto load = [&](auto& la, auto& lb, int kt) {
+    const int k0 = kt * GBK;
+    const bool edge_k = k0 + GBK > K;
+    la.load(A, M, K, m0, k0, edge_m || edge_k);
+    lb.load(Bm, N, K, n0, k0, edge_n || edge_k);
+  };
+  // row sums of A (blocks of the first N tile): THREADS / 256 threads per
+  // row, each adding 64 / (THREADS / 256) consecutive k
+  constexpr int TPR = THREADS / BBM;
+  const bool rs_on = rowsum != nullptr && n0 == 0;
+  float rs = 0.f;
+  auto rowsum_step = [&](const bf16_t* as) {
+    if (rs_on) {
+      const bf16_t* p = as + (threadIdx.x / TPR) * GLD + (threadIdx.x % TPR) * (GBK / TPR);
+#pragma unroll
+      for (int v = 0; v < GBK / TPR / 8; ++v) {
+        const u32x4 x = *reinterpret_cast<const u32x4*>(p + v * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          rs += __uint_as_float(x[e] << 16);
+          rs += __uint_as_float(x[e] & 0xffff0000u);
+        }
+      }
+    }
+  };
+  if (ktiles > 0) load(la0, lb0, 0);
+  if (ktiles > 1) load(la1, lb1, 1);
+  if (ktiles > 0) {
+    la0.store(As[0]);
+    lb0.store(Bs[0]);
+  }
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 2 <= ktiles; kt += 2) {
+    if (kt + 2 < ktiles) load(la0, lb0, kt + 2);
+    mma_big_k64<FN>(As[0], Bs[0], wm, wn, lane, acc);
+    rowsum_step(As[0]);
+    la1.store(As[1]);
+    lb1.store(Bs[1]);
+    __syncthreads();
+    if (kt + 3 < ktiles) load(la1, lb1, kt + 3);
+    mma_big_k64<FN>(As[1], Bs[1], wm, wn, lane, acc);
+    rowsum_step(As[1]);
+    if (kt + 2 < ktiles) {
+      la0.store(As[0]);
+      lb0.store(Bs[0]);
+    }
+    __syncthreads();
+  }
+  if (kt < ktiles) {
+    mma_big_k64<FN>(As[0], Bs[0], wm, wn, lane, acc);
+    rowsum_step(As[0]);
+    __syncthreads();
+  }
+  if (rs_on) {
+    if (TPR == 2) rs += __shfl_xor(rs, 1, 64);  // the two halves of the row, fixed order
+    const int row = m0 + threadIdx.x / TPR;
+    if (threadIdx.x % TPR == 0 && row < M) rowsum[row] = rs;
+  }
+
+  // epilogue in two halves of 128 rows: the waves of row half h stage their
+  // fp32 fragments, then all threads write the half's rows, 8 columns each
+  float* Cs = reinterpret_cast<float*>(gemm_smem);
+#pragma unroll 1
+  for (int h = 0; h < 2; ++h) {
+    if (wm == h) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int cl = wn * FN * 32 + j * 32 + (lane & 31);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int rl = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            Cs[rl * BCLD + cl] = acc[i][j][r];
+          }
+        }
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int q = 0; q < (BBM / 2) * BBN / 8 / THREADS; ++q) {
+      const int chunk = threadIdx.x + q * THREADS;
+      const int rl = chunk / (BBN / 8), cl = (chunk % (BBN / 8)) * 8;
+      const int row = m0 + h * 128 + rl, col = n0 + cl;
+      if (row >= M || col >= N) continue;
+      float v[8];
+      ld8f(Cs + rl * BCLD + cl, v);
+      if (vec && col + 8 <= N) {
+        epi_store8<CT>(C, ldc, row, col, v, epi, 0);
+      } else {
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (col + t < N) epi_store<CT>(C, ldc, row, col + t, v[t], epi, 0);
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // --- fp32 VALU GEMM (fp32 workloads): 64x64 tile, 4x4 per thread, any layout ---
 template <typename CT>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, int64_t lda,
@@ -519,8 +700,43 @@ static int epi_vec_ok(const GemmArgs& g) {
   return 1;
 }
 
+// The 256x256 kernel takes products with vector loaders and at least one
+// full wave of its tiles (and no batching).
+static bool gemm_use_big(const GemmArgs& g) {
+  return g.batch <= 1 && (int64_t)cdiv(g.M, BBM) * cdiv(g.N, BBN) >= 256;
+}
+
+template <bool TA, bool TB>
+static hipError_t gemm_big_launch(const GemmArgs& g, hipStream_t st) {
+  constexpr int NW = 4;  // 8 waves of 128x64 measured slower
+  Epi epi = make_epi(g);
+  Opnd a{(const bf16_t*)g.A, g.lda, g.kseg, g.ksA};
+  Opnd b{(const bf16_t*)g.B, g.ldb, g.kseg, g.ksB};
+  const int vec = epi_vec_ok(g);
+  const dim3 grid(cdiv(g.N, BBN) * cdiv(g.M, BBM));
+  static std::once_flag once_bf, once_f;
+  if (g.c_dt == DT_BF16) {
+    auto k = gemm_big_kernel<TA, TB, bf16_t, NW>;
+    std::call_once(once_bf, [&] {
+      (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_BIG_LDS);
+    });
+    k<<<grid, NW * 64, GEMM_BIG_LDS, st>>>(a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, epi, vec, g.rowsum);
+  } else {
+    auto k = gemm_big_kernel<TA, TB, float, NW>;
+    std::call_once(once_f, [&] {
+      (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_BIG_LDS);
+    });
+    k<<<grid, NW * 64, GEMM_BIG_LDS, st>>>(a, b, (float*)g.C, g.ldc, g.M, g.N, g.K, epi, vec, g.rowsum);
+  }
+  LAT_LAUNCH_CHECK();
+  return hipSuccess;
+}
+
 template <bool TA, bool TB, bool VA, bool VB>
 static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st) {
+  if constexpr (VA && VB) {
+    if (gemm_use_big(g)) return gemm_big_launch<TA, TB>(g, st);
+  }
   const int splits = gemm_splits(g);
   if (splits > 1 && !ws) {
     set_error("split-K GEMM without a workspace");

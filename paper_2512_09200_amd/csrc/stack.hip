@@ -13,6 +13,10 @@
 
 namespace lat {
 
+// The weight gradients summed over samples (dW, dC) have tiny outputs and a
+// contraction over B*d: split K widely so the whole chip takes part.
+constexpr int SAMPLE_SUM_SPLITS = 256;
+
 // ---------------------------------------------------------------------------
 // LayerNorm over d (= 64*E elements per vector), one wave per vector
 // ---------------------------------------------------------------------------
@@ -111,14 +115,22 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(
     dgamma_part[(int64_t)blockIdx.x * D + a] = red[0][a] + red[1][a] + red[2][a] + red[3][a];
 }
 
+// out[i] = sum over p of part[p][i]: one block per output, thread t adds
+// parts t, t + 256, ..., then a fixed-shape tree (deterministic order).
 __global__ __launch_bounds__(256) void stack_sum_parts_kernel(const float* __restrict__ part,
                                                               int parts, int64_t len,
                                                               float* __restrict__ out) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= len) return;
+  __shared__ float red[256];
+  const int64_t i = blockIdx.x;
   float s = 0.f;
-  for (int p = 0; p < parts; ++p) s += part[(int64_t)p * len + i];
-  out[i] = s;
+  for (int p = threadIdx.x; p < parts; p += 256) s += part[(int64_t)p * len + i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[i] = red[0];
 }
 
 constexpr int LN_BWD_BLOCKS = 1024;
@@ -160,6 +172,7 @@ StackPlan stack_plan(const StackShape& sh, int B) {
     g.max_splits = 16;
     g.M = (int)nvd; g.N = n * sh.k; g.K = B;
     gw = gw > gemm_workspace(g) ? gw : gemm_workspace(g);
+    g.max_splits = SAMPLE_SUM_SPLITS;
     g.M = n; g.N = sh.k; g.K = B * sh.d;
     gw = gw > gemm_workspace(g) ? gw : gemm_workspace(g);
     if (l == 0 && sh.has_C0) {
@@ -200,7 +213,7 @@ static hipError_t ln_bwd_launch(int E, const float* H, const RT* res, const floa
   else if (E == 2) ln_bwd_kernel<2, RT, YT><<<grid, 256, 0, s>>>(H, res, gamma, mean, rstd, dY, dy_stride, nvec, nv, du, duR, dgp);
   else ln_bwd_kernel<4, RT, YT><<<grid, 256, 0, s>>>(H, res, gamma, mean, rstd, dY, dy_stride, nvec, nv, du, duR, dgp);
   LAT_LAUNCH_CHECK();
-  stack_sum_parts_kernel<<<cdiv(d, 256), 256, 0, s>>>(dgp, grid, d, dgamma);
+  stack_sum_parts_kernel<<<d, 256, 0, s>>>(dgp, grid, d, dgamma);
   LAT_LAUNCH_CHECK();
   return hipSuccess;
 }
@@ -362,7 +375,7 @@ hipError_t stack_bwd(const StackShape& sh, const StackLayer* Ls, int B, const vo
     w1.A = Xl; w1.lda = d; w1.kseg = d; w1.ksA = (int64_t)n * d;
     w1.B = dP; w1.ldb = k; w1.tb = 1; w1.ksB = (int64_t)d * k;
     w1.C = Ls[l].dW; w1.ldc = k; w1.c_dt = DT_F32;
-    w1.M = n; w1.N = k; w1.K = B * d; w1.max_splits = 16;
+    w1.M = n; w1.N = k; w1.K = B * d; w1.max_splits = SAMPLE_SUM_SPLITS;
     STK_CHECK(gemm(w1, gws, s));
     if (c_res) {
       // dC = sum_b duR_b X_b^T: M = nv (v), N = n0 (u), K = (b, a)
@@ -370,7 +383,7 @@ hipError_t stack_bwd(const StackShape& sh, const StackLayer* Ls, int B, const vo
       c1.A = duR; c1.lda = d; c1.kseg = d; c1.ksA = nvd;
       c1.B = Xl; c1.ldb = d; c1.ksB = (int64_t)sh.n0 * d;
       c1.C = Ls[0].dC; c1.ldc = sh.n0; c1.c_dt = DT_F32;
-      c1.M = nv; c1.N = sh.n0; c1.K = B * d; c1.max_splits = 16;
+      c1.M = nv; c1.N = sh.n0; c1.K = B * d; c1.max_splits = SAMPLE_SUM_SPLITS;
       STK_CHECK(gemm(c1, gws, s));
       // dX_b = C^T duR_b + dXf_b: M = n0 (u), N = d (a), K = nv (v)
       GemmArgs c2;

@@ -23,6 +23,10 @@ SHAPES = {
     # the last partial vector must not let the padding into the contraction
     "bf16-padded-in-415": ("bf16", 300, (415, 512, 256, 8), False),
     "bf16-padded-in-13": ("bf16", 260, (13, 256, 64), True),
+    # products with >= 256 tiles of 256x256 (the large-tile kernel): forward
+    # with bias + ReLU, and the second layer's input gradient with the ReLU
+    # mask; ragged M, N and K edges
+    "bf16-big-tiles": ("bf16", 4100, (1032, 4104, 8), False),
 }
 PADDED = {"bf16-padded-in-415", "bf16-padded-in-13"}
 
