@@ -700,10 +700,18 @@ static int epi_vec_ok(const GemmArgs& g) {
   return 1;
 }
 
-// The 256x256 kernel takes products with vector loaders and at least one
-// full wave of its tiles (and no batching).
+// The 256x256 kernel takes products with vector loaders (and no batching)
+// when its estimated time is lower.  In units of one CU doing a 128x128xK
+// tile alone at the small kernel's rate: the small kernel runs waves of 512
+// tiles (two blocks per CU, K / splits each), 2K / splits per wave; the large
+// kernel runs waves of 256 tiles (one per CU, no split) of four times the
+// work at about 1.3x the rate, 3.08K per wave.
 static bool gemm_use_big(const GemmArgs& g) {
-  return g.batch <= 1 && (int64_t)cdiv(g.M, BBM) * cdiv(g.N, BBN) >= 256;
+  if (g.batch > 1) return false;
+  const int64_t s = gemm_splits(g);
+  const int64_t big_waves = cdiv((int64_t)cdiv(g.M, BBM) * cdiv(g.N, BBN), 256);
+  const int64_t small_waves = cdiv((int64_t)cdiv(g.M, GBM) * cdiv(g.N, GBN) * s, 512);
+  return 308 * big_waves * s < 200 * small_waves;
 }
 
 template <bool TA, bool TB>
