@@ -1,6 +1,6 @@
 // Factorization-machine block O_b = X_b (X_b^T W) (Section 3.3.2) on bf16 MFMA
-// (v_mfma_f32_32x32x16_bf16), forward and backward, for n <= 96 vectors,
-// d in {64, 128}, rank k in {32, 64}.
+// (v_mfma_f32_32x32x16_bf16), forward and backward, for up to 96 vectors in
+// tiles (97 with a head row, below), d in {64, 128}, rank k in {32, 64}.
 //
 // Each block of 8 waves loops over samples.  A sample's X [n, d] is read once
 // with coalesced 4-byte loads (8 rows x 2 columns per thread) into registers
@@ -15,38 +15,83 @@
 //             dW += X dP accumulates in the waves' registers across the
 //             block's samples (fixed order), and the per-block partials are
 //             summed in block order afterwards.
+// Head row: when n = 32 t + 1 (the dense vector plus 32 t features), row 0 is
+// taken out of the tiles (HEAD): the MFMA tiles cover rows 1 .. n-1 exactly
+// instead of padding to the next multiple of 32, and row 0's rank-1 terms
+// (x0^T w0, x0^T g0) and its own outputs (O[0], dX[0], dW[0]) are a few
+// hundred FMAs per sample on the vector units, reduced in a fixed order.
 #include "common.h"
 #include "kernels.h"
 #include "mfma_tile.h"
 
 namespace lat {
 
-template <int NP, int D, int K>
+// sum over the 16 lanes of an aligned lane group, in a fixed butterfly order
+__device__ inline float group16_sum(float v) {
+  v += __shfl_xor(v, 8, 64);
+  v += __shfl_xor(v, 4, 64);
+  v += __shfl_xor(v, 2, 64);
+  v += __shfl_xor(v, 1, 64);
+  return v;
+}
+
+// Head row in registers one sample ahead: thread t < COLS/2 holds columns
+// 2t, 2t+1 of row 0 (bf16 pair).
+template <int COLS>
+struct HeadRow {
+  uint32_t v = 0;
+  __device__ inline void load(const bf16_t* __restrict__ g) {
+    if (threadIdx.x < COLS / 2) v = *reinterpret_cast<const uint32_t*>(g + 2 * threadIdx.x);
+  }
+  __device__ inline void store(float* dst) const {
+    if (threadIdx.x < COLS / 2) {
+      dst[2 * threadIdx.x] = __uint_as_float(v << 16);
+      dst[2 * threadIdx.x + 1] = __uint_as_float(v & 0xffff0000u);
+    }
+  }
+};
+
+template <int NP, int D, int K, bool HEAD>
 __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restrict__ X,
                                                           const bf16_t* __restrict__ W, int B,
                                                           int n, bf16_t* __restrict__ out,
                                                           int64_t ostride, int emit0) {
   constexpr int LX = D + 8, LT = NP + 8, LP = D + 8, LR = K + 8;
+  constexpr int H = HEAD ? 1 : 0;  // rows ahead of the MFMA rows
   __shared__ __attribute__((aligned(16))) bf16_t Xs[NP * LX];
   __shared__ __attribute__((aligned(16))) bf16_t XT[D * LT];
   __shared__ __attribute__((aligned(16))) bf16_t PT[K * LP];
   __shared__ __attribute__((aligned(16))) bf16_t WR[NP * LR];
   __shared__ __attribute__((aligned(16))) bf16_t WT[K * LT];
+  __shared__ float X0[HEAD ? D : 1], W0[HEAD ? K : 1];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nm = n - H;  // rows in the tiles
   {
     Stager<NP, K, 512> sw;
-    sw.load(W, K, n);
+    sw.load(W + H * K, K, nm);
     sw.store(WR, LR, WT, LT);
+    if (HEAD)
+      for (int c = threadIdx.x; c < K; c += blockDim.x) W0[c] = bf2f(W[c]);
   }
   const int off = emit0 ? D : 0;
   Stager<NP, D, 512> sx;
-  if (blockIdx.x < B) sx.load(X + (int64_t)blockIdx.x * n * D, D, n);
+  HeadRow<D> hx;
+  if (blockIdx.x < B) {
+    const bf16_t* xb = X + (int64_t)blockIdx.x * n * D;
+    sx.load(xb + H * D, D, nm);
+    if (HEAD) hx.load(xb);
+  }
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
     sx.store(Xs, LX, XT, LT);
+    if (HEAD) hx.store(X0);
     __syncthreads();
     // the next sample's X is in flight while this one is computed
-    if (b + (int)gridDim.x < B) sx.load(X + (int64_t)(b + gridDim.x) * n * D, D, n);
-    // P[a][c] = sum_j X^T[a][j] W^T[c][j]; tile (ta, tc) per wave
+    if (b + (int)gridDim.x < B) {
+      const bf16_t* xb = X + (int64_t)(b + gridDim.x) * n * D;
+      sx.load(xb + H * D, D, nm);
+      if (HEAD) hx.load(xb);
+    }
+    // P[a][c] = sum_j X^T[a][j] W^T[c][j] (+ x0[a] w0[c]); tile (ta, tc) per wave
     constexpr int PT_TILES = (D / 32) * (K / 32);
     for (int t = w; t < PT_TILES; t += 8) {
       const int ta = t / (K / 32), tc = t % (K / 32);
@@ -55,7 +100,11 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
       mfma_tile<NP>(acc, XT + ta * 32 * LT, LT, WT + tc * 32 * LT, LT);
       const int c = tc * 32 + (lane & 31);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) PT[c * LP + ta * 32 + frag_row(r)] = f2bf(acc[r]);
+      for (int r = 0; r < 16; ++r) {
+        const int a = ta * 32 + frag_row(r);
+        const float v = HEAD ? acc[r] + X0[a] * W0[c] : acc[r];
+        PT[c * LP + a] = f2bf(v);
+      }
     }
     __syncthreads();
     // O[j][c] = sum_a X[j][a] P^T[c][a]
@@ -70,22 +119,40 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = tj * 32 + frag_row(r);
-        if (j < n) ob[off + j * K + c] = f2bf(acc[r]);
+        if (j < nm) ob[off + (j + H) * K + c] = f2bf(acc[r]);
       }
     }
-    if (emit0)
+    if (HEAD) {
+      // O[0][c] = sum_a x0[a] P[a][c]: 16 lanes per c, D/16 terms each
+      const int q = threadIdx.x & 15;
+#pragma unroll
+      for (int c = threadIdx.x >> 4; c < K; c += 32) {
+        float sum = 0.f;
+#pragma unroll
+        for (int i = 0; i < D / 16; ++i) {
+          const int a = q * (D / 16) + i;
+          sum += X0[a] * bf2f(PT[c * LP + a]);
+        }
+        sum = group16_sum(sum);
+        if (q == 0) ob[off + c] = f2bf(sum);
+      }
+      if (emit0)
+        for (int a = threadIdx.x; a < D; a += blockDim.x) ob[a] = f2bf(X0[a]);
+    } else if (emit0) {
       for (int a = threadIdx.x; a < D; a += blockDim.x) ob[a] = Xs[a];
+    }
     __syncthreads();
   }
 }
 
 // Backward.  dX_f32 (optional) receives the unrounded fp32 dX instead of dX.
-template <int NP, int D, int K>
+template <int NP, int D, int K, bool HEAD>
 __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int B, int n,
     const bf16_t* __restrict__ dout, int64_t dstride, int emit0, const float* __restrict__ addend,
     bf16_t* __restrict__ dX, float* __restrict__ dX_f32, float* __restrict__ dw_part) {
   constexpr int LX = D + 8, LT = NP + 8, LG = 2 * K + 8, LPD = 2 * K + 8, LDT = D + 8;
+  constexpr int H = HEAD ? 1 : 0;
   __shared__ __attribute__((aligned(16))) bf16_t Xs[NP * LX];
   __shared__ __attribute__((aligned(16))) bf16_t XT[D * LT];
   __shared__ __attribute__((aligned(16))) bf16_t PT_[K * LDT];  // dP^T [K][LDT]
@@ -93,35 +160,55 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
   __shared__ __attribute__((aligned(16))) bf16_t GT[K * LT];
   __shared__ __attribute__((aligned(16))) bf16_t WT[K * LT];
   __shared__ __attribute__((aligned(16))) bf16_t PD[D * LPD];   // [a][ P (K) | dP (K) ]
+  __shared__ float X0[HEAD ? D : 1], GW0[HEAD ? 2 * K : 1];    // head row: x0, [g0 | w0]
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nm = n - H;
   {
     Stager<NP, K, 512> sw;
-    sw.load(W, K, n);
+    sw.load(W + H * K, K, nm);
     sw.store(GW + K, LG, WT, LT);
+    if (HEAD)
+      for (int c = threadIdx.x; c < K; c += blockDim.x) GW0[K + c] = bf2f(W[c]);
   }
   constexpr int DW_TILES = (NP / 32) * (K / 32);
   f32x16 dw[(DW_TILES + 7) / 8];
 #pragma unroll
   for (int i = 0; i < (DW_TILES + 7) / 8; ++i) zero16(dw[i]);
+  // head row of dW, accumulated over the block's samples: lane group
+  // tid / 16 owns columns c = tid / 16 + 32 i
+  float dw0[(K + 31) / 32];
+#pragma unroll
+  for (int i = 0; i < (K + 31) / 32; ++i) dw0[i] = 0.f;
   const int off = emit0 ? D : 0;
   Stager<NP, D, 512> sx;
   Stager<NP, K, 512> sg;
-  if (blockIdx.x < B) {
-    sx.load(X + (int64_t)blockIdx.x * n * D, D, n);
-    sg.load(dout + (int64_t)blockIdx.x * dstride + off, K, n);
-  }
+  HeadRow<D> hx;
+  HeadRow<K> hg;
+  auto prefetch = [&](int bb) {
+    const bf16_t* xb = X + (int64_t)bb * n * D;
+    const bf16_t* gb = dout + (int64_t)bb * dstride + off;
+    sx.load(xb + H * D, D, nm);
+    sg.load(gb + H * K, K, nm);
+    if (HEAD) {
+      hx.load(xb);
+      hg.load(gb);
+    }
+  };
+  if (blockIdx.x < B) prefetch(blockIdx.x);
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
     const bf16_t* gb = dout + (int64_t)b * dstride;
     sx.store(Xs, LX, XT, LT);
     sg.store(GW, LG, GT, LT);
+    if (HEAD) {
+      hx.store(X0);
+      hg.store(GW0);
+    }
     __syncthreads();
     // the next sample's X and G are in flight while this one is computed
-    if (b + (int)gridDim.x < B) {
-      sx.load(X + (int64_t)(b + gridDim.x) * n * D, D, n);
-      sg.load(dout + (int64_t)(b + gridDim.x) * dstride + off, K, n);
-    }
+    if (b + (int)gridDim.x < B) prefetch(b + gridDim.x);
     // P = X^T W and dP = X^T G into PD[a][P | dP], and dP^T[c][a] = G^T X
-    // into DT (the dW operand), all rounded to bf16
+    // into DT (the dW operand), all rounded to bf16 (+ the head row's
+    // rank-1 terms)
     constexpr int P_TILES = (D / 32) * (K / 32);
     bf16_t* DT = PT_;
     for (int t = w; t < 3 * P_TILES; t += 8) {
@@ -131,19 +218,30 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
       if (which < 2) {
         const int ta = tt / (K / 32), tc = tt % (K / 32);
         mfma_tile<NP>(acc, XT + ta * 32 * LT, LT, (which ? GT : WT) + tc * 32 * LT, LT);
-        const int c = tc * 32 + (lane & 31) + which * K;
+        const int c = tc * 32 + (lane & 31);
+        const float h = HEAD ? GW0[which ? c : K + c] : 0.f;  // g0[c] or w0[c]
 #pragma unroll
-        for (int r = 0; r < 16; ++r) PD[(ta * 32 + frag_row(r)) * LPD + c] = f2bf(acc[r]);
+        for (int r = 0; r < 16; ++r) {
+          const int a = ta * 32 + frag_row(r);
+          const float v = HEAD ? acc[r] + X0[a] * h : acc[r];
+          PD[a * LPD + c + which * K] = f2bf(v);
+        }
       } else {
         const int tc = tt / (D / 32), ta = tt % (D / 32);
         mfma_tile<NP>(acc, GT + tc * 32 * LT, LT, XT + ta * 32 * LT, LT);
         const int a = ta * 32 + (lane & 31);
+        const float x0 = HEAD ? X0[a] : 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) DT[(tc * 32 + frag_row(r)) * LDT + a] = f2bf(acc[r]);
+        for (int r = 0; r < 16; ++r) {
+          const int c = tc * 32 + frag_row(r);
+          const float v = HEAD ? acc[r] + GW0[c] * x0 : acc[r];
+          DT[c * LDT + a] = f2bf(v);
+        }
       }
     }
     __syncthreads();
     // dX[j][a] = sum_kk GW[j][kk] PD[a][kk]  (+ addend, + slot-0 gradient)
+    const int64_t sbase = (int64_t)b * n * D;  // this sample's [n, D] block
     constexpr int DX_TILES = (NP / 32) * (D / 32);
     for (int t = w; t < DX_TILES; t += 8) {
       const int tj = t / (D / 32), ta = t % (D / 32);
@@ -151,18 +249,38 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
       zero16(acc);
       mfma_tile<2 * K>(acc, GW + tj * 32 * LG, LG, PD + ta * 32 * LPD, LPD);
       const int a = ta * 32 + (lane & 31);
-      const int64_t sbase = (int64_t)b * n * D;  // this sample's [n, D] block
-      const float g0 = (emit0 && tj == 0) ? bf2f(gb[a]) : 0.f;
+      const float g0 = (!HEAD && emit0 && tj == 0) ? bf2f(gb[a]) : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = tj * 32 + frag_row(r);
-        if (j < n) {
+        if (j < nm) {
           float v = acc[r];
-          const int e = j * D + a;
+          const int e = (j + H) * D + a;
           if (addend) v += addend[sbase + e];
-          if (j == 0) v += g0;
+          if (!HEAD && j == 0) v += g0;
           if (dX_f32) dX_f32[sbase + e] = v;
           else dX[sbase + e] = f2bf(v);
+        }
+      }
+    }
+    if (HEAD) {
+      // dX[0][a] = sum_kk [g0 | w0][kk] PD[a][kk]: 4 lanes per a, K/2 terms
+      // each, then the slot-0 gradient and the addend
+      const int a = threadIdx.x >> 2, q = threadIdx.x & 3;
+      if (a < D) {
+        float sum = 0.f;
+#pragma unroll
+        for (int i = 0; i < 2 * K / 4; ++i) {
+          const int kk = q * (2 * K / 4) + i;
+          sum += GW0[kk] * bf2f(PD[a * LPD + kk]);
+        }
+        sum += __shfl_xor(sum, 2, 64);
+        sum += __shfl_xor(sum, 1, 64);
+        if (q == 0) {
+          if (addend) sum += addend[sbase + a];
+          if (emit0) sum += bf2f(gb[a]);
+          if (dX_f32) dX_f32[sbase + a] = sum;
+          else dX[sbase + a] = f2bf(sum);
         }
       }
     }
@@ -170,6 +288,23 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
     for (int t = w, i = 0; t < DW_TILES; t += 8, ++i) {
       const int tj = t / (K / 32), tc = t % (K / 32);
       mfma_tile<D>(dw[i], Xs + tj * 32 * LX, LX, DT + tc * 32 * LDT, LDT);
+    }
+    if (HEAD) {
+      // dW[0][c] += sum_a x0[a] dP[a][c]: 16 lanes per c
+      const int q = threadIdx.x & 15;
+#pragma unroll
+      for (int i0 = 0; i0 < (K + 31) / 32; ++i0) {
+        const int c = (threadIdx.x >> 4) + 32 * i0;
+        if (c < K) {
+          float sum = 0.f;
+#pragma unroll
+          for (int i = 0; i < D / 16; ++i) {
+            const int a = q * (D / 16) + i;
+            sum += X0[a] * bf2f(DT[c * LDT + a]);
+          }
+          dw0[i0] += group16_sum(sum);
+        }
+      }
     }
     __syncthreads();
   }
@@ -179,9 +314,15 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int j = tj * 32 + frag_row(r);
-      if (j < n) dw_part[((int64_t)blockIdx.x * n + j) * K + c] = dw[i][r];
+      if (j < nm) dw_part[((int64_t)blockIdx.x * n + j + H) * K + c] = dw[i][r];
     }
   }
+  if (HEAD && (threadIdx.x & 15) == 0)
+#pragma unroll
+    for (int i0 = 0; i0 < (K + 31) / 32; ++i0) {
+      const int c = (threadIdx.x >> 4) + 32 * i0;
+      if (c < K) dw_part[(int64_t)blockIdx.x * n * K + c] = dw0[i0];
+    }
 }
 
 __global__ __launch_bounds__(256) void sum_parts_unrolled_kernel(const float* __restrict__ part,
@@ -206,14 +347,16 @@ constexpr int FM_MFMA_BLOCKS = 256;
 
 bool fm_mfma_supported(int n, int d, int k) {
   if (n < 1) return false;
-  if (k == 32) return n <= 96 && (d == 64 || d == 128);
-  if (k == 64) return n <= 64 && d == 128;
+  // up to three (k = 32) or two (k = 64) tiles of 32 rows, plus a head row
+  // when n = 32 t + 1
+  if (k == 32) return n <= 97 && (d == 64 || d == 128);
+  if (k == 64) return n <= 65 && d == 128;
   return false;
 }
 
 size_t fm_mfma_bwd_workspace(int n, int k) { return (size_t)FM_MFMA_BLOCKS * n * k * sizeof(float); }
 
-template <int NP, int D, int K>
+template <int NP, int D, int K, bool HEAD>
 static hipError_t fm_mfma_launch(bool fwd, const void* X, const void* W, int B, int n, void* out,
                                  int64_t ostride, int emit0, const void* dout, int64_t dstride,
                                  const float* addend, void* dX, float* dX_f32, float* dW,
@@ -223,14 +366,14 @@ static hipError_t fm_mfma_launch(bool fwd, const void* X, const void* W, int B, 
     if (B == 0) return hipSuccess;
     // the forward fits two blocks per compute unit
     const int fblocks = B < 2 * FM_MFMA_BLOCKS ? B : 2 * FM_MFMA_BLOCKS;
-    fm_fwd_mfma_kernel<NP, D, K><<<fblocks, 512, 0, s>>>((const bf16_t*)X, (const bf16_t*)W, B, n,
+    fm_fwd_mfma_kernel<NP, D, K, HEAD><<<fblocks, 512, 0, s>>>((const bf16_t*)X, (const bf16_t*)W, B, n,
                                                         (bf16_t*)out, ostride, emit0);
     LAT_LAUNCH_CHECK();
     return hipSuccess;
   }
   float* part = (float*)ws;
   if (B > 0) {
-    fm_bwd_mfma_kernel<NP, D, K><<<blocks, 512, 0, s>>>(
+    fm_bwd_mfma_kernel<NP, D, K, HEAD><<<blocks, 512, 0, s>>>(
         (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
         (bf16_t*)dX, dX_f32, part);
     LAT_LAUNCH_CHECK();
@@ -245,10 +388,15 @@ hipError_t fm_mfma(bool fwd, const void* X, const void* W, int B, int n, int d, 
                    int64_t ostride, int emit0, const void* dout, int64_t dstride,
                    const float* addend, void* dX, float* dX_f32, float* dW, void* ws,
                    hipStream_t s) {
+  // n = 32 t + 1: row 0 outside the tiles (exactly t tiles of rows)
+  const bool head = n > 1 && (n - 1) % 32 == 0;
 #define LAT_FMM(NPV, DV, KV)                                                                    \
-  if (n <= NPV && d == DV && k == KV)                                                           \
-    return fm_mfma_launch<NPV, DV, KV>(fwd, X, W, B, n, out, ostride, emit0, dout, dstride,     \
-                                       addend, dX, dX_f32, dW, ws, s);
+  if (head && n - 1 == NPV && d == DV && k == KV)                                               \
+    return fm_mfma_launch<NPV, DV, KV, true>(fwd, X, W, B, n, out, ostride, emit0, dout,        \
+                                             dstride, addend, dX, dX_f32, dW, ws, s);           \
+  if (!head && n <= NPV && d == DV && k == KV)                                                  \
+    return fm_mfma_launch<NPV, DV, KV, false>(fwd, X, W, B, n, out, ostride, emit0, dout,       \
+                                              dstride, addend, dX, dX_f32, dW, ws, s);
   LAT_FMM(32, 128, 32) LAT_FMM(64, 128, 32) LAT_FMM(96, 128, 32)
   LAT_FMM(32, 64, 32) LAT_FMM(64, 64, 32) LAT_FMM(96, 64, 32)
   LAT_FMM(32, 128, 64) LAT_FMM(64, 128, 64)

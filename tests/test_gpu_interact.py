@@ -25,6 +25,11 @@ CASES = {
     "fm-bf16-n65-many": ("fm", "bf16", 700, 65, 128, 32, True, False), # > 1 sample per block
     "fm-bf16-n30-d64-k32": ("fm", "bf16", 37, 30, 64, 32, False, False),  # MFMA, other tiles
     "fm-bf16-n29-d128-k64": ("fm", "bf16", 41, 29, 128, 64, True, False),
+    # head row (n = 32 t + 1): row 0 outside the tiles
+    "fm-bf16-n33-d64-k32-head": ("fm", "bf16", 45, 33, 64, 32, False, False),
+    "fm-bf16-n97-d128-k32-head": ("fm", "bf16", 600, 97, 128, 32, True, False),
+    "fm-bf16-n65-d128-k64-head": ("fm", "bf16", 50, 65, 128, 64, True, False),
+    "fm-bf16-n64-d128-k32": ("fm", "bf16", 60, 64, 128, 32, True, False),
     "fm-bf16-valu": ("fm", "bf16", 33, 10, 32, 16, False, False),       # VALU path (d=32)
     "fm-f32-small": ("fm", "f32", 50, 10, 32, 16, False, False),
 }
