@@ -275,8 +275,9 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
                  single_stream=False):
     """One forward+backward step; ws is a uint8 device tensor of at least
     lattice_step_plan(...).total_bytes.  stage_events: optional list of
-    2*len(STAGES) torch.cuda.Event(enable_timing=True): [2s] and [2s+1] are
-    recorded when stage s begins and ends, on the stream that runs it.
+    2*len(STAGES) torch.cuda.Event(enable_timing=True) or None: [2s] and
+    [2s+1] are recorded when stage s begins and ends, on the stream that runs
+    it (None: not recorded).
     single_stream: keep the sparse gradient's sort on the step's stream
     instead of the library's side stream."""
     lib = load()
@@ -291,7 +292,8 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
     if stage_events is not None:
         if len(stage_events) != 2 * len(A.STAGES):
             raise ValueError("need 2*len(STAGES) events")
-        arr = (ctypes.c_void_p * len(stage_events))(*[e.cuda_event for e in stage_events])
+        arr = (ctypes.c_void_p * len(stage_events))(*[e.cuda_event if e is not None else None
+                                                       for e in stage_events])
         opts.stage_events = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
     check(lib.lattice_step(byref(model.desc), byref(batch), byref(opts), _p(ws), ws.numel(),
                            _stream(stream)))

@@ -783,10 +783,10 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   void* const* ev = opts->stage_events;
   auto stage_ev = [&](int i) -> void* const* { return ev ? ev + 2 * i : nullptr; };
   auto begin = [&](int i) -> hipError_t {
-    return ev ? hipEventRecord((hipEvent_t)ev[2 * i], s) : hipSuccess;
+    return ev && ev[2 * i] ? hipEventRecord((hipEvent_t)ev[2 * i], s) : hipSuccess;
   };
   auto end = [&](int i) -> hipError_t {
-    return ev ? hipEventRecord((hipEvent_t)ev[2 * i + 1], s) : hipSuccess;
+    return ev && ev[2 * i + 1] ? hipEventRecord((hipEvent_t)ev[2 * i + 1], s) : hipSuccess;
   };
   char* base = (char*)ws;
   auto at = [&](int64_t o) -> void* { return o < 0 ? nullptr : base + o; };
@@ -889,10 +889,10 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   HIPRET(end(LATTICE_STAGE_INTERACT_BWD));
   if (side) HIPRET(hipEventRecord(side->dx_ready, s));
   auto wbegin = [&](int i) -> hipError_t {
-    return ev ? hipEventRecord((hipEvent_t)ev[2 * i], ws_stream) : hipSuccess;
+    return ev && ev[2 * i] ? hipEventRecord((hipEvent_t)ev[2 * i], ws_stream) : hipSuccess;
   };
   auto wend = [&](int i) -> hipError_t {
-    return ev ? hipEventRecord((hipEvent_t)ev[2 * i + 1], ws_stream) : hipSuccess;
+    return ev && ev[2 * i + 1] ? hipEventRecord((hipEvent_t)ev[2 * i + 1], ws_stream) : hipSuccess;
   };
   HIPRET(wbegin(LATTICE_STAGE_TOP_WGRAD));
   HIPRET(mlp_backward_weights(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, gtop,

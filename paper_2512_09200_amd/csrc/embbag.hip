@@ -677,8 +677,9 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
                                     float* grad_rows, void* E, float lr, hipStream_t s,
                                     void* const* ev) {
   // ev (optional): 4 events, begin / end of the reduction and of the fixup
+  // (null entries are not recorded)
   auto record = [&](int i) -> hipError_t {
-    return ev ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
+    return ev && ev[i] ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
   };
   const int ranges = cdiv(n, RANGE);
   LAT_HIP_CHECK(record(0));
@@ -741,8 +742,9 @@ hipError_t embbag_bwd_sort(const int64_t* row_base, int64_t max_local_rows, cons
                            void* ws, hipStream_t s, const int* keys_in, const int* vals_in,
                            void* const* ev) {
   // ev (optional): 4 events, begin / end of the sort and of the run bookkeeping
+  // (null entries are not recorded)
   auto record = [&](int i) -> hipError_t {
-    return ev ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
+    return ev && ev[i] ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
   };
   LAT_HIP_CHECK(record(0));
   if (nnz == 0) {
@@ -791,7 +793,8 @@ hipError_t embbag_bwd_apply(const int32_t* offsets, int F, int B, int64_t nnz, i
                             void* const* ev) {
   if (nnz == 0) {
     if (ev)
-      for (int i = 0; i < 4; ++i) LAT_HIP_CHECK(hipEventRecord((hipEvent_t)ev[i], s));
+      for (int i = 0; i < 4; ++i)
+        if (ev[i]) LAT_HIP_CHECK(hipEventRecord((hipEvent_t)ev[i], s));
     return hipSuccess;
   }
   const int n = (int)nnz;

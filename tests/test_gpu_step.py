@@ -177,3 +177,14 @@ def test_step_side_stream_matches_single_stream(name):
     assert before("top_bwd", "top_wgrad")
     assert before("top_wgrad", "bottom_bwd")
     assert before("interact_bwd", "bottom_bwd")
+    # a sparse event array: only the reduction's pair is recorded
+    part = [None] * (2 * len(STAGES))
+    part[2 * i["embbag_reduce"]] = torch.cuda.Event(enable_timing=True)
+    part[2 * i["embbag_reduce"] + 1] = torch.cuda.Event(enable_timing=True)
+    for e in part:
+        if e is not None:
+            e.record()
+    w.E.copy_(E0)
+    _, v3, _ = run_step(w, lr, stage_events=part)
+    assert part[2 * i["embbag_reduce"]].elapsed_time(part[2 * i["embbag_reduce"] + 1]) >= 0
+    assert torch.equal(v3["dX"], v1["dX"]) and torch.equal(E1, w.E)
