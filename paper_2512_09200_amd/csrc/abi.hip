@@ -347,13 +347,17 @@ static lattice_status check_mlp(const lattice_mlp_desc* d, int32_t B) {
   return LATTICE_OK;
 }
 
+// split-K bound of the MLP backward products (the factor itself comes from
+// gemm_splits' time estimate)
+constexpr int MLP_MAX_SPLITS = 64;
+
 static size_t mlp_bwd_ws(const lattice_mlp_desc* d, int B) {
   size_t s = 0;
   for (int i = 0; i < d->n_layers; ++i) {
     const lattice_linear& L = d->layers[i];
     GemmArgs g;
     g.dt = dt_of(d->dtype);
-    g.max_splits = 16;
+    g.max_splits = MLP_MAX_SPLITS;
     g.M = L.out_dim; g.N = L.in_dim; g.K = B;
     s = std::max(s, gemm_workspace(g));
     g.M = B; g.N = L.in_dim; g.K = L.out_dim;
@@ -405,7 +409,7 @@ static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const
     w.B = in_i; w.ldb = ld_in; w.tb = 1;
     w.C = L.dW; w.ldc = L.in_dim; w.c_dt = DT_F32;
     w.M = L.out_dim; w.N = L.in_dim; w.K = B;
-    w.max_splits = 16;
+    w.max_splits = MLP_MAX_SPLITS;
     // bf16: db is the row sum of A = gᵀ, taken by the same GEMM
     if (dt == DT_BF16 && L.db) {
       w.rowsum = L.db;
@@ -430,7 +434,7 @@ static hipError_t mlp_layer_dgrad(const lattice_mlp_desc* d, int i, int B, const
   x.B = L.W; x.ldb = L.in_dim; x.tb = 1;
   x.C = dst; x.ldc = dst_ld; x.c_dt = x.dt;
   x.M = B; x.N = L.in_dim; x.K = L.out_dim;
-  x.max_splits = 16;
+  x.max_splits = MLP_MAX_SPLITS;
   if (mask) {
     x.mask = mask;
     x.mask_dt = x.dt;

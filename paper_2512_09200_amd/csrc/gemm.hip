@@ -663,13 +663,29 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
+// Split-K factor by an estimated time: ceil(blocks / 512) waves (two blocks
+// per CU) of K / s each, in K steps, plus the fp32 partials each split writes
+// and the reduction reads back (2 * 4 * M * N bytes at ~5 TB/s, against
+// ~1.8 us per wave and K step), so any factor (not only powers of two) that
+// balances the waves is considered; ties keep fewer splits.
 int gemm_splits(const GemmArgs& g) {
-  if (g.dt != DT_BF16 || g.batch > 1) return 1;
-  const int tiles = cdiv(g.M, GBM) * cdiv(g.N, GBN);
-  int s = 1;
-  // fill the 256 compute units at least twice over when K is long enough
-  while (tiles * s < 512 && g.K / (s * 2) >= 512 && s * 2 <= g.max_splits) s *= 2;
-  return s;
+  if (g.dt != DT_BF16 || g.batch > 1 || g.max_splits <= 1) return 1;
+  const int64_t tiles = (int64_t)cdiv(g.M, GBM) * cdiv(g.N, GBN);
+  double best = 0.0;
+  int best_s = 1;
+  for (int s = 1; s <= g.max_splits; ++s) {
+    const int64_t kps = ((int64_t)cdiv(g.K, s) + GBK - 1) / GBK * GBK;
+    if (s > 1 && kps < 4 * GBK) break;          // at least four K steps per split
+    if ((int64_t)(s - 1) * kps >= g.K) continue;  // the last split would be empty
+    const double waves = (double)cdiv(tiles * s, (int64_t)512);
+    const double cost = waves * (double)(kps / GBK) +
+                        (s > 1 ? (double)s * g.M * g.N / 1.125e6 : 0.0);
+    if (s == 1 || cost < 0.98 * best) {
+      best = cost;
+      best_s = s;
+    }
+  }
+  return best_s;
 }
 
 // split-K partial tiles [splits][M][N], then the row-sum partials [splits][M]
