@@ -146,29 +146,42 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
 }
 
 // Backward.  dX_f32 (optional) receives the unrounded fp32 dX instead of dX.
-template <int NP, int D, int K, bool HEAD>
+// SPB samples per block iteration (their buffers side by side in LDS): each
+// phase then has SPB times the tiles to spread over the 8 waves between the
+// same barriers.
+template <int NP, int D, int K, bool HEAD, int SPB>
+struct FmBwdLds {
+  static constexpr int LX = D + 8, LT = NP + 8, LG = 2 * K + 8, LPD = 2 * K + 8, LDT = D + 8;
+  static constexpr size_t bytes =
+      2 * ((size_t)SPB * (NP * LX + D * LT + K * LDT + NP * LG + K * LT + D * LPD) + K * LT) +
+      4 * (size_t)SPB * (HEAD ? D + 2 * K : 2);
+};
+
+template <int NP, int D, int K, bool HEAD, int SPB>
 __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int B, int n,
     const bf16_t* __restrict__ dout, int64_t dstride, int emit0, const float* __restrict__ addend,
     bf16_t* __restrict__ dX, float* __restrict__ dX_f32, float* __restrict__ dw_part) {
-  constexpr int LX = D + 8, LT = NP + 8, LG = 2 * K + 8, LPD = 2 * K + 8, LDT = D + 8;
+  using L = FmBwdLds<NP, D, K, HEAD, SPB>;
+  constexpr int LX = L::LX, LT = L::LT, LG = L::LG, LPD = L::LPD, LDT = L::LDT;
   constexpr int H = HEAD ? 1 : 0;
-  __shared__ __attribute__((aligned(16))) bf16_t Xs[NP * LX];
-  __shared__ __attribute__((aligned(16))) bf16_t XT[D * LT];
-  __shared__ __attribute__((aligned(16))) bf16_t PT_[K * LDT];  // dP^T [K][LDT]
-  __shared__ __attribute__((aligned(16))) bf16_t GW[NP * LG];   // [j][ G (K) | W (K) ]
-  __shared__ __attribute__((aligned(16))) bf16_t GT[K * LT];
+  __shared__ __attribute__((aligned(16))) bf16_t Xs[SPB][NP * LX];
+  __shared__ __attribute__((aligned(16))) bf16_t XT[SPB][D * LT];
+  __shared__ __attribute__((aligned(16))) bf16_t DT[SPB][K * LDT];  // dP^T [K][LDT]
+  __shared__ __attribute__((aligned(16))) bf16_t GW[SPB][NP * LG];  // [j][ G (K) | W (K) ]
+  __shared__ __attribute__((aligned(16))) bf16_t GT[SPB][K * LT];
   __shared__ __attribute__((aligned(16))) bf16_t WT[K * LT];
-  __shared__ __attribute__((aligned(16))) bf16_t PD[D * LPD];   // [a][ P (K) | dP (K) ]
-  __shared__ float X0[HEAD ? D : 1], GW0[HEAD ? 2 * K : 1];    // head row: x0, [g0 | w0]
+  __shared__ __attribute__((aligned(16))) bf16_t PD[SPB][D * LPD];  // [a][ P (K) | dP (K) ]
+  __shared__ float X0[SPB][HEAD ? D : 1], GW0[SPB][HEAD ? 2 * K : 1];  // head row: x0, [g0 | w0]
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nm = n - H;
   {
     Stager<NP, K, 512> sw;
     sw.load(W + H * K, K, nm);
-    sw.store(GW + K, LG, WT, LT);
+    for (int q = 0; q < SPB; ++q) sw.store(GW[q] + K, LG, q == 0 ? WT : nullptr, LT);
     if (HEAD)
-      for (int c = threadIdx.x; c < K; c += blockDim.x) GW0[K + c] = bf2f(W[c]);
+      for (int c = threadIdx.x; c < K; c += blockDim.x)
+        for (int q = 0; q < SPB; ++q) GW0[q][K + c] = bf2f(W[c]);
   }
   constexpr int DW_TILES = (NP / 32) * (K / 32);
   f32x16 dw[(DW_TILES + 7) / 8];
@@ -180,76 +193,101 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
 #pragma unroll
   for (int i = 0; i < (K + 31) / 32; ++i) dw0[i] = 0.f;
   const int off = emit0 ? D : 0;
-  Stager<NP, D, 512> sx;
-  Stager<NP, K, 512> sg;
-  HeadRow<D> hx;
-  HeadRow<K> hg;
-  auto prefetch = [&](int bb) {
-    const bf16_t* xb = X + (int64_t)bb * n * D;
-    const bf16_t* gb = dout + (int64_t)bb * dstride + off;
-    sx.load(xb + H * D, D, nm);
-    sg.load(gb + H * K, K, nm);
-    if (HEAD) {
-      hx.load(xb);
-      hg.load(gb);
+  Stager<NP, D, 512> sx[SPB];
+  Stager<NP, K, 512> sg[SPB];
+  HeadRow<D> hx[SPB];
+  HeadRow<K> hg[SPB];
+  auto prefetch = [&](int b0) {
+#pragma unroll
+    for (int q = 0; q < SPB; ++q) {
+      const int bb = b0 + q;
+      if (bb >= B) break;
+      const bf16_t* xb = X + (int64_t)bb * n * D;
+      const bf16_t* gb = dout + (int64_t)bb * dstride + off;
+      sx[q].load(xb + H * D, D, nm);
+      sg[q].load(gb + H * K, K, nm);
+      if (HEAD) {
+        hx[q].load(xb);
+        hg[q].load(gb);
+      }
     }
   };
-  if (blockIdx.x < B) prefetch(blockIdx.x);
-  for (int b = blockIdx.x; b < B; b += gridDim.x) {
-    const bf16_t* gb = dout + (int64_t)b * dstride;
-    sx.store(Xs, LX, XT, LT);
-    sg.store(GW, LG, GT, LT);
-    if (HEAD) {
-      hx.store(X0);
-      hg.store(GW0);
+  const int step = gridDim.x * SPB;
+  if (blockIdx.x * SPB < B) prefetch(blockIdx.x * SPB);
+  for (int b0 = blockIdx.x * SPB; b0 < B; b0 += step) {
+    const int ns = B - b0 < SPB ? B - b0 : SPB;  // samples in this iteration
+#pragma unroll
+    for (int q = 0; q < SPB; ++q) {
+      if (q >= ns) break;
+      sx[q].store(Xs[q], LX, XT[q], LT);
+      sg[q].store(GW[q], LG, GT[q], LT);
+      if (HEAD) {
+        hx[q].store(X0[q]);
+        hg[q].store(GW0[q]);
+      }
     }
     __syncthreads();
-    // the next sample's X and G are in flight while this one is computed
-    if (b + (int)gridDim.x < B) prefetch(b + gridDim.x);
+    // the next samples' X and G are in flight while these are computed
+    if (b0 + step < B) prefetch(b0 + step);
     // P = X^T W and dP = X^T G into PD[a][P | dP], and dP^T[c][a] = G^T X
     // into DT (the dW operand), all rounded to bf16 (+ the head row's
     // rank-1 terms)
     constexpr int P_TILES = (D / 32) * (K / 32);
-    bf16_t* DT = PT_;
-    for (int t = w; t < 3 * P_TILES; t += 8) {
-      const int which = t / P_TILES, tt = t % P_TILES;
+    for (int t = w; t < ns * 3 * P_TILES; t += 8) {
+      const int q = t / (3 * P_TILES), which = (t / P_TILES) % 3, tt = t % P_TILES;
       f32x16 acc;
       zero16(acc);
       if (which < 2) {
         const int ta = tt / (K / 32), tc = tt % (K / 32);
-        mfma_tile<NP>(acc, XT + ta * 32 * LT, LT, (which ? GT : WT) + tc * 32 * LT, LT);
+        mfma_tile<NP>(acc, XT[q] + ta * 32 * LT, LT, (which ? GT[q] : WT) + tc * 32 * LT, LT);
         const int c = tc * 32 + (lane & 31);
-        const float h = HEAD ? GW0[which ? c : K + c] : 0.f;  // g0[c] or w0[c]
+        const float h = HEAD ? GW0[q][which ? c : K + c] : 0.f;  // g0[c] or w0[c]
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int a = ta * 32 + frag_row(r);
-          const float v = HEAD ? acc[r] + X0[a] * h : acc[r];
-          PD[a * LPD + c + which * K] = f2bf(v);
+          const float v = HEAD ? acc[r] + X0[q][a] * h : acc[r];
+          PD[q][a * LPD + c + which * K] = f2bf(v);
         }
       } else {
         const int tc = tt / (D / 32), ta = tt % (D / 32);
-        mfma_tile<NP>(acc, GT + tc * 32 * LT, LT, XT + ta * 32 * LT, LT);
+        mfma_tile<NP>(acc, GT[q] + tc * 32 * LT, LT, XT[q] + ta * 32 * LT, LT);
         const int a = ta * 32 + (lane & 31);
-        const float x0 = HEAD ? X0[a] : 0.f;
+        const float x0 = HEAD ? X0[q][a] : 0.f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int c = tc * 32 + frag_row(r);
-          const float v = HEAD ? acc[r] + GW0[c] * x0 : acc[r];
-          DT[c * LDT + a] = f2bf(v);
+          const float v = HEAD ? acc[r] + GW0[q][c] * x0 : acc[r];
+          DT[q][c * LDT + a] = f2bf(v);
         }
       }
     }
     __syncthreads();
-    // dX[j][a] = sum_kk GW[j][kk] PD[a][kk]  (+ addend, + slot-0 gradient)
-    const int64_t sbase = (int64_t)b * n * D;  // this sample's [n, D] block
+    // dX[j][a] = sum_kk GW[j][kk] PD[a][kk]  (+ addend, + slot-0 gradient).
+    // Plain bf16 output: each tile is rounded into XT (free after the phase
+    // above) as [j][a] and the sample's rows j >= H are then written with
+    // 16-byte stores (they are contiguous in dX).
     constexpr int DX_TILES = (NP / 32) * (D / 32);
-    for (int t = w; t < DX_TILES; t += 8) {
-      const int tj = t / (D / 32), ta = t % (D / 32);
+    constexpr int LY = NP * (D + 8) <= D * LT ? D + 8 : D;  // row stride of the staged dX
+    static_assert(NP * LY <= D * LT, "staged dX must fit in X^T");
+    const bool staged = !addend && !dX_f32 && (reinterpret_cast<uintptr_t>(dX) & 15) == 0;
+    for (int t = w; t < ns * DX_TILES; t += 8) {
+      const int q = t / DX_TILES, tj = (t % DX_TILES) / (D / 32), ta = t % (D / 32);
+      const int b = b0 + q;
+      const int64_t sbase = (int64_t)b * n * D;  // this sample's [n, D] block
       f32x16 acc;
       zero16(acc);
-      mfma_tile<2 * K>(acc, GW + tj * 32 * LG, LG, PD + ta * 32 * LPD, LPD);
+      mfma_tile<2 * K>(acc, GW[q] + tj * 32 * LG, LG, PD[q] + ta * 32 * LPD, LPD);
       const int a = ta * 32 + (lane & 31);
-      const float g0 = (!HEAD && emit0 && tj == 0) ? bf2f(gb[a]) : 0.f;
+      const float g0 = (!HEAD && emit0 && tj == 0) ? bf2f(dout[(int64_t)b * dstride + a]) : 0.f;
+      if (staged) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = tj * 32 + frag_row(r);
+          const float v = (!HEAD && j == 0) ? acc[r] + g0 : acc[r];
+          XT[q][j * LY + a] = f2bf(v);
+        }
+        continue;
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = tj * 32 + frag_row(r);
@@ -266,47 +304,72 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
     if (HEAD) {
       // dX[0][a] = sum_kk [g0 | w0][kk] PD[a][kk]: 4 lanes per a, K/2 terms
       // each, then the slot-0 gradient and the addend
-      const int a = threadIdx.x >> 2, q = threadIdx.x & 3;
-      if (a < D) {
-        float sum = 0.f;
+      const int a = threadIdx.x >> 2, qq = threadIdx.x & 3;
 #pragma unroll
-        for (int i = 0; i < 2 * K / 4; ++i) {
-          const int kk = q * (2 * K / 4) + i;
-          sum += GW0[kk] * bf2f(PD[a * LPD + kk]);
-        }
-        sum += __shfl_xor(sum, 2, 64);
-        sum += __shfl_xor(sum, 1, 64);
-        if (q == 0) {
-          if (addend) sum += addend[sbase + a];
-          if (emit0) sum += bf2f(gb[a]);
-          if (dX_f32) dX_f32[sbase + a] = sum;
-          else dX[sbase + a] = f2bf(sum);
+      for (int q = 0; q < SPB; ++q) {
+        if (q >= ns) break;
+        const int b = b0 + q;
+        const int64_t sbase = (int64_t)b * n * D;
+        if (a < D) {
+          float sum = 0.f;
+#pragma unroll
+          for (int i = 0; i < 2 * K / 4; ++i) {
+            const int kk = qq * (2 * K / 4) + i;
+            sum += GW0[q][kk] * bf2f(PD[q][a * LPD + kk]);
+          }
+          sum += __shfl_xor(sum, 2, 64);
+          sum += __shfl_xor(sum, 1, 64);
+          if (qq == 0) {
+            if (addend) sum += addend[sbase + a];
+            if (emit0) sum += bf2f(dout[(int64_t)b * dstride + a]);
+            if (dX_f32) dX_f32[sbase + a] = sum;
+            else dX[sbase + a] = f2bf(sum);
+          }
         }
       }
     }
-    // dW[j][c] += sum_a X[j][a] dP^T[c][a]
+    // dW[j][c] += sum_a X[j][a] dP^T[c][a], the samples in order
     for (int t = w, i = 0; t < DW_TILES; t += 8, ++i) {
       const int tj = t / (K / 32), tc = t % (K / 32);
-      mfma_tile<D>(dw[i], Xs + tj * 32 * LX, LX, DT + tc * 32 * LDT, LDT);
+#pragma unroll
+      for (int q = 0; q < SPB; ++q) {
+        if (q >= ns) break;
+        mfma_tile<D>(dw[i], Xs[q] + tj * 32 * LX, LX, DT[q] + tc * 32 * LDT, LDT);
+      }
     }
     if (HEAD) {
-      // dW[0][c] += sum_a x0[a] dP[a][c]: 16 lanes per c
-      const int q = threadIdx.x & 15;
+      // dW[0][c] += sum_a x0[a] dP[a][c]: 16 lanes per c, the samples in order
+      const int qq = threadIdx.x & 15;
 #pragma unroll
       for (int i0 = 0; i0 < (K + 31) / 32; ++i0) {
         const int c = (threadIdx.x >> 4) + 32 * i0;
         if (c < K) {
-          float sum = 0.f;
 #pragma unroll
-          for (int i = 0; i < D / 16; ++i) {
-            const int a = q * (D / 16) + i;
-            sum += X0[a] * bf2f(DT[c * LDT + a]);
+          for (int q = 0; q < SPB; ++q) {
+            if (q >= ns) break;
+            float sum = 0.f;
+#pragma unroll
+            for (int i = 0; i < D / 16; ++i) {
+              const int a = qq * (D / 16) + i;
+              sum += X0[q][a] * bf2f(DT[q][c * LDT + a]);
+            }
+            dw0[i0] += group16_sum(sum);
           }
-          dw0[i0] += group16_sum(sum);
         }
       }
     }
     __syncthreads();
+    if (staged) {
+      // rows H .. n-1 of each sample: nm * D contiguous bf16, 8 per store
+      for (int q = 0; q < ns; ++q) {
+        bf16_t* dst = dX + (int64_t)(b0 + q) * n * D + H * D;
+        for (int v = threadIdx.x; v < nm * D / 8; v += blockDim.x) {
+          const int j = v / (D / 8), a = (v % (D / 8)) * 8;
+          stg16(dst + j * D + a, *reinterpret_cast<const u32x4*>(XT[q] + j * LY + a));
+        }
+      }
+      __syncthreads();  // X^T is restaged for the next samples
+    }
   }
   for (int t = w, i = 0; t < DW_TILES; t += 8, ++i) {
     const int tj = t / (K / 32), tc = t % (K / 32);
@@ -372,14 +435,18 @@ static hipError_t fm_mfma_launch(bool fwd, const void* X, const void* W, int B, 
     return hipSuccess;
   }
   float* part = (float*)ws;
+  // two samples per block iteration when both fit in LDS
+  constexpr int SPB = FmBwdLds<NP, D, K, HEAD, 2>::bytes <= 160 * 1024 ? 2 : 1;
+  const int bblocks = (B + SPB - 1) / SPB < FM_MFMA_BLOCKS ? ((B + SPB - 1) / SPB > 0 ? (B + SPB - 1) / SPB : 1)
+                                                           : FM_MFMA_BLOCKS;
   if (B > 0) {
-    fm_bwd_mfma_kernel<NP, D, K, HEAD><<<blocks, 512, 0, s>>>(
+    fm_bwd_mfma_kernel<NP, D, K, HEAD, SPB><<<bblocks, 512, 0, s>>>(
         (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
         (bf16_t*)dX, dX_f32, part);
     LAT_LAUNCH_CHECK();
   }
   const int64_t len = (int64_t)n * K;
-  sum_parts_unrolled_kernel<<<cdiv(len, 256), 256, 0, s>>>(part, B > 0 ? blocks : 0, len, dW);
+  sum_parts_unrolled_kernel<<<cdiv(len, 256), 256, 0, s>>>(part, B > 0 ? bblocks : 0, len, dW);
   LAT_LAUNCH_CHECK();
   return hipSuccess;
 }
