@@ -302,8 +302,7 @@ typedef enum {
  * (non-blocking, default priority, one per device, created on first use and
  * kept until the process ends): the sort is forked from the caller's stream
  * after the pooled lookups and overlaps the dense forward and backward; the
- * weight gradients are forked after the top MLP's gradient chain and overlap
- * the interaction backward (which the bottom backward waits for) and the
+ * weight gradients are forked after the interaction backward and overlap the
  * segmented reduction, which waits for the sort.  All
  * work is still ordered after the caller's prior work on `stream`, and the
  * call's work is complete when `stream` reaches the end of it, as with a
