@@ -84,10 +84,15 @@ __global__ __launch_bounds__(1024) void scan_sums_kernel(int* __restrict__ sums,
   }
 }
 
+// sums: the tile totals (not scanned); each block adds up those before it
 __global__ __launch_bounds__(SCAN_THREADS) void scan_apply_kernel(const int* __restrict__ in, int n,
                                                                    const int* __restrict__ sums,
                                                                    int* __restrict__ out) {
   __shared__ int lds[SCAN_THREADS / 64];
+  int p = 0;
+  for (int i = threadIdx.x; i < (int)blockIdx.x; i += SCAN_THREADS) p += sums[i];
+  int prefix;
+  block_exclusive_scan(p, lds, &prefix);
   // blocked arrangement: thread t owns items [t*ITEMS, (t+1)*ITEMS) of the tile
   const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + (int64_t)threadIdx.x * SCAN_ITEMS;
   int v[SCAN_ITEMS];
@@ -98,7 +103,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_apply_kernel(const int* __r
     s += v[i];
   }
   int tot;
-  int run = block_exclusive_scan(s, lds, &tot) + sums[blockIdx.x];
+  int run = block_exclusive_scan(s, lds, &tot) + prefix;
 #pragma unroll
   for (int i = 0; i < SCAN_ITEMS; ++i) {
     if (base + i < n) out[base + i] = run;
@@ -112,8 +117,6 @@ hipError_t exclusive_scan(const int* in, int* out, int64_t n, int* tmp, hipStrea
   if (n <= 0) return hipSuccess;
   const int tiles = cdiv(n, SCAN_TILE);
   scan_reduce_kernel<<<tiles, SCAN_THREADS, 0, s>>>(in, (int)n, tmp);
-  LAT_LAUNCH_CHECK();
-  scan_sums_kernel<<<1, 1024, 0, s>>>(tmp, tiles);
   LAT_LAUNCH_CHECK();
   scan_apply_kernel<<<tiles, SCAN_THREADS, 0, s>>>(in, (int)n, tmp, out);
   LAT_LAUNCH_CHECK();
