@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 4
+#define LATTICE_ABI_VERSION 5
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -339,7 +339,6 @@ typedef struct {
   int64_t bottom_act[LATTICE_MAX_LAYERS];   /* [B, out_i] hidden bottom outputs (last: in X) */
   int64_t top_act[LATTICE_MAX_LAYERS];      /* [B, out_i] hidden top outputs (last: logits) */
   int64_t unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows;
-  int64_t keys, vals;   /* [nnz] int32: sort keys (global row) and bag ids, built by the forward */
   int64_t interact;     /* interaction workspace (saved state from forward to backward) */
   int64_t scratch;      /* scratch shared by the dense stages */
   int64_t scratch_bytes;

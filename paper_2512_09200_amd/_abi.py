@@ -88,7 +88,7 @@ class lattice_step_layout(Structure):
                  ("loss", c_int64), ("d_t", c_int64), ("dX", c_int64),
                  ("bottom_act", c_int64 * MAX_LAYERS), ("top_act", c_int64 * MAX_LAYERS)]
                 + [(k, c_int64) for k in ("unique_rows", "seg_offsets", "sorted_bags",
-                                          "num_unique", "grad_rows", "keys", "vals", "interact", "scratch",
+                                          "num_unique", "grad_rows", "interact", "scratch",
                                           "scratch_bytes", "sparse", "sparse_bytes")])
 
 

@@ -690,8 +690,6 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   L.sorted_bags = take((size_t)nn * 4);
   L.num_unique = take(4);
   L.grad_rows = (o && o->emit_grad_rows) ? take((size_t)nn * d * 4) : -1;
-  L.keys = take((size_t)nn * 4);
-  L.vals = take((size_t)nn * 4);
   size_t sc = 0;
   sc = std::max(sc, mlp_bwd_ws(&m->top, B));
   if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
@@ -808,7 +806,6 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                            batch->bags.indices, m->num_features, B, nnz, d,
                            (int*)at(L.unique_rows), (int*)at(L.seg_offsets),
                            (int*)at(L.sorted_bags), (int*)at(L.num_unique), sparse, on,
-                           (const int*)at(L.keys), (const int*)at(L.vals),
                            stage_ev(LATTICE_STAGE_EMBBAG_SORT));
   };
 
@@ -816,7 +813,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   HIPRET(begin(LATTICE_STAGE_EMBBAG_FWD));
   HIPRET(embbag_fwd(m->tables.data, dt, d, m->tables.row_base, batch->bags.offsets,
                     batch->bags.indices, m->num_features, B, m->pool == LATTICE_POOL_MEAN, X, dt,
-                    n, s0, s, (int*)at(L.keys), (int*)at(L.vals)));
+                    n, s0, s));
   HIPRET(end(LATTICE_STAGE_EMBBAG_FWD));
   // fork: the sort and run bookkeeping go to the side stream, overlapping
   // the dense stages; the lock is held until the join is enqueued

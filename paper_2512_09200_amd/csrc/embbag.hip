@@ -154,14 +154,12 @@ __device__ inline void fwd_group(int s0, int cnt, uint64_t emask, int grow, int 
 // bag end.  Per chunk of 64 positions: indices (one per lane), their bags, the
 // global rows and the destination slots; then in groups of S positions the S
 // table rows are loaded together and summed in order.  Empty bags are written
-// as zeros.  With keys != NULL the backward's sort keys (global row) and
-// values (bag id) are written per position as well.
+// as zeros.
 template <typename TT, typename XT, int BPL, bool MEAN, bool FULL>
 __global__ __launch_bounds__(256) void embbag_fwd_kernel(
     const TT* __restrict__ E, const int64_t* __restrict__ row_base,
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ indices, int F, int B,
-    int dim, XT* __restrict__ X, int n_slots, int first_slot, int* __restrict__ keys,
-    int* __restrict__ vals) {
+    int dim, XT* __restrict__ X, int n_slots, int first_slot) {
   constexpr int EPL = BPL / (int)sizeof(TT);
   constexpr int S = BPL == 4 ? 32 : (BPL == 8 ? 16 : 8);
   const int lane = threadIdx.x & 63;
@@ -206,10 +204,6 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
       grow = (int)(row_base[f] + indices[p]);
       xrow = b * n_slots + first_slot + f;
       if (MEAN) inv_len = 1.f / (float)(next_off - this_off);
-      if (keys) {
-        keys[p] = grow;
-        vals[p] = bag;
-      }
     }
     int s0 = 0;
     for (; s0 + S <= cnt; s0 += S)
@@ -234,15 +228,14 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
 template <typename TT, typename XT>
 static hipError_t embbag_fwd_t(const void* E, int dim, const int64_t* row_base,
                                const int32_t* offsets, const int32_t* indices, int F, int B,
-                               int mean, void* X, int n_slots, int first_slot, int* keys,
-                               int* vals, hipStream_t s) {
+                               int mean, void* X, int n_slots, int first_slot, hipStream_t s) {
   const int64_t bags = (int64_t)F * B;
   if (bags == 0) return hipSuccess;
   const int row_bytes = dim * (int)sizeof(TT);
   const int grid = cdiv(cdiv(bags, FWD_BAGS), 4);
 #define LAT_FWD(BPLV, MV, FV)                                                              \
   embbag_fwd_kernel<TT, XT, BPLV, MV, FV><<<grid, 256, 0, s>>>(                           \
-      (const TT*)E, row_base, offsets, indices, F, B, dim, (XT*)X, n_slots, first_slot, keys, vals)
+      (const TT*)E, row_base, offsets, indices, F, B, dim, (XT*)X, n_slots, first_slot)
   if (row_bytes == 256) {
     if (mean) LAT_FWD(4, true, true); else LAT_FWD(4, false, true);
   } else if (row_bytes < 256) {
@@ -259,35 +252,14 @@ static hipError_t embbag_fwd_t(const void* E, int dim, const int64_t* row_base,
 
 hipError_t embbag_fwd(const void* E, DType edt, int dim, const int64_t* row_base,
                       const int32_t* offsets, const int32_t* indices, int F, int B, int mean,
-                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s, int* keys,
-                      int* vals) {
+                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s) {
   if (edt == DT_BF16 && xdt == DT_BF16)
-    return embbag_fwd_t<bf16_t, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
+    return embbag_fwd_t<bf16_t, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
   if (edt == DT_BF16 && xdt == DT_F32)
-    return embbag_fwd_t<bf16_t, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
+    return embbag_fwd_t<bf16_t, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
   if (edt == DT_F32 && xdt == DT_F32)
-    return embbag_fwd_t<float, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
-  return embbag_fwd_t<float, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, keys, vals, s);
-}
-
-// ---------------------------------------------------------------------------
-// backward: keys
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void embbag_keys_kernel(const int64_t* __restrict__ row_base,
-                                                          const int32_t* __restrict__ offsets,
-                                                          const int32_t* __restrict__ indices,
-                                                          int F, int B, int* __restrict__ keys,
-                                                          int* __restrict__ vals) {
-  const int lane = threadIdx.x & 63;
-  const int64_t bag = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (bag >= (int64_t)F * B) return;
-  const int f = (int)(bag / B);
-  const int start = offsets[bag], end = offsets[bag + 1];
-  const int rb = (int)row_base[f];
-  for (int p = start + lane; p < end; p += 64) {
-    keys[p] = rb + indices[p];
-    vals[p] = (int)bag;
-  }
+    return embbag_fwd_t<float, float>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
+  return embbag_fwd_t<float, bf16_t>(E, dim, row_base, offsets, indices, F, B, mean, X, n_slots, first_slot, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -658,7 +630,6 @@ size_t embbag_bwd_workspace(int64_t nnz, int dim, int F) {
   const int64_t n = nnz > 0 ? nnz : 1;
   const int64_t ranges = cdiv(n, RANGE);
   size_t s = 0;
-  s += 2 * align256((size_t)n * 4);                    // keys, vals (unsorted)
   s += align256((size_t)n * 4);                        // sorted keys
   s += align256(radix_sort_segments_workspace(n, F));
   s += align256((size_t)(cdiv(n, SEG_TILE) + 1) * 4);  // segment tile counts
@@ -712,7 +683,7 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
 
 // The sparse gradient's workspace, shared by its two phases.
 struct EmbBwdWs {
-  int *keys, *vals, *skeys;
+  int* skeys;
   void* sort_ws;
   int *tile_counts, *range_ubefore, *part_uid, *span_list, *span_count;
   float* part;
@@ -723,8 +694,6 @@ static EmbBwdWs emb_bwd_ws(void* ws, int64_t nnz, int dim, int F) {
   char* p = static_cast<char*>(ws);
   auto take = [&](size_t bytes) { char* q = p; p += align256(bytes); return q; };
   EmbBwdWs w;
-  w.keys = (int*)take((size_t)n * 4);
-  w.vals = (int*)take((size_t)n * 4);
   w.skeys = (int*)take((size_t)n * 4);
   w.sort_ws = take(radix_sort_segments_workspace(n, F));
   w.tile_counts = (int*)take((size_t)(cdiv(n, SEG_TILE) + 1) * 4);
@@ -739,8 +708,7 @@ static EmbBwdWs emb_bwd_ws(void* ws, int64_t nnz, int dim, int F) {
 hipError_t embbag_bwd_sort(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
                            const int32_t* indices, int F, int B, int64_t nnz, int dim,
                            int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
-                           void* ws, hipStream_t s, const int* keys_in, const int* vals_in,
-                           void* const* ev) {
+                           void* ws, hipStream_t s, void* const* ev) {
   // ev (optional): 4 events, begin / end of the sort and of the run bookkeeping
   // (null entries are not recorded)
   auto record = [&](int i) -> hipError_t {
@@ -757,17 +725,7 @@ hipError_t embbag_bwd_sort(const int64_t* row_base, int64_t max_local_rows, cons
   }
   const int n = (int)nnz;
   EmbBwdWs w = emb_bwd_ws(ws, nnz, dim, F);
-  int* keys = w.keys;
-  int* vals = w.vals;
-  const int64_t bags = (int64_t)F * B;
-  if (keys_in && vals_in) {
-    keys = const_cast<int*>(keys_in);  // read-only from here on
-    vals = const_cast<int*>(vals_in);
-  } else {
-    embbag_keys_kernel<<<cdiv(bags, 4), 256, 0, s>>>(row_base, offsets, indices, F, B, keys, vals);
-    LAT_LAUNCH_CHECK();
-  }
-  hipError_t e = radix_sort_segments(keys, vals, n, offsets, F, B, row_base, max_local_rows,
+  hipError_t e = radix_sort_segments(indices, n, offsets, F, B, row_base, max_local_rows,
                                      w.skeys, sorted_bags, w.sort_ws, s);
   if (e != hipSuccess) return e;
   LAT_HIP_CHECK(record(1));
@@ -823,8 +781,7 @@ hipError_t embbag_bwd(const int64_t* row_base, int64_t max_local_rows, const int
                       int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
                       float* grad_rows, void* E, DType et, float lr, void* ws, hipStream_t s) {
   hipError_t e = embbag_bwd_sort(row_base, max_local_rows, offsets, indices, F, B, nnz, dim,
-                                 unique_rows, seg_offsets, sorted_bags, num_unique, ws, s,
-                                 nullptr, nullptr, nullptr);
+                                 unique_rows, seg_offsets, sorted_bags, num_unique, ws, s, nullptr);
   if (e != hipSuccess) return e;
   return embbag_bwd_apply(offsets, F, B, nnz, mean, dX, dxt, n_slots, first_slot, dim, unique_rows,
                           seg_offsets, sorted_bags, grad_rows, E, et, lr, ws, s, nullptr);

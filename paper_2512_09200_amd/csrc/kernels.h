@@ -11,29 +11,28 @@ hipError_t exclusive_scan(const int* in, int* out, int64_t n, int* tmp, hipStrea
 hipError_t exclusive_scan_inplace_small(int* a, int n, hipStream_t s);
 // Sort of a jagged batch's (global row, bag) pairs whose positions are grouped
 // by feature: each feature segment is sorted by its local row (< max_local_rows).
+// The first pass reads the batch's indices directly (keys = row_base[f] +
+// index, values = bag ids expanded from the offsets).
 size_t radix_sort_segments_workspace(int64_t n, int F);
-hipError_t radix_sort_segments(int* keys, int* vals, int64_t n, const int32_t* offsets, int F,
+hipError_t radix_sort_segments(const int32_t* indices, int64_t n, const int32_t* offsets, int F,
                                int B, const int64_t* row_base, int64_t max_local_rows,
                                int* keys_out, int* vals_out, void* ws, hipStream_t s);
 
 // embbag.hip
-// keys/vals (optional): also write the backward's sort keys (global row) and
-// values (bag id) per position, so the backward can skip building them.
 hipError_t embbag_fwd(const void* E, DType edt, int dim, const int64_t* row_base,
                       const int32_t* offsets, const int32_t* indices, int F, int B, int mean,
-                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s,
-                      int* keys = nullptr, int* vals = nullptr);
+                      void* X, DType xdt, int n_slots, int first_slot, hipStream_t s);
 size_t embbag_bwd_workspace(int64_t nnz, int dim, int F);
 // max_local_rows: rows of the largest table (bounds every local index).
 // The sparse gradient in two phases over one workspace: embbag_bwd_sort needs
-// only the batch (or the forward's keys/vals) -- sort, unique rows, run
-// offsets; embbag_bwd_apply needs dX -- segmented reduction and SGD.
-// ev (optional): 4 events each, begin/end of the phase's two parts.
+// only the batch -- sort, unique rows, run offsets; embbag_bwd_apply needs
+// dX -- segmented reduction and SGD.
+// ev (optional): 4 events each, begin/end of the phase's two parts (null
+// entries are not recorded).
 hipError_t embbag_bwd_sort(const int64_t* row_base, int64_t max_local_rows, const int32_t* offsets,
                            const int32_t* indices, int F, int B, int64_t nnz, int dim,
                            int* unique_rows, int* seg_offsets, int* sorted_bags, int* num_unique,
-                           void* ws, hipStream_t s, const int* keys_in, const int* vals_in,
-                           void* const* ev);
+                           void* ws, hipStream_t s, void* const* ev);
 hipError_t embbag_bwd_apply(const int32_t* offsets, int F, int B, int64_t nnz, int mean,
                             const void* dX, DType dxt, int n_slots, int first_slot, int dim,
                             const int* unique_rows, const int* seg_offsets, const int* sorted_bags,

@@ -158,6 +158,22 @@ __global__ __launch_bounds__(256) void seg_tilemap_kernel(const int* __restrict_
   for (int t = tile_base[f] + threadIdx.x; t < tile_base[f + 1]; t += 256) tile_seg[t] = f;
 }
 
+// tile -> first bag: every non-empty bag writes its index to the tiles that
+// start inside it (each tile start lies in exactly one non-empty bag)
+__global__ __launch_bounds__(256) void seg_tilebag_kernel(const int32_t* __restrict__ offsets,
+                                                          int F, int B,
+                                                          const int* __restrict__ tile_base,
+                                                          int* __restrict__ tile_bag0) {
+  const int64_t bag = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (bag >= (int64_t)F * B) return;
+  const int f = (int)(bag / B);
+  const int seg0 = offsets[(int64_t)f * B];
+  const int lo = offsets[bag], hi = offsets[bag + 1];
+  if (lo == hi) return;
+  for (int lt = (lo - seg0 + SORT_TILE - 1) / SORT_TILE; seg0 + lt * SORT_TILE < hi; ++lt)
+    tile_bag0[tile_base[f] + lt] = (int)bag;
+}
+
 struct SegTile {
   int f, lt, nt, base, cnt, cb;  // segment, tile within it, its tile count, first position, items, count base
   int64_t key0;                  // row_base[f]
@@ -179,10 +195,12 @@ __device__ inline bool seg_tile(const int* tile_base, const int* tile_seg, const
   return true;
 }
 
+// keys: global rows, or (local = 1, the first pass) the batch's indices,
+// i.e. rows local to the segment's table
 __global__ __launch_bounds__(SORT_THREADS) void radix_hist_seg_kernel(
-    const int* __restrict__ keys, const int32_t* __restrict__ offsets, const int64_t* __restrict__ row_base,
-    int F, int B, const int* __restrict__ tile_base, const int* __restrict__ tile_seg, int shift,
-    int dbits, int* __restrict__ counts) {
+    const int* __restrict__ keys, int local, const int32_t* __restrict__ offsets,
+    const int64_t* __restrict__ row_base, int F, int B, const int* __restrict__ tile_base,
+    const int* __restrict__ tile_seg, int shift, int dbits, int* __restrict__ counts) {
   __shared__ int hist[RADIX];
   const int radix = 1 << dbits;
   SegTile t;
@@ -193,7 +211,7 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_hist_seg_kernel(
   }
   for (int i = threadIdx.x; i < radix; i += SORT_THREADS) hist[i] = 0;
   __syncthreads();
-  const int key0 = (int)t.key0;
+  const int key0 = local ? 0 : (int)t.key0;
 #pragma unroll
   for (int i = 0; i < SORT_ITEMS; ++i) {
     const int k = i * SORT_THREADS + threadIdx.x;
@@ -203,8 +221,14 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_hist_seg_kernel(
   for (int d = threadIdx.x; d < radix; d += SORT_THREADS) counts[t.cb + (int64_t)d * t.nt + t.lt] = hist[d];
 }
 
+// FIRST (the first pass): keys_in are the batch's indices (local rows) and
+// vals_in is unused: the keys become global rows (+ row_base of the
+// segment) and the values the bag ids, expanded from the offsets of the
+// bags the tile covers (tile_bag0: the first of them).
+template <bool FIRST>
 __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
-    const int* __restrict__ keys_in, const int* __restrict__ vals_in, const int32_t* __restrict__ offsets,
+    const int* __restrict__ keys_in, const int* __restrict__ vals_in,
+    const int* __restrict__ tile_bag0, const int32_t* __restrict__ offsets,
     const int64_t* __restrict__ row_base, int F, int B, const int* __restrict__ tile_base,
     const int* __restrict__ tile_seg, int shift, int dbits, const int* __restrict__ coffs,
     int* __restrict__ keys_out, int* __restrict__ vals_out) {
@@ -223,6 +247,19 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < NW * RADIX; i += SORT_THREADS) (&wcnt[0][0])[i] = 0;
   __syncthreads();
+  if constexpr (FIRST) {
+    // bag id of every tile position, staged in lvals (free until the ranks
+    // are known): bag0 + i for i = thread, thread + 256, ... until the bags
+    // start past the tile
+    const int tend = t.base + t.cnt, bag_end = (t.f + 1) * B;
+    for (int bag = tile_bag0[blockIdx.x] + threadIdx.x; bag < bag_end; bag += SORT_THREADS) {
+      const int lo = offsets[bag];
+      if (lo >= tend) break;
+      const int hi = offsets[bag + 1] < tend ? offsets[bag + 1] : tend;
+      for (int q = lo > t.base ? lo : t.base; q < hi; ++q) lvals[q - t.base] = bag;
+    }
+    __syncthreads();
+  }
   const int cbase = w * CHUNK;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int key[ROUNDS], val[ROUNDS], rank[ROUNDS];
@@ -230,8 +267,13 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   for (int r = 0; r < ROUNDS; ++r) {
     const int k = cbase + r * 64 + lane;
     const bool valid = k < t.cnt;
-    key[r] = valid ? keys_in[t.base + k] : 0;
-    val[r] = valid ? vals_in[t.base + k] : 0;
+    if constexpr (FIRST) {
+      key[r] = valid ? keys_in[t.base + k] + key0 : 0;
+      val[r] = valid ? lvals[k] : 0;
+    } else {
+      key[r] = valid ? keys_in[t.base + k] : 0;
+      val[r] = valid ? vals_in[t.base + k] : 0;
+    }
   }
   // stable rank of each item among the wave's items with the same digit
 #pragma unroll
@@ -301,10 +343,10 @@ size_t radix_sort_segments_workspace(int64_t n, int F) {
   return 2 * (size_t)(n > 0 ? n : 1) * sizeof(int)  // ping-pong keys/vals
          + 2 * c * sizeof(int)                        // counts + offsets
          + scan_workspace((int64_t)c)
-         + (size_t)(F + 1 + tmax) * sizeof(int) + 1024;  // tile_base, tile_seg
+         + (size_t)(F + 1 + 2 * tmax) * sizeof(int) + 1024;  // tile_base, tile_seg, tile_bag0
 }
 
-hipError_t radix_sort_segments(int* keys, int* vals, int64_t n, const int32_t* offsets, int F,
+hipError_t radix_sort_segments(const int32_t* indices, int64_t n, const int32_t* offsets, int F,
                                int B, const int64_t* row_base, int64_t max_local_rows,
                                int* keys_out, int* vals_out, void* ws, hipStream_t s) {
   if (n <= 0) return hipSuccess;
@@ -317,7 +359,8 @@ hipError_t radix_sort_segments(int* keys, int* vals, int64_t n, const int32_t* o
   int* offs = reinterpret_cast<int*>(p); p += c * sizeof(int);
   int* tmp = reinterpret_cast<int*>(p); p += scan_workspace((int64_t)c);
   int* tile_base = reinterpret_cast<int*>(p); p += (size_t)(F + 1) * sizeof(int);
-  int* tile_seg = reinterpret_cast<int*>(p);
+  int* tile_seg = reinterpret_cast<int*>(p); p += (size_t)tmax * sizeof(int);
+  int* tile_bag0 = reinterpret_cast<int*>(p);
 
   seg_ntiles_kernel<<<cdiv(F + 1, 256), 256, 0, s>>>(offsets, F, B, tile_base);
   LAT_LAUNCH_CHECK();
@@ -325,26 +368,34 @@ hipError_t radix_sort_segments(int* keys, int* vals, int64_t n, const int32_t* o
   if (e != hipSuccess) return e;
   seg_tilemap_kernel<<<F, 256, 0, s>>>(tile_base, tile_seg);
   LAT_LAUNCH_CHECK();
+  seg_tilebag_kernel<<<cdiv((int64_t)F * B, 256), 256, 0, s>>>(offsets, F, B, tile_base, tile_bag0);
+  LAT_LAUNCH_CHECK();
 
   const int bits = key_bits(max_local_rows > 0 ? max_local_rows - 1 : 0);
   const int passes = bits == 0 ? 1 : (bits + RADIX_BITS - 1) / RADIX_BITS;
   const int dbits = bits == 0 ? 1 : (bits + passes - 1) / passes;
   const int radix = 1 << dbits;
-  int* src_k = keys; int* src_v = vals;
+  const int* src_k = indices;
+  const int* src_v = nullptr;
   for (int pass = 0; pass < passes; ++pass) {
     const bool last = pass == passes - 1;
     const int remaining = passes - 1 - pass;
     int* dst_k = last ? keys_out : ((remaining % 2 == 1) ? kb : keys_out);
     int* dst_v = last ? vals_out : ((remaining % 2 == 1) ? vb : vals_out);
     const int shift = pass * dbits;
-    radix_hist_seg_kernel<<<tmax, SORT_THREADS, 0, s>>>(src_k, offsets, row_base, F, B, tile_base,
-                                                         tile_seg, shift, dbits, counts);
+    radix_hist_seg_kernel<<<tmax, SORT_THREADS, 0, s>>>(src_k, pass == 0, offsets, row_base, F, B,
+                                                         tile_base, tile_seg, shift, dbits, counts);
     LAT_LAUNCH_CHECK();
     e = exclusive_scan(counts, offs, (int64_t)radix * tmax, tmp, s);
     if (e != hipSuccess) return e;
-    radix_scatter_seg_kernel<<<tmax, SORT_THREADS, 0, s>>>(src_k, src_v, offsets, row_base, F, B,
-                                                            tile_base, tile_seg, shift, dbits, offs,
-                                                            dst_k, dst_v);
+    if (pass == 0)
+      radix_scatter_seg_kernel<true><<<tmax, SORT_THREADS, 0, s>>>(
+          src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, shift, dbits, offs,
+          dst_k, dst_v);
+    else
+      radix_scatter_seg_kernel<false><<<tmax, SORT_THREADS, 0, s>>>(
+          src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, shift, dbits, offs,
+          dst_k, dst_v);
     LAT_LAUNCH_CHECK();
     src_k = dst_k; src_v = dst_v;
   }
