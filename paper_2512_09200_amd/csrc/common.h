@@ -14,6 +14,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
@@ -112,6 +113,8 @@ constexpr int NUM_XCD = 8;
 
 // Word 3 of a raw (untyped, unswizzled) buffer resource on gfx9-family GPUs.
 constexpr int BUF_RSRC_WORD3 = 0x00020000;
+// Cache-policy operand of a buffer access: non-temporal (the nt bit of gfx94x/gfx950).
+constexpr int BUF_NT = 2;
 __device__ inline int xcd_block(int bid, int nblocks) {
   const int x = bid % NUM_XCD, i = bid / NUM_XCD;
   const int q = nblocks / NUM_XCD, r = nblocks % NUM_XCD;

@@ -364,8 +364,8 @@ __global__ void set_empty_kernel(int* num_unique, int* seg_offsets) {
 // One wave per RANGE consecutive sorted occurrences.  The wave walks the
 // occurrences one dX row per step: lane l holds bytes [l*BPL, (l+1)*BPL) of
 // the row, so run starts and ends are the same for every lane and the
-// segmented sum is a single running fp32 accumulator per column, reset at
-// each run start and added to in position order (uniform branches, no
+// segmented sum is a single running fp32 accumulator per column, added to in
+// position order and cleared after each piece end (uniform branches, no
 // cross-lane arithmetic).  Per chunk of 64 occurrences:
 //   1. keys and bag ids (one per lane, prefetched a chunk ahead); run starts
 //      and ends by comparing neighbouring keys (ballots)
@@ -376,95 +376,256 @@ __global__ void set_empty_kernel(int* num_unique, int* seg_offsets) {
 //      the SGD update; the run cut by the range start (no start inside the
 //      range) goes to partial slot 0, the run cut by the range end to slot 1
 // No floating-point atomics; every sum is taken in position order.
-// FULL: the row is exactly 64*BPL bytes (every lane active, no predication).
-template <typename DT, typename ET, int BPL, bool MEAN, bool FULL>
+// FULL: the dX row is exactly 64*BPL bytes (every lane active, no predication).
+// SGD: table rows are updated.  The step is bound by instruction issue as much
+// as by memory, so the per-occurrence work is kept to a few instructions: row
+// offsets are read from lanes (v_readlane) straight into the scalar offset of
+// a buffer access, group positions are compile-time constants in full chunks,
+// and the table is addressed through a buffer resource based at the range's
+// first row whenever the range's rows span less than 4 GiB (EBUF).
+template <typename DT, typename ET, int BPL, bool MEAN, bool FULL, bool SGD>
 struct SegWave {
-  static constexpr int EPL = BPL / (int)sizeof(DT);       // columns per lane
+  static constexpr int EPL = BPL / (int)sizeof(DT);              // columns per lane
   static constexpr int S = BPL == 4 ? 32 : (BPL == 8 ? 16 : 8);  // rows in flight
-  // per-wave state (wave-uniform scalars and this lane's accumulators)
+  static constexpr int ENB = EPL * (int)sizeof(ET);              // table bytes per lane
+  // constants of the wave
+  __amdgpu_buffer_rsrc_t dXr;  // dX (< 4 GiB, checked by the launcher)
+  const char* dXb;
+  ET* E;
+  float *grad_rows, *part;
+  float lr;
+  int wave, dim, col, lane_b, lane_e;
+  int64_t erow_bytes;
+  bool active;
+  // running state: this lane's accumulators; wave-uniform run bookkeeping
   float acc[EPL];
-  bool started;
-  int u_before;
+  bool started;  // a run started at or after the range start
+  int u_before;  // run id of the run before the current chunk
+
+  // NB bytes of a buffer at byte offset voff + soff (streamed: each table row
+  // is read and written exactly once)
+  template <int NB>
+  __device__ static inline void buf_load(uint32_t* w, __amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    if constexpr (NB == 2) {
+      w[0] = __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, BUF_NT);
+    } else if constexpr (NB == 4) {
+      w[0] = __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, BUF_NT);
+    } else if constexpr (NB == 8) {
+      const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, BUF_NT);
+      w[0] = v[0];
+      w[1] = v[1];
+    } else {
+#pragma unroll
+      for (int q = 0; q < NB / 16; ++q) {
+        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff + 16 * q, soff, BUF_NT);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[4 * q + t] = v[t];
+      }
+    }
+  }
+  template <int NB>
+  __device__ static inline void buf_store(const uint32_t* w, __amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    if constexpr (NB == 2) {
+      __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w[0], r, voff, soff, BUF_NT);
+    } else if constexpr (NB == 4) {
+      __builtin_amdgcn_raw_buffer_store_b32(w[0], r, voff, soff, BUF_NT);
+    } else if constexpr (NB == 8) {
+      __builtin_amdgcn_raw_buffer_store_b64(u32x2{w[0], w[1]}, r, voff, soff, BUF_NT);
+    } else {
+#pragma unroll
+      for (int q = 0; q < NB / 16; ++q)
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]},
+                                               r, voff + 16 * q, soff, BUF_NT);
+    }
+  }
+  // the updated row values rounded to ET, as 32-bit words
+  __device__ static inline void pack(uint32_t* o, const float* v) {
+    if constexpr (sizeof(ET) == 2) {
+      if constexpr (EPL == 1) {
+        o[0] = f2bf(v[0]);
+      } else {
+#pragma unroll
+        for (int t = 0; t < EPL / 2; ++t) o[t] = pack_bf2(v[2 * t], v[2 * t + 1]);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < EPL; ++t) o[t] = __float_as_uint(v[t]);
+    }
+  }
 
   // One group of S occurrences starting at chunk row s0 (s0 + S <= cnt when
-  // CHECK is false).  xoff: per-lane byte offset of the occurrence's dX row;
-  // key: per-lane global row.
-  template <bool CHECK>
-  __device__ inline void group(int s0, int cnt, uint64_t smask, uint64_t cmask, uint64_t pmask,
-                               int xoff, int key, float scl, const char* dXb,
-                               __amdgpu_buffer_rsrc_t dXr, ET* E, float* grad_rows, float* part,
-                               int wave, int dim, int lane_b, int col, bool active, float lr) {
+  // CHECK is false).  Per lane (= chunk row): xoff, the byte offset of the
+  // occurrence's dX row; erow, its table row as a byte offset into er (EBUF)
+  // or as a row number (otherwise); scl, its bag's 1/length (MEAN).
+  template <bool CHECK, bool EBUF>
+  __device__ inline void group(const int s0, const int cnt, const uint64_t smask,
+                               const uint64_t cmask, const uint64_t pmask, const int xoff,
+                               const int erow, const float scl, const __amdgpu_buffer_rsrc_t er) {
     Frag<DT, EPL> xf[S];
     Frag<ET, EPL> ef[S];
-    const int lane_e = col * (int)sizeof(ET);
     // the group's run bits at positions 0 .. S-1 (constant-position tests below)
-    const uint64_t sm = smask >> s0, cm = cmask >> s0, pm = pmask >> s0;
+    static_assert(S <= 32, "group masks are 32-bit");
+    const uint32_t cm = (uint32_t)(cmask >> s0), pm = (uint32_t)(pmask >> s0);
 #pragma unroll
     for (int i = 0; i < S; ++i) {
       const int r = s0 + i;
       if (CHECK && r >= cnt) break;
       const int xr = __builtin_amdgcn_readlane(xoff, r);
       if constexpr (FULL) {
-        // 256-byte rows: one dword per lane, scalar row offset (buffer load)
         xf[i].w[0] = __builtin_amdgcn_raw_buffer_load_b32(dXr, lane_b, xr, 0);
       } else {
         if (active) xf[i].load(reinterpret_cast<const DT*>(dXb + (uint32_t)xr + lane_b));
       }
-      if (E && ((cm >> i) & 1)) {
-        const int kr = __builtin_amdgcn_readlane(key, r);
-        const char* erow = reinterpret_cast<const char*>(E) +
-                           (FULL ? ((int64_t)kr << 8) : (int64_t)kr * dim * (int64_t)sizeof(ET));
-        // each occurring table row is read and written exactly once: streamed
-        if (FULL || active) ef[i].load_nt(reinterpret_cast<const ET*>(erow + lane_e));
+      if (SGD && ((cm >> i) & 1)) {
+        const int er_r = __builtin_amdgcn_readlane(erow, r);
+        if (FULL || active) {
+          if constexpr (EBUF) {
+            buf_load<ENB>(ef[i].w, er, lane_e, er_r);
+          } else {
+            const char* p = reinterpret_cast<const char*>(E) + (int64_t)er_r * erow_bytes + lane_e;
+            ef[i].load_nt(reinterpret_cast<const ET*>(p));
+          }
+        }
       }
     }
+    // the table row offsets are read from their lanes again at the update, and
+    // the run-end bits tested again, rather than held in 2*S scalar registers
+    // across the group (opaque copies the compiler cannot fold into the loads')
+    int erow2 = erow;
+    uint32_t cm2 = cm;
+    if constexpr (SGD) asm volatile("" : "+v"(erow2), "+s"(cm2));
 #pragma unroll
     for (int i = 0; i < S; ++i) {
       const int r = s0 + i;
       if (CHECK && r >= cnt) break;
-      float sc = 1.f;
-      if (MEAN) sc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scl), r));
-      // running sum, restarted at a run start: acc * keep + v with keep = 0 or 1
-      // (exact for finite values in both cases)
-      const float keep = ((sm >> i) & 1) ? 0.f : 1.f;
+      if (MEAN) {
+        const float sc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scl), r));
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        const float v = MEAN ? xf[i].get(e) * sc : xf[i].get(e);
-        acc[e] = __builtin_fmaf(acc[e], keep, v);
+        for (int e = 0; e < EPL; ++e) acc[e] += xf[i].get(e) * sc;
+      } else {
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] += xf[i].get(e);
       }
-      if ((pm >> i) & 1) {
+      if ((pm >> i) & 1) {  // a piece ends here
         const uint64_t le = (r == 63) ? ~0ull : ((2ull << r) - 1);
-        if ((cm >> i) & 1) {
+        if ((cm2 >> i) & 1) {  // ... completing its run
           if (grad_rows && (FULL || active))
             Frag<float, EPL>::store(grad_rows + (int64_t)(u_before + __popcll(smask & le)) * dim + col, acc);
-          if (E) {
+          if constexpr (SGD) {
             float upd[EPL];
 #pragma unroll
             for (int e = 0; e < EPL; ++e) upd[e] = ef[i].get(e) - lr * acc[e];
-            const int kr = __builtin_amdgcn_readlane(key, r);
-            ET* erow = FULL ? reinterpret_cast<ET*>(reinterpret_cast<char*>(E) + ((int64_t)kr << 8))
-                            : E + (int64_t)kr * dim;
-            if (FULL || active) Frag<ET, EPL>::store_nt(erow + col, upd);
+            const int er_r = __builtin_amdgcn_readlane(erow2, r);
+            if (FULL || active) {
+              if constexpr (EBUF) {
+                uint32_t o[Frag<ET, EPL>::W];
+                pack(o, upd);
+                buf_store<ENB>(o, er, lane_e, er_r);
+              } else {
+                Frag<ET, EPL>::store_nt(reinterpret_cast<ET*>(reinterpret_cast<char*>(E) +
+                                                              (int64_t)er_r * erow_bytes + lane_e),
+                                        upd);
+              }
+            }
           }
         } else {
           const bool has_start = started || (smask & le);
           if (FULL || active)
             Frag<float, EPL>::store(part + ((int64_t)wave * 2 + (has_start ? 1 : 0)) * dim + col, acc);
         }
+        // the next occurrence starts a new run (or lies past the range)
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
       }
+    }
+  }
+
+  // The range's occurrences [r0, rend), chunk by chunk.  EBUF: er covers the
+  // table rows from row k_first on.
+  template <bool EBUF>
+  __device__ inline void run(const int* __restrict__ skeys, const int* __restrict__ sbags, int n,
+                             int r0, int rend, int B, int n_slots, int first_slot, int row_bytes,
+                             const int32_t* __restrict__ offsets, int lane, int k_first,
+                             __amdgpu_buffer_rsrc_t er, int* __restrict__ part_uid,
+                             int* __restrict__ span_list, int* __restrict__ span_count) {
+    int prev_key = r0 > 0 ? __builtin_amdgcn_readfirstlane(skeys[r0 - 1]) : -1;
+    int last_nxt = -1;
+    int p0 = r0;
+    int key = -1, bag = 0, nxt;
+    {
+      const int cnt = rend - p0 < 64 ? rend - p0 : 64;
+      if (lane < cnt) {
+        key = skeys[p0 + lane];
+        bag = sbags[p0 + lane];
+      }
+      nxt = p0 + cnt < n ? __builtin_amdgcn_readfirstlane(skeys[p0 + cnt]) : -1;
+    }
+    while (p0 < rend) {
+      const int cnt = rend - p0 < 64 ? rend - p0 : 64;
+      const bool valid = lane < cnt;
+      const int q0 = p0 + cnt;
+      int nkey = -1, nbag = 0, nnxt = -1;
+      if (q0 < rend) {
+        const int ncnt = rend - q0 < 64 ? rend - q0 : 64;
+        if (lane < ncnt) {
+          nkey = skeys[q0 + lane];
+          nbag = sbags[q0 + lane];
+        }
+        nnxt = q0 + ncnt < n ? __builtin_amdgcn_readfirstlane(skeys[q0 + ncnt]) : -1;
+      }
+      int kp = __shfl_up(key, 1, 64);
+      if (lane == 0) kp = prev_key;
+      int kn = __shfl_down(key, 1, 64);
+      if (lane == cnt - 1) kn = nxt;
+      const uint64_t smask = __ballot(valid && key != kp);  // run starts
+      const uint64_t emask = __ballot(valid && key != kn);  // run ends
+      // runs ending here are complete if a start lies at or before them in the range
+      const uint64_t ge_first = smask ? ~((smask & (~smask + 1)) - 1) : 0ull;
+      const uint64_t cmask = emask & (started ? ~0ull : ge_first);
+      const uint64_t pmask = emask | (q0 == rend ? (1ull << (cnt - 1)) : 0ull);  // piece ends
+      int xoff = 0, erow = 0;
+      float scl = 1.f;
+      if (valid) {
+        const int f = bag / B, b = bag - f * B;
+        xoff = (int)((uint32_t)(b * n_slots + first_slot + f) * (uint32_t)row_bytes);  // < 2^32
+        erow = EBUF ? (int)((uint32_t)(key - k_first) * (uint32_t)erow_bytes) : key;   // < 2^32
+        if (MEAN) scl = 1.f / (float)(offsets[bag + 1] - offsets[bag]);
+      }
+      // full chunks: the groups unrolled with constant positions (not for the
+      // far-apart-rows fallback of the SGD path, which is rare)
+      if ((!SGD || EBUF) && cnt == 64) {
+#pragma unroll
+        for (int g = 0; g < 64 / S; ++g)
+          group<false, EBUF>(g * S, 64, smask, cmask, pmask, xoff, erow, scl, er);
+      } else {
+        for (int s0 = 0; s0 < cnt; s0 += S)
+          group<true, EBUF>(s0, cnt, smask, cmask, pmask, xoff, erow, scl, er);
+      }
+      started = started || smask != 0;
+      prev_key = __builtin_amdgcn_readlane(key, cnt - 1);
+      u_before += __popcll(smask);
+      last_nxt = nxt;
+      key = nkey;
+      bag = nbag;
+      nxt = nnxt;
+      p0 = q0;
+    }
+    if (lane == 0) {
+      const bool touch_end = rend < n && last_nxt == prev_key;
+      part_uid[wave] = touch_end ? u_before : -1;
+      if (touch_end && started) span_list[atomicAdd(span_count, 1)] = wave;
     }
   }
 };
 
-template <typename DT, typename ET, int BPL, bool MEAN, bool FULL>
+template <typename DT, typename ET, int BPL, bool MEAN, bool FULL, bool SGD>
 __global__ __launch_bounds__(256) void seg_reduce_kernel(
     const int* __restrict__ skeys, const int* __restrict__ sbags, int n,
     const DT* __restrict__ dX, int B, int n_slots, int first_slot, int dim,
     const int32_t* __restrict__ offsets, const int* __restrict__ range_ubefore,
     float* __restrict__ part, int* __restrict__ part_uid, int* __restrict__ span_list,
     int* __restrict__ span_count, float* __restrict__ grad_rows, ET* __restrict__ E, float lr) {
-  using W = SegWave<DT, ET, BPL, MEAN, FULL>;
-  constexpr int EPL = W::EPL, S = W::S;
+  using W = SegWave<DT, ET, BPL, MEAN, FULL, SGD>;
   const int lane = threadIdx.x & 63;
   // Each XCD takes a contiguous span of ranges, so the dX rows of one table's
   // occurrences stay in that XCD's L2 while it works through them.  Wave-
@@ -474,87 +635,45 @@ __global__ __launch_bounds__(256) void seg_reduce_kernel(
   const int r0 = wave * RANGE;
   if (r0 >= n) return;
   const int rend = n - r0 < RANGE ? n : r0 + RANGE;
-  const int col = lane * EPL;
-  const bool active = col < dim;
-  const int lane_b = lane * BPL;
-  const int row_bytes = dim * (int)sizeof(DT);
-  const char* dXb = reinterpret_cast<const char*>(dX);
-  // dX as a buffer of B*n_slots*dim elements (< 4 GiB, checked by the launcher)
-  const __amdgpu_buffer_rsrc_t dXr = __builtin_amdgcn_make_buffer_rsrc(
+  W w;
+  w.wave = wave;
+  w.dim = dim;
+  w.col = lane * W::EPL;
+  w.active = w.col < dim;
+  w.lane_b = lane * BPL;
+  w.lane_e = w.col * (int)sizeof(ET);
+  w.erow_bytes = (int64_t)dim * (int64_t)sizeof(ET);
+  w.dXb = reinterpret_cast<const char*>(dX);
+  w.dXr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<DT*>(dX), (short)0,
       (int)(uint32_t)((uint64_t)B * n_slots * dim * sizeof(DT) < 0xffffffffull
                           ? (uint64_t)B * n_slots * dim * sizeof(DT) : 0xffffffffull),
       BUF_RSRC_WORD3);
-
-  W w;
+  w.E = E;
+  w.grad_rows = grad_rows;
+  w.part = part;
+  w.lr = lr;
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) w.acc[e] = 0.f;
-  w.started = false;                                       // a run started at or after r0
-  w.u_before = __builtin_amdgcn_readfirstlane(range_ubefore[wave]);  // run id before the chunk
-  int prev_key = r0 > 0 ? __builtin_amdgcn_readfirstlane(skeys[r0 - 1]) : -1;
-  int last_nxt = -1;
-
-  int p0 = r0;
-  int key = -1, bag = 0, nxt;
-  {
-    const int cnt = rend - p0 < 64 ? rend - p0 : 64;
-    if (lane < cnt) {
-      key = skeys[p0 + lane];
-      bag = sbags[p0 + lane];
+  for (int e = 0; e < W::EPL; ++e) w.acc[e] = 0.f;
+  w.started = false;
+  w.u_before = __builtin_amdgcn_readfirstlane(range_ubefore[wave]);
+  const int row_bytes = dim * (int)sizeof(DT);
+  if constexpr (SGD) {
+    // the range's keys are sorted: its table rows lie in [k_first, k_last]
+    const int k_first = __builtin_amdgcn_readfirstlane(skeys[r0]);
+    const int k_last = __builtin_amdgcn_readfirstlane(skeys[rend - 1]);
+    const uint64_t span = (uint64_t)(k_last - k_first + 1) * (uint64_t)w.erow_bytes;
+    if (span <= 0xffffffffull) {
+      const __amdgpu_buffer_rsrc_t er = __builtin_amdgcn_make_buffer_rsrc(
+          reinterpret_cast<char*>(E) + (int64_t)k_first * w.erow_bytes, (short)0,
+          (int)(uint32_t)span, BUF_RSRC_WORD3);
+      w.template run<true>(skeys, sbags, n, r0, rend, B, n_slots, first_slot, row_bytes, offsets,
+                           lane, k_first, er, part_uid, span_list, span_count);
+      return;
     }
-    nxt = p0 + cnt < n ? __builtin_amdgcn_readfirstlane(skeys[p0 + cnt]) : -1;
   }
-  while (p0 < rend) {
-    const int cnt = rend - p0 < 64 ? rend - p0 : 64;
-    const bool valid = lane < cnt;
-    const int q0 = p0 + cnt;
-    int nkey = -1, nbag = 0, nnxt = -1;
-    if (q0 < rend) {
-      const int ncnt = rend - q0 < 64 ? rend - q0 : 64;
-      if (lane < ncnt) {
-        nkey = skeys[q0 + lane];
-        nbag = sbags[q0 + lane];
-      }
-      nnxt = q0 + ncnt < n ? __builtin_amdgcn_readfirstlane(skeys[q0 + ncnt]) : -1;
-    }
-    int kp = __shfl_up(key, 1, 64);
-    if (lane == 0) kp = prev_key;
-    int kn = __shfl_down(key, 1, 64);
-    if (lane == cnt - 1) kn = nxt;
-    const uint64_t smask = __ballot(valid && key != kp);   // run starts
-    const uint64_t emask = __ballot(valid && key != kn);   // run ends
-    // runs ending here are complete if a start lies at or before them in the range
-    const uint64_t ge_first = smask ? ~((smask & (~smask + 1)) - 1) : 0ull;
-    const uint64_t cmask = emask & (w.started ? ~0ull : ge_first);
-    const uint64_t pmask = emask | (q0 == rend ? (1ull << (cnt - 1)) : 0ull);  // piece ends
-    int xoff = 0;
-    float scl = 1.f;
-    if (valid) {
-      const int f = bag / B, b = bag - f * B;
-      xoff = (int)((uint32_t)(b * n_slots + first_slot + f) * (uint32_t)row_bytes);  // < 2^32 (host check)
-      if (MEAN) scl = 1.f / (float)(offsets[bag + 1] - offsets[bag]);
-    }
-    int s0 = 0;
-    for (; s0 + S <= cnt; s0 += S)
-      w.template group<false>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, dXr, E, grad_rows,
-                              part, wave, dim, lane_b, col, active, lr);
-    if (s0 < cnt)
-      w.template group<true>(s0, cnt, smask, cmask, pmask, xoff, key, scl, dXb, dXr, E, grad_rows,
-                             part, wave, dim, lane_b, col, active, lr);
-    w.started = w.started || smask != 0;
-    prev_key = __builtin_amdgcn_readlane(key, cnt - 1);
-    w.u_before += __popcll(smask);
-    last_nxt = nxt;
-    key = nkey;
-    bag = nbag;
-    nxt = nnxt;
-    p0 = q0;
-  }
-  if (lane == 0) {
-    const bool touch_end = rend < n && last_nxt == prev_key;
-    part_uid[wave] = touch_end ? w.u_before : -1;
-    if (touch_end && w.started) span_list[atomicAdd(span_count, 1)] = wave;
-  }
+  w.template run<false>(skeys, sbags, n, r0, rend, B, n_slots, first_slot, row_bytes, offsets,
+                        lane, 0, w.dXr, part_uid, span_list, span_count);
 }
 
 // One wave per run that crosses a range boundary: its partial sums (slot 1 of
@@ -656,10 +775,17 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
   LAT_HIP_CHECK(record(0));
   const int row_bytes = dim * (int)sizeof(DT);
   const int grid = cdiv(ranges, 4);
-#define LAT_SEG(BPLV, MV, FV)                                                               \
-  seg_reduce_kernel<DT, ET, BPLV, MV, FV><<<grid, 256, 0, s>>>(                            \
-      skeys, sbags, n, (const DT*)dX, B, n_slots, first_slot, dim, offsets, range_ubefore, \
-      part, part_uid, span_list, span_count, grad_rows, (ET*)E, lr)
+#define LAT_SEG(BPLV, MV, FV)                                                                \
+  do {                                                                                      \
+    if (E)                                                                                  \
+      seg_reduce_kernel<DT, ET, BPLV, MV, FV, true><<<grid, 256, 0, s>>>(                   \
+          skeys, sbags, n, (const DT*)dX, B, n_slots, first_slot, dim, offsets, range_ubefore, \
+          part, part_uid, span_list, span_count, grad_rows, (ET*)E, lr);                    \
+    else                                                                                    \
+      seg_reduce_kernel<DT, ET, BPLV, MV, FV, false><<<grid, 256, 0, s>>>(                  \
+          skeys, sbags, n, (const DT*)dX, B, n_slots, first_slot, dim, offsets, range_ubefore, \
+          part, part_uid, span_list, span_count, grad_rows, (ET*)E, lr);                    \
+  } while (0)
   if (row_bytes == 256) {
     if (mean) LAT_SEG(4, true, true); else LAT_SEG(4, false, true);
   } else if (row_bytes < 256) {

@@ -237,3 +237,84 @@ def test_embbag_bwd_range_boundaries(d, dtype, pool, lr):
         assert np.array_equal(E1[untouched], E0[untouched]), "untouched rows changed"
     else:
         assert np.array_equal(E1, E0)
+
+
+MIXED = [(128, "bf16", "f32"), (64, "f32", "bf16"), (32, "bf16", "f32"), (256, "f32", "bf16")]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("d,dx_dtype,table_dtype", MIXED, ids=[f"d{d}-dX{a}-E{b}" for d, a, b in MIXED])
+def test_embbag_bwd_mixed_dtypes(d, dx_dtype, table_dtype):
+    """The gradient's storage dtype differs from the table's: the table rows
+    are addressed by their own width (dX rows of 256 bytes with 512- or
+    128-byte table rows included)."""
+    from paper_2512_09200_amd import api
+    print(f"[embbag_bwd_mixed] d={d} dX {dx_dtype} table {table_dtype}", flush=True)
+    F, B, rows, lr = 3, 37, 700, 0.25
+    rng = np.random.default_rng(77 + d)
+    offsets, idx = _structured_bags(rng, F, B, rows)
+    row_base = np.arange(F + 1, dtype=np.int64) * rows
+    E = torch.from_numpy(synth.randn((F * rows, d), seed=d, stream=5, scale=0.1, dtype=table_dtype)).to(
+        synth.torch_dtype(table_dtype)).to(DEV)
+    dX_np = synth.randn((B, F + 1, d), seed=d, stream=6, dtype=dx_dtype)
+    dX = torch.from_numpy(dX_np).to(synth.torch_dtype(dx_dtype)).to(DEV)
+    E0 = E.float().cpu().double().numpy()
+    out = api.lattice_embbag_bwd(E, torch.from_numpy(row_base).to(DEV), torch.from_numpy(offsets).to(DEV),
+                                 torch.from_numpy(idx).to(DEV), F, B, dX, 1, lr=lr)
+    torch.cuda.synchronize()
+    uniq, G = oe.pool_backward(dX_np[:, 1:], row_base, offsets, idx, F, B, "sum")
+    U = int(out["num_unique"].item())
+    assert U == uniq.size
+    # dX values are exact in fp64: the fp32 sums are within fp32 rounding
+    assert_close("grad_rows", out["grad_rows"][:U], G, 1e-5)
+    E1 = E.float().cpu().double().numpy()
+    t = 1e-5 if table_dtype == "f32" else 2e-2
+    assert_close("updated_rows", E1[uniq], oe.sgd_rows(E0[uniq], G, lr, rounding(table_dtype)), t)
+    untouched = np.ones(E0.shape[0], bool)
+    untouched[uniq] = False
+    assert np.array_equal(E1[untouched], E0[untouched]), "untouched rows changed"
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("rows", [(1 << 24) - 1, (1 << 24) + 1], ids=["span-4GiB-minus-256B", "span-over-4GiB"])
+def test_embbag_bwd_far_apart_rows(rows):
+    """A 4 GiB bf16 table (d=128, 256-byte rows) whose first and last rows
+    occur in the same reduction range: the rows such a range touches span
+    just under 4 GiB (one buffer window) or just over it (64-bit row
+    addresses).  The table is zero except the touched rows; only those and
+    their neighbours are compared."""
+    from paper_2512_09200_amd import api
+    print(f"[embbag_bwd_far] rows={rows}", flush=True)
+    d, F, B, lr = 128, 1, 8, 0.5
+    touched = np.array([0, 1, 5, rows // 2, rows - 3, rows - 1], np.int64)
+    rng = np.random.default_rng(rows)
+    idx = rng.choice(touched, size=40).astype(np.int32)
+    idx[:2] = [0, rows - 1]
+    cuts = np.sort(rng.integers(0, idx.size + 1, size=B - 1))
+    offsets = np.concatenate([[0], cuts, [idx.size]]).astype(np.int32)
+    row_base = np.array([0, rows], np.int64)
+    E = torch.zeros((rows, d), dtype=torch.bfloat16, device=DEV)
+    look = np.unique(np.clip(np.concatenate([touched - 1, touched, touched + 1]), 0, rows - 1))
+    vals = torch.from_numpy(synth.randn((look.size, d), seed=3, stream=7, scale=0.1, dtype="bf16")).to(
+        torch.bfloat16).to(DEV)
+    look_t = torch.from_numpy(look).to(DEV)
+    E[look_t] = vals
+    E0 = E[look_t].float().cpu().double().numpy()
+    dX_np = synth.randn((B, F, d), seed=4, stream=8, dtype="bf16")
+    dX = torch.from_numpy(dX_np).to(torch.bfloat16).to(DEV)
+    out = api.lattice_embbag_bwd(E, torch.from_numpy(row_base).to(DEV), torch.from_numpy(offsets).to(DEV),
+                                 torch.from_numpy(idx).to(DEV), F, B, dX, 0, lr=lr)
+    torch.cuda.synchronize()
+    uniq, G = oe.pool_backward(dX_np, row_base, offsets, idx, F, B, "sum")
+    U = int(out["num_unique"].item())
+    assert U == uniq.size
+    np.testing.assert_array_equal(out["unique_rows"][:U].cpu().numpy(), uniq)
+    assert_close("grad_rows", out["grad_rows"][:U], G, 1e-5)
+    E1 = E[look_t].float().cpu().double().numpy()
+    pos = np.searchsorted(look, uniq)
+    assert_close("updated_rows", E1[pos], oe.sgd_rows(E0[pos], G, lr, rounding("bf16")), 2e-2)
+    other = np.ones(look.size, bool)
+    other[pos] = False
+    assert np.array_equal(E1[other], E0[other]), "untouched rows changed"
+    del E
+    torch.cuda.empty_cache()
