@@ -184,13 +184,32 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
   float acc[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+  // bag (index k within the wave's bags) of position p
+  auto bag_of = [&](int p) {
+    int k = 0;
+    for (int q = 1; q < nb; ++q) k += p >= __builtin_amdgcn_readlane(offv, q) ? 1 : 0;
+    return k;
+  };
+  // a chunk's indices and table bases are loaded one chunk ahead: while the
+  // rows of one chunk are summed, the next chunk's row numbers are in flight
+  int k = 0, idx = 0;
+  int64_t rb = 0;
+  if (p_begin + lane < p_end) {
+    k = bag_of(p_begin + lane);
+    idx = indices[p_begin + lane];
+    rb = row_base[(b0 + k) / B];
+  }
   for (int p0 = p_begin; p0 < p_end; p0 += 64) {
     const int cnt = p_end - p0 < 64 ? p_end - p0 : 64;
     const int p = p0 + lane;
     const bool valid = lane < cnt;
-    // bag (index k within the wave's bags) of this lane's position
-    int k = 0;
-    for (int q = 1; q < nb; ++q) k += p >= __builtin_amdgcn_readlane(offv, q) ? 1 : 0;
+    int nk = 0, nidx = 0;
+    int64_t nrb = 0;
+    if (p + 64 < p_end) {
+      nk = bag_of(p + 64);
+      nidx = indices[p + 64];
+      nrb = row_base[(b0 + nk) / B];
+    }
     // (shuffles stay outside divergent code: a shuffle from a lane that is
     // switched off reads nothing)
     const int next_off = __shfl(offv, k + 1, 64);
@@ -201,7 +220,7 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
     int grow = 0, xrow = 0;
     float inv_len = 1.f;
     if (valid) {
-      grow = (int)(row_base[f] + indices[p]);
+      grow = (int)(rb + idx);
       xrow = b * n_slots + first_slot + f;
       if (MEAN) inv_len = 1.f / (float)(next_off - this_off);
     }
@@ -212,6 +231,9 @@ __global__ __launch_bounds__(256) void embbag_fwd_kernel(
     if (s0 < cnt)
       fwd_group<TT, XT, EPL, S, MEAN, FULL, true>(s0, cnt, emask, grow, xrow, inv_len, Eb, row_bytes,
                                                    lane_b, X, dim, col, active, acc);
+    k = nk;
+    idx = nidx;
+    rb = nrb;
   }
   // empty bags pool to zero
   for (int q = 0; q < nb; ++q) {
