@@ -6,8 +6,6 @@
 namespace lat {
 
 // sort.hip
-size_t scan_workspace(int64_t n);
-hipError_t exclusive_scan(const int* in, int* out, int64_t n, int* tmp, hipStream_t s);
 hipError_t exclusive_scan_inplace_small(int* a, int n, hipStream_t s);
 // Sort of a jagged batch's (global row, bag) pairs whose positions are grouped
 // by feature: each feature segment is sorted by its local row (< max_local_rows).

@@ -1,13 +1,16 @@
-// Stable LSD radix sort of (int32 key, int32 value) pairs and a device-wide
-// exclusive scan, used by the deterministic embedding backward to group the
-// occurrences of each table row.
+// Stable LSD radix sort of the occurrences of a jagged batch by table row
+// (int32 key, int32 bag id), used by the deterministic embedding backward to
+// group the occurrences of each row.
 //
-// Sort pass (digit of up to 8 bits):
-//   hist    : per tile of 4096 items, digit histogram in LDS -> counts
-//   scan    : exclusive scan of the counts -> global bucket offsets
-//   scatter : each wave ranks its contiguous 1024-item chunk with ballots
-//             (items with equal digits keep their order), waves are ordered
-//             within the tile, tiles within the bucket: a stable pass.
+// One histogram pass over the batch's indices counts every digit of every
+// pass per feature segment (the counts of a digit do not depend on the order
+// the previous passes leave).  Each sort pass is then a single kernel: a tile
+// of 4096 items is ranked with wave ballots (items with equal digits keep
+// their order), its digit counts are published, and its output offsets come
+// from the segment's digit bases plus the counts of the segment's earlier
+// tiles, read by decoupled look-back over the tiles' published counts (tiles
+// take their ids in the order they start, so every tile looked back at is
+// running and publishes without waiting).
 #include "common.h"
 #include "kernels.h"
 
@@ -20,12 +23,10 @@ constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 
 constexpr int SCAN_THREADS = 256;
-constexpr int SCAN_ITEMS = 16;
-constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;  // 4096
 static_assert(SORT_THREADS == RADIX, "one thread per digit in the scatter's tile scan");
 
 // ---------------------------------------------------------------------------
-// device-wide exclusive scan of int32 (counts fit int32: totals < 2^31)
+// block-wide and small exclusive scans of int32 (counts fit int32: totals < 2^31)
 // ---------------------------------------------------------------------------
 __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
   // lds: at least SCAN_THREADS/64 ints
@@ -50,21 +51,6 @@ __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
   return wbase + x - v;
 }
 
-__global__ __launch_bounds__(SCAN_THREADS) void scan_reduce_kernel(const int* __restrict__ in, int n,
-                                                                    int* __restrict__ sums) {
-  __shared__ int lds[SCAN_THREADS / 64];
-  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
-  int s = 0;
-#pragma unroll
-  for (int i = 0; i < SCAN_ITEMS; ++i) {
-    int64_t k = base + (int64_t)i * SCAN_THREADS + threadIdx.x;
-    if (k < n) s += in[k];
-  }
-  int tot;
-  block_exclusive_scan(s, lds, &tot);
-  if (threadIdx.x == 0) sums[blockIdx.x] = tot;
-}
-
 // single block: exclusive scan of the tile sums in place
 __global__ __launch_bounds__(1024) void scan_sums_kernel(int* __restrict__ sums, int n) {
   __shared__ int lds[1024 / 64];
@@ -84,45 +70,6 @@ __global__ __launch_bounds__(1024) void scan_sums_kernel(int* __restrict__ sums,
   }
 }
 
-// sums: the tile totals (not scanned); each block adds up those before it
-__global__ __launch_bounds__(SCAN_THREADS) void scan_apply_kernel(const int* __restrict__ in, int n,
-                                                                   const int* __restrict__ sums,
-                                                                   int* __restrict__ out) {
-  __shared__ int lds[SCAN_THREADS / 64];
-  int p = 0;
-  for (int i = threadIdx.x; i < (int)blockIdx.x; i += SCAN_THREADS) p += sums[i];
-  int prefix;
-  block_exclusive_scan(p, lds, &prefix);
-  // blocked arrangement: thread t owns items [t*ITEMS, (t+1)*ITEMS) of the tile
-  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + (int64_t)threadIdx.x * SCAN_ITEMS;
-  int v[SCAN_ITEMS];
-  int s = 0;
-#pragma unroll
-  for (int i = 0; i < SCAN_ITEMS; ++i) {
-    v[i] = (base + i < n) ? in[base + i] : 0;
-    s += v[i];
-  }
-  int tot;
-  int run = block_exclusive_scan(s, lds, &tot) + prefix;
-#pragma unroll
-  for (int i = 0; i < SCAN_ITEMS; ++i) {
-    if (base + i < n) out[base + i] = run;
-    run += v[i];
-  }
-}
-
-size_t scan_workspace(int64_t n) { return (size_t)(cdiv(n, SCAN_TILE) + 1) * sizeof(int); }
-
-hipError_t exclusive_scan(const int* in, int* out, int64_t n, int* tmp, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  const int tiles = cdiv(n, SCAN_TILE);
-  scan_reduce_kernel<<<tiles, SCAN_THREADS, 0, s>>>(in, (int)n, tmp);
-  LAT_LAUNCH_CHECK();
-  scan_apply_kernel<<<tiles, SCAN_THREADS, 0, s>>>(in, (int)n, tmp, out);
-  LAT_LAUNCH_CHECK();
-  return hipSuccess;
-}
-
 // ---------------------------------------------------------------------------
 // radix sort
 // ---------------------------------------------------------------------------
@@ -140,15 +87,16 @@ static int key_bits(int64_t max_key) {
 // lie in [row_base[f], row_base[f] + rows_f).  Sorting every segment by its
 // local row (key - row_base[f]) is therefore a sort by global key, and needs
 // only as many digit passes as the largest table has row bits.  Tiles never
-// straddle segments; a pass scatters each tile inside its own segment, with
-// bucket offsets from one device-wide scan of the counts laid out as
-// [segment][digit][tile of the segment].
+// straddle segments; a pass scatters each tile inside its own segment.
 
+// tiles per segment (tile_base, scanned afterwards); also clears zero[0 .. nzero)
 __global__ __launch_bounds__(256) void seg_ntiles_kernel(const int32_t* __restrict__ offsets, int F,
-                                                         int B, int* __restrict__ tile_base) {
-  const int f = blockIdx.x * 256 + threadIdx.x;
-  if (f > F) return;
-  tile_base[f] = f < F ? (offsets[(int64_t)(f + 1) * B] - offsets[(int64_t)f * B] + SORT_TILE - 1) / SORT_TILE : 0;
+                                                         int B, int* __restrict__ tile_base,
+                                                         int* __restrict__ zero, int nzero) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < nzero) zero[i] = 0;
+  if (i <= F)
+    tile_base[i] = i < F ? (offsets[(int64_t)(i + 1) * B] - offsets[(int64_t)i * B] + SORT_TILE - 1) / SORT_TILE : 0;
 }
 
 // tile -> segment map: block f fills its segment's tiles
@@ -175,62 +123,80 @@ __global__ __launch_bounds__(256) void seg_tilebag_kernel(const int32_t* __restr
 }
 
 struct SegTile {
-  int f, lt, nt, base, cnt, cb;  // segment, tile within it, its tile count, first position, items, count base
-  int64_t key0;                  // row_base[f]
+  int f, lt, base, cnt;  // segment, tile within it, first position, items
+  int64_t key0;          // row_base[f]
 };
 
-__device__ inline bool seg_tile(const int* tile_base, const int* tile_seg, const int32_t* offsets,
-                                const int64_t* row_base, int F, int B, int radix, SegTile& t) {
-  const int tix = blockIdx.x;
-  if (tix >= tile_base[F]) return false;
+__device__ inline void seg_tile(int tix, const int* tile_base, const int* tile_seg,
+                                const int32_t* offsets, const int64_t* row_base, int B, SegTile& t) {
   t.f = tile_seg[tix];
-  const int tb = tile_base[t.f];
-  t.lt = tix - tb;
-  t.nt = tile_base[t.f + 1] - tb;
+  t.lt = tix - tile_base[t.f];
   const int s0 = offsets[(int64_t)t.f * B], s1 = offsets[(int64_t)(t.f + 1) * B];
   t.base = s0 + t.lt * SORT_TILE;
   t.cnt = s1 - t.base < SORT_TILE ? s1 - t.base : SORT_TILE;
-  t.cb = tb * radix;
   t.key0 = row_base[t.f];
-  return true;
 }
 
-// keys: global rows, or (local = 1, the first pass) the batch's indices,
-// i.e. rows local to the segment's table
-__global__ __launch_bounds__(SORT_THREADS) void radix_hist_seg_kernel(
-    const int* __restrict__ keys, int local, const int32_t* __restrict__ offsets,
+// Digit counts of every pass per segment, ghist[pass][f][digit] (zeroed
+// before), from the batch's indices (rows local to the segment's table); each
+// tile also clears its look-back words of every pass.
+__global__ __launch_bounds__(SORT_THREADS) void radix_hist_all_kernel(
+    const int32_t* __restrict__ indices, const int32_t* __restrict__ offsets,
     const int64_t* __restrict__ row_base, int F, int B, const int* __restrict__ tile_base,
-    const int* __restrict__ tile_seg, int shift, int dbits, int* __restrict__ counts) {
-  __shared__ int hist[RADIX];
+    const int* __restrict__ tile_seg, int passes, int dbits, int tmax, int* __restrict__ ghist,
+    uint32_t* __restrict__ state) {
+  __shared__ int hist[4][RADIX];
+  const int tix = blockIdx.x;
+  if (tix >= tile_base[F]) return;
   const int radix = 1 << dbits;
   SegTile t;
-  if (!seg_tile(tile_base, tile_seg, offsets, row_base, F, B, radix, t)) {
-    // blocks past the last tile clear the unused tail of the counts
-    for (int d = threadIdx.x; d < radix; d += SORT_THREADS) counts[(int64_t)blockIdx.x * radix + d] = 0;
-    return;
+  seg_tile(tix, tile_base, tile_seg, offsets, row_base, B, t);
+  for (int i = threadIdx.x; i < passes * radix; i += SORT_THREADS) {
+    hist[i / radix][i % radix] = 0;
+    state[((int64_t)(i / radix) * tmax + tix) * radix + i % radix] = 0u;
   }
-  for (int i = threadIdx.x; i < radix; i += SORT_THREADS) hist[i] = 0;
   __syncthreads();
-  const int key0 = local ? 0 : (int)t.key0;
 #pragma unroll
   for (int i = 0; i < SORT_ITEMS; ++i) {
     const int k = i * SORT_THREADS + threadIdx.x;
-    if (k < t.cnt) atomicAdd(&hist[((uint32_t)(keys[t.base + k] - key0) >> shift) & (radix - 1)], 1);
+    if (k < t.cnt) {
+      const uint32_t r = (uint32_t)indices[t.base + k];
+      for (int p = 0; p < passes; ++p) atomicAdd(&hist[p][(r >> (p * dbits)) & (radix - 1)], 1);
+    }
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < radix; d += SORT_THREADS) counts[t.cb + (int64_t)d * t.nt + t.lt] = hist[d];
+  for (int i = threadIdx.x; i < passes * radix; i += SORT_THREADS) {
+    const int c = hist[i / radix][i % radix];
+    if (c) atomicAdd(&ghist[((int64_t)(i / radix) * F + t.f) * radix + i % radix], c);
+  }
 }
 
-// FIRST (the first pass): keys_in are the batch's indices (local rows) and
-// vals_in is unused: the keys become global rows (+ row_base of the
-// segment) and the values the bag ids, expanded from the offsets of the
+// Look-back words: bits 30-31 = 0 (not yet published), 1 (the tile's own
+// count of the digit), 2 (inclusive count over the segment's tiles up to
+// this one); bits 0-29 the count (< 2^30 occurrences).
+constexpr uint32_t LB_AGG = 1u << 30, LB_INC = 2u << 30, LB_VAL = (1u << 30) - 1;
+constexpr int LB_WIN = 8;
+// tile counters of the sort passes, one per (pass, segment), 128 bytes apart
+constexpr int CTR_STRIDE = 32;
+
+__device__ inline void lb_store(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint32_t lb_load(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One sort pass.  FIRST (the first pass): keys_in are the batch's indices
+// (local rows) and vals_in is unused: the keys become global rows (+ row_base
+// of the segment) and the values the bag ids, expanded from the offsets of the
 // bags the tile covers (tile_bag0: the first of them).
 template <bool FIRST>
 __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
     const int* __restrict__ keys_in, const int* __restrict__ vals_in,
     const int* __restrict__ tile_bag0, const int32_t* __restrict__ offsets,
     const int64_t* __restrict__ row_base, int F, int B, const int* __restrict__ tile_base,
-    const int* __restrict__ tile_seg, int shift, int dbits, const int* __restrict__ coffs,
+    const int* __restrict__ tile_seg, int pass, int dbits, int tmax,
+    const int* __restrict__ ghist, uint32_t* __restrict__ state, int* __restrict__ tile_ctr,
     int* __restrict__ keys_out, int* __restrict__ vals_out) {
   constexpr int NW = SORT_THREADS / 64;
   constexpr int CHUNK = SORT_TILE / NW;  // 1024 consecutive items per wave
@@ -240,9 +206,21 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   __shared__ int scan_tmp[SORT_THREADS / 64];
   __shared__ int lkeys[SORT_TILE];
   __shared__ int lvals[SORT_TILE];
+  __shared__ int s_tix;
+  // Block b works on a tile of the segment static tile b lies in; which one
+  // is the order the segment's blocks start in (one counter per segment and
+  // pass: a single device-wide counter serialises every block's start)
+  if ((int)blockIdx.x >= tile_base[F]) return;
+  if (threadIdx.x == 0) {
+    const int f0 = tile_seg[blockIdx.x];
+    s_tix = tile_base[f0] + atomicAdd(&tile_ctr[((int64_t)pass * F + f0) * CTR_STRIDE], 1);
+  }
+  __syncthreads();
+  const int tix = s_tix;
   const int radix = 1 << dbits;
+  const int shift = pass * dbits;
   SegTile t;
-  if (!seg_tile(tile_base, tile_seg, offsets, row_base, F, B, radix, t)) return;
+  seg_tile(tix, tile_base, tile_seg, offsets, row_base, B, t);
   const int key0 = (int)t.key0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < NW * RADIX; i += SORT_THREADS) (&wcnt[0][0])[i] = 0;
@@ -252,7 +230,7 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
     // are known): bag0 + i for i = thread, thread + 256, ... until the bags
     // start past the tile
     const int tend = t.base + t.cnt, bag_end = (t.f + 1) * B;
-    for (int bag = tile_bag0[blockIdx.x] + threadIdx.x; bag < bag_end; bag += SORT_THREADS) {
+    for (int bag = tile_bag0[tix] + threadIdx.x; bag < bag_end; bag += SORT_THREADS) {
       const int lo = offsets[bag];
       if (lo >= tend) break;
       const int hi = offsets[bag + 1] < tend ? offsets[bag + 1] : tend;
@@ -296,16 +274,54 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   }
   __syncthreads();
-  // tile-level digit starts (exclusive scan over digits) and per-wave bases
   {
     const int d = threadIdx.x;  // SORT_THREADS == RADIX >= radix
     int tot = 0;
     if (d < radix)
       for (int i = 0; i < NW; ++i) tot += wcnt[i][d];
+    // publish this tile's count of digit d, then add up the counts of the
+    // segment's earlier tiles: back over published counts until an
+    // inclusive one (the segment's first tile publishes its count as such)
+    uint32_t* st = state + (int64_t)pass * tmax * radix;
+    int excl = 0;
+    if (d < radix) {
+      lb_store(st + (int64_t)tix * radix + d, (t.lt == 0 ? LB_INC : LB_AGG) | (uint32_t)tot);
+      if (t.lt > 0) {
+        // LB_WIN predecessors read per round trip, nearest first; a word not
+        // yet published ends the round (it is read again next round)
+        const int jlo = tix - t.lt;  // the segment's first tile
+        for (int j = tix - 1;;) {
+          uint32_t v[LB_WIN];
+#pragma unroll
+          for (int q = 0; q < LB_WIN; ++q)
+            v[q] = j - q >= jlo ? lb_load(st + (int64_t)(j - q) * radix + d) : LB_INC;
+          bool done = false;
+          int q = 0;
+#pragma unroll
+          for (; q < LB_WIN; ++q) {
+            if ((v[q] & ~LB_VAL) == 0u) break;
+            excl += (int)(v[q] & LB_VAL);
+            if (v[q] & LB_INC) {
+              done = true;
+              break;
+            }
+          }
+          if (done) break;
+          j -= q;
+          if (q < LB_WIN) __builtin_amdgcn_s_sleep(1);
+        }
+        lb_store(st + (int64_t)tix * radix + d, LB_INC | (uint32_t)(excl + tot));
+      }
+    }
+    // the segment's bucket of digit d starts after the segment's items of
+    // smaller digits
+    const int g = d < radix ? ghist[((int64_t)pass * F + t.f) * radix + d] : 0;
     int all;
-    const int st = block_exclusive_scan(tot, scan_tmp, &all);
-    if (d < radix) dbase[d] = coffs[t.cb + (int64_t)d * t.nt + t.lt] - st;
-    int run = st;
+    const int gex = block_exclusive_scan(g, scan_tmp, &all);
+    // tile-level digit starts (exclusive scan over digits) and per-wave bases
+    const int tst = block_exclusive_scan(tot, scan_tmp, &all);
+    if (d < radix) dbase[d] = offsets[(int64_t)t.f * B] + gex + excl - tst;
+    int run = tst;
     if (d < radix)
       for (int i = 0; i < NW; ++i) {
         const int c = wcnt[i][d];
@@ -336,14 +352,15 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
 }
 
 static int seg_sort_tiles_max(int64_t n, int F) { return cdiv(n, SORT_TILE) + F; }
+constexpr int MAX_PASSES = 4;  // 31-bit rows, digits of up to 8 bits
 
 size_t radix_sort_segments_workspace(int64_t n, int F) {
   const int64_t tmax = seg_sort_tiles_max(n > 0 ? n : 1, F);
-  const size_t c = (size_t)RADIX * tmax;
-  return 2 * (size_t)(n > 0 ? n : 1) * sizeof(int)  // ping-pong keys/vals
-         + 2 * c * sizeof(int)                        // counts + offsets
-         + scan_workspace((int64_t)c)
-         + (size_t)(F + 1 + 2 * tmax) * sizeof(int) + 1024;  // tile_base, tile_seg, tile_bag0
+  return 2 * (size_t)(n > 0 ? n : 1) * sizeof(int)              // ping-pong keys/vals
+         + (size_t)MAX_PASSES * RADIX * tmax * sizeof(uint32_t)  // look-back words
+         + (size_t)MAX_PASSES * F * RADIX * sizeof(int)          // digit counts per segment
+         + (size_t)MAX_PASSES * F * CTR_STRIDE * sizeof(int)     // tile counters
+         + (size_t)(F + 1 + 2 * tmax) * sizeof(int) + 1024;      // tile_base, tile_seg, tile_bag0
 }
 
 hipError_t radix_sort_segments(const int32_t* indices, int64_t n, const int32_t* offsets, int F,
@@ -351,18 +368,23 @@ hipError_t radix_sort_segments(const int32_t* indices, int64_t n, const int32_t*
                                int* keys_out, int* vals_out, void* ws, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const int tmax = seg_sort_tiles_max(n, F);
-  const size_t c = (size_t)RADIX * tmax;
   char* p = static_cast<char*>(ws);
   int* kb = reinterpret_cast<int*>(p); p += (size_t)n * sizeof(int);
   int* vb = reinterpret_cast<int*>(p); p += (size_t)n * sizeof(int);
-  int* counts = reinterpret_cast<int*>(p); p += c * sizeof(int);
-  int* offs = reinterpret_cast<int*>(p); p += c * sizeof(int);
-  int* tmp = reinterpret_cast<int*>(p); p += scan_workspace((int64_t)c);
+  uint32_t* state = reinterpret_cast<uint32_t*>(p); p += (size_t)MAX_PASSES * RADIX * tmax * sizeof(uint32_t);
+  int* ghist = reinterpret_cast<int*>(p); p += (size_t)MAX_PASSES * F * RADIX * sizeof(int);
+  int* tile_ctr = reinterpret_cast<int*>(p); p += (size_t)MAX_PASSES * F * CTR_STRIDE * sizeof(int);
   int* tile_base = reinterpret_cast<int*>(p); p += (size_t)(F + 1) * sizeof(int);
   int* tile_seg = reinterpret_cast<int*>(p); p += (size_t)tmax * sizeof(int);
   int* tile_bag0 = reinterpret_cast<int*>(p);
 
-  seg_ntiles_kernel<<<cdiv(F + 1, 256), 256, 0, s>>>(offsets, F, B, tile_base);
+  const int bits = key_bits(max_local_rows > 0 ? max_local_rows - 1 : 0);
+  const int passes = bits == 0 ? 1 : (bits + RADIX_BITS - 1) / RADIX_BITS;
+  const int dbits = bits == 0 ? 1 : (bits + passes - 1) / passes;
+
+  // the digit counts and tile id counters (ghist and tile_ctr are adjacent)
+  const int nzero = MAX_PASSES * F * (RADIX + CTR_STRIDE);
+  seg_ntiles_kernel<<<cdiv(nzero, 256), 256, 0, s>>>(offsets, F, B, tile_base, ghist, nzero);
   LAT_LAUNCH_CHECK();
   hipError_t e = exclusive_scan_inplace_small(tile_base, F + 1, s);
   if (e != hipSuccess) return e;
@@ -370,11 +392,10 @@ hipError_t radix_sort_segments(const int32_t* indices, int64_t n, const int32_t*
   LAT_LAUNCH_CHECK();
   seg_tilebag_kernel<<<cdiv((int64_t)F * B, 256), 256, 0, s>>>(offsets, F, B, tile_base, tile_bag0);
   LAT_LAUNCH_CHECK();
+  radix_hist_all_kernel<<<tmax, SORT_THREADS, 0, s>>>(indices, offsets, row_base, F, B, tile_base,
+                                                      tile_seg, passes, dbits, tmax, ghist, state);
+  LAT_LAUNCH_CHECK();
 
-  const int bits = key_bits(max_local_rows > 0 ? max_local_rows - 1 : 0);
-  const int passes = bits == 0 ? 1 : (bits + RADIX_BITS - 1) / RADIX_BITS;
-  const int dbits = bits == 0 ? 1 : (bits + passes - 1) / passes;
-  const int radix = 1 << dbits;
   const int* src_k = indices;
   const int* src_v = nullptr;
   for (int pass = 0; pass < passes; ++pass) {
@@ -382,20 +403,14 @@ hipError_t radix_sort_segments(const int32_t* indices, int64_t n, const int32_t*
     const int remaining = passes - 1 - pass;
     int* dst_k = last ? keys_out : ((remaining % 2 == 1) ? kb : keys_out);
     int* dst_v = last ? vals_out : ((remaining % 2 == 1) ? vb : vals_out);
-    const int shift = pass * dbits;
-    radix_hist_seg_kernel<<<tmax, SORT_THREADS, 0, s>>>(src_k, pass == 0, offsets, row_base, F, B,
-                                                         tile_base, tile_seg, shift, dbits, counts);
-    LAT_LAUNCH_CHECK();
-    e = exclusive_scan(counts, offs, (int64_t)radix * tmax, tmp, s);
-    if (e != hipSuccess) return e;
     if (pass == 0)
       radix_scatter_seg_kernel<true><<<tmax, SORT_THREADS, 0, s>>>(
-          src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, shift, dbits, offs,
-          dst_k, dst_v);
+          src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, pass, dbits, tmax,
+          ghist, state, tile_ctr, dst_k, dst_v);
     else
       radix_scatter_seg_kernel<false><<<tmax, SORT_THREADS, 0, s>>>(
-          src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, shift, dbits, offs,
-          dst_k, dst_v);
+          src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, pass, dbits, tmax,
+          ghist, state, tile_ctr, dst_k, dst_v);
     LAT_LAUNCH_CHECK();
     src_k = dst_k; src_v = dst_v;
   }
