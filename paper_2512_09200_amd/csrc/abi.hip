@@ -694,6 +694,7 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   sc = std::max(sc, mlp_bwd_ws(&m->top, B));
   if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
   sc = std::max(sc, bce_workspace((int64_t)B * P->T));
+  sc = std::max(sc, head_workspace(B));
   L.interact = take(interact_ws(&m->interact, B));
   L.scratch = take(sc);
   L.scratch_bytes = (int64_t)sc;
@@ -847,7 +848,10 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   HIPRET(begin(LATTICE_STAGE_INTERACT_FWD));
   HIPRET(interact_fwd_impl(&m->interact, B, X, t, P.t_stride, at(L.interact), s));
   HIPRET(end(LATTICE_STAGE_INTERACT_FWD));
-  // 4. top MLP -> logits; 5. masked BCE
+  // 4. top MLP -> logits; 5. masked BCE.  bf16 models with at most 64 heads
+  // run the last layer as the fused heads: its forward with the loss
+  // partials, then dz, the loss and the last layer's input gradient (which
+  // starts the gradient chain of 6.) in the loss stage.
   HIPRET(begin(LATTICE_STAGE_TOP_FWD));
   const int nt = m->top.n_layers;
   void* tacts[LATTICE_MAX_LAYERS];
@@ -858,18 +862,46 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   }
   tacts[nt - 1] = at(L.logits);
   tstr[nt - 1] = T;
-  HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, s));
-  HIPRET(end(LATTICE_STAGE_TOP_FWD));
-  HIPRET(begin(LATTICE_STAGE_LOSS));
-  HIPRET(bce((const float*)at(L.logits), batch->labels, batch->mask, (int64_t)B * T,
-             (float*)at(L.loss), (float*)at(L.d_logits), at(L.d_logits_op), dt, scratch, s));
-  HIPRET(end(LATTICE_STAGE_LOSS));
-  // 6. top backward, gradient chain only -> d_t (weight gradients: 8.)
   void* gtop[LATTICE_MAX_LAYERS];
   for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) gtop[i] = at(P.g_top[i]);
+  const lattice_linear& head = m->top.layers[nt - 1];
+  const void* head_in = nt > 1 ? tacts[nt - 2] : t;
+  const int64_t head_ld = nt > 1 ? tstr[nt - 2] : P.t_stride;
+  const bool fused_heads = dt == DT_BF16 && head_fusable(T, head.in_dim, head_in, head_ld, head.W);
+  lattice_mlp_desc hidden = m->top;  // the layers before the heads
+  hidden.n_layers = nt - 1;
+  hidden.relu_last = 1;
+  if (fused_heads) {
+    if (nt > 1) HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, s));
+    HIPRET(head_fwd((const bf16_t*)head_in, head_ld, B, head.in_dim, (const bf16_t*)head.W, head.b,
+                    T, batch->labels, batch->mask, (float*)at(L.logits), scratch, s));
+  } else {
+    HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, s));
+  }
+  HIPRET(end(LATTICE_STAGE_TOP_FWD));
+  HIPRET(begin(LATTICE_STAGE_LOSS));
+  if (fused_heads) {
+    void* g_head = nt > 1 ? gtop[nt - 2] : at(L.d_t);
+    const int64_t g_ld = nt > 1 ? head.in_dim : P.t_stride;
+    HIPRET(head_bwd((const float*)at(L.logits), batch->labels, batch->mask, B, T,
+                    (const bf16_t*)head.W, head.in_dim, nt > 1 ? (const bf16_t*)head_in : nullptr,
+                    head_ld, (float*)at(L.loss), (float*)at(L.d_logits), (bf16_t*)at(L.d_logits_op),
+                    (bf16_t*)g_head, g_ld, scratch, s));
+  } else {
+    HIPRET(bce((const float*)at(L.logits), batch->labels, batch->mask, (int64_t)B * T,
+               (float*)at(L.loss), (float*)at(L.d_logits), at(L.d_logits_op), dt, scratch, s));
+  }
+  HIPRET(end(LATTICE_STAGE_LOSS));
+  // 6. top backward, gradient chain only -> d_t (weight gradients: 8.)
   HIPRET(begin(LATTICE_STAGE_TOP_BWD));
-  HIPRET(mlp_backward_data(&m->top, B, tacts, tstr, at(L.d_logits_op), T, at(L.d_t), P.t_stride,
-                           gtop, scratch, s));
+  if (fused_heads) {
+    if (nt > 1)
+      HIPRET(mlp_backward_data(&hidden, B, tacts, tstr, gtop[nt - 2], head.in_dim, at(L.d_t),
+                               P.t_stride, gtop, scratch, s));
+  } else {
+    HIPRET(mlp_backward_data(&m->top, B, tacts, tstr, at(L.d_logits_op), T, at(L.d_t), P.t_stride,
+                             gtop, scratch, s));
+  }
   HIPRET(end(LATTICE_STAGE_TOP_BWD));
   // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
   HIPRET(begin(LATTICE_STAGE_INTERACT_BWD));

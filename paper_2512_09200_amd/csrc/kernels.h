@@ -128,4 +128,18 @@ size_t bce_workspace(int64_t n);
 hipError_t bce(const float* z, const float* y, const uint8_t* m, int64_t n, float* loss, float* dz,
                void* dz_op, DType op_dt, void* ws, hipStream_t s);
 
+// head.hip (bf16 objective heads: last top layer fused with the masked BCE
+// and with its input gradient; workspace: per-block partials, written by
+// head_fwd and read by head_bwd)
+constexpr int HEAD_MAX_T = 64;
+bool head_fusable(int T, int K, const void* h, int64_t ldh, const void* W);
+size_t head_workspace(int B);
+hipError_t head_fwd(const bf16_t* h, int64_t ldh, int B, int K, const bf16_t* W,
+                    const float* bias, int T, const float* y, const uint8_t* m, float* z,
+                    void* ws, hipStream_t s);
+hipError_t head_bwd(const float* z, const float* y, const uint8_t* m, int B, int T,
+                    const bf16_t* W, int K, const bf16_t* mask, int64_t ldm, float* loss,
+                    float* dz, bf16_t* dz_op, bf16_t* g, int64_t ldg, const void* ws,
+                    hipStream_t s);
+
 }  // namespace lat
