@@ -388,22 +388,38 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
     }
 }
 
-__global__ __launch_bounds__(256) void sum_parts_unrolled_kernel(const float* __restrict__ part,
-                                                                 int parts, int64_t len,
-                                                                 float* __restrict__ out) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= len) return;
+// out[i] = sum over the blocks' partials part[p][i], in a fixed order: the
+// parts are split into 8 consecutive groups, each summed in part order by
+// one thread (16 loads in flight), and the 8 group sums are added in group
+// order.  A block covers 32 outputs.
+__global__ __launch_bounds__(256) void sum_parts_grouped_kernel(const float* __restrict__ part,
+                                                                int parts, int64_t len,
+                                                                float* __restrict__ out) {
+  __shared__ float gs[8][33];
+  const int c = threadIdx.x & 31, g = threadIdx.x >> 5;
+  const int64_t i = (int64_t)blockIdx.x * 32 + c;
+  const int per = (parts + 7) / 8;
+  const int p0 = g * per, p1 = min(parts, p0 + per);
   float s = 0.f;
-  int p = 0;
-  for (; p + 8 <= parts; p += 8) {
-    float v[8];
+  if (i < len) {
+    int p = p0;
+    for (; p + 16 <= p1; p += 16) {
+      float v[16];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v[q] = part[(int64_t)(p + q) * len + i];
+      for (int q = 0; q < 16; ++q) v[q] = part[(int64_t)(p + q) * len + i];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) s += v[q];
+      for (int q = 0; q < 16; ++q) s += v[q];
+    }
+    for (; p < p1; ++p) s += part[(int64_t)p * len + i];
   }
-  for (; p < parts; ++p) s += part[(int64_t)p * len + i];
-  out[i] = s;
+  gs[g][c] = s;
+  __syncthreads();
+  if (g == 0 && i < len) {
+    float t = gs[0][c];
+#pragma unroll
+    for (int q = 1; q < 8; ++q) t += gs[q][c];
+    out[i] = t;
+  }
 }
 
 constexpr int FM_MFMA_BLOCKS = 256;
@@ -446,7 +462,7 @@ static hipError_t fm_mfma_launch(bool fwd, const void* X, const void* W, int B, 
     LAT_LAUNCH_CHECK();
   }
   const int64_t len = (int64_t)n * K;
-  sum_parts_unrolled_kernel<<<cdiv(len, 256), 256, 0, s>>>(part, B > 0 ? bblocks : 0, len, dW);
+  sum_parts_grouped_kernel<<<cdiv(len, 32), 256, 0, s>>>(part, B > 0 ? bblocks : 0, len, dW);
   LAT_LAUNCH_CHECK();
   return hipSuccess;
 }

@@ -429,6 +429,23 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   }
 }
 
+// Sum of the splits' partials in split order; the loads of 16 splits are
+// issued before their adds (a split's partial is a separate [M, N] slice, so
+// a plain loop would wait for one load at a time).
+__device__ inline float sum_splits(const float* __restrict__ p, int splits, int64_t stride) {
+  float s = 0.f;
+  int z = 0;
+  for (; z + 16 <= splits; z += 16) {
+    float v[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) v[q] = p[(int64_t)(z + q) * stride];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) s += v[q];
+  }
+  for (; z < splits; ++z) s += p[(int64_t)z * stride];
+  return s;
+}
+
 template <typename CT>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial,
                                                             int splits, int M, int N,
@@ -436,16 +453,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
                                                             Epi epi, const float* __restrict__ rs_partial,
                                                             float* __restrict__ rowsum) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (rowsum && i < M) {
-    float r = 0.f;
-    for (int z = 0; z < splits; ++z) r += rs_partial[(int64_t)z * M + i];
-    rowsum[i] = r;
-  }
+  if (rowsum && i < M) rowsum[i] = sum_splits(rs_partial + i, splits, M);
   if (i >= (int64_t)M * N) return;
   const int row = (int)(i / N), col = (int)(i % N);
-  float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += partial[(int64_t)z * M * N + i];
-  epi_store<CT>(C, ldc, row, col, s, epi, 0);
+  epi_store<CT>(C, ldc, row, col, sum_splits(partial + i, splits, (int64_t)M * N), epi, 0);
 }
 
 // --- large products: block tile 256x256, 4 waves of 128x128 (4x4 fragments) ---
