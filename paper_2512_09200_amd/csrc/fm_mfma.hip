@@ -40,13 +40,16 @@ __device__ inline float group16_sum(float v) {
 template <int COLS>
 struct HeadRow {
   uint32_t v = 0;
-  __device__ inline void load(const bf16_t* __restrict__ g) {
-    if (threadIdx.x < COLS / 2) v = *reinterpret_cast<const uint32_t*>(g + 2 * threadIdx.x);
+  __device__ inline void load(const bf16_t* __restrict__ g, int tid = threadIdx.x) {
+    if (tid < COLS / 2) v = *reinterpret_cast<const uint32_t*>(g + 2 * tid);
   }
-  __device__ inline void store(float* dst) const {
-    if (threadIdx.x < COLS / 2) {
-      dst[2 * threadIdx.x] = __uint_as_float(v << 16);
-      dst[2 * threadIdx.x + 1] = __uint_as_float(v & 0xffff0000u);
+  __device__ inline void store_bf16(bf16_t* dst, int tid = threadIdx.x) const {
+    if (tid < COLS / 2) *reinterpret_cast<uint32_t*>(dst + 2 * tid) = v;
+  }
+  __device__ inline void store(float* dst, int tid = threadIdx.x) const {
+    if (tid < COLS / 2) {
+      dst[2 * tid] = __uint_as_float(v << 16);
+      dst[2 * tid + 1] = __uint_as_float(v & 0xffff0000u);
     }
   }
 };
@@ -388,6 +391,305 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
     }
 }
 
+// Backward for d = 128 with the products chained through registers.  Four
+// waves work on one sample, wave ta on the columns a in [32 ta, 32 ta + 32);
+// SPB samples per block iteration.  A wave computes its tiles of P^T (c x a),
+// dP^T (c x a) and dP (a x c) from the staged X^T, G^T and W^T, rounds them
+// to bf16 and uses them directly as MFMA operands: a result tile's lane
+// holds one column and, for rows 16 s .. 16 s + 15, the rows
+// 16 s + 4 h + {0..3} and 16 s + 8 + 4 h + {0..3} (h = lane / 32), which is
+// an operand fragment of the k step s with its k order permuted; the other
+// operand is read from LDS in the same order (two 8-byte reads).  So
+//   dX[j][a] += sum_c G[j][c] P^T[c][a] + W[j][c] dP^T[c][a]   (rows j of G, W)
+//   dW[j][c] += sum_{a in the wave's columns} X[j][a] dP[a][c]   (rows j of X)
+// need no LDS round trip for P, dP and dP^T, and an iteration has two
+// barriers.  dW accumulates in the waves' registers across the block's
+// samples; at the end the eight waves' partial tiles are added in wave order
+// through LDS into the block's partial.
+__device__ inline bf16x8 ld_perm(const bf16_t* p) {
+  const u32x2 lo = *reinterpret_cast<const u32x2*>(p);
+  const u32x2 hi = *reinterpret_cast<const u32x2*>(p + 8);
+  return __builtin_bit_cast(bf16x8, (u32x4{lo[0], lo[1], hi[0], hi[1]}));
+}
+
+// bf16 fragment of result rows 16 s .. 16 s + 15 (values r = 8 s .. 8 s + 7)
+__device__ inline bf16x8 frag_of(const f32x16& v, int s) {
+  return __builtin_bit_cast(
+      bf16x8, (u32x4{pack_bf2(v[8 * s], v[8 * s + 1]), pack_bf2(v[8 * s + 2], v[8 * s + 3]),
+                     pack_bf2(v[8 * s + 4], v[8 * s + 5]), pack_bf2(v[8 * s + 6], v[8 * s + 7])}));
+}
+
+// LDS of the chained kernel, one buffer: the staged operands during the
+// sample loop; afterwards the first bytes hold the dW reduction.
+// operand fragment with v (a bf16 value held as fp32) in the first k slot of
+// the lane's row and zeros elsewhere
+__device__ inline bf16x8 slot0(float v) {
+  const uint32_t lo = ((threadIdx.x & 63) >> 5) == 0 ? (uint32_t)f2bf(v) : 0u;
+  return __builtin_bit_cast(bf16x8, (u32x4{lo, 0u, 0u, 0u}));
+}
+
+// operand fragment of row 0 only: the row at p in the permuted k order for
+// lane 0 / 32 (rows 0 of the tile), zeros for the other rows
+__device__ inline bf16x8 row0(const bf16_t* p) {
+  return (threadIdx.x & 31) == 0 ? ld_perm(p) : __builtin_bit_cast(bf16x8, (u32x4{0u, 0u, 0u, 0u}));
+}
+
+template <int NP, int K, bool HEAD, int SPB>
+struct FmChainLds {
+  static constexpr int D = 128, NW = SPB * 4;
+  static constexpr int LT = NP + 8, LX = D + 4, LG = K + 4;
+  static constexpr size_t al(size_t b) { return (b + 15) / 16 * 16; }
+  // byte offsets
+  static constexpr size_t XT = 0;                                   // [SPB][D][LT]  X^T
+  static constexpr size_t XS = XT + al(2 * (size_t)SPB * D * LT);   // [SPB][NP][LX] X
+  static constexpr size_t GT = XS + al(2 * (size_t)SPB * NP * LX);  // [SPB][K][LT]  G^T
+  static constexpr size_t GS = GT + al(2 * (size_t)SPB * K * LT);   // [SPB][NP][LG] G
+  static constexpr size_t WT = GS + al(2 * (size_t)SPB * NP * LG);  // [K][LT]       W^T
+  static constexpr size_t WS = WT + al(2 * (size_t)K * LT);         // [NP][LG]      W
+  static constexpr size_t X0 = WS + al(2 * (size_t)NP * LG);        // [SPB][D] f32  head x0
+  static constexpr size_t G0 = X0 + al(4 * (size_t)SPB * D);        // [SPB][K] f32  head g0
+  static constexpr size_t W0 = G0 + al(4 * (size_t)SPB * K);        // [K] f32       head w0
+  static constexpr size_t G0B = W0 + al(4 * (size_t)K);             // [SPB][K + 8]  head g0, bf16
+  static constexpr size_t W0B = G0B + al(2 * (size_t)SPB * (K + 8)); // [K + 8]      head w0, bf16
+  static constexpr size_t stage_bytes = W0B + al(2 * (size_t)(K + 8));
+  static constexpr size_t red_bytes = 4 * ((size_t)NW * 16 * 64 + (size_t)NW * K);
+  static constexpr size_t bytes = stage_bytes > red_bytes ? stage_bytes : red_bytes;
+};
+
+template <int NP, int K, bool HEAD, int SPB>
+__global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int B, int n,
+    const bf16_t* __restrict__ dout, int64_t dstride, int emit0, const float* __restrict__ addend,
+    bf16_t* __restrict__ dX, float* __restrict__ dX_f32, float* __restrict__ dw_part) {
+  constexpr int D = 128, THREADS = SPB * 256, NW = THREADS / 64;
+  constexpr int NJ = NP / 32, NC = K / 32;
+  using L = FmChainLds<NP, K, HEAD, SPB>;
+  constexpr int LT = L::LT, LX = L::LX, LG = L::LG;
+  constexpr int H = HEAD ? 1 : 0;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[L::bytes];
+  auto XT = [&](int qq) { return reinterpret_cast<bf16_t*>(smem + L::XT) + (size_t)qq * D * LT; };
+  auto Xs = [&](int qq) { return reinterpret_cast<bf16_t*>(smem + L::XS) + (size_t)qq * NP * LX; };
+  auto GT = [&](int qq) { return reinterpret_cast<bf16_t*>(smem + L::GT) + (size_t)qq * K * LT; };
+  auto Gs = [&](int qq) { return reinterpret_cast<bf16_t*>(smem + L::GS) + (size_t)qq * NP * LG; };
+  bf16_t* WT = reinterpret_cast<bf16_t*>(smem + L::WT);
+  bf16_t* Ws = reinterpret_cast<bf16_t*>(smem + L::WS);
+  auto X0 = [&](int qq) { return reinterpret_cast<float*>(smem + L::X0) + qq * D; };
+  auto G0 = [&](int qq) { return reinterpret_cast<float*>(smem + L::G0) + qq * K; };
+  float* W0 = reinterpret_cast<float*>(smem + L::W0);
+  auto G0b = [&](int qq) { return reinterpret_cast<bf16_t*>(smem + L::G0B) + qq * (K + 8); };
+  bf16_t* W0b = reinterpret_cast<bf16_t*>(smem + L::W0B);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int q = w >> 2, ta = w & 3;  // this wave's sample and column block
+  const int h = lane >> 5, l32 = lane & 31;
+  const int nm = n - H;
+  {
+    Stager<NP, K, THREADS> sw;
+    sw.load(W + H * K, K, nm);
+    sw.store(Ws, LG, WT, LT);
+    if (HEAD)
+      for (int c = threadIdx.x; c < K; c += THREADS) {
+        W0[c] = bf2f(W[c]);
+        W0b[c] = W[c];
+      }
+  }
+  f32x16 dw[NJ][NC];
+#pragma unroll
+  for (int tj = 0; tj < NJ; ++tj)
+#pragma unroll
+    for (int tc = 0; tc < NC; ++tc) zero16(dw[tj][tc]);
+  float dw0[NC];
+#pragma unroll
+  for (int tc = 0; tc < NC; ++tc) dw0[tc] = 0.f;
+  const int off = emit0 ? D : 0;
+  Stager<NP, D, THREADS> sx[SPB];
+  Stager<NP, K, THREADS> sg[SPB];
+  HeadRow<D> hx[SPB];
+  HeadRow<K> hg[SPB];
+  auto prefetch = [&](int b0) {
+#pragma unroll
+    for (int qq = 0; qq < SPB; ++qq) {
+      const int bb = b0 + qq;
+      if (bb >= B) break;
+      const bf16_t* xb = X + (int64_t)bb * n * D;
+      const bf16_t* gb = dout + (int64_t)bb * dstride + off;
+      sx[qq].load(xb + H * D, D, nm);
+      sg[qq].load(gb + H * K, K, nm);
+      if (HEAD) {
+        hx[qq].load(xb);
+        hg[qq].load(gb);
+      }
+    }
+  };
+  const int step = gridDim.x * SPB;
+  if (blockIdx.x * SPB < B) prefetch(blockIdx.x * SPB);
+  for (int b0 = blockIdx.x * SPB; b0 < B; b0 += step) {
+    const int ns = B - b0 < SPB ? B - b0 : SPB;
+#pragma unroll
+    for (int qq = 0; qq < SPB; ++qq) {
+      if (qq >= ns) break;
+      sx[qq].store(Xs(qq), LX, XT(qq), LT);
+      sg[qq].store(Gs(qq), LG, GT(qq), LT);
+      if (HEAD) {
+        hx[qq].store(X0(qq));
+        hg[qq].store(G0(qq));
+        hg[qq].store_bf16(G0b(qq));
+      }
+    }
+    __syncthreads();
+    // the slot-0 gradient of this lane's column is read before the next
+    // samples' loads are issued: a wait for it then does not wait for them
+    // (an address inside dout whatever emit0 and ns are; used only with emit0)
+    const bf16_t g0raw = dout[(int64_t)(q < ns ? b0 + q : B - 1) * dstride + (emit0 ? ta * 32 + l32 : 0)];
+    if (b0 + step < B) prefetch(b0 + step);
+    if (q < ns) {
+      const int b = b0 + q;
+      const int64_t sbase = (int64_t)b * n * D;
+      const int a = ta * 32 + l32;  // this lane's column of dX
+      const bf16_t* xt_a = XT(q) + ta * 32 * LT;
+      f32x16 ax[NJ];
+#pragma unroll
+      for (int tj = 0; tj < NJ; ++tj) zero16(ax[tj]);
+      const float x0a = HEAD ? X0(q)[a] : 0.f;
+      // One product at a time (its tile, then its bf16 fragments -- the
+      // rounding of P and dP -- then the MFMAs that take them), and dX
+      // finished before dP is formed, so few tiles are live at once.  The head row's rank-1 terms are one more
+      // MFMA per product whose operands hold x0[a], w0[c] or g0[c] in their
+      // first k slot (zero elsewhere), and its dX row is a tile whose A
+      // operand is zero except row 0 (g0 or w0).
+      f32x16 axh;
+      zero16(axh);
+#pragma unroll
+      for (int tc = 0; tc < NC; ++tc) {
+        const float w0c = HEAD ? W0[tc * 32 + l32] : 0.f, g0c = HEAD ? G0(q)[tc * 32 + l32] : 0.f;
+        // P^T [c][a] (+ w0[c] x0[a]) -> dX += G P^T
+        {
+          f32x16 t;
+          zero16(t);
+          mfma_tile<NP>(t, WT + tc * 32 * LT, LT, xt_a, LT);
+          if (HEAD) t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(slot0(w0c), slot0(x0a), t, 0, 0, 0);
+#pragma unroll
+          for (int s = 0; s < 2; ++s) {
+            const bf16x8 f = frag_of(t, s);
+            const int kc = tc * 32 + 16 * s + 4 * h;
+#pragma unroll
+            for (int tj = 0; tj < NJ; ++tj)
+              ax[tj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_perm(Gs(q) + (tj * 32 + l32) * LG + kc),
+                                                               f, ax[tj], 0, 0, 0);
+            if (HEAD)
+              axh = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row0(G0b(q) + kc), f, axh, 0, 0, 0);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // dP^T [c][a] (+ g0[c] x0[a]) -> dX += W dP^T
+        {
+          f32x16 t;
+          zero16(t);
+          mfma_tile<NP>(t, GT(q) + tc * 32 * LT, LT, xt_a, LT);
+          if (HEAD) t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(slot0(g0c), slot0(x0a), t, 0, 0, 0);
+#pragma unroll
+          for (int s = 0; s < 2; ++s) {
+            const bf16x8 f = frag_of(t, s);
+            const int kc = tc * 32 + 16 * s + 4 * h;
+#pragma unroll
+            for (int tj = 0; tj < NJ; ++tj)
+              ax[tj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_perm(Ws + (tj * 32 + l32) * LG + kc),
+                                                               f, ax[tj], 0, 0, 0);
+            if (HEAD) axh = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row0(W0b + kc), f, axh, 0, 0, 0);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      float hx0 = axh[0];  // dX[0][a] in the lanes with h == 0
+      // dX rows (+ addend, + slot-0 gradient on row 0 when it is in the tiles)
+      {
+        const float g0v = emit0 ? bf2f(g0raw) : 0.f;
+        const float g0 = HEAD ? 0.f : g0v;
+#pragma unroll
+        for (int tj = 0; tj < NJ; ++tj)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int j = tj * 32 + frag_row(r);
+            if (j < nm) {
+              float v = ax[tj][r];
+              const int e = (j + H) * D + a;
+              if (addend) v += addend[sbase + e];
+              if (!HEAD && j == 0) v += g0;
+              if (dX_f32) dX_f32[sbase + e] = v;
+              else dX[sbase + e] = f2bf(v);
+            }
+          }
+        if (HEAD) {
+          if (h == 0) {
+            if (addend) hx0 += addend[sbase + a];
+            hx0 += g0v;
+            if (dX_f32) dX_f32[sbase + a] = hx0;
+            else dX[sbase + a] = f2bf(hx0);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      // dP [a][c] (+ x0[a] g0[c]) -> dW += X dP
+#pragma unroll
+      for (int tc = 0; tc < NC; ++tc) {
+        const float g0c = HEAD ? G0(q)[tc * 32 + l32] : 0.f;
+        f32x16 t;
+        zero16(t);
+        mfma_tile<NP>(t, xt_a, LT, GT(q) + tc * 32 * LT, LT);
+        if (HEAD) t = __builtin_amdgcn_mfma_f32_32x32x16_bf16(slot0(x0a), slot0(g0c), t, 0, 0, 0);
+        float d0 = 0.f;  // with the bf16-rounded dP (the operand the fragments carry)
+        if (HEAD)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) d0 += X0(q)[ta * 32 + frag_row(r)] * bf2f(f2bf(t[r]));
+        if (HEAD) {
+          d0 += __shfl_xor(d0, 32, 64);
+          dw0[tc] += d0;
+        }
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          const bf16x8 f = frag_of(t, s);
+          const int ka = ta * 32 + 16 * s + 4 * h;
+#pragma unroll
+          for (int tj = 0; tj < NJ; ++tj)
+            dw[tj][tc] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                ld_perm(Xs(q) + (tj * 32 + l32) * LX + ka), f, dw[tj][tc], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();  // the LDS is restaged for the next samples
+  }
+  // block partial of dW: the waves' tiles added in wave order
+  float* red = reinterpret_cast<float*>(smem);  // [NW][16][64], then [NW][K]
+  float* red0 = red + NW * 16 * 64;
+#pragma unroll
+  for (int tj = 0; tj < NJ; ++tj)
+#pragma unroll
+    for (int tc = 0; tc < NC; ++tc) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) red[(w * 16 + r) * 64 + lane] = dw[tj][tc][r];
+      __syncthreads();
+      for (int e = threadIdx.x; e < 16 * 64; e += THREADS) {
+        float v = red[e];
+        for (int ww = 1; ww < NW; ++ww) v += red[ww * 16 * 64 + e];
+        const int r = e >> 6, ln = e & 63;
+        const int j = tj * 32 + 8 * (r >> 2) + 4 * (ln >> 5) + (r & 3);
+        const int c = tc * 32 + (ln & 31);
+        if (j < nm) dw_part[((int64_t)blockIdx.x * n + j + H) * K + c] = v;
+      }
+      __syncthreads();
+    }
+  if (HEAD) {
+    if (h == 0)
+#pragma unroll
+      for (int tc = 0; tc < NC; ++tc) red0[w * K + tc * 32 + l32] = dw0[tc];
+    __syncthreads();
+    for (int c = threadIdx.x; c < K; c += THREADS) {
+      float v = red0[c];
+      for (int ww = 1; ww < NW; ++ww) v += red0[ww * K + c];
+      dw_part[(int64_t)blockIdx.x * n * K + c] = v;
+    }
+  }
+}
+
 // out[i] = sum over the blocks' partials part[p][i], in a fixed order: the
 // parts are split into 8 consecutive groups, each summed in part order by
 // one thread (16 loads in flight), and the 8 group sums are added in group
@@ -451,15 +753,33 @@ static hipError_t fm_mfma_launch(bool fwd, const void* X, const void* W, int B, 
     return hipSuccess;
   }
   float* part = (float*)ws;
-  // two samples per block iteration when both fit in LDS
-  constexpr int SPB = FmBwdLds<NP, D, K, HEAD, 2>::bytes <= 160 * 1024 ? 2 : 1;
-  const int bblocks = (B + SPB - 1) / SPB < FM_MFMA_BLOCKS ? ((B + SPB - 1) / SPB > 0 ? (B + SPB - 1) / SPB : 1)
-                                                           : FM_MFMA_BLOCKS;
-  if (B > 0) {
-    fm_bwd_mfma_kernel<NP, D, K, HEAD, SPB><<<bblocks, 512, 0, s>>>(
-        (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
-        (bf16_t*)dX, dX_f32, part);
-    LAT_LAUNCH_CHECK();
+  int bblocks = 0;
+  // the chained kernel where its registers fit (up to 64 rows in tiles; not
+  // rank 64 with a head row)
+  constexpr bool CHAIN = D == 128 && NP <= 64 && !(K == 64 && HEAD);
+  if constexpr (CHAIN) {
+    // two samples per block iteration (8 waves)
+    constexpr int SPB = 2;
+    static_assert(FmChainLds<NP, K, HEAD, SPB>::bytes <= 160 * 1024, "FM chain LDS");
+    const int iters = (B + SPB - 1) / SPB;
+    bblocks = iters < FM_MFMA_BLOCKS ? (iters > 0 ? iters : 1) : FM_MFMA_BLOCKS;
+    if (B > 0) {
+      fm_bwd_chain_kernel<NP, K, HEAD, SPB><<<bblocks, SPB * 256, 0, s>>>(
+          (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
+          (bf16_t*)dX, dX_f32, part);
+      LAT_LAUNCH_CHECK();
+    }
+  } else {
+    // two samples per block iteration when both fit in LDS
+    constexpr int SPB = FmBwdLds<NP, D, K, HEAD, 2>::bytes <= 160 * 1024 ? 2 : 1;
+    bblocks = (B + SPB - 1) / SPB < FM_MFMA_BLOCKS ? ((B + SPB - 1) / SPB > 0 ? (B + SPB - 1) / SPB : 1)
+                                                   : FM_MFMA_BLOCKS;
+    if (B > 0) {
+      fm_bwd_mfma_kernel<NP, D, K, HEAD, SPB><<<bblocks, 512, 0, s>>>(
+          (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
+          (bf16_t*)dX, dX_f32, part);
+      LAT_LAUNCH_CHECK();
+    }
   }
   const int64_t len = (int64_t)n * K;
   sum_parts_grouped_kernel<<<cdiv(len, 32), 256, 0, s>>>(part, B > 0 ? bblocks : 0, len, dW);

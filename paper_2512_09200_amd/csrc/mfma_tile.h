@@ -40,7 +40,23 @@ struct Stager {
   static constexpr int ITEMS = (RP / 8) * (COLS / 2);
   static constexpr int PER = (ITEMS + THREADS - 1) / THREADS;
   uint32_t v[PER][8];
+  // When every row is present the loads carry no per-row select: a load
+  // whose value is selected at once is waited for where it is issued, which
+  // would serialise the prefetch.
   __device__ inline void load(const bf16_t* __restrict__ g, int64_t gld, int nrows) {
+    if (nrows >= RP) {
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int it = threadIdx.x + q * THREADS;
+        if (ITEMS % THREADS == 0 || it < ITEMS) {
+          const int j0 = (it / (COLS / 2)) * 8, c = (it % (COLS / 2)) * 2;
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            v[q][i] = *reinterpret_cast<const uint32_t*>(g + (int64_t)(j0 + i) * gld + c);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
       const int it = threadIdx.x + q * THREADS;

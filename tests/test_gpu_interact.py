@@ -30,6 +30,11 @@ CASES = {
     "fm-bf16-n97-d128-k32-head": ("fm", "bf16", 600, 97, 128, 32, True, False),
     "fm-bf16-n65-d128-k64-head": ("fm", "bf16", 50, 65, 128, 64, True, False),
     "fm-bf16-n64-d128-k32": ("fm", "bf16", 60, 64, 128, 32, True, False),
+    # d = 128 register-chained backward: an odd batch (last iteration one
+    # sample), head and no head, rank 32 and 64, slot-0 gradient or none
+    "fm-bf16-n33-d128-k32-head-odd": ("fm", "bf16", 37, 33, 128, 32, True, False),
+    "fm-bf16-n64-d128-k64": ("fm", "bf16", 45, 64, 128, 64, False, False),
+    "fm-bf16-n40-d128-k32": ("fm", "bf16", 515, 40, 128, 32, False, False),
     "fm-bf16-valu": ("fm", "bf16", 33, 10, 32, 16, False, False),       # VALU path (d=32)
     "fm-f32-small": ("fm", "f32", 50, 10, 32, 16, False, False),
 }
