@@ -43,7 +43,7 @@ __global__ __launch_bounds__(DOT_THREADS) void dot_fwd_mfma_kernel(const bf16_t*
   Stager<NP, D, DOT_THREADS> sx;
   if (blockIdx.x < B) sx.load(X + (int64_t)blockIdx.x * n * D, D, n);
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
-    sx.store(Xs, LX, nullptr, 0);
+    sx.store(Xs, LX, nullptr, 0, n);
     __syncthreads();
     if (b + (int)gridDim.x < B) sx.load(X + (int64_t)(b + gridDim.x) * n * D, D, n);
     for (int t = w; t < ZT; t += DOT_THREADS / 64) {
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(DOT_THREADS, 2) void dot_bwd_mfma_kernel(
       const int m = threadIdx.x + q * DOT_THREADS;
       gv[q] = m < P ? gb[m] : 0u;
     }
-    sx.store(nullptr, 0, XT, LT);
+    sx.store(nullptr, 0, XT, LT, n);
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const int m = threadIdx.x + q * DOT_THREADS;

@@ -40,8 +40,9 @@ __device__ inline float group16_sum(float v) {
 template <int COLS>
 struct HeadRow {
   uint32_t v = 0;
+  // straight-line (threads past the row re-read its first pair)
   __device__ inline void load(const bf16_t* __restrict__ g, int tid = threadIdx.x) {
-    if (tid < COLS / 2) v = *reinterpret_cast<const uint32_t*>(g + 2 * tid);
+    v = *reinterpret_cast<const uint32_t*>(g + 2 * (tid < COLS / 2 ? tid : 0));
   }
   __device__ inline void store_bf16(bf16_t* dst, int tid = threadIdx.x) const {
     if (tid < COLS / 2) *reinterpret_cast<uint32_t*>(dst + 2 * tid) = v;
@@ -72,7 +73,7 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
   {
     Stager<NP, K, 512> sw;
     sw.load(W + H * K, K, nm);
-    sw.store(WR, LR, WT, LT);
+    sw.store(WR, LR, WT, LT, nm);
     if (HEAD)
       for (int c = threadIdx.x; c < K; c += blockDim.x) W0[c] = bf2f(W[c]);
   }
@@ -85,7 +86,7 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
     if (HEAD) hx.load(xb);
   }
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
-    sx.store(Xs, LX, XT, LT);
+    sx.store(Xs, LX, XT, LT, nm);
     if (HEAD) hx.store(X0);
     __syncthreads();
     // the next sample's X is in flight while this one is computed
@@ -181,7 +182,7 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
   {
     Stager<NP, K, 512> sw;
     sw.load(W + H * K, K, nm);
-    for (int q = 0; q < SPB; ++q) sw.store(GW[q] + K, LG, q == 0 ? WT : nullptr, LT);
+    for (int q = 0; q < SPB; ++q) sw.store(GW[q] + K, LG, q == 0 ? WT : nullptr, LT, nm);
     if (HEAD)
       for (int c = threadIdx.x; c < K; c += blockDim.x)
         for (int q = 0; q < SPB; ++q) GW0[q][K + c] = bf2f(W[c]);
@@ -222,8 +223,8 @@ __global__ __launch_bounds__(512) void fm_bwd_mfma_kernel(
 #pragma unroll
     for (int q = 0; q < SPB; ++q) {
       if (q >= ns) break;
-      sx[q].store(Xs[q], LX, XT[q], LT);
-      sg[q].store(GW[q], LG, GT[q], LT);
+      sx[q].store(Xs[q], LX, XT[q], LT, nm);
+      sg[q].store(GW[q], LG, GT[q], LT, nm);
       if (HEAD) {
         hx[q].store(X0[q]);
         hg[q].store(GW0[q]);
@@ -451,7 +452,8 @@ struct FmChainLds {
   static constexpr size_t W0 = G0 + al(4 * (size_t)SPB * K);        // [K] f32       head w0
   static constexpr size_t G0B = W0 + al(4 * (size_t)K);             // [SPB][K + 8]  head g0, bf16
   static constexpr size_t W0B = G0B + al(2 * (size_t)SPB * (K + 8)); // [K + 8]      head w0, bf16
-  static constexpr size_t stage_bytes = W0B + al(2 * (size_t)(K + 8));
+  static constexpr size_t S0 = W0B + al(2 * (size_t)(K + 8));       // [SPB][D] f32  slot-0 gradient
+  static constexpr size_t stage_bytes = S0 + al(4 * (size_t)SPB * D);
   static constexpr size_t red_bytes = 4 * ((size_t)NW * 16 * 64 + (size_t)NW * K);
   static constexpr size_t bytes = stage_bytes > red_bytes ? stage_bytes : red_bytes;
 };
@@ -478,6 +480,7 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
   float* W0 = reinterpret_cast<float*>(smem + L::W0);
   auto G0b = [&](int qq) { return reinterpret_cast<bf16_t*>(smem + L::G0B) + qq * (K + 8); };
   bf16_t* W0b = reinterpret_cast<bf16_t*>(smem + L::W0B);
+  auto S0 = [&](int qq) { return reinterpret_cast<float*>(smem + L::S0) + qq * D; };
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int q = w >> 2, ta = w & 3;  // this wave's sample and column block
   const int h = lane >> 5, l32 = lane & 31;
@@ -485,7 +488,7 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
   {
     Stager<NP, K, THREADS> sw;
     sw.load(W + H * K, K, nm);
-    sw.store(Ws, LG, WT, LT);
+    sw.store(Ws, LG, WT, LT, nm);
     if (HEAD)
       for (int c = threadIdx.x; c < K; c += THREADS) {
         W0[c] = bf2f(W[c]);
@@ -505,11 +508,14 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
   Stager<NP, K, THREADS> sg[SPB];
   HeadRow<D> hx[SPB];
   HeadRow<K> hg[SPB];
+  HeadRow<D> hs[SPB];  // slot-0 gradient (emit0): staged like the operands, so
+                       // the compute reads no global memory
   auto prefetch = [&](int b0) {
 #pragma unroll
     for (int qq = 0; qq < SPB; ++qq) {
-      const int bb = b0 + qq;
-      if (bb >= B) break;
+      // a valid sample for every qq (stored only if b0 + qq < B): the loads
+      // are straight-line code
+      const int bb = b0 + qq < B ? b0 + qq : B - 1;
       const bf16_t* xb = X + (int64_t)bb * n * D;
       const bf16_t* gb = dout + (int64_t)bb * dstride + off;
       sx[qq].load(xb + H * D, D, nm);
@@ -518,6 +524,7 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
         hx[qq].load(xb);
         hg[qq].load(gb);
       }
+      if (emit0) hs[qq].load(dout + (int64_t)bb * dstride);
     }
   };
   const int step = gridDim.x * SPB;
@@ -527,19 +534,16 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
 #pragma unroll
     for (int qq = 0; qq < SPB; ++qq) {
       if (qq >= ns) break;
-      sx[qq].store(Xs(qq), LX, XT(qq), LT);
-      sg[qq].store(Gs(qq), LG, GT(qq), LT);
+      sx[qq].store(Xs(qq), LX, XT(qq), LT, nm);
+      sg[qq].store(Gs(qq), LG, GT(qq), LT, nm);
       if (HEAD) {
         hx[qq].store(X0(qq));
         hg[qq].store(G0(qq));
         hg[qq].store_bf16(G0b(qq));
       }
+      if (emit0) hs[qq].store(S0(qq));
     }
     __syncthreads();
-    // the slot-0 gradient of this lane's column is read before the next
-    // samples' loads are issued: a wait for it then does not wait for them
-    // (an address inside dout whatever emit0 and ns are; used only with emit0)
-    const bf16_t g0raw = dout[(int64_t)(q < ns ? b0 + q : B - 1) * dstride + (emit0 ? ta * 32 + l32 : 0)];
     if (b0 + step < B) prefetch(b0 + step);
     if (q < ns) {
       const int b = b0 + q;
@@ -602,7 +606,7 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
       float hx0 = axh[0];  // dX[0][a] in the lanes with h == 0
       // dX rows (+ addend, + slot-0 gradient on row 0 when it is in the tiles)
       {
-        const float g0v = emit0 ? bf2f(g0raw) : 0.f;
+        const float g0v = emit0 ? S0(q)[a] : 0.f;
         const float g0 = HEAD ? 0.f : g0v;
 #pragma unroll
         for (int tj = 0; tj < NJ; ++tj)

@@ -35,55 +35,48 @@ __device__ inline int frag_row(int r) { return 8 * (r >> 2) + 4 * ((threadIdx.x 
 // (group of 8 rows, pair of columns); RP = padded row count (multiple of 8).
 // load() fetches this thread's items into registers (so the next sample can
 // be in flight while the current one is computed), store() writes them.
+// load() is straight-line code: rows past nrows and items past the last
+// read a valid element (nrows >= 1) and store() writes zeros for them.  A
+// load inside a branch, or whose value is selected at once, makes the
+// compiler wait for it (and for every load issued before it) right there,
+// which would serialise the prefetch with the compute.
 template <int RP, int COLS, int THREADS>
 struct Stager {
   static constexpr int ITEMS = (RP / 8) * (COLS / 2);
   static constexpr int PER = (ITEMS + THREADS - 1) / THREADS;
   uint32_t v[PER][8];
-  // When every row is present the loads carry no per-row select: a load
-  // whose value is selected at once is waited for where it is issued, which
-  // would serialise the prefetch.
   __device__ inline void load(const bf16_t* __restrict__ g, int64_t gld, int nrows) {
-    if (nrows >= RP) {
-#pragma unroll
-      for (int q = 0; q < PER; ++q) {
-        const int it = threadIdx.x + q * THREADS;
-        if (ITEMS % THREADS == 0 || it < ITEMS) {
-          const int j0 = (it / (COLS / 2)) * 8, c = (it % (COLS / 2)) * 2;
-#pragma unroll
-          for (int i = 0; i < 8; ++i)
-            v[q][i] = *reinterpret_cast<const uint32_t*>(g + (int64_t)(j0 + i) * gld + c);
-        }
-      }
-      return;
-    }
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
-      const int it = threadIdx.x + q * THREADS;
-      if (it < ITEMS) {
-        const int j0 = (it / (COLS / 2)) * 8, c = (it % (COLS / 2)) * 2;
+      int it = threadIdx.x + q * THREADS;
+      it = it < ITEMS ? it : ITEMS - 1;
+      const int j0 = (it / (COLS / 2)) * 8, c = (it % (COLS / 2)) * 2;
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-          v[q][i] = (j0 + i < nrows) ? *reinterpret_cast<const uint32_t*>(g + (int64_t)(j0 + i) * gld + c) : 0u;
+      for (int i = 0; i < 8; ++i) {
+        const int row = j0 + i < nrows ? j0 + i : 0;
+        v[q][i] = *reinterpret_cast<const uint32_t*>(g + (int64_t)row * gld + c);
       }
     }
   }
-  // R or T may be null (that layout is not written)
-  __device__ inline void store(bf16_t* R, int ldr, bf16_t* T, int ldt) const {
+  // R or T may be null (that layout is not written); nrows as in load()
+  __device__ inline void store(bf16_t* R, int ldr, bf16_t* T, int ldt, int nrows) const {
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
       const int it = threadIdx.x + q * THREADS;
       if (it < ITEMS) {
         const int j0 = (it / (COLS / 2)) * 8, c = (it % (COLS / 2)) * 2;
+        uint32_t x[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = j0 + i < nrows ? v[q][i] : 0u;
         if (R)
 #pragma unroll
-          for (int i = 0; i < 8; ++i) *reinterpret_cast<uint32_t*>(R + (j0 + i) * ldr + c) = v[q][i];
+          for (int i = 0; i < 8; ++i) *reinterpret_cast<uint32_t*>(R + (j0 + i) * ldr + c) = x[i];
         if (!T) continue;
         u32x4 lo, hi;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          lo[i] = __builtin_amdgcn_perm(v[q][2 * i + 1], v[q][2 * i], 0x05040100u);
-          hi[i] = __builtin_amdgcn_perm(v[q][2 * i + 1], v[q][2 * i], 0x07060302u);
+          lo[i] = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], 0x05040100u);
+          hi[i] = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], 0x07060302u);
         }
         *reinterpret_cast<u32x4*>(T + c * ldt + j0) = lo;
         *reinterpret_cast<u32x4*>(T + (c + 1) * ldt + j0) = hi;
