@@ -133,35 +133,47 @@ __device__ inline int64_t koff(const Opnd& o, int k) {
 // --- operand tile loaders: fill S[rows][GLD] (k contiguous) for rows r0.., k k0.. ---
 // K-contiguous, 16-byte vectors: ROWS rows x 64 k = 8 vectors per row,
 // ROWS / 32 per thread.
+// The loads are straight-line code: an element outside the matrix reads
+// element (0, 0) instead (its address is selected, not its value) and
+// store() writes zeros for it.  A load inside a branch, or whose value is
+// selected at once, makes the compiler wait there for it and for every load
+// issued before it, which would cut the prefetch distance to one step.
 template <int ROWS = GBM, int THREADS = 256>
 struct LoadK {
   static constexpr int NV = ROWS * 8 / THREADS;
   u32x4 r[NV];
+  int R_, K_, r0_, k0_;
+  bool edge_;
   // edge: the tile may reach past R rows or K columns (uniform per block and step)
   __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool edge) {
+    R_ = R; K_ = K; r0_ = r0; k0_ = k0; edge_ = edge;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int v = threadIdx.x + i * THREADS;
       const int rr = v >> 3, kc = (v & 7) * 8;
       const int gr = r0 + rr, gk = k0 + kc;
-      if (!edge || (gr < R && gk < K)) {
-        r[i] = ldg16(o.p + (int64_t)gr * o.ld + koff<false>(o, gk));
-        // a vector reaching past K (rows padded to 8 elements): zero the tail
-        if (edge && gk + 8 > K) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (gk + e >= K) r[i][e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-        }
-      } else {
-        r[i] = u32x4{0, 0, 0, 0};
-      }
+      const bool ok = !edge || (gr < R && gk < K);
+      r[i] = ldg16(o.p + (ok ? (int64_t)gr * o.ld + koff<false>(o, gk) : 0));
     }
   }
   __device__ inline void store(bf16_t* S) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int v = threadIdx.x + i * THREADS;
-      *reinterpret_cast<u32x4*>(S + (v >> 3) * GLD + (v & 7) * 8) = r[i];
+      const int rr = v >> 3, kc = (v & 7) * 8;
+      u32x4 x = r[i];
+      if (edge_) {
+        const int gr = r0_ + rr, gk = k0_ + kc;
+        if (!(gr < R_ && gk < K_)) {
+          x = u32x4{0, 0, 0, 0};
+        } else if (gk + 8 > K_) {
+          // a vector reaching past K (rows padded to 8 elements): zero the tail
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (gk + e >= K_) x[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+        }
+      }
+      *reinterpret_cast<u32x4*>(S + rr * GLD + kc) = x;
     }
   }
 };
@@ -176,7 +188,10 @@ template <int ROWS = GBM, int THREADS = 256>
 struct LoadMN {
   static constexpr int NI = ROWS * 2 / THREADS;
   u32x4 r[NI][4];
+  int R_, K_, r0_, k0_;
+  bool edge_;
   __device__ inline void load(const Opnd& o, int R, int K, int r0, int k0, bool edge) {
+    R_ = R; K_ = K; r0_ = r0; k0_ = k0; edge_ = edge;
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
       const int it = threadIdx.x + q * THREADS;
@@ -184,8 +199,8 @@ struct LoadMN {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int gk = kb + i;
-        if (!edge || (gk < K && gr < R)) r[q][i] = ldg16(o.p + koff<true>(o, gk) + gr);
-        else r[q][i] = u32x4{0, 0, 0, 0};
+        const bool ok = !edge || (gk < K && gr < R);
+        r[q][i] = ldg16(o.p + (ok ? koff<true>(o, gk) + gr : 0));
       }
     }
   }
@@ -193,13 +208,22 @@ struct LoadMN {
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
       const int it = threadIdx.x + q * THREADS;
+      u32x4 x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[i] = r[q][i];
+        if (edge_) {
+          const int gr = r0_ + (it >> 4) * 8, gk = k0_ + (it & 15) * 4 + i;
+          if (!(gk < K_ && gr < R_)) x[i] = u32x4{0, 0, 0, 0};
+        }
+      }
       bf16_t* s = S + ((it >> 4) * 8) * GLD + (it & 15) * 4;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        // row j of the group: (k0, k1, k2, k3) = half (j & 1) of word j/2 of r[q][0..3]
+        // row j of the group: (k0, k1, k2, k3) = half (j & 1) of word j/2 of x[0..3]
         const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t lo = __builtin_amdgcn_perm(r[q][1][j >> 1], r[q][0][j >> 1], sel);
-        const uint32_t hi = __builtin_amdgcn_perm(r[q][3][j >> 1], r[q][2][j >> 1], sel);
+        const uint32_t lo = __builtin_amdgcn_perm(x[1][j >> 1], x[0][j >> 1], sel);
+        const uint32_t hi = __builtin_amdgcn_perm(x[3][j >> 1], x[2][j >> 1], sel);
         *reinterpret_cast<uint2*>(s + j * GLD) = uint2{lo, hi};
       }
     }
