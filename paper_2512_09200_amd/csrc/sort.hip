@@ -156,13 +156,19 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_hist_all_kernel(
     state[((int64_t)(i / radix) * tmax + tix) * radix + i % radix] = 0u;
   }
   __syncthreads();
+  // all of the thread's indices in flight together (positions past the
+  // tile's end read position 0 and are not counted)
+  uint32_t rv[SORT_ITEMS];
 #pragma unroll
   for (int i = 0; i < SORT_ITEMS; ++i) {
     const int k = i * SORT_THREADS + threadIdx.x;
-    if (k < t.cnt) {
-      const uint32_t r = (uint32_t)indices[t.base + k];
-      for (int p = 0; p < passes; ++p) atomicAdd(&hist[p][(r >> (p * dbits)) & (radix - 1)], 1);
-    }
+    rv[i] = (uint32_t)indices[t.base + (k < t.cnt ? k : 0)];
+  }
+#pragma unroll
+  for (int i = 0; i < SORT_ITEMS; ++i) {
+    const int k = i * SORT_THREADS + threadIdx.x;
+    if (k < t.cnt)
+      for (int p = 0; p < passes; ++p) atomicAdd(&hist[p][(rv[i] >> (p * dbits)) & (radix - 1)], 1);
   }
   __syncthreads();
   for (int i = threadIdx.x; i < passes * radix; i += SORT_THREADS) {
@@ -246,8 +252,12 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
     const int k = cbase + r * 64 + lane;
     const bool valid = k < t.cnt;
     if constexpr (FIRST) {
-      key[r] = valid ? keys_in[t.base + k] + key0 : 0;
-      val[r] = valid ? lvals[k] : 0;
+      // a lane past the tile's end reads position 0 (its key and value are
+      // never used): no select on the loaded value, so the loads of all
+      // rounds are in flight together
+      const int kk = valid ? k : 0;
+      key[r] = keys_in[t.base + kk] + key0;
+      val[r] = lvals[kk];
     } else {
       key[r] = valid ? keys_in[t.base + k] : 0;
       val[r] = valid ? vals_in[t.base + k] : 0;
