@@ -37,6 +37,12 @@ using namespace lat;
     hipError_t e__ = (expr);                          \
     if (e__ != hipSuccess) return LATTICE_ERR_HIP;    \
   } while (0)
+// inside helpers that return a hipError_t
+#define HIP_TRY(expr)                                 \
+  do {                                                \
+    hipError_t e__ = (expr);                          \
+    if (e__ != hipSuccess) return e__;                \
+  } while (0)
 
 static inline DType dt_of(lattice_dtype d) { return d == LATTICE_BF16 ? DT_BF16 : DT_F32; }
 static inline size_t esize(lattice_dtype d) { return d == LATTICE_BF16 ? 2 : 4; }
@@ -716,6 +722,9 @@ struct SideStream {
   // fork after the pooled lookups and after the interaction backward; join
   // after the sort and run bookkeeping and after the dense weight gradients
   hipEvent_t fork_fwd = nullptr, fork_bwd = nullptr, sorted = nullptr, done = nullptr;
+  // fork at the step's start and join of the bottom MLP's forward (which
+  // runs beside the pooled lookups)
+  hipEvent_t fork_start = nullptr, bottom_done = nullptr;
 };
 constexpr int kMaxDevices = 64;
 std::mutex g_side_mu;
@@ -733,7 +742,8 @@ lattice_status side_stream_of(hipStream_t main, SideStream** out) {
     if (hipGetDevice(&cur) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipGetDevice failed");
     if (cur != dev && hipSetDevice(dev) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipSetDevice failed");
     hipError_t e = hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking);
-    for (hipEvent_t* ev : {&ss.fork_fwd, &ss.fork_bwd, &ss.sorted, &ss.done})
+    for (hipEvent_t* ev : {&ss.fork_fwd, &ss.fork_bwd, &ss.sorted, &ss.done, &ss.fork_start,
+                           &ss.bottom_done})
       if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
     if (cur != dev) (void)hipSetDevice(cur);
     if (e != hipSuccess) {
@@ -810,6 +820,43 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                            stage_ev(LATTICE_STAGE_EMBBAG_SORT));
   };
 
+  std::unique_lock<std::mutex> lock(g_side_mu, std::defer_lock);
+  SideStream* side = nullptr;
+  if (!opts->single_stream) {
+    lock.lock();
+    st = side_stream_of(s, &side);
+    if (st != LATTICE_OK) return st;
+  }
+  // 2. bottom MLP -> slot 0 of X.  It needs only the dense input, so with the
+  // side stream it runs there beside the pooled lookups (latency-bound small
+  // GEMMs next to a bandwidth-bound gather); slot 0 of a row is its own
+  // cache lines, which the lookups do not write.
+  void* bacts[LATTICE_MAX_LAYERS];
+  int64_t bstr[LATTICE_MAX_LAYERS];
+  auto bottom_forward = [&](hipStream_t on) -> hipError_t {
+    if (ev && ev[2 * LATTICE_STAGE_BOTTOM_FWD])
+      HIP_TRY(hipEventRecord((hipEvent_t)ev[2 * LATTICE_STAGE_BOTTOM_FWD], on));
+    if (m->dense_in > 0) {
+      const int nb = m->bottom.n_layers;
+      for (int i = 0; i + 1 < nb; ++i) {
+        bacts[i] = at(L.bottom_act[i]);
+        bstr[i] = m->bottom.layers[i].out_dim;
+      }
+      bacts[nb - 1] = X;
+      bstr[nb - 1] = (int64_t)n * d;
+      HIP_TRY(mlp_forward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, on));
+    }
+    if (ev && ev[2 * LATTICE_STAGE_BOTTOM_FWD + 1])
+      HIP_TRY(hipEventRecord((hipEvent_t)ev[2 * LATTICE_STAGE_BOTTOM_FWD + 1], on));
+    return hipSuccess;
+  };
+  const bool bottom_on_side = side && m->dense_in > 0;
+  if (bottom_on_side) {
+    HIPRET(hipEventRecord(side->fork_start, s));
+    HIPRET(hipStreamWaitEvent(side->s, side->fork_start, 0));
+    HIPRET(bottom_forward(side->s));
+    HIPRET(hipEventRecord(side->bottom_done, side->s));
+  }
   // 1. pooled lookups -> embedding slots of X
   HIPRET(begin(LATTICE_STAGE_EMBBAG_FWD));
   HIPRET(embbag_fwd(m->tables.data, dt, d, m->tables.row_base, batch->bags.offsets,
@@ -818,32 +865,14 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   HIPRET(end(LATTICE_STAGE_EMBBAG_FWD));
   // fork: the sort and run bookkeeping go to the side stream, overlapping
   // the dense stages; the lock is held until the join is enqueued
-  std::unique_lock<std::mutex> lock(g_side_mu, std::defer_lock);
-  SideStream* side = nullptr;
-  if (!opts->single_stream) {
-    lock.lock();
-    st = side_stream_of(s, &side);
-    if (st != LATTICE_OK) return st;
+  if (side) {
     HIPRET(hipEventRecord(side->fork_fwd, s));
     HIPRET(hipStreamWaitEvent(side->s, side->fork_fwd, 0));
     HIPRET(sparse_sort(side->s));
     HIPRET(hipEventRecord(side->sorted, side->s));
   }
-  // 2. bottom MLP -> slot 0 of X
-  HIPRET(begin(LATTICE_STAGE_BOTTOM_FWD));
-  void* bacts[LATTICE_MAX_LAYERS];
-  int64_t bstr[LATTICE_MAX_LAYERS];
-  if (m->dense_in > 0) {
-    const int nb = m->bottom.n_layers;
-    for (int i = 0; i + 1 < nb; ++i) {
-      bacts[i] = at(L.bottom_act[i]);
-      bstr[i] = m->bottom.layers[i].out_dim;
-    }
-    bacts[nb - 1] = X;
-    bstr[nb - 1] = (int64_t)n * d;
-    HIPRET(mlp_forward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, s));
-  }
-  HIPRET(end(LATTICE_STAGE_BOTTOM_FWD));
+  if (bottom_on_side) HIPRET(hipStreamWaitEvent(s, side->bottom_done, 0));
+  else HIPRET(bottom_forward(s));
   // 3. interaction -> top input t = [X[:,0,:], interaction]
   HIPRET(begin(LATTICE_STAGE_INTERACT_FWD));
   HIPRET(interact_fwd_impl(&m->interact, B, X, t, P.t_stride, at(L.interact), s));
