@@ -453,12 +453,15 @@ struct FmChainLds {
   static constexpr size_t G0B = W0 + al(4 * (size_t)K);             // [SPB][K + 8]  head g0, bf16
   static constexpr size_t W0B = G0B + al(2 * (size_t)SPB * (K + 8)); // [K + 8]      head w0, bf16
   static constexpr size_t S0 = W0B + al(2 * (size_t)(K + 8));       // [SPB][D] f32  slot-0 gradient
-  static constexpr size_t stage_bytes = S0 + al(4 * (size_t)SPB * D);
+  static constexpr int LQ = 32 + 8;                                 // dX patch row stride
+  static constexpr size_t DQ = S0 + al(4 * (size_t)SPB * D);        // [NW][32][LQ]  per-wave dX patch
+  static constexpr size_t stage_bytes = DQ + al(2 * (size_t)NW * 32 * LQ);
   static constexpr size_t red_bytes = 4 * ((size_t)NW * 16 * 64 + (size_t)NW * K);
   static constexpr size_t bytes = stage_bytes > red_bytes ? stage_bytes : red_bytes;
 };
 
-template <int NP, int K, bool HEAD, int SPB>
+// PLAIN: a bf16 dX (16-byte aligned), no addend, no fp32 copy
+template <int NP, int K, bool HEAD, int SPB, bool PLAIN>
 __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int B, int n,
     const bf16_t* __restrict__ dout, int64_t dstride, int emit0, const float* __restrict__ addend,
@@ -481,6 +484,11 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
   auto G0b = [&](int qq) { return reinterpret_cast<bf16_t*>(smem + L::G0B) + qq * (K + 8); };
   bf16_t* W0b = reinterpret_cast<bf16_t*>(smem + L::W0B);
   auto S0 = [&](int qq) { return reinterpret_cast<float*>(smem + L::S0) + qq * D; };
+  constexpr int LQ = L::LQ;
+  // this wave's 32 x 32 patch for transposing dX tiles to row segments
+  bf16_t* dq = reinterpret_cast<bf16_t*>(smem + L::DQ) + (threadIdx.x >> 6) * 32 * LQ;
+  // PLAIN: tiles leave as 16-byte row segments through the patch instead of
+  // 2-byte column stores
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int q = w >> 2, ta = w & 3;  // this wave's sample and column block
   const int h = lane >> 5, l32 = lane & 31;
@@ -609,24 +617,49 @@ __global__ __launch_bounds__(SPB * 256) void fm_bwd_chain_kernel(
         const float g0v = emit0 ? S0(q)[a] : 0.f;
         const float g0 = HEAD ? 0.f : g0v;
 #pragma unroll
-        for (int tj = 0; tj < NJ; ++tj)
+        for (int tj = 0; tj < NJ; ++tj) {
+          if constexpr (PLAIN) {
+            // tile -> patch (row frag_row(r), column l32), then lane l writes
+            // row l / 4 (+ 16) columns 8 (l % 4) .. + 7 of the tile
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int j = tj * 32 + frag_row(r);
-            if (j < nm) {
-              float v = ax[tj][r];
-              const int e = (j + H) * D + a;
-              if (addend) v += addend[sbase + e];
-              if (!HEAD && j == 0) v += g0;
-              if (dX_f32) dX_f32[sbase + e] = v;
-              else dX[sbase + e] = f2bf(v);
+            for (int r = 0; r < 16; ++r) {
+              const int jl = frag_row(r);
+              const float v = (!HEAD && tj == 0 && jl == 0) ? ax[tj][r] + g0 : ax[tj][r];
+              dq[jl * LQ + l32] = f2bf(v);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+              const int jl = half * 16 + (lane >> 2), c8 = (lane & 3) * 8;
+              const int j = tj * 32 + jl;
+              const u32x4 v = *reinterpret_cast<const u32x4*>(dq + jl * LQ + c8);
+              if (j < nm) stg16(dX + sbase + (int64_t)(j + H) * D + ta * 32 + c8, v);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          } else {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int j = tj * 32 + frag_row(r);
+              if (j < nm) {
+                float v = ax[tj][r];
+                const int e = (j + H) * D + a;
+                if (addend) v += addend[sbase + e];
+                if (!HEAD && j == 0) v += g0;
+                if (dX_f32) dX_f32[sbase + e] = v;
+                else dX[sbase + e] = f2bf(v);
+              }
             }
           }
+        }
         if (HEAD) {
           if (h == 0) {
-            if (addend) hx0 += addend[sbase + a];
+            if (!PLAIN && addend) hx0 += addend[sbase + a];
             hx0 += g0v;
-            if (dX_f32) dX_f32[sbase + a] = hx0;
+            if (!PLAIN && dX_f32) dX_f32[sbase + a] = hx0;
             else dX[sbase + a] = f2bf(hx0);
           }
         }
@@ -768,9 +801,14 @@ static hipError_t fm_mfma_launch(bool fwd, const void* X, const void* W, int B, 
     const int iters = (B + SPB - 1) / SPB;
     bblocks = iters < FM_MFMA_BLOCKS ? (iters > 0 ? iters : 1) : FM_MFMA_BLOCKS;
     if (B > 0) {
-      fm_bwd_chain_kernel<NP, K, HEAD, SPB><<<bblocks, SPB * 256, 0, s>>>(
-          (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
-          (bf16_t*)dX, dX_f32, part);
+      if (!addend && !dX_f32 && (reinterpret_cast<uintptr_t>(dX) & 15) == 0)
+        fm_bwd_chain_kernel<NP, K, HEAD, SPB, true><<<bblocks, SPB * 256, 0, s>>>(
+            (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
+            (bf16_t*)dX, dX_f32, part);
+      else
+        fm_bwd_chain_kernel<NP, K, HEAD, SPB, false><<<bblocks, SPB * 256, 0, s>>>(
+            (const bf16_t*)X, (const bf16_t*)W, B, n, (const bf16_t*)dout, dstride, emit0, addend,
+            (bf16_t*)dX, dX_f32, part);
       LAT_LAUNCH_CHECK();
     }
   } else {
