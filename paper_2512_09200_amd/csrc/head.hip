@@ -16,7 +16,9 @@
 //   its bf16 operand copy; then the layer's input gradient
 //   g = (dz_bf16 W) ⊙ [mask > 0] (mask: the layer's input, i.e. the previous
 //   layer's ReLU output, or none) in bf16, one MFMA per 32 x 32 tile and 16
-//   heads, the dz fragments built in registers in the operand layout.
+//   heads, the dz fragments built in registers in the operand layout; the
+//   mask is read and the gradient written as 16-byte row segments through a
+//   per-wave LDS patch (not as 2-byte columns of the MFMA layout).
 #include "common.h"
 #include "kernels.h"
 #include "mfma_tile.h"
@@ -132,6 +134,15 @@ __global__ __launch_bounds__(HEAD_THREADS) void head_fwd_kernel(
   }
 }
 
+constexpr int HEAD_LQ = 32 + 8;  // patch row stride (bf16)
+
+// LDS writes of this wave visible to its reads (the patch is wave-private)
+__device__ inline void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // TS: 16-wide steps of heads (T <= 16 TS)
 template <int TS>
 __global__ __launch_bounds__(HEAD_THREADS) void head_bwd_kernel(
@@ -144,6 +155,8 @@ __global__ __launch_bounds__(HEAD_THREADS) void head_bwd_kernel(
   const int r0 = blockIdx.x * HEAD_ROWS;
   const int row = r0 + (lane & 31);
   const int tofs = (lane >> 5) * 8;
+  __shared__ __attribute__((aligned(16))) bf16_t patch[HEAD_WAVES][32 * HEAD_LQ];
+  bf16_t* pq = patch[w];  // this wave's 32 x 32 transposition patch
   // loss operands of this lane's dz fragment (row, heads ts*16 + tofs + j)
   float zv[TS][8], yv[TS][8];
   uint8_t mv[TS][8];
@@ -163,11 +176,14 @@ __global__ __launch_bounds__(HEAD_THREADS) void head_bwd_kernel(
   constexpr int HEAD_KPW = head_kpw<TS>();
   const int ktiles = (K + 31) / 32;
   uint32_t bw[HEAD_KPW][TS][4];
-  bf16_t mk[HEAD_KPW][16];
+  // mask rows of each tile as 16-byte segments: lane l holds row
+  // half * 16 + l / 4, columns 8 (l % 4) .. + 7 (no mask: all positive)
+  u32x4 mk[HEAD_KPW][2];
   auto load_chunk = [&](int c0) {
 #pragma unroll
     for (int i = 0; i < HEAD_KPW; ++i) {
-      const int k = (c0 + w + i * HEAD_WAVES) * 32 + (lane & 31);
+      const int kb = (c0 + w + i * HEAD_WAVES) * 32;
+      const int k = kb + (lane & 31);
 #pragma unroll
       for (int ts = 0; ts < TS; ++ts)
 #pragma unroll
@@ -178,9 +194,12 @@ __global__ __launch_bounds__(HEAD_THREADS) void head_bwd_kernel(
           bw[i][ts][j / 2] = b0 | (b1 << 16);
         }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int rr = r0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        mk[i][r] = (mask && rr < B && k < K) ? mask[(int64_t)rr * ldm + k] : (bf16_t)0x3f80;
+      for (int half = 0; half < 2; ++half) {
+        const int rr = r0 + half * 16 + (lane >> 2), c8 = kb + (lane & 3) * 8;
+        const bool ok = mask && rr < B && c8 < K;
+        // (an address inside the mask whatever ok is; the value is used only if ok)
+        const u32x4 v = mask ? ldg16(mask + (ok ? (int64_t)rr * ldm + c8 : 0)) : u32x4{0u, 0u, 0u, 0u};
+        mk[i][half] = ok ? v : u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
       }
     }
   };
@@ -238,22 +257,40 @@ __global__ __launch_bounds__(HEAD_THREADS) void head_bwd_kernel(
             __builtin_bit_cast(bf16x8, (u32x4{bw[i][ts][0], bw[i][ts][1], bw[i][ts][2], bw[i][ts][3]})),
             acc[i], 0, 0, 0);
     }
-    bf16_t mc[HEAD_KPW][16];
+    u32x4 mc[HEAD_KPW][2];
 #pragma unroll
-    for (int i = 0; i < HEAD_KPW; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mc[i][r] = mk[i][r];
+    for (int i = 0; i < HEAD_KPW; ++i) {
+      mc[i][0] = mk[i][0];
+      mc[i][1] = mk[i][1];
+    }
     if (c0 + HEAD_WAVES * HEAD_KPW < ktiles) load_chunk(c0 + HEAD_WAVES * HEAD_KPW);
 #pragma unroll
     for (int i = 0; i < HEAD_KPW; ++i) {
-      const int k = (c0 + w + i * HEAD_WAVES) * 32 + (lane & 31);
-      if (k < K) {
+      const int kb = (c0 + w + i * HEAD_WAVES) * 32;
+      if (kb >= K) continue;  // wave-uniform
+      // mask rows into the patch, read back in the tile's layout; the masked
+      // gradient written there and read out as 16-byte row segments
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rr = r0 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (rr < B) g[(int64_t)rr * ldg + k] = f2bf(bf2f(mc[i][r]) > 0.f ? acc[i][r] : 0.f);
-        }
+      for (int half = 0; half < 2; ++half)
+        *reinterpret_cast<u32x4*>(pq + (half * 16 + (lane >> 2)) * HEAD_LQ + (lane & 3) * 8) = mc[i][half];
+      wave_sync();
+      bf16_t gv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int jl = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        gv[r] = f2bf(bf2f(pq[jl * HEAD_LQ + (lane & 31)]) > 0.f ? acc[i][r] : 0.f);
       }
+      wave_sync();
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pq[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * HEAD_LQ + (lane & 31)] = gv[r];
+      wave_sync();
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int rl = half * 16 + (lane >> 2), c8 = (lane & 3) * 8;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(pq + rl * HEAD_LQ + c8);
+        if (r0 + rl < B && kb + c8 < K) stg16(g + (int64_t)(r0 + rl) * ldg + kb + c8, v);
+      }
+      wave_sync();
     }
   }
 }
