@@ -35,6 +35,13 @@ __device__ inline float group16_sum(float v) {
   return v;
 }
 
+// LDS writes of this wave visible to its own reads (wave-private patches)
+__device__ inline void fm_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Head row in registers one sample ahead: thread t < COLS/2 holds columns
 // 2t, 2t+1 of row 0 (bf16 pair).
 template <int COLS>
@@ -68,6 +75,16 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
   __shared__ __attribute__((aligned(16))) bf16_t WR[NP * LR];
   __shared__ __attribute__((aligned(16))) bf16_t WT[K * LT];
   __shared__ float X0[HEAD ? D : 1], W0[HEAD ? K : 1];
+  // per-wave 32 x 32 patch: an O tile leaves as 16-byte row segments (its
+  // rows are contiguous in the output) instead of 2-byte columns, where the
+  // patches leave room for two blocks per compute unit
+  constexpr int LQ = 32 + 8;
+  constexpr int OT = (NP / 32) * (K / 32);  // O tiles, one wave each (OT <= 8)
+  constexpr size_t BASE = 2 * ((size_t)NP * LX + D * LT + K * LP + NP * LR + K * LT) +
+                          4 * ((HEAD ? D : 1) + (HEAD ? K : 1));
+  constexpr bool VEC = BASE + (size_t)OT * 2 * 32 * LQ <= 80 * 1024;
+  __shared__ __attribute__((aligned(16))) bf16_t OQ[VEC ? OT : 1][VEC ? 32 * LQ : 8];
+  const bool vec_out = VEC && (reinterpret_cast<uintptr_t>(out) & 15) == 0 && (ostride & 7) == 0;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nm = n - H;  // rows in the tiles
   {
@@ -120,6 +137,21 @@ __global__ __launch_bounds__(512) void fm_fwd_mfma_kernel(const bf16_t* __restri
       zero16(acc);
       mfma_tile<D>(acc, Xs + tj * 32 * LX, LX, PT + tc * 32 * LP, LP);
       const int c = tc * 32 + (lane & 31);
+      if (vec_out) {
+        bf16_t* pq = OQ[VEC ? w : 0];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pq[frag_row(r) * LQ + (lane & 31)] = f2bf(acc[r]);
+        fm_wave_sync();
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int rl = half * 16 + (lane >> 2), c8 = (lane & 3) * 8;
+          const int j = tj * 32 + rl;
+          if (j < nm)
+            stg16(ob + off + (j + H) * K + tc * 32 + c8, *reinterpret_cast<const u32x4*>(pq + rl * LQ + c8));
+        }
+        fm_wave_sync();
+        continue;
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = tj * 32 + frag_row(r);
