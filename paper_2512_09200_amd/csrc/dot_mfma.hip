@@ -80,6 +80,13 @@ __global__ __launch_bounds__(DOT_THREADS) void dot_fwd_mfma_kernel(const bf16_t*
   }
 }
 
+// LDS writes of this wave visible to its own reads (wave-private patches)
+__device__ inline void dot_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int NP, int D>
 __global__ __launch_bounds__(DOT_THREADS, 2) void dot_bwd_mfma_kernel(
     const bf16_t* __restrict__ X, int B, int n, const bf16_t* __restrict__ dout, int64_t dstride,
@@ -90,6 +97,10 @@ __global__ __launch_bounds__(DOT_THREADS, 2) void dot_bwd_mfma_kernel(
   constexpr int Q = (PMAX + DOT_THREADS - 1) / DOT_THREADS;  // pairs per thread
   __shared__ __attribute__((aligned(16))) bf16_t XT[D * LT];
   __shared__ __attribute__((aligned(16))) bf16_t S[NP * LS];
+  // per-wave 32 x 32 patch: dX tiles leave as 16-byte row segments
+  constexpr int LQ = 32 + 8;
+  __shared__ __attribute__((aligned(16))) bf16_t DQ[DOT_THREADS / 64][32 * LQ];
+  const bool vec_dx = (reinterpret_cast<uintptr_t>(dX) & 15) == 0;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int P = n * (n - 1) / 2;
   const int off = emit0 ? D : 0;
@@ -121,11 +132,13 @@ __global__ __launch_bounds__(DOT_THREADS, 2) void dot_bwd_mfma_kernel(
   for (int b = blockIdx.x; b < B; b += gridDim.x) {
     // the pair gradients of this sample, then S and X^T into LDS
     const bf16_t* gb = dout + (int64_t)b * dstride + off;
+    // straight-line loads (a pair past the last reads pair 0 and is not
+    // used): selecting the loaded value would make each load wait alone
     uint32_t gv[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const int m = threadIdx.x + q * DOT_THREADS;
-      gv[q] = m < P ? gb[m] : 0u;
+      gv[q] = gb[m < P ? m : 0];
     }
     sx.store(nullptr, 0, XT, LT, n);
 #pragma unroll
@@ -139,16 +152,39 @@ __global__ __launch_bounds__(DOT_THREADS, 2) void dot_bwd_mfma_kernel(
       }
     }
     __syncthreads();
+    // the slot-0 gradient of the column this wave's first tile covers, read
+    // before the next sample's loads are issued (a wait for it then does not
+    // wait for them); used only with emit0, by the tiles of row block 0
+    const bf16_t* g0 = dout + (int64_t)b * dstride;
+    const bf16_t g0raw = g0[(w % (D / 32)) * 32 + (lane & 31)];
     if (b + (int)gridDim.x < B) sx.load(X + (int64_t)(b + gridDim.x) * n * D, D, n);
-    const bf16_t* g0 = dout + (int64_t)b * dstride;  // slot-0 part of the gradient (emit0)
     bf16_t* dxb = dX + (int64_t)b * n * D;
+    bf16_t* pq = DQ[w];
     for (int t = w; t < TT * (D / 32); t += DOT_THREADS / 64) {
       const int ti = t / (D / 32), ta = t % (D / 32);
       f32x16 acc;
       zero16(acc);
       mfma_tile<NP>(acc, S + ti * 32 * LS, LS, XT + ta * 32 * LT, LT);
+      const float gz = (emit0 && ti == 0) ? bf2f(g0raw) : 0.f;  // ti == 0: t == w
+      if (vec_dx) {
+        // tile -> patch (row frag_row(r), column lane % 32) -> 16-byte row segments
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int il = frag_row(r);
+          const float v = (ti == 0 && il == 0) ? acc[r] + gz : acc[r];
+          pq[il * LQ + (lane & 31)] = f2bf(v);
+        }
+        dot_wave_sync();
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int rl = half * 16 + (lane >> 2), c8 = (lane & 3) * 8;
+          const int i = ti * 32 + rl;
+          if (i < n) stg16(dxb + i * D + ta * 32 + c8, *reinterpret_cast<const u32x4*>(pq + rl * LQ + c8));
+        }
+        dot_wave_sync();
+        continue;
+      }
       const int a = ta * 32 + (lane & 31);
-      const float gz = (emit0 && ti == 0) ? bf2f(g0[a]) : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int i = ti * 32 + frag_row(r);
