@@ -294,7 +294,20 @@ constexpr int SEG_TILE = SEG_THREADS * SEG_ITEMS;
 // arise where a run crosses a multiple of RANGE.
 constexpr int RANGE = 256;
 
-__device__ inline int seg_flag(const int* k, int64_t i) { return (i == 0 || k[i] != k[i - 1]) ? 1 : 0; }
+// The keys of a tile's SEG_ITEMS stripes and of the positions before them,
+// loaded as straight-line code from clamped positions (n >= 1), so that all
+// of them are in flight together: a load in a branch, or whose value is
+// selected at once, makes the compiler wait for it right there.
+__device__ inline void seg_load(const int* __restrict__ keys, int n, int64_t base,
+                                int (&key)[SEG_ITEMS], int (&prev)[SEG_ITEMS]) {
+#pragma unroll
+  for (int i = 0; i < SEG_ITEMS; ++i) {
+    const int64_t k = base + (int64_t)i * SEG_THREADS + threadIdx.x;
+    const int64_t kc = k < n ? k : n - 1;
+    key[i] = keys[kc];
+    prev[i] = keys[kc > 0 ? kc - 1 : 0];
+  }
+}
 
 __device__ inline int block_sum_scan(int v, int* lds, int* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -320,11 +333,13 @@ __global__ __launch_bounds__(SEG_THREADS) void seg_count_kernel(const int* __res
                                                                 int* __restrict__ tile_counts) {
   __shared__ int lds[SEG_THREADS / 64];
   const int64_t base = (int64_t)blockIdx.x * SEG_TILE;
+  int key[SEG_ITEMS], prev[SEG_ITEMS];
+  seg_load(keys, n, base, key, prev);
   int c = 0;
 #pragma unroll
   for (int i = 0; i < SEG_ITEMS; ++i) {
-    int64_t k = base + (int64_t)i * SEG_THREADS + threadIdx.x;
-    if (k < n) c += seg_flag(keys, k);
+    const int64_t k = base + (int64_t)i * SEG_THREADS + threadIdx.x;
+    c += (k < n && (k == 0 || key[i] != prev[i])) ? 1 : 0;
   }
   int tot;
   block_sum_scan(c, lds, &tot);
@@ -344,11 +359,14 @@ __global__ __launch_bounds__(SEG_THREADS) void seg_write_kernel(
   const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
   int run = tile_base[blockIdx.x];
   const int64_t base = (int64_t)blockIdx.x * SEG_TILE;
+  int keyv[SEG_ITEMS], prev[SEG_ITEMS];
+  seg_load(keys, n, base, keyv, prev);
+#pragma unroll
   for (int i = 0; i < SEG_ITEMS; ++i) {
     const int64_t k = base + (int64_t)i * SEG_THREADS + threadIdx.x;
     const bool in = k < n;
-    const int key = in ? keys[k] : 0;
-    const int fl = in && (k == 0 || key != keys[k - 1]) ? 1 : 0;
+    const int key = keyv[i];
+    const int fl = in && (k == 0 || key != prev[i]) ? 1 : 0;
     const uint64_t m = __ballot(fl);
     if (lane == 0) wsum[w] = __popcll(m);
     __syncthreads();

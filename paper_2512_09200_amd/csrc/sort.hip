@@ -51,21 +51,44 @@ __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
   return wbase + x - v;
 }
 
-// single block: exclusive scan of the tile sums in place
+// single block: exclusive scan of the tile sums in place (n >= 1).  Thread t
+// owns elements [t*per, (t+1)*per); they are read SCAN_REG at a time from
+// clamped positions (straight-line loads, all in flight together), and kept
+// in registers for the second sweep when per <= SCAN_REG.
+constexpr int SCAN_REG = 4;
 __global__ __launch_bounds__(1024) void scan_sums_kernel(int* __restrict__ sums, int n) {
   __shared__ int lds[1024 / 64];
   const int per = (n + blockDim.x - 1) / blockDim.x;
   const int lo = threadIdx.x * per;
+  int v[SCAN_REG];
   int s = 0;
-  for (int i = 0; i < per; ++i)
-    if (lo + i < n) s += sums[lo + i];
+  for (int i0 = 0; i0 < per; i0 += SCAN_REG) {
+#pragma unroll
+    for (int r = 0; r < SCAN_REG; ++r) {
+      const int i = lo + i0 + r;
+      v[r] = sums[i < n ? i : n - 1];
+    }
+#pragma unroll
+    for (int r = 0; r < SCAN_REG; ++r)
+      if (i0 + r < per && lo + i0 + r < n) s += v[r];
+  }
   int tot;
   int run = block_exclusive_scan(s, lds, &tot);
-  for (int i = 0; i < per; ++i) {
-    if (lo + i < n) {
-      int v = sums[lo + i];
-      sums[lo + i] = run;
-      run += v;
+  for (int i0 = 0; i0 < per; i0 += SCAN_REG) {
+    if (per > SCAN_REG) {
+#pragma unroll
+      for (int r = 0; r < SCAN_REG; ++r) {
+        const int i = lo + i0 + r;
+        v[r] = sums[i < n ? i : n - 1];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < SCAN_REG; ++r) {
+      const int i = lo + i0 + r;
+      if (i0 + r < per && i < n) {
+        sums[i] = run;
+        run += v[r];
+      }
     }
   }
 }
@@ -251,16 +274,16 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   for (int r = 0; r < ROUNDS; ++r) {
     const int k = cbase + r * 64 + lane;
     const bool valid = k < t.cnt;
+    // a lane past the tile's end reads position 0 (its key and value are
+    // never used): no select on the loaded value, so the loads of all
+    // rounds are in flight together
+    const int kk = valid ? k : 0;
     if constexpr (FIRST) {
-      // a lane past the tile's end reads position 0 (its key and value are
-      // never used): no select on the loaded value, so the loads of all
-      // rounds are in flight together
-      const int kk = valid ? k : 0;
       key[r] = keys_in[t.base + kk] + key0;
       val[r] = lvals[kk];
     } else {
-      key[r] = valid ? keys_in[t.base + k] : 0;
-      val[r] = valid ? vals_in[t.base + k] : 0;
+      key[r] = keys_in[t.base + kk];
+      val[r] = vals_in[t.base + kk];
     }
   }
   // stable rank of each item among the wave's items with the same digit
