@@ -5,7 +5,7 @@
 // One histogram pass over the batch's indices counts every digit of every
 // pass per feature segment (the counts of a digit do not depend on the order
 // the previous passes leave).  Each sort pass is then a single kernel: a tile
-// of 4096 items is ranked with wave ballots (items with equal digits keep
+// of 8192 items is ranked with wave ballots (items with equal digits keep
 // their order), its digit counts are published, and its output offsets come
 // from the segment's digit bases plus the counts of the segment's earlier
 // tiles, read by decoupled look-back over the tiles' published counts (tiles
@@ -16,14 +16,18 @@
 
 namespace lat {
 
-constexpr int SORT_THREADS = 256;
+// 512 threads x 16 items: a scatter block holds 73 KB of LDS, so two fit a
+// CU and one leaving frees room for a 72 KB GEMM block of the dense stages
+// that run beside the sort (with 4096-item tiles four 37 KB blocks filled the
+// LDS and a freed slot was always refilled by the next sort block).
+constexpr int SORT_THREADS = 512;
 constexpr int SORT_ITEMS = 16;
-constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;  // 4096
+constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;  // 8192
 constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 
 constexpr int SCAN_THREADS = 256;
-static_assert(SORT_THREADS == RADIX, "one thread per digit in the scatter's tile scan");
+static_assert(SORT_THREADS >= RADIX, "one thread per digit in the scatter's tile scan");
 
 // ---------------------------------------------------------------------------
 // block-wide and small exclusive scans of int32 (counts fit int32: totals < 2^31)
@@ -308,7 +312,7 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   }
   __syncthreads();
   {
-    const int d = threadIdx.x;  // SORT_THREADS == RADIX >= radix
+    const int d = threadIdx.x;  // SORT_THREADS >= RADIX >= radix
     int tot = 0;
     if (d < radix)
       for (int i = 0; i < NW; ++i) tot += wcnt[i][d];

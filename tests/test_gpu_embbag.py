@@ -16,6 +16,8 @@ CASES = {
     "multidomain-small-empty-bags": synth.small(synth.MULTIDOMAIN, B=192, rows=1500),
     "large-fm-small": synth.small(synth.LARGE_FM, B=64, rows=20000),
     "d256-bf16-mean": synth.small(synth.MID, B=96, rows=800, F=5, d=256, pool="mean"),
+    # ~20K lookups per feature: several sort tiles per segment and a ragged last one
+    "mid-multitile": synth.small(synth.MID, B=2048, rows=100000, F=3),
 }
 
 
