@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import step
+from oracle import interact, step
 
 
 def _tiny_cfg(kind, pool="sum"):
@@ -83,8 +83,10 @@ def _check_kinks(cfg, params, table, batch):
             assert np.min(np.abs(a)) > 1e-4, "seed puts a pre-activation on a ReLU kink"
 
 
-@pytest.mark.parametrize("kind,pool", [("dot", "sum"), ("dot", "mean"), ("fm", "sum"), ("stack", "sum")])
-def test_finite_differences(kind, pool):
+def _fd_worst(kind, pool="sum", n_coords=12):
+    """Largest relative disagreement between the oracle's analytic gradients
+    and central finite differences of its loss, over sampled coordinates of
+    every parameter and every touched table row."""
     cfg = _tiny_cfg(kind, pool)
     batch, params, table = _setup(cfg)
     assert batch["mask"].min() == 0 and batch["mask"].max() == 1
@@ -101,23 +103,68 @@ def test_finite_differences(kind, pool):
         assert grad.shape == arr.shape, name
         scale = max(np.sqrt(np.mean(grad ** 2)), 1e-12)
         flat = [np.unravel_index(k, arr.shape) for k in
-                rng.choice(arr.size, size=min(arr.size, 12), replace=False)]
+                rng.choice(arr.size, size=min(arr.size, n_coords), replace=False)]
         for idx in flat:
             h = 1e-6 * max(1.0, abs(arr[idx]))
             fd = _fd(loss_fn, arr, idx, h)
-            err = abs(fd - grad[idx]) / max(abs(grad[idx]), scale)
-            worst = max(worst, err)
-            assert err < 1e-6, (name, idx, fd, grad[idx])
+            worst = max(worst, abs(fd - grad[idx]) / max(abs(grad[idx]), scale))
     # embedding gradient: every touched row, a few coordinates
     uniq, G = g["unique_rows"], g["grad_rows"]
     scale = max(np.sqrt(np.mean(G ** 2)), 1e-12)
     for u, r in enumerate(uniq):
         for a in rng.choice(cfg.d, size=2, replace=False):
             fd = _fd(loss_fn, table, (r, a), 1e-6)
-            err = abs(fd - G[u, a]) / max(abs(G[u, a]), scale)
-            worst = max(worst, err)
-            assert err < 1e-6, ("table", r, a, fd, G[u, a])
+            worst = max(worst, abs(fd - G[u, a]) / max(abs(G[u, a]), scale))
     # rows that no bag touches have no gradient: perturbing them leaves the loss unchanged
     untouched = np.setdiff1d(np.arange(table.shape[0]), uniq)
     if untouched.size:
         assert _fd(loss_fn, table, (int(untouched[0]), 0), 1e-3) == 0.0
+    return worst
+
+
+@pytest.mark.parametrize("kind,pool", [("dot", "sum"), ("dot", "mean"), ("fm", "sum"), ("stack", "sum")])
+def test_finite_differences(kind, pool):
+    assert _fd_worst(kind, pool) < 1e-6
+
+
+# ------------------------------------------------------------------------
+# Planted mistakes: each copy of a backward function below carries one
+# plausible error; the finite-difference pin must catch it.
+def _fm_backward_wrong_sign(G, X, W, P, rnd):
+    G, X, W = (np.asarray(a, np.float64) for a in (G, X, W))
+    dP = rnd(X.transpose(0, 2, 1) @ G)
+    dX = G @ P.transpose(0, 2, 1) - W[None] @ dP.transpose(0, 2, 1)     # sign of the W term
+    return dX, (X @ dP).sum(axis=0)
+
+
+def _layernorm_backward_dropped_term(dy, xhat, rstd, gamma):
+    dy = np.asarray(dy, np.float64)
+    dgamma = (dy * xhat).reshape(-1, xhat.shape[-1]).sum(axis=0)
+    dxh = dy * np.asarray(gamma, np.float64)
+    du = rstd * (dxh - dxh.mean(axis=-1, keepdims=True))              # xhat term dropped
+    return du, dgamma
+
+
+def _mlp_backward_no_relu_mask(g_out, hs, masks, layers, rnd, relu_last, need_input_grad):
+    masks = [None if m is None else np.ones_like(m) for m in masks]
+    return _ORIG["mlp_backward"](g_out, hs, masks, layers, rnd, relu_last, need_input_grad)
+
+
+def _dot_backward_no_slot0(dp, X):
+    dX = _ORIG["dot_backward"](dp, X)
+    dX[:, 0] = 0.0                                                    # dense slot's gradient dropped
+    return dX
+
+
+_ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward)
+
+
+@pytest.mark.parametrize("target,module,name,kind", [
+    (_fm_backward_wrong_sign, step, "fm_backward", "fm"),
+    (_layernorm_backward_dropped_term, interact, "layernorm_backward", "stack"),
+    (_mlp_backward_no_relu_mask, step, "mlp_backward", "dot"),
+    (_dot_backward_no_slot0, step, "dot_backward", "dot"),
+], ids=["fm-sign", "layernorm-term", "relu-mask", "slot0-gradient"])
+def test_planted_backward_mistakes_fail_the_finite_difference_pin(monkeypatch, target, module, name, kind):
+    monkeypatch.setattr(module, name, target)
+    assert _fd_worst(kind, n_coords=6) > 1e-3
