@@ -32,12 +32,12 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="large-emb-fm",
                     help="one of: tiny-dot-f32, mid-dot-bf16, large-emb-fm, multidomain-dot, deep-stack")
-    ap.add_argument("--batches", type=int, default=2, help="distinct batches cycled")
+    ap.add_argument("--batches", type=int, default=4, help="distinct batches cycled")
     ap.add_argument("--cpu-sample", type=int, default=2048, help="samples in the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--uniform", action="store_true", help="uniform indices (control run)")
     ap.add_argument("--single-stream", action="store_true",
-                    help="run the sparse gradient's sort on the step's stream (no overlap)")
+                    help="no side stream: every stage on the step's stream (no overlap)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, stream 1 GiB through a plain elementwise kernel "
                          "(torch.neg, 1 GiB read + 1 GiB written) as a counter calibration point")
@@ -83,7 +83,7 @@ def main():
             indices=torch.from_numpy(b["indices"]).to(dev),
             dense=torch.from_numpy(b["dense"]).to(sdt).to(dev),
             labels=torch.from_numpy(b["labels"]).to(dev), mask=torch.from_numpy(b["mask"]).to(dev),
-            nnz=int(b["offsets"][-1])))
+            nnz=int(b["offsets"][-1]), U=distinct_rows(b, cfg)))
     row_base = torch.from_numpy(batches[0]["np"]["row_base"]).to(dev)
     log(f"[bench] batches ready ({time.time() - t0:.1f}s); generating tables")
     E = synth.make_tables(cfg, device=dev)
@@ -118,11 +118,13 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs resident ({time.time() - t0:.1f}s); workspace {lay.total_bytes / 2**30:.2f} GiB")
 
-    def step(i, events=None, single_stream=args.single_stream):
+    side = api.SideStream()
+
+    def step(i, events=None, one_stream=args.single_stream):
         b = batches[i % len(batches)]
         api.lattice_step(model, b["offsets"], b["indices"], b["dense"], b["labels"], b["mask"], ws,
                          cfg.lr_tables, False, stage_events=events, nnz_capacity=nnz_max,
-                         single_stream=single_stream)
+                         side=None if one_stream else side)
 
     for i in range(args.warmup):
         step(i)
@@ -172,7 +174,7 @@ def main():
     else:
         ev_iso = make_events(args.steps)
         for i in range(args.steps):
-            step(args.warmup + 2 * args.steps + i, ev_iso[i], single_stream=True)
+            step(args.warmup + 2 * args.steps + i, ev_iso[i], one_stream=True)
         torch.cuda.synchronize()
         iso_ms = stage_times(ev_iso)
         log("[bench] stage ms, one stream: " + ", ".join(f"{k}={v:.3f}" for k, v in iso_ms.items()))
@@ -180,23 +182,31 @@ def main():
     # ---- algorithmic work -------------------------------------------------
     es = 2 if cfg.dtype == "bf16" else 4
     nnz = float(np.mean([b["nnz"] for b in batches]))
+    U = float(np.mean([b["U"] for b in batches]))        # distinct rows per batch
     bags = cfg.F * cfg.B
     row_bytes = cfg.d * es
-    # unique rows of the last batch used (read back outside the timed region)
-    v = api.step_views(model, ws, lay, cfg.B, cfg.T, nnz_max)
-    U = int(v["num_unique"].item())
-    # pooled lookup: per lookup one table row + its index; per bag its offset and pooled row
-    fwd_bytes = nnz * (row_bytes + 4) + bags * 4 + bags * cfg.d * es
-    # segmented reduction: per occurrence its dX row, sorted key and bag id; per
-    # occurring row the table row read and written (SGD) or its fp32 gradient written
-    red_bytes = nnz * (cfg.d * es + 8) + (U * 2 * row_bytes if cfg.lr_tables else U * 4 * cfg.d)
-    # whole sparse-gradient stage (sort and bookkeeping are implementation overhead)
-    bwd_bytes = nnz * (cfg.d * es + 4) + bags * 4 + (U * 2 * row_bytes if cfg.lr_tables else U * (4 * cfg.d + 4))
+    upd = U * 2 * row_bytes if cfg.lr_tables else U * 4 * cfg.d   # SGD read+write, or fp32 G
+    # Compulsory bytes (what the kernel must move at least once): each
+    # distinct table row once, each index / offset once, each pooled row or
+    # dX row once.
+    fwd_bytes = U * row_bytes + nnz * 4 + bags * 4 + bags * cfg.d * es
+    red_bytes = nnz * 8 + bags * cfg.d * es + upd
+    # Logical bytes (every lookup counted as a row read, every occurrence as
+    # a dX row read): the rate the kernels deliver to the arithmetic,
+    # including rows re-read from L2 / MALL.
+    fwd_logical = nnz * (row_bytes + 4) + bags * 4 + bags * cfg.d * es
+    red_logical = nnz * (cfg.d * es + 8) + upd
+    # whole sparse-gradient stage, logical (sort and bookkeeping are overhead)
+    bwd_bytes = nnz * (cfg.d * es + 4) + bags * 4 + upd
     bwd_stages = ["embbag_sort", "embbag_runs", "embbag_reduce", "embbag_fixup"]
     bwd_ms = sum(iso_ms[s] for s in bwd_stages)
-    fwd_gbs = fwd_bytes / (timed_ms["embbag_fwd"] * 1e-3) / 1e9
-    red_gbs = red_bytes / (timed_ms["embbag_reduce"] * 1e-3) / 1e9
-    bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
+
+    def gbs(nbytes, ms):
+        return nbytes / (ms * 1e-3) / 1e9
+
+    fwd_gbs = gbs(fwd_bytes, timed_ms["embbag_fwd"])
+    red_gbs = gbs(red_bytes, timed_ms["embbag_reduce"])
+    bwd_gbs = gbs(bwd_bytes, bwd_ms)
     n = cfg.n_slots
     flops_fwd = mlp_fwd_flops((cfg.dense_in,) + tuple(cfg.bottom), cfg.B) if cfg.has_dense else 0.0
     flops_fwd += mlp_fwd_flops((cfg.top_in,) + tuple(cfg.top), cfg.B)
@@ -212,21 +222,27 @@ def main():
             if l == 0 and nl != cfg.stack_n:
                 flops_fwd += 2.0 * cfg.B * cfg.stack_n * nl * cfg.d                  # residual C X
             nl = cfg.stack_n
-    dense_stages = ["bottom_fwd", "interact_fwd", "top_fwd", "top_bwd", "interact_bwd", "top_wgrad",
-                    "bottom_bwd"]
+    dense_stages = ["bottom_fwd", "interact_fwd", "top_fwd", "loss", "top_bwd", "interact_bwd",
+                    "top_wgrad", "bottom_bwd"]
     dense_ms = sum(iso_ms[s] for s in dense_stages)
     mfma_tfs = 3.0 * flops_fwd / (dense_ms * 1e-3) / 1e12
     samples_per_s = cfg.B / (ms_per_step * 1e-3)
 
+    def roof(kernel, stage, nbytes, logical):
+        ms = timed_ms[stage]
+        t = counted_traffic(cfg.name, kernel)
+        r = {"bound": "hbm", "kernel": kernel, "achieved": round(gbs(nbytes, ms), 1),
+             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs(nbytes, ms) / HBM_PEAK_GBS, 4),
+             "traffic": t, "bytes_per_launch": int(nbytes), "launch_ms": round(ms, 4),
+             "logical_bytes_per_launch": int(logical), "logical_GBps": round(gbs(logical, ms), 1)}
+        if t:
+            r["dram_GBps"] = round(gbs(t, ms), 1)
+            r["dram_frac"] = round(gbs(t, ms) / HBM_PEAK_GBS, 4)
+        return r
+
     # dominant kernel: the segmented reduction of the sparse gradient
-    roofline = {"bound": "hbm", "kernel": "seg_reduce_kernel", "achieved": round(red_gbs, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(red_gbs / HBM_PEAK_GBS, 4),
-                "traffic": counted_traffic(cfg.name, "seg_reduce_kernel"),
-                "bytes_per_launch": int(red_bytes), "launch_ms": round(timed_ms["embbag_reduce"], 4)}
-    gather_roofline = {"bound": "hbm", "kernel": "embbag_fwd_kernel", "achieved": round(fwd_gbs, 1),
-                       "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(fwd_gbs / HBM_PEAK_GBS, 4),
-                       "traffic": counted_traffic(cfg.name, "embbag_fwd_kernel"),
-                       "bytes_per_launch": int(fwd_bytes), "launch_ms": round(timed_ms["embbag_fwd"], 4)}
+    roofline = roof("seg_reduce_kernel", "embbag_reduce", red_bytes, red_logical)
+    gather_roofline = roof("embbag_fwd_kernel", "embbag_fwd", fwd_bytes, fwd_logical)
 
     if args.calib_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
@@ -252,13 +268,13 @@ def main():
                    "rows_per_table": cfg.rows, "dim": cfg.d,
                    "index_dist": list(cfg.index_dist), "bag_dist": list(cfg.bag_dist),
                    "interaction": cfg.interact, "top": list(cfg.top), "lr_tables": cfg.lr_tables,
-                   "nnz_per_step": int(nnz), "unique_rows_last_step": U, "parallelism": "single-gpu",
+                   "nnz_per_step": int(nnz), "distinct_rows_per_step": int(U),
+                   "batches_cycled": len(batches), "parallelism": "single-gpu",
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,
         "gather_roofline": gather_roofline,
-        "embbag_fwd_GBps": round(fwd_gbs, 1), "embbag_bwd_GBps": round(bwd_gbs, 1),
-        "embbag_fwd_hbm_frac": round(fwd_gbs / HBM_PEAK_GBS, 4),
-        "embbag_bwd_hbm_frac": round(bwd_gbs / HBM_PEAK_GBS, 4),
+        "embbag_fwd_GBps": round(fwd_gbs, 1), "embbag_fwd_hbm_frac": round(fwd_gbs / HBM_PEAK_GBS, 4),
+        "embbag_bwd_logical_GBps": round(bwd_gbs, 1),
         "embbag_bwd_ms": round(bwd_ms, 4),
         "interaction_mlp_TFLOPs": round(mfma_tfs, 1),
         "interaction_mlp_mfma_frac": round(mfma_tfs / MFMA_BF16_PEAK_TFS, 4),
@@ -267,6 +283,16 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def distinct_rows(batch, cfg):
+    """Distinct global table rows a batch touches (host-side bookkeeping of the
+    bench's byte counts; the step computes its own on the GPU)."""
+    import numpy as np
+    lengths = np.diff(batch["offsets"].astype(np.int64))
+    feat = np.repeat(np.arange(cfg.F * cfg.B, dtype=np.int64) // cfg.B, lengths)
+    keys = batch["row_base"].astype(np.int64)[feat] + batch["indices"].astype(np.int64)
+    return int(np.unique(keys).size)
 
 
 def source_digest(files):

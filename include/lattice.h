@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 5
+#define LATTICE_ABI_VERSION 6
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -297,18 +297,25 @@ typedef enum {
 
 /* Streams.  The sort and run bookkeeping of the sparse gradient need only
  * the batch, and the dense weight gradients (top MLP weights, bottom MLP
- * backward) are not needed by the sparse gradient, so by default lattice_step
- * runs them on a library-owned side stream of the caller's device
- * (non-blocking, default priority, one per device, created on first use and
- * kept until the process ends): the sort is forked from the caller's stream
- * after the pooled lookups and overlaps the dense forward and backward; the
- * weight gradients are forked after the interaction backward and overlap the
- * segmented reduction, which waits for the sort.  All
- * work is still ordered after the caller's prior work on `stream`, and the
- * call's work is complete when `stream` reaches the end of it, as with a
- * single stream.  Concurrent calls (any threads) share the side stream and
- * serialise their sparse stages on it.  single_stream = 1 keeps every stage
- * on the caller's stream; results are identical either way. */
+ * backward) are not needed by the sparse gradient, so lattice_step can run
+ * them on a second stream that the CALLER provides (side_stream, a
+ * hipStream_t of the same device, default priority) together with
+ * LATTICE_STEP_SIDE_EVENTS events (hipEvent_t, created by the caller; timing
+ * may be disabled) that it uses to fork work from `stream` onto the side
+ * stream and to join it back: the bottom MLP's forward is forked at the
+ * step's start and runs beside the pooled lookups; the sort is forked after
+ * the pooled lookups and overlaps the dense forward and backward; the weight
+ * gradients are forked after the interaction backward and overlap the
+ * segmented reduction, which waits for the sort.  All work is still ordered
+ * after the caller's prior work on `stream`, and the call's work is complete
+ * when `stream` reaches the end of it, as with a single stream.  The library
+ * keeps no stream or event of its own.  Two calls that share a side stream
+ * or events must not be enqueued concurrently from different host threads
+ * (they would interleave their event records).  side_stream = NULL (or equal
+ * to `stream`) keeps every stage on `stream`; results are bit-identical
+ * either way. */
+#define LATTICE_STEP_SIDE_EVENTS 6
+
 typedef struct {
   float lr_tables;             /* row-sparse SGD step on the tables (0: none) */
   int32_t emit_grad_rows;      /* 1: also write the [nnz, dim] fp32 row gradients */
@@ -317,11 +324,13 @@ typedef struct {
   void* const* stage_events;   /* host array of 2*LATTICE_STEP_STAGES hipEvent_t or NULL:
                                   [2s] is recorded when stage s begins and [2s+1] when
                                   it ends, on the stream that runs the stage (the side
-                                  stream for EMBBAG_SORT, EMBBAG_RUNS, TOP_WGRAD and
-                                  BOTTOM_BWD unless single_stream); NULL entries are
-                                  not recorded (each record costs a few microseconds
-                                  of GPU time) */
-  int32_t single_stream;       /* 1: no side stream (see above) */
+                                  stream for BOTTOM_FWD, EMBBAG_SORT, EMBBAG_RUNS,
+                                  TOP_WGRAD and BOTTOM_BWD when a side stream is given);
+                                  NULL entries are not recorded (each record costs a
+                                  few microseconds of GPU time) */
+  void* side_stream;           /* hipStream_t or NULL (see above) */
+  void* const* side_events;    /* host array of LATTICE_STEP_SIDE_EVENTS hipEvent_t;
+                                  required when side_stream is used */
 } lattice_step_opts;
 
 /* Byte offsets of every intermediate inside the step workspace (-1: absent). */
@@ -338,6 +347,12 @@ typedef struct {
   int64_t dX;           /* [B, n, dim] gradient of the stacked vectors */
   int64_t bottom_act[LATTICE_MAX_LAYERS];   /* [B, out_i] hidden bottom outputs (last: in X) */
   int64_t top_act[LATTICE_MAX_LAYERS];      /* [B, out_i] hidden top outputs (last: logits) */
+  /* Gradient chain, storage dtype, [B, out_i]: the gradient of layer i's
+   * output masked by its ReLU, i.e. the left operand of that layer's weight
+   * gradient dW_i = g_i^T h_i.  top_grad[last] is d_logits_op; bottom_grad[last]
+   * is the masked gradient of the bottom output (slot 0 of X). */
+  int64_t top_grad[LATTICE_MAX_LAYERS];
+  int64_t bottom_grad[LATTICE_MAX_LAYERS];
   int64_t unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows;
   int64_t interact;     /* interaction workspace (saved state from forward to backward) */
   int64_t scratch;      /* scratch shared by the dense stages */

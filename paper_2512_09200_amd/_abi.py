@@ -72,9 +72,13 @@ class lattice_batch_desc(Structure):
                 ("mask", c_void_p)]
 
 
+SIDE_EVENTS = 6
+
+
 class lattice_step_opts(Structure):
     _fields_ = [("lr_tables", c_float), ("emit_grad_rows", c_int32), ("nnz_capacity", c_int64),
-                ("stage_events", POINTER(c_void_p)), ("single_stream", c_int32)]
+                ("stage_events", POINTER(c_void_p)), ("side_stream", c_void_p),
+                ("side_events", POINTER(c_void_p))]
 
 
 STAGES = ["embbag_fwd", "bottom_fwd", "interact_fwd", "top_fwd", "loss", "top_bwd",
@@ -86,7 +90,8 @@ class lattice_step_layout(Structure):
     _fields_ = ([("total_bytes", c_int64), ("X", c_int64), ("t", c_int64), ("t_stride", c_int64),
                  ("logits", c_int64), ("d_logits", c_int64), ("d_logits_op", c_int64),
                  ("loss", c_int64), ("d_t", c_int64), ("dX", c_int64),
-                 ("bottom_act", c_int64 * MAX_LAYERS), ("top_act", c_int64 * MAX_LAYERS)]
+                 ("bottom_act", c_int64 * MAX_LAYERS), ("top_act", c_int64 * MAX_LAYERS),
+                 ("top_grad", c_int64 * MAX_LAYERS), ("bottom_grad", c_int64 * MAX_LAYERS)]
                 + [(k, c_int64) for k in ("unique_rows", "seg_offsets", "sorted_bags",
                                           "num_unique", "grad_rows", "interact", "scratch",
                                           "scratch_bytes", "sparse", "sparse_bytes")])

@@ -270,16 +270,33 @@ def lattice_step_plan(model, B, nnz, lr_tables=0.0, emit_grad_rows=False):
     return lay
 
 
+class SideStream:
+    """A second stream of the caller's device and the fork / join events that
+    lattice_step uses to overlap the sparse gradient's sort and the dense
+    weight gradients with the rest of the step (default priority; the
+    events are created here, by torch, and recorded once so they exist)."""
+
+    def __init__(self, device=None):
+        self.stream = torch.cuda.Stream(device=device)
+        self.events = [torch.cuda.Event() for _ in range(A.SIDE_EVENTS)]
+        for e in self.events:
+            e.record(self.stream)
+        self._arr = (ctypes.c_void_p * A.SIDE_EVENTS)(*[e.cuda_event for e in self.events])
+
+    def ptrs(self):
+        return self.stream.cuda_stream, ctypes.cast(self._arr, ctypes.POINTER(ctypes.c_void_p))
+
+
 def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0,
                  emit_grad_rows=False, stream=None, stage_events=None, nnz_capacity=0,
-                 single_stream=False):
+                 side=None):
     """One forward+backward step; ws is a uint8 device tensor of at least
     lattice_step_plan(...).total_bytes.  stage_events: optional list of
     2*len(STAGES) torch.cuda.Event(enable_timing=True) or None: [2s] and
     [2s+1] are recorded when stage s begins and ends, on the stream that runs
     it (None: not recorded).
-    single_stream: keep the sparse gradient's sort on the step's stream
-    instead of the library's side stream."""
+    side: a SideStream to overlap the sort and the weight gradients on (None:
+    every stage on the step's stream)."""
     lib = load()
     _contig(dense, labels, mask, ws)
     B = labels.shape[0]
@@ -287,8 +304,9 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
                                  dense=dense.data_ptr() if dense is not None and dense.numel() else None,
                                  labels=labels.data_ptr(), mask=mask.data_ptr())
     opts = A.lattice_step_opts(lr_tables=float(lr_tables), emit_grad_rows=int(emit_grad_rows),
-                               nnz_capacity=int(nnz_capacity or indices.numel()),
-                               single_stream=int(bool(single_stream)))
+                               nnz_capacity=int(nnz_capacity or indices.numel()))
+    if side is not None:
+        opts.side_stream, opts.side_events = side.ptrs()
     if stage_events is not None:
         if len(stage_events) != 2 * len(A.STAGES):
             raise ValueError("need 2*len(STAGES) events")
@@ -326,8 +344,11 @@ def step_views(model, ws, layout, B, T, nnz):
              grad_rows=view(layout.grad_rows, (max(nnz, 1), d), torch.float32))
     tops = model.tensors["top"]
     v["top_act"] = [view(layout.top_act[i], (B, tops[i]["W"].shape[0]), dt) for i in range(len(tops) - 1)]
+    v["top_grad"] = [view(layout.top_grad[i], (B, tops[i]["W"].shape[0]), dt) for i in range(len(tops))]
     bots = model.tensors["bottom"]
     v["bottom_act"] = [view(layout.bottom_act[i], (B, bots[i]["W"].shape[0]), dt)
                        for i in range(len(bots) - 1)] if model.dense_in > 0 else []
+    v["bottom_grad"] = [view(layout.bottom_grad[i], (B, bots[i]["W"].shape[0]), dt)
+                        for i in range(len(bots))] if model.dense_in > 0 else []
     _ = es
     return v

@@ -73,6 +73,46 @@ static lattice_status check_tables(const lattice_tables* t, const lattice_jagged
   return check_dim(t->dim, t->dtype);
 }
 
+// Parameter gradients of an empty batch are sums over no samples: zero.  A
+// fill kernel (not hipMemsetAsync) so that a captured graph replays it.
+__global__ void zero_f32_kernel(float* p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
+static hipError_t zero_f32(float* p, int64_t n, hipStream_t s) {
+  if (!p || n <= 0) return hipSuccess;
+  zero_f32_kernel<<<cdiv(n, 256), 256, 0, s>>>(p, n);
+  return hipGetLastError();
+}
+
+static hipError_t zero_mlp_grads(const lattice_mlp_desc* d, hipStream_t s) {
+  for (int i = 0; i < d->n_layers; ++i) {
+    const lattice_linear& L = d->layers[i];
+    hipError_t e = zero_f32(L.dW, (int64_t)L.out_dim * L.in_dim, s);
+    if (e == hipSuccess) e = zero_f32(L.db, L.out_dim, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+static hipError_t zero_interact_grads(const lattice_interact_desc* d, hipStream_t s) {
+  if (d->kind == LATTICE_INTERACT_FM) return zero_f32(d->fm_dW, (int64_t)d->n * d->rank, s);
+  if (d->kind != LATTICE_INTERACT_STACK) return hipSuccess;
+  int n_in = d->n;
+  for (int l = 0; l < d->n_layers; ++l) {
+    const lattice_stack_layer& L = d->layers[l];
+    const int64_t nd = (int64_t)d->stack_n * d->dim;
+    hipError_t e = zero_f32(L.dW, (int64_t)n_in * d->rank, s);
+    if (e == hipSuccess) e = zero_f32(L.dA, nd * n_in * d->rank, s);
+    if (e == hipSuccess && L.C) e = zero_f32(L.dC, (int64_t)d->stack_n * n_in, s);
+    if (e == hipSuccess) e = zero_f32(L.dgamma, d->dim, s);
+    if (e != hipSuccess) return e;
+    n_in = d->stack_n;
+  }
+  return hipSuccess;
+}
+
 extern "C" {
 
 const char* lattice_status_string(lattice_status s) {
@@ -328,8 +368,12 @@ lattice_status lattice_interact_bwd(const lattice_interact_desc* desc, int32_t B
     }
   const size_t need = interact_ws(desc, B);
   if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
-  if (B > 0) REQUIRE(X && d_out && dX, "null X/d_out/dX");
-  REQUIRE(d_out_stride >= interact_width(desc) || B == 0, "d_out_stride too small");
+  if (B == 0) {
+    HIPRET(zero_interact_grads(desc, strm(stream)));
+    return LATTICE_OK;
+  }
+  REQUIRE(X && d_out && dX, "null X/d_out/dX");
+  REQUIRE(d_out_stride >= interact_width(desc), "d_out_stride too small");
   HIPRET(interact_bwd_impl(desc, B, X, d_out, d_out_stride, dX, ws, strm(stream)));
   return LATTICE_OK;
 }
@@ -585,6 +629,10 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
   const int T = desc->layers[L - 1].out_dim;
   REQUIRE(d_out_stride >= T, "d_out_stride too small");
   if (d_in) REQUIRE(d_in_stride >= desc->layers[0].in_dim, "d_in_stride too small");
+  if (B == 0) {
+    HIPRET(zero_mlp_grads(desc, strm(stream)));
+    return LATTICE_OK;
+  }
   char* p = (char*)ws;
   void* gemm_ws = p; p += mlp_bwd_ws(desc, B);
   const size_t g = al256(mlp_gbuf_elems(desc, B) * esize(desc->dtype));
@@ -690,6 +738,13 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
       P->g_bot[i] = take((size_t)B * m->bottom.layers[i].out_dim * es);
     P->g_masked = take((size_t)B * d * es);
   }
+  for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) L.top_grad[i] = L.bottom_grad[i] = -1;
+  for (int i = 0; i + 1 < m->top.n_layers; ++i) L.top_grad[i] = P->g_top[i];
+  L.top_grad[m->top.n_layers - 1] = L.d_logits_op;
+  if (m->dense_in > 0) {
+    for (int i = 0; i + 1 < m->bottom.n_layers; ++i) L.bottom_grad[i] = P->g_bot[i];
+    L.bottom_grad[m->bottom.n_layers - 1] = P->g_masked;
+  }
   const int64_t nn = nnz > 0 ? nnz : 1;
   L.unique_rows = take((size_t)nn * 4);
   L.seg_offsets = take((size_t)(nn + 1) * 4);
@@ -713,47 +768,17 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   return LATTICE_OK;
 }
 
-// Side stream of each device for the sparse gradient's sort and run
-// bookkeeping, with its fork / join events.  Created on first use, kept until
-// the process ends; g_side_mu serialises every use.
+// The caller's side stream and its fork / join events (see lattice.h).
 namespace {
 struct SideStream {
   hipStream_t s = nullptr;
-  // fork after the pooled lookups and after the interaction backward; join
-  // after the sort and run bookkeeping and after the dense weight gradients
-  hipEvent_t fork_fwd = nullptr, fork_bwd = nullptr, sorted = nullptr, done = nullptr;
-  // fork at the step's start and join of the bottom MLP's forward (which
-  // runs beside the pooled lookups)
-  hipEvent_t fork_start = nullptr, bottom_done = nullptr;
+  // fork at the step's start, after the pooled lookups and after the
+  // interaction backward; join of the bottom MLP's forward, of the sort and
+  // run bookkeeping and of the dense weight gradients
+  hipEvent_t fork_start = nullptr, fork_fwd = nullptr, fork_bwd = nullptr;
+  hipEvent_t bottom_done = nullptr, sorted = nullptr, done = nullptr;
 };
-constexpr int kMaxDevices = 64;
-std::mutex g_side_mu;
-SideStream g_side[kMaxDevices];
-
-// Requires g_side_mu held.
-lattice_status side_stream_of(hipStream_t main, SideStream** out) {
-  hipDevice_t dev = 0;
-  if (hipStreamGetDevice(main, &dev) != hipSuccess)
-    FAIL(LATTICE_ERR_HIP, "hipStreamGetDevice failed");
-  REQUIRE(dev >= 0 && dev < kMaxDevices, "device %d out of range", (int)dev);
-  SideStream& ss = g_side[dev];
-  if (!ss.s) {
-    int cur = 0;
-    if (hipGetDevice(&cur) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipGetDevice failed");
-    if (cur != dev && hipSetDevice(dev) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipSetDevice failed");
-    hipError_t e = hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking);
-    for (hipEvent_t* ev : {&ss.fork_fwd, &ss.fork_bwd, &ss.sorted, &ss.done, &ss.fork_start,
-                           &ss.bottom_done})
-      if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
-    if (cur != dev) (void)hipSetDevice(cur);
-    if (e != hipSuccess) {
-      ss = SideStream{};  // handles of a failed set-up stay unused
-      FAIL(LATTICE_ERR_HIP, "side stream set-up failed: %s", hipGetErrorString(e));
-    }
-  }
-  *out = &ss;
-  return LATTICE_OK;
-}
+static_assert(LATTICE_STEP_SIDE_EVENTS == 6, "side events");
 }  // namespace
 
 extern "C" {
@@ -786,9 +811,25 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   if (st != LATTICE_OK) return st;
   if (ws_bytes < (size_t)P.L.total_bytes || !ws)
     FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %lld", ws_bytes, (long long)P.L.total_bytes);
-  REQUIRE(batch->labels && batch->mask, "null labels/mask");
+  REQUIRE((batch->labels && batch->mask) || B == 0, "null labels/mask");
   if (m->dense_in > 0) REQUIRE(batch->dense || B == 0, "null dense input");
-  if (B == 0) return LATTICE_OK;
+  if (opts->side_stream && opts->side_stream != stream) {
+    REQUIRE(opts->side_events, "side_stream needs side_events");
+    for (int i = 0; i < LATTICE_STEP_SIDE_EVENTS; ++i)
+      REQUIRE(opts->side_events[i], "side_events[%d] is null", i);
+  }
+  if (B == 0) {
+    // sums over an empty batch: every parameter gradient, the loss and the
+    // unique-row count are zero; the tables are untouched
+    hipStream_t s0 = strm(stream);
+    char* base0 = (char*)ws;
+    if (m->dense_in > 0) HIPRET(zero_mlp_grads(&m->bottom, s0));
+    HIPRET(zero_mlp_grads(&m->top, s0));
+    HIPRET(zero_interact_grads(&m->interact, s0));
+    HIPRET(zero_f32((float*)(base0 + P.L.loss), 1, s0));
+    HIPRET(zero_f32((float*)(base0 + P.L.num_unique), 1, s0));
+    return LATTICE_OK;
+  }
 
   hipStream_t s = strm(stream);
   void* const* ev = opts->stage_events;
@@ -820,12 +861,14 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                            stage_ev(LATTICE_STAGE_EMBBAG_SORT));
   };
 
-  std::unique_lock<std::mutex> lock(g_side_mu, std::defer_lock);
+  SideStream side_;
   SideStream* side = nullptr;
-  if (!opts->single_stream) {
-    lock.lock();
-    st = side_stream_of(s, &side);
-    if (st != LATTICE_OK) return st;
+  if (opts->side_stream && strm(opts->side_stream) != s) {
+    side_.s = strm(opts->side_stream);
+    hipEvent_t* evs[LATTICE_STEP_SIDE_EVENTS] = {&side_.fork_start, &side_.fork_fwd, &side_.fork_bwd,
+                                                 &side_.bottom_done, &side_.sorted, &side_.done};
+    for (int i = 0; i < LATTICE_STEP_SIDE_EVENTS; ++i) *evs[i] = (hipEvent_t)opts->side_events[i];
+    side = &side_;
   }
   // 2. bottom MLP -> slot 0 of X.  It needs only the dense input, so with the
   // side stream it runs there beside the pooled lookups (latency-bound small
@@ -864,7 +907,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                     n, s0, s));
   HIPRET(end(LATTICE_STAGE_EMBBAG_FWD));
   // fork: the sort and run bookkeeping go to the side stream, overlapping
-  // the dense stages; the lock is held until the join is enqueued
+  // the dense stages
   if (side) {
     HIPRET(hipEventRecord(side->fork_fwd, s));
     HIPRET(hipStreamWaitEvent(side->s, side->fork_fwd, 0));
@@ -985,10 +1028,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
                           (const int*)at(L.sorted_bags), (float*)at(L.grad_rows), m->tables.data,
                           dt, opts->lr_tables, sparse, s, stage_ev(LATTICE_STAGE_EMBBAG_REDUCE)));
   // join: the caller's stream passes this point after all of the step's work
-  if (side) {
-    HIPRET(hipStreamWaitEvent(s, side->done, 0));
-    lock.unlock();
-  }
+  if (side) HIPRET(hipStreamWaitEvent(s, side->done, 0));
   return LATTICE_OK;
 }
 

@@ -3,6 +3,10 @@ import numpy as np
 import torch
 
 import synth
+from oracle import bounds as obounds
+from oracle import embbag as oembbag
+from oracle import interact as ointeract
+from oracle import loss as oloss
 from oracle import mlp as omlp
 from oracle import step as ostep
 from oracle.metrics import max_rel_err, max_rel_err_normwise
@@ -22,22 +26,264 @@ def assert_close(name, got, ref, t):
     assert err <= t, f"{name}: max_rel_err {err} > {t}"
 
 
-def assert_close_composed(name, got, ref, t, strict_bound=None):
-    """Comparison of a tensor produced by a composed (multi-stage) bf16
-    computation: the normwise max relative error must meet t; the element-wise
-    row-rms metric must stay under strict_bound (a sanity bound against
-    localised bugs; default 3t).  fp32 workloads use the strict metric at t."""
-    got = got.detach().float().cpu().numpy() if torch.is_tensor(got) else np.asarray(got)
-    strict = max_rel_err(got, ref)
+def _np64(x):
+    if torch.is_tensor(x):
+        return x.detach().float().cpu().double().numpy()
+    return np.asarray(x, np.float64)
+
+
+def _row_floor(ref):
+    """max(|r|, rms of r's last-axis row), the element-wise metric's scale."""
+    rr = ref.reshape(1, -1) if ref.ndim <= 1 else ref.reshape(-1, ref.shape[-1])
+    rms = np.sqrt(np.mean(rr * rr, axis=-1, keepdims=True))
+    return np.maximum(np.abs(rr), rms).reshape(ref.shape)
+
+
+def assert_close_derived(name, got, ref, e, t):
+    """A tensor of the composed step (downstream of several bf16 storage
+    points), compared element by element: an element passes when it is
+    within t of its reference by the element-wise metric (scale max(|r|,
+    row rms)), or within the accepted deviation ``oracle.bounds.allowed(e)``
+    that the arithmetic itself allows that element (the spread between two
+    correct evaluations that round differently); the normwise error must
+    also meet t.  fp32 workloads: the strict metric at t."""
+    got, ref = _np64(got), np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
     if t <= 1e-5:
-        print(f"  {name}: max_rel_err={strict:.3e} (tol {t:.0e})", flush=True)
-        assert strict <= t, f"{name}: max_rel_err {strict} > {t}"
+        err = max_rel_err(got, ref)
+        print(f"  {name}: max_rel_err={err:.3e} (tol {t:.0e})", flush=True)
+        assert err <= t, f"{name}: max_rel_err {err} > {t}"
         return
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
     norm = max_rel_err_normwise(got, ref)
-    sb = 3 * t if strict_bound is None else strict_bound
-    print(f"  {name}: normwise={norm:.3e} (tol {t:.0e}), element-wise={strict:.3e} (bound {sb:.0e})", flush=True)
+    diff = np.abs(got - ref)
+    strict_ok = diff <= t * _row_floor(ref)
+    acc = obounds.allowed(e)
+    derived_ok = diff <= acc
+    bad = ~(strict_ok | derived_ok)
+    n_der = int(np.count_nonzero(~strict_ok & derived_ok))
+    worst = float(np.max(diff / np.maximum(acc, 1e-300), initial=0.0))
+    print(f"  {name}: normwise={norm:.3e} (tol {t:.0e}); {n_der} of {diff.size} elements beyond "
+          f"{t:.0e} and within the derived deviation (worst |x-r|/allowed {worst:.2f})", flush=True)
     assert norm <= t, f"{name}: normwise max relative error {norm} > {t}"
-    assert strict <= sb, f"{name}: element-wise error {strict} > {sb}"
+    if bad.any():
+        i = np.unravel_index(np.argmax(np.where(bad, diff / np.maximum(acc, 1e-300), 0)), diff.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())} elements outside both the element-wise "
+                             f"tolerance and the derived deviation; worst at {i}: got {got[i]}, "
+                             f"ref {ref[i]}, allowed {acc[i]}")
+
+
+def assert_product(name, got, ref, absref, K, storage_unit=None, t=2e-2):
+    """One stage recomputed by the oracle from the accelerator's own stored
+    operands: ``ref`` is the exact result, ``absref`` the same product of
+    absolute values and ``K`` the number of terms per element.  An fp32 sum
+    of K terms in any order is within (K+3) 2^-24 absref of the exact value
+    (bf16 x bf16 products are exact in fp32); a result stored at storage
+    unit ``us`` adds one rounding, us (|ref| + that).  Every element must
+    meet this bound, and the tensor the element-wise metric at t."""
+    got, ref, absref = _np64(got), np.asarray(ref, np.float64), np.asarray(absref, np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    acc = (K + 3) * 2.0 ** -24 * absref
+    bound = acc + (storage_unit * (np.abs(ref) + acc) if storage_unit else 0.0) + 1e-37
+    ratio = float(np.max(np.abs(got - ref) / bound, initial=0.0))
+    err = max_rel_err(got, ref)
+    print(f"  {name} [stage]: max_rel_err={err:.3e} (tol {t:.0e}), worst |x-r|/bound={ratio:.3f}", flush=True)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    assert ratio <= 1.0, f"{name}: outside the fp32 accumulation bound (ratio {ratio})"
+    assert err <= t, f"{name}: max_rel_err {err} > {t}"
+
+
+def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None):
+    """Stage-wise parity of one step: every stage recomputed in float64 by
+    the oracle from the accelerator's own stored inputs of that stage, so the
+    only admissible difference is that stage's own arithmetic.  v: the step's
+    workspace views; grads: the accelerator's parameter gradients (dict:
+    top_dW/top_db/bottom_dW/bottom_db lists, fm_dW, stack list of dicts);
+    rows (optional): samples for the per-sample stages (all if None);
+    wgrad_rows (optional): dict ("top"|"bottom", layer) -> output rows of
+    that weight gradient to recompute over the whole batch (all if absent).
+    Sample-summed interaction gradients are checked when rows is None."""
+    us = 2.0 ** -8 if cfg.dtype == "bf16" else None
+    t = tol(cfg)
+    B, d = cfg.B, cfg.d
+    R = np.arange(B) if rows is None else np.asarray(rows)
+    wr = wgrad_rows or {}
+    L = len(params["top"])
+    tin = _np64(v["t"][:, :cfg.top_in])
+    h_top = [tin] + [_np64(a) for a in v["top_act"]]
+    g_top = [_np64(g) for g in v["top_grad"]]
+    # top MLP forward, layer by layer from the stored inputs
+    for i, (W, b) in enumerate(params["top"]):
+        W, b = np.asarray(W, np.float64), np.asarray(b, np.float64)
+        h = h_top[i][R]
+        a = h @ W.T + b
+        ab = np.abs(h) @ np.abs(W).T + np.abs(b)
+        if i < L - 1:
+            assert_product(f"top{i} forward", h_top[i + 1][R], np.maximum(a, 0), ab, W.shape[1] + 1, us, t)
+        else:
+            assert_product("logits", _np64(v["logits"])[R], a, ab, W.shape[1] + 1, None, t)
+    # loss and dz from the stored logits
+    z = _np64(v["logits"])
+    N = max(1.0, float(np.asarray(batch["mask"]).sum()))
+    L_ref, dz_ref = oloss.masked_bce(z, batch["labels"], batch["mask"], N)
+    e_loss = max_rel_err(_np64(v["loss"]), np.array([L_ref]))
+    e_dz = max_rel_err(_np64(v["d_logits"]), dz_ref)
+    print(f"  loss [stage]: {e_loss:.3e}; d_logits [stage]: {e_dz:.3e} (tol 1e-5)", flush=True)
+    assert e_loss <= 1e-5 and e_dz <= 1e-5
+    # the gradient chain: g_{i-1} = (g_i W_i) masked by the stored h_i > 0
+    for i in range(L - 1, -1, -1):
+        W = np.asarray(params["top"][i][0], np.float64)
+        prod = g_top[i][R] @ W
+        ab = np.abs(g_top[i][R]) @ np.abs(W)
+        if i > 0:
+            on = h_top[i][R] > 0
+            assert_product(f"top{i} grad chain", g_top[i - 1][R], prod * on, ab * on, W.shape[0], us, t)
+        else:
+            assert_product("d_t", tin_grad(v, cfg)[R], prod, ab, W.shape[0], us, t)
+    # weight and bias gradients from the stored chain and activations
+    for i in range(L):
+        r = wr.get(("top", i), slice(None))
+        gi, hi = g_top[i][:, r], h_top[i]
+        assert_product(f"top{i}.dW", _np64(grads["top_dW"][i])[r], gi.T @ hi, np.abs(gi).T @ np.abs(hi),
+                       B, None, t)
+        assert_product(f"top{i}.db", _np64(grads["top_db"][i])[r], gi.sum(0), np.abs(gi).sum(0), B, None, t)
+    X = _np64(v["X"])
+    dX = _np64(v["dX"])
+    gt = tin_grad(v, cfg)
+    if cfg.has_dense:
+        hb = [_np64(batch["dense"])] + [_np64(a) for a in v["bottom_act"]] + [X[:, 0]]
+        gb = [_np64(g) for g in v["bottom_grad"]]
+        nb = len(params["bottom"])
+        for i, (W, b) in enumerate(params["bottom"]):
+            W, b = np.asarray(W, np.float64), np.asarray(b, np.float64)
+            a = hb[i][R] @ W.T + b
+            assert_product(f"bottom{i} forward", hb[i + 1][R], np.maximum(a, 0),
+                           np.abs(hb[i][R]) @ np.abs(W).T + np.abs(b), W.shape[1] + 1, us, t)
+        # the bottom output's gradient is the stored slot-0 gradient, masked
+        assert np.array_equal(gb[nb - 1], dX[:, 0] * (X[:, 0] > 0)), "bottom output gradient"
+        for i in range(nb - 1, 0, -1):
+            W = np.asarray(params["bottom"][i][0], np.float64)
+            on = hb[i][R] > 0
+            assert_product(f"bottom{i} grad chain", gb[i - 1][R], (gb[i][R] @ W) * on,
+                           (np.abs(gb[i][R]) @ np.abs(W)) * on, W.shape[0], us, t)
+        for i in range(nb):
+            r = wr.get(("bottom", i), slice(None))
+            assert_product(f"bottom{i}.dW", _np64(grads["bottom_dW"][i])[r], gb[i][:, r].T @ hb[i],
+                           np.abs(gb[i][:, r]).T @ np.abs(hb[i]), B, None, t)
+            assert_product(f"bottom{i}.db", _np64(grads["bottom_db"][i])[r], gb[i][:, r].sum(0),
+                           np.abs(gb[i][:, r]).sum(0), B, None, t)
+    # the interaction, forward and backward, from the stored X and d_t
+    rnd = ostep.rounding(cfg.dtype)
+    u_ = us or 2.0 ** -24
+    off = d if cfg.has_dense else 0
+    Xs, gts, ts, dXs = X[R], gt[R], tin[R], dX[R]
+    head = np.zeros_like(Xs)                  # the top input's slot-0 gradient enters dX[:, 0]
+    if cfg.has_dense:
+        head[:, 0] = gts[:, :d]
+    zero = lambda x: (np.zeros(x.shape), np.zeros(x.shape))
+    if cfg.interact == "dot":
+        n = cfg.n_slots
+        i_, j_ = ointeract.pair_indices(n)
+        G = Xs @ Xs.transpose(0, 2, 1)
+        aG = np.abs(Xs) @ np.abs(Xs).transpose(0, 2, 1)
+        assert_product("interaction forward", ts[:, off:], G[:, i_, j_], aG[:, i_, j_], d, us, t)
+        S = np.zeros((Xs.shape[0], n, n))
+        S[:, i_, j_] = gts[:, off:]
+        S[:, j_, i_] = gts[:, off:]
+        assert_product("interaction backward dX", dXs, S @ Xs + head,
+                       np.abs(S) @ np.abs(Xs) + np.abs(head), n + 1, us, t)
+    elif cfg.interact == "fm":
+        W = np.asarray(params["fm_W"], np.float64)
+        n, k = cfg.n_slots, cfg.fm_rank
+        O, P = ointeract.fm_forward(Xs, W, rnd)
+        eP, eO = obounds._fm_forward_bounds(Xs, zero(Xs), W, P, O, u_)
+        nr = O.shape[0]
+        assert_close_derived("interaction forward [stage]", ts[:, off:], O.reshape(nr, -1),
+                             (eO[0].reshape(nr, -1), eO[1].reshape(nr, -1)), t)
+        G = gts[:, off:].reshape(-1, n, k)
+        dXr, dWr = ointeract.fm_backward(G, Xs, W, P, rnd)
+        edX, edW = obounds._fm_backward_bounds(G, zero(G), Xs, zero(Xs), W, P, eP, rnd, u_)
+        full = dXr + head
+        assert_close_derived("interaction backward dX [stage]", dXs, rnd(full), obounds.rounded(edX, full, u_), t)
+        if rows is None:
+            assert_close_derived("fm.dW [stage]", grads["fm_dW"], dWr, edW, t)
+    else:
+        layers = params["stack"]
+        XL, caches = ointeract.stack_forward(Xs, layers, cfg.stack_n, d, rnd, cfg.ln_eps)
+        dY = gts.reshape(-1, cfg.stack_n, d)
+        dX1, sg = ointeract.stack_backward(dY, layers, caches, rnd)
+        e_out, edX, eg = obounds.stack_bounds(Xs, zero(Xs), dY, zero(dY), layers, caches, cfg.dtype)
+        nr = XL.shape[0]
+        assert_close_derived("stack forward [stage]", ts, XL.reshape(nr, -1),
+                             (e_out[0].reshape(nr, -1), e_out[1].reshape(nr, -1)), t)
+        assert_close_derived("stack backward dX [stage]", dXs, rnd(dX1), obounds.rounded(edX, dX1, u_), t)
+        if rows is None:
+            for l, (gl, el) in enumerate(zip(sg, eg)):
+                for key in gl:
+                    assert_close_derived(f"stack{l}.{key} [stage]", grads["stack"][l][key], gl[key], el[key], t)
+
+
+def tin_grad(v, cfg):
+    """The stored gradient of the top input."""
+    return _np64(v["d_t"][:, :cfg.top_in])
+
+
+def grads_of(w):
+    """The accelerator's parameter gradients of a Workload, by name."""
+    g = dict(top_dW=[L["dW"] for L in w.top], top_db=[L["db"] for L in w.top],
+             bottom_dW=[L["dW"] for L in w.bottom], bottom_db=[L["db"] for L in w.bottom],
+             fm_dW=w.fm_dW)
+    if w.stack is not None:
+        g["stack"] = [{k: lay[k] for k in ("dW", "dA", "dgamma", "dC") if lay.get(k) is not None}
+                      for lay in w.stack]
+    return g
+
+
+def check_sparse_stage(cfg, batch, v, nnz, E0=None, E1=None, lr=0.0, t=None, sample=None, bk=None):
+    """The sparse gradient from the accelerator's own stored dX: integer
+    bookkeeping bit-exact, every row gradient within the fp32 sum bound of
+    its occurrences, and (with SGD) every updated row within one rounding of
+    E0 - lr G on the accelerator's own G; rows that do not occur unchanged.
+    sample (optional): indices into the unique rows to recompute (all if
+    None); E0 / E1 are then the rows of those samples before / after."""
+    t = tol(cfg) if t is None else t
+    B, F = cfg.B, cfg.F
+    s0 = cfg.first_emb_slot
+    if bk is None:
+        bk = oembbag.bookkeeping(batch["row_base"], batch["offsets"], batch["indices"], F, B)
+    U = int(v["num_unique"].item())
+    assert U == bk["unique_rows"].size
+    np.testing.assert_array_equal(v["unique_rows"][:U].cpu().numpy(), bk["unique_rows"])
+    np.testing.assert_array_equal(v["seg_offsets"][:U + 1].cpu().numpy(), np.append(bk["seg_offsets"], nnz))
+    np.testing.assert_array_equal(v["sorted_bags"][:nnz].cpu().numpy(), bk["sorted_bags"])
+    if U == 0:
+        return
+    u_idx = np.arange(U) if sample is None else np.asarray(sample)
+    counts, seg = bk["counts"][u_idx], bk["seg_offsets"][u_idx]
+    occ = np.concatenate([np.arange(a, a + c) for a, c in zip(seg, counts)])
+    bags = bk["sorted_bags"][occ]
+    f, b = bags // B, bags % B
+    lens = np.diff(np.asarray(batch["offsets"], np.int64))
+    dX = v["dX"]
+    sel_b = torch.from_numpy(b).to(dX.device)
+    sel_s = torch.from_numpy(s0 + f).to(dX.device)
+    contrib = _np64(dX[sel_b, sel_s])
+    if cfg.pool == "mean":
+        contrib = contrib / lens[bags][:, None]
+    starts = np.concatenate([[0], np.cumsum(counts)[:-1]])
+    G = np.add.reduceat(contrib, starts, axis=0)
+    aG = np.add.reduceat(np.abs(contrib), starts, axis=0)
+    Gg = _np64(v["grad_rows"][torch.from_numpy(u_idx).to(dX.device)])
+    assert_product("grad_rows", Gg, G, aG, counts.astype(np.float64)[:, None] + 1, None, t)
+    if lr and E0 is not None:
+        us = 2.0 ** -8 if cfg.dtype == "bf16" else 2.0 ** -24
+        E0 = np.asarray(E0, np.float64)
+        ref = E0 - lr * Gg                      # on the accelerator's own G
+        got = np.asarray(E1, np.float64)
+        bound = 2 * us * np.abs(ref) + 4 * 2.0 ** -24 * (np.abs(E0) + abs(lr) * np.abs(Gg))
+        flips = int(np.count_nonzero(got != ostep.rounding(cfg.dtype)(ref)))
+        print(f"  updated rows [stage]: {flips} of {got.size} elements rounded the other way", flush=True)
+        assert np.all(np.abs(got - ref) <= bound + 1e-37)
 
 
 def to_dev(x, dtype=None):

@@ -109,15 +109,24 @@ SAMPLED = {"large-emb-fm": synth.LARGE_FM, "multidomain-dot": synth.MULTIDOMAIN,
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("name", list(SAMPLED))
-def test_fullsize_step_per_sample(name):
+def test_fullsize_step(name):
     """lattice_step at a workload's full size as the benchmark runs it (with
-    its SGD step, if any): full bookkeeping bit-exact; per-sample forward and
-    backward outputs, and the row gradients (and SGD updates) of cold rows,
-    each recomputed by the oracle on the samples involved (with the full
-    batch's loss normaliser)."""
+    its SGD step, if any).  (1) Full bookkeeping bit-exact.  (2) Every stage
+    recomputed by the oracle from the accelerator's own stored inputs over the
+    whole batch: MLP forward and gradient chain, every dense weight and bias
+    gradient (top, bottom, FM), the interaction forward / backward, and
+    sampled row gradients and SGD updates; for the deep stack (16384
+    samples) the per-sample stages on sampled samples and sampled output rows
+    of the two largest weight gradients.  (3) The composed step per sample:
+    forward and backward outputs and the row gradients (and SGD updates) of
+    cold rows, recomputed by the oracle on the samples involved (with the full
+    batch's loss normaliser), within the element-wise tolerance or the derived
+    deviation."""
+    from oracle import bounds as obounds
     from oracle import step as ostep
     from paper_2512_09200_amd import api
-    from tests._util import Workload, assert_close_composed, relu_overrides
+    from tests._util import (Workload, assert_close_derived, check_sparse_stage, check_stages, grads_of,
+                             relu_overrides)
     cfg = SAMPLED[name]
     lr = cfg.lr_tables
     print(f"[fullsize-step] {name}: generating inputs", flush=True)
@@ -127,30 +136,43 @@ def test_fullsize_step_per_sample(name):
                           bottom=w.bottom, top=w.top, interact=cfg.interact, fm_W=w.fm_W,
                           fm_dW=w.fm_dW, pool=cfg.pool, stack=w.stack, stack_n=cfg.stack_n,
                           ln_eps=cfg.ln_eps, max_rows=cfg.rows)
+    print("[fullsize-step] oracle bookkeeping", flush=True)
     bk = oe.bookkeeping(b["row_base"], b["offsets"], b["indices"], cfg.F, cfg.B)
     uniq, counts, seg = bk["unique_rows"], bk["counts"], bk["seg_offsets"]
     r = np.random.default_rng(2)
     cold_u = r.choice(np.flatnonzero(counts <= 2), 40, replace=False)
+    sample_u = np.unique(np.concatenate([r.choice(uniq.size, 3000, replace=False), cold_u,
+                                         np.argsort(counts)[-20:], [0, uniq.size - 1]]))
     occ_bags = np.concatenate([bk["sorted_bags"][seg[u]: seg[u] + counts[u]] for u in cold_u])
     probe = r.choice(cfg.B, 6, replace=False)
     samples = np.unique(np.concatenate([probe, occ_bags % cfg.B]))
-    E_cold_before = _rows(w.E, uniq[cold_u])
-    # the oracle's inputs: the involved samples and their table rows before the step
+    E_sample_before = _rows(w.E, uniq[sample_u])
+    untouched = r.integers(0, cfg.F * cfg.rows, 4000)
+    untouched = untouched[~np.isin(untouched, uniq)][:500]
+    E_untouched = _rows(w.E, untouched)
+    # the oracle's inputs for the composed check: the involved samples and
+    # their table rows before the step
     scfg, sub, grows = synth.sub_batch(cfg, b, samples)
     table = _rows(w.E, grows)
-    pos = {int(g): i for i, g in enumerate(grows)}
+    pos = {int(gr): i for i, gr in enumerate(grows)}
     lay = api.lattice_step_plan(model, cfg.B, w.nnz, lr, True)
     ws = torch.zeros(lay.total_bytes, dtype=torch.uint8, device=DEV)
-    print(f"[fullsize-step] workspace {lay.total_bytes / 2**30:.2f} GiB; {samples.size} samples checked", flush=True)
-    api.lattice_step(model, w.offsets, w.indices, w.dense, w.labels, w.mask, ws, lr, True)
+    print(f"[fullsize-step] workspace {lay.total_bytes / 2**30:.2f} GiB", flush=True)
+    api.lattice_step(model, w.offsets, w.indices, w.dense, w.labels, w.mask, ws, lr, True,
+                     side=api.SideStream())
     torch.cuda.synchronize()
     v = api.step_views(model, ws, lay, cfg.B, cfg.T, w.nnz)
-    U = int(v["num_unique"].item())
-    print(f"[fullsize-step] num_unique GPU {U} oracle {uniq.size}", flush=True)
-    assert U == uniq.size
-    np.testing.assert_array_equal(v["unique_rows"][:U].cpu().numpy(), uniq)
-    np.testing.assert_array_equal(v["seg_offsets"][:U + 1].cpu().numpy(), np.append(seg, w.nnz))
-    np.testing.assert_array_equal(v["sorted_bags"][:w.nnz].cpu().numpy(), bk["sorted_bags"])
+
+    print("[fullsize-step] stages on the accelerator's own inputs", flush=True)
+    big = cfg.B > 8192
+    rows = r.choice(cfg.B, 64, replace=False) if big else None
+    wrows = ({("top", 0): r.choice(cfg.top[0], 64, replace=False)} if big else None)
+    check_stages(cfg, w.params, b, v, grads_of(w), rows=rows, wgrad_rows=wrows)
+    check_sparse_stage(cfg, b, v, w.nnz, E_sample_before if lr else None,
+                       _rows(w.E, uniq[sample_u]) if lr else None, lr, sample=sample_u, bk=bk)
+    assert np.array_equal(_rows(w.E, untouched), E_untouched), "untouched rows changed"
+
+    print(f"[fullsize-step] composed step on {samples.size} samples", flush=True)
     sel = torch.from_numpy(samples).to(DEV)
     gin = dict(bottom=([w.dense[sel]] + [a[sel] for a in v["bottom_act"]]) if cfg.has_dense else [],
                top=[v["t"][sel, :cfg.top_in]] + [a[sel] for a in v["top_act"]])
@@ -158,24 +180,21 @@ def test_fullsize_step_per_sample(name):
                 top=[a[sel] for a in v["top_act"]])
     N = float(b["mask"].sum())
     ov, nb, nf = relu_overrides(scfg, w.params, table, sub, gin, gout)
-    print(f"[fullsize-step] oracle on {samples.size} samples", flush=True)
     c, g = ostep.step(scfg, w.params, table, sub, lr_tables=0.0, overrides=ov, loss_normalizer=N)
+    bd = obounds.step_bounds(scfg, w.params, table, sub, c, g, lr_tables=0.0, loss_normalizer=N)
     print(f"  ReLU band {nb}, taken the other way {nf}", flush=True)
     s0 = cfg.first_emb_slot
     assert_close("X[emb] (sampled)", v["X"][sel, s0:], c["X"][:, s0:], 2e-2)
-    for nm, got, ref in [("X", v["X"][sel], c["X"]), ("t", v["t"][sel, :cfg.top_in], c["t"]),
-                         ("logits", v["logits"][sel], c["logits"]),
-                         ("d_logits", v["d_logits"][sel], c["dz"]),
-                         ("d_t", v["d_t"][sel, :cfg.top_in], g["d_top_in"])]:
-        assert_close_composed(nm + " (sampled)", got, ref, 2e-2)
-    assert_close_composed("dX_emb (sampled)", v["dX"][sel, s0:], g["dX_emb"], 2e-2,
-                          strict_bound=0.1 if cfg.interact == "stack" else None)
+    for nm, got, ref, e in [("X", v["X"][sel], c["X"], bd["X"]),
+                            ("t", v["t"][sel, :cfg.top_in], c["t"], bd["t"]),
+                            ("logits", v["logits"][sel], c["logits"], bd["logits"]),
+                            ("d_logits", v["d_logits"][sel], c["dz"], bd["dz"]),
+                            ("d_t", v["d_t"][sel, :cfg.top_in], g["d_top_in"], bd["d_top_in"]),
+                            ("dX_emb", v["dX"][sel, s0:], g["dX_emb"], bd["dX_emb"])]:
+        assert_close_derived(nm + " (sampled)", got, ref, e, 2e-2)
     # cold rows: every occurrence's sample is in the sub-batch, so the oracle's G is exact
-    Gref = np.stack([g["grad_rows"][np.searchsorted(g["unique_rows"], pos[int(uniq[u])])] for u in cold_u])
-    assert_close_composed("cold grad_rows", v["grad_rows"][torch.from_numpy(cold_u).to(DEV)], Gref, 2e-2,
-                          strict_bound=0.1 if cfg.interact == "stack" else None)
-    if lr:
-        assert_close_composed("cold updated rows", _rows(w.E, uniq[cold_u]),
-                              oe.sgd_rows(E_cold_before, Gref, lr, round_bf16), 2e-2)
+    ci = np.array([np.searchsorted(g["unique_rows"], pos[int(uniq[u])]) for u in cold_u])
+    assert_close_derived("cold grad_rows", v["grad_rows"][torch.from_numpy(cold_u).to(DEV)],
+                         g["grad_rows"][ci], (bd["grad_rows"][0][ci], bd["grad_rows"][1][ci]), 2e-2)
     del w, ws
     torch.cuda.empty_cache()
