@@ -133,6 +133,26 @@ lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_ja
                                   const lattice_sparse_grad* out, float lr,
                                   void* ws, size_t ws_bytes, void* stream);
 
+/* The same computation as lattice_embbag_bwd, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving or
+ * training loops, harnesses that forbid allocation): no workspace argument
+ * and no hipMalloc / hipFree or other allocating call.  The scratch lives in
+ * one device array of LATTICE_NOALLOC_SCRATCH_BYTES per GPU, part of the
+ * library's code object, held until the process ends; its address is looked
+ * up once per device on the first call there.  Every call on a GPU shares
+ * that GPU's array: calls that overlap on one GPU (concurrent streams or
+ * threads) race and give undefined results; calls ordered on one stream are
+ * fine (the kernels clear what they need).  Errors: as lattice_embbag_bwd,
+ * plus UNSUPPORTED when the batch needs more scratch than the array holds
+ * (lattice_embbag_bwd_workspace(...) > LATTICE_NOALLOC_SCRATCH_BYTES: about
+ * 16.1M lookups at dim 128 and 64 features) and HIP if the address lookup
+ * fails. */
+#define LATTICE_NOALLOC_SCRATCH_BYTES (256u << 20)
+lattice_status lattice_embbag_bwd_noalloc(const lattice_tables* tables, const lattice_jagged* bags,
+                                          lattice_pool pool, const void* dX, lattice_dtype dx_dtype,
+                                          int32_t n_slots, int32_t first_slot,
+                                          const lattice_sparse_grad* out, float lr, void* stream);
+
 /* Synchronous check of a batch against the tables: offsets[0] == 0,
  * non-decreasing, offsets[F*B] == nnz, 0 <= indices[j] < rows of its
  * table, and (if max_rows != 0) no table has more than max_rows rows.

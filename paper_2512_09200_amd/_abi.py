@@ -12,6 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liblattice.so")
 
 MAX_LAYERS = 8
+NOALLOC_SCRATCH_BYTES = 256 << 20
 F32, BF16 = 0, 1
 POOL_SUM, POOL_MEAN = 0, 1
 DOT, FM, STACK = 0, 1, 2
@@ -105,6 +106,9 @@ _SIGS = [
     ("lattice_embbag_bwd", c_int, [POINTER(lattice_tables), POINTER(lattice_jagged), c_int, c_void_p,
                                    c_int, c_int32, c_int32, POINTER(lattice_sparse_grad), c_float,
                                    c_void_p, c_size_t, c_void_p]),
+    ("lattice_embbag_bwd_noalloc", c_int, [POINTER(lattice_tables), POINTER(lattice_jagged), c_int,
+                                           c_void_p, c_int, c_int32, c_int32,
+                                           POINTER(lattice_sparse_grad), c_float, c_void_p]),
     ("lattice_validate_batch", c_int, [POINTER(lattice_tables), POINTER(lattice_jagged),
                                        POINTER(c_int64), c_void_p]),
     ("lattice_interact_workspace", c_size_t, [POINTER(lattice_interact_desc), c_int32]),

@@ -77,6 +77,23 @@ def lattice_embbag_fwd(table, row_base, offsets, indices, F, B, X, first_slot=0,
     return X
 
 
+def lattice_embbag_bwd_noalloc(table, row_base, offsets, indices, F, B, dX, out, first_slot=0, lr=0.0,
+                               pool="sum", stream=None, max_rows=None):
+    """lattice_embbag_bwd without a workspace (the library's own per-GPU
+    scratch array); out: dict of preallocated output tensors as returned by
+    lattice_embbag_bwd (unique_rows, seg_offsets, sorted_bags, num_unique,
+    grad_rows or None).  Allocates nothing."""
+    _contig(dX)
+    lib = load()
+    t, j = _tables(table, row_base, max_rows), _jagged(offsets, indices, F, B)
+    sg = A.lattice_sparse_grad(*(o.data_ptr() if o is not None else None for o in
+                                 (out["unique_rows"], out["seg_offsets"], out["sorted_bags"],
+                                  out["num_unique"], out.get("grad_rows"))))
+    check(lib.lattice_embbag_bwd_noalloc(byref(t), byref(j), _POOL[pool], _p(dX), _dt(dX), dX.shape[1],
+                                         first_slot, byref(sg), float(lr), _stream(stream)))
+    return out
+
+
 def lattice_embbag_bwd(table, row_base, offsets, indices, F, B, dX, first_slot=0, lr=0.0,
                        pool="sum", emit_grad_rows=True, stream=None, max_rows=None):
     """Returns dict(unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows); with lr != 0

@@ -177,6 +177,80 @@ lattice_status lattice_embbag_bwd(const lattice_tables* tables, const lattice_ja
   return LATTICE_OK;
 }
 
+// ---------------------------------------------------------------------------
+// The sparse gradient without a caller workspace: its scratch (sort buffers,
+// run bookkeeping, partial sums of runs crossing reduction ranges) is one
+// file-scope device array per GPU, held until the process ends.  In host
+// code `scratch` names a host-side stand-in, never the device memory: the
+// device address comes from hipGetSymbolAddress, taken once per device with
+// that device current, and only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[LATTICE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of this device's scratch array (set up on first use).
+lattice_status scratch_of(hipStream_t s, void** out) {
+  hipDevice_t dev = 0;
+  if (s) {
+    if (hipStreamGetDevice(s, &dev) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipStreamGetDevice failed");
+  } else {
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipGetDevice failed");
+    dev = cur;
+  }
+  REQUIRE(dev >= 0 && dev < kMaxScratchDevices, "device %d out of range", (int)dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipGetDevice failed");
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) FAIL(LATTICE_ERR_HIP, "hipSetDevice failed");
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !ptr)
+      FAIL(LATTICE_ERR_HIP, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return LATTICE_OK;
+}
+}  // namespace
+
+lattice_status lattice_embbag_bwd_noalloc(const lattice_tables* tables, const lattice_jagged* bags,
+                                          lattice_pool pool, const void* dX, lattice_dtype dx_dtype,
+                                          int32_t n_slots, int32_t first_slot,
+                                          const lattice_sparse_grad* out, float lr, void* stream) {
+  lattice_status st = check_tables(tables, bags);
+  if (st != LATTICE_OK) return st;
+  REQUIRE(out && out->unique_rows && out->seg_offsets && out->sorted_bags && out->num_unique,
+          "null sparse-gradient output");
+  REQUIRE(dx_dtype == LATTICE_F32 || dx_dtype == LATTICE_BF16, "bad dX dtype");
+  REQUIRE(pool == LATTICE_POOL_SUM || pool == LATTICE_POOL_MEAN, "bad pool mode");
+  REQUIRE(first_slot >= 0 && first_slot + bags->num_features <= n_slots, "slots out of range");
+  if (bags->nnz > 0) REQUIRE(dX, "null dX");
+  if ((int64_t)bags->batch * n_slots * tables->dim * (int64_t)esize(dx_dtype) > (int64_t)UINT32_MAX)
+    FAIL(LATTICE_ERR_UNSUPPORTED, "dX larger than 4 GiB");
+  const size_t need = embbag_bwd_workspace(bags->nnz, tables->dim, bags->num_features);
+  if (need > (size_t)LATTICE_NOALLOC_SCRATCH_BYTES)
+    FAIL(LATTICE_ERR_UNSUPPORTED,
+         "the sparse gradient of %lld lookups (dim %d, %d features) needs %zu bytes of scratch; "
+         "the allocation-free entry point holds %zu (use lattice_embbag_bwd with a workspace)",
+         (long long)bags->nnz, tables->dim, bags->num_features, need,
+         (size_t)LATTICE_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  st = scratch_of(strm(stream), &ws);
+  if (st != LATTICE_OK) return st;
+  HIPRET(embbag_bwd(tables->row_base, local_rows_bound(tables), bags->offsets, bags->indices,
+                    bags->num_features, bags->batch, bags->nnz, pool == LATTICE_POOL_MEAN, dX,
+                    dt_of(dx_dtype), n_slots, first_slot, tables->dim, out->unique_rows,
+                    out->seg_offsets, out->sorted_bags, out->num_unique, out->grad_rows,
+                    tables->data, dt_of(tables->dtype), lr, ws, strm(stream)));
+  return LATTICE_OK;
+}
+
 __device__ unsigned long long g_validate_result[2];
 static std::mutex g_validate_mu;
 
