@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--uniform", action="store_true", help="uniform indices (control run)")
     ap.add_argument("--single-stream", action="store_true",
                     help="no side stream: every stage on the step's stream (no overlap)")
+    ap.add_argument("--fp8", choices=["precise", "fast"], default=None,
+                    help="mixed FP8/BF16 training: the top MLP's hidden-layer forward GEMMs in FP8 e4m3 "
+                         "(row-wise scales) with fast accumulation off (precise) or on (fast)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, stream 1 GiB through a plain elementwise kernel "
                          "(torch.neg, 1 GiB read + 1 GiB written) as a counter calibration point")
@@ -113,7 +116,7 @@ def main():
                           bottom=bottom, top=top, interact=cfg.interact, fm_W=fm_W, fm_dW=fm_dW,
                           pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps)
     nnz_max = max(b["nnz"] for b in batches)
-    lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False)
+    lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False, fp8_top=args.fp8)
     ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     log(f"[bench] inputs resident ({time.time() - t0:.1f}s); workspace {lay.total_bytes / 2**30:.2f} GiB")
@@ -124,7 +127,7 @@ def main():
         b = batches[i % len(batches)]
         api.lattice_step(model, b["offsets"], b["indices"], b["dense"], b["labels"], b["mask"], ws,
                          cfg.lr_tables, False, stage_events=events, nnz_capacity=nnz_max,
-                         side=None if one_stream else side)
+                         side=None if one_stream else side, fp8_top=args.fp8)
 
     for i in range(args.warmup):
         step(i)
@@ -262,7 +265,8 @@ def main():
         "metric": "train samples/s (fwd+bwd) at 1 GPU; EmbBag HBM GB/s and interaction MFMA util",
         "value": round(samples_per_s, 1), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype if not args.fp8 else f"{cfg.dtype}+fp8-e4m3(top hidden fwd, {args.fp8} accumulation)",
         "data": "synthetic (seeded; Zipf/Poisson jagged batches, random-init weights)",
         "config": {"workload": cfg.name, "global_batch": cfg.B, "features": cfg.F,
                    "rows_per_table": cfg.rows, "dim": cfg.d,
@@ -270,6 +274,7 @@ def main():
                    "interaction": cfg.interact, "top": list(cfg.top), "lr_tables": cfg.lr_tables,
                    "nnz_per_step": int(nnz), "distinct_rows_per_step": int(U),
                    "batches_cycled": len(batches), "parallelism": "single-gpu",
+                   "fp8_top": args.fp8,
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,
         "gather_roofline": gather_roofline,

@@ -276,6 +276,51 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
                                      void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* FP8 linear layers (Section 3.5.2)                                        */
+/* ------------------------------------------------------------------------ */
+
+/* Linear-layer GEMMs in FP8 with tensor-wise or row-wise scales (not
+ * block-wise), the format the paper uses for FP8 training and inference;
+ * normalisation stays in fp32.  The FP8 format is OCP e4m3 (bias 7, largest
+ * finite value 448, no infinities). */
+typedef enum {
+  LATTICE_FP8_ROWWISE = 0,     /* one scale per row of the matrix */
+  LATTICE_FP8_TENSORWISE = 1   /* one scale for the whole matrix */
+} lattice_fp8_scaling;
+
+/* Quantise x [rows, cols] (row stride ld elements, bf16 or fp32): s = amax /
+ * 448 over each row (ROWWISE, scales [rows]) or over the matrix (TENSORWISE,
+ * scales [1]), s = 1 where the amax is 0; q = e4m3(x * (1 / s)), with s, 1 / s
+ * and the product in fp32 (correctly rounded) and the product rounded to the
+ * nearest e4m3 value, ties to even, saturating at +-448 (x must be finite).  q is [rows, ldq] bytes,
+ * ldq a multiple of 16 and >= cols, 16-byte aligned; bytes cols .. ldq-1 of
+ * each row are written as 0.  TENSORWISE needs a workspace of
+ * lattice_fp8_quantize_workspace() bytes.  Errors: INVALID_ARG, WORKSPACE,
+ * HIP. */
+size_t lattice_fp8_quantize_workspace(void);
+lattice_status lattice_fp8_quantize(const void* x, lattice_dtype x_dtype, int64_t rows, int64_t cols,
+                                    int64_t ld, lattice_fp8_scaling scaling, uint8_t* q, int64_t ldq,
+                                    float* scales, void* ws, size_t ws_bytes, void* stream);
+
+/* Y[m, n] = act((sum_k qA[m,k] qW[n,k]) * sA[m or 0] * sW[n or 0] + bias[n]):
+ * a linear layer Y = X W^T + b on quantised X [M, K] and W [N, K] (codes from
+ * lattice_fp8_quantize, row strides lda / ldw bytes: multiples of 16, >= K
+ * rounded up to 16, 16-byte aligned).  The matrix instruction adds 64
+ * products and its incoming partial sum after aligning them to the largest
+ * exponent among them with about 13 fraction bits.  fast_accum = 1 chains
+ * the partial sum through all of K (fastest; low bits are lost relative to
+ * the running sum: inference); fast_accum = 0 starts every 64-k instruction
+ * from zero and adds the partial sums in fp32 (training).  The sum is scaled by sA then
+ * sW, in fp32.  bias may be NULL; relu != 0 applies ReLU; Y is [M, ldy] in
+ * y_dtype (bf16 rounded to nearest even).  Errors: INVALID_ARG, HIP. */
+lattice_status lattice_linear_fp8_fwd(const uint8_t* qA, int64_t lda, const float* sA,
+                                      lattice_fp8_scaling a_scaling, const uint8_t* qW, int64_t ldw,
+                                      const float* sW, lattice_fp8_scaling w_scaling,
+                                      const float* bias, int32_t M, int32_t N, int32_t K,
+                                      int32_t relu, int32_t fast_accum, void* Y,
+                                      lattice_dtype y_dtype, int64_t ldy, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Whole training step                                                      */
 /* ------------------------------------------------------------------------ */
 
@@ -351,6 +396,15 @@ typedef struct {
   void* side_stream;           /* hipStream_t or NULL (see above) */
   void* const* side_events;    /* host array of LATTICE_STEP_SIDE_EVENTS hipEvent_t;
                                   required when side_stream is used */
+  int32_t fp8_top;             /* mixed FP8 / BF16 training (Section 3.5.2), bf16 models:
+                                  0 = off; 1 = the forward GEMMs of the top MLP's hidden
+                                  layers in FP8 e4m3 with row-wise scales (inputs per
+                                  sample, weights per output unit, quantised every step)
+                                  and fast accumulation off; 2 = the same with fast
+                                  accumulation on.  The objective heads, every backward
+                                  GEMM and all stored activations stay bf16; the
+                                  gradients treat quantisation as the identity.  Plan
+                                  and step must use the same value. */
 } lattice_step_opts;
 
 /* Byte offsets of every intermediate inside the step workspace (-1: absent). */
@@ -379,6 +433,8 @@ typedef struct {
   int64_t scratch_bytes;
   int64_t sparse;       /* scratch of the sparse gradient (sort, runs, reduction) */
   int64_t sparse_bytes;
+  int64_t fp8;          /* e4m3 codes and scales of the FP8 forward (fp8_top), or -1 */
+  int64_t fp8_bytes;
 } lattice_step_layout;
 
 /* Workspace layout for batches of B samples and at most

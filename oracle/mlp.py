@@ -13,6 +13,8 @@ activation being positive (ReLU) and stored as ``rnd(...)``.
 """
 import numpy as np
 
+from . import fp8 as _fp8
+
 
 def linear(h, W, b):
     return np.asarray(h, np.float64) @ np.asarray(W, np.float64).T + np.asarray(b, np.float64)
@@ -35,7 +37,16 @@ def relu_band(h, W, b):
     return (K + 1) * 2.0 ** -24 * (h @ np.abs(np.asarray(W, np.float64)).T + np.abs(np.asarray(b, np.float64)))
 
 
-def mlp_forward(h0, layers, rnd, relu_last, overrides=None):
+def linear_fp8(h, W, b):
+    """The FP8 forward of a layer (Section 3.5.2): input rows and weight rows
+    quantised to e4m3 with row-wise scales, their exact product, plus the
+    bias."""
+    qa, sa = _fp8.quantize(h, rowwise=True)
+    qw, sw = _fp8.quantize(W, rowwise=True)
+    return _fp8.linear_fp8(qa, sa, qw, sw, b)
+
+
+def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=()):
     """Returns ``(hs, masks)``: the layer inputs/outputs ``[h0, h1, ..., hL]``
     and, per layer, its ReLU decision (``None`` for a linear last layer).
     Every layer but (optionally) the last applies ReLU and storage rounding.
@@ -44,11 +55,12 @@ def mlp_forward(h0, layers, rnd, relu_last, overrides=None):
     ``where`` the ReLU of layer i takes the decision ``positive`` instead of
     the sign of the float64 pre-activation.  Parity tests use it only inside
     ``relu_band``, where either decision is a correct result of fp32
-    arithmetic."""
+    arithmetic.  Layers listed in ``fp8_layers`` run their forward product
+    in FP8 (``linear_fp8``)."""
     hs = [np.asarray(h0, np.float64)]
     masks = []
     for i, (W, b) in enumerate(layers):
-        a = linear(hs[-1], W, b)
+        a = linear_fp8(hs[-1], W, b) if i in fp8_layers else linear(hs[-1], W, b)
         last = i == len(layers) - 1
         if relu_last or not last:
             on = a > 0

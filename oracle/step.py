@@ -33,11 +33,14 @@ def rounding(dtype):
     return _bf16.round_bf16 if dtype == "bf16" else _bf16.identity
 
 
-def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None):
+def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None, fp8_top=False):
     """``overrides`` (optional) maps "bottom"/"top" to per-layer ReLU decision
     overrides (see ``mlp.mlp_forward``); ``loss_normalizer`` (optional) is the
     labelled-entry count of the full batch when ``batch`` holds a subset of
-    its samples."""
+    its samples.  ``fp8_top``: the top MLP's hidden layers run their forward
+    product in FP8 with row-wise scales (mixed FP8 / BF16 training, Section
+    3.5.2); the objective heads and the whole backward keep the stored bf16
+    values (the gradient treats quantisation as the identity)."""
     rnd = rounding(cfg.dtype)
     B, F, d = int(cfg.B), int(cfg.F), int(cfg.d)
     n, s0 = cfg.n_slots, cfg.first_emb_slot
@@ -69,7 +72,8 @@ def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None):
         raise ValueError(cfg.interact)
     c["inter"] = inter
     hs_top, mt = mlp_forward(t, params["top"], rnd, relu_last=False,
-                         overrides=(overrides or {}).get("top"))
+                         overrides=(overrides or {}).get("top"),
+                         fp8_layers=tuple(range(len(params["top"]) - 1)) if fp8_top else ())
     c["hs_top"], c["masks_top"] = hs_top, mt
     z = hs_top[-1]
     loss, dz = masked_bce(z, batch["labels"], batch["mask"], loss_normalizer)
@@ -115,7 +119,7 @@ def backward(cfg, params, table, batch, c, lr_tables=None):
     return g
 
 
-def step(cfg, params, table, batch, lr_tables=None, overrides=None, loss_normalizer=None):
-    c = forward(cfg, params, table, batch, overrides, loss_normalizer)
+def step(cfg, params, table, batch, lr_tables=None, overrides=None, loss_normalizer=None, fp8_top=False):
+    c = forward(cfg, params, table, batch, overrides, loss_normalizer, fp8_top)
     g = backward(cfg, params, table, batch, c, lr_tables)
     return c, g

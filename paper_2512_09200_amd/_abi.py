@@ -16,6 +16,7 @@ NOALLOC_SCRATCH_BYTES = 256 << 20
 F32, BF16 = 0, 1
 POOL_SUM, POOL_MEAN = 0, 1
 DOT, FM, STACK = 0, 1, 2
+FP8_ROWWISE, FP8_TENSORWISE = 0, 1
 
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "BAD_INPUT", 5: "HIP"}
 
@@ -79,7 +80,7 @@ SIDE_EVENTS = 6
 class lattice_step_opts(Structure):
     _fields_ = [("lr_tables", c_float), ("emit_grad_rows", c_int32), ("nnz_capacity", c_int64),
                 ("stage_events", POINTER(c_void_p)), ("side_stream", c_void_p),
-                ("side_events", POINTER(c_void_p))]
+                ("side_events", POINTER(c_void_p)), ("fp8_top", c_int32)]
 
 
 STAGES = ["embbag_fwd", "bottom_fwd", "interact_fwd", "top_fwd", "loss", "top_bwd",
@@ -95,7 +96,8 @@ class lattice_step_layout(Structure):
                  ("top_grad", c_int64 * MAX_LAYERS), ("bottom_grad", c_int64 * MAX_LAYERS)]
                 + [(k, c_int64) for k in ("unique_rows", "seg_offsets", "sorted_bags",
                                           "num_unique", "grad_rows", "interact", "scratch",
-                                          "scratch_bytes", "sparse", "sparse_bytes")])
+                                          "scratch_bytes", "sparse", "sparse_bytes", "fp8",
+                                          "fp8_bytes")])
 
 
 # (name, restype, argtypes)
@@ -123,6 +125,12 @@ _SIGS = [
     ("lattice_mlp_heads_bwd", c_int, [POINTER(lattice_mlp_desc), c_int32, c_void_p, c_int64,
                                       POINTER(c_void_p), POINTER(c_int64), c_void_p, c_int64,
                                       c_void_p, c_int64, c_void_p, c_size_t, c_void_p]),
+    ("lattice_fp8_quantize_workspace", c_size_t, []),
+    ("lattice_fp8_quantize", c_int, [c_void_p, c_int, c_int64, c_int64, c_int64, c_int, c_void_p, c_int64,
+                                     c_void_p, c_void_p, c_size_t, c_void_p]),
+    ("lattice_linear_fp8_fwd", c_int, [c_void_p, c_int64, c_void_p, c_int, c_void_p, c_int64, c_void_p, c_int,
+                                       c_void_p, c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p,
+                                       c_int, c_int64, c_void_p]),
     ("lattice_step_plan", c_int, [POINTER(lattice_model_desc), c_int32, c_int64,
                                   POINTER(lattice_step_opts), POINTER(lattice_step_layout)]),
     ("lattice_step", c_int, [POINTER(lattice_model_desc), POINTER(lattice_batch_desc),

@@ -240,6 +240,46 @@ def lattice_mlp_heads_bwd(layers, x, acts, d_out, relu_last, d_in=None, stream=N
 
 
 # ---------------------------------------------------------------------------
+_FP8_SCALING = {"row": A.FP8_ROWWISE, "tensor": A.FP8_TENSORWISE}
+
+
+def fp8_ld(cols):
+    """Row stride (bytes) of the e4m3 codes of a matrix with `cols` columns."""
+    return (cols + 15) // 16 * 16
+
+
+def lattice_fp8_quantize(x, scaling="row", stream=None):
+    """e4m3 codes [rows, fp8_ld(cols)] (uint8) and fp32 scales ([rows] or [1])
+    of a 2-D bf16 / fp32 tensor (unit column stride)."""
+    lib = load()
+    rows, cols = x.shape
+    q = torch.empty((rows, fp8_ld(cols)), dtype=torch.uint8, device=x.device)
+    sc = torch.empty((rows if scaling == "row" else 1,), dtype=torch.float32, device=x.device)
+    wsb = lib.lattice_fp8_quantize_workspace()
+    ws = torch.empty(wsb, dtype=torch.uint8, device=x.device)
+    check(lib.lattice_fp8_quantize(_p(x), _dt(x), rows, cols, _row_stride(x), _FP8_SCALING[scaling], _p(q),
+                                   q.stride(0), _p(sc), _p(ws), wsb, _stream(stream)))
+    return q, sc
+
+
+def lattice_linear_fp8_fwd(qa, sa, qw, sw, K, bias=None, relu=False, out=None, out_dtype=torch.bfloat16,
+                           fast_accum=False, stream=None):
+    """Y = act(deq(qa) deq(qw)^T + bias) from e4m3 codes and their scales
+    (row-wise when the scale vector has one entry per row); fast_accum as in
+    lattice.h (False: per-64-k partial sums added in fp32)."""
+    lib = load()
+    M, N = qa.shape[0], qw.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=qa.device)
+    a_sc = A.FP8_ROWWISE if sa.numel() == M and M > 1 else A.FP8_TENSORWISE
+    w_sc = A.FP8_ROWWISE if sw.numel() == N and N > 1 else A.FP8_TENSORWISE
+    check(lib.lattice_linear_fp8_fwd(_p(qa), qa.stride(0), _p(sa), a_sc, _p(qw), qw.stride(0), _p(sw), w_sc,
+                                     _p(bias), M, N, K, int(bool(relu)), int(bool(fast_accum)), _p(out), _dt(out),
+                                     _row_stride(out), _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------------------
 class StepModel:
     """Marshals a model's device tensors into a lattice_model_desc.
 
@@ -276,12 +316,15 @@ class StepModel:
         self.d = d
 
 
-def lattice_step_plan(model, B, nnz, lr_tables=0.0, emit_grad_rows=False):
+_FP8_TOP = {None: 0, False: 0, "precise": 1, "fast": 2}
+
+
+def lattice_step_plan(model, B, nnz, lr_tables=0.0, emit_grad_rows=False, fp8_top=None):
     """Layout of a workspace for batches of B samples and up to nnz lookups;
-    pass the same nnz as nnz_capacity to lattice_step."""
+    pass the same nnz as nnz_capacity (and the same fp8_top) to lattice_step."""
     lib = load()
     opts = A.lattice_step_opts(lr_tables=float(lr_tables), emit_grad_rows=int(emit_grad_rows),
-                               nnz_capacity=int(nnz))
+                               nnz_capacity=int(nnz), fp8_top=_FP8_TOP[fp8_top])
     lay = A.lattice_step_layout()
     check(lib.lattice_step_plan(byref(model.desc), B, nnz, byref(opts), byref(lay)))
     return lay
@@ -306,14 +349,15 @@ class SideStream:
 
 def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0,
                  emit_grad_rows=False, stream=None, stage_events=None, nnz_capacity=0,
-                 side=None):
+                 side=None, fp8_top=None):
     """One forward+backward step; ws is a uint8 device tensor of at least
     lattice_step_plan(...).total_bytes.  stage_events: optional list of
     2*len(STAGES) torch.cuda.Event(enable_timing=True) or None: [2s] and
     [2s+1] are recorded when stage s begins and ends, on the stream that runs
     it (None: not recorded).
     side: a SideStream to overlap the sort and the weight gradients on (None:
-    every stage on the step's stream)."""
+    every stage on the step's stream).  fp8_top: None, "precise" or "fast"
+    (the top MLP's hidden-layer forward in FP8; see lattice.h)."""
     lib = load()
     _contig(dense, labels, mask, ws)
     B = labels.shape[0]
@@ -321,7 +365,7 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
                                  dense=dense.data_ptr() if dense is not None and dense.numel() else None,
                                  labels=labels.data_ptr(), mask=mask.data_ptr())
     opts = A.lattice_step_opts(lr_tables=float(lr_tables), emit_grad_rows=int(emit_grad_rows),
-                               nnz_capacity=int(nnz_capacity or indices.numel()))
+                               nnz_capacity=int(nnz_capacity or indices.numel()), fp8_top=_FP8_TOP[fp8_top])
     if side is not None:
         opts.side_stream, opts.side_events = side.ptrs()
     if stage_events is not None:

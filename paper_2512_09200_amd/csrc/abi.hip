@@ -455,6 +455,57 @@ lattice_status lattice_interact_bwd(const lattice_interact_desc* desc, int32_t B
 }  // extern "C"
 
 // ---------------------------------------------------------------------------
+// FP8 linear layers
+// ---------------------------------------------------------------------------
+extern "C" {
+
+size_t lattice_fp8_quantize_workspace(void) { return fp8_quantize_workspace(); }
+
+lattice_status lattice_fp8_quantize(const void* x, lattice_dtype x_dtype, int64_t rows, int64_t cols,
+                                    int64_t ld, lattice_fp8_scaling scaling, uint8_t* q, int64_t ldq,
+                                    float* scales, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(rows >= 0 && cols >= 0 && rows < ((int64_t)1 << 31) && cols < ((int64_t)1 << 31),
+          "bad rows/cols");
+  REQUIRE(x_dtype == LATTICE_F32 || x_dtype == LATTICE_BF16, "bad dtype");
+  REQUIRE(scaling == LATTICE_FP8_ROWWISE || scaling == LATTICE_FP8_TENSORWISE, "bad scaling");
+  REQUIRE(ld >= cols, "ld < cols");
+  REQUIRE(ldq >= cols && ldq % 16 == 0, "ldq must be >= cols and a multiple of 16");
+  if (rows == 0) return LATTICE_OK;
+  REQUIRE(x && q && scales, "null x/q/scales");
+  REQUIRE(((uintptr_t)q & 15) == 0, "q must be 16-byte aligned");
+  if (scaling == LATTICE_FP8_TENSORWISE && (ws_bytes < fp8_quantize_workspace() || !ws))
+    FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, fp8_quantize_workspace());
+  HIPRET(fp8_quantize(x, dt_of(x_dtype), (int)rows, (int)cols, ld, scaling == LATTICE_FP8_ROWWISE, q,
+                      ldq, scales, ws, strm(stream)));
+  return LATTICE_OK;
+}
+
+lattice_status lattice_linear_fp8_fwd(const uint8_t* qA, int64_t lda, const float* sA,
+                                      lattice_fp8_scaling a_scaling, const uint8_t* qW, int64_t ldw,
+                                      const float* sW, lattice_fp8_scaling w_scaling,
+                                      const float* bias, int32_t M, int32_t N, int32_t K,
+                                      int32_t relu, int32_t fast_accum, void* Y,
+                                      lattice_dtype y_dtype, int64_t ldy, void* stream) {
+  REQUIRE(M >= 0 && N >= 0 && K >= 0, "negative size");
+  REQUIRE(y_dtype == LATTICE_F32 || y_dtype == LATTICE_BF16, "bad output dtype");
+  REQUIRE(a_scaling == LATTICE_FP8_ROWWISE || a_scaling == LATTICE_FP8_TENSORWISE, "bad a_scaling");
+  REQUIRE(w_scaling == LATTICE_FP8_ROWWISE || w_scaling == LATTICE_FP8_TENSORWISE, "bad w_scaling");
+  const int64_t kpad = ((int64_t)K + 15) / 16 * 16;
+  REQUIRE(lda >= kpad && ldw >= kpad && lda % 16 == 0 && ldw % 16 == 0,
+          "lda/ldw must be multiples of 16 and >= K rounded up to 16");
+  REQUIRE(ldy >= N, "ldy < N");
+  if ((int64_t)M * N == 0) return LATTICE_OK;
+  REQUIRE(qA && sA && qW && sW && Y, "null operand");
+  REQUIRE(((uintptr_t)qA & 15) == 0 && ((uintptr_t)qW & 15) == 0, "codes must be 16-byte aligned");
+  HIPRET(gemm_fp8(qA, lda, sA, a_scaling == LATTICE_FP8_ROWWISE, qW, ldw, sW,
+                  w_scaling == LATTICE_FP8_ROWWISE, bias, Y, dt_of(y_dtype), ldy, M, N, K,
+                  relu != 0, fast_accum != 0, strm(stream)));
+  return LATTICE_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
 // MLP + heads
 // ---------------------------------------------------------------------------
 static lattice_status check_mlp(const lattice_mlp_desc* d, int32_t B) {
@@ -514,6 +565,49 @@ static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, 
     g.bias = L.b;
     g.relu = (!last || d->relu_last) ? 1 : 0;
     hipError_t e = gemm(g, nullptr, s);  // forward GEMMs never split K
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// FP8 forward of hidden ReLU layers (bf16 model): per layer, the input and
+// the weights quantised row-wise to e4m3, then the FP8 GEMM with bias and
+// ReLU into the layer's bf16 activation.  Workspace: codes of the widest
+// input [B, ldq] and weights [out, ldq], and their scales.
+static int64_t fp8_ldq(int cols) { return ((int64_t)cols + 15) / 16 * 16; }
+
+static size_t fp8_mlp_workspace(const lattice_mlp_desc* d, int B) {
+  int64_t kmax = 1, nmax = 1;
+  for (int i = 0; i < d->n_layers; ++i) {
+    kmax = std::max<int64_t>(kmax, fp8_ldq(d->layers[i].in_dim));
+    nmax = std::max<int64_t>(nmax, d->layers[i].out_dim);
+  }
+  return al256((size_t)B * kmax) + al256((size_t)nmax * kmax) + al256((size_t)B * 4) + al256((size_t)nmax * 4);
+}
+
+static hipError_t mlp_forward_fp8(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
+                                  void* const* acts, const int64_t* strides, void* ws, int fast,
+                                  hipStream_t s) {
+  int64_t kmax = 1, nmax = 1;
+  for (int i = 0; i < d->n_layers; ++i) {
+    kmax = std::max<int64_t>(kmax, fp8_ldq(d->layers[i].in_dim));
+    nmax = std::max<int64_t>(nmax, d->layers[i].out_dim);
+  }
+  char* p = (char*)ws;
+  uint8_t* qa = (uint8_t*)p; p += al256((size_t)B * kmax);
+  uint8_t* qw = (uint8_t*)p; p += al256((size_t)nmax * kmax);
+  float* sa = (float*)p; p += al256((size_t)B * 4);
+  float* sw = (float*)p;
+  for (int i = 0; i < d->n_layers; ++i) {
+    const lattice_linear& L = d->layers[i];
+    const void* x = i == 0 ? in : acts[i - 1];
+    const int64_t ldx = i == 0 ? in_stride : strides[i - 1];
+    const int64_t ldq = fp8_ldq(L.in_dim);
+    hipError_t e = fp8_quantize(x, DT_BF16, B, L.in_dim, ldx, 1, qa, ldq, sa, nullptr, s);
+    if (e == hipSuccess) e = fp8_quantize(L.W, DT_BF16, L.out_dim, L.in_dim, L.in_dim, 1, qw, ldq, sw, nullptr, s);
+    if (e == hipSuccess)
+      e = gemm_fp8(qa, ldq, sa, 1, qw, ldq, sw, 1, L.b, acts[i], DT_BF16, strides[i], B, L.out_dim,
+                   L.in_dim, 1, fast, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -783,6 +877,10 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   lattice_status st = check_model(m, B);
   if (st != LATTICE_OK) return st;
   REQUIRE(nnz >= 0 && nnz < ((int64_t)1 << 31), "bad nnz");
+  if (o && o->fp8_top) {
+    REQUIRE(o->fp8_top == 1 || o->fp8_top == 2, "fp8_top must be 0, 1 or 2");
+    if (m->dtype != LATTICE_BF16) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs a bf16 model");
+  }
   const size_t es = esize(m->dtype);
   const int d = m->tables.dim;
   P->n = m->interact.n;
@@ -838,6 +936,13 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   const size_t sp = embbag_bwd_workspace(nnz, d, m->num_features);
   L.sparse = take(sp);
   L.sparse_bytes = (int64_t)sp;
+  L.fp8 = -1;
+  L.fp8_bytes = 0;
+  if (o && o->fp8_top) {
+    const size_t f8 = fp8_mlp_workspace(&m->top, B);
+    L.fp8 = take(f8);
+    L.fp8_bytes = (int64_t)f8;
+  }
   L.total_bytes = off;
   return LATTICE_OK;
 }
@@ -1018,10 +1123,14 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   hidden.n_layers = nt - 1;
   hidden.relu_last = 1;
   if (fused_heads) {
-    if (nt > 1) HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, s));
+    if (nt > 1 && opts->fp8_top)
+      HIPRET(mlp_forward_fp8(&hidden, B, t, P.t_stride, tacts, tstr, at(L.fp8), opts->fp8_top == 2, s));
+    else if (nt > 1)
+      HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, s));
     HIPRET(head_fwd((const bf16_t*)head_in, head_ld, B, head.in_dim, (const bf16_t*)head.W, head.b,
                     T, batch->labels, batch->mask, (float*)at(L.logits), scratch, s));
   } else {
+    if (opts->fp8_top) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs the fused bf16 heads (<= 64 objectives)");
     HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, s));
   }
   HIPRET(end(LATTICE_STAGE_TOP_FWD));

@@ -142,4 +142,13 @@ hipError_t head_bwd(const float* z, const float* y, const uint8_t* m, int B, int
                     float* dz, bf16_t* dz_op, bf16_t* g, int64_t ldg, const void* ws,
                     hipStream_t s);
 
+// fp8.hip (OCP e4m3 linear layers, tensor- or row-wise scales)
+size_t fp8_quantize_workspace();
+hipError_t fp8_quantize(const void* x, DType xdt, int rows, int cols, int64_t ld, int rowwise,
+                        uint8_t* q, int64_t ldq, float* scales, void* ws, hipStream_t s);
+hipError_t gemm_fp8(const uint8_t* A, int64_t lda, const float* sa, int sa_rowwise, const uint8_t* B,
+                    int64_t ldb, const float* sb, int sb_rowwise, const float* bias, void* C,
+                    DType cdt, int64_t ldc, int M, int N, int K, int relu, int fast_accum,
+                    hipStream_t s);
+
 }  // namespace lat

@@ -5,6 +5,7 @@ import torch
 import synth
 from oracle import bounds as obounds
 from oracle import embbag as oembbag
+from oracle import fp8 as ofp8
 from oracle import interact as ointeract
 from oracle import loss as oloss
 from oracle import mlp as omlp
@@ -93,7 +94,26 @@ def assert_product(name, got, ref, absref, K, storage_unit=None, t=2e-2):
     assert err <= t, f"{name}: max_rel_err {err} > {t}"
 
 
-def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None):
+def assert_fp8_layer(name, got, h, W, b, fast, t=2e-2):
+    """A hidden layer whose forward product ran in FP8 (row-wise e4m3 input
+    and weights): within oracle.fp8.linear_fp8_bound of the exact product of
+    the codes the oracle takes from the same stored input, plus bf16 output
+    rounding (ReLU is 1-Lipschitz)."""
+    qa, sa = ofp8.quantize(h, rowwise=True)
+    qw, sw = ofp8.quantize(W, rowwise=True)
+    ref = ofp8.linear_fp8(qa, sa, qw, sw, b, relu=True)
+    bound = ofp8.linear_fp8_bound(qa, sa, qw, sw, b, fast_accum=fast)
+    bound = bound + 2.0 ** -8 * (np.abs(ref) + bound) + 1e-37
+    got = _np64(got)
+    ratio = float(np.max(np.abs(got - ref) / bound, initial=0.0))
+    err = max_rel_err(got, ref)
+    print(f"  {name} [fp8 stage]: max_rel_err={err:.3e}, worst |x-r|/bound={ratio:.3f}", flush=True)
+    assert np.all(np.isfinite(got)) and ratio <= 1.0, f"{name}: outside the fp8 bound ({ratio})"
+    if not fast:
+        assert err <= t, f"{name}: max_rel_err {err} > {t}"
+
+
+def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_top=None):
     """Stage-wise parity of one step: every stage recomputed in float64 by
     the oracle from the accelerator's own stored inputs of that stage, so the
     only admissible difference is that stage's own arithmetic.  v: the step's
@@ -102,7 +122,9 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None):
     rows (optional): samples for the per-sample stages (all if None);
     wgrad_rows (optional): dict ("top"|"bottom", layer) -> output rows of
     that weight gradient to recompute over the whole batch (all if absent).
-    Sample-summed interaction gradients are checked when rows is None."""
+    Sample-summed interaction gradients are checked when rows is None.
+    fp8_top ("precise" / "fast"): the top MLP's hidden layers ran their
+    forward product in FP8 (assert_fp8_layer)."""
     us = 2.0 ** -8 if cfg.dtype == "bf16" else None
     t = tol(cfg)
     B, d = cfg.B, cfg.d
@@ -118,7 +140,9 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None):
         h = h_top[i][R]
         a = h @ W.T + b
         ab = np.abs(h) @ np.abs(W).T + np.abs(b)
-        if i < L - 1:
+        if i < L - 1 and fp8_top:
+            assert_fp8_layer(f"top{i} forward", h_top[i + 1][R], h, W, b, fp8_top == "fast", t)
+        elif i < L - 1:
             assert_product(f"top{i} forward", h_top[i + 1][R], np.maximum(a, 0), ab, W.shape[1] + 1, us, t)
         else:
             assert_product("logits", _np64(v["logits"])[R], a, ab, W.shape[1] + 1, None, t)

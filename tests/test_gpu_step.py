@@ -35,19 +35,19 @@ def gpu_relu_io(cfg, w, v):
     return dict(bottom=bin_, top=tin), dict(bottom=bout, top=tout)
 
 
-def run_step(w, lr, emit=True, spare=0, side="new", **kw):
+def run_step(w, lr, emit=True, spare=0, side="new", fp8_top=None, **kw):
     """One step; the workspace is planned for nnz + spare lookups.  side:
     "new" overlaps on a fresh side stream (as the benchmark does), None runs
     every stage on one stream, or a SideStream to reuse."""
     from paper_2512_09200_amd import api
     cfg = w.cfg
     model = w.step_model()
-    lay = api.lattice_step_plan(model, cfg.B, w.nnz + spare, lr, emit)
+    lay = api.lattice_step_plan(model, cfg.B, w.nnz + spare, lr, emit, fp8_top=fp8_top)
     ws = torch.zeros(lay.total_bytes, dtype=torch.uint8, device=DEV)
     if side == "new":
         side = api.SideStream()
     api.lattice_step(model, w.offsets, w.indices, w.dense, w.labels, w.mask, ws, lr, emit,
-                     nnz_capacity=w.nnz + spare, side=side, **kw)
+                     nnz_capacity=w.nnz + spare, side=side, fp8_top=fp8_top, **kw)
     torch.cuda.synchronize()
     return model, api.step_views(model, ws, lay, cfg.B, cfg.T, w.nnz), ws
 
@@ -118,6 +118,41 @@ def check_step(cfg, lr, spare=0, w=None):
         assert np.array_equal(E1[keep], E0[keep])
     else:
         assert np.array_equal(E1, E0)
+
+
+FP8_CASES = {
+    "large-fm-small": synth.small(synth.LARGE_FM, B=160, rows=6000),
+    "mid-small": synth.small(synth.MID, B=256, rows=3000),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mode", ["precise", "fast"])
+@pytest.mark.parametrize("name", list(FP8_CASES))
+def test_step_fp8_top(name, mode):
+    """Mixed FP8 / BF16 training (Section 3.5.2): the top MLP's hidden-layer
+    forward products in FP8 with row-wise scales.  Every stage on the GPU's
+    own stored inputs (the FP8 layers within their derived bound), and the
+    step's loss and logits against the oracle's FP8 forward."""
+    cfg = FP8_CASES[name]
+    lr = 0.01
+    print(f"[step-fp8] {name} {mode}", flush=True)
+    w = Workload(cfg)
+    E0 = w.table_np()
+    _, v, _ = run_step(w, lr, fp8_top=mode)
+    E1 = w.table_np()
+    check_stages(cfg, w.params, w.batch, v, grads_of(w), fp8_top=mode)
+    c, g = ostep.step(cfg, w.params, E0, w.batch, lr_tables=lr, fp8_top=True)
+    bk0 = g["bookkeeping"]
+    check_sparse_stage(cfg, w.batch, v, w.nnz, E0[bk0["unique_rows"]], E1[bk0["unique_rows"]], lr, bk=bk0)
+    from oracle.metrics import max_rel_err_normwise
+    for nm, got, ref in (("logits", v["logits"], c["logits"]), ("loss", v["loss"], np.array([c["loss"]]))):
+        e = max_rel_err_normwise(got.float().cpu().numpy(), ref)
+        print(f"  {nm} (composed, fp8): normwise {e:.3e}", flush=True)
+        assert e <= 2e-2
+    # the FP8 forward changes the step: the bf16 step's logits differ
+    c16, _ = ostep.step(cfg, w.params, E0, w.batch, lr_tables=lr)
+    assert not np.allclose(c16["logits"], c["logits"], rtol=0, atol=0)
 
 
 @pytest.mark.gpu
