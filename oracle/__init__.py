@@ -16,15 +16,22 @@ Modules:
   bf16      -- round-to-nearest-even from float64 to the bfloat16 grid
   embbag    -- pooled embedding lookup, its gradient, the row bookkeeping and
                the row-sparse SGD update (Section 3.3.1; Section 3.2 zero-padding)
-  mlp       -- linear layers with bias and ReLU (feature processor, task modules)
+  mlp       -- linear layers with bias and ReLU or SwishRN (feature processor,
+               task modules)
+  swishrn   -- Swish RMSNorm with BlockNorm groups and the hard-sigmoid gate
+               (Sections 3.3.4, 3.5.3), its backward and fp32 error bounds
+  fp8       -- OCP e4m3 quantisation with tensor- or row-wise scales and the
+               FP8 linear layer with its accumulation bound (Section 3.5.2)
   interact  -- dot-product Gram interaction, factorization-machine block and the
                stacked FM -> linear -> residual -> LayerNorm block (Section 3.3.2)
   loss      -- masked multi-objective binary cross-entropy (Section 3.2.1 routing)
   step      -- the whole forward + backward step composed from the above
   metrics   -- the comparison metric used by the parity tests
+  bounds    -- element-wise error scales of the composed bf16 step (how far
+               two correct evaluations may lie apart)
 
 Parity status: every function is pinned by tests under ``tests/`` against
 brute force, closed forms, invariants and central finite differences; none is
 "parity unpinned".
 """
-from . import bf16, embbag, mlp, interact, loss, step, metrics  # noqa: F401
+from . import bf16, embbag, mlp, interact, loss, step, metrics, swishrn, fp8, bounds  # noqa: F401

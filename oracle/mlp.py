@@ -1,6 +1,6 @@
-"""Linear layers with bias and ReLU: the dense feature processor ("bottom"
-MLP, Section 3.3.1) and the task modules ("top" MLP with one output per
-objective, Section 3.3.3).
+"""Linear layers with bias and ReLU (or SwishRN): the dense feature processor
+("bottom" MLP, Section 3.3.1) and the task modules ("top" MLP with one output
+per objective, Section 3.3.3).
 
 Test infrastructure only (see the package docstring).
 
@@ -10,10 +10,17 @@ last top layer returns the logits ``a`` unrounded.  Backward of one layer,
 given the gradient ``g`` of its output: ``dW = g^T h``, ``db = sum_b g``,
 ``dh = g W``; the gradient reaching a hidden activation is masked by that
 activation being positive (ReLU) and stored as ``rnd(...)``.
+
+SwishRN layers (Section 3.3.4, ``swishrn``) replace the ReLU: the layer
+stores its pre-activation ``rnd(a)`` and its output ``rnd(swishrn(a))``; in
+the backward the gradient of the output is stored as ``rnd(g W)`` and the
+gradient of the pre-activation as ``rnd(swishrn.backward(...))``, and the
+gains get their gradients from the stored output gradient.
 """
 import numpy as np
 
 from . import fp8 as _fp8
+from . import swishrn as _swishrn
 
 
 def linear(h, W, b):
@@ -46,7 +53,7 @@ def linear_fp8(h, W, b):
     return _fp8.linear_fp8(qa, sa, qw, sw, b)
 
 
-def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=()):
+def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=None):
     """Returns ``(hs, masks)``: the layer inputs/outputs ``[h0, h1, ..., hL]``
     and, per layer, its ReLU decision (``None`` for a linear last layer).
     Every layer but (optionally) the last applies ReLU and storage rounding.
@@ -56,13 +63,24 @@ def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=()):
     the sign of the float64 pre-activation.  Parity tests use it only inside
     ``relu_band``, where either decision is a correct result of fp32
     arithmetic.  Layers listed in ``fp8_layers`` run their forward product
-    in FP8 (``linear_fp8``)."""
+    in FP8 (``linear_fp8``).
+
+    ``act`` (optional) makes the activated layers SwishRN layers: a dict with
+    ``kind`` ("sigmoid" | "hard"), ``block`` (0: RMSNorm over the row; b:
+    BlockNorm groups of b features), ``eps`` and ``gains`` (per layer
+    ``(ga, gb)``).  Their entry in the returned list is then a dict
+    ``{"pre": a, "rho": ...}`` instead of a ReLU mask."""
     hs = [np.asarray(h0, np.float64)]
     masks = []
     for i, (W, b) in enumerate(layers):
         a = linear_fp8(hs[-1], W, b) if i in fp8_layers else linear(hs[-1], W, b)
         last = i == len(layers) - 1
-        if relu_last or not last:
+        if act is not None and (relu_last or not last):
+            ga, gb = act["gains"][i]
+            out, _, rho = _swishrn.forward(a, ga, gb, act["block"], act["eps"], act["kind"])
+            hs.append(rnd(out))
+            masks.append({"pre": a, "rho": rho})
+        elif relu_last or not last:
             on = a > 0
             if overrides is not None and overrides[i] is not None:
                 where, positive = overrides[i]
@@ -75,13 +93,27 @@ def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=()):
     return hs, masks
 
 
-def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad):
+def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=None, dgains=None):
     """Backward through ``mlp_forward``.  ``g_out`` is dL/d(hs[-1]) (before the
-    last ReLU mask when ``relu_last``).  Returns (dWs, dbs, dL/dh0 or None)."""
+    last ReLU mask when ``relu_last``).  Returns (dWs, dbs, dL/dh0 or None).
+    With ``act`` (as in ``mlp_forward``) the gain gradients of the SwishRN
+    layers go to ``dgains[i] = (dga, dgb)``."""
     L = len(layers)
+
+    def through(i, g):
+        """Gradient of layer i's pre-activation from that of its output."""
+        if act is None:
+            return rnd(g * masks[i])
+        ga, gb = act["gains"][i]
+        go = rnd(g)
+        dh, dga, dgb = _swishrn.backward(go, masks[i]["pre"], ga, gb, act["block"], act["eps"], act["kind"])
+        if dgains is not None:
+            dgains[i] = (dga, dgb)
+        return rnd(dh)
+
     g = np.asarray(g_out, np.float64)
     if relu_last:
-        g = rnd(g * masks[-1])
+        g = through(L - 1, g)
     dWs, dbs = [None] * L, [None] * L
     dh0 = None
     for i in range(L - 1, -1, -1):
@@ -89,7 +121,7 @@ def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad):
         dW, db, dh = linear_grads(g, hs[i], W)
         dWs[i], dbs[i] = dW, db
         if i > 0:
-            g = rnd(dh * masks[i - 1])
+            g = through(i - 1, dh)
         elif need_input_grad:
             dh0 = dh
     return dWs, dbs, dh0

@@ -10,7 +10,8 @@ Forward (per sample b; Section 3.3):
   3. interaction (DOT, FM or STACK, see ``interact``);
   4. top input: ``concat(X_b[0], flatten(interaction))`` (DOT/FM), or the
      flattened STACK output;
-  5. top MLP, ReLU on hidden layers, one logit per objective (Section 3.3.3);
+  5. top MLP, ReLU (or SwishRN, Section 3.3.4) on hidden layers, one logit
+     per objective (Section 3.3.3);
   6. masked BCE (Section 3.2.1).
 Backward: the exact chain rule through 1-6, with GEMM operands (activation
 gradients) rounded to the storage precision where the accelerator stores them:
@@ -31,6 +32,15 @@ from .loss import masked_bce
 def rounding(dtype):
     """Storage rounding of a workload: bf16 RNE, or none for fp32."""
     return _bf16.round_bf16 if dtype == "bf16" else _bf16.identity
+
+
+def top_act(cfg, params):
+    """The SwishRN description of the top MLP's hidden layers (see
+    ``mlp.mlp_forward``), or None for ReLU."""
+    if getattr(cfg, "top_act", "relu") == "relu":
+        return None
+    kind = {"swishrn": "sigmoid", "hardswishrn": "hard"}[cfg.top_act]
+    return dict(kind=kind, block=cfg.norm_block, eps=cfg.norm_eps, gains=params["top_gain"])
 
 
 def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None, fp8_top=False):
@@ -73,7 +83,8 @@ def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None, fp8
     c["inter"] = inter
     hs_top, mt = mlp_forward(t, params["top"], rnd, relu_last=False,
                          overrides=(overrides or {}).get("top"),
-                         fp8_layers=tuple(range(len(params["top"]) - 1)) if fp8_top else ())
+                         fp8_layers=tuple(range(len(params["top"]) - 1)) if fp8_top else (),
+                         act=top_act(cfg, params))
     c["hs_top"], c["masks_top"] = hs_top, mt
     z = hs_top[-1]
     loss, dz = masked_bce(z, batch["labels"], batch["mask"], loss_normalizer)
@@ -88,9 +99,13 @@ def backward(cfg, params, table, batch, c, lr_tables=None):
     X = c["X"]
     g = {}
     gz = rnd(c["dz"])
+    act = top_act(cfg, params)
+    dgains = [None] * (len(params["top"]) - 1)
     dWt, dbt, dt = mlp_backward(gz, c["hs_top"], c["masks_top"], params["top"], rnd, relu_last=False,
-                                need_input_grad=True)
+                                need_input_grad=True, act=act, dgains=dgains)
     g["top_dW"], g["top_db"] = dWt, dbt
+    if act is not None:
+        g["top_dgain"] = dgains
     gt = rnd(dt)
     g["d_top_in"] = gt
     off = d if cfg.has_dense else 0

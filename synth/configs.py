@@ -43,6 +43,9 @@ class Config:
     lr_tables: float = 0.0                   # row-sparse SGD step on the tables (0: none)
     seed: int = 0
     ln_eps: float = 1e-5
+    top_act: str = "relu"                    # hidden top layers: "relu" | "swishrn" | "hardswishrn"
+    norm_block: int = 128                    # SwishRN groups: 128 (BlockNorm) or 0 (the whole row)
+    norm_eps: float = 1e-6
 
     # ---- derived shapes -------------------------------------------------
     @property

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import interact, step
+from oracle import interact, step, swishrn
 
 
 def _tiny_cfg(kind, pool="sum"):
@@ -24,6 +24,11 @@ def _tiny_cfg(kind, pool="sum"):
     if kind == "stack":
         return synth.Config(name="t-stack", F=5, dense_in=0, bottom=(), interact="stack",
                             fm_rank=2, stack_layers=2, stack_n=3, top=(4, 2), **base)
+    if kind in ("swishrn", "hardswishrn"):
+        # SwishRN hidden top layers, BlockNorm groups of 2 (3, 2, 2, 1 features
+        # over widths 7 and 5: a ragged last group)
+        return synth.Config(name="t-" + kind, F=3, dense_in=3, bottom=(6, 4), interact="dot",
+                            top=(7, 5, 3), top_act=kind, norm_block=2, norm_eps=1e-3, **base)
     raise ValueError(kind)
 
 
@@ -37,6 +42,8 @@ def _setup(cfg):
     }
     if "fm_W" in p:
         params["fm_W"] = p["fm_W"].astype(np.float64)
+    if "top_gain" in p:
+        params["top_gain"] = [(ga.astype(np.float64), gb.astype(np.float64)) for ga, gb in p["top_gain"]]
     if "stack" in p:
         params["stack"] = [{k: (None if v is None else v.astype(np.float64)) for k, v in lay.items()}
                            for lay in p["stack"]]
@@ -53,6 +60,8 @@ def _pairs(cfg, params, g):
         out += [(W, g["top_dW"][i], f"top{i}.W"), (b, g["top_db"][i], f"top{i}.b")]
     if "fm_W" in params:
         out.append((params["fm_W"], g["fm_dW"], "fm.W"))
+    for i, (ga, gb) in enumerate(params.get("top_gain", [])):
+        out += [(ga, g["top_dgain"][i][0], f"top{i}.ga"), (gb, g["top_dgain"][i][1], f"top{i}.gb")]
     for i, lay in enumerate(params.get("stack", [])):
         sg = g["stack"][i]
         out += [(lay["W"], sg["dW"], f"stack{i}.W"), (lay["A"], sg["dA"], f"stack{i}.A"),
@@ -73,13 +82,21 @@ def _fd(loss_fn, arr, idx, h):
 
 
 def _check_kinks(cfg, params, table, batch):
-    """The FD test is only meaningful away from ReLU kinks."""
+    """The FD test is only meaningful away from ReLU kinks (and the hard
+    gate's kinks at +-3)."""
     c = step.forward(cfg, params, table, batch)
-    for hs, layers in ((c.get("hs_bottom"), params["bottom"]), (c["hs_top"], params["top"])):
+    act = step.top_act(cfg, params)
+    for hs, layers, top in ((c.get("hs_bottom"), params["bottom"], False), (c["hs_top"], params["top"], True)):
         if hs is None:
             continue
         for i, (W, b) in enumerate(layers):
             a = hs[i] @ W.T + b
+            if top and act is not None and i < len(layers) - 1:
+                if act["kind"] == "hard":
+                    _, n, _ = swishrn.forward(a, *act["gains"][i], act["block"], act["eps"], "hard")
+                    z = act["gains"][i][1] * n
+                    assert np.min(np.abs(np.abs(z) - 3.0)) > 1e-4, "seed puts a gate input on a kink"
+                continue
             assert np.min(np.abs(a)) > 1e-4, "seed puts a pre-activation on a ReLU kink"
 
 
@@ -122,7 +139,8 @@ def _fd_worst(kind, pool="sum", n_coords=12):
     return worst
 
 
-@pytest.mark.parametrize("kind,pool", [("dot", "sum"), ("dot", "mean"), ("fm", "sum"), ("stack", "sum")])
+@pytest.mark.parametrize("kind,pool", [("dot", "sum"), ("dot", "mean"), ("fm", "sum"), ("stack", "sum"),
+                                       ("swishrn", "sum"), ("hardswishrn", "sum")])
 def test_finite_differences(kind, pool):
     assert _fd_worst(kind, pool) < 1e-6
 
@@ -145,9 +163,32 @@ def _layernorm_backward_dropped_term(dy, xhat, rstd, gamma):
     return du, dgamma
 
 
-def _mlp_backward_no_relu_mask(g_out, hs, masks, layers, rnd, relu_last, need_input_grad):
+def _mlp_backward_no_relu_mask(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, **kw):
     masks = [None if m is None else np.ones_like(m) for m in masks]
-    return _ORIG["mlp_backward"](g_out, hs, masks, layers, rnd, relu_last, need_input_grad)
+    return _ORIG["mlp_backward"](g_out, hs, masks, layers, rnd, relu_last, need_input_grad, **kw)
+
+
+def _swishrn_backward_no_mean_term(do, h, ga, gb, block, eps, kind, rho=None, kink_grad=None):
+    do = np.asarray(do, np.float64)
+    _, n, rho = swishrn.forward(h, ga, gb, block, eps, kind, rho)
+    a, z = ga * n, gb * n
+    s, sp = swishrn.gate(z, kind), swishrn.gate_grad(z, kind)
+    dn = ga * do * s + gb * do * a * sp
+    dh = swishrn.expand(rho, n.shape[1], block) * dn                  # the normalisation's mean term dropped
+    return dh, (do * s * n).sum(0), (do * a * sp * n).sum(0)
+
+
+def _swishrn_backward_whole_row_mean(do, h, ga, gb, block, eps, kind, rho=None, kink_grad=None):
+    dh, dga, dgb = _ORIG["swishrn_backward"](do, h, ga, gb, block, eps, kind, rho, kink_grad)
+    _, n, rho = swishrn.forward(h, ga, gb, block, eps, kind, rho)
+    a, z = ga * n, gb * n
+    dn = ga * do * swishrn.gate(z, kind) + gb * do * a * swishrn.gate_grad(z, kind)
+    R = swishrn.expand(rho, n.shape[1], block)
+    return R * (dn - n * np.mean(dn * n, axis=1, keepdims=True)), dga, dgb   # mean over the row, not the group
+
+
+def _swishrn_backward_gate_gain_swapped(do, h, ga, gb, block, eps, kind, rho=None, kink_grad=None):
+    return _ORIG["swishrn_backward"](do, h, gb, ga, block, eps, kind, rho, kink_grad)
 
 
 def _dot_backward_no_slot0(dp, X):
@@ -156,7 +197,8 @@ def _dot_backward_no_slot0(dp, X):
     return dX
 
 
-_ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward)
+_ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward,
+             swishrn_backward=swishrn.backward)
 
 
 @pytest.mark.parametrize("target,module,name,kind", [
@@ -164,7 +206,11 @@ _ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward)
     (_layernorm_backward_dropped_term, interact, "layernorm_backward", "stack"),
     (_mlp_backward_no_relu_mask, step, "mlp_backward", "dot"),
     (_dot_backward_no_slot0, step, "dot_backward", "dot"),
-], ids=["fm-sign", "layernorm-term", "relu-mask", "slot0-gradient"])
+    (_swishrn_backward_no_mean_term, swishrn, "backward", "swishrn"),
+    (_swishrn_backward_whole_row_mean, swishrn, "backward", "hardswishrn"),
+    (_swishrn_backward_gate_gain_swapped, swishrn, "backward", "swishrn"),
+], ids=["fm-sign", "layernorm-term", "relu-mask", "slot0-gradient", "swishrn-mean-term",
+        "blocknorm-group", "swishrn-gains"])
 def test_planted_backward_mistakes_fail_the_finite_difference_pin(monkeypatch, target, module, name, kind):
     monkeypatch.setattr(module, name, target)
     assert _fd_worst(kind, n_coords=6) > 1e-3
