@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 6
+#define LATTICE_ABI_VERSION 7
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -221,20 +221,56 @@ lattice_status lattice_interact_bwd(const lattice_interact_desc* desc, int32_t B
 /* MLPs and multi-objective heads (Sections 3.3.1, 3.3.3, 3.2.1)            */
 /* ------------------------------------------------------------------------ */
 
+/* Activation of the hidden layers of an MLP.
+ *
+ * SwishRN (Section 3.3.4) replaces the ReLU of a feed-forward layer: with
+ * the layer's pre-activation h = x W^T + b split into normalisation groups
+ * G of its features,
+ *   rho_G = 1 / sqrt(mean_{j in G} h_j^2 + eps),  n = h rho_G,
+ *   out   = (g_a n) * gate(g_b n),
+ * two per-feature gains (g_a of the normalised value, g_b of the RMSNorm
+ * that feeds the self-gate; both share rho).  gate is the logistic sigmoid
+ * (SWISHRN) or the hard sigmoid clip(z/6 + 1/2, 0, 1), which avoids the
+ * exponential (HARDSWISHRN, Section 3.5.3).  The groups are the whole row
+ * (norm_block = 0: RMSNorm) or BlockNorm's groups of 128 consecutive
+ * features (norm_block = 128, Section 3.5.3: the columns of one GEMM tile,
+ * so bf16 models compute the statistic in the GEMM's epilogue without
+ * data from other workgroups); the last group is shorter when 128 does not
+ * divide the width.  The forward stores h (storage dtype) and every
+ * group's rho (fp32) for the backward. */
+typedef enum {
+  LATTICE_ACT_RELU = 0,
+  LATTICE_ACT_SWISHRN = 1,
+  LATTICE_ACT_HARDSWISHRN = 2
+} lattice_activation;
+
+#define LATTICE_BLOCKNORM_COLS 128
+
 typedef struct {
   int32_t in_dim, out_dim;
   const void* W;    /* device [out_dim, in_dim], storage dtype */
   const float* b;   /* device [out_dim] or NULL */
   float* dW;        /* device [out_dim, in_dim] fp32 (bwd, overwritten) */
   float* db;        /* device [out_dim] fp32 or NULL (bwd, overwritten) */
+  /* SwishRN layers only (ignored otherwise): */
+  const float* gain;  /* device [2, out_dim] fp32: g_a, then g_b */
+  float* dgain;       /* device [2, out_dim] fp32 or NULL (bwd, overwritten) */
+  void* pre;          /* lattice_mlp_heads_fwd/bwd: device [B, out_dim] storage dtype,
+                         the pre-activation h (fwd writes, bwd reads); lattice_step
+                         keeps it in its workspace instead */
+  float* rinv;        /* lattice_mlp_heads_fwd/bwd: device [B, groups] fp32, rho of
+                         every row and group (fwd writes, bwd reads) */
 } lattice_linear;
 
 typedef struct {
   lattice_dtype dtype;
   int32_t n_layers;                 /* 1 .. LATTICE_MAX_LAYERS */
   const lattice_linear* layers;     /* host [n_layers] */
-  int32_t relu_last;                /* 1: ReLU on every layer (bottom MLP);
+  int32_t relu_last;                /* 1: the activation on every layer (bottom MLP);
                                        0: last layer linear, fp32 output (heads) */
+  lattice_activation act;           /* activation of the activated layers */
+  int32_t norm_block;               /* SwishRN groups: 0 (whole row) or 128 (BlockNorm) */
+  float norm_eps;                   /* SwishRN eps (>= 0) */
 } lattice_mlp_desc;
 
 /* Masked multi-objective BCE with logits z [B, T]: with N = max(1, sum m),
@@ -253,8 +289,10 @@ typedef struct {
 size_t lattice_mlp_heads_workspace(const lattice_mlp_desc* desc, int32_t B);
 
 /* Forward: acts[i] (host array of device pointers) receives layer i's output
- * [B, out_i] with row stride act_strides[i] (host array, elements): ReLU then
- * storage rounding on hidden layers; fp32 logits on a linear last layer.  If
+ * [B, out_i] with row stride act_strides[i] (host array, elements): the
+ * activation (ReLU or SwishRN, then storage rounding) on hidden layers; fp32
+ * logits on a linear last layer.  SwishRN layers also write their pre and
+ * rinv buffers (lattice_linear).  If
  * loss != NULL the masked BCE is evaluated on the logits (which must then be
  * contiguous, act_strides[last] == T).  `in` is [B, in_0] with row stride
  * in_stride, storage dtype.  Errors: INVALID_ARG, WORKSPACE, HIP. */
@@ -264,9 +302,11 @@ lattice_status lattice_mlp_heads_fwd(const lattice_mlp_desc* desc, int32_t B, co
                                      void* ws, size_t ws_bytes, void* stream);
 
 /* Backward: d_out is the gradient of the last layer's output (storage dtype;
- * for relu_last the gradient of the post-ReLU output, masked here by
- * acts[last] > 0).  Writes dW/db of every layer (fp32, overwritten, summed
- * over the batch in a fixed order) and, if d_in != NULL, the input gradient
+ * for relu_last the gradient of the activated output, taken through the
+ * activation here: masked by acts[last] > 0, or the SwishRN backward).
+ * Writes dW/db (and dgain of SwishRN layers) of every layer (fp32,
+ * overwritten, summed over the batch in a fixed order) and, if d_in != NULL,
+ * the input gradient
  * [B, in_0] (stride d_in_stride, storage dtype, unmasked).  Errors:
  * INVALID_ARG, WORKSPACE, HIP. */
 lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, const void* in,
@@ -330,9 +370,10 @@ typedef struct {
   lattice_tables tables;
   int32_t num_features;        /* F */
   int32_t dense_in;            /* dense inputs (0: no dense path, no bottom MLP) */
-  lattice_mlp_desc bottom;     /* relu_last = 1, output width = dim */
+  lattice_mlp_desc bottom;     /* relu_last = 1, ReLU, output width = dim */
   lattice_interact_desc interact;  /* n = F + (dense_in > 0); emit_slot0 = dense_in > 0 (DOT/FM) */
-  lattice_mlp_desc top;        /* relu_last = 0, output width = T */
+  lattice_mlp_desc top;        /* relu_last = 0, output width = T; hidden layers ReLU
+                                  or SwishRN (act) */
 } lattice_model_desc;
 
 typedef struct {
@@ -422,11 +463,19 @@ typedef struct {
   int64_t bottom_act[LATTICE_MAX_LAYERS];   /* [B, out_i] hidden bottom outputs (last: in X) */
   int64_t top_act[LATTICE_MAX_LAYERS];      /* [B, out_i] hidden top outputs (last: logits) */
   /* Gradient chain, storage dtype, [B, out_i]: the gradient of layer i's
-   * output masked by its ReLU, i.e. the left operand of that layer's weight
-   * gradient dW_i = g_i^T h_i.  top_grad[last] is d_logits_op; bottom_grad[last]
+   * pre-activation (its output's gradient masked by the ReLU, or taken
+   * through the SwishRN backward), i.e. the left operand of that layer's
+   * weight gradient dW_i = g_i^T h_i.  top_grad[last] is d_logits_op; bottom_grad[last]
    * is the masked gradient of the bottom output (slot 0 of X). */
   int64_t top_grad[LATTICE_MAX_LAYERS];
   int64_t bottom_grad[LATTICE_MAX_LAYERS];
+  /* SwishRN hidden top layers (else -1): the pre-activation h [B, out_i]
+   * (storage dtype), rho [B, groups_i] (fp32), and the gradient of the layer's
+   * output [B, out_i] (storage dtype) from which top_grad[i] is taken through
+   * the SwishRN backward. */
+  int64_t top_pre[LATTICE_MAX_LAYERS];
+  int64_t top_rinv[LATTICE_MAX_LAYERS];
+  int64_t top_gout[LATTICE_MAX_LAYERS];
   int64_t unique_rows, seg_offsets, sorted_bags, num_unique, grad_rows;
   int64_t interact;     /* interaction workspace (saved state from forward to backward) */
   int64_t scratch;      /* scratch shared by the dense stages */

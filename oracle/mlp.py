@@ -97,7 +97,8 @@ def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=
     """Backward through ``mlp_forward``.  ``g_out`` is dL/d(hs[-1]) (before the
     last ReLU mask when ``relu_last``).  Returns (dWs, dbs, dL/dh0 or None).
     With ``act`` (as in ``mlp_forward``) the gain gradients of the SwishRN
-    layers go to ``dgains[i] = (dga, dgb)``."""
+    layers go to ``dgains[i] = (dga, dgb)``; ``act["overrides"][i]``, when
+    given, is layer i's ``swishrn.backward`` gate-derivative override."""
     L = len(layers)
 
     def through(i, g):
@@ -106,7 +107,8 @@ def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=
             return rnd(g * masks[i])
         ga, gb = act["gains"][i]
         go = rnd(g)
-        dh, dga, dgb = _swishrn.backward(go, masks[i]["pre"], ga, gb, act["block"], act["eps"], act["kind"])
+        dh, dga, dgb = _swishrn.backward(go, masks[i]["pre"], ga, gb, act["block"], act["eps"], act["kind"],
+                                         grad_override=(act.get("overrides") or {}).get(i))
         if dgains is not None:
             dgains[i] = (dga, dgb)
         return rnd(dh)

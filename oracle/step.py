@@ -45,7 +45,8 @@ def top_act(cfg, params):
 
 def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None, fp8_top=False):
     """``overrides`` (optional) maps "bottom"/"top" to per-layer ReLU decision
-    overrides (see ``mlp.mlp_forward``); ``loss_normalizer`` (optional) is the
+    overrides (see ``mlp.mlp_forward``) and "top_gate" to per-layer hard-gate
+    derivative overrides of the backward (see ``swishrn.backward``); ``loss_normalizer`` (optional) is the
     labelled-entry count of the full batch when ``batch`` holds a subset of
     its samples.  ``fp8_top``: the top MLP's hidden layers run their forward
     product in FP8 with row-wise scales (mixed FP8 / BF16 training, Section
@@ -86,6 +87,7 @@ def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None, fp8
                          fp8_layers=tuple(range(len(params["top"]) - 1)) if fp8_top else (),
                          act=top_act(cfg, params))
     c["hs_top"], c["masks_top"] = hs_top, mt
+    c["gate_overrides"] = (overrides or {}).get("top_gate")
     z = hs_top[-1]
     loss, dz = masked_bce(z, batch["labels"], batch["mask"], loss_normalizer)
     c.update(logits=z, loss=loss, dz=dz, t=t)
@@ -100,6 +102,8 @@ def backward(cfg, params, table, batch, c, lr_tables=None):
     g = {}
     gz = rnd(c["dz"])
     act = top_act(cfg, params)
+    if act is not None:
+        act["overrides"] = c.get("gate_overrides")
     dgains = [None] * (len(params["top"]) - 1)
     dWt, dbt, dt = mlp_backward(gz, c["hs_top"], c["masks_top"], params["top"], rnd, relu_last=False,
                                 need_input_grad=True, act=act, dgains=dgains)

@@ -89,17 +89,20 @@ def forward(h, ga, gb, block, eps, kind, rho=None):
     return ga * n * gate(gb * n, kind), n, rho
 
 
-def backward(do, h, ga, gb, block, eps, kind, rho=None, kink_grad=None):
-    """Returns ``(dh, dga, dgb)`` given ``do = dL/d out``.  ``kink_grad``
-    (optional, hard gate): the value ``gate'`` takes where ``|z| == 3``
-    exactly (default: 0, the outside value)."""
+def backward(do, h, ga, gb, block, eps, kind, rho=None, grad_override=None):
+    """Returns ``(dh, dga, dgb)`` given ``do = dL/d out``.
+    ``grad_override`` (optional, hard gate): ``(where, value)``, the value
+    ``gate'`` takes at the positions ``where`` instead of its own (parity
+    tests use it only where the side of a kink at +-3 is not fixed by the
+    arithmetic; either one-sided derivative is then a correct result)."""
     do = np.asarray(do, np.float64)
     ga, gb = np.asarray(ga, np.float64), np.asarray(gb, np.float64)
     _, n, rho = forward(h, ga, gb, block, eps, kind, rho)
     a, z = ga * n, gb * n
     s, sp = gate(z, kind), gate_grad(z, kind)
-    if kind == "hard" and kink_grad is not None:
-        sp = np.where(np.abs(z) == 3.0, kink_grad, sp)
+    if grad_override is not None:
+        where, value = grad_override
+        sp = np.where(where, value, sp)
     da = do * s
     dz = do * a * sp
     dga = (da * n).sum(axis=0)

@@ -17,6 +17,8 @@ F32, BF16 = 0, 1
 POOL_SUM, POOL_MEAN = 0, 1
 DOT, FM, STACK = 0, 1, 2
 FP8_ROWWISE, FP8_TENSORWISE = 0, 1
+ACT_RELU, ACT_SWISHRN, ACT_HARDSWISHRN = 0, 1, 2
+BLOCKNORM_COLS = 128
 
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "WORKSPACE", 4: "BAD_INPUT", 5: "HIP"}
 
@@ -50,12 +52,13 @@ class lattice_interact_desc(Structure):
 
 class lattice_linear(Structure):
     _fields_ = [("in_dim", c_int32), ("out_dim", c_int32), ("W", c_void_p), ("b", c_void_p),
-                ("dW", c_void_p), ("db", c_void_p)]
+                ("dW", c_void_p), ("db", c_void_p), ("gain", c_void_p), ("dgain", c_void_p),
+                ("pre", c_void_p), ("rinv", c_void_p)]
 
 
 class lattice_mlp_desc(Structure):
     _fields_ = [("dtype", c_int), ("n_layers", c_int32), ("layers", POINTER(lattice_linear)),
-                ("relu_last", c_int32)]
+                ("relu_last", c_int32), ("act", c_int), ("norm_block", c_int32), ("norm_eps", c_float)]
 
 
 class lattice_loss_desc(Structure):
@@ -93,7 +96,9 @@ class lattice_step_layout(Structure):
                  ("logits", c_int64), ("d_logits", c_int64), ("d_logits_op", c_int64),
                  ("loss", c_int64), ("d_t", c_int64), ("dX", c_int64),
                  ("bottom_act", c_int64 * MAX_LAYERS), ("top_act", c_int64 * MAX_LAYERS),
-                 ("top_grad", c_int64 * MAX_LAYERS), ("bottom_grad", c_int64 * MAX_LAYERS)]
+                 ("top_grad", c_int64 * MAX_LAYERS), ("bottom_grad", c_int64 * MAX_LAYERS),
+                 ("top_pre", c_int64 * MAX_LAYERS), ("top_rinv", c_int64 * MAX_LAYERS),
+                 ("top_gout", c_int64 * MAX_LAYERS)]
                 + [(k, c_int64) for k in ("unique_rows", "seg_offsets", "sorted_bags",
                                           "num_unique", "grad_rows", "interact", "scratch",
                                           "scratch_bytes", "sparse", "sparse_bytes", "fp8",

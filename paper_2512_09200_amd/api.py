@@ -32,7 +32,11 @@ def _stream(stream):
 
 
 def _row_stride(t):
-    if t.dim() != 2 or t.stride(1) != 1:
+    if t.dim() != 2:
+        raise ValueError("expected a 2-D tensor")
+    if t.shape[0] == 0:
+        return t.shape[1]            # no rows: any stride >= the width
+    if t.stride(1) != 1 and t.shape[1] > 1:
         raise ValueError("expected a 2-D tensor with unit column stride")
     return t.stride(0)
 
@@ -189,26 +193,40 @@ def lattice_interact_bwd(kind, X, d_out, dX, emit_slot0=False, fm_W=None, fm_dW=
 
 
 # ---------------------------------------------------------------------------
-def mlp_desc(layers, relu_last, dtype):
-    """layers: list of dicts with W, b (optional), dW, db (optional)."""
+_ACT = {None: A.ACT_RELU, "relu": A.ACT_RELU, "swishrn": A.ACT_SWISHRN, "hardswishrn": A.ACT_HARDSWISHRN}
+
+
+def mlp_desc(layers, relu_last, dtype, act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
+    """layers: list of dicts with W, b (optional), dW, db (optional); SwishRN
+    layers (act "swishrn" / "hardswishrn") also gain [2, out] fp32, dgain
+    (optional), and for lattice_mlp_heads_fwd/bwd pre [B, out] (storage
+    dtype) and rinv [B, groups] fp32."""
     arr = (A.lattice_linear * len(layers))()
     for i, L in enumerate(layers):
         W = L["W"]
         _contig(W)
         arr[i] = A.lattice_linear(in_dim=W.shape[1], out_dim=W.shape[0], W=W.data_ptr(),
-                                  b=L["b"].data_ptr() if L.get("b") is not None else None,
-                                  dW=L["dW"].data_ptr() if L.get("dW") is not None else None,
-                                  db=L["db"].data_ptr() if L.get("db") is not None else None)
-    d = A.lattice_mlp_desc(dtype=dtype, n_layers=len(layers), layers=arr, relu_last=int(relu_last))
+                                  b=_ptr(L.get("b")), dW=_ptr(L.get("dW")), db=_ptr(L.get("db")),
+                                  gain=_ptr(L.get("gain")), dgain=_ptr(L.get("dgain")),
+                                  pre=_ptr(L.get("pre")), rinv=_ptr(L.get("rinv")))
+    d = A.lattice_mlp_desc(dtype=dtype, n_layers=len(layers), layers=arr, relu_last=int(relu_last),
+                           act=_ACT[act], norm_block=int(norm_block), norm_eps=float(norm_eps))
     d._keep = arr
     return d
 
 
-def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None):
+def swishrn_groups(N, norm_block):
+    """Normalisation groups of a SwishRN layer of width N (columns of rinv)."""
+    return 1 if norm_block <= 0 or norm_block >= N else -(-N // norm_block)
+
+
+def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None, act=None,
+                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
     """acts: list of output tensors (2-D, unit column stride); loss: optional
-    dict(labels, mask, loss, d_logits, d_logits_op)."""
+    dict(labels, mask, loss, d_logits, d_logits_op); act / norm_block /
+    norm_eps: the activation (see mlp_desc)."""
     lib = load()
-    d = mlp_desc(layers, relu_last, _dt(x))
+    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps)
     n = len(layers)
     ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
     strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
@@ -225,9 +243,10 @@ def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None):
                                     _stream(stream)))
 
 
-def lattice_mlp_heads_bwd(layers, x, acts, d_out, relu_last, d_in=None, stream=None):
+def lattice_mlp_heads_bwd(layers, x, acts, d_out, relu_last, d_in=None, stream=None, act=None,
+                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
     lib = load()
-    d = mlp_desc(layers, relu_last, _dt(x))
+    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps)
     n = len(layers)
     ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
     strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
@@ -284,18 +303,21 @@ class StepModel:
     """Marshals a model's device tensors into a lattice_model_desc.
 
     tables [R, d], row_base int64 [F+1]; bottom/top: lists of dicts
-    {W, b, dW, db}; fm_W / fm_dW for the FM interaction; max_rows: rows of the
-    largest table (None: read from row_base once, here)."""
+    {W, b, dW, db} (SwishRN top layers: also gain, dgain); fm_W / fm_dW for
+    the FM interaction; max_rows: rows of the largest table (None: read from
+    row_base once, here); top_act: None / "relu", "swishrn" or "hardswishrn"
+    for the top MLP's hidden layers."""
 
     def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
                  fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5,
-                 max_rows=None):
+                 max_rows=None, top_act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
         _contig(tables, row_base)
         dt = _dt(tables)
         d = tables.shape[1]
         n = num_features + (1 if dense_in > 0 else 0)
         self._bottom = mlp_desc(bottom, True, dt) if dense_in > 0 else A.lattice_mlp_desc(dtype=dt)
-        self._top = mlp_desc(top, False, dt)
+        self._top = mlp_desc(top, False, dt, top_act, norm_block, norm_eps)
+        self.top_act, self.norm_block = top_act, norm_block
         self._stack = stack_layers(stack) if stack else None
         rank = fm_W.shape[1] if fm_W is not None else (stack[0]["W"].shape[1] if stack else 0)
         idesc = A.lattice_interact_desc(kind=_KIND[interact], dtype=dt, n=n, dim=d, rank=rank,
@@ -406,6 +428,11 @@ def step_views(model, ws, layout, B, T, nnz):
     tops = model.tensors["top"]
     v["top_act"] = [view(layout.top_act[i], (B, tops[i]["W"].shape[0]), dt) for i in range(len(tops) - 1)]
     v["top_grad"] = [view(layout.top_grad[i], (B, tops[i]["W"].shape[0]), dt) for i in range(len(tops))]
+    outs = [tops[i]["W"].shape[0] for i in range(len(tops) - 1)]
+    v["top_pre"] = [view(layout.top_pre[i], (B, o), dt) for i, o in enumerate(outs)]
+    v["top_rinv"] = [view(layout.top_rinv[i], (B, swishrn_groups(o, model.norm_block)), torch.float32)
+                     for i, o in enumerate(outs)]
+    v["top_gout"] = [view(layout.top_gout[i], (B, o), dt) for i, o in enumerate(outs)]
     bots = model.tensors["bottom"]
     v["bottom_act"] = [view(layout.bottom_act[i], (B, bots[i]["W"].shape[0]), dt)
                        for i in range(len(bots) - 1)] if model.dense_in > 0 else []

@@ -4,12 +4,14 @@
 // reports.
 #include <cstdarg>
 #include <cstdio>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 
 #include "../../include/lattice.h"
 #include "common.h"
 #include "kernels.h"
+#include "swishrn.h"
 
 namespace lat {
 static thread_local char g_err[1024] = "";
@@ -86,11 +88,17 @@ static hipError_t zero_f32(float* p, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
+// layer i applies SwishRN
+static bool swish_layer(const lattice_mlp_desc* d, int i) {
+  return d->act != LATTICE_ACT_RELU && (i < d->n_layers - 1 || d->relu_last);
+}
+
 static hipError_t zero_mlp_grads(const lattice_mlp_desc* d, hipStream_t s) {
   for (int i = 0; i < d->n_layers; ++i) {
     const lattice_linear& L = d->layers[i];
     hipError_t e = zero_f32(L.dW, (int64_t)L.out_dim * L.in_dim, s);
     if (e == hipSuccess) e = zero_f32(L.db, L.out_dim, s);
+    if (e == hipSuccess && swish_layer(d, i)) e = zero_f32(L.dgain, 2 * (int64_t)L.out_dim, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -514,13 +522,33 @@ static lattice_status check_mlp(const lattice_mlp_desc* d, int32_t B) {
   REQUIRE(d->n_layers >= 1 && d->n_layers <= LATTICE_MAX_LAYERS, "n_layers %d outside 1..%d",
           d->n_layers, LATTICE_MAX_LAYERS);
   REQUIRE(d->dtype == LATTICE_F32 || d->dtype == LATTICE_BF16, "bad dtype");
+  REQUIRE(d->act == LATTICE_ACT_RELU || d->act == LATTICE_ACT_SWISHRN ||
+              d->act == LATTICE_ACT_HARDSWISHRN, "bad activation %d", (int)d->act);
+  if (d->act != LATTICE_ACT_RELU) {
+    REQUIRE(d->norm_block == 0 || d->norm_block == LATTICE_BLOCKNORM_COLS,
+            "norm_block must be 0 or %d", LATTICE_BLOCKNORM_COLS);
+    REQUIRE(d->norm_eps >= 0.f && d->norm_eps < INFINITY, "norm_eps must be finite and >= 0");
+  }
   for (int i = 0; i < d->n_layers; ++i) {
     const lattice_linear& L = d->layers[i];
     REQUIRE(L.in_dim >= 1 && L.out_dim >= 1 && L.W, "layer %d: bad dims or null W", i);
     if (i > 0) REQUIRE(L.in_dim == d->layers[i - 1].out_dim, "layer %d: in_dim mismatch", i);
+    if (swish_layer(d, i)) REQUIRE(L.gain, "layer %d: SwishRN needs gains", i);
   }
   return LATTICE_OK;
 }
+
+static int gate_of(const lattice_mlp_desc* d) {
+  return d->act == LATTICE_ACT_SWISHRN ? GATE_SIGMOID : GATE_HARD;
+}
+
+// Where the SwishRN layers keep what the backward needs: per layer, the
+// pre-activation, rho, and (backward) the gradient of the layer's output.
+struct ActBufs {
+  void* pre[LATTICE_MAX_LAYERS] = {};
+  float* rinv[LATTICE_MAX_LAYERS] = {};
+  void* gout[LATTICE_MAX_LAYERS] = {};
+};
 
 // split-K bound of the MLP backward products (the factor itself comes from
 // gemm_splits' time estimate)
@@ -538,6 +566,7 @@ static size_t mlp_bwd_ws(const lattice_mlp_desc* d, int B) {
     g.M = B; g.N = L.in_dim; g.K = L.out_dim;
     s = std::max(s, gemm_workspace(g));
     s = std::max(s, colsum_workspace(B, L.out_dim));
+    if (swish_layer(d, i)) s = std::max(s, swishrn_gain_workspace(B, L.out_dim));
   }
   return al256(s);
 }
@@ -549,20 +578,47 @@ static size_t mlp_gbuf_elems(const lattice_mlp_desc* d, int B) {
   return (size_t)w * B;
 }
 
+// SwishRN layers (ab): bf16 models with BlockNorm groups take the statistic
+// in the GEMM's epilogue; otherwise the GEMM stores the pre-activation and a
+// row kernel normalises it.
 static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
-                              void* const* acts, const int64_t* strides, hipStream_t s) {
+                              void* const* acts, const int64_t* strides, const ActBufs* ab,
+                              hipStream_t s) {
+  const DType dt = dt_of(d->dtype);
   for (int i = 0; i < d->n_layers; ++i) {
     const lattice_linear& L = d->layers[i];
     const bool last = i == d->n_layers - 1;
     GemmArgs g;
-    g.dt = dt_of(d->dtype);
+    g.dt = dt;
     g.A = i == 0 ? in : acts[i - 1];
     g.lda = i == 0 ? in_stride : strides[i - 1];
     g.B = L.W; g.ldb = L.in_dim;
     g.C = acts[i]; g.ldc = strides[i];
-    g.c_dt = (last && !d->relu_last) ? DT_F32 : dt_of(d->dtype);
+    g.c_dt = (last && !d->relu_last) ? DT_F32 : dt;
     g.M = B; g.N = L.out_dim; g.K = L.in_dim;
     g.bias = L.b;
+    if (swish_layer(d, i)) {
+      if (dt == DT_BF16 && d->norm_block == LATTICE_BLOCKNORM_COLS) {
+        g.norm_gate = gate_of(d);
+        g.gain = L.gain;
+        g.eps = d->norm_eps;
+        g.pre = ab->pre[i];
+        g.ldp = L.out_dim;
+        g.rinv = ab->rinv[i];
+        g.nblk = cdiv(L.out_dim, LATTICE_BLOCKNORM_COLS);
+        hipError_t e = gemm(g, nullptr, s);
+        if (e != hipSuccess) return e;
+      } else {
+        g.C = ab->pre[i];
+        g.ldc = L.out_dim;
+        hipError_t e = gemm(g, nullptr, s);
+        if (e == hipSuccess)
+          e = swishrn_fwd_rows(dt, ab->pre[i], L.out_dim, B, L.out_dim, d->norm_block, gate_of(d),
+                               L.gain, d->norm_eps, acts[i], strides[i], ab->rinv[i], s);
+        if (e != hipSuccess) return e;
+      }
+      continue;
+    }
     g.relu = (!last || d->relu_last) ? 1 : 0;
     hipError_t e = gemm(g, nullptr, s);  // forward GEMMs never split K
     if (e != hipSuccess) return e;
@@ -661,14 +717,49 @@ static hipError_t mlp_layer_dgrad(const lattice_mlp_desc* d, int i, int B, const
   return gemm(x, ws, s);
 }
 
-// g_last: gradient of the last layer's output, already ReLU-masked where needed.
-// Layer by layer (weights, then input gradient); hidden gradients alternate
-// between gbuf0 and gbuf1.
+// Gradient of layer j's pre-activation from the gradient of its output
+// (layer j applies SwishRN): the row kernel of the SwishRN backward.
+static hipError_t swish_back(const lattice_mlp_desc* d, int j, int B, const void* gout,
+                             int64_t gout_ld, const ActBufs* ab, void* dst, int64_t dst_ld,
+                             hipStream_t s) {
+  const lattice_linear& L = d->layers[j];
+  return swishrn_bwd_rows(dt_of(d->dtype), gout, gout_ld, ab->pre[j], L.out_dim, ab->rinv[j], B,
+                          L.out_dim, d->norm_block, gate_of(d), L.gain, dst, dst_ld, s);
+}
+
+static hipError_t swish_gain_grad(const lattice_mlp_desc* d, int j, int B, const void* gout,
+                                  int64_t gout_ld, const ActBufs* ab, void* ws, hipStream_t s) {
+  const lattice_linear& L = d->layers[j];
+  return swishrn_gain_grad(dt_of(d->dtype), gout, gout_ld, ab->pre[j], L.out_dim, ab->rinv[j], B,
+                           L.out_dim, d->norm_block, gate_of(d), L.gain, L.dgain, ws, s);
+}
+
+// Gradient of layer i-1's pre-activation (i > 0) or of the MLP's input
+// (i == 0) from g, the gradient of layer i's pre-activation: g W_i, then
+// through layer i-1's activation (ReLU mask, or the SwishRN backward via its
+// output gradient ab->gout[i-1]).
+static hipError_t mlp_chain_step(const lattice_mlp_desc* d, int i, int B, const void* g, int64_t gs,
+                                 const void* const* acts, const int64_t* strides, const ActBufs* ab,
+                                 void* dst, int64_t dst_ld, void* ws, hipStream_t s) {
+  if (i > 0 && swish_layer(d, i - 1)) {
+    const int64_t ldo = d->layers[i - 1].out_dim;
+    hipError_t e = mlp_layer_dgrad(d, i, B, g, gs, ab->gout[i - 1], ldo, nullptr, 0, ws, s);
+    if (e != hipSuccess) return e;
+    return swish_back(d, i - 1, B, ab->gout[i - 1], ldo, ab, dst, dst_ld, s);
+  }
+  return mlp_layer_dgrad(d, i, B, g, gs, dst, dst_ld, i > 0 ? acts[i - 1] : nullptr,
+                         i > 0 ? strides[i - 1] : 0, ws, s);
+}
+
+// g_last: gradient of the last layer's pre-activation (already taken through
+// its activation where it has one).  Layer by layer (weights, gains of the
+// layer below, then input gradient); hidden gradients alternate between
+// gbuf0 and gbuf1.
 static hipError_t mlp_backward(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
                                const void* const* acts, const int64_t* strides,
                                const void* g_last, int64_t g_last_stride, void* d_in,
-                               int64_t d_in_stride, void* gbuf0, void* gbuf1, void* ws,
-                               hipStream_t s) {
+                               int64_t d_in_stride, void* gbuf0, void* gbuf1, const ActBufs* ab,
+                               void* ws, hipStream_t s) {
   const void* g = g_last;
   int64_t gs = g_last_stride;
   for (int i = d->n_layers - 1; i >= 0; --i) {
@@ -680,8 +771,9 @@ static hipError_t mlp_backward(const lattice_mlp_desc* d, int B, const void* in,
     if (i > 0 || d_in) {
       void* dst = i > 0 ? ((d->n_layers - 1 - i) % 2 == 0 ? gbuf0 : gbuf1) : d_in;
       const int64_t dst_ld = i > 0 ? L.in_dim : d_in_stride;
-      e = mlp_layer_dgrad(d, i, B, g, gs, dst, dst_ld, i > 0 ? acts[i - 1] : nullptr,
-                          i > 0 ? strides[i - 1] : 0, ws, s);
+      e = mlp_chain_step(d, i, B, g, gs, acts, strides, ab, dst, dst_ld, ws, s);
+      if (e == hipSuccess && i > 0 && swish_layer(d, i - 1))
+        e = swish_gain_grad(d, i - 1, B, ab->gout[i - 1], L.in_dim, ab, ws, s);
       if (e != hipSuccess) return e;
       g = dst;
       gs = dst_ld;
@@ -691,19 +783,19 @@ static hipError_t mlp_backward(const lattice_mlp_desc* d, int B, const void* in,
 }
 
 // The gradient chain alone: hidden gradients into gl[i] (gradient of layer
-// i's output, [B, out_i], i < n-1) and the input gradient into d_in (if any).
+// i's pre-activation, [B, out_i], i < n-1) and the input gradient into d_in
+// (if any).
 static hipError_t mlp_backward_data(const lattice_mlp_desc* d, int B, const void* const* acts,
                                     const int64_t* strides, const void* g_last,
                                     int64_t g_last_stride, void* d_in, int64_t d_in_stride,
-                                    void* const* gl, void* ws, hipStream_t s) {
+                                    void* const* gl, const ActBufs* ab, void* ws, hipStream_t s) {
   const void* g = g_last;
   int64_t gs = g_last_stride;
   for (int i = d->n_layers - 1; i >= 0; --i) {
     if (i == 0 && !d_in) break;
     void* dst = i > 0 ? gl[i - 1] : d_in;
     const int64_t dst_ld = i > 0 ? d->layers[i].in_dim : d_in_stride;
-    hipError_t e = mlp_layer_dgrad(d, i, B, g, gs, dst, dst_ld, i > 0 ? acts[i - 1] : nullptr,
-                                   i > 0 ? strides[i - 1] : 0, ws, s);
+    hipError_t e = mlp_chain_step(d, i, B, g, gs, acts, strides, ab, dst, dst_ld, ws, s);
     if (e != hipSuccess) return e;
     g = dst;
     gs = dst_ld;
@@ -711,17 +803,20 @@ static hipError_t mlp_backward_data(const lattice_mlp_desc* d, int B, const void
   return hipSuccess;
 }
 
-// Weight and bias gradients of every layer from the stored chain.
+// Weight and bias gradients of every layer from the stored chain, and the
+// gains of the hidden SwishRN layers from their stored output gradients.
 static hipError_t mlp_backward_weights(const lattice_mlp_desc* d, int B, const void* in,
                                        int64_t in_stride, const void* const* acts,
                                        const int64_t* strides, const void* g_last,
-                                       int64_t g_last_stride, void* const* gl, void* ws,
-                                       hipStream_t s) {
+                                       int64_t g_last_stride, void* const* gl, const ActBufs* ab,
+                                       void* ws, hipStream_t s) {
   for (int i = d->n_layers - 1; i >= 0; --i) {
     const void* g = i == d->n_layers - 1 ? g_last : gl[i];
     const int64_t gs = i == d->n_layers - 1 ? g_last_stride : d->layers[i].out_dim;
     hipError_t e = mlp_layer_wgrad(d, i, B, g, gs, i == 0 ? in : acts[i - 1],
                                    i == 0 ? in_stride : strides[i - 1], ws, s);
+    if (e == hipSuccess && i < d->n_layers - 1 && swish_layer(d, i))
+      e = swish_gain_grad(d, i, B, ab->gout[i], d->layers[i].out_dim, ab, ws, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -745,7 +840,19 @@ __global__ void relu_mask_kernel(const void* g, int64_t gs, const void* act, int
 static size_t mlp_heads_ws(const lattice_mlp_desc* d, int B) {
   const size_t g = al256(mlp_gbuf_elems(d, B) * esize(d->dtype));
   const int T = d->layers[d->n_layers - 1].out_dim;
-  return mlp_bwd_ws(d, B) + 3 * g + al256(bce_workspace((int64_t)B * T));
+  return mlp_bwd_ws(d, B) + 4 * g + al256(bce_workspace((int64_t)B * T));
+}
+
+// The caller's per-layer SwishRN buffers (lattice_linear.pre / rinv).
+static lattice_status layer_bufs(const lattice_mlp_desc* d, int B, ActBufs* ab) {
+  for (int i = 0; i < d->n_layers; ++i) {
+    if (!swish_layer(d, i)) continue;
+    const lattice_linear& L = d->layers[i];
+    REQUIRE((L.pre && L.rinv) || B == 0, "layer %d: SwishRN needs pre and rinv buffers", i);
+    ab->pre[i] = L.pre;
+    ab->rinv[i] = L.rinv;
+  }
+  return LATTICE_OK;
 }
 
 extern "C" {
@@ -774,7 +881,10 @@ lattice_status lattice_mlp_heads_fwd(const lattice_mlp_desc* desc, int32_t B, co
     const size_t need = bce_workspace((int64_t)B * T);
     if (ws_bytes < need || !ws) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
   }
-  if (B > 0) HIPRET(mlp_forward(desc, B, in, in_stride, acts, act_strides, strm(stream)));
+  ActBufs ab;
+  st = layer_bufs(desc, B, &ab);
+  if (st != LATTICE_OK) return st;
+  if (B > 0) HIPRET(mlp_forward(desc, B, in, in_stride, acts, act_strides, &ab, strm(stream)));
   if (loss)
     HIPRET(bce((const float*)acts[desc->n_layers - 1], loss->labels, loss->mask, (int64_t)B * T,
                loss->loss, loss->d_logits, loss->d_logits_op, dt_of(desc->dtype), ws,
@@ -801,16 +911,27 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
     HIPRET(zero_mlp_grads(desc, strm(stream)));
     return LATTICE_OK;
   }
+  ActBufs ab;
+  st = layer_bufs(desc, B, &ab);
+  if (st != LATTICE_OK) return st;
   char* p = (char*)ws;
   void* gemm_ws = p; p += mlp_bwd_ws(desc, B);
   const size_t g = al256(mlp_gbuf_elems(desc, B) * esize(desc->dtype));
   void* gb0 = p; p += g;
   void* gb1 = p; p += g;
-  void* masked = p;
+  void* masked = p; p += g;
+  void* gout = p;  // gradient of a hidden SwishRN layer's output (one at a time)
+  for (int i = 0; i + 1 < L; ++i) ab.gout[i] = gout;
   const void* g_last = d_out;
   int64_t g_ld = d_out_stride;
-  if (desc->relu_last && B > 0) {
-    relu_mask_kernel<<<cdiv((int64_t)B * T, 256), 256, 0, strm(stream)>>>(
+  hipStream_t s = strm(stream);
+  if (desc->relu_last && swish_layer(desc, L - 1)) {
+    HIPRET(swish_gain_grad(desc, L - 1, B, d_out, d_out_stride, &ab, gemm_ws, s));
+    HIPRET(swish_back(desc, L - 1, B, d_out, d_out_stride, &ab, masked, T, s));
+    g_last = masked;
+    g_ld = T;
+  } else if (desc->relu_last) {
+    relu_mask_kernel<<<cdiv((int64_t)B * T, 256), 256, 0, s>>>(
         d_out, d_out_stride, acts[L - 1], act_strides[L - 1], B, T, desc->dtype == LATTICE_BF16,
         masked);
     if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
@@ -818,7 +939,7 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
     g_ld = T;
   }
   HIPRET(mlp_backward(desc, B, in, in_stride, acts, act_strides, g_last, g_ld, d_in, d_in_stride,
-                      gb0, gb1, gemm_ws, strm(stream)));
+                      gb0, gb1, &ab, gemm_ws, s));
   return LATTICE_OK;
 }
 
@@ -853,6 +974,8 @@ static lattice_status check_model(const lattice_model_desc* m, int B) {
     REQUIRE(m->bottom.layers[0].in_dim == m->dense_in, "bottom input width != dense_in");
     REQUIRE(m->bottom.layers[m->bottom.n_layers - 1].out_dim == d, "bottom output width != dim");
     REQUIRE(m->bottom.dtype == m->dtype, "bottom dtype");
+    if (m->bottom.act != LATTICE_ACT_RELU)
+      FAIL(LATTICE_ERR_UNSUPPORTED, "the step's bottom MLP uses ReLU (SwishRN: top MLP)");
   }
   st = check_mlp(&m->top, B);
   if (st != LATTICE_OK) return st;
@@ -880,6 +1003,7 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   if (o && o->fp8_top) {
     REQUIRE(o->fp8_top == 1 || o->fp8_top == 2, "fp8_top must be 0, 1 or 2");
     if (m->dtype != LATTICE_BF16) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs a bf16 model");
+    if (m->top.act != LATTICE_ACT_RELU) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs ReLU layers");
   }
   const size_t es = esize(m->dtype);
   const int d = m->tables.dim;
@@ -896,6 +1020,14 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   if (m->dense_in > 0)
     for (int i = 0; i + 1 < m->bottom.n_layers; ++i) L.bottom_act[i] = take((size_t)B * m->bottom.layers[i].out_dim * es);
   for (int i = 0; i + 1 < m->top.n_layers; ++i) L.top_act[i] = take((size_t)B * m->top.layers[i].out_dim * es);
+  for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) L.top_pre[i] = L.top_rinv[i] = L.top_gout[i] = -1;
+  if (m->top.act != LATTICE_ACT_RELU)
+    for (int i = 0; i + 1 < m->top.n_layers; ++i) {
+      const int o = m->top.layers[i].out_dim;
+      L.top_pre[i] = take((size_t)B * o * es);
+      L.top_rinv[i] = take((size_t)B * swishrn_groups(o, m->top.norm_block) * 4);
+      L.top_gout[i] = take((size_t)B * o * es);
+    }
   L.logits = take((size_t)B * P->T * 4);
   L.d_logits = take((size_t)B * P->T * 4);
   L.d_logits_op = take((size_t)B * P->T * es);
@@ -1066,7 +1198,8 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
       }
       bacts[nb - 1] = X;
       bstr[nb - 1] = (int64_t)n * d;
-      HIP_TRY(mlp_forward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, on));
+      const ActBufs none;
+      HIP_TRY(mlp_forward(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, &none, on));
     }
     if (ev && ev[2 * LATTICE_STAGE_BOTTOM_FWD + 1])
       HIP_TRY(hipEventRecord((hipEvent_t)ev[2 * LATTICE_STAGE_BOTTOM_FWD + 1], on));
@@ -1115,6 +1248,13 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   tstr[nt - 1] = T;
   void* gtop[LATTICE_MAX_LAYERS];
   for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) gtop[i] = at(P.g_top[i]);
+  ActBufs tab;  // SwishRN hidden layers: pre-activations, statistics, output gradients
+  for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) {
+    tab.pre[i] = at(L.top_pre[i]);
+    tab.rinv[i] = (float*)at(L.top_rinv[i]);
+    tab.gout[i] = at(L.top_gout[i]);
+  }
+  const bool top_swish = m->top.act != LATTICE_ACT_RELU;
   const lattice_linear& head = m->top.layers[nt - 1];
   const void* head_in = nt > 1 ? tacts[nt - 2] : t;
   const int64_t head_ld = nt > 1 ? tstr[nt - 2] : P.t_stride;
@@ -1126,21 +1266,25 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     if (nt > 1 && opts->fp8_top)
       HIPRET(mlp_forward_fp8(&hidden, B, t, P.t_stride, tacts, tstr, at(L.fp8), opts->fp8_top == 2, s));
     else if (nt > 1)
-      HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, s));
+      HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, &tab, s));
     HIPRET(head_fwd((const bf16_t*)head_in, head_ld, B, head.in_dim, (const bf16_t*)head.W, head.b,
                     T, batch->labels, batch->mask, (float*)at(L.logits), scratch, s));
   } else {
     if (opts->fp8_top) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs the fused bf16 heads (<= 64 objectives)");
-    HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, s));
+    HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, &tab, s));
   }
   HIPRET(end(LATTICE_STAGE_TOP_FWD));
   HIPRET(begin(LATTICE_STAGE_LOSS));
   if (fused_heads) {
-    void* g_head = nt > 1 ? gtop[nt - 2] : at(L.d_t);
+    // the heads' input gradient: masked by the ReLU, or (SwishRN) the
+    // gradient of the last hidden layer's output, taken through the SwishRN
+    // backward at the start of the top backward
+    void* g_head = nt > 1 ? (top_swish ? tab.gout[nt - 2] : gtop[nt - 2]) : at(L.d_t);
     const int64_t g_ld = nt > 1 ? head.in_dim : P.t_stride;
     HIPRET(head_bwd((const float*)at(L.logits), batch->labels, batch->mask, B, T,
-                    (const bf16_t*)head.W, head.in_dim, nt > 1 ? (const bf16_t*)head_in : nullptr,
-                    head_ld, (float*)at(L.loss), (float*)at(L.d_logits), (bf16_t*)at(L.d_logits_op),
+                    (const bf16_t*)head.W, head.in_dim,
+                    nt > 1 && !top_swish ? (const bf16_t*)head_in : nullptr, head_ld,
+                    (float*)at(L.loss), (float*)at(L.d_logits), (bf16_t*)at(L.d_logits_op),
                     (bf16_t*)g_head, g_ld, scratch, s));
   } else {
     HIPRET(bce((const float*)at(L.logits), batch->labels, batch->mask, (int64_t)B * T,
@@ -1150,12 +1294,15 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   // 6. top backward, gradient chain only -> d_t (weight gradients: 8.)
   HIPRET(begin(LATTICE_STAGE_TOP_BWD));
   if (fused_heads) {
+    if (nt > 1 && top_swish)
+      HIPRET(swish_back(&hidden, nt - 2, B, tab.gout[nt - 2], head.in_dim, &tab, gtop[nt - 2],
+                        head.in_dim, s));
     if (nt > 1)
       HIPRET(mlp_backward_data(&hidden, B, tacts, tstr, gtop[nt - 2], head.in_dim, at(L.d_t),
-                               P.t_stride, gtop, scratch, s));
+                               P.t_stride, gtop, &tab, scratch, s));
   } else {
     HIPRET(mlp_backward_data(&m->top, B, tacts, tstr, at(L.d_logits_op), T, at(L.d_t), P.t_stride,
-                             gtop, scratch, s));
+                             gtop, &tab, scratch, s));
   }
   HIPRET(end(LATTICE_STAGE_TOP_BWD));
   // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
@@ -1181,7 +1328,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   };
   HIPRET(wbegin(LATTICE_STAGE_TOP_WGRAD));
   HIPRET(mlp_backward_weights(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, gtop,
-                              scratch, ws_stream));
+                              &tab, scratch, ws_stream));
   HIPRET(wend(LATTICE_STAGE_TOP_WGRAD));
   // 9. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
   HIPRET(wbegin(LATTICE_STAGE_BOTTOM_BWD));
@@ -1192,10 +1339,11 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
     void* gbot[LATTICE_MAX_LAYERS];
     for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) gbot[i] = at(P.g_bot[i]);
-    HIPRET(mlp_backward_data(&m->bottom, B, bacts, bstr, masked, d, nullptr, 0, gbot, scratch,
+    const ActBufs none;
+    HIPRET(mlp_backward_data(&m->bottom, B, bacts, bstr, masked, d, nullptr, 0, gbot, &none, scratch,
                              ws_stream));
     HIPRET(mlp_backward_weights(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, masked, d,
-                                gbot, scratch, ws_stream));
+                                gbot, &none, scratch, ws_stream));
   }
   HIPRET(wend(LATTICE_STAGE_BOTTOM_BWD));
   // 10. row-coalesced embedding gradient (+ row-sparse SGD) once the sort is done

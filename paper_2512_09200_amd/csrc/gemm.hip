@@ -22,10 +22,20 @@
 // Epilogue: + bias[n], + addend[m, n], + C (accumulate), ReLU, or multiply by
 // (mask[m, n] > 0) (the ReLU derivative read from a stored activation), then
 // round to the output dtype.
+//
+// BlockNorm epilogue (SwishRN, Sections 3.3.4 and 3.5.3): the pre-activation
+// h = acc + bias is normalised over each row's 128-column group -- exactly
+// the columns of one 128x128 tile (half a 256x256 tile), so the statistic
+// needs no data from another workgroup -- and C = (g_a n) * gate(g_b n) with
+// n = h / sqrt(mean h^2 + eps); h (rounded to C's dtype) and the group's
+// 1 / sqrt(...) are stored for the backward.  The 8 columns of a thread
+// belong to one aligned 16-lane group per 128 columns, so the sum of squares
+// is a 16-lane butterfly.
 #include <mutex>
 
 #include "common.h"
 #include "kernels.h"
+#include "swishrn.h"
 
 namespace lat {
 
@@ -43,7 +53,65 @@ struct Epi {
   const float* addend;  // + addend[m*ld_add + n] (fp32) or null
   int64_t ld_add, s_add;
   int accumulate;       // + the existing (fp32) C
+  // BlockNorm / SwishRN (kernels instantiated with NORM = gate): gain [2, N],
+  // pre [M, ldp] (C's dtype), rinv [M, nblk]
+  const float* gain;
+  float eps;
+  void* pre;
+  int64_t ldp;
+  float* rinv;
+  int nblk;
 };
+
+// SwishRN with BlockNorm on 8 columns col.. of row `row` of the finished
+// fp32 tile (see the header comment).  Every lane of the wave calls it (the
+// shuffles need the whole 16-lane group); rows past M and columns past N
+// store nothing.
+template <typename CT, int GATE>
+__device__ inline void epi_blocknorm8(CT* C, int64_t ldc, int row, int col, int M, int N, float* v,
+                                      const Epi& e, int vec) {
+  float ss = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const bool ok = col + t < N;
+    if (e.bias && ok) v[t] += e.bias[col + t];
+    v[t] = ok ? v[t] : 0.f;
+    ss += v[t] * v[t];
+  }
+  ss = sum16(ss);
+  const int blk = col / NORM_TILE;
+  const int cnt = max(1, min(NORM_TILE, N - blk * NORM_TILE));
+  const float r = rsqrtf(ss / (float)cnt + e.eps);
+  if (row >= M || col >= N) return;
+  if (col % NORM_TILE == 0) e.rinv[(int64_t)row * e.nblk + blk] = r;
+  float o[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const int k = min(col + t, N - 1);  // past N: any valid gain (not stored)
+    const float n = v[t] * r;
+    o[t] = (e.gain[k] * n) * gate_fn<GATE>(e.gain[N + k] * n);
+  }
+  CT* c = C + (int64_t)row * ldc + col;
+  CT* p = reinterpret_cast<CT*>(e.pre) + (int64_t)row * e.ldp + col;
+  if (vec && col + 8 <= N) {
+    if constexpr (sizeof(CT) == 2) {
+      stg16(c, Vec16<bf16_t>::pack(o));
+      stg16(p, Vec16<bf16_t>::pack(v));
+    } else {
+      stg16(c, Vec16<float>::pack(o));
+      stg16(c + 4, Vec16<float>::pack(o + 4));
+      stg16(p, Vec16<float>::pack(v));
+      stg16(p + 4, Vec16<float>::pack(v + 4));
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      if (col + t < N) {
+        st(c + t, o[t]);
+        st(p + t, v[t]);
+      }
+  }
+}
 
 template <typename CT>
 __device__ inline void epi_store(CT* C, int64_t ldc, int row, int col, float v, const Epi& e,
@@ -305,7 +373,7 @@ __device__ inline void mma_k64(const bf16_t* As, const bf16_t* Bs, int wm, int w
 // rowsum (optional, not batched): rowsum[m] = sum over k of A[m][k], added in
 // k order by the blocks of the first N tile from their LDS A tiles; with
 // split-K each split's sum goes to rs_partial[split][m].
-template <bool TA, bool TB, bool VA, bool VB, typename CT>
+template <bool TA, bool TB, bool VA, bool VB, typename CT, int NORM = 0>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     Opnd A, Opnd Bm, CT* __restrict__ C, int64_t ldc, int M, int N, int K, int k_per_split,
     float* __restrict__ partial, Epi epi, int64_t sA, int64_t sB, int64_t sC, int batched, int vec,
@@ -424,6 +492,18 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
       }
     }
   __syncthreads();
+  if constexpr (NORM != 0) {
+    // one 128-column norm group per tile row: 16 lanes per row
+#pragma unroll
+    for (int q = 0; q < (GBM * GBN / 8) / 256; ++q) {
+      const int chunk = threadIdx.x + q * 256;
+      const int rl = chunk / (GBN / 8), cl = (chunk % (GBN / 8)) * 8;
+      float v[8];
+      ld8f(Cs + rl * CLD + cl, v);
+      epi_blocknorm8<CT, NORM>(C, ldc, m0 + rl, n0 + cl, M, N, v, epi, vec);
+    }
+    return;
+  }
   // Rows of the tile, 8 columns per thread.
 #pragma unroll
   for (int q = 0; q < (GBM * GBN / 8) / 256; ++q) {
@@ -520,7 +600,7 @@ __device__ inline void mma_big_k64(const bf16_t* As, const bf16_t* Bs, int wm, i
   }
 }
 
-template <bool TA, bool TB, typename CT, int NW>
+template <bool TA, bool TB, typename CT, int NW, int NORM = 0>
 __global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, CT* __restrict__ C,
                                                               int64_t ldc, int M, int N, int K,
                                                               Epi epi, int vec,
@@ -631,6 +711,20 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, C
         }
     }
     __syncthreads();
+    if constexpr (NORM != 0) {
+      // two 128-column norm groups per tile row: lanes 0-15 and 16-31 of
+      // each 32-lane row
+#pragma unroll 4
+      for (int q = 0; q < (BBM / 2) * BBN / 8 / THREADS; ++q) {
+        const int chunk = threadIdx.x + q * THREADS;
+        const int rl = chunk / (BBN / 8), cl = (chunk % (BBN / 8)) * 8;
+        float v[8];
+        ld8f(Cs + rl * BCLD + cl, v);
+        epi_blocknorm8<CT, NORM>(C, ldc, m0 + h * 128 + rl, n0 + cl, M, N, v, epi, vec);
+      }
+      __syncthreads();
+      continue;
+    }
 #pragma unroll 4
     for (int q = 0; q < (BBM / 2) * BBN / 8 / THREADS; ++q) {
       const int chunk = threadIdx.x + q * THREADS;
@@ -730,8 +824,9 @@ size_t gemm_workspace(const GemmArgs& g) {
 }
 
 static Epi make_epi(const GemmArgs& g) {
-  return Epi{g.bias, g.relu, g.mask, g.mask_dt, g.ldm, g.s_mask, g.addend, g.ld_add, g.s_add,
-             g.accumulate};
+  return Epi{g.bias,   g.relu,     g.mask, g.mask_dt, g.ldm,  g.s_mask, g.addend,
+             g.ld_add, g.s_add,    g.accumulate,      g.gain, g.eps,    g.pre,
+             g.ldp,    g.rinv,     g.nblk};
 }
 
 static bool a16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -748,6 +843,7 @@ static int epi_vec_ok(const GemmArgs& g) {
     const int64_t me = g.mask_dt == DT_BF16 ? 8 : 4;
     if (!a16(g.mask) || g.ldm % me || g.s_mask % me) return 0;
   }
+  if (g.norm_gate && (!a16(g.pre) || g.ldp % ce)) return 0;
   return 1;
 }
 
@@ -765,7 +861,7 @@ static bool gemm_use_big(const GemmArgs& g) {
   return 308 * big_waves * s < 200 * small_waves;
 }
 
-template <bool TA, bool TB>
+template <bool TA, bool TB, int NORM>
 static hipError_t gemm_big_launch(const GemmArgs& g, hipStream_t st) {
   constexpr int NW = 4;  // 8 waves of 128x64 measured slower
   Epi epi = make_epi(g);
@@ -775,13 +871,13 @@ static hipError_t gemm_big_launch(const GemmArgs& g, hipStream_t st) {
   const dim3 grid(cdiv(g.N, BBN) * cdiv(g.M, BBM));
   static std::once_flag once_bf, once_f;
   if (g.c_dt == DT_BF16) {
-    auto k = gemm_big_kernel<TA, TB, bf16_t, NW>;
+    auto k = gemm_big_kernel<TA, TB, bf16_t, NW, NORM>;
     std::call_once(once_bf, [&] {
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_BIG_LDS);
     });
     k<<<grid, NW * 64, GEMM_BIG_LDS, st>>>(a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, epi, vec, g.rowsum);
   } else {
-    auto k = gemm_big_kernel<TA, TB, float, NW>;
+    auto k = gemm_big_kernel<TA, TB, float, NW, NORM>;
     std::call_once(once_f, [&] {
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_BIG_LDS);
     });
@@ -791,10 +887,10 @@ static hipError_t gemm_big_launch(const GemmArgs& g, hipStream_t st) {
   return hipSuccess;
 }
 
-template <bool TA, bool TB, bool VA, bool VB>
+template <bool TA, bool TB, bool VA, bool VB, int NORM>
 static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st) {
   if constexpr (VA && VB) {
-    if (gemm_use_big(g)) return gemm_big_launch<TA, TB>(g, st);
+    if (gemm_use_big(g)) return gemm_big_launch<TA, TB, NORM>(g, st);
   }
   const int splits = gemm_splits(g);
   if (splits > 1 && !ws) {
@@ -814,14 +910,14 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
   // The kernels use 72 KiB of dynamic LDS (above the 64 KiB default limit).
   static std::once_flag once_bf, once_f;
   if (g.c_dt == DT_BF16) {
-    auto k = gemm_bf16_kernel<TA, TB, VA, VB, bf16_t>;
+    auto k = gemm_bf16_kernel<TA, TB, VA, VB, bf16_t, NORM>;
     std::call_once(once_bf, [&] {
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
     });
     k<<<grid, 256, GEMM_LDS, st>>>(a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA,
                                    g.sB, g.sC, batched, vec, g.rowsum, rs_partial);
   } else {
-    auto k = gemm_bf16_kernel<TA, TB, VA, VB, float>;
+    auto k = gemm_bf16_kernel<TA, TB, VA, VB, float, NORM>;
     std::call_once(once_f, [&] {
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
     });
@@ -842,7 +938,7 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
   return hipSuccess;
 }
 
-template <bool TA, bool TB>
+template <bool TA, bool TB, int NORM = 0>
 static hipError_t gemm_bf16_dispatch(const GemmArgs& g, float* ws, hipStream_t st) {
   // 16-byte vectors (along K, or along M/N for a transposed operand) need
   // 8-element-aligned rows, segments and batch strides.
@@ -857,10 +953,10 @@ static hipError_t gemm_bf16_dispatch(const GemmArgs& g, float* ws, hipStream_t s
   const bool vb = TB ? (g.ldb % 8 == 0 && aligned16(g.B) && fits(g.N, g.ldb) && g.sB % 8 == 0 &&
                         (g.kseg == 0 || g.ksB % 8 == 0))
                      : (g.ldb % 8 == 0 && aligned16(g.B) && fits(g.K, g.ldb) && g.sB % 8 == 0 && seg_ok);
-  if (va && vb) return gemm_bf16_launch<TA, TB, true, true>(g, ws, st);
-  if (va) return gemm_bf16_launch<TA, TB, true, false>(g, ws, st);
-  if (vb) return gemm_bf16_launch<TA, TB, false, true>(g, ws, st);
-  return gemm_bf16_launch<TA, TB, false, false>(g, ws, st);
+  if (va && vb) return gemm_bf16_launch<TA, TB, true, true, NORM>(g, ws, st);
+  if (va) return gemm_bf16_launch<TA, TB, true, false, NORM>(g, ws, st);
+  if (vb) return gemm_bf16_launch<TA, TB, false, true, NORM>(g, ws, st);
+  return gemm_bf16_launch<TA, TB, false, false, NORM>(g, ws, st);
 }
 
 hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t st) {
@@ -872,6 +968,19 @@ hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t st) {
   if (g.rowsum && (g.dt != DT_BF16 || g.batch > 1)) {
     set_error("GEMM row sums: bf16 and not batched only");
     return hipErrorInvalidValue;
+  }
+  if (g.norm_gate) {
+    // the BlockNorm epilogue: forward products (A and B K-contiguous), one
+    // product, K not split, pre-activation and statistics stored
+    if (g.dt != DT_BF16 || g.ta || g.tb || g.batch > 1 || g.kseg || g.max_splits > 1 || g.mask ||
+        g.addend || g.accumulate || g.relu || g.rowsum || !g.gain || !g.pre || !g.rinv ||
+        g.nblk != cdiv(g.N, NORM_TILE) ||
+        (g.norm_gate != GATE_SIGMOID && g.norm_gate != GATE_HARD)) {
+      set_error("BlockNorm GEMM epilogue: unsupported arguments");
+      return hipErrorInvalidValue;
+    }
+    if (g.norm_gate == GATE_SIGMOID) return gemm_bf16_dispatch<false, false, GATE_SIGMOID>(g, (float*)ws, st);
+    return gemm_bf16_dispatch<false, false, GATE_HARD>(g, (float*)ws, st);
   }
   if (g.dt == DT_BF16) {
     float* w = (float*)ws;

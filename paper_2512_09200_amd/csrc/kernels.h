@@ -63,6 +63,17 @@ struct GemmArgs {
   int kseg = 0;                // K segmentation: k -> (k / kseg) * ks + k % kseg (0: none)
   int64_t ksA = 0, ksB = 0;
   float* rowsum = nullptr;     // bf16, not batched: rowsum[m] = sum_k A[m][k] (fp32, k order)
+  // BlockNorm epilogue (SwishRN over 128-column groups): gate 1 = sigmoid,
+  // 2 = hard sigmoid; gain [2, N] (g_a; g_b); pre [M, ldp] receives h =
+  // acc + bias in C's dtype, rinv [M, nblk = ceil(N / 128)] each group's
+  // 1 / sqrt(mean h^2 + eps)
+  int norm_gate = 0;
+  const float* gain = nullptr;
+  float eps = 0.f;
+  void* pre = nullptr;
+  int64_t ldp = 0;
+  float* rinv = nullptr;
+  int nblk = 0;
 };
 int gemm_splits(const GemmArgs& g);
 size_t gemm_workspace(const GemmArgs& g);
@@ -70,6 +81,21 @@ hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t s);
 size_t colsum_workspace(int M, int N);
 hipError_t colsum(const void* G, DType dt, int64_t ld, int M, int N, float* out, void* ws,
                   hipStream_t s);
+
+// swishrn.hip (SwishRN rows: the unfused forward, the backward chain and the
+// gain gradients; block = 0: the whole row, 128: BlockNorm groups; gate 1 =
+// sigmoid, 2 = hard sigmoid; rinv [M, swishrn_groups(N, block)])
+int swishrn_groups(int N, int block);
+hipError_t swishrn_fwd_rows(DType dt, const void* pre, int64_t ldp, int M, int N, int block, int gate,
+                            const float* gain, float eps, void* out, int64_t ldo, float* rinv,
+                            hipStream_t s);
+hipError_t swishrn_bwd_rows(DType dt, const void* go, int64_t ldg, const void* pre, int64_t ldp,
+                            const float* rinv, int M, int N, int block, int gate, const float* gain,
+                            void* dh, int64_t ldd, hipStream_t s);
+size_t swishrn_gain_workspace(int M, int N);
+hipError_t swishrn_gain_grad(DType dt, const void* go, int64_t ldg, const void* pre, int64_t ldp,
+                             const float* rinv, int M, int N, int block, int gate,
+                             const float* gain, float* dgain, void* ws, hipStream_t s);
 
 // interact.hip
 size_t dot_lds_bytes(int n, int d);

@@ -10,6 +10,7 @@ from oracle import interact as ointeract
 from oracle import loss as oloss
 from oracle import mlp as omlp
 from oracle import step as ostep
+from oracle import swishrn as oswish
 from oracle.metrics import max_rel_err, max_rel_err_normwise
 
 DEV = "cuda"
@@ -113,6 +114,60 @@ def assert_fp8_layer(name, got, h, W, b, fast, t=2e-2):
         assert err <= t, f"{name}: max_rel_err {err} > {t}"
 
 
+def assert_bounded(name, got, ref, e, storage_unit=None, t=2e-2):
+    """Element-wise: |got - ref| <= e (+ one rounding to the storage grid,
+    us (|ref| + e)), and the element-wise metric at t."""
+    got, ref, e = _np64(got), np.asarray(ref, np.float64), np.asarray(e, np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    bound = e + (storage_unit * (np.abs(ref) + e) if storage_unit else 0.0) + 1e-37
+    ratio = float(np.max(np.abs(got - ref) / bound, initial=0.0))
+    err = max_rel_err(got, ref)
+    print(f"  {name} [stage]: max_rel_err={err:.3e} (tol {t:.0e}), worst |x-r|/bound={ratio:.3f}", flush=True)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    assert ratio <= 1.0, f"{name}: outside the derived bound (ratio {ratio})"
+    assert err <= t, f"{name}: max_rel_err {err} > {t}"
+
+
+def check_swishrn_forward(name, cfg, act, i, h, W, b, pre, rinv, out, us, t):
+    """A SwishRN layer's forward from its stored input h: the pre-activation
+    (a product), then the activation -- from the exact pre-activation within
+    the GEMM's accumulation error when bf16 models normalise in the GEMM's
+    epilogue (BlockNorm), else from the stored pre-activation -- and rho."""
+    ga, gb = act["gains"][i]
+    a = h @ W.T + b
+    ab = np.abs(h) @ np.abs(W).T + np.abs(b)
+    K = W.shape[1] + 1
+    assert_product(f"{name} pre-activation", pre, a, ab, K, us, t)
+    if cfg.dtype == "bf16" and act["block"] == 128:
+        src, eh = a, (K + 3) * 2.0 ** -24 * ab
+    else:
+        src, eh = _np64(pre), 0.0
+    ref, _, rho = oswish.forward(src, ga, gb, act["block"], act["eps"], act["kind"])
+    e_out, e_rho = oswish.forward_bound(src, eh, ga, gb, act["block"], act["eps"], act["kind"])
+    assert_bounded(f"{name} SwishRN", out, ref, e_out, us, t)
+    assert_bounded(f"{name} rho", rinv, rho, e_rho, None, t)
+
+
+def check_swishrn_backward(name, act, i, gout, pre, rinv, dh, us, t):
+    """A SwishRN layer's backward chain from its stored output gradient,
+    pre-activation and rho."""
+    ga, gb = act["gains"][i]
+    gout, pre, rinv = _np64(gout), _np64(pre), _np64(rinv)
+    ref, _, _ = oswish.backward(gout, pre, ga, gb, act["block"], act["eps"], act["kind"], rho=rinv)
+    e, _, _ = oswish.backward_bound(gout, 0.0, pre, ga, gb, act["block"], act["eps"], act["kind"], rinv)
+    assert_bounded(f"{name} SwishRN backward", dh, ref, e, us, t)
+
+
+def check_swishrn_gains(name, act, i, gout, pre, rinv, dgain, t):
+    ga, gb = act["gains"][i]
+    gout, pre, rinv = _np64(gout), _np64(pre), _np64(rinv)
+    _, dga, dgb = oswish.backward(gout, pre, ga, gb, act["block"], act["eps"], act["kind"], rho=rinv)
+    _, e_a, e_b = oswish.backward_bound(gout, 0.0, pre, ga, gb, act["block"], act["eps"], act["kind"], rinv)
+    dg = _np64(dgain)
+    assert_bounded(f"{name}.dga", dg[0], dga, e_a, None, t)
+    assert_bounded(f"{name}.dgb", dg[1], dgb, e_b, None, t)
+
+
 def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_top=None):
     """Stage-wise parity of one step: every stage recomputed in float64 by
     the oracle from the accelerator's own stored inputs of that stage, so the
@@ -134,13 +189,17 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
     tin = _np64(v["t"][:, :cfg.top_in])
     h_top = [tin] + [_np64(a) for a in v["top_act"]]
     g_top = [_np64(g) for g in v["top_grad"]]
+    act = ostep.top_act(cfg, params)
     # top MLP forward, layer by layer from the stored inputs
     for i, (W, b) in enumerate(params["top"]):
         W, b = np.asarray(W, np.float64), np.asarray(b, np.float64)
         h = h_top[i][R]
         a = h @ W.T + b
         ab = np.abs(h) @ np.abs(W).T + np.abs(b)
-        if i < L - 1 and fp8_top:
+        if i < L - 1 and act is not None:
+            check_swishrn_forward(f"top{i}", cfg, act, i, h, W, b, _np64(v["top_pre"][i])[R],
+                                  _np64(v["top_rinv"][i])[R], h_top[i + 1][R], us, t)
+        elif i < L - 1 and fp8_top:
             assert_fp8_layer(f"top{i} forward", h_top[i + 1][R], h, W, b, fp8_top == "fast", t)
         elif i < L - 1:
             assert_product(f"top{i} forward", h_top[i + 1][R], np.maximum(a, 0), ab, W.shape[1] + 1, us, t)
@@ -155,11 +214,18 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
     print(f"  loss [stage]: {e_loss:.3e}; d_logits [stage]: {e_dz:.3e} (tol 1e-5)", flush=True)
     assert e_loss <= 1e-5 and e_dz <= 1e-5
     # the gradient chain: g_{i-1} = (g_i W_i) masked by the stored h_i > 0
+    # (SwishRN: g_i W_i is the stored output gradient, taken through the
+    # SwishRN backward)
     for i in range(L - 1, -1, -1):
         W = np.asarray(params["top"][i][0], np.float64)
         prod = g_top[i][R] @ W
         ab = np.abs(g_top[i][R]) @ np.abs(W)
-        if i > 0:
+        if i > 0 and act is not None:
+            gout = _np64(v["top_gout"][i - 1])[R]
+            assert_product(f"top{i} output grad", gout, prod, ab, W.shape[0], us, t)
+            check_swishrn_backward(f"top{i - 1}", act, i - 1, gout, _np64(v["top_pre"][i - 1])[R],
+                                   _np64(v["top_rinv"][i - 1])[R], g_top[i - 1][R], us, t)
+        elif i > 0:
             on = h_top[i][R] > 0
             assert_product(f"top{i} grad chain", g_top[i - 1][R], prod * on, ab * on, W.shape[0], us, t)
         else:
@@ -171,6 +237,10 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
         assert_product(f"top{i}.dW", _np64(grads["top_dW"][i])[r], gi.T @ hi, np.abs(gi).T @ np.abs(hi),
                        B, None, t)
         assert_product(f"top{i}.db", _np64(grads["top_db"][i])[r], gi.sum(0), np.abs(gi).sum(0), B, None, t)
+    if act is not None and rows is None:
+        for i in range(L - 1):
+            check_swishrn_gains(f"top{i}", act, i, v["top_gout"][i], v["top_pre"][i], v["top_rinv"][i],
+                                grads["top_dgain"][i], t)
     X = _np64(v["X"])
     dX = _np64(v["dX"])
     gt = tin_grad(v, cfg)
@@ -256,7 +326,7 @@ def grads_of(w):
     """The accelerator's parameter gradients of a Workload, by name."""
     g = dict(top_dW=[L["dW"] for L in w.top], top_db=[L["db"] for L in w.top],
              bottom_dW=[L["dW"] for L in w.bottom], bottom_db=[L["db"] for L in w.bottom],
-             fm_dW=w.fm_dW)
+             fm_dW=w.fm_dW, top_dgain=[L["dgain"] for L in w.top if "dgain" in L])
     if w.stack is not None:
         g["stack"] = [{k: lay[k] for k in ("dW", "dA", "dgamma", "dC") if lay.get(k) is not None}
                       for lay in w.stack]
@@ -356,6 +426,9 @@ class Workload:
 
         self.bottom = [lin(W, bb) for W, bb in self.params["bottom"]]
         self.top = [lin(W, bb) for W, bb in self.params["top"]]
+        for L, (ga, gb) in zip(self.top, self.params.get("top_gain", [])):
+            L["gain"] = to_dev(np.stack([ga, gb]))
+            L["dgain"] = torch.zeros(L["gain"].shape, dtype=torch.float32, device=DEV)
         self.fm_W = to_dev(self.params["fm_W"], sdt) if "fm_W" in self.params else None
         self.fm_dW = torch.zeros(self.fm_W.shape, dtype=torch.float32, device=DEV) \
             if self.fm_W is not None else None
@@ -370,7 +443,8 @@ class Workload:
         return api.StepModel(tables=self.E, row_base=self.row_base, num_features=c.F,
                              dense_in=c.dense_in, bottom=self.bottom, top=self.top,
                              interact=c.interact, fm_W=self.fm_W, fm_dW=self.fm_dW, pool=c.pool,
-                             stack=self.stack, stack_n=c.stack_n, ln_eps=c.ln_eps)
+                             stack=self.stack, stack_n=c.stack_n, ln_eps=c.ln_eps,
+                             top_act=c.top_act, norm_block=c.norm_block, norm_eps=c.norm_eps)
 
 
 def relu_overrides(cfg, params, table, batch, gpu_in, gpu_out, max_iter=4):

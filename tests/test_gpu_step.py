@@ -9,6 +9,8 @@ import synth
 from oracle import embbag as oe
 from oracle import step as ostep
 from oracle import bounds as obounds
+from oracle import interact as oint
+from oracle import swishrn as oswish
 from tests._util import (DEV, Workload, assert_close, assert_close_derived, check_sparse_stage,
                           check_stages, grads_of, relu_overrides, tol)
 
@@ -153,6 +155,118 @@ def test_step_fp8_top(name, mode):
     # the FP8 forward changes the step: the bf16 step's logits differ
     c16, _ = ostep.step(cfg, w.params, E0, w.batch, lr_tables=lr)
     assert not np.allclose(c16["logits"], c["logits"], rtol=0, atol=0)
+
+
+SWISH_CASES = {
+    # bf16, BlockNorm in the GEMM epilogue; top (512, 256, 8): 4 and 2 groups
+    "mid-small-swishrn": synth.small(synth.MID, B=256, rows=3000, top_act="swishrn"),
+    # bf16, whole-row RMSNorm (GEMM, then the row kernel), ragged batch
+    "mid-small-hardswishrn-rms": synth.small(synth.MID, B=200, rows=3000, top_act="hardswishrn",
+                                             norm_block=0),
+    "large-fm-small-hardswishrn": synth.small(synth.LARGE_FM, B=160, rows=6000, top_act="hardswishrn"),
+    # ragged last groups: 200 = 128 + 72 features, 72 in one group
+    "deep-stack-small-swishrn": synth.DEEP_STACK.scaled(B=48, F=24, rows=1500, d=64, stack_n=8, fm_rank=16,
+                                                        top=(200, 72, 8), top_act="swishrn"),
+    # fp32: the row kernels, BlockNorm groups and whole rows
+    "tiny-f32-swishrn": synth.TINY.scaled(top=(200, 4), top_act="swishrn"),
+    "tiny-f32-hardswishrn-rms": synth.TINY.scaled(top_act="hardswishrn", norm_block=0),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(SWISH_CASES))
+def test_step_swishrn_top(name):
+    """SwishRN hidden top layers (Sections 3.3.4, 3.5.3): every stage on the
+    GPU's own stored inputs (the SwishRN forward, its backward chain and the
+    gain gradients within their derived bounds), then the composed step
+    against the oracle's SwishRN step (fp32: element-wise at 1e-5; bf16:
+    normwise at 2e-2)."""
+    from oracle.metrics import max_rel_err, max_rel_err_normwise
+    cfg = SWISH_CASES[name]
+    lr = 0.01
+    print(f"[step-swishrn] {name} B={cfg.B} top={cfg.top} {cfg.top_act} block={cfg.norm_block}", flush=True)
+    w = Workload(cfg)
+    E0 = w.table_np()
+    _, v, _ = run_step(w, lr)
+    E1 = w.table_np()
+    check_stages(cfg, w.params, w.batch, v, grads_of(w))
+    ov, n_amb = gate_overrides(cfg, w.params, v, ostep.forward(cfg, w.params, E0, w.batch))
+    print(f"  hard-gate kinks taken the other way within their band: {n_amb}", flush=True)
+    c, g = ostep.step(cfg, w.params, E0, w.batch, lr_tables=lr, overrides={"top_gate": ov})
+    bk0 = g["bookkeeping"]
+    check_sparse_stage(cfg, w.batch, v, w.nnz, E0[bk0["unique_rows"]], E1[bk0["unique_rows"]], lr, bk=bk0)
+    t = tol(cfg)
+    s0 = cfg.first_emb_slot
+    pairs = [("logits", v["logits"], c["logits"]), ("loss", v["loss"], np.array([c["loss"]])),
+             ("d_t", v["d_t"][:, :cfg.top_in], g["d_top_in"])]
+    for i in range(len(w.top)):
+        pairs += [(f"top{i}.dW", w.top[i]["dW"], g["top_dW"][i]), (f"top{i}.db", w.top[i]["db"], g["top_db"][i])]
+    for i in range(len(w.top) - 1):
+        dga, dgb = g["top_dgain"][i]
+        pairs.append((f"top{i}.dgain", w.top[i]["dgain"], np.stack([dga, dgb])))
+    for nm, got, ref in pairs:
+        got = got.float().cpu().numpy()
+        e = max_rel_err(got, ref) if t <= 1e-5 else max_rel_err_normwise(got, ref)
+        print(f"  {nm} (composed): {'max_rel_err' if t <= 1e-5 else 'normwise'} {e:.3e} (tol {t:.0e})",
+              flush=True)
+        assert e <= t, nm
+    dX = v["dX"][:, s0:].float().cpu().numpy()
+    if t > 1e-5:
+        e = max_rel_err_normwise(dX, g["dX_emb"])
+        print(f"  dX_emb (composed): normwise {e:.3e} (tol {t:.0e})", flush=True)
+        assert e <= t
+    else:
+        assert_dot_dX_composed(cfg, v, c, g, t)
+
+
+def gate_overrides(cfg, params, v, c):
+    """Hard-gate derivative decisions (inside or outside the kinks at +-3)
+    that the GPU may legitimately take the other way: where the oracle's
+    gate input z lies within |z_gpu - z| (the observed difference, which
+    the stage checks bound) plus fp32 slack of a kink, the GPU's decision,
+    read from its stored pre-activation and rho, is accepted.  Returns
+    (per-layer overrides for oracle.swishrn.backward, count)."""
+    act = ostep.top_act(cfg, params)
+    if act is None or act["kind"] != "hard":
+        return None, 0
+    ov, count = {}, 0
+    for i in range(len(params["top"]) - 1):
+        ga, gb = (np.asarray(x, np.float64) for x in act["gains"][i])
+        pre, rinv = (v[k][i].float().cpu().double().numpy() for k in ("top_pre", "top_rinv"))
+        z_g = gb * pre * oswish.expand(rinv, pre.shape[1], act["block"])
+        _, n_r, _ = oswish.forward(c["masks_top"][i]["pre"], ga, gb, act["block"], act["eps"], "hard")
+        z_r = gb * n_r
+        in_g, in_r = np.abs(z_g) < 3, np.abs(z_r) < 3
+        where = (in_g != in_r) & (np.abs(np.abs(z_r) - 3) <= np.abs(z_g - z_r) + 2.0 ** -20 * 3)
+        count += int(where.sum())
+        ov[i] = (where, np.where(in_g, 1.0 / 6.0, 0.0))
+    return ov, count
+
+
+def assert_dot_dX_composed(cfg, v, c, g, t):
+    """fp32, DOT interaction: the composed gradient of the embedding slots
+    element by element -- within t of the oracle's (element-wise metric), or
+    where the interaction's cancellation amplifies its inputs' composed
+    deviations, within those deviations carried through the same linear
+    map, |S(d_t_gpu - d_t)| |X| + |S(d_t)| |X_gpu - X|, plus the stage's
+    own fp32 bound."""
+    from oracle.metrics import max_rel_err
+    assert cfg.interact == "dot"
+    s0, off = cfg.first_emb_slot, (cfg.d if cfg.has_dense else 0)
+    n64 = lambda x: x.float().cpu().double().numpy()
+    got, ref = n64(v["dX"])[:, s0:], g["dX_emb"]
+    dt_g, dt_r = n64(v["d_t"])[:, off:cfg.top_in], g["d_top_in"][:, off:]
+    X_g, X_r = n64(v["X"]), c["X"]
+    prop = (oint.dot_backward(np.abs(dt_g - dt_r), np.abs(X_g)) + oint.dot_backward(np.abs(dt_r), np.abs(X_g - X_r))
+            + (cfg.n_slots + 3) * 2.0 ** -24 * oint.dot_backward(np.abs(dt_g), np.abs(X_g)))[:, s0:]
+    rr = ref.reshape(-1, ref.shape[-1])
+    floor = np.maximum(np.abs(rr), np.sqrt(np.mean(rr * rr, axis=-1, keepdims=True))).reshape(ref.shape)
+    diff = np.abs(got - ref)
+    bad = diff > t * floor + prop
+    n_prop = int(np.count_nonzero((diff > t * floor) & ~bad))
+    print(f"  dX_emb (composed): max_rel_err {max_rel_err(got, ref):.3e} (tol {t:.0e}); {n_prop} of {diff.size} "
+          f"elements beyond it and within their inputs' propagated deviation", flush=True)
+    assert not bad.any(), f"dX_emb: {int(bad.sum())} elements outside t and the propagated deviation"
 
 
 @pytest.mark.gpu

@@ -168,7 +168,7 @@ def _mlp_backward_no_relu_mask(g_out, hs, masks, layers, rnd, relu_last, need_in
     return _ORIG["mlp_backward"](g_out, hs, masks, layers, rnd, relu_last, need_input_grad, **kw)
 
 
-def _swishrn_backward_no_mean_term(do, h, ga, gb, block, eps, kind, rho=None, kink_grad=None):
+def _swishrn_backward_no_mean_term(do, h, ga, gb, block, eps, kind, rho=None, grad_override=None):
     do = np.asarray(do, np.float64)
     _, n, rho = swishrn.forward(h, ga, gb, block, eps, kind, rho)
     a, z = ga * n, gb * n
@@ -178,8 +178,8 @@ def _swishrn_backward_no_mean_term(do, h, ga, gb, block, eps, kind, rho=None, ki
     return dh, (do * s * n).sum(0), (do * a * sp * n).sum(0)
 
 
-def _swishrn_backward_whole_row_mean(do, h, ga, gb, block, eps, kind, rho=None, kink_grad=None):
-    dh, dga, dgb = _ORIG["swishrn_backward"](do, h, ga, gb, block, eps, kind, rho, kink_grad)
+def _swishrn_backward_whole_row_mean(do, h, ga, gb, block, eps, kind, rho=None, grad_override=None):
+    dh, dga, dgb = _ORIG["swishrn_backward"](do, h, ga, gb, block, eps, kind, rho, grad_override)
     _, n, rho = swishrn.forward(h, ga, gb, block, eps, kind, rho)
     a, z = ga * n, gb * n
     dn = ga * do * swishrn.gate(z, kind) + gb * do * a * swishrn.gate_grad(z, kind)
@@ -187,8 +187,8 @@ def _swishrn_backward_whole_row_mean(do, h, ga, gb, block, eps, kind, rho=None, 
     return R * (dn - n * np.mean(dn * n, axis=1, keepdims=True)), dga, dgb   # mean over the row, not the group
 
 
-def _swishrn_backward_gate_gain_swapped(do, h, ga, gb, block, eps, kind, rho=None, kink_grad=None):
-    return _ORIG["swishrn_backward"](do, h, gb, ga, block, eps, kind, rho, kink_grad)
+def _swishrn_backward_gate_gain_swapped(do, h, ga, gb, block, eps, kind, rho=None, grad_override=None):
+    return _ORIG["swishrn_backward"](do, h, gb, ga, block, eps, kind, rho, grad_override)
 
 
 def _dot_backward_no_slot0(dp, X):

@@ -172,3 +172,31 @@ def test_bounds_cover_perturbed_evaluations(kind, block):
         worst = max(worst, max(float(np.max(np.abs(x - y) / e)) for x, y, e in
                                zip(d2, (dh, dga, dgb), (e_dh, e_dga, e_dgb))))
     assert 0.05 < worst <= 1.0, worst
+
+
+def test_gate_derivative_override_is_local_to_its_group():
+    """Overriding the hard gate's derivative with its own value changes
+    nothing; changing it at one element changes dh only inside that
+    element's normalisation group, and the gain gradients only in its
+    column."""
+    M, N, block = 6, 40, 16
+    h = _rows(M, N, 2.0)
+    ga, gb = 1 + 0.3 * RNG.standard_normal(N), 1 + 0.3 * RNG.standard_normal(N)
+    do = RNG.standard_normal((M, N))
+    _, n, _ = swishrn.forward(h, ga, gb, block, 1e-6, "hard")
+    z = gb * n
+    base = swishrn.backward(do, h, ga, gb, block, 1e-6, "hard")
+    same = swishrn.backward(do, h, ga, gb, block, 1e-6, "hard",
+                            grad_override=(np.ones((M, N), bool), swishrn.gate_grad(z, "hard")))
+    for a, b in zip(base, same):
+        assert np.array_equal(a, b)
+    r, k = 2, 21                                  # group 1 (columns 16..31)
+    where = np.zeros((M, N), bool)
+    where[r, k] = True
+    val = np.full((M, N), 1 / 6 - swishrn.gate_grad(z, "hard")[r, k])   # flip 0 <-> 1/6
+    dh, dga, dgb = swishrn.backward(do, h, ga, gb, block, 1e-6, "hard", grad_override=(where, val))
+    changed = dh != base[0]
+    assert changed[r, 16:32].any() and not changed[:, :16].any() and not changed[:, 32:].any()
+    assert not changed[np.arange(M) != r].any()
+    assert np.array_equal(dga, base[1])
+    assert np.flatnonzero(dgb != base[2]).tolist() == [k]
