@@ -41,6 +41,11 @@ def parse():
     ap.add_argument("--fp8", choices=["precise", "fast"], default=None,
                     help="mixed FP8/BF16 training: the top MLP's hidden-layer forward GEMMs in FP8 e4m3 "
                          "(row-wise scales) with fast accumulation off (precise) or on (fast)")
+    ap.add_argument("--top-act", choices=["relu", "swishrn", "hardswishrn"], default="relu",
+                    help="activation of the top MLP's hidden layers (SwishRN: RMS-normalised self-gated, "
+                         "sigmoid or hard-sigmoid gate)")
+    ap.add_argument("--norm-block", type=int, choices=[128, 0], default=128,
+                    help="SwishRN groups: 128 (BlockNorm, in the GEMM epilogue) or 0 (whole-row RMSNorm)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, stream 1 GiB through a plain elementwise kernel "
                          "(torch.neg, 1 GiB read + 1 GiB written) as a counter calibration point")
@@ -74,6 +79,11 @@ def main():
     cfg = synth.WORKLOADS[args.workload]
     if args.uniform:
         cfg = cfg.scaled(index_dist=("uniform",))
+    if args.top_act != "relu":
+        if args.fp8:
+            print("--fp8 needs ReLU top layers", file=sys.stderr)
+            sys.exit(2)
+        cfg = cfg.scaled(top_act=args.top_act, norm_block=args.norm_block)
     dev = "cuda"
     sdt = synth.torch_dtype(cfg.dtype)
     t0 = time.time()
@@ -98,6 +108,9 @@ def main():
 
     bottom = [lin(W, b) for W, b in p["bottom"]]
     top = [lin(W, b) for W, b in p["top"]]
+    for L, (ga, gb) in zip(top, p.get("top_gain", [])):
+        L["gain"] = torch.from_numpy(np.stack([ga, gb])).to(dev)
+        L["dgain"] = torch.empty(tuple(L["gain"].shape), device=dev)
     fm_W = torch.from_numpy(p["fm_W"]).to(sdt).to(dev) if "fm_W" in p else None
     fm_dW = torch.empty(tuple(fm_W.shape), device=dev) if fm_W is not None else None
     stack = None
@@ -114,7 +127,8 @@ def main():
     model = api.StepModel(tables=E, row_base=row_base, num_features=cfg.F, dense_in=cfg.dense_in,
                           max_rows=cfg.rows,
                           bottom=bottom, top=top, interact=cfg.interact, fm_W=fm_W, fm_dW=fm_dW,
-                          pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps)
+                          pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps,
+                          top_act=cfg.top_act, norm_block=cfg.norm_block, norm_eps=cfg.norm_eps)
     nnz_max = max(b["nnz"] for b in batches)
     lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False, fp8_top=args.fp8)
     ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
@@ -275,6 +289,8 @@ def main():
                    "nnz_per_step": int(nnz), "distinct_rows_per_step": int(U),
                    "batches_cycled": len(batches), "parallelism": "single-gpu",
                    "fp8_top": args.fp8,
+                   "top_act": cfg.top_act,
+                   "norm_block": cfg.norm_block if cfg.top_act != "relu" else None,
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,
         "gather_roofline": gather_roofline,

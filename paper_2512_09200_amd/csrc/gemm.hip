@@ -63,56 +63,6 @@ struct Epi {
   int nblk;
 };
 
-// SwishRN with BlockNorm on 8 columns col.. of row `row` of the finished
-// fp32 tile (see the header comment).  Every lane of the wave calls it (the
-// shuffles need the whole 16-lane group); rows past M and columns past N
-// store nothing.
-template <typename CT, int GATE>
-__device__ inline void epi_blocknorm8(CT* C, int64_t ldc, int row, int col, int M, int N, float* v,
-                                      const Epi& e, int vec) {
-  float ss = 0.f;
-#pragma unroll
-  for (int t = 0; t < 8; ++t) {
-    const bool ok = col + t < N;
-    if (e.bias && ok) v[t] += e.bias[col + t];
-    v[t] = ok ? v[t] : 0.f;
-    ss += v[t] * v[t];
-  }
-  ss = sum16(ss);
-  const int blk = col / NORM_TILE;
-  const int cnt = max(1, min(NORM_TILE, N - blk * NORM_TILE));
-  const float r = rsqrtf(ss / (float)cnt + e.eps);
-  if (row >= M || col >= N) return;
-  if (col % NORM_TILE == 0) e.rinv[(int64_t)row * e.nblk + blk] = r;
-  float o[8];
-#pragma unroll
-  for (int t = 0; t < 8; ++t) {
-    const int k = min(col + t, N - 1);  // past N: any valid gain (not stored)
-    const float n = v[t] * r;
-    o[t] = (e.gain[k] * n) * gate_fn<GATE>(e.gain[N + k] * n);
-  }
-  CT* c = C + (int64_t)row * ldc + col;
-  CT* p = reinterpret_cast<CT*>(e.pre) + (int64_t)row * e.ldp + col;
-  if (vec && col + 8 <= N) {
-    if constexpr (sizeof(CT) == 2) {
-      stg16(c, Vec16<bf16_t>::pack(o));
-      stg16(p, Vec16<bf16_t>::pack(v));
-    } else {
-      stg16(c, Vec16<float>::pack(o));
-      stg16(c + 4, Vec16<float>::pack(o + 4));
-      stg16(p, Vec16<float>::pack(v));
-      stg16(p + 4, Vec16<float>::pack(v + 4));
-    }
-  } else {
-#pragma unroll
-    for (int t = 0; t < 8; ++t)
-      if (col + t < N) {
-        st(c + t, o[t]);
-        st(p + t, v[t]);
-      }
-  }
-}
-
 template <typename CT>
 __device__ inline void epi_store(CT* C, int64_t ldc, int row, int col, float v, const Epi& e,
                                  int64_t bz) {
@@ -136,6 +86,74 @@ __device__ inline void ld8f(const float* p, float* v) {
     v[4 + i] = b[i];
   }
 }
+
+// Per-thread coefficients of the BlockNorm epilogue: a thread stores the
+// same 8 columns col.. in every row it handles, so bias, g_a, g_b (zeros
+// past N) and 1 / |group| are loaded once.
+struct NormCoef {
+  float b[8], ga[8], gb[8];
+  float inv_cnt;
+};
+
+__device__ inline void load_norm_coef(const Epi& e, int col, int N, NormCoef& c) {
+  load_gains8(e.gain, N, col, c.ga, c.gb);
+  if (e.bias && col + 8 <= N && ((uintptr_t)e.bias & 15) == 0) {
+    ld8f(e.bias + col, c.b);
+  } else {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const bool ok = e.bias && col + t < N;
+      c.b[t] = ok ? e.bias[ok ? col + t : 0] : 0.f;
+    }
+  }
+  c.inv_cnt = inv_group_size(col, N);
+}
+
+// SwishRN with BlockNorm on 8 columns col.. of row `row` of the finished
+// fp32 tile (see the header comment).  Every lane of the wave calls it (the
+// shuffles need the whole 16-lane group); rows past M and columns past N
+// store nothing.
+template <typename CT, int GATE>
+__device__ inline void epi_blocknorm8(CT* C, int64_t ldc, int row, int col, int M, int N, float* v,
+                                      const Epi& e, const NormCoef& nc, int vec) {
+  float ss = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    v[t] = col + t < N ? v[t] + nc.b[t] : 0.f;
+    ss += v[t] * v[t];
+  }
+  ss = sum16(ss);
+  const float r = rsqrtf(ss * nc.inv_cnt + e.eps);
+  if (row >= M || col >= N) return;
+  if (col % NORM_TILE == 0) e.rinv[(int64_t)row * e.nblk + col / NORM_TILE] = r;
+  float o[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const float n = v[t] * r;
+    o[t] = (nc.ga[t] * n) * gate_fn<GATE>(nc.gb[t] * n);
+  }
+  CT* c = C + (int64_t)row * ldc + col;
+  CT* p = reinterpret_cast<CT*>(e.pre) + (int64_t)row * e.ldp + col;
+  if (vec && col + 8 <= N) {
+    if constexpr (sizeof(CT) == 2) {
+      stg16(c, Vec16<bf16_t>::pack(o));
+      stg16(p, Vec16<bf16_t>::pack(v));
+    } else {
+      stg16(c, Vec16<float>::pack(o));
+      stg16(c + 4, Vec16<float>::pack(o + 4));
+      stg16(p, Vec16<float>::pack(v));
+      stg16(p + 4, Vec16<float>::pack(v + 4));
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      if (col + t < N) {
+        st(c + t, o[t]);
+        st(p + t, v[t]);
+      }
+  }
+}
+
 
 // Epilogue of 8 consecutive columns of one row with 16-byte vectors (the
 // caller guarantees alignment and col + 8 <= N).
@@ -493,14 +511,17 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     }
   __syncthreads();
   if constexpr (NORM != 0) {
-    // one 128-column norm group per tile row: 16 lanes per row
+    // one 128-column norm group per tile row: 16 lanes per row, the same
+    // 8 columns for a thread in every row
+    const int cl = (threadIdx.x % (GBN / 8)) * 8;
+    NormCoef nc;
+    load_norm_coef(epi, n0 + cl, N, nc);
 #pragma unroll
     for (int q = 0; q < (GBM * GBN / 8) / 256; ++q) {
-      const int chunk = threadIdx.x + q * 256;
-      const int rl = chunk / (GBN / 8), cl = (chunk % (GBN / 8)) * 8;
+      const int rl = (threadIdx.x + q * 256) / (GBN / 8);
       float v[8];
       ld8f(Cs + rl * CLD + cl, v);
-      epi_blocknorm8<CT, NORM>(C, ldc, m0 + rl, n0 + cl, M, N, v, epi, vec);
+      epi_blocknorm8<CT, NORM>(C, ldc, m0 + rl, n0 + cl, M, N, v, epi, nc, vec);
     }
     return;
   }
@@ -713,14 +734,16 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, C
     __syncthreads();
     if constexpr (NORM != 0) {
       // two 128-column norm groups per tile row: lanes 0-15 and 16-31 of
-      // each 32-lane row
+      // each 32-lane row; a thread keeps its 8 columns in every row
+      const int cl = (threadIdx.x % (BBN / 8)) * 8;
+      NormCoef nc;
+      load_norm_coef(epi, n0 + cl, N, nc);
 #pragma unroll 4
       for (int q = 0; q < (BBM / 2) * BBN / 8 / THREADS; ++q) {
-        const int chunk = threadIdx.x + q * THREADS;
-        const int rl = chunk / (BBN / 8), cl = (chunk % (BBN / 8)) * 8;
+        const int rl = (threadIdx.x + q * THREADS) / (BBN / 8);
         float v[8];
         ld8f(Cs + rl * BCLD + cl, v);
-        epi_blocknorm8<CT, NORM>(C, ldc, m0 + h * 128 + rl, n0 + cl, M, N, v, epi, vec);
+        epi_blocknorm8<CT, NORM>(C, ldc, m0 + h * 128 + rl, n0 + cl, M, N, v, epi, nc, vec);
       }
       __syncthreads();
       continue;

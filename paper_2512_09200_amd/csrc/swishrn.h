@@ -10,10 +10,12 @@ namespace lat {
 enum NormGate { GATE_NONE = 0, GATE_SIGMOID = 1, GATE_HARD = 2 };
 constexpr int NORM_TILE = 128;  // BlockNorm group: the GEMM's 128-column tile
 
+// The sigmoid from the hardware exponential and reciprocal (about 1 ulp
+// each; exp(-z) = inf for very negative z gives 0).
 template <int GATE>
 __device__ inline float gate_fn(float z) {
   if constexpr (GATE == GATE_SIGMOID) {
-    return 1.f / (1.f + __expf(-z));
+    return __builtin_amdgcn_rcpf(1.f + __expf(-z));
   } else {
     return fminf(fmaxf(fmaf(z, 1.f / 6.f, 0.5f), 0.f), 1.f);
   }
@@ -38,6 +40,38 @@ __device__ inline float sum16(float x) {
   x += __shfl_xor(x, 4, 64);
   x += __shfl_xor(x, 8, 64);
   return x;
+}
+
+// g_a and g_b of the 8 columns c.. of a layer of width N (gain = [g_a; g_b],
+// two rows of N); zeros past N.  Two 16-byte loads each when aligned.
+__device__ __forceinline__ void load_gains8(const float* gain, int N, int c, float* ga, float* gb) {
+  if (c + 8 <= N && (N & 3) == 0 && ((uintptr_t)gain & 15) == 0) {
+    const f32x4* a = reinterpret_cast<const f32x4*>(gain + c);
+    const f32x4* b = reinterpret_cast<const f32x4*>(gain + N + c);
+    const f32x4 a0 = a[0], a1 = a[1], b0 = b[0], b1 = b[1];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      ga[t] = a0[t];
+      ga[4 + t] = a1[t];
+      gb[t] = b0[t];
+      gb[4 + t] = b1[t];
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const bool ok = c + t < N;
+      const int k = ok ? c + t : 0;
+      const float x = gain[k], y = gain[N + k];
+      ga[t] = ok ? x : 0.f;
+      gb[t] = ok ? y : 0.f;
+    }
+  }
+}
+
+// 1 / (number of columns of the 128-column group holding column c)
+__device__ __forceinline__ float inv_group_size(int c, int N) {
+  const int cnt = max(1, min(NORM_TILE, N - (c / NORM_TILE) * NORM_TILE));
+  return cnt == NORM_TILE ? 1.f / NORM_TILE : __builtin_amdgcn_rcpf((float)cnt);
 }
 
 __device__ inline float sum64(float x) {

@@ -57,31 +57,27 @@ __device__ __forceinline__ void store8(T* p, int c, int N, int vec, const float*
   }
 }
 
-// out of 8 columns from h (already loaded, zero past N) and rho.  Straight
-// line: columns past N read gain[0] and give 0.
+// out of 8 columns from h (zero past N), rho and the columns' gains
 template <int GATE>
-__device__ __forceinline__ void swish8(const float* h, float r, const float* gain, int N, int c,
+__device__ __forceinline__ void swish8(const float* h, float r, const float* ga, const float* gb,
                                        float* o) {
 #pragma unroll
   for (int t = 0; t < 8; ++t) {
-    const int k = c + t < N ? c + t : 0;
     const float n = h[t] * r;
-    o[t] = (gain[k] * n) * gate_fn<GATE>(gain[N + k] * n);
+    o[t] = (ga[t] * n) * gate_fn<GATE>(gb[t] * n);
   }
 }
 
 // dn and n of 8 columns (g and h zero past N, so are n and dn there)
 template <int GATE>
-__device__ __forceinline__ void dn8(const float* g, const float* h, float r, const float* gain, int N,
-                                    int c, float* n, float* dn) {
+__device__ __forceinline__ void dn8(const float* g, const float* h, float r, const float* ga,
+                                    const float* gb, float* n, float* dn) {
 #pragma unroll
   for (int t = 0; t < 8; ++t) {
-    const int k = c + t < N ? c + t : 0;
-    const float ga = gain[k], gb = gain[N + k];
     n[t] = h[t] * r;
-    const float a = ga * n[t], z = gb * n[t];
+    const float a = ga[t] * n[t], z = gb[t] * n[t];
     const float s = gate_fn<GATE>(z);
-    dn[t] = g[t] * (ga * s + gb * a * gate_deriv<GATE>(z, s));
+    dn[t] = g[t] * (ga[t] * s + gb[t] * a * gate_deriv<GATE>(z, s));
   }
 }
 
@@ -106,29 +102,29 @@ __global__ __launch_bounds__(256) void swishrn_fwd_rows_kernel(const T* __restri
       for (int t = 0; t < 8; ++t) ss += v[t] * v[t];
     }
     ss = sum64(ss);
-    const float r = rsqrtf(ss / (float)N + eps);
+    const float r = rsqrtf(ss * __builtin_amdgcn_rcpf((float)N) + eps);
     if (lane == 0) rinv[(int64_t)row * nblk] = r;
     for (int c = lane * 8; c < N; c += 512) {
-      float v[8], y[8];
+      float v[8], y[8], ga[8], gb[8];
       load8(p, c, N, vec, v);
-      swish8<GATE>(v, r, gain, N, c, y);
+      load_gains8(gain, N, c, ga, gb);
+      swish8<GATE>(v, r, ga, gb, y);
       store8(o, c, N, vec, y);
     }
   } else {
     for (int c0 = 0; c0 < N; c0 += 512) {
       const int c = c0 + lane * 8;
-      float v[8], y[8];
+      float v[8], y[8], ga[8], gb[8];
       load8(p, c, N, vec, v);
+      load_gains8(gain, N, c, ga, gb);
       float ss = 0.f;
 #pragma unroll
       for (int t = 0; t < 8; ++t) ss += v[t] * v[t];
       ss = sum16(ss);
-      const int blk = c / NORM_TILE;
-      const int cnt = max(1, min(NORM_TILE, N - blk * NORM_TILE));
-      const float r = rsqrtf(ss / (float)cnt + eps);
+      const float r = rsqrtf(ss * inv_group_size(c, N) + eps);
       if (c < N) {
-        if ((lane & 15) == 0) rinv[(int64_t)row * nblk + blk] = r;
-        swish8<GATE>(v, r, gain, N, c, y);
+        if ((lane & 15) == 0) rinv[(int64_t)row * nblk + c / NORM_TILE] = r;
+        swish8<GATE>(v, r, ga, gb, y);
         store8(o, c, N, vec, y);
       }
     }
@@ -150,19 +146,21 @@ __global__ __launch_bounds__(256) void swishrn_bwd_rows_kernel(
     const float r = rinv[(int64_t)row * nblk];
     float acc = 0.f;
     for (int c = lane * 8; c < N; c += 512) {
-      float gv[8], hv[8], n[8], dn[8];
+      float gv[8], hv[8], n[8], dn[8], ga[8], gb[8];
       load8(g, c, N, vec, gv);
       load8(p, c, N, vec, hv);
-      dn8<GATE>(gv, hv, r, gain, N, c, n, dn);
+      load_gains8(gain, N, c, ga, gb);
+      dn8<GATE>(gv, hv, r, ga, gb, n, dn);
 #pragma unroll
       for (int t = 0; t < 8; ++t) acc += dn[t] * n[t];
     }
-    const float m = sum64(acc) / (float)N;
+    const float m = sum64(acc) * __builtin_amdgcn_rcpf((float)N);
     for (int c = lane * 8; c < N; c += 512) {
-      float gv[8], hv[8], n[8], dn[8], y[8];
+      float gv[8], hv[8], n[8], dn[8], y[8], ga[8], gb[8];
       load8(g, c, N, vec, gv);
       load8(p, c, N, vec, hv);
-      dn8<GATE>(gv, hv, r, gain, N, c, n, dn);
+      load_gains8(gain, N, c, ga, gb);
+      dn8<GATE>(gv, hv, r, ga, gb, n, dn);
 #pragma unroll
       for (int t = 0; t < 8; ++t) y[t] = r * (dn[t] - n[t] * m);
       store8(d, c, N, vec, y);
@@ -172,15 +170,15 @@ __global__ __launch_bounds__(256) void swishrn_bwd_rows_kernel(
       const int c = c0 + lane * 8;
       const int blk = c / NORM_TILE;
       const float r = c < N ? rinv[(int64_t)row * nblk + blk] : 0.f;
-      float gv[8], hv[8], n[8], dn[8], y[8];
+      float gv[8], hv[8], n[8], dn[8], y[8], ga[8], gb[8];
       load8(g, c, N, vec, gv);
       load8(p, c, N, vec, hv);
-      dn8<GATE>(gv, hv, r, gain, N, c, n, dn);
+      load_gains8(gain, N, c, ga, gb);
+      dn8<GATE>(gv, hv, r, ga, gb, n, dn);
       float acc = 0.f;
 #pragma unroll
       for (int t = 0; t < 8; ++t) acc += dn[t] * n[t];
-      const int cnt = max(1, min(NORM_TILE, N - blk * NORM_TILE));
-      const float m = sum16(acc) / (float)cnt;
+      const float m = sum16(acc) * inv_group_size(c, N);
       if (c < N) {
 #pragma unroll
         for (int t = 0; t < 8; ++t) y[t] = r * (dn[t] - n[t] * m);
@@ -208,21 +206,27 @@ __global__ __launch_bounds__(256) void swishrn_gain_partial_kernel(
 #pragma unroll
   for (int t = 0; t < 8; ++t) sa[t] = sb[t] = 0.f;
   if (col0 < N) {
-    for (int row = r0 + rl; row < r1; row += 32) {
-      float gv[8], hv[8];
-      load8(go + (int64_t)row * ldg, col0, N, vec, gv);
-      load8(pre + (int64_t)row * ldp, col0, N, vec, hv);
-      const float r = rinv[(int64_t)row * nblk + blk];
+    float ga[8], gb[8];
+    load_gains8(gain, N, col0, ga, gb);
+    // straight line over the thread's GG_ROWS / 32 rows (all loads in
+    // flight together); rows past M read row r0 and count as zero
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const int k = col0 + t;
-        if (k < N) {
-          const float n = hv[t] * r;
-          const float a = gain[k] * n, z = gain[N + k] * n;
-          const float s = gate_fn<GATE>(z);
-          sa[t] += gv[t] * s * n;
-          sb[t] += gv[t] * a * gate_deriv<GATE>(z, s) * n;
-        }
+    for (int i = 0; i < GG_ROWS / 32; ++i) {
+      const int row = r0 + rl + 32 * i;
+      const bool ok = row < r1;
+      const int rr = ok ? row : r0;
+      float gv[8], hv[8];
+      load8(go + (int64_t)rr * ldg, col0, N, vec, gv);
+      load8(pre + (int64_t)rr * ldp, col0, N, vec, hv);
+      const float r = ok ? rinv[(int64_t)rr * nblk + blk] : 0.f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {   // zero past N (gv, hv and the gains are) and past M
+        gv[t] = ok ? gv[t] : 0.f;
+        const float n = hv[t] * r;
+        const float a = ga[t] * n, z = gb[t] * n;
+        const float s = gate_fn<GATE>(z);
+        sa[t] += gv[t] * s * n;
+        sb[t] += gv[t] * a * gate_deriv<GATE>(z, s) * n;
       }
     }
   }
@@ -247,8 +251,19 @@ __global__ __launch_bounds__(256) void swishrn_gain_final_kernel(const float* __
   const int j = blockIdx.x * 256 + threadIdx.x;  // j < 2N: [g_a; g_b]
   if (j >= 2 * N) return;
   const int w = j / N, col = j - w * N;
+  const float* p = part + (int64_t)w * N + col;
+  const int64_t stride = 2 * (int64_t)N;
+  // chunks in order; the loads of 8 chunks are issued before their adds
   float s = 0.f;
-  for (int c = 0; c < chunks; ++c) s += part[((int64_t)c * 2 + w) * N + col];
+  int c = 0;
+  for (; c + 8 <= chunks; c += 8) {
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = p[(c + q) * stride];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += v[q];
+  }
+  for (; c < chunks; ++c) s += p[c * stride];
   dgain[j] = s;
 }
 
