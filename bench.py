@@ -46,6 +46,9 @@ def parse():
                          "sigmoid or hard-sigmoid gate)")
     ap.add_argument("--norm-block", type=int, choices=[128, 0], default=128,
                     help="SwishRN groups: 128 (BlockNorm, in the GEMM epilogue) or 0 (whole-row RMSNorm)")
+    ap.add_argument("--lcb-n", type=int, default=0,
+                    help="stacked workloads: output vectors of each fusion block's linear compression "
+                         "block (full DHEN/Wukong fusion blocks; 0: FM block only)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, stream 1 GiB through a plain elementwise kernel "
                          "(torch.neg, 1 GiB read + 1 GiB written) as a counter calibration point")
@@ -79,6 +82,11 @@ def main():
     cfg = synth.WORKLOADS[args.workload]
     if args.uniform:
         cfg = cfg.scaled(index_dist=("uniform",))
+    if args.lcb_n:
+        if cfg.interact != "stack":
+            print("--lcb-n needs a stacked workload", file=sys.stderr)
+            sys.exit(2)
+        cfg = cfg.scaled(lcb_n=args.lcb_n)
     if args.top_act != "relu":
         if args.fp8:
             print("--fp8 needs ReLU top layers", file=sys.stderr)
@@ -120,7 +128,8 @@ def main():
             d = {k: torch.from_numpy(lay[k]).to(sdt).to(dev) for k in ("W", "A")}
             d["gamma"] = torch.from_numpy(lay["gamma"]).to(dev)
             d["C"] = torch.from_numpy(lay["C"]).to(sdt).to(dev) if lay["C"] is not None else None
-            for k in ("W", "A", "gamma", "C"):
+            d["L"] = torch.from_numpy(lay["L"]).to(sdt).to(dev) if lay.get("L") is not None else None
+            for k in ("W", "A", "gamma", "C", "L"):
                 if d[k] is not None:
                     d["d" + k] = torch.empty(tuple(d[k].shape), device=dev)
             stack.append(d)
@@ -235,7 +244,9 @@ def main():
         nl = n
         for l in range(cfg.stack_layers):
             flops_fwd += 4.0 * cfg.B * nl * cfg.d * cfg.fm_rank                      # FM block
-            flops_fwd += 2.0 * cfg.B * (nl * cfg.fm_rank) * (cfg.stack_n * cfg.d)    # compression
+            nF = cfg.stack_n - cfg.lcb_n
+            flops_fwd += 2.0 * cfg.B * (nl * cfg.fm_rank) * (nF * cfg.d)             # FM projection
+            flops_fwd += 2.0 * cfg.B * cfg.lcb_n * nl * cfg.d                        # linear compression block
             if l == 0 and nl != cfg.stack_n:
                 flops_fwd += 2.0 * cfg.B * cfg.stack_n * nl * cfg.d                  # residual C X
             nl = cfg.stack_n
@@ -290,6 +301,7 @@ def main():
                    "batches_cycled": len(batches), "parallelism": "single-gpu",
                    "fp8_top": args.fp8,
                    "top_act": cfg.top_act,
+                   "lcb_n": cfg.lcb_n if cfg.interact == "stack" else None,
                    "norm_block": cfg.norm_block if cfg.top_act != "relu" else None,
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,

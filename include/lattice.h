@@ -166,19 +166,24 @@ lattice_status lattice_validate_batch(const lattice_tables* tables, const lattic
 /* Interaction (Section 3.3.2)                                              */
 /* ------------------------------------------------------------------------ */
 
-/* One layer of the FM stack: F = X (X^T W) (rank k), H = A vec(F) reshaped
- * to [n_out, dim] (no bias: bias-less backbone, Section 3.3.4), residual
- * R = C X (C != NULL, a linear compression block) or R = X, output
- * LayerNorm_gamma(H + R) per vector over dim (gain only, fp32 math). */
+/* One layer of the stacked fusion blocks (DHEN/Wukong fusion block, Section
+ * 3.3.2): the factorization-machine block F = X (X^T W) (rank k), H_F =
+ * A vec(F) reshaped to [n_out - n_lcb, dim] (no bias: bias-less backbone,
+ * Section 3.3.4); with n_lcb > 0 the linear compression block H_L = L X
+ * ([n_lcb, dim]) is concatenated after it, H = [H_F; H_L]; residual R = C X
+ * (C != NULL, a linear projection) or R = X; output LayerNorm_gamma(H + R)
+ * per vector over dim (gain only, fp32 math). */
 typedef struct {
   const void* W;        /* device [n_in, rank] */
-  const void* A;        /* device [n_out*dim, n_in*rank] */
+  const void* A;        /* device [(n_out - n_lcb)*dim, n_in*rank] */
   const void* C;        /* device [n_out, n_in] or NULL (requires n_in == n_out) */
   const float* gamma;   /* device [dim] */
   float* dW;            /* device fp32 grads, same shapes (bwd) */
   float* dA;
   float* dC;
   float* dgamma;
+  const void* L;        /* device [n_lcb, n_in] (n_lcb > 0), else ignored */
+  float* dL;            /* device [n_lcb, n_in] fp32 (bwd) */
 } lattice_stack_layer;
 
 typedef struct {
@@ -194,6 +199,8 @@ typedef struct {
   int32_t stack_n;       /* STACK: vectors per layer output */
   float ln_eps;          /* STACK: LayerNorm epsilon */
   const lattice_stack_layer* layers;  /* host [n_layers] */
+  int32_t lcb_n;         /* STACK: output vectors of each layer's linear compression
+                            block (0: FM block only; < stack_n) */
 } lattice_interact_desc;
 
 /* DOT: out[b, m(i,j)] = <X[b,i], X[b,j]> for i<j, m(i,j) row-major over the

@@ -246,6 +246,12 @@ def _stack_forward_bounds(layers, caches, eX, d, rnd, us):
         eH = matmul_err(vecF, eF2, A.T, None, nl * k)
         eH = (eH[0].reshape(B, -1, d), eH[1].reshape(B, -1, d))
         H = (vecF @ A.T).reshape(B, -1, d)
+        if lay.get("L") is not None:              # linear compression block rows
+            Lm = np.asarray(lay["L"], np.float64)
+            Lb = np.broadcast_to(Lm[None], (B,) + Lm.shape)
+            eHL = matmul_err(Lb, None, Xl, eXl, nl)
+            H = np.concatenate([H, Lb @ Xl], axis=1)
+            eH = (np.concatenate([eH[0], eHL[0]], axis=1), np.concatenate([eH[1], eHL[1]], axis=1))
         if lay.get("C") is not None:
             C = np.asarray(lay["C"], np.float64)
             Cb = np.broadcast_to(C[None], (B,) + C.shape)
@@ -297,8 +303,9 @@ def _stack_backward_bounds(layers, caches, st_fwd, dY, edY, rnd, us):
                (edY[1] * ax + np.abs(dY) * sf["ex"][1]).reshape(-1, d).max(0))
         duR = rnd(du)
         eduR = rounded(edu, duR, us)
-        du2 = duR.reshape(B, -1)
-        edu2 = (eduR[0].reshape(B, -1), eduR[1].reshape(B, -1))
+        nF = A.shape[0] // d
+        du2 = duR[:, :nF].reshape(B, -1)
+        edu2 = (eduR[0][:, :nF].reshape(B, -1), eduR[1][:, :nF].reshape(B, -1))
         vecF = cl["vecF"]
         eF2 = (sf["eF"][0].reshape(B, -1), sf["eF"][1].reshape(B, -1))
         edA = matmul_err(du2.T, _Te2(edu2), vecF, eF2, B)
@@ -308,6 +315,16 @@ def _stack_backward_bounds(layers, caches, st_fwd, dY, edY, rnd, us):
         edXl, edW = _fm_backward_bounds(dF, edF, Xl, sf["eX"], W, P, sf["eP"], rnd, us)
         gl = dict(dW=edW, dA=edA, dgamma=edg)
         dFm, _ = fm_backward(dF, Xl, W, P, rnd)
+        if lay.get("L") is not None:              # linear compression block
+            Lm = np.asarray(lay["L"], np.float64)
+            Xt = _T(Xl)
+            dL_, edL_ = duR[:, nF:], (eduR[0][:, nF:], eduR[1][:, nF:])
+            sb, mb = _add(matmul_err(dL_, edL_, Xt, None, 0), matmul_err(dL_, None, Xt, _Te(sf["eX"]), 0))
+            gl["dL"] = (np.sqrt(_sq(sb).sum(0) + B * d * UA * UA * _sq((np.abs(dL_) @ np.abs(Xt)).sum(0))),
+                        mb.max(0))
+            LTb = np.broadcast_to(Lm.T[None], (B,) + Lm.T.shape)
+            edXl = _add(edXl, matmul_err(LTb, None, dL_, edL_, Lm.shape[0]))
+            dFm = dFm + LTb @ dL_
         if lay.get("C") is not None:
             C = np.asarray(lay["C"], np.float64)
             Xt = _T(Xl)

@@ -88,14 +88,24 @@ def layernorm_backward(dy, xhat, rstd, gamma):
 
 
 def stack_forward(X1, layers, n_out, d, rnd, eps):
-    """Returns (X_{L+1}, per-layer caches)."""
+    """Returns (X_{L+1}, per-layer caches).  A layer with an ``L`` matrix
+    ([n_lcb, n_in]) is a full fusion block: its FM block fills the first
+    ``n_out - n_lcb`` output vectors and the linear compression block
+    ``L X`` the last ``n_lcb`` (concatenated before the residual and the
+    LayerNorm)."""
     X = np.asarray(X1, np.float64)
     B = X.shape[0]
     caches = []
     for lay in layers:
         Fm, P = fm_forward(X, lay["W"], rnd)                  # [B, n, k]
         vecF = Fm.reshape(B, -1)
-        H = (vecF @ np.asarray(lay["A"], np.float64).T).reshape(B, n_out, d)
+        HF = (vecF @ np.asarray(lay["A"], np.float64).T).reshape(B, -1, d)
+        if lay.get("L") is not None:
+            HL = np.einsum("vu,bud->bvd", np.asarray(lay["L"], np.float64), X)
+            H = np.concatenate([HF, HL], axis=1)
+        else:
+            H = HF
+        assert H.shape[1] == n_out
         if lay.get("C") is not None:
             res = np.einsum("vu,bud->bvd", np.asarray(lay["C"], np.float64), X)
         else:
@@ -117,12 +127,17 @@ def stack_backward(dY, layers, caches, rnd):
         B, n, _ = X.shape
         du, dgamma = layernorm_backward(dY, c["xhat"], c["rstd"], lay["gamma"])
         duR = rnd(du)
-        du2 = duR.reshape(B, -1)
         A = np.asarray(lay["A"], np.float64)
+        nF = A.shape[0] // du.shape[2]                       # FM-block output vectors
+        du2 = duR[:, :nF].reshape(B, -1)
         dA = du2.T @ c["vecF"]
         dF = rnd((du2 @ A).reshape(B, n, -1))
         dX, dW = fm_backward(dF, X, lay["W"], c["P"], rnd)
         g = dict(dW=dW, dA=dA, dgamma=dgamma)
+        if lay.get("L") is not None:
+            Lm = np.asarray(lay["L"], np.float64)
+            g["dL"] = np.einsum("bvd,bud->vu", duR[:, nF:], X)
+            dX = dX + np.einsum("vu,bvd->bud", Lm, duR[:, nF:])
         if lay.get("C") is not None:
             C = np.asarray(lay["C"], np.float64)
             g["dC"] = np.einsum("bvd,bud->vu", duR, X)

@@ -40,14 +40,15 @@ class lattice_sparse_grad(Structure):
 
 class lattice_stack_layer(Structure):
     _fields_ = [("W", c_void_p), ("A", c_void_p), ("C", c_void_p), ("gamma", c_void_p),
-                ("dW", c_void_p), ("dA", c_void_p), ("dC", c_void_p), ("dgamma", c_void_p)]
+                ("dW", c_void_p), ("dA", c_void_p), ("dC", c_void_p), ("dgamma", c_void_p),
+                ("L", c_void_p), ("dL", c_void_p)]
 
 
 class lattice_interact_desc(Structure):
     _fields_ = [("kind", c_int), ("dtype", c_int), ("n", c_int32), ("dim", c_int32),
                 ("rank", c_int32), ("emit_slot0", c_int32), ("fm_W", c_void_p),
                 ("fm_dW", c_void_p), ("n_layers", c_int32), ("stack_n", c_int32),
-                ("ln_eps", c_float), ("layers", POINTER(lattice_stack_layer))]
+                ("ln_eps", c_float), ("layers", POINTER(lattice_stack_layer)), ("lcb_n", c_int32)]
 
 
 class lattice_linear(Structure):

@@ -142,13 +142,18 @@ def _ptr(t):
 
 
 def stack_layers(layers):
-    """layers: list of dicts W, A, C (or None), gamma, dW, dA, dC, dgamma (device tensors)."""
+    """layers: list of dicts W, A, C (or None), gamma, dW, dA, dC, dgamma, and
+    for full fusion blocks L, dL (device tensors)."""
     arr = (A.lattice_stack_layer * len(layers))()
     for i, L in enumerate(layers):
-        _contig(*(L.get(k) for k in ("W", "A", "C", "gamma")))
+        _contig(*(L.get(k) for k in ("W", "A", "C", "gamma", "L")))
         arr[i] = A.lattice_stack_layer(*(_ptr(L.get(k)) for k in
-                                         ("W", "A", "C", "gamma", "dW", "dA", "dC", "dgamma")))
+                                         ("W", "A", "C", "gamma", "dW", "dA", "dC", "dgamma", "L", "dL")))
     return arr
+
+
+def _lcb_n(stack):
+    return int(stack[0]["L"].shape[0]) if stack and stack[0].get("L") is not None else 0
 
 
 def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0, stack=None, stack_n=0,
@@ -161,7 +166,7 @@ def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0, stack=None
                                 rank=(fm_W.shape[1] if fm_W is not None else rank),
                                 emit_slot0=int(emit_slot0), fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
                                 n_layers=len(stack) if stack else 0, stack_n=stack_n,
-                                ln_eps=ln_eps, layers=arr)
+                                ln_eps=ln_eps, layers=arr, lcb_n=_lcb_n(stack))
     d._keep = arr
     return d
 
@@ -324,7 +329,7 @@ class StepModel:
                                         emit_slot0=int(dense_in > 0 and interact != "stack"),
                                         fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
                                         n_layers=len(stack) if stack else 0, stack_n=stack_n,
-                                        ln_eps=ln_eps, layers=self._stack)
+                                        ln_eps=ln_eps, layers=self._stack, lcb_n=_lcb_n(stack))
         self.desc = A.lattice_model_desc(dtype=dt, pool=_POOL[pool],
                                          tables=_tables(tables, row_base, max_rows),
                                          num_features=num_features, dense_in=dense_in,

@@ -110,10 +110,11 @@ static hipError_t zero_interact_grads(const lattice_interact_desc* d, hipStream_
   int n_in = d->n;
   for (int l = 0; l < d->n_layers; ++l) {
     const lattice_stack_layer& L = d->layers[l];
-    const int64_t nd = (int64_t)d->stack_n * d->dim;
+    const int64_t nd = (int64_t)(d->stack_n - d->lcb_n) * d->dim;
     hipError_t e = zero_f32(L.dW, (int64_t)n_in * d->rank, s);
     if (e == hipSuccess) e = zero_f32(L.dA, nd * n_in * d->rank, s);
     if (e == hipSuccess && L.C) e = zero_f32(L.dC, (int64_t)d->stack_n * n_in, s);
+    if (e == hipSuccess && d->lcb_n > 0) e = zero_f32(L.dL, (int64_t)d->lcb_n * n_in, s);
     if (e == hipSuccess) e = zero_f32(L.dgamma, d->dim, s);
     if (e != hipSuccess) return e;
     n_in = d->stack_n;
@@ -308,13 +309,14 @@ static StackShape stack_shape(const lattice_interact_desc* d) {
   sh.k = d->rank;
   sh.has_C0 = (d->layers && d->n_layers > 0 && d->layers[0].C) ? 1 : 0;
   sh.eps = d->ln_eps;
+  sh.nL = d->lcb_n;
   return sh;
 }
 
 static void stack_layers(const lattice_interact_desc* d, StackLayer* out) {
   for (int l = 0; l < d->n_layers; ++l) {
     const lattice_stack_layer& L = d->layers[l];
-    out[l] = StackLayer{L.W, L.A, L.C, L.gamma, L.dW, L.dA, L.dC, L.dgamma};
+    out[l] = StackLayer{L.W, L.A, L.C, L.gamma, L.dW, L.dA, L.dC, L.dgamma, L.L, L.dL};
   }
 }
 
@@ -338,9 +340,11 @@ static lattice_status check_interact(const lattice_interact_desc* d, int32_t B) 
             LATTICE_MAX_LAYERS);
     REQUIRE(d->rank >= 1 && d->stack_n >= 1 && d->ln_eps > 0.f, "STACK needs rank, stack_n, ln_eps > 0");
     REQUIRE(!d->emit_slot0, "STACK does not emit slot 0");
+    REQUIRE(d->lcb_n >= 0 && d->lcb_n < d->stack_n, "lcb_n must be in 0 .. stack_n - 1");
     for (int l = 0; l < d->n_layers; ++l) {
       const lattice_stack_layer& L = d->layers[l];
       REQUIRE(L.W && L.A && L.gamma, "STACK layer %d: null W/A/gamma", l);
+      if (d->lcb_n > 0) REQUIRE(L.L, "STACK layer %d: lcb_n > 0 needs L", l);
       if (l == 0 && d->n != d->stack_n) REQUIRE(L.C, "STACK layer 0 needs C when n != stack_n");
       if (l > 0) REQUIRE(!L.C, "STACK layer %d: only layer 0 may have C", l);
     }

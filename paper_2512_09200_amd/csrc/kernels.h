@@ -127,15 +127,18 @@ hipError_t dot_mfma(bool fwd, const void* X, int B, int n, int d, void* out, int
 // stack.hip (stacked FM -> linear -> residual -> LayerNorm interaction)
 struct StackShape {
   int L, n0, nv, d, k;  // layers, input vectors, vectors per layer output, dim, FM rank
-  int has_C0;           // layer 0 uses a compression residual C [nv, n0]
+  int has_C0;           // layer 0 uses a projection residual C [nv, n0]
   float eps;
+  int nL;               // output vectors of the linear compression block (0: none)
 };
 struct StackLayer {
   const void* W;        // [n, k] bf16
-  const void* A;        // [nv*d, n*k] bf16
+  const void* A;        // [(nv - nL)*d, n*k] bf16
   const void* C;        // [nv, n0] bf16 (layer 0) or null
   const float* gamma;   // [d]
   float* dW; float* dA; float* dC; float* dgamma;
+  const void* Lc;       // [nL, n] bf16 (nL > 0)
+  float* dL;
 };
 struct StackPlan {       // byte offsets inside the interaction workspace
   size_t P[8], F[8], H[8], mean[8], rstd[8], Xn[8], R0, state_bytes;

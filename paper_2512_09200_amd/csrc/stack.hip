@@ -1,7 +1,9 @@
-// Stacked interaction of the deep workload: L layers of
-//   F = X (X^T W)                      (FM block, rank k; Section 3.3.2)
-//   H = vec(F) A^T                     (linear compression to nv vectors of dim d, no bias)
-//   u = H + R,  R = C X or R = X       (residual; C is a linear compression block)
+// Stacked interaction of the deep workload: L fusion blocks (DHEN/Wukong,
+// Section 3.3.2) of
+//   F = X (X^T W)                      (FM block, rank k)
+//   H_F = vec(F) A^T                   (its projection to nv - nL vectors of dim d, no bias)
+//   H_L = L X                          (linear compression block, nL vectors; nL = 0: none)
+//   u = [H_F; H_L] + R,  R = C X or X  (residual; C a linear projection)
 //   X' = LayerNorm_gamma(u)            (per vector over d, gain only, fp32 math)
 // and the exact backward.  The contractions run on the bf16 MFMA GEMM
 // (batched over samples where they are per-sample products, K-segmented
@@ -179,6 +181,10 @@ StackPlan stack_plan(const StackShape& sh, int B) {
       g.M = sh.nv; g.N = sh.n0; g.K = B * sh.d;
       gw = gw > gemm_workspace(g) ? gw : gemm_workspace(g);
     }
+    if (sh.nL > 0) {
+      g.M = sh.nL; g.N = n; g.K = B * sh.d;
+      gw = gw > gemm_workspace(g) ? gw : gemm_workspace(g);
+    }
   }
   p.gemm_ws = take(gw);
   p.total_bytes = off;
@@ -221,7 +227,7 @@ static hipError_t ln_bwd_launch(int E, const float* H, const RT* res, const floa
 bool stack_supported(const StackShape& sh) {
   return sh.L >= 1 && sh.L <= 8 && (sh.d == 64 || sh.d == 128 || sh.d == 256) && sh.k >= 1 &&
          sh.n0 >= 1 && sh.nv >= 1 && (sh.has_C0 || sh.n0 == sh.nv) && sh.k % 8 == 0 &&
-         sh.n0 % 2 == 0 && sh.nv % 2 == 0;
+         sh.n0 % 2 == 0 && sh.nv % 2 == 0 && sh.nL >= 0 && sh.nL < sh.nv;
 }
 
 // Forward.  X [B, n0, d] bf16; out rows (stride out_stride) receive vec(X_L).
@@ -252,13 +258,23 @@ hipError_t stack_fwd(const StackShape& sh, const StackLayer* Ls, int B, const vo
     g2.C = F; g2.ldc = k; g2.c_dt = DT_BF16; g2.sC = (int64_t)n * k;
     g2.M = n; g2.N = k; g2.K = d; g2.batch = B;
     STK_CHECK(gemm(g2, nullptr, s));
-    // H = vec(F) A^T: M = B, N = nv*d, K = n*k
+    // H_F = vec(F) A^T: M = B, N = (nv - nL)*d, K = n*k (the first nv - nL vectors of H)
+    const int nF = nv - sh.nL;
     GemmArgs g3;
     g3.A = F; g3.lda = (int64_t)n * k;
     g3.B = Ls[l].A; g3.ldb = (int64_t)n * k;
     g3.C = H; g3.ldc = nvd; g3.c_dt = DT_F32;
-    g3.M = B; g3.N = (int)nvd; g3.K = n * k;
+    g3.M = B; g3.N = nF * d; g3.K = n * k;
     STK_CHECK(gemm(g3, nullptr, s));
+    if (sh.nL > 0) {
+      // H_L,b = L X_b (the last nL vectors of H): M = nL, N = d, K = n
+      GemmArgs gl;
+      gl.A = Ls[l].Lc; gl.lda = n;
+      gl.B = Xl; gl.ldb = d; gl.tb = 1; gl.sB = (int64_t)n * d;
+      gl.C = H + (int64_t)nF * d; gl.ldc = d; gl.c_dt = DT_F32; gl.sC = nvd;
+      gl.M = sh.nL; gl.N = d; gl.K = n; gl.batch = B;
+      STK_CHECK(gemm(gl, nullptr, s));
+    }
     bf16_t* Xn = l + 1 < sh.L ? (bf16_t*)(base + p.Xn[l]) : (bf16_t*)out;
     const int64_t ostr = l + 1 < sh.L ? nvd : out_stride;
     float* mean = (float*)(base + p.mean[l]);
@@ -326,19 +342,21 @@ hipError_t stack_bwd(const StackShape& sh, const StackLayer* Ls, int B, const vo
         STK_CHECK(ln_bwd_launch<bf16_t, float>(d / 64, H, Xl, Ls[l].gamma, mean, rstd, dY, nvd,
                                                nvec, nv, du, duR, dgp, Ls[l].dgamma, d, s));
     }
-    // dA = duR^T vec(F): M = nv*d, N = n*k, K = B
+    // the FM block's part of du: its first nF vectors
+    const int nF = nv - sh.nL;
+    // dA = duR_F^T vec(F): M = nF*d, N = n*k, K = B
     GemmArgs a1;
     a1.A = duR; a1.lda = nvd; a1.ta = 1;
     a1.B = F; a1.ldb = (int64_t)n * k; a1.tb = 1;
     a1.C = Ls[l].dA; a1.ldc = (int64_t)n * k; a1.c_dt = DT_F32;
-    a1.M = (int)nvd; a1.N = n * k; a1.K = B; a1.max_splits = 16;
+    a1.M = nF * d; a1.N = n * k; a1.K = B; a1.max_splits = 16;
     STK_CHECK(gemm(a1, gws, s));
-    // dF = round(duR A): M = B, N = n*k, K = nv*d
+    // dF = round(duR_F A): M = B, N = n*k, K = nF*d
     GemmArgs a2;
     a2.A = duR; a2.lda = nvd;
     a2.B = Ls[l].A; a2.ldb = (int64_t)n * k; a2.tb = 1;
     a2.C = dF; a2.ldc = (int64_t)n * k; a2.c_dt = DT_BF16;
-    a2.M = B; a2.N = n * k; a2.K = (int)nvd;
+    a2.M = B; a2.N = n * k; a2.K = nF * d;
     STK_CHECK(gemm(a2, nullptr, s));
     // dP_b = round(X_b^T G_b): M = d, N = k, K = n
     GemmArgs f1;
@@ -358,6 +376,23 @@ hipError_t stack_bwd(const StackShape& sh, const StackLayer* Ls, int B, const vo
       f2.addend = du; f2.ld_add = d; f2.s_add = nvd;
     }
     STK_CHECK(gemm(f2, nullptr, s));
+    if (sh.nL > 0) {
+      const bf16_t* duL = duR + (int64_t)nF * d;
+      // dX_b += L^T duR_L,b: M = n, N = d, K = nL
+      GemmArgs l2;
+      l2.A = Ls[l].Lc; l2.lda = n; l2.ta = 1;
+      l2.B = duL; l2.ldb = d; l2.tb = 1; l2.sB = nvd;
+      l2.C = dXf; l2.ldc = d; l2.c_dt = DT_F32; l2.sC = (int64_t)n * d; l2.accumulate = 1;
+      l2.M = n; l2.N = d; l2.K = sh.nL; l2.batch = B;
+      STK_CHECK(gemm(l2, nullptr, s));
+      // dL = sum_b duR_L,b X_b^T: M = nL, N = n, K = (b, a)
+      GemmArgs l1;
+      l1.A = duL; l1.lda = d; l1.kseg = d; l1.ksA = nvd;
+      l1.B = Xl; l1.ldb = d; l1.ksB = (int64_t)n * d;
+      l1.C = Ls[l].dL; l1.ldc = n; l1.c_dt = DT_F32;
+      l1.M = sh.nL; l1.N = n; l1.K = B * d; l1.max_splits = SAMPLE_SUM_SPLITS;
+      STK_CHECK(gemm(l1, gws, s));
+    }
     // dX_b += W dP_b^T: M = n, N = d, K = k  (bf16 output when this ends the chain)
     GemmArgs f3;
     f3.A = Ls[l].W; f3.lda = k;

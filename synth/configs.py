@@ -36,6 +36,7 @@ class Config:
     fm_rank: int = 0             # k of the FM block (fm / stack)
     stack_layers: int = 0        # number of FM-stack layers
     stack_n: int = 0             # vectors kept per stack layer
+    lcb_n: int = 0               # of those, vectors from the linear compression block (0: FM block only)
     label_p: Tuple = ("fixed", 0.3)          # or ("uniform", lo, hi) per objective
     mask: Tuple = ("none",)                  # ("none",) | ("iid", keep) | ("domain",)
     domains: Optional[Tuple] = None          # (proportions, active features, labelled heads)

@@ -235,10 +235,13 @@ def make_dense_params(cfg: Config) -> Dict[str, object]:
         n_l = n
         for l in range(cfg.stack_layers):
             Wl = w(r.standard_normal((n_l, cfg.fm_rank)) / math.sqrt(n_l))
-            Al = w(_glorot(r, cfg.stack_n * cfg.d, n_l * cfg.fm_rank))
+            Al = w(_glorot(r, (cfg.stack_n - cfg.lcb_n) * cfg.d, n_l * cfg.fm_rank))
             Cl = w(_glorot(r, cfg.stack_n, n_l)) if n_l != cfg.stack_n else None
             gl = f32(1.0 + 0.1 * r.standard_normal(cfg.d))
-            layers.append(dict(W=Wl, A=Al, C=Cl, gamma=gl))
+            lay = dict(W=Wl, A=Al, C=Cl, gamma=gl)
+            if cfg.lcb_n:
+                lay["L"] = w(_glorot(r, cfg.lcb_n, n_l))
+            layers.append(lay)
             n_l = cfg.stack_n
         out["stack"] = layers
     return out

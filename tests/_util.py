@@ -328,7 +328,7 @@ def grads_of(w):
              bottom_dW=[L["dW"] for L in w.bottom], bottom_db=[L["db"] for L in w.bottom],
              fm_dW=w.fm_dW, top_dgain=[L["dgain"] for L in w.top if "dgain" in L])
     if w.stack is not None:
-        g["stack"] = [{k: lay[k] for k in ("dW", "dA", "dgamma", "dC") if lay.get(k) is not None}
+        g["stack"] = [{k: lay[k] for k in ("dW", "dA", "dgamma", "dC", "dL") if lay.get(k) is not None}
                       for lay in w.stack]
     return g
 
@@ -397,6 +397,8 @@ def stack_dev(layers, sdt):
                  C=to_dev(lay["C"], sdt) if lay["C"] is not None else None)
         d.update(dW=z(lay["W"]), dA=z(lay["A"]), dgamma=z(lay["gamma"]),
                  dC=z(lay["C"]) if lay["C"] is not None else None)
+        if lay.get("L") is not None:
+            d.update(L=to_dev(lay["L"], sdt), dL=z(lay["L"]))
         out.append(d)
     return out
 

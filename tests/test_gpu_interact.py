@@ -104,9 +104,13 @@ def check_interact(kind, dt, B, n, d, k, emit0, zero_slots, pad=0):
 
 
 STACK_CASES = {
-    # name: (B, n0, stack_n, d, rank, layers)
-    "stack-C-d64": (96, 24, 8, 64, 16, 3),     # compression residual on layer 1
-    "stack-id-d128": (40, 16, 16, 128, 32, 2),  # identity residual throughout
+    # name: (B, n0, stack_n, d, rank, layers, lcb_n)
+    "stack-C-d64": (96, 24, 8, 64, 16, 3, 0),     # compression residual on layer 1
+    "stack-id-d128": (40, 16, 16, 128, 32, 2, 0),  # identity residual throughout
+    # full fusion blocks: FM block and linear compression block concatenated
+    "dwfb-C-d64": (96, 24, 8, 64, 16, 3, 3),
+    "dwfb-id-d128": (40, 16, 16, 128, 32, 2, 6),
+    "dwfb-C-d128-lcb1": (33, 30, 10, 128, 16, 2, 1),
 }
 
 
@@ -116,10 +120,10 @@ def test_stack_fwd_bwd(name):
     from paper_2512_09200_amd import api
     from oracle import bounds as obounds
     from tests._util import assert_close_derived, stack_dev
-    B, n0, nv, d, k, L = STACK_CASES[name]
+    B, n0, nv, d, k, L, nL = STACK_CASES[name]
     print(f"[stack] {name}", flush=True)
     cfg = synth.DEEP_STACK.scaled(B=B, F=n0, d=d, stack_n=nv, fm_rank=k, stack_layers=L,
-                            top=(16, 4), seed=77)
+                                  lcb_n=nL, top=(16, 4), seed=77)
     params = synth.make_dense_params(cfg)
     layers = params["stack"]
     rnd = rounding("bf16")
@@ -146,6 +150,6 @@ def test_stack_fwd_bwd(name):
                          2e-2)
     assert_close_derived("dX", dX, rnd(dX1), obounds.rounded(edX, dX1, 2.0 ** -8), 2e-2)
     for l, (gl, dl, el) in enumerate(zip(grads, dev_layers, eg)):
-        for key in ("dW", "dA", "dgamma", "dC"):
+        for key in ("dW", "dA", "dgamma", "dC", "dL"):
             if key in gl:
                 assert_close_derived(f"layer{l}.{key}", dl[key], gl[key], el[key], 2e-2)

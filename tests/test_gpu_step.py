@@ -24,6 +24,9 @@ CASES = {
                                          top=(128, 32, 8)), 0.0),
     "deep-stack-small-d128": (synth.DEEP_STACK.scaled(B=48, F=32, rows=1000, stack_n=16, fm_rank=32,
                                           top=(256, 64, 16)), 0.0),
+    # full fusion blocks (FM block + linear compression block)
+    "deep-dwfb-small-d64": (synth.DEEP_STACK.scaled(B=64, F=24, rows=1500, d=64, stack_n=8, fm_rank=16,
+                                                    lcb_n=3, top=(128, 32, 8)), 0.01),
 }
 SPARE = {"mid-small": 12345}   # workspace planned with more lookups than the batch has
 
@@ -103,7 +106,7 @@ def check_step(cfg, lr, spare=0, w=None):
         assert_close_derived("fm.dW", w.fm_dW, g["fm_dW"], bd["fm_dW"], t)
     if cfg.interact == "stack":
         for l, (gl, dl, el) in enumerate(zip(g["stack"], w.stack, bd["stack"])):
-            for key in ("dW", "dA", "dgamma", "dC"):
+            for key in ("dW", "dA", "dgamma", "dC", "dL"):
                 if key in gl:
                     assert_close_derived(f"stack{l}.{key}", dl[key], gl[key], el[key], t)
     assert_close_derived("dX_emb", v["dX"][:, s0:], g["dX_emb"], bd["dX_emb"], t)

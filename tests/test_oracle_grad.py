@@ -24,6 +24,11 @@ def _tiny_cfg(kind, pool="sum"):
     if kind == "stack":
         return synth.Config(name="t-stack", F=5, dense_in=0, bottom=(), interact="stack",
                             fm_rank=2, stack_layers=2, stack_n=3, top=(4, 2), **base)
+    if kind == "dwfb":
+        # full fusion blocks: 2 of the 3 output vectors from the FM block, 1 from
+        # the linear compression block
+        return synth.Config(name="t-dwfb", F=5, dense_in=0, bottom=(), interact="stack",
+                            fm_rank=2, stack_layers=2, stack_n=3, lcb_n=1, top=(4, 2), **base)
     if kind in ("swishrn", "hardswishrn"):
         # SwishRN hidden top layers, BlockNorm groups of 2 (3, 2, 2, 1 features
         # over widths 7 and 5: a ragged last group)
@@ -66,6 +71,8 @@ def _pairs(cfg, params, g):
         sg = g["stack"][i]
         out += [(lay["W"], sg["dW"], f"stack{i}.W"), (lay["A"], sg["dA"], f"stack{i}.A"),
                 (lay["gamma"], sg["dgamma"], f"stack{i}.gamma")]
+        if lay.get("L") is not None:
+            out.append((lay["L"], sg["dL"], f"stack{i}.L"))
         if lay["C"] is not None:
             out.append((lay["C"], sg["dC"], f"stack{i}.C"))
     return out
@@ -140,7 +147,7 @@ def _fd_worst(kind, pool="sum", n_coords=12):
 
 
 @pytest.mark.parametrize("kind,pool", [("dot", "sum"), ("dot", "mean"), ("fm", "sum"), ("stack", "sum"),
-                                       ("swishrn", "sum"), ("hardswishrn", "sum")])
+                                       ("dwfb", "sum"), ("swishrn", "sum"), ("hardswishrn", "sum")])
 def test_finite_differences(kind, pool):
     assert _fd_worst(kind, pool) < 1e-6
 

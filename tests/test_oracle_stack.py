@@ -134,7 +134,33 @@ def check_two_layers(fn=None, seed=3):
     return max(_maxabs(got2 - exp2), 0.0 if np.all(np.isfinite(got)) else np.inf)
 
 
-PINS = [check_selection, check_normalised, check_residual_only, check_two_layers]
+def check_lcb(fn=None, seed=4):
+    """A full fusion block: the selection case's FM-block vectors followed
+    by linear-compression vectors (L X, brute-force sums), then + C X and
+    LayerNorm."""
+    rng = np.random.default_rng(seed)
+    n, d, nF, nL = 4, 6, 3, 2
+    X, lay, _ = _selection_case(rng, n=n, d=d, n_out=nF, with_C=False)
+    Lm = rng.standard_normal((nL, n))
+    C = rng.standard_normal((nF + nL, n))
+    lay = dict(lay, L=Lm, C=C)
+    got = _run(X, [lay], nF + nL, d, fn=fn)
+    k = n - 1
+    A, perm, gamma = lay["A"], lay["perm"], lay["gamma"]
+    worst = 0.0
+    for b in range(X.shape[0]):
+        Fm = np.array([[_brute_dot(X[b, i], X[b, perm[j]]) for j in range(k)] for i in range(n)])
+        HF = (A @ Fm.reshape(-1)).reshape(nF, d)
+        for v in range(nF + nL):
+            u = np.zeros(d)
+            for c in range(d):
+                h = HF[v, c] if v < nF else sum(Lm[v - nF, w] * X[b, w, c] for w in range(n))
+                u[c] = h + sum(C[v, w] * X[b, w, c] for w in range(n))
+            worst = max(worst, _maxabs(got[b, v] - _ln_ref(u, gamma)))
+    return worst
+
+
+PINS = [check_selection, check_normalised, check_residual_only, check_two_layers, check_lcb]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -151,9 +177,16 @@ def _stack_variant(mistake):
         for lay in layers:
             Fm, _ = interact.fm_forward(X, lay["W"], rnd)
             vecF = (Fm.transpose(0, 2, 1) if mistake == "vec_colmajor" else Fm).reshape(B, -1)
-            H = (vecF @ np.asarray(lay["A"]).T).reshape(B, n_out, d)
+            nF = np.asarray(lay["A"]).shape[0] // d
+            H = (vecF @ np.asarray(lay["A"]).T).reshape(B, nF, d)
             if mistake == "reshape_transposed":
-                H = (vecF @ np.asarray(lay["A"]).T).reshape(B, d, n_out).transpose(0, 2, 1)
+                H = (vecF @ np.asarray(lay["A"]).T).reshape(B, d, nF).transpose(0, 2, 1)
+            if lay.get("L") is not None:
+                Lm = np.asarray(lay["L"])
+                HL = np.einsum("vu,bud->bvd", Lm, X)
+                if mistake == "lcb_transposed_order":
+                    HL = np.einsum("vu,bud->bvd", Lm[::-1], X)
+                H = np.concatenate([HL, H] if mistake == "lcb_first" else [H, HL], axis=1)
             if lay.get("C") is not None:
                 R = np.einsum("vu,bud->bvd", lay["C"], X)
                 if mistake == "C_transposed" and lay["C"].shape[0] == lay["C"].shape[1]:
@@ -175,7 +208,8 @@ def _stack_variant(mistake):
 
 
 @pytest.mark.parametrize("mistake", ["vec_colmajor", "reshape_transposed", "ln_then_residual",
-                                     "no_residual", "ln_bessel", "C_transposed"])
+                                     "no_residual", "ln_bessel", "C_transposed", "lcb_first",
+                                     "lcb_transposed_order"])
 def test_planted_stack_mistakes_fail_a_pin(mistake):
     fn = _stack_variant(mistake)
     # the unmutated copy passes every pin (so a failure below is the mistake's)
