@@ -34,6 +34,24 @@ def linear_grads(g, h, W):
     return g.T @ h, g.sum(axis=0), g @ np.asarray(W, np.float64)
 
 
+def grouped_linear(h, W, b):
+    """Per-objective towers' heads (Section 3.3.3): W is ``[T, H]`` and output
+    t reads only its tower's inputs ``h[:, t*H:(t+1)*H]``:
+    ``a[:, t] = h[:, t*H:(t+1)*H] W[t] + b[t]``."""
+    h, W = np.asarray(h, np.float64), np.asarray(W, np.float64)
+    T, H = W.shape
+    assert h.shape[1] == T * H
+    return np.einsum("bth,th->bt", h.reshape(-1, T, H), W) + np.asarray(b, np.float64)
+
+
+def grouped_linear_grads(g, h, W):
+    """(dW [T, H], db, dh) of ``grouped_linear`` given ``g = dL/da``."""
+    g, h, W = (np.asarray(x, np.float64) for x in (g, h, W))
+    T, H = W.shape
+    h3 = h.reshape(-1, T, H)
+    return np.einsum("bt,bth->th", g, h3), g.sum(axis=0), (g[:, :, None] * W[None]).reshape(-1, T * H)
+
+
 def relu_band(h, W, b):
     """Half-width of the band around zero inside which the sign of a
     pre-activation is not fixed by fp32 accumulation: the worst-case error of
@@ -53,7 +71,7 @@ def linear_fp8(h, W, b):
     return _fp8.linear_fp8(qa, sa, qw, sw, b)
 
 
-def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=None):
+def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=None, grouped_last=False):
     """Returns ``(hs, masks)``: the layer inputs/outputs ``[h0, h1, ..., hL]``
     and, per layer, its ReLU decision (``None`` for a linear last layer).
     Every layer but (optionally) the last applies ReLU and storage rounding.
@@ -69,12 +87,16 @@ def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=N
     ``kind`` ("sigmoid" | "hard"), ``block`` (0: RMSNorm over the row; b:
     BlockNorm groups of b features), ``eps`` and ``gains`` (per layer
     ``(ga, gb)``).  Their entry in the returned list is then a dict
-    ``{"pre": a, "rho": ...}`` instead of a ReLU mask."""
+    ``{"pre": a, "rho": ...}`` instead of a ReLU mask.  ``grouped_last``:
+    the last (linear) layer is the towers' heads (``grouped_linear``)."""
     hs = [np.asarray(h0, np.float64)]
     masks = []
     for i, (W, b) in enumerate(layers):
-        a = linear_fp8(hs[-1], W, b) if i in fp8_layers else linear(hs[-1], W, b)
         last = i == len(layers) - 1
+        if grouped_last and last:
+            a = grouped_linear(hs[-1], W, b)
+        else:
+            a = linear_fp8(hs[-1], W, b) if i in fp8_layers else linear(hs[-1], W, b)
         if act is not None and (relu_last or not last):
             ga, gb = act["gains"][i]
             out, _, rho = _swishrn.forward(a, ga, gb, act["block"], act["eps"], act["kind"])
@@ -93,7 +115,8 @@ def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=N
     return hs, masks
 
 
-def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=None, dgains=None):
+def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=None, dgains=None,
+                 grouped_last=False):
     """Backward through ``mlp_forward``.  ``g_out`` is dL/d(hs[-1]) (before the
     last ReLU mask when ``relu_last``).  Returns (dWs, dbs, dL/dh0 or None).
     With ``act`` (as in ``mlp_forward``) the gain gradients of the SwishRN
@@ -120,7 +143,8 @@ def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=
     dh0 = None
     for i in range(L - 1, -1, -1):
         W, _ = layers[i]
-        dW, db, dh = linear_grads(g, hs[i], W)
+        grads = grouped_linear_grads if grouped_last and i == L - 1 else linear_grads
+        dW, db, dh = grads(g, hs[i], W)
         dWs[i], dbs[i] = dW, db
         if i > 0:
             g = through(i - 1, dh)

@@ -32,7 +32,7 @@ class Config:
     dense_in: int                # number of dense inputs (0: no dense path)
     bottom: Tuple[int, ...]      # bottom-MLP output widths; last == d
     interact: str                # "dot" | "fm" | "stack"
-    top: Tuple[int, ...]         # top-MLP output widths; last == T
+    top: Tuple[int, ...]         # top-MLP output widths; last == T (with towers: [..., T*towers, T])
     fm_rank: int = 0             # k of the FM block (fm / stack)
     stack_layers: int = 0        # number of FM-stack layers
     stack_n: int = 0             # vectors kept per stack layer
@@ -44,6 +44,8 @@ class Config:
     lr_tables: float = 0.0                   # row-sparse SGD step on the tables (0: none)
     seed: int = 0
     ln_eps: float = 1e-5
+    towers: int = 0                          # per-objective towers: hidden units per tower (0: none);
+                                             # the last top layer then reads only its tower's units
     top_act: str = "relu"                    # hidden top layers: "relu" | "swishrn" | "hardswishrn"
     norm_block: int = 128                    # SwishRN groups: 128 (BlockNorm) or 0 (the whole row)
     norm_eps: float = 1e-6

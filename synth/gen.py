@@ -44,7 +44,7 @@ from .configs import Config
 # stream ids (arbitrary, fixed)
 _S_BAGLEN, _S_INDEX, _S_DENSE, _S_LABEL_P, _S_LABEL, _S_MASK = 1, 2, 3, 4, 5, 6
 _S_DOMAIN, _S_PERM = 7, 8
-_S_BOTTOM, _S_TOP, _S_FM, _S_STACK, _S_TABLE, _S_GAIN = 20, 21, 22, 23, 24, 25
+_S_BOTTOM, _S_TOP, _S_FM, _S_STACK, _S_TABLE, _S_GAIN, _S_TOWER = 20, 21, 22, 23, 24, 25, 26
 _S_AUX = 40
 
 
@@ -221,6 +221,13 @@ def make_dense_params(cfg: Config) -> Dict[str, object]:
     out["bottom"] = [(w(W), f32(b)) for W, b in _mlp(cfg, _rng(cfg.seed, _S_BOTTOM), bdims)] if bdims else []
     tdims = (cfg.top_in,) + tuple(cfg.top)
     out["top"] = [(w(W), f32(b)) for W, b in _mlp(cfg, _rng(cfg.seed, _S_TOP), tdims)]
+    if cfg.towers:
+        # one tower per objective: objective t's head has weights on its
+        # tower's hidden units only, [T, towers]
+        T, H = cfg.top[-1], cfg.towers
+        assert cfg.top[-2] == T * H, "with towers the last hidden width is T * towers"
+        r = _rng(cfg.seed, _S_TOWER)
+        out["top"][-1] = (w(_glorot(r, T, H)), f32(r.standard_normal(T) * 0.01))
     if cfg.top_act != "relu":
         # SwishRN gains of the hidden layers: (g_a, g_b) per layer, near 1
         r = _rng(cfg.seed, _S_GAIN)

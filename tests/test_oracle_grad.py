@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import interact, step, swishrn
+from oracle import interact, mlp, step, swishrn
 
 
 def _tiny_cfg(kind, pool="sum"):
@@ -24,6 +24,10 @@ def _tiny_cfg(kind, pool="sum"):
     if kind == "stack":
         return synth.Config(name="t-stack", F=5, dense_in=0, bottom=(), interact="stack",
                             fm_rank=2, stack_layers=2, stack_n=3, top=(4, 2), **base)
+    if kind == "towers":
+        # per-objective towers: 3 objectives x 2 hidden units, then grouped heads
+        return synth.Config(name="t-towers", F=3, dense_in=3, bottom=(6, 4), interact="dot",
+                            top=(5, 6, 3), towers=2, **base)
     if kind == "dwfb":
         # full fusion blocks: 2 of the 3 output vectors from the FM block, 1 from
         # the linear compression block
@@ -97,6 +101,8 @@ def _check_kinks(cfg, params, table, batch):
         if hs is None:
             continue
         for i, (W, b) in enumerate(layers):
+            if top and i == len(layers) - 1:
+                continue                                   # the heads are linear
             a = hs[i] @ W.T + b
             if top and act is not None and i < len(layers) - 1:
                 if act["kind"] == "hard":
@@ -147,7 +153,8 @@ def _fd_worst(kind, pool="sum", n_coords=12):
 
 
 @pytest.mark.parametrize("kind,pool", [("dot", "sum"), ("dot", "mean"), ("fm", "sum"), ("stack", "sum"),
-                                       ("dwfb", "sum"), ("swishrn", "sum"), ("hardswishrn", "sum")])
+                                       ("dwfb", "sum"), ("towers", "sum"), ("swishrn", "sum"),
+                                       ("hardswishrn", "sum")])
 def test_finite_differences(kind, pool):
     assert _fd_worst(kind, pool) < 1e-6
 
@@ -173,6 +180,12 @@ def _layernorm_backward_dropped_term(dy, xhat, rstd, gamma):
 def _mlp_backward_no_relu_mask(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, **kw):
     masks = [None if m is None else np.ones_like(m) for m in masks]
     return _ORIG["mlp_backward"](g_out, hs, masks, layers, rnd, relu_last, need_input_grad, **kw)
+
+
+def _grouped_grads_wrong_tower(g, h, W):
+    dW, db, dh = _ORIG["grouped_linear_grads"](g, h, W)
+    T, H = W.shape
+    return dW, db, dh.reshape(-1, T, H)[:, ::-1].reshape(-1, T * H)      # gradient sent to the wrong tower
 
 
 def _swishrn_backward_no_mean_term(do, h, ga, gb, block, eps, kind, rho=None, grad_override=None):
@@ -205,7 +218,7 @@ def _dot_backward_no_slot0(dp, X):
 
 
 _ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward,
-             swishrn_backward=swishrn.backward)
+             swishrn_backward=swishrn.backward, grouped_linear_grads=mlp.grouped_linear_grads)
 
 
 @pytest.mark.parametrize("target,module,name,kind", [
@@ -216,8 +229,9 @@ _ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward,
     (_swishrn_backward_no_mean_term, swishrn, "backward", "swishrn"),
     (_swishrn_backward_whole_row_mean, swishrn, "backward", "hardswishrn"),
     (_swishrn_backward_gate_gain_swapped, swishrn, "backward", "swishrn"),
+    (_grouped_grads_wrong_tower, mlp, "grouped_linear_grads", "towers"),
 ], ids=["fm-sign", "layernorm-term", "relu-mask", "slot0-gradient", "swishrn-mean-term",
-        "blocknorm-group", "swishrn-gains"])
+        "blocknorm-group", "swishrn-gains", "tower-routing"])
 def test_planted_backward_mistakes_fail_the_finite_difference_pin(monkeypatch, target, module, name, kind):
     monkeypatch.setattr(module, name, target)
     assert _fd_worst(kind, n_coords=6) > 1e-3
