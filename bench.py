@@ -46,6 +46,9 @@ def parse():
                          "sigmoid or hard-sigmoid gate)")
     ap.add_argument("--norm-block", type=int, choices=[128, 0], default=128,
                     help="SwishRN groups: 128 (BlockNorm, in the GEMM epilogue) or 0 (whole-row RMSNorm)")
+    ap.add_argument("--towers", type=int, default=0,
+                    help="per-objective towers: the last hidden top layer becomes T towers of this many "
+                         "units each (replacing its width) and every head reads only its tower")
     ap.add_argument("--lcb-n", type=int, default=0,
                     help="stacked workloads: output vectors of each fusion block's linear compression "
                          "block (full DHEN/Wukong fusion blocks; 0: FM block only)")
@@ -82,6 +85,12 @@ def main():
     cfg = synth.WORKLOADS[args.workload]
     if args.uniform:
         cfg = cfg.scaled(index_dist=("uniform",))
+    if args.towers:
+        if args.fp8:
+            print("--fp8 needs the dense heads", file=sys.stderr)
+            sys.exit(2)
+        T = cfg.top[-1]
+        cfg = cfg.scaled(top=tuple(cfg.top[:-2]) + (T * args.towers, T), towers=args.towers)
     if args.lcb_n:
         if cfg.interact != "stack":
             print("--lcb-n needs a stacked workload", file=sys.stderr)
@@ -137,7 +146,8 @@ def main():
                           max_rows=cfg.rows,
                           bottom=bottom, top=top, interact=cfg.interact, fm_W=fm_W, fm_dW=fm_dW,
                           pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps,
-                          top_act=cfg.top_act, norm_block=cfg.norm_block, norm_eps=cfg.norm_eps)
+                          top_act=cfg.top_act, norm_block=cfg.norm_block, norm_eps=cfg.norm_eps,
+                          towers=bool(cfg.towers))
     nnz_max = max(b["nnz"] for b in batches)
     lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False, fp8_top=args.fp8)
     ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
@@ -235,7 +245,8 @@ def main():
     bwd_gbs = gbs(bwd_bytes, bwd_ms)
     n = cfg.n_slots
     flops_fwd = mlp_fwd_flops((cfg.dense_in,) + tuple(cfg.bottom), cfg.B) if cfg.has_dense else 0.0
-    flops_fwd += mlp_fwd_flops((cfg.top_in,) + tuple(cfg.top), cfg.B)
+    flops_fwd += mlp_fwd_flops((cfg.top_in,) + tuple(cfg.top[:-1]), cfg.B)
+    flops_fwd += 2.0 * cfg.B * cfg.top[-1] * (cfg.towers if cfg.towers else cfg.top[-2])   # heads
     if cfg.interact == "fm":
         flops_fwd += 4.0 * cfg.B * n * cfg.d * cfg.fm_rank
     elif cfg.interact == "dot":
@@ -302,6 +313,7 @@ def main():
                    "fp8_top": args.fp8,
                    "top_act": cfg.top_act,
                    "lcb_n": cfg.lcb_n if cfg.interact == "stack" else None,
+                   "towers": cfg.towers or None,
                    "norm_block": cfg.norm_block if cfg.top_act != "relu" else None,
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,

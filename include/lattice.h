@@ -278,6 +278,12 @@ typedef struct {
   lattice_activation act;           /* activation of the activated layers */
   int32_t norm_block;               /* SwishRN groups: 0 (whole row) or 128 (BlockNorm) */
   float norm_eps;                   /* SwishRN eps (>= 0) */
+  int32_t tower_heads;              /* 1: per-objective towers (Section 3.3.3): the last
+                                       (linear) layer's input holds T = out_dim groups of
+                                       H = in_dim / out_dim units, one tower per objective,
+                                       and output t reads only group t: its W and dW are
+                                       [T, H] (not [T, in_dim]); H % 8 == 0, the logits
+                                       contiguous.  0: a dense last layer. */
 } lattice_mlp_desc;
 
 /* Masked multi-objective BCE with logits z [B, T]: with N = max(1, sum m),

@@ -59,7 +59,8 @@ class lattice_linear(Structure):
 
 class lattice_mlp_desc(Structure):
     _fields_ = [("dtype", c_int), ("n_layers", c_int32), ("layers", POINTER(lattice_linear)),
-                ("relu_last", c_int32), ("act", c_int), ("norm_block", c_int32), ("norm_eps", c_float)]
+                ("relu_last", c_int32), ("act", c_int), ("norm_block", c_int32), ("norm_eps", c_float),
+                ("tower_heads", c_int32)]
 
 
 class lattice_loss_desc(Structure):

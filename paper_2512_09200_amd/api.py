@@ -201,7 +201,8 @@ def lattice_interact_bwd(kind, X, d_out, dX, emit_slot0=False, fm_W=None, fm_dW=
 _ACT = {None: A.ACT_RELU, "relu": A.ACT_RELU, "swishrn": A.ACT_SWISHRN, "hardswishrn": A.ACT_HARDSWISHRN}
 
 
-def mlp_desc(layers, relu_last, dtype, act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
+def mlp_desc(layers, relu_last, dtype, act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6,
+             tower_heads=False):
     """layers: list of dicts with W, b (optional), dW, db (optional); SwishRN
     layers (act "swishrn" / "hardswishrn") also gain [2, out] fp32, dgain
     (optional), and for lattice_mlp_heads_fwd/bwd pre [B, out] (storage
@@ -210,12 +211,15 @@ def mlp_desc(layers, relu_last, dtype, act=None, norm_block=A.BLOCKNORM_COLS, no
     for i, L in enumerate(layers):
         W = L["W"]
         _contig(W)
-        arr[i] = A.lattice_linear(in_dim=W.shape[1], out_dim=W.shape[0], W=W.data_ptr(),
+        # tower heads: W is [T, H] and the layer's input holds T groups of H
+        in_dim = W.shape[0] * W.shape[1] if (tower_heads and i == len(layers) - 1) else W.shape[1]
+        arr[i] = A.lattice_linear(in_dim=in_dim, out_dim=W.shape[0], W=W.data_ptr(),
                                   b=_ptr(L.get("b")), dW=_ptr(L.get("dW")), db=_ptr(L.get("db")),
                                   gain=_ptr(L.get("gain")), dgain=_ptr(L.get("dgain")),
                                   pre=_ptr(L.get("pre")), rinv=_ptr(L.get("rinv")))
     d = A.lattice_mlp_desc(dtype=dtype, n_layers=len(layers), layers=arr, relu_last=int(relu_last),
-                           act=_ACT[act], norm_block=int(norm_block), norm_eps=float(norm_eps))
+                           act=_ACT[act], norm_block=int(norm_block), norm_eps=float(norm_eps),
+                           tower_heads=int(bool(tower_heads)))
     d._keep = arr
     return d
 
@@ -226,12 +230,13 @@ def swishrn_groups(N, norm_block):
 
 
 def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None, act=None,
-                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
+                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6, tower_heads=False):
     """acts: list of output tensors (2-D, unit column stride); loss: optional
     dict(labels, mask, loss, d_logits, d_logits_op); act / norm_block /
-    norm_eps: the activation (see mlp_desc)."""
+    norm_eps: the activation, tower_heads: the last layer is the heads of
+    per-objective towers (see mlp_desc)."""
     lib = load()
-    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps)
+    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps, tower_heads)
     n = len(layers)
     ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
     strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
@@ -249,9 +254,9 @@ def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None, ac
 
 
 def lattice_mlp_heads_bwd(layers, x, acts, d_out, relu_last, d_in=None, stream=None, act=None,
-                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
+                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6, tower_heads=False):
     lib = load()
-    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps)
+    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps, tower_heads)
     n = len(layers)
     ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
     strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
@@ -311,17 +316,19 @@ class StepModel:
     {W, b, dW, db} (SwishRN top layers: also gain, dgain); fm_W / fm_dW for
     the FM interaction; max_rows: rows of the largest table (None: read from
     row_base once, here); top_act: None / "relu", "swishrn" or "hardswishrn"
-    for the top MLP's hidden layers."""
+    for the top MLP's hidden layers; towers: the top MLP's last layer is the
+    heads of per-objective towers (its W [T, H])."""
 
     def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
                  fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5,
-                 max_rows=None, top_act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6):
+                 max_rows=None, top_act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6,
+                 towers=False):
         _contig(tables, row_base)
         dt = _dt(tables)
         d = tables.shape[1]
         n = num_features + (1 if dense_in > 0 else 0)
         self._bottom = mlp_desc(bottom, True, dt) if dense_in > 0 else A.lattice_mlp_desc(dtype=dt)
-        self._top = mlp_desc(top, False, dt, top_act, norm_block, norm_eps)
+        self._top = mlp_desc(top, False, dt, top_act, norm_block, norm_eps, tower_heads=towers)
         self.top_act, self.norm_block = top_act, norm_block
         self._stack = stack_layers(stack) if stack else None
         rank = fm_W.shape[1] if fm_W is not None else (stack[0]["W"].shape[1] if stack else 0)

@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblattice.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["sort.hip", "embbag.hip", "gemm.hip", "interact.hip", "fm_mfma.hip", "dot_mfma.hip", "stack.hip", "loss.hip", "head.hip", "fp8.hip", "swishrn.hip", "abi.hip"]
+SOURCES = ["sort.hip", "embbag.hip", "gemm.hip", "interact.hip", "fm_mfma.hip", "dot_mfma.hip", "stack.hip", "loss.hip", "head.hip", "fp8.hip", "swishrn.hip", "towers.hip", "abi.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # keep the compiler from emitting packed fp32 arithmetic
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -93,10 +93,20 @@ static bool swish_layer(const lattice_mlp_desc* d, int i) {
   return d->act != LATTICE_ACT_RELU && (i < d->n_layers - 1 || d->relu_last);
 }
 
+// layer i is the heads of per-objective towers (W [T, H], H = in / T)
+static bool tower_layer(const lattice_mlp_desc* d, int i) {
+  return d->tower_heads && i == d->n_layers - 1;
+}
+
+static int64_t w_elems(const lattice_mlp_desc* d, int i) {
+  const lattice_linear& L = d->layers[i];
+  return tower_layer(d, i) ? (int64_t)L.in_dim : (int64_t)L.out_dim * L.in_dim;
+}
+
 static hipError_t zero_mlp_grads(const lattice_mlp_desc* d, hipStream_t s) {
   for (int i = 0; i < d->n_layers; ++i) {
     const lattice_linear& L = d->layers[i];
-    hipError_t e = zero_f32(L.dW, (int64_t)L.out_dim * L.in_dim, s);
+    hipError_t e = zero_f32(L.dW, w_elems(d, i), s);
     if (e == hipSuccess) e = zero_f32(L.db, L.out_dim, s);
     if (e == hipSuccess && swish_layer(d, i)) e = zero_f32(L.dgain, 2 * (int64_t)L.out_dim, s);
     if (e != hipSuccess) return e;
@@ -539,6 +549,12 @@ static lattice_status check_mlp(const lattice_mlp_desc* d, int32_t B) {
     if (i > 0) REQUIRE(L.in_dim == d->layers[i - 1].out_dim, "layer %d: in_dim mismatch", i);
     if (swish_layer(d, i)) REQUIRE(L.gain, "layer %d: SwishRN needs gains", i);
   }
+  if (d->tower_heads) {
+    const lattice_linear& L = d->layers[d->n_layers - 1];
+    REQUIRE(!d->relu_last, "tower heads need a linear last layer");
+    REQUIRE(L.in_dim % L.out_dim == 0 && (L.in_dim / L.out_dim) % 8 == 0,
+            "tower heads: in_dim must be out_dim x H with H a multiple of 8");
+  }
   return LATTICE_OK;
 }
 
@@ -571,6 +587,7 @@ static size_t mlp_bwd_ws(const lattice_mlp_desc* d, int B) {
     s = std::max(s, gemm_workspace(g));
     s = std::max(s, colsum_workspace(B, L.out_dim));
     if (swish_layer(d, i)) s = std::max(s, swishrn_gain_workspace(B, L.out_dim));
+    if (tower_layer(d, i)) s = std::max(s, tower_wgrad_workspace(B, L.out_dim, L.in_dim / L.out_dim));
   }
   return al256(s);
 }
@@ -601,6 +618,16 @@ static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, 
     g.c_dt = (last && !d->relu_last) ? DT_F32 : dt;
     g.M = B; g.N = L.out_dim; g.K = L.in_dim;
     g.bias = L.b;
+    if (tower_layer(d, i)) {
+      if (strides[i] != L.out_dim) {
+        set_error("tower heads write contiguous logits");
+        return hipErrorInvalidValue;
+      }
+      hipError_t e = tower_head_fwd(dt, g.A, g.lda, B, L.out_dim, L.in_dim / L.out_dim, L.W, L.b,
+                                    (float*)acts[i], s);
+      if (e != hipSuccess) return e;
+      continue;
+    }
     if (swish_layer(d, i)) {
       if (dt == DT_BF16 && d->norm_block == LATTICE_BLOCKNORM_COLS) {
         g.norm_gate = gate_of(d);
@@ -679,6 +706,11 @@ static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const
                                   hipStream_t s) {
   const lattice_linear& L = d->layers[i];
   const DType dt = dt_of(d->dtype);
+  if (tower_layer(d, i)) {
+    hipError_t e = tower_wgrad(dt, g, gs, in_i, ld_in, B, L.out_dim, L.in_dim / L.out_dim, L.dW, ws, s);
+    if (e == hipSuccess && L.db) e = colsum(g, dt, gs, B, L.out_dim, L.db, ws, s);
+    return e;
+  }
   bool db_done = false;
   if (L.dW) {
     GemmArgs w;
@@ -745,6 +777,18 @@ static hipError_t swish_gain_grad(const lattice_mlp_desc* d, int j, int B, const
 static hipError_t mlp_chain_step(const lattice_mlp_desc* d, int i, int B, const void* g, int64_t gs,
                                  const void* const* acts, const int64_t* strides, const ActBufs* ab,
                                  void* dst, int64_t dst_ld, void* ws, hipStream_t s) {
+  if (tower_layer(d, i)) {
+    const lattice_linear& L = d->layers[i];
+    const DType dt = dt_of(d->dtype);
+    const int T = L.out_dim, H = L.in_dim / L.out_dim;
+    if (i > 0 && swish_layer(d, i - 1)) {
+      hipError_t e = tower_head_dgrad(dt, g, gs, B, T, H, L.W, nullptr, 0, ab->gout[i - 1], L.in_dim, s);
+      if (e != hipSuccess) return e;
+      return swish_back(d, i - 1, B, ab->gout[i - 1], L.in_dim, ab, dst, dst_ld, s);
+    }
+    return tower_head_dgrad(dt, g, gs, B, T, H, L.W, i > 0 ? acts[i - 1] : nullptr,
+                            i > 0 ? strides[i - 1] : 0, dst, dst_ld, s);
+  }
   if (i > 0 && swish_layer(d, i - 1)) {
     const int64_t ldo = d->layers[i - 1].out_dim;
     hipError_t e = mlp_layer_dgrad(d, i, B, g, gs, ab->gout[i - 1], ldo, nullptr, 0, ws, s);
@@ -1262,7 +1306,8 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   const lattice_linear& head = m->top.layers[nt - 1];
   const void* head_in = nt > 1 ? tacts[nt - 2] : t;
   const int64_t head_ld = nt > 1 ? tstr[nt - 2] : P.t_stride;
-  const bool fused_heads = dt == DT_BF16 && head_fusable(T, head.in_dim, head_in, head_ld, head.W);
+  const bool fused_heads = dt == DT_BF16 && !m->top.tower_heads &&
+                           head_fusable(T, head.in_dim, head_in, head_ld, head.W);
   lattice_mlp_desc hidden = m->top;  // the layers before the heads
   hidden.n_layers = nt - 1;
   hidden.relu_last = 1;

@@ -97,6 +97,16 @@ hipError_t swishrn_gain_grad(DType dt, const void* go, int64_t ldg, const void* 
                              const float* rinv, int M, int N, int block, int gate,
                              const float* gain, float* dgain, void* ws, hipStream_t s);
 
+// towers.hip (heads of per-objective towers: objective t reads only units
+// t*H .. t*H+H-1 of its input; w [T, H]; H % 8 == 0)
+hipError_t tower_head_fwd(DType dt, const void* h, int64_t ldh, int B, int NT, int H, const void* w,
+                          const float* bias, float* z, hipStream_t s);
+hipError_t tower_head_dgrad(DType dt, const void* g, int64_t ldg, int B, int NT, int H, const void* w,
+                            const void* mask, int64_t ldm, void* dh, int64_t ldd, hipStream_t s);
+size_t tower_wgrad_workspace(int B, int NT, int H);
+hipError_t tower_wgrad(DType dt, const void* g, int64_t ldg, const void* h, int64_t ldh, int B, int NT,
+                       int H, float* dw, void* ws, hipStream_t s);
+
 // interact.hip
 size_t dot_lds_bytes(int n, int d);
 size_t fm_lds_bytes(int n, int d, int k);

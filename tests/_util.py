@@ -191,11 +191,24 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
     g_top = [_np64(g) for g in v["top_grad"]]
     act = ostep.top_act(cfg, params)
     # top MLP forward, layer by layer from the stored inputs
+    towers = bool(getattr(cfg, "towers", 0))
+    # the heads' products: dense, or the towers' grouped heads (objective t
+    # reads only its tower's units)
+    def heads_fwd(h, W, b):
+        return omlp.grouped_linear(h, W, b) if towers else h @ W.T + b
+
+    def heads_dgrad(g, W):
+        return omlp.grouped_linear_grads(g, np.zeros((g.shape[0], W.size)), W)[2] if towers else g @ W
+
+    def heads_wgrad(g, h, W):
+        return omlp.grouped_linear_grads(g, h, W)[0] if towers else g.T @ h
+
     for i, (W, b) in enumerate(params["top"]):
         W, b = np.asarray(W, np.float64), np.asarray(b, np.float64)
         h = h_top[i][R]
-        a = h @ W.T + b
-        ab = np.abs(h) @ np.abs(W).T + np.abs(b)
+        last = i == L - 1
+        a = heads_fwd(h, W, b) if last else h @ W.T + b
+        ab = heads_fwd(np.abs(h), np.abs(W), np.abs(b)) if last else np.abs(h) @ np.abs(W).T + np.abs(b)
         if i < L - 1 and act is not None:
             check_swishrn_forward(f"top{i}", cfg, act, i, h, W, b, _np64(v["top_pre"][i])[R],
                                   _np64(v["top_rinv"][i])[R], h_top[i + 1][R], us, t)
@@ -218,21 +231,31 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
     # SwishRN backward)
     for i in range(L - 1, -1, -1):
         W = np.asarray(params["top"][i][0], np.float64)
-        prod = g_top[i][R] @ W
-        ab = np.abs(g_top[i][R]) @ np.abs(W)
+        if i == L - 1:
+            prod, ab = heads_dgrad(g_top[i][R], W), heads_dgrad(np.abs(g_top[i][R]), np.abs(W))
+            Kc = 1 if towers else W.shape[0]
+        else:
+            prod, ab, Kc = g_top[i][R] @ W, np.abs(g_top[i][R]) @ np.abs(W), W.shape[0]
         if i > 0 and act is not None:
             gout = _np64(v["top_gout"][i - 1])[R]
-            assert_product(f"top{i} output grad", gout, prod, ab, W.shape[0], us, t)
+            assert_product(f"top{i} output grad", gout, prod, ab, Kc, us, t)
             check_swishrn_backward(f"top{i - 1}", act, i - 1, gout, _np64(v["top_pre"][i - 1])[R],
                                    _np64(v["top_rinv"][i - 1])[R], g_top[i - 1][R], us, t)
         elif i > 0:
             on = h_top[i][R] > 0
-            assert_product(f"top{i} grad chain", g_top[i - 1][R], prod * on, ab * on, W.shape[0], us, t)
+            assert_product(f"top{i} grad chain", g_top[i - 1][R], prod * on, ab * on, Kc, us, t)
         else:
-            assert_product("d_t", tin_grad(v, cfg)[R], prod, ab, W.shape[0], us, t)
+            assert_product("d_t", tin_grad(v, cfg)[R], prod, ab, Kc, us, t)
     # weight and bias gradients from the stored chain and activations
     for i in range(L):
         r = wr.get(("top", i), slice(None))
+        if i == L - 1 and towers:
+            Wl = np.asarray(params["top"][i][0], np.float64)
+            gi, hi = g_top[i], h_top[i]
+            assert_product(f"top{i}.dW (towers)", _np64(grads["top_dW"][i]), heads_wgrad(gi, hi, Wl),
+                           heads_wgrad(np.abs(gi), np.abs(hi), Wl), B, None, t)
+            assert_product(f"top{i}.db", _np64(grads["top_db"][i]), gi.sum(0), np.abs(gi).sum(0), B, None, t)
+            continue
         gi, hi = g_top[i][:, r], h_top[i]
         assert_product(f"top{i}.dW", _np64(grads["top_dW"][i])[r], gi.T @ hi, np.abs(gi).T @ np.abs(hi),
                        B, None, t)
@@ -446,7 +469,8 @@ class Workload:
                              dense_in=c.dense_in, bottom=self.bottom, top=self.top,
                              interact=c.interact, fm_W=self.fm_W, fm_dW=self.fm_dW, pool=c.pool,
                              stack=self.stack, stack_n=c.stack_n, ln_eps=c.ln_eps,
-                             top_act=c.top_act, norm_block=c.norm_block, norm_eps=c.norm_eps)
+                             top_act=c.top_act, norm_block=c.norm_block, norm_eps=c.norm_eps,
+                             towers=bool(c.towers))
 
 
 def relu_overrides(cfg, params, table, batch, gpu_in, gpu_out, max_iter=4):

@@ -184,10 +184,39 @@ def test_step_swishrn_top(name):
     gain gradients within their derived bounds), then the composed step
     against the oracle's SwishRN step (fp32: element-wise at 1e-5; bf16:
     normwise at 2e-2)."""
-    from oracle.metrics import max_rel_err, max_rel_err_normwise
     cfg = SWISH_CASES[name]
-    lr = 0.01
     print(f"[step-swishrn] {name} B={cfg.B} top={cfg.top} {cfg.top_act} block={cfg.norm_block}", flush=True)
+    check_step_staged(cfg)
+
+
+TOWER_CASES = {
+    # 8 objectives x 32 units per tower after the shared 512-wide layer
+    "mid-small-towers": synth.small(synth.MID, B=256, rows=3000, top=(512, 8 * 32, 8), towers=32),
+    # SwishRN tower layer: its BlockNorm groups of 128 span 8 towers of 16 units
+    "large-fm-small-towers-swishrn": synth.small(synth.LARGE_FM, B=160, rows=6000, top=(1024, 16 * 16, 16),
+                                                 towers=16, top_act="swishrn"),
+    "tiny-f32-towers": synth.TINY.scaled(top=(64, 4 * 8, 4), towers=8),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(TOWER_CASES))
+def test_step_towers(name):
+    """Per-objective towers (Section 3.3.3): the grouped heads on their own
+    stored inputs (forward, input gradient, weight gradient), every other
+    stage likewise, then the composed step against the oracle's."""
+    cfg = TOWER_CASES[name]
+    print(f"[step-towers] {name} B={cfg.B} top={cfg.top} towers={cfg.towers} {cfg.top_act}", flush=True)
+    check_step_staged(cfg)
+
+
+def check_step_staged(cfg, lr=0.01):
+    """Stage-wise parity of a whole step (check_stages, check_sparse_stage)
+    and the composed step against the oracle: fp32 element-wise at 1e-5
+    (dX_emb with its inputs' propagated deviation), bf16 normwise at 2e-2
+    (hard-gate kinks the GPU takes the other way within their band adopted
+    first)."""
+    from oracle.metrics import max_rel_err, max_rel_err_normwise
     w = Workload(cfg)
     E0 = w.table_np()
     _, v, _ = run_step(w, lr)
@@ -204,9 +233,8 @@ def test_step_swishrn_top(name):
              ("d_t", v["d_t"][:, :cfg.top_in], g["d_top_in"])]
     for i in range(len(w.top)):
         pairs += [(f"top{i}.dW", w.top[i]["dW"], g["top_dW"][i]), (f"top{i}.db", w.top[i]["db"], g["top_db"][i])]
-    for i in range(len(w.top) - 1):
-        dga, dgb = g["top_dgain"][i]
-        pairs.append((f"top{i}.dgain", w.top[i]["dgain"], np.stack([dga, dgb])))
+    for i, dg in enumerate(g.get("top_dgain", [])):
+        pairs.append((f"top{i}.dgain", w.top[i]["dgain"], np.stack(dg)))
     for nm, got, ref in pairs:
         got = got.float().cpu().numpy()
         e = max_rel_err(got, ref) if t <= 1e-5 else max_rel_err_normwise(got, ref)
