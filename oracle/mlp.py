@@ -34,6 +34,29 @@ def linear_grads(g, h, W):
     return g.T @ h, g.sum(axis=0), g @ np.asarray(W, np.float64)
 
 
+def untied_linear(h, W, b, domain):
+    """Parameter untying (Section 3.3.4): W ``[D, out, in]``, b ``[D, out]``;
+    sample r uses set ``domain[r]``."""
+    h = np.asarray(h, np.float64)
+    a = np.empty((h.shape[0], np.shape(W)[1]))
+    for g in range(np.shape(W)[0]):
+        r = np.asarray(domain) == g
+        a[r] = linear(h[r], W[g], b[g])
+    return a
+
+
+def untied_linear_grads(g, h, W, domain):
+    """(dW [D, out, in], db [D, out], dh) of ``untied_linear``: each set's
+    gradients sum over its own samples only."""
+    g, h, W = (np.asarray(x, np.float64) for x in (g, h, W))
+    dW, db = np.zeros(W.shape), np.zeros(W.shape[:2])
+    dh = np.zeros(h.shape)
+    for k in range(W.shape[0]):
+        r = np.asarray(domain) == k
+        dW[k], db[k], dh[r] = linear_grads(g[r], h[r], W[k])
+    return dW, db, dh
+
+
 def grouped_linear(h, W, b):
     """Per-objective towers' heads (Section 3.3.3): W is ``[T, H]`` and output
     t reads only its tower's inputs ``h[:, t*H:(t+1)*H]``:
@@ -71,7 +94,23 @@ def linear_fp8(h, W, b):
     return _fp8.linear_fp8(qa, sa, qw, sw, b)
 
 
-def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=None, grouped_last=False):
+def _swish_fwd(a, act, i, domain):
+    """SwishRN of layer i's pre-activation, per domain when its gains are
+    untied ([D, out])."""
+    ga, gb = act["gains"][i]
+    if np.ndim(ga) == 1:
+        out, _, rho = _swishrn.forward(a, ga, gb, act["block"], act["eps"], act["kind"])
+        return out, rho
+    out = np.empty_like(a)
+    rho = np.empty((a.shape[0], len(_swishrn.groups(a.shape[1], act["block"]))))
+    for k in range(ga.shape[0]):
+        r = np.asarray(domain) == k
+        out[r], _, rho[r] = _swishrn.forward(a[r], ga[k], gb[k], act["block"], act["eps"], act["kind"])
+    return out, rho
+
+
+def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=None, grouped_last=False,
+                domain=None):
     """Returns ``(hs, masks)``: the layer inputs/outputs ``[h0, h1, ..., hL]``
     and, per layer, its ReLU decision (``None`` for a linear last layer).
     Every layer but (optionally) the last applies ReLU and storage rounding.
@@ -88,18 +127,21 @@ def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=N
     BlockNorm groups of b features), ``eps`` and ``gains`` (per layer
     ``(ga, gb)``).  Their entry in the returned list is then a dict
     ``{"pre": a, "rho": ...}`` instead of a ReLU mask.  ``grouped_last``:
-    the last (linear) layer is the towers' heads (``grouped_linear``)."""
+    the last (linear) layer is the towers' heads (``grouped_linear``).
+    Layers whose W is ``[D, out, in]`` are untied (``untied_linear``, and
+    their SwishRN gains ``[D, out]``) over the per-sample ``domain``."""
     hs = [np.asarray(h0, np.float64)]
     masks = []
     for i, (W, b) in enumerate(layers):
         last = i == len(layers) - 1
         if grouped_last and last:
             a = grouped_linear(hs[-1], W, b)
+        elif np.ndim(W) == 3:
+            a = untied_linear(hs[-1], W, b, domain)
         else:
             a = linear_fp8(hs[-1], W, b) if i in fp8_layers else linear(hs[-1], W, b)
         if act is not None and (relu_last or not last):
-            ga, gb = act["gains"][i]
-            out, _, rho = _swishrn.forward(a, ga, gb, act["block"], act["eps"], act["kind"])
+            out, rho = _swish_fwd(a, act, i, domain)
             hs.append(rnd(out))
             masks.append({"pre": a, "rho": rho})
         elif relu_last or not last:
@@ -116,7 +158,7 @@ def mlp_forward(h0, layers, rnd, relu_last, overrides=None, fp8_layers=(), act=N
 
 
 def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=None, dgains=None,
-                 grouped_last=False):
+                 grouped_last=False, domain=None):
     """Backward through ``mlp_forward``.  ``g_out`` is dL/d(hs[-1]) (before the
     last ReLU mask when ``relu_last``).  Returns (dWs, dbs, dL/dh0 or None).
     With ``act`` (as in ``mlp_forward``) the gain gradients of the SwishRN
@@ -130,8 +172,17 @@ def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=
             return rnd(g * masks[i])
         ga, gb = act["gains"][i]
         go = rnd(g)
-        dh, dga, dgb = _swishrn.backward(go, masks[i]["pre"], ga, gb, act["block"], act["eps"], act["kind"],
-                                         grad_override=(act.get("overrides") or {}).get(i))
+        ov = (act.get("overrides") or {}).get(i)
+        if np.ndim(ga) == 1:
+            dh, dga, dgb = _swishrn.backward(go, masks[i]["pre"], ga, gb, act["block"], act["eps"], act["kind"],
+                                             grad_override=ov)
+        else:                                   # untied gains: each domain's rows
+            dh, dga, dgb = np.empty_like(go), np.zeros(ga.shape), np.zeros(gb.shape)
+            for k in range(ga.shape[0]):
+                r = np.asarray(domain) == k
+                ovk = None if ov is None else (ov[0][r], ov[1][r])
+                dh[r], dga[k], dgb[k] = _swishrn.backward(go[r], masks[i]["pre"][r], ga[k], gb[k], act["block"],
+                                                          act["eps"], act["kind"], grad_override=ovk)
         if dgains is not None:
             dgains[i] = (dga, dgb)
         return rnd(dh)
@@ -143,8 +194,12 @@ def mlp_backward(g_out, hs, masks, layers, rnd, relu_last, need_input_grad, act=
     dh0 = None
     for i in range(L - 1, -1, -1):
         W, _ = layers[i]
-        grads = grouped_linear_grads if grouped_last and i == L - 1 else linear_grads
-        dW, db, dh = grads(g, hs[i], W)
+        if grouped_last and i == L - 1:
+            dW, db, dh = grouped_linear_grads(g, hs[i], W)
+        elif np.ndim(W) == 3:
+            dW, db, dh = untied_linear_grads(g, hs[i], W, domain)
+        else:
+            dW, db, dh = linear_grads(g, hs[i], W)
         dWs[i], dbs[i] = dW, db
         if i > 0:
             g = through(i - 1, dh)

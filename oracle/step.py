@@ -12,7 +12,9 @@ Forward (per sample b; Section 3.3):
      flattened STACK output;
   5. top MLP, ReLU (or SwishRN, Section 3.3.4) on hidden layers, one logit
      per objective (Section 3.3.3; with towers the last hidden layer holds
-     one group of units per objective and each logit reads only its group);
+     one group of units per objective and each logit reads only its group;
+     untied layers use the parameter set of the sample's domain, Section
+     3.3.4);
   6. masked BCE (Section 3.2.1).
 Backward: the exact chain rule through 1-6, with GEMM operands (activation
 gradients) rounded to the storage precision where the accelerator stores them:
@@ -86,7 +88,8 @@ def forward(cfg, params, table, batch, overrides=None, loss_normalizer=None, fp8
     hs_top, mt = mlp_forward(t, params["top"], rnd, relu_last=False,
                          overrides=(overrides or {}).get("top"),
                          fp8_layers=tuple(range(len(params["top"]) - 1)) if fp8_top else (),
-                         act=top_act(cfg, params), grouped_last=bool(getattr(cfg, "towers", 0)))
+                         act=top_act(cfg, params), grouped_last=bool(getattr(cfg, "towers", 0)),
+                         domain=batch.get("domain"))
     c["hs_top"], c["masks_top"] = hs_top, mt
     c["gate_overrides"] = (overrides or {}).get("top_gate")
     z = hs_top[-1]
@@ -108,7 +111,7 @@ def backward(cfg, params, table, batch, c, lr_tables=None):
     dgains = [None] * (len(params["top"]) - 1)
     dWt, dbt, dt = mlp_backward(gz, c["hs_top"], c["masks_top"], params["top"], rnd, relu_last=False,
                                 need_input_grad=True, act=act, dgains=dgains,
-                                grouped_last=bool(getattr(cfg, "towers", 0)))
+                                grouped_last=bool(getattr(cfg, "towers", 0)), domain=batch.get("domain"))
     g["top_dW"], g["top_db"] = dWt, dbt
     if act is not None:
         g["top_dgain"] = dgains

@@ -46,6 +46,9 @@ class Config:
     ln_eps: float = 1e-5
     towers: int = 0                          # per-objective towers: hidden units per tower (0: none);
                                              # the last top layer then reads only its tower's units
+    untie: int = 0                           # parameter untying: leading top layers with one
+                                             # parameter set per domain (batches then arrive
+                                             # grouped by domain)
     top_act: str = "relu"                    # hidden top layers: "relu" | "swishrn" | "hardswishrn"
     norm_block: int = 128                    # SwishRN groups: 128 (BlockNorm) or 0 (the whole row)
     norm_eps: float = 1e-6

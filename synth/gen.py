@@ -44,7 +44,7 @@ from .configs import Config
 # stream ids (arbitrary, fixed)
 _S_BAGLEN, _S_INDEX, _S_DENSE, _S_LABEL_P, _S_LABEL, _S_MASK = 1, 2, 3, 4, 5, 6
 _S_DOMAIN, _S_PERM = 7, 8
-_S_BOTTOM, _S_TOP, _S_FM, _S_STACK, _S_TABLE, _S_GAIN, _S_TOWER = 20, 21, 22, 23, 24, 25, 26
+_S_BOTTOM, _S_TOP, _S_FM, _S_STACK, _S_TABLE, _S_GAIN, _S_TOWER, _S_UNTIE = 20, 21, 22, 23, 24, 25, 26, 27
 _S_AUX = 40
 
 
@@ -130,7 +130,9 @@ def make_batch(cfg: Config, batch_id: int = 0) -> Dict[str, np.ndarray]:
         props, feats, heads = _domain_plan(cfg)
         counts = domain_counts(B, props)
         dom = np.concatenate([np.full(c, i, dtype=np.uint8) for i, c in enumerate(counts)])
-        _rng(seed, _S_DOMAIN, 1000 + batch_id).shuffle(dom)
+        if not cfg.untie:
+            _rng(seed, _S_DOMAIN, 1000 + batch_id).shuffle(dom)
+        # (untied parameters: samples grouped by domain, in domain order)
         domain = dom
         active[:] = False
         mask[:] = 0
@@ -185,8 +187,10 @@ def make_batch(cfg: Config, batch_id: int = 0) -> Dict[str, np.ndarray]:
         p = _rng(seed, _S_LABEL_P, 0).uniform(cfg.label_p[1], cfg.label_p[2], size=cfg.T)
     labels = (_rng(seed, _S_LABEL, batch_id).random((B, cfg.T)) < p).astype(np.float32)
 
+    n_dom = len(cfg.domains[0]) if cfg.domains else 1
+    domain_offsets = np.concatenate([[0], np.cumsum(np.bincount(domain, minlength=n_dom))]).astype(np.int64)
     return dict(offsets=offsets.astype(np.int32), indices=indices, lengths=lens,
-                dense=dense, labels=labels, mask=mask, domain=domain,
+                dense=dense, labels=labels, mask=mask, domain=domain, domain_offsets=domain_offsets,
                 row_base=np.arange(F + 1, dtype=np.int64) * N)
 
 
@@ -233,6 +237,19 @@ def make_dense_params(cfg: Config) -> Dict[str, object]:
         r = _rng(cfg.seed, _S_GAIN)
         out["top_gain"] = [(f32(1.0 + 0.2 * r.standard_normal(o)), f32(1.0 + 0.2 * r.standard_normal(o)))
                            for o in cfg.top[:-1]]
+    if cfg.untie:
+        # one parameter set per domain for the first `untie` top layers (and
+        # their SwishRN gains): W [D, out, in], b [D, out]
+        D = len(cfg.domains[0])
+        assert cfg.untie <= len(cfg.top) - 1, "untied layers are hidden layers"
+        r = _rng(cfg.seed, _S_UNTIE)
+        for i in range(cfg.untie):
+            o, n = cfg.top[i], tdims[i]
+            out["top"][i] = (w(np.stack([_glorot(r, o, n) for _ in range(D)])),
+                             f32(r.standard_normal((D, o)) * 0.01))
+            if "top_gain" in out:
+                out["top_gain"][i] = (f32(1.0 + 0.2 * r.standard_normal((D, o))),
+                                      f32(1.0 + 0.2 * r.standard_normal((D, o))))
     n = cfg.n_slots
     if cfg.interact == "fm":
         out["fm_W"] = w(_rng(cfg.seed, _S_FM).standard_normal((n, cfg.fm_rank)) / math.sqrt(n))

@@ -24,6 +24,11 @@ def _tiny_cfg(kind, pool="sum"):
     if kind == "stack":
         return synth.Config(name="t-stack", F=5, dense_in=0, bottom=(), interact="stack",
                             fm_rank=2, stack_layers=2, stack_n=3, top=(4, 2), **base)
+    if kind == "untied":
+        # two domains (seeded sizes), the first two top layers untied, SwishRN
+        return synth.Config(name="t-untied", F=4, dense_in=3, bottom=(6, 4), interact="dot",
+                            top=(5, 6, 3), untie=2, top_act="swishrn", norm_block=2, norm_eps=1e-3,
+                            domains=((0.6, 0.4), 3, 2), **dict(base, mask=("domain",)))
     if kind == "towers":
         # per-objective towers: 3 objectives x 2 hidden units, then grouped heads
         return synth.Config(name="t-towers", F=3, dense_in=3, bottom=(6, 4), interact="dot",
@@ -103,9 +108,10 @@ def _check_kinks(cfg, params, table, batch):
         for i, (W, b) in enumerate(layers):
             if top and i == len(layers) - 1:
                 continue                                   # the heads are linear
-            a = hs[i] @ W.T + b
+            a = mlp.untied_linear(hs[i], W, b, batch["domain"]) if np.ndim(W) == 3 else hs[i] @ W.T + b
             if top and act is not None and i < len(layers) - 1:
                 if act["kind"] == "hard":
+                    assert np.ndim(act["gains"][i][0]) == 1, "hard-gate kink check: tied gains only"
                     _, n, _ = swishrn.forward(a, *act["gains"][i], act["block"], act["eps"], "hard")
                     z = act["gains"][i][1] * n
                     assert np.min(np.abs(np.abs(z) - 3.0)) > 1e-4, "seed puts a gate input on a kink"
@@ -153,7 +159,7 @@ def _fd_worst(kind, pool="sum", n_coords=12):
 
 
 @pytest.mark.parametrize("kind,pool", [("dot", "sum"), ("dot", "mean"), ("fm", "sum"), ("stack", "sum"),
-                                       ("dwfb", "sum"), ("towers", "sum"), ("swishrn", "sum"),
+                                       ("dwfb", "sum"), ("towers", "sum"), ("untied", "sum"), ("swishrn", "sum"),
                                        ("hardswishrn", "sum")])
 def test_finite_differences(kind, pool):
     assert _fd_worst(kind, pool) < 1e-6
@@ -188,6 +194,11 @@ def _grouped_grads_wrong_tower(g, h, W):
     return dW, db, dh.reshape(-1, T, H)[:, ::-1].reshape(-1, T * H)      # gradient sent to the wrong tower
 
 
+def _untied_grads_swapped_sets(g, h, W, domain):
+    dW, db, dh = _ORIG["untied_linear_grads"](g, h, W, domain)
+    return dW[::-1].copy(), db[::-1].copy(), dh                      # each domain's gradient to the other set
+
+
 def _swishrn_backward_no_mean_term(do, h, ga, gb, block, eps, kind, rho=None, grad_override=None):
     do = np.asarray(do, np.float64)
     _, n, rho = swishrn.forward(h, ga, gb, block, eps, kind, rho)
@@ -218,7 +229,8 @@ def _dot_backward_no_slot0(dp, X):
 
 
 _ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward,
-             swishrn_backward=swishrn.backward, grouped_linear_grads=mlp.grouped_linear_grads)
+             swishrn_backward=swishrn.backward, grouped_linear_grads=mlp.grouped_linear_grads,
+             untied_linear_grads=mlp.untied_linear_grads)
 
 
 @pytest.mark.parametrize("target,module,name,kind", [
@@ -230,8 +242,9 @@ _ORIG = dict(mlp_backward=step.mlp_backward, dot_backward=step.dot_backward,
     (_swishrn_backward_whole_row_mean, swishrn, "backward", "hardswishrn"),
     (_swishrn_backward_gate_gain_swapped, swishrn, "backward", "swishrn"),
     (_grouped_grads_wrong_tower, mlp, "grouped_linear_grads", "towers"),
+    (_untied_grads_swapped_sets, mlp, "untied_linear_grads", "untied"),
 ], ids=["fm-sign", "layernorm-term", "relu-mask", "slot0-gradient", "swishrn-mean-term",
-        "blocknorm-group", "swishrn-gains", "tower-routing"])
+        "blocknorm-group", "swishrn-gains", "tower-routing", "untied-sets"])
 def test_planted_backward_mistakes_fail_the_finite_difference_pin(monkeypatch, target, module, name, kind):
     monkeypatch.setattr(module, name, target)
     assert _fd_worst(kind, n_coords=6) > 1e-3
