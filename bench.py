@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--towers", type=int, default=0,
                     help="per-objective towers: the last hidden top layer becomes T towers of this many "
                          "units each (replacing its width) and every head reads only its tower")
+    ap.add_argument("--untie", type=int, default=0,
+                    help="multi-domain workloads: the first N top layers hold one parameter set per "
+                         "domain (parameter untying; batches grouped by domain)")
     ap.add_argument("--lcb-n", type=int, default=0,
                     help="stacked workloads: output vectors of each fusion block's linear compression "
                          "block (full DHEN/Wukong fusion blocks; 0: FM block only)")
@@ -91,6 +94,11 @@ def main():
             sys.exit(2)
         T = cfg.top[-1]
         cfg = cfg.scaled(top=tuple(cfg.top[:-2]) + (T * args.towers, T), towers=args.towers)
+    if args.untie:
+        if not cfg.domains or args.fp8:
+            print("--untie needs a multi-domain workload and tied FP8 layers", file=sys.stderr)
+            sys.exit(2)
+        cfg = cfg.scaled(untie=args.untie)
     if args.lcb_n:
         if cfg.interact != "stack":
             print("--lcb-n needs a stacked workload", file=sys.stderr)
@@ -113,7 +121,8 @@ def main():
             indices=torch.from_numpy(b["indices"]).to(dev),
             dense=torch.from_numpy(b["dense"]).to(sdt).to(dev),
             labels=torch.from_numpy(b["labels"]).to(dev), mask=torch.from_numpy(b["mask"]).to(dev),
-            nnz=int(b["offsets"][-1]), U=distinct_rows(b, cfg)))
+            nnz=int(b["offsets"][-1]), U=distinct_rows(b, cfg),
+            domain_offsets=b["domain_offsets"] if cfg.untie else None))
     row_base = torch.from_numpy(batches[0]["np"]["row_base"]).to(dev)
     log(f"[bench] batches ready ({time.time() - t0:.1f}s); generating tables")
     E = synth.make_tables(cfg, device=dev)
@@ -126,7 +135,7 @@ def main():
     bottom = [lin(W, b) for W, b in p["bottom"]]
     top = [lin(W, b) for W, b in p["top"]]
     for L, (ga, gb) in zip(top, p.get("top_gain", [])):
-        L["gain"] = torch.from_numpy(np.stack([ga, gb])).to(dev)
+        L["gain"] = torch.from_numpy(np.stack([ga, gb], axis=-2)).to(dev)
         L["dgain"] = torch.empty(tuple(L["gain"].shape), device=dev)
     fm_W = torch.from_numpy(p["fm_W"]).to(sdt).to(dev) if "fm_W" in p else None
     fm_dW = torch.empty(tuple(fm_W.shape), device=dev) if fm_W is not None else None
@@ -147,7 +156,8 @@ def main():
                           bottom=bottom, top=top, interact=cfg.interact, fm_W=fm_W, fm_dW=fm_dW,
                           pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps,
                           top_act=cfg.top_act, norm_block=cfg.norm_block, norm_eps=cfg.norm_eps,
-                          towers=bool(cfg.towers))
+                          towers=bool(cfg.towers), n_domains=len(cfg.domains[0]) if cfg.untie else 0,
+                          untied_layers=cfg.untie)
     nnz_max = max(b["nnz"] for b in batches)
     lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False, fp8_top=args.fp8)
     ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
@@ -160,7 +170,8 @@ def main():
         b = batches[i % len(batches)]
         api.lattice_step(model, b["offsets"], b["indices"], b["dense"], b["labels"], b["mask"], ws,
                          cfg.lr_tables, False, stage_events=events, nnz_capacity=nnz_max,
-                         side=None if one_stream else side, fp8_top=args.fp8)
+                         side=None if one_stream else side, fp8_top=args.fp8,
+                         domain_offsets=b["domain_offsets"])
 
     for i in range(args.warmup):
         step(i)
@@ -314,6 +325,7 @@ def main():
                    "top_act": cfg.top_act,
                    "lcb_n": cfg.lcb_n if cfg.interact == "stack" else None,
                    "towers": cfg.towers or None,
+                   "untied_top_layers": cfg.untie or None,
                    "norm_block": cfg.norm_block if cfg.top_act != "relu" else None,
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,

@@ -284,6 +284,18 @@ typedef struct {
                                        and output t reads only group t: its W and dW are
                                        [T, H] (not [T, in_dim]); H % 8 == 0, the logits
                                        contiguous.  0: a dense last layer. */
+  int32_t n_domains;                /* parameter untying (Section 3.3.4): >= 2 gives each of
+                                       the first untied_layers layers one parameter set per
+                                       domain, stacked: W [n_domains, out, in], b, gain and
+                                       their gradients likewise; the samples of domain g use
+                                       set g.  0 or 1: every layer tied. */
+  int32_t untied_layers;            /* layers 0 .. untied_layers-1 are untied (not the
+                                       towers' heads) */
+  const int64_t* domain_offsets;    /* lattice_mlp_heads_fwd/bwd with untied layers: host
+                                       [n_domains + 1], samples grouped by domain, domain g
+                                       = rows off[g] .. off[g+1]-1 (off[0] = 0, non-
+                                       decreasing, off[n_domains] = B).  lattice_step uses
+                                       the batch's offsets instead. */
 } lattice_mlp_desc;
 
 /* Masked multi-objective BCE with logits z [B, T]: with N = max(1, sum m),
@@ -383,10 +395,11 @@ typedef struct {
   lattice_tables tables;
   int32_t num_features;        /* F */
   int32_t dense_in;            /* dense inputs (0: no dense path, no bottom MLP) */
-  lattice_mlp_desc bottom;     /* relu_last = 1, ReLU, output width = dim */
+  lattice_mlp_desc bottom;     /* relu_last = 1, ReLU, tied, output width = dim */
   lattice_interact_desc interact;  /* n = F + (dense_in > 0); emit_slot0 = dense_in > 0 (DOT/FM) */
   lattice_mlp_desc top;        /* relu_last = 0, output width = T; hidden layers ReLU
-                                  or SwishRN (act) */
+                                  or SwishRN (act), tied or untied per domain; dense or
+                                  tower heads */
 } lattice_model_desc;
 
 typedef struct {
@@ -394,6 +407,9 @@ typedef struct {
   const void* dense;           /* device [B, dense_in], storage dtype */
   const float* labels;         /* device [B, T] */
   const uint8_t* mask;         /* device [B, T] */
+  const int64_t* domain_offsets;  /* host [top.n_domains + 1] when the top MLP has untied
+                                     layers (samples grouped by domain, see
+                                     lattice_mlp_desc), else ignored */
 } lattice_batch_desc;
 
 /* Stages of lattice_step, in order (for optional per-stage timing). */

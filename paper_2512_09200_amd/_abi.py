@@ -60,7 +60,8 @@ class lattice_linear(Structure):
 class lattice_mlp_desc(Structure):
     _fields_ = [("dtype", c_int), ("n_layers", c_int32), ("layers", POINTER(lattice_linear)),
                 ("relu_last", c_int32), ("act", c_int), ("norm_block", c_int32), ("norm_eps", c_float),
-                ("tower_heads", c_int32)]
+                ("tower_heads", c_int32), ("n_domains", c_int32), ("untied_layers", c_int32),
+                ("domain_offsets", POINTER(c_int64))]
 
 
 class lattice_loss_desc(Structure):
@@ -76,7 +77,7 @@ class lattice_model_desc(Structure):
 
 class lattice_batch_desc(Structure):
     _fields_ = [("bags", lattice_jagged), ("dense", c_void_p), ("labels", c_void_p),
-                ("mask", c_void_p)]
+                ("mask", c_void_p), ("domain_offsets", POINTER(c_int64))]
 
 
 SIDE_EVENTS = 6

@@ -202,25 +202,34 @@ _ACT = {None: A.ACT_RELU, "relu": A.ACT_RELU, "swishrn": A.ACT_SWISHRN, "hardswi
 
 
 def mlp_desc(layers, relu_last, dtype, act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6,
-             tower_heads=False):
+             tower_heads=False, n_domains=0, untied_layers=0, domain_offsets=None):
     """layers: list of dicts with W, b (optional), dW, db (optional); SwishRN
     layers (act "swishrn" / "hardswishrn") also gain [2, out] fp32, dgain
     (optional), and for lattice_mlp_heads_fwd/bwd pre [B, out] (storage
-    dtype) and rinv [B, groups] fp32."""
+    dtype) and rinv [B, groups] fp32.  Untied layers (the first
+    untied_layers, n_domains >= 2) hold stacked sets: W [D, out, in],
+    b [D, out], gain [D, 2, out] and gradients alike; domain_offsets (host,
+    [D + 1]) groups the rows for lattice_mlp_heads_fwd/bwd."""
     arr = (A.lattice_linear * len(layers))()
     for i, L in enumerate(layers):
         W = L["W"]
         _contig(W)
-        # tower heads: W is [T, H] and the layer's input holds T groups of H
-        in_dim = W.shape[0] * W.shape[1] if (tower_heads and i == len(layers) - 1) else W.shape[1]
-        arr[i] = A.lattice_linear(in_dim=in_dim, out_dim=W.shape[0], W=W.data_ptr(),
+        # tower heads: W is [T, H] and the layer's input holds T groups of H;
+        # untied layers: W is [D, out, in]
+        in_dim = W.shape[0] * W.shape[1] if (tower_heads and i == len(layers) - 1) else W.shape[-1]
+        arr[i] = A.lattice_linear(in_dim=in_dim, out_dim=W.shape[-2], W=W.data_ptr(),
                                   b=_ptr(L.get("b")), dW=_ptr(L.get("dW")), db=_ptr(L.get("db")),
                                   gain=_ptr(L.get("gain")), dgain=_ptr(L.get("dgain")),
                                   pre=_ptr(L.get("pre")), rinv=_ptr(L.get("rinv")))
     d = A.lattice_mlp_desc(dtype=dtype, n_layers=len(layers), layers=arr, relu_last=int(relu_last),
                            act=_ACT[act], norm_block=int(norm_block), norm_eps=float(norm_eps),
-                           tower_heads=int(bool(tower_heads)))
-    d._keep = arr
+                           tower_heads=int(bool(tower_heads)), n_domains=int(n_domains),
+                           untied_layers=int(untied_layers))
+    d._keep = [arr]
+    if domain_offsets is not None:
+        off = (ctypes.c_int64 * len(domain_offsets))(*[int(x) for x in domain_offsets])
+        d.domain_offsets = ctypes.cast(off, ctypes.POINTER(ctypes.c_int64))
+        d._keep.append(off)
     return d
 
 
@@ -230,13 +239,16 @@ def swishrn_groups(N, norm_block):
 
 
 def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None, act=None,
-                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6, tower_heads=False):
+                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6, tower_heads=False, n_domains=0,
+                          untied_layers=0, domain_offsets=None):
     """acts: list of output tensors (2-D, unit column stride); loss: optional
     dict(labels, mask, loss, d_logits, d_logits_op); act / norm_block /
     norm_eps: the activation, tower_heads: the last layer is the heads of
-    per-objective towers (see mlp_desc)."""
+    per-objective towers; n_domains / untied_layers / domain_offsets:
+    parameter untying (see mlp_desc)."""
     lib = load()
-    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps, tower_heads)
+    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps, tower_heads, n_domains, untied_layers,
+                 domain_offsets)
     n = len(layers)
     ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
     strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
@@ -254,9 +266,11 @@ def lattice_mlp_heads_fwd(layers, x, acts, relu_last, loss=None, stream=None, ac
 
 
 def lattice_mlp_heads_bwd(layers, x, acts, d_out, relu_last, d_in=None, stream=None, act=None,
-                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6, tower_heads=False):
+                          norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6, tower_heads=False, n_domains=0,
+                          untied_layers=0, domain_offsets=None):
     lib = load()
-    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps, tower_heads)
+    d = mlp_desc(layers, relu_last, _dt(x), act, norm_block, norm_eps, tower_heads, n_domains, untied_layers,
+                 domain_offsets)
     n = len(layers)
     ptrs = (ctypes.c_void_p * n)(*[a.data_ptr() for a in acts])
     strides = (ctypes.c_int64 * n)(*[_row_stride(a) for a in acts])
@@ -317,18 +331,21 @@ class StepModel:
     the FM interaction; max_rows: rows of the largest table (None: read from
     row_base once, here); top_act: None / "relu", "swishrn" or "hardswishrn"
     for the top MLP's hidden layers; towers: the top MLP's last layer is the
-    heads of per-objective towers (its W [T, H])."""
+    heads of per-objective towers (its W [T, H]); n_domains / untied_layers:
+    the first untied_layers top layers hold one parameter set per domain
+    (lattice_step then takes the batch's domain_offsets)."""
 
     def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
                  fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5,
                  max_rows=None, top_act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6,
-                 towers=False):
+                 towers=False, n_domains=0, untied_layers=0):
         _contig(tables, row_base)
         dt = _dt(tables)
         d = tables.shape[1]
         n = num_features + (1 if dense_in > 0 else 0)
         self._bottom = mlp_desc(bottom, True, dt) if dense_in > 0 else A.lattice_mlp_desc(dtype=dt)
-        self._top = mlp_desc(top, False, dt, top_act, norm_block, norm_eps, tower_heads=towers)
+        self._top = mlp_desc(top, False, dt, top_act, norm_block, norm_eps, tower_heads=towers,
+                             n_domains=n_domains, untied_layers=untied_layers)
         self.top_act, self.norm_block = top_act, norm_block
         self._stack = stack_layers(stack) if stack else None
         rank = fm_W.shape[1] if fm_W is not None else (stack[0]["W"].shape[1] if stack else 0)
@@ -383,7 +400,7 @@ class SideStream:
 
 def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0,
                  emit_grad_rows=False, stream=None, stage_events=None, nnz_capacity=0,
-                 side=None, fp8_top=None):
+                 side=None, fp8_top=None, domain_offsets=None):
     """One forward+backward step; ws is a uint8 device tensor of at least
     lattice_step_plan(...).total_bytes.  stage_events: optional list of
     2*len(STAGES) torch.cuda.Event(enable_timing=True) or None: [2s] and
@@ -391,13 +408,18 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
     it (None: not recorded).
     side: a SideStream to overlap the sort and the weight gradients on (None:
     every stage on the step's stream).  fp8_top: None, "precise" or "fast"
-    (the top MLP's hidden-layer forward in FP8; see lattice.h)."""
+    (the top MLP's hidden-layer forward in FP8; see lattice.h).
+    domain_offsets: host [D + 1] offsets of the domain-grouped samples
+    (models with untied layers)."""
     lib = load()
     _contig(dense, labels, mask, ws)
     B = labels.shape[0]
     batch = A.lattice_batch_desc(bags=_jagged(offsets, indices, model.num_features, B),
                                  dense=dense.data_ptr() if dense is not None and dense.numel() else None,
                                  labels=labels.data_ptr(), mask=mask.data_ptr())
+    if domain_offsets is not None:       # host offsets of the domain-grouped samples
+        off = (ctypes.c_int64 * len(domain_offsets))(*[int(x) for x in domain_offsets])
+        batch.domain_offsets = ctypes.cast(off, ctypes.POINTER(ctypes.c_int64))
     opts = A.lattice_step_opts(lr_tables=float(lr_tables), emit_grad_rows=int(emit_grad_rows),
                                nnz_capacity=int(nnz_capacity or indices.numel()), fp8_top=_FP8_TOP[fp8_top])
     if side is not None:
@@ -438,9 +460,9 @@ def step_views(model, ws, layout, B, T, nnz):
              num_unique=view(layout.num_unique, (1,), torch.int32),
              grad_rows=view(layout.grad_rows, (max(nnz, 1), d), torch.float32))
     tops = model.tensors["top"]
-    v["top_act"] = [view(layout.top_act[i], (B, tops[i]["W"].shape[0]), dt) for i in range(len(tops) - 1)]
-    v["top_grad"] = [view(layout.top_grad[i], (B, tops[i]["W"].shape[0]), dt) for i in range(len(tops))]
-    outs = [tops[i]["W"].shape[0] for i in range(len(tops) - 1)]
+    v["top_act"] = [view(layout.top_act[i], (B, tops[i]["W"].shape[-2]), dt) for i in range(len(tops) - 1)]
+    v["top_grad"] = [view(layout.top_grad[i], (B, tops[i]["W"].shape[-2]), dt) for i in range(len(tops))]
+    outs = [tops[i]["W"].shape[-2] for i in range(len(tops) - 1)]
     v["top_pre"] = [view(layout.top_pre[i], (B, o), dt) for i, o in enumerate(outs)]
     v["top_rinv"] = [view(layout.top_rinv[i], (B, swishrn_groups(o, model.norm_block)), torch.float32)
                      for i, o in enumerate(outs)]

@@ -106,9 +106,10 @@ static int64_t w_elems(const lattice_mlp_desc* d, int i) {
 static hipError_t zero_mlp_grads(const lattice_mlp_desc* d, hipStream_t s) {
   for (int i = 0; i < d->n_layers; ++i) {
     const lattice_linear& L = d->layers[i];
-    hipError_t e = zero_f32(L.dW, w_elems(d, i), s);
-    if (e == hipSuccess) e = zero_f32(L.db, L.out_dim, s);
-    if (e == hipSuccess && swish_layer(d, i)) e = zero_f32(L.dgain, 2 * (int64_t)L.out_dim, s);
+    const int64_t sets = (d->n_domains > 1 && i < d->untied_layers) ? d->n_domains : 1;
+    hipError_t e = zero_f32(L.dW, sets * w_elems(d, i), s);
+    if (e == hipSuccess) e = zero_f32(L.db, sets * L.out_dim, s);
+    if (e == hipSuccess && swish_layer(d, i)) e = zero_f32(L.dgain, sets * 2 * (int64_t)L.out_dim, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -555,8 +556,14 @@ static lattice_status check_mlp(const lattice_mlp_desc* d, int32_t B) {
     REQUIRE(L.in_dim % L.out_dim == 0 && (L.in_dim / L.out_dim) % 8 == 0,
             "tower heads: in_dim must be out_dim x H with H a multiple of 8");
   }
+  REQUIRE(d->n_domains >= 0, "negative n_domains");
+  if (d->n_domains > 1) {
+    REQUIRE(d->untied_layers >= 0 && d->untied_layers <= d->n_layers - (d->tower_heads ? 1 : 0),
+            "untied_layers %d outside 0..%d", d->untied_layers, d->n_layers - (d->tower_heads ? 1 : 0));
+  }
   return LATTICE_OK;
 }
+
 
 static int gate_of(const lattice_mlp_desc* d) {
   return d->act == LATTICE_ACT_SWISHRN ? GATE_SIGMOID : GATE_HARD;
@@ -569,6 +576,108 @@ struct ActBufs {
   float* rinv[LATTICE_MAX_LAYERS] = {};
   void* gout[LATTICE_MAX_LAYERS] = {};
 };
+
+// Parameter untying (Section 3.3.4): samples grouped by domain, host
+// offsets off[0..n] (off[0] = 0, off[n] = B); layers i < untied_layers hold
+// n_domains parameter sets, stacked, and the samples of domain g use set g.
+struct Domains {
+  int n = 1;
+  const int64_t* off = nullptr;
+};
+
+static bool untied(const lattice_mlp_desc* d, int i) {
+  return d->n_domains > 1 && i < d->untied_layers;
+}
+
+// Host domain offsets: off[0] = 0, non-decreasing, off[n] = B.
+static lattice_status check_domains(const lattice_mlp_desc* d, const int64_t* off, int B, Domains* dom) {
+  dom->n = 1;
+  dom->off = nullptr;
+  if (d->n_domains <= 1 || d->untied_layers == 0) return LATTICE_OK;
+  REQUIRE(off, "untied layers need domain offsets");
+  REQUIRE(off[0] == 0 && off[d->n_domains] == B, "domain offsets must run from 0 to B = %d", B);
+  for (int g = 0; g < d->n_domains; ++g) REQUIRE(off[g + 1] >= off[g], "domain offsets decrease at %d", g);
+  dom->n = d->n_domains;
+  dom->off = off;
+  return LATTICE_OK;
+}
+
+// SwishRN statistic groups of layer i (columns of its rho rows)
+static int rinv_cols(const lattice_mlp_desc* d, int i) {
+  return swishrn_groups(d->layers[i].out_dim, d->norm_block);
+}
+
+// The MLP seen by the samples of domain g: every untied layer's parameters
+// (and gradients) point at set g.
+struct MlpView {
+  lattice_mlp_desc d;
+  lattice_linear L[LATTICE_MAX_LAYERS];
+};
+
+static void domain_view(const lattice_mlp_desc* d, int g, MlpView* v) {
+  v->d = *d;
+  const int64_t es = (int64_t)esize(d->dtype);
+  for (int i = 0; i < d->n_layers; ++i) {
+    lattice_linear L = d->layers[i];
+    if (untied(d, i)) {
+      const int64_t wn = w_elems(d, i), o = L.out_dim;
+      L.W = (const char*)L.W + g * wn * es;
+      if (L.b) L.b += g * o;
+      if (L.dW) L.dW += g * wn;
+      if (L.db) L.db += g * o;
+      if (L.gain) L.gain += g * 2 * o;
+      if (L.dgain) L.dgain += g * 2 * o;
+    }
+    v->L[i] = L;
+  }
+  v->d.layers = v->L;
+}
+
+static const void* row_at(const void* p, int64_t r0, int64_t ld, int64_t es) {
+  return p ? (const char*)p + r0 * ld * es : nullptr;
+}
+static void* row_at(void* p, int64_t r0, int64_t ld, int64_t es) {
+  return p ? (char*)p + r0 * ld * es : nullptr;
+}
+
+// Rows r0.. of the activations (storage dtype; a linear last layer's fp32
+// logits) and of the SwishRN buffers.
+struct RowView {
+  const void* acts[LATTICE_MAX_LAYERS];
+  void* wacts[LATTICE_MAX_LAYERS];
+  ActBufs ab;
+};
+
+static void row_view(const lattice_mlp_desc* d, const void* const* acts, const int64_t* strides,
+                     const ActBufs* ab, int64_t r0, RowView* v) {
+  const int64_t es = (int64_t)esize(d->dtype);
+  for (int i = 0; i < d->n_layers; ++i) {
+    const bool logits = i == d->n_layers - 1 && !d->relu_last;
+    const int64_t e = logits ? 4 : es;
+    v->acts[i] = acts ? row_at(acts[i], r0, strides[i], e) : nullptr;
+    v->wacts[i] = const_cast<void*>(v->acts[i]);
+    const int64_t o = d->layers[i].out_dim;
+    v->ab.pre[i] = ab ? row_at(ab->pre[i], r0, o, es) : nullptr;
+    v->ab.rinv[i] = ab && ab->rinv[i] ? (float*)row_at(ab->rinv[i], r0, rinv_cols(d, i), 4) : nullptr;
+    v->ab.gout[i] = ab ? row_at(ab->gout[i], r0, o, es) : nullptr;
+  }
+}
+
+// f(desc, r0, rows) over the whole batch, or once per domain with that
+// domain's parameters when `split` (segments of no samples are skipped).
+template <typename F>
+static hipError_t per_domain(const lattice_mlp_desc* d, const Domains* dom, bool split, int B, F&& f) {
+  if (!split || !dom || dom->n <= 1) return f(d, (int64_t)0, B);
+  for (int g = 0; g < dom->n; ++g) {
+    const int64_t r0 = dom->off[g], rows = dom->off[g + 1] - r0;
+    if (rows <= 0) continue;
+    MlpView v;
+    domain_view(d, g, &v);
+    hipError_t e = f(&v.d, r0, (int)rows);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
 
 // split-K bound of the MLP backward products (the factor itself comes from
 // gemm_splits' time estimate)
@@ -599,59 +708,66 @@ static size_t mlp_gbuf_elems(const lattice_mlp_desc* d, int B) {
   return (size_t)w * B;
 }
 
-// SwishRN layers (ab): bf16 models with BlockNorm groups take the statistic
-// in the GEMM's epilogue; otherwise the GEMM stores the pre-activation and a
-// row kernel normalises it.
+// Layer i's forward on B rows: A [B, in] -> C [B, out] (and the SwishRN
+// buffers ab).  SwishRN layers: bf16 models with BlockNorm groups take the
+// statistic in the GEMM's epilogue; otherwise the GEMM stores the
+// pre-activation and a row kernel normalises it.
+static hipError_t mlp_forward_layer(const lattice_mlp_desc* d, int i, int B, const void* A,
+                                    int64_t lda, void* C, int64_t ldc, const ActBufs* ab,
+                                    hipStream_t s) {
+  const DType dt = dt_of(d->dtype);
+  const lattice_linear& L = d->layers[i];
+  const bool last = i == d->n_layers - 1;
+  GemmArgs g;
+  g.dt = dt;
+  g.A = A; g.lda = lda;
+  g.B = L.W; g.ldb = L.in_dim;
+  g.C = C; g.ldc = ldc;
+  g.c_dt = (last && !d->relu_last) ? DT_F32 : dt;
+  g.M = B; g.N = L.out_dim; g.K = L.in_dim;
+  g.bias = L.b;
+  if (tower_layer(d, i)) {
+    if (ldc != L.out_dim) {
+      set_error("tower heads write contiguous logits");
+      return hipErrorInvalidValue;
+    }
+    return tower_head_fwd(dt, A, lda, B, L.out_dim, L.in_dim / L.out_dim, L.W, L.b, (float*)C, s);
+  }
+  if (swish_layer(d, i)) {
+    if (dt == DT_BF16 && d->norm_block == LATTICE_BLOCKNORM_COLS) {
+      g.norm_gate = gate_of(d);
+      g.gain = L.gain;
+      g.eps = d->norm_eps;
+      g.pre = ab->pre[i];
+      g.ldp = L.out_dim;
+      g.rinv = ab->rinv[i];
+      g.nblk = cdiv(L.out_dim, LATTICE_BLOCKNORM_COLS);
+      return gemm(g, nullptr, s);
+    }
+    g.C = ab->pre[i];
+    g.ldc = L.out_dim;
+    hipError_t e = gemm(g, nullptr, s);
+    if (e == hipSuccess)
+      e = swishrn_fwd_rows(dt, ab->pre[i], L.out_dim, B, L.out_dim, d->norm_block, gate_of(d), L.gain,
+                           d->norm_eps, C, ldc, ab->rinv[i], s);
+    return e;
+  }
+  g.relu = (!last || d->relu_last) ? 1 : 0;
+  return gemm(g, nullptr, s);  // forward GEMMs never split K
+}
+
 static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
                               void* const* acts, const int64_t* strides, const ActBufs* ab,
-                              hipStream_t s) {
-  const DType dt = dt_of(d->dtype);
+                              hipStream_t s, const Domains* dom = nullptr) {
+  const int64_t es = (int64_t)esize(d->dtype);
   for (int i = 0; i < d->n_layers; ++i) {
-    const lattice_linear& L = d->layers[i];
-    const bool last = i == d->n_layers - 1;
-    GemmArgs g;
-    g.dt = dt;
-    g.A = i == 0 ? in : acts[i - 1];
-    g.lda = i == 0 ? in_stride : strides[i - 1];
-    g.B = L.W; g.ldb = L.in_dim;
-    g.C = acts[i]; g.ldc = strides[i];
-    g.c_dt = (last && !d->relu_last) ? DT_F32 : dt;
-    g.M = B; g.N = L.out_dim; g.K = L.in_dim;
-    g.bias = L.b;
-    if (tower_layer(d, i)) {
-      if (strides[i] != L.out_dim) {
-        set_error("tower heads write contiguous logits");
-        return hipErrorInvalidValue;
-      }
-      hipError_t e = tower_head_fwd(dt, g.A, g.lda, B, L.out_dim, L.in_dim / L.out_dim, L.W, L.b,
-                                    (float*)acts[i], s);
-      if (e != hipSuccess) return e;
-      continue;
-    }
-    if (swish_layer(d, i)) {
-      if (dt == DT_BF16 && d->norm_block == LATTICE_BLOCKNORM_COLS) {
-        g.norm_gate = gate_of(d);
-        g.gain = L.gain;
-        g.eps = d->norm_eps;
-        g.pre = ab->pre[i];
-        g.ldp = L.out_dim;
-        g.rinv = ab->rinv[i];
-        g.nblk = cdiv(L.out_dim, LATTICE_BLOCKNORM_COLS);
-        hipError_t e = gemm(g, nullptr, s);
-        if (e != hipSuccess) return e;
-      } else {
-        g.C = ab->pre[i];
-        g.ldc = L.out_dim;
-        hipError_t e = gemm(g, nullptr, s);
-        if (e == hipSuccess)
-          e = swishrn_fwd_rows(dt, ab->pre[i], L.out_dim, B, L.out_dim, d->norm_block, gate_of(d),
-                               L.gain, d->norm_eps, acts[i], strides[i], ab->rinv[i], s);
-        if (e != hipSuccess) return e;
-      }
-      continue;
-    }
-    g.relu = (!last || d->relu_last) ? 1 : 0;
-    hipError_t e = gemm(g, nullptr, s);  // forward GEMMs never split K
+    hipError_t e = per_domain(d, dom, untied(d, i), B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+      RowView v;
+      row_view(dv, acts, strides, ab, r0, &v);
+      const void* A = i == 0 ? row_at(in, r0, in_stride, es) : v.acts[i - 1];
+      return mlp_forward_layer(dv, i, rows, A, i == 0 ? in_stride : strides[i - 1], v.wacts[i],
+                               strides[i], &v.ab, s);
+    });
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -799,6 +915,40 @@ static hipError_t mlp_chain_step(const lattice_mlp_desc* d, int i, int B, const 
                          i > 0 ? strides[i - 1] : 0, ws, s);
 }
 
+// The chain step of layer i (see mlp_chain_step) over the batch, per domain
+// where layer i or the activation below it has untied parameters.
+static hipError_t chain_step_all(const lattice_mlp_desc* d, const Domains* dom, int i, int B,
+                                 const void* g, int64_t gs, const void* const* acts,
+                                 const int64_t* strides, const ActBufs* ab, void* dst, int64_t dst_ld,
+                                 void* ws, hipStream_t s) {
+  const int64_t es = (int64_t)esize(d->dtype);
+  const bool split = untied(d, i) || (i > 0 && untied(d, i - 1));
+  return per_domain(d, dom, split, B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+    RowView v;
+    row_view(dv, acts, strides, ab, r0, &v);
+    return mlp_chain_step(dv, i, rows, row_at(g, r0, gs, es), gs, v.acts, strides, &v.ab,
+                          row_at(dst, r0, dst_ld, es), dst_ld, ws, s);
+  });
+}
+
+static hipError_t wgrad_all(const lattice_mlp_desc* d, const Domains* dom, int i, int B, const void* g,
+                            int64_t gs, const void* in_i, int64_t ld_in, void* ws, hipStream_t s) {
+  const int64_t es = (int64_t)esize(d->dtype);
+  return per_domain(d, dom, untied(d, i), B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+    return mlp_layer_wgrad(dv, i, rows, row_at(g, r0, gs, es), gs, row_at(in_i, r0, ld_in, es), ld_in,
+                           ws, s);
+  });
+}
+
+static hipError_t gain_grad_all(const lattice_mlp_desc* d, const Domains* dom, int j, int B,
+                                const ActBufs* ab, void* ws, hipStream_t s) {
+  return per_domain(d, dom, untied(d, j), B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+    RowView v;
+    row_view(dv, nullptr, nullptr, ab, r0, &v);
+    return swish_gain_grad(dv, j, rows, v.ab.gout[j], dv->layers[j].out_dim, &v.ab, ws, s);
+  });
+}
+
 // g_last: gradient of the last layer's pre-activation (already taken through
 // its activation where it has one).  Layer by layer (weights, gains of the
 // layer below, then input gradient); hidden gradients alternate between
@@ -807,21 +957,20 @@ static hipError_t mlp_backward(const lattice_mlp_desc* d, int B, const void* in,
                                const void* const* acts, const int64_t* strides,
                                const void* g_last, int64_t g_last_stride, void* d_in,
                                int64_t d_in_stride, void* gbuf0, void* gbuf1, const ActBufs* ab,
-                               void* ws, hipStream_t s) {
+                               void* ws, hipStream_t s, const Domains* dom = nullptr) {
   const void* g = g_last;
   int64_t gs = g_last_stride;
   for (int i = d->n_layers - 1; i >= 0; --i) {
     const lattice_linear& L = d->layers[i];
     const void* in_i = i == 0 ? in : acts[i - 1];
     const int64_t ld_in = i == 0 ? in_stride : strides[i - 1];
-    hipError_t e = mlp_layer_wgrad(d, i, B, g, gs, in_i, ld_in, ws, s);
+    hipError_t e = wgrad_all(d, dom, i, B, g, gs, in_i, ld_in, ws, s);
     if (e != hipSuccess) return e;
     if (i > 0 || d_in) {
       void* dst = i > 0 ? ((d->n_layers - 1 - i) % 2 == 0 ? gbuf0 : gbuf1) : d_in;
       const int64_t dst_ld = i > 0 ? L.in_dim : d_in_stride;
-      e = mlp_chain_step(d, i, B, g, gs, acts, strides, ab, dst, dst_ld, ws, s);
-      if (e == hipSuccess && i > 0 && swish_layer(d, i - 1))
-        e = swish_gain_grad(d, i - 1, B, ab->gout[i - 1], L.in_dim, ab, ws, s);
+      e = chain_step_all(d, dom, i, B, g, gs, acts, strides, ab, dst, dst_ld, ws, s);
+      if (e == hipSuccess && i > 0 && swish_layer(d, i - 1)) e = gain_grad_all(d, dom, i - 1, B, ab, ws, s);
       if (e != hipSuccess) return e;
       g = dst;
       gs = dst_ld;
@@ -836,14 +985,15 @@ static hipError_t mlp_backward(const lattice_mlp_desc* d, int B, const void* in,
 static hipError_t mlp_backward_data(const lattice_mlp_desc* d, int B, const void* const* acts,
                                     const int64_t* strides, const void* g_last,
                                     int64_t g_last_stride, void* d_in, int64_t d_in_stride,
-                                    void* const* gl, const ActBufs* ab, void* ws, hipStream_t s) {
+                                    void* const* gl, const ActBufs* ab, void* ws, hipStream_t s,
+                                    const Domains* dom = nullptr) {
   const void* g = g_last;
   int64_t gs = g_last_stride;
   for (int i = d->n_layers - 1; i >= 0; --i) {
     if (i == 0 && !d_in) break;
     void* dst = i > 0 ? gl[i - 1] : d_in;
     const int64_t dst_ld = i > 0 ? d->layers[i].in_dim : d_in_stride;
-    hipError_t e = mlp_chain_step(d, i, B, g, gs, acts, strides, ab, dst, dst_ld, ws, s);
+    hipError_t e = chain_step_all(d, dom, i, B, g, gs, acts, strides, ab, dst, dst_ld, ws, s);
     if (e != hipSuccess) return e;
     g = dst;
     gs = dst_ld;
@@ -857,14 +1007,13 @@ static hipError_t mlp_backward_weights(const lattice_mlp_desc* d, int B, const v
                                        int64_t in_stride, const void* const* acts,
                                        const int64_t* strides, const void* g_last,
                                        int64_t g_last_stride, void* const* gl, const ActBufs* ab,
-                                       void* ws, hipStream_t s) {
+                                       void* ws, hipStream_t s, const Domains* dom = nullptr) {
   for (int i = d->n_layers - 1; i >= 0; --i) {
     const void* g = i == d->n_layers - 1 ? g_last : gl[i];
     const int64_t gs = i == d->n_layers - 1 ? g_last_stride : d->layers[i].out_dim;
-    hipError_t e = mlp_layer_wgrad(d, i, B, g, gs, i == 0 ? in : acts[i - 1],
-                                   i == 0 ? in_stride : strides[i - 1], ws, s);
-    if (e == hipSuccess && i < d->n_layers - 1 && swish_layer(d, i))
-      e = swish_gain_grad(d, i, B, ab->gout[i], d->layers[i].out_dim, ab, ws, s);
+    hipError_t e = wgrad_all(d, dom, i, B, g, gs, i == 0 ? in : acts[i - 1],
+                             i == 0 ? in_stride : strides[i - 1], ws, s);
+    if (e == hipSuccess && i < d->n_layers - 1 && swish_layer(d, i)) e = gain_grad_all(d, dom, i, B, ab, ws, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -932,7 +1081,10 @@ lattice_status lattice_mlp_heads_fwd(const lattice_mlp_desc* desc, int32_t B, co
   ActBufs ab;
   st = layer_bufs(desc, B, &ab);
   if (st != LATTICE_OK) return st;
-  if (B > 0) HIPRET(mlp_forward(desc, B, in, in_stride, acts, act_strides, &ab, strm(stream)));
+  Domains dom;
+  st = check_domains(desc, desc->domain_offsets, B, &dom);
+  if (st != LATTICE_OK) return st;
+  if (B > 0) HIPRET(mlp_forward(desc, B, in, in_stride, acts, act_strides, &ab, strm(stream), &dom));
   if (loss)
     HIPRET(bce((const float*)acts[desc->n_layers - 1], loss->labels, loss->mask, (int64_t)B * T,
                loss->loss, loss->d_logits, loss->d_logits_op, dt_of(desc->dtype), ws,
@@ -962,6 +1114,9 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
   ActBufs ab;
   st = layer_bufs(desc, B, &ab);
   if (st != LATTICE_OK) return st;
+  Domains dom;
+  st = check_domains(desc, desc->domain_offsets, B, &dom);
+  if (st != LATTICE_OK) return st;
   char* p = (char*)ws;
   void* gemm_ws = p; p += mlp_bwd_ws(desc, B);
   const size_t g = al256(mlp_gbuf_elems(desc, B) * esize(desc->dtype));
@@ -974,8 +1129,16 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
   int64_t g_ld = d_out_stride;
   hipStream_t s = strm(stream);
   if (desc->relu_last && swish_layer(desc, L - 1)) {
-    HIPRET(swish_gain_grad(desc, L - 1, B, d_out, d_out_stride, &ab, gemm_ws, s));
-    HIPRET(swish_back(desc, L - 1, B, d_out, d_out_stride, &ab, masked, T, s));
+    // the last layer's SwishRN backward from d_out (per domain if untied)
+    const int64_t es = (int64_t)esize(desc->dtype);
+    HIPRET(per_domain(desc, &dom, untied(desc, L - 1), B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+      RowView v;
+      row_view(dv, nullptr, nullptr, &ab, r0, &v);
+      const void* go = row_at(d_out, r0, d_out_stride, es);
+      hipError_t e = swish_gain_grad(dv, L - 1, rows, go, d_out_stride, &v.ab, gemm_ws, s);
+      if (e == hipSuccess) e = swish_back(dv, L - 1, rows, go, d_out_stride, &v.ab, row_at(masked, r0, T, es), T, s);
+      return e;
+    }));
     g_last = masked;
     g_ld = T;
   } else if (desc->relu_last) {
@@ -987,7 +1150,7 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
     g_ld = T;
   }
   HIPRET(mlp_backward(desc, B, in, in_stride, acts, act_strides, g_last, g_ld, d_in, d_in_stride,
-                      gb0, gb1, &ab, gemm_ws, s));
+                      gb0, gb1, &ab, gemm_ws, s, &dom));
   return LATTICE_OK;
 }
 
@@ -1024,6 +1187,8 @@ static lattice_status check_model(const lattice_model_desc* m, int B) {
     REQUIRE(m->bottom.dtype == m->dtype, "bottom dtype");
     if (m->bottom.act != LATTICE_ACT_RELU)
       FAIL(LATTICE_ERR_UNSUPPORTED, "the step's bottom MLP uses ReLU (SwishRN: top MLP)");
+    if (m->bottom.n_domains > 1 && m->bottom.untied_layers > 0)
+      FAIL(LATTICE_ERR_UNSUPPORTED, "the step's bottom MLP is tied (untying: top MLP)");
   }
   st = check_mlp(&m->top, B);
   if (st != LATTICE_OK) return st;
@@ -1052,6 +1217,8 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
     REQUIRE(o->fp8_top == 1 || o->fp8_top == 2, "fp8_top must be 0, 1 or 2");
     if (m->dtype != LATTICE_BF16) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs a bf16 model");
     if (m->top.act != LATTICE_ACT_RELU) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs ReLU layers");
+    if (m->top.n_domains > 1 && m->top.untied_layers > 0)
+      FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs tied layers");
   }
   const size_t es = esize(m->dtype);
   const int d = m->tables.dim;
@@ -1171,6 +1338,9 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   if (ws_bytes < (size_t)P.L.total_bytes || !ws)
     FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %lld", ws_bytes, (long long)P.L.total_bytes);
   REQUIRE((batch->labels && batch->mask) || B == 0, "null labels/mask");
+  Domains dom;
+  st = check_domains(&m->top, batch->domain_offsets, B, &dom);
+  if (st != LATTICE_OK) return st;
   if (m->dense_in > 0) REQUIRE(batch->dense || B == 0, "null dense input");
   if (opts->side_stream && opts->side_stream != stream) {
     REQUIRE(opts->side_events, "side_stream needs side_events");
@@ -1315,12 +1485,12 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     if (nt > 1 && opts->fp8_top)
       HIPRET(mlp_forward_fp8(&hidden, B, t, P.t_stride, tacts, tstr, at(L.fp8), opts->fp8_top == 2, s));
     else if (nt > 1)
-      HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, &tab, s));
+      HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, &tab, s, &dom));
     HIPRET(head_fwd((const bf16_t*)head_in, head_ld, B, head.in_dim, (const bf16_t*)head.W, head.b,
                     T, batch->labels, batch->mask, (float*)at(L.logits), scratch, s));
   } else {
     if (opts->fp8_top) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs the fused bf16 heads (<= 64 objectives)");
-    HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, &tab, s));
+    HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, &tab, s, &dom));
   }
   HIPRET(end(LATTICE_STAGE_TOP_FWD));
   HIPRET(begin(LATTICE_STAGE_LOSS));
@@ -1343,15 +1513,22 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   // 6. top backward, gradient chain only -> d_t (weight gradients: 8.)
   HIPRET(begin(LATTICE_STAGE_TOP_BWD));
   if (fused_heads) {
-    if (nt > 1 && top_swish)
-      HIPRET(swish_back(&hidden, nt - 2, B, tab.gout[nt - 2], head.in_dim, &tab, gtop[nt - 2],
-                        head.in_dim, s));
+    if (nt > 1 && top_swish) {
+      const int64_t es = (int64_t)esize(m->dtype);
+      HIPRET(per_domain(&hidden, &dom, untied(&hidden, nt - 2), B,
+                        [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+                          RowView v;
+                          row_view(dv, nullptr, nullptr, &tab, r0, &v);
+                          return swish_back(dv, nt - 2, rows, v.ab.gout[nt - 2], head.in_dim, &v.ab,
+                                            row_at(gtop[nt - 2], r0, head.in_dim, es), head.in_dim, s);
+                        }));
+    }
     if (nt > 1)
       HIPRET(mlp_backward_data(&hidden, B, tacts, tstr, gtop[nt - 2], head.in_dim, at(L.d_t),
-                               P.t_stride, gtop, &tab, scratch, s));
+                               P.t_stride, gtop, &tab, scratch, s, &dom));
   } else {
     HIPRET(mlp_backward_data(&m->top, B, tacts, tstr, at(L.d_logits_op), T, at(L.d_t), P.t_stride,
-                             gtop, &tab, scratch, s));
+                             gtop, &tab, scratch, s, &dom));
   }
   HIPRET(end(LATTICE_STAGE_TOP_BWD));
   // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
@@ -1377,7 +1554,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   };
   HIPRET(wbegin(LATTICE_STAGE_TOP_WGRAD));
   HIPRET(mlp_backward_weights(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, gtop,
-                              &tab, scratch, ws_stream));
+                              &tab, scratch, ws_stream, &dom));
   HIPRET(wend(LATTICE_STAGE_TOP_WGRAD));
   // 9. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
   HIPRET(wbegin(LATTICE_STAGE_BOTTOM_BWD));

@@ -203,21 +203,44 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
     def heads_wgrad(g, h, W):
         return omlp.grouped_linear_grads(g, h, W)[0] if towers else g.T @ h
 
-    for i, (W, b) in enumerate(params["top"]):
-        W, b = np.asarray(W, np.float64), np.asarray(b, np.float64)
-        h = h_top[i][R]
+    dom = np.asarray(batch.get("domain", np.zeros(B, np.int64)))
+
+    def parts(i, rows_sel):
+        """(params of layer i, act view, row subset) per domain for an untied
+        layer (W [D, out, in]), else one part with the whole row set."""
+        W, b = (np.asarray(x, np.float64) for x in params["top"][i])
+        if W.ndim == 2:
+            return [(W, b, act, rows_sel)]
+        out = []
+        for k in range(W.shape[0]):
+            sel = rows_sel[dom[rows_sel] == k]
+            av = None
+            if act is not None:
+                av = dict(act, gains=list(act["gains"]))
+                ga, gb = act["gains"][i]
+                av["gains"][i] = (ga[k], gb[k])
+            if sel.size:
+                out.append((W[k], b[k], av, sel))
+        return out
+
+    def untied_at(i):
+        return np.ndim(params["top"][i][0]) == 3
+
+    for i in range(L):
         last = i == L - 1
-        a = heads_fwd(h, W, b) if last else h @ W.T + b
-        ab = heads_fwd(np.abs(h), np.abs(W), np.abs(b)) if last else np.abs(h) @ np.abs(W).T + np.abs(b)
-        if i < L - 1 and act is not None:
-            check_swishrn_forward(f"top{i}", cfg, act, i, h, W, b, _np64(v["top_pre"][i])[R],
-                                  _np64(v["top_rinv"][i])[R], h_top[i + 1][R], us, t)
-        elif i < L - 1 and fp8_top:
-            assert_fp8_layer(f"top{i} forward", h_top[i + 1][R], h, W, b, fp8_top == "fast", t)
-        elif i < L - 1:
-            assert_product(f"top{i} forward", h_top[i + 1][R], np.maximum(a, 0), ab, W.shape[1] + 1, us, t)
-        else:
-            assert_product("logits", _np64(v["logits"])[R], a, ab, W.shape[1] + 1, None, t)
+        for W, b, av, Rp in parts(i, R):
+            h = h_top[i][Rp]
+            a = heads_fwd(h, W, b) if last else h @ W.T + b
+            ab = heads_fwd(np.abs(h), np.abs(W), np.abs(b)) if last else np.abs(h) @ np.abs(W).T + np.abs(b)
+            if i < L - 1 and av is not None:
+                check_swishrn_forward(f"top{i}", cfg, av, i, h, W, b, _np64(v["top_pre"][i])[Rp],
+                                      _np64(v["top_rinv"][i])[Rp], h_top[i + 1][Rp], us, t)
+            elif i < L - 1 and fp8_top:
+                assert_fp8_layer(f"top{i} forward", h_top[i + 1][Rp], h, W, b, fp8_top == "fast", t)
+            elif i < L - 1:
+                assert_product(f"top{i} forward", h_top[i + 1][Rp], np.maximum(a, 0), ab, W.shape[1] + 1, us, t)
+            else:
+                assert_product("logits", _np64(v["logits"])[Rp], a, ab, W.shape[1] + 1, None, t)
     # loss and dz from the stored logits
     z = _np64(v["logits"])
     N = max(1.0, float(np.asarray(batch["mask"]).sum()))
@@ -228,25 +251,33 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
     assert e_loss <= 1e-5 and e_dz <= 1e-5
     # the gradient chain: g_{i-1} = (g_i W_i) masked by the stored h_i > 0
     # (SwishRN: g_i W_i is the stored output gradient, taken through the
-    # SwishRN backward)
+    # SwishRN backward); untied layers per domain
     for i in range(L - 1, -1, -1):
-        W = np.asarray(params["top"][i][0], np.float64)
-        if i == L - 1:
-            prod, ab = heads_dgrad(g_top[i][R], W), heads_dgrad(np.abs(g_top[i][R]), np.abs(W))
-            Kc = 1 if towers else W.shape[0]
-        else:
-            prod, ab, Kc = g_top[i][R] @ W, np.abs(g_top[i][R]) @ np.abs(W), W.shape[0]
-        if i > 0 and act is not None:
-            gout = _np64(v["top_gout"][i - 1])[R]
-            assert_product(f"top{i} output grad", gout, prod, ab, Kc, us, t)
-            check_swishrn_backward(f"top{i - 1}", act, i - 1, gout, _np64(v["top_pre"][i - 1])[R],
-                                   _np64(v["top_rinv"][i - 1])[R], g_top[i - 1][R], us, t)
-        elif i > 0:
-            on = h_top[i][R] > 0
-            assert_product(f"top{i} grad chain", g_top[i - 1][R], prod * on, ab * on, Kc, us, t)
-        else:
-            assert_product("d_t", tin_grad(v, cfg)[R], prod, ab, Kc, us, t)
-    # weight and bias gradients from the stored chain and activations
+        # parameter views of layer i and, for the activation below, layer i-1
+        lower = parts(i - 1, R) if i > 0 and untied_at(i - 1) else None
+        for W, _, _, Rp in parts(i, R):
+            subs = [(Rp, act)] if lower is None else [(np.intersect1d(Rp, q[3]), q[2]) for q in lower]
+            for Rq, av in subs:
+                if Rq.size == 0:
+                    continue
+                if i == L - 1:
+                    prod, ab = heads_dgrad(g_top[i][Rq], W), heads_dgrad(np.abs(g_top[i][Rq]), np.abs(W))
+                    Kc = 1 if towers else W.shape[0]
+                else:
+                    prod, ab, Kc = g_top[i][Rq] @ W, np.abs(g_top[i][Rq]) @ np.abs(W), W.shape[0]
+                if i > 0 and av is not None:
+                    gout = _np64(v["top_gout"][i - 1])[Rq]
+                    assert_product(f"top{i} output grad", gout, prod, ab, Kc, us, t)
+                    check_swishrn_backward(f"top{i - 1}", av, i - 1, gout, _np64(v["top_pre"][i - 1])[Rq],
+                                           _np64(v["top_rinv"][i - 1])[Rq], g_top[i - 1][Rq], us, t)
+                elif i > 0:
+                    on = h_top[i][Rq] > 0
+                    assert_product(f"top{i} grad chain", g_top[i - 1][Rq], prod * on, ab * on, Kc, us, t)
+                else:
+                    assert_product("d_t", tin_grad(v, cfg)[Rq], prod, ab, Kc, us, t)
+    # weight and bias gradients from the stored chain and activations (an
+    # untied layer: each domain's set from its own samples)
+    allrows = np.arange(B)
     for i in range(L):
         r = wr.get(("top", i), slice(None))
         if i == L - 1 and towers:
@@ -256,14 +287,20 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
                            heads_wgrad(np.abs(gi), np.abs(hi), Wl), B, None, t)
             assert_product(f"top{i}.db", _np64(grads["top_db"][i]), gi.sum(0), np.abs(gi).sum(0), B, None, t)
             continue
-        gi, hi = g_top[i][:, r], h_top[i]
-        assert_product(f"top{i}.dW", _np64(grads["top_dW"][i])[r], gi.T @ hi, np.abs(gi).T @ np.abs(hi),
-                       B, None, t)
-        assert_product(f"top{i}.db", _np64(grads["top_db"][i])[r], gi.sum(0), np.abs(gi).sum(0), B, None, t)
+        dWg, dbg = _np64(grads["top_dW"][i]), _np64(grads["top_db"][i])
+        for k, (_, _, _, Rp) in enumerate(parts(i, allrows)):
+            gi, hi = g_top[i][Rp][:, r], h_top[i][Rp]
+            dW_k = dWg[k] if untied_at(i) else dWg
+            db_k = dbg[k] if untied_at(i) else dbg
+            tag = f"top{i}[domain {k}]" if untied_at(i) else f"top{i}"
+            assert_product(f"{tag}.dW", dW_k[r], gi.T @ hi, np.abs(gi).T @ np.abs(hi), Rp.size, None, t)
+            assert_product(f"{tag}.db", db_k[r], gi.sum(0), np.abs(gi).sum(0), Rp.size, None, t)
     if act is not None and rows is None:
         for i in range(L - 1):
-            check_swishrn_gains(f"top{i}", act, i, v["top_gout"][i], v["top_pre"][i], v["top_rinv"][i],
-                                grads["top_dgain"][i], t)
+            dgk = _np64(grads["top_dgain"][i])
+            for k, (_, _, av, Rp) in enumerate(parts(i, allrows)):
+                check_swishrn_gains(f"top{i}", av, i, _np64(v["top_gout"][i])[Rp], _np64(v["top_pre"][i])[Rp],
+                                    _np64(v["top_rinv"][i])[Rp], dgk[k] if untied_at(i) else dgk, t)
     X = _np64(v["X"])
     dX = _np64(v["dX"])
     gt = tin_grad(v, cfg)
@@ -452,8 +489,10 @@ class Workload:
         self.bottom = [lin(W, bb) for W, bb in self.params["bottom"]]
         self.top = [lin(W, bb) for W, bb in self.params["top"]]
         for L, (ga, gb) in zip(self.top, self.params.get("top_gain", [])):
-            L["gain"] = to_dev(np.stack([ga, gb]))
+            # [2, out], or [D, 2, out] for an untied layer
+            L["gain"] = to_dev(np.stack([ga, gb], axis=-2))
             L["dgain"] = torch.zeros(L["gain"].shape, dtype=torch.float32, device=DEV)
+        self.domain_offsets = self.batch["domain_offsets"] if cfg.untie else None
         self.fm_W = to_dev(self.params["fm_W"], sdt) if "fm_W" in self.params else None
         self.fm_dW = torch.zeros(self.fm_W.shape, dtype=torch.float32, device=DEV) \
             if self.fm_W is not None else None
@@ -470,7 +509,8 @@ class Workload:
                              interact=c.interact, fm_W=self.fm_W, fm_dW=self.fm_dW, pool=c.pool,
                              stack=self.stack, stack_n=c.stack_n, ln_eps=c.ln_eps,
                              top_act=c.top_act, norm_block=c.norm_block, norm_eps=c.norm_eps,
-                             towers=bool(c.towers))
+                             towers=bool(c.towers), n_domains=len(c.domains[0]) if c.untie else 0,
+                             untied_layers=c.untie)
 
 
 def relu_overrides(cfg, params, table, batch, gpu_in, gpu_out, max_iter=4):

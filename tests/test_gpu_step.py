@@ -52,7 +52,8 @@ def run_step(w, lr, emit=True, spare=0, side="new", fp8_top=None, **kw):
     if side == "new":
         side = api.SideStream()
     api.lattice_step(model, w.offsets, w.indices, w.dense, w.labels, w.mask, ws, lr, emit,
-                     nnz_capacity=w.nnz + spare, side=side, fp8_top=fp8_top, **kw)
+                     nnz_capacity=w.nnz + spare, side=side, fp8_top=fp8_top,
+                     domain_offsets=w.domain_offsets, **kw)
     torch.cuda.synchronize()
     return model, api.step_views(model, ws, lay, cfg.B, cfg.T, w.nnz), ws
 
@@ -199,6 +200,27 @@ TOWER_CASES = {
 }
 
 
+UNTIE_CASES = {
+    # four domains of the multi-domain workload, the first two top layers untied
+    "multidomain-small-untied": synth.small(synth.MULTIDOMAIN, B=256, rows=2000, untie=2),
+    # untied SwishRN layers (per-domain gains) and towers
+    "multidomain-small-untied-swishrn-towers": synth.small(synth.MULTIDOMAIN, B=200, rows=2000,
+                                                           top=(256, 32 * 8, 32), towers=8, untie=2,
+                                                           top_act="swishrn"),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(UNTIE_CASES))
+def test_step_untied(name):
+    """Parameter untying (Section 3.3.4): per-domain parameter sets of the
+    top MLP's hidden layers on domain-grouped samples; every stage per
+    domain on the GPU's own stored inputs, then the composed step."""
+    cfg = UNTIE_CASES[name]
+    print(f"[step-untied] {name} B={cfg.B} top={cfg.top} untie={cfg.untie} {cfg.top_act}", flush=True)
+    check_step_staged(cfg)
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("name", list(TOWER_CASES))
 def test_step_towers(name):
@@ -234,7 +256,7 @@ def check_step_staged(cfg, lr=0.01):
     for i in range(len(w.top)):
         pairs += [(f"top{i}.dW", w.top[i]["dW"], g["top_dW"][i]), (f"top{i}.db", w.top[i]["db"], g["top_db"][i])]
     for i, dg in enumerate(g.get("top_dgain", [])):
-        pairs.append((f"top{i}.dgain", w.top[i]["dgain"], np.stack(dg)))
+        pairs.append((f"top{i}.dgain", w.top[i]["dgain"], np.stack(dg, axis=-2)))
     for nm, got, ref in pairs:
         got = got.float().cpu().numpy()
         e = max_rel_err(got, ref) if t <= 1e-5 else max_rel_err_normwise(got, ref)
