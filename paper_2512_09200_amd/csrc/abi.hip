@@ -712,9 +712,15 @@ static size_t mlp_gbuf_elems(const lattice_mlp_desc* d, int B) {
 // buffers ab).  SwishRN layers: bf16 models with BlockNorm groups take the
 // statistic in the GEMM's epilogue; otherwise the GEMM stores the
 // pre-activation and a row kernel normalises it.
+// The domains of an untied bf16 layer as the groups of one grouped GEMM (or
+// null: the layer is tied, or the model fp32 -- then per domain).
+static const Domains* gemm_groups(const lattice_mlp_desc* d, int i, const Domains* dom) {
+  return (untied(d, i) && dom && dom->n > 1 && dom->n <= 16 && d->dtype == LATTICE_BF16) ? dom : nullptr;
+}
+
 static hipError_t mlp_forward_layer(const lattice_mlp_desc* d, int i, int B, const void* A,
                                     int64_t lda, void* C, int64_t ldc, const ActBufs* ab,
-                                    hipStream_t s) {
+                                    hipStream_t s, const Domains* grp = nullptr) {
   const DType dt = dt_of(d->dtype);
   const lattice_linear& L = d->layers[i];
   const bool last = i == d->n_layers - 1;
@@ -726,6 +732,11 @@ static hipError_t mlp_forward_layer(const lattice_mlp_desc* d, int i, int B, con
   g.c_dt = (last && !d->relu_last) ? DT_F32 : dt;
   g.M = B; g.N = L.out_dim; g.K = L.in_dim;
   g.bias = L.b;
+  if (grp) {  // every domain's rows with its own W, b and gains, one launch
+    g.ngroups = grp->n;
+    g.goff = grp->off;
+    g.gsB = (int64_t)L.out_dim * L.in_dim;
+  }
   if (tower_layer(d, i)) {
     if (ldc != L.out_dim) {
       set_error("tower heads write contiguous logits");
@@ -747,10 +758,14 @@ static hipError_t mlp_forward_layer(const lattice_mlp_desc* d, int i, int B, con
     g.C = ab->pre[i];
     g.ldc = L.out_dim;
     hipError_t e = gemm(g, nullptr, s);
-    if (e == hipSuccess)
-      e = swishrn_fwd_rows(dt, ab->pre[i], L.out_dim, B, L.out_dim, d->norm_block, gate_of(d), L.gain,
-                           d->norm_eps, C, ldc, ab->rinv[i], s);
-    return e;
+    if (e != hipSuccess) return e;
+    const int64_t es = (int64_t)esize(d->dtype);
+    return per_domain(d, grp, grp != nullptr, B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+      const lattice_linear& Lv = dv->layers[i];
+      return swishrn_fwd_rows(dt, row_at(ab->pre[i], r0, L.out_dim, es), L.out_dim, rows, L.out_dim,
+                              d->norm_block, gate_of(d), Lv.gain, d->norm_eps, row_at(C, r0, ldc, es), ldc,
+                              (float*)row_at(ab->rinv[i], r0, rinv_cols(d, i), 4), s);
+    });
   }
   g.relu = (!last || d->relu_last) ? 1 : 0;
   return gemm(g, nullptr, s);  // forward GEMMs never split K
@@ -761,6 +776,12 @@ static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, 
                               hipStream_t s, const Domains* dom = nullptr) {
   const int64_t es = (int64_t)esize(d->dtype);
   for (int i = 0; i < d->n_layers; ++i) {
+    if (const Domains* grp = gemm_groups(d, i, dom)) {
+      hipError_t e = mlp_forward_layer(d, i, B, i == 0 ? in : acts[i - 1], i == 0 ? in_stride : strides[i - 1],
+                                       acts[i], strides[i], ab, s, grp);
+      if (e != hipSuccess) return e;
+      continue;
+    }
     hipError_t e = per_domain(d, dom, untied(d, i), B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
       RowView v;
       row_view(dv, acts, strides, ab, r0, &v);
@@ -819,7 +840,7 @@ static hipError_t mlp_forward_fp8(const lattice_mlp_desc* d, int B, const void* 
 // Weight and bias gradients of layer i: dW = gᵀ · in (fp32), db = Σ_b g.
 static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const void* g,
                                   int64_t gs, const void* in_i, int64_t ld_in, void* ws,
-                                  hipStream_t s) {
+                                  hipStream_t s, const Domains* grp = nullptr) {
   const lattice_linear& L = d->layers[i];
   const DType dt = dt_of(d->dtype);
   if (tower_layer(d, i)) {
@@ -836,6 +857,12 @@ static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const
     w.C = L.dW; w.ldc = L.in_dim; w.c_dt = DT_F32;
     w.M = L.out_dim; w.N = L.in_dim; w.K = B;
     w.max_splits = MLP_MAX_SPLITS;
+    if (grp) {  // every domain's samples into its own dW (and db), one launch
+      w.ngroups = grp->n;
+      w.goff = grp->off;
+      w.gk = 1;
+      w.gsC = (int64_t)L.out_dim * L.in_dim;
+    }
     // bf16: db is the row sum of A = gᵀ, taken by the same GEMM
     if (dt == DT_BF16 && L.db) {
       w.rowsum = L.db;
@@ -852,7 +879,7 @@ static hipError_t mlp_layer_wgrad(const lattice_mlp_desc* d, int i, int B, const
 // input activation, i.e. the previous layer's ReLU output; null: no mask).
 static hipError_t mlp_layer_dgrad(const lattice_mlp_desc* d, int i, int B, const void* g,
                                   int64_t gs, void* dst, int64_t dst_ld, const void* mask,
-                                  int64_t ldm, void* ws, hipStream_t s) {
+                                  int64_t ldm, void* ws, hipStream_t s, const Domains* grp = nullptr) {
   const lattice_linear& L = d->layers[i];
   GemmArgs x;
   x.dt = dt_of(d->dtype);
@@ -861,6 +888,11 @@ static hipError_t mlp_layer_dgrad(const lattice_mlp_desc* d, int i, int B, const
   x.C = dst; x.ldc = dst_ld; x.c_dt = x.dt;
   x.M = B; x.N = L.in_dim; x.K = L.out_dim;
   x.max_splits = MLP_MAX_SPLITS;
+  if (grp) {  // every domain's rows with its own W, one launch
+    x.ngroups = grp->n;
+    x.goff = grp->off;
+    x.gsB = (int64_t)L.out_dim * L.in_dim;
+  }
   if (mask) {
     x.mask = mask;
     x.mask_dt = x.dt;
@@ -922,6 +954,23 @@ static hipError_t chain_step_all(const lattice_mlp_desc* d, const Domains* dom, 
                                  const int64_t* strides, const ActBufs* ab, void* dst, int64_t dst_ld,
                                  void* ws, hipStream_t s) {
   const int64_t es = (int64_t)esize(d->dtype);
+  if (const Domains* grp = gemm_groups(d, i, dom)) {
+    // one grouped product for every domain's rows; then the activation
+    // below (ReLU: in the product's epilogue; SwishRN: its row kernel, per
+    // domain when that layer is untied)
+    if (i > 0 && swish_layer(d, i - 1)) {
+      const int64_t ldo = d->layers[i - 1].out_dim;
+      hipError_t e = mlp_layer_dgrad(d, i, B, g, gs, ab->gout[i - 1], ldo, nullptr, 0, ws, s, grp);
+      if (e != hipSuccess) return e;
+      return per_domain(d, dom, untied(d, i - 1), B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
+        RowView v;
+        row_view(dv, nullptr, nullptr, ab, r0, &v);
+        return swish_back(dv, i - 1, rows, v.ab.gout[i - 1], ldo, &v.ab, row_at(dst, r0, dst_ld, es), dst_ld, s);
+      });
+    }
+    return mlp_layer_dgrad(d, i, B, g, gs, dst, dst_ld, i > 0 ? acts[i - 1] : nullptr,
+                           i > 0 ? strides[i - 1] : 0, ws, s, grp);
+  }
   const bool split = untied(d, i) || (i > 0 && untied(d, i - 1));
   return per_domain(d, dom, split, B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
     RowView v;
@@ -934,6 +983,8 @@ static hipError_t chain_step_all(const lattice_mlp_desc* d, const Domains* dom, 
 static hipError_t wgrad_all(const lattice_mlp_desc* d, const Domains* dom, int i, int B, const void* g,
                             int64_t gs, const void* in_i, int64_t ld_in, void* ws, hipStream_t s) {
   const int64_t es = (int64_t)esize(d->dtype);
+  if (const Domains* grp = gemm_groups(d, i, dom))
+    return mlp_layer_wgrad(d, i, B, g, gs, in_i, ld_in, ws, s, grp);
   return per_domain(d, dom, untied(d, i), B, [&](const lattice_mlp_desc* dv, int64_t r0, int rows) {
     return mlp_layer_wgrad(dv, i, rows, row_at(g, r0, gs, es), gs, row_at(in_i, r0, ld_in, es), ld_in,
                            ws, s);

@@ -386,8 +386,22 @@ __device__ inline void mma_k64(const bf16_t* As, const bf16_t* Bs, int wm, int w
   }
 }
 
+// Grouped products (parameter untying): blockIdx.z = group.  Rows (gk = 0):
+// group z is rows off[z] .. off[z+1]-1 of A, C and the epilogue operands,
+// with its own B operand (+ z sB), bias (+ z N) and gains (+ z 2N); blocks
+// past a group's rows exit at once.  K (gk = 1): group z sums k = off[z] ..
+// off[z+1]-1 into its own C (+ z sC) and row sums (+ z M).
+constexpr int GEMM_MAX_GROUPS = 16;
+struct GroupSpec {
+  int n;    // 0: not grouped
+  int gk;
+  int off[GEMM_MAX_GROUPS + 1];
+  int64_t sB, sC;
+};
+
 // grid: x = M tiles * N tiles (renumbered per XCD), z = split index (split-K)
-// or batch index (batched; never both).  vec: 16-byte epilogue vectors allowed.
+// or batch index (batched) or group (grouped; never two of them).  vec:
+// 16-byte epilogue vectors allowed.
 // rowsum (optional, not batched): rowsum[m] = sum over k of A[m][k], added in
 // k order by the blocks of the first N tile from their LDS A tiles; with
 // split-K each split's sum goes to rs_partial[split][m].
@@ -395,7 +409,7 @@ template <bool TA, bool TB, bool VA, bool VB, typename CT, int NORM = 0>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     Opnd A, Opnd Bm, CT* __restrict__ C, int64_t ldc, int M, int N, int K, int k_per_split,
     float* __restrict__ partial, Epi epi, int64_t sA, int64_t sB, int64_t sC, int batched, int vec,
-    float* __restrict__ rowsum, float* __restrict__ rs_partial) {
+    float* __restrict__ rowsum, float* __restrict__ rs_partial, GroupSpec grp) {
   extern __shared__ __attribute__((aligned(16))) unsigned char gemm_smem[];
   bf16_t* As[2];
   bf16_t* Bs[2];
@@ -414,8 +428,33 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
     Bm.p += bz * sB;
     C += bz * sC;
   }
-  const int kbeg = batched ? 0 : blockIdx.z * k_per_split;
-  const int kend = batched ? K : min(K, kbeg + k_per_split);
+  int kbeg = batched ? 0 : blockIdx.z * k_per_split;
+  int kend = batched ? K : min(K, kbeg + k_per_split);
+  if (grp.n > 0) {
+    const int gz = blockIdx.z;
+    Bm.p += gz * grp.sB;
+    if (grp.gk) {
+      kbeg = grp.off[gz];
+      kend = grp.off[gz + 1];
+      C += gz * grp.sC;
+      if (rowsum) rowsum += (int64_t)gz * M;
+    } else {
+      kbeg = 0;  // (blockIdx.z is the group, not a split index)
+      kend = K;
+      const int r0 = grp.off[gz];
+      M = grp.off[gz + 1] - r0;
+      if (m0 >= M) return;  // the whole block: past this group's rows
+      A.p += TA ? (int64_t)r0 : (int64_t)r0 * A.ld;
+      C += (int64_t)r0 * ldc;
+      if (epi.bias) epi.bias += (int64_t)gz * N;
+      if (epi.gain) epi.gain += (int64_t)gz * 2 * N;
+      if (epi.pre) epi.pre = reinterpret_cast<CT*>(epi.pre) + (int64_t)r0 * epi.ldp;
+      if (epi.rinv) epi.rinv += (int64_t)r0 * epi.nblk;
+      if (epi.mask)
+        epi.mask = reinterpret_cast<const char*>(epi.mask) + (int64_t)r0 * epi.ldm * (epi.mask_dt == DT_BF16 ? 2 : 4);
+      if (epi.addend) epi.addend += (int64_t)r0 * epi.ld_add;
+    }
+  }
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -877,7 +916,7 @@ static int epi_vec_ok(const GemmArgs& g) {
 // kernel runs waves of 256 tiles (one per CU, no split) of four times the
 // work at about 1.3x the rate, 3.08K per wave.
 static bool gemm_use_big(const GemmArgs& g) {
-  if (g.batch > 1) return false;
+  if (g.batch > 1 || g.ngroups > 0) return false;
   const int64_t s = gemm_splits(g);
   const int64_t big_waves = cdiv((int64_t)cdiv(g.M, BBM) * cdiv(g.N, BBN), 256);
   const int64_t small_waves = cdiv((int64_t)cdiv(g.M, GBM) * cdiv(g.N, GBN) * s, 512);
@@ -923,7 +962,19 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
   int kps = (g.K + splits - 1) / splits;
   kps = ((kps + GBK - 1) / GBK) * GBK;
   const int batched = g.batch > 1 ? 1 : 0;
-  dim3 grid(cdiv(g.N, GBN) * cdiv(g.M, GBM), 1, batched ? g.batch : splits);
+  GroupSpec grp{};
+  int grid_m = g.M;
+  if (g.ngroups > 0) {
+    grp.n = g.ngroups;
+    grp.gk = g.gk;
+    grp.sB = g.gsB;
+    grp.sC = g.gsC;
+    int maxrows = 0;
+    for (int i = 0; i <= g.ngroups; ++i) grp.off[i] = (int)g.goff[i];
+    for (int i = 0; i < g.ngroups; ++i) maxrows = std::max(maxrows, grp.off[i + 1] - grp.off[i]);
+    if (!g.gk) grid_m = std::max(maxrows, 1);
+  }
+  dim3 grid(cdiv(g.N, GBN) * cdiv(grid_m, GBM), 1, g.ngroups > 0 ? g.ngroups : (batched ? g.batch : splits));
   Epi epi = make_epi(g);
   Opnd a{(const bf16_t*)g.A, g.lda, g.kseg, g.ksA};
   Opnd b{(const bf16_t*)g.B, g.ldb, g.kseg, g.ksB};
@@ -938,14 +989,14 @@ static hipError_t gemm_bf16_launch(const GemmArgs& g, float* ws, hipStream_t st)
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
     });
     k<<<grid, 256, GEMM_LDS, st>>>(a, b, (bf16_t*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA,
-                                   g.sB, g.sC, batched, vec, g.rowsum, rs_partial);
+                                   g.sB, g.sC, batched, vec, g.rowsum, rs_partial, grp);
   } else {
     auto k = gemm_bf16_kernel<TA, TB, VA, VB, float, NORM>;
     std::call_once(once_f, [&] {
       (void)hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS);
     });
     k<<<grid, 256, GEMM_LDS, st>>>(a, b, (float*)g.C, g.ldc, g.M, g.N, g.K, kps, partial, epi, g.sA,
-                                   g.sB, g.sC, batched, vec, g.rowsum, rs_partial);
+                                   g.sB, g.sC, batched, vec, g.rowsum, rs_partial, grp);
   }
   LAT_LAUNCH_CHECK();
   if (splits > 1) {
@@ -982,8 +1033,18 @@ static hipError_t gemm_bf16_dispatch(const GemmArgs& g, float* ws, hipStream_t s
   return gemm_bf16_launch<TA, TB, false, false, NORM>(g, ws, st);
 }
 
-hipError_t gemm(const GemmArgs& g, void* ws, hipStream_t st) {
+hipError_t gemm(const GemmArgs& g0, void* ws, hipStream_t st) {
+  GemmArgs g = g0;
   if (g.M == 0 || g.N == 0 || g.batch == 0) return hipSuccess;
+  if (g.ngroups > 0) {
+    if (g.dt != DT_BF16 || g.batch > 1 || g.kseg || g.ngroups > GEMM_MAX_GROUPS || !g.goff ||
+        g.goff[0] != 0 || g.goff[g.ngroups] != (g.gk ? g.K : g.M)) {
+      set_error("grouped GEMM: bf16, not batched, at most %d groups covering %s", GEMM_MAX_GROUPS,
+                g.gk ? "K" : "M");
+      return hipErrorInvalidValue;
+    }
+    g.max_splits = 1;  // each group's K range or rows in one pass
+  }
   if (g.accumulate && g.c_dt != DT_F32) {
     set_error("accumulating GEMM needs an fp32 output");
     return hipErrorInvalidValue;

@@ -67,6 +67,14 @@ struct GemmArgs {
   // 2 = hard sigmoid; gain [2, N] (g_a; g_b); pre [M, ldp] receives h =
   // acc + bias in C's dtype, rinv [M, nblk = ceil(N / 128)] each group's
   // 1 / sqrt(mean h^2 + eps)
+  // Grouped product (parameter untying), bf16 only: ngroups groups with
+  // host offsets goff[0..ngroups] over the rows of A and C (gk = 0; B, bias
+  // and gains per group, B + z gsB) or over K (gk = 1; C + z gsC, row sums
+  // + z M).  At most 16 groups.
+  int ngroups = 0;
+  const int64_t* goff = nullptr;
+  int gk = 0;
+  int64_t gsB = 0, gsC = 0;
   int norm_gate = 0;
   const float* gain = nullptr;
   float eps = 0.f;
