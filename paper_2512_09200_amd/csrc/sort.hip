@@ -8,9 +8,12 @@
 // of 8192 items is ranked with wave ballots (items with equal digits keep
 // their order), its digit counts are published, and its output offsets come
 // from the segment's digit bases plus the counts of the segment's earlier
-// tiles, read by decoupled look-back over the tiles' published counts (tiles
-// take their ids in the order they start, so every tile looked back at is
-// running and publishes without waiting).
+// tiles, read by decoupled look-back over the tiles' published counts (the
+// single-pass prefix scan of Merrill and Garland, "Single-pass Parallel
+// Prefix Scan with Decoupled Look-back", NVIDIA technical report NVR-2016-002,
+// implemented here from its description; tiles take their ids in the order
+// they start, so every tile looked back at is running and publishes without
+// waiting).
 #include "common.h"
 #include "kernels.h"
 
