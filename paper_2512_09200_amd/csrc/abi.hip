@@ -794,47 +794,66 @@ static hipError_t mlp_forward(const lattice_mlp_desc* d, int B, const void* in, 
   return hipSuccess;
 }
 
-// FP8 forward of hidden ReLU layers (bf16 model): per layer, the input and
-// the weights quantised row-wise to e4m3, then the FP8 GEMM with bias and
-// ReLU into the layer's bf16 activation.  Workspace: codes of the widest
-// input [B, ldq] and weights [out, ldq], and their scales.
+// FP8 forward of hidden ReLU layers (bf16 model): the input and every
+// layer's weights quantised row-wise to e4m3 in one launch, then per layer
+// the FP8 GEMM with bias and ReLU into the layer's bf16 activation, and the
+// next layer's input quantised.  Workspace: codes of the widest input
+// [B, ldq] and its scales (reused layer after layer), then each layer's
+// weight codes [out, ldq] and scales.
 static int64_t fp8_ldq(int cols) { return ((int64_t)cols + 15) / 16 * 16; }
 
-static size_t fp8_mlp_workspace(const lattice_mlp_desc* d, int B) {
-  int64_t kmax = 1, nmax = 1;
+struct Fp8MlpWs {
+  uint8_t* qa;
+  float* sa;
+  uint8_t* qw[LATTICE_MAX_LAYERS];
+  float* sw[LATTICE_MAX_LAYERS];
+  size_t bytes;
+};
+
+static Fp8MlpWs fp8_mlp_ws(const lattice_mlp_desc* d, int B, void* ws) {
+  int64_t kmax = 1;
+  for (int i = 0; i < d->n_layers; ++i) kmax = std::max<int64_t>(kmax, fp8_ldq(d->layers[i].in_dim));
+  Fp8MlpWs w{};
+  char* base = (char*)ws;
+  size_t o = 0;
+  w.qa = (uint8_t*)(base + o); o += al256((size_t)B * kmax);
+  w.sa = (float*)(base + o);   o += al256((size_t)B * 4);
   for (int i = 0; i < d->n_layers; ++i) {
-    kmax = std::max<int64_t>(kmax, fp8_ldq(d->layers[i].in_dim));
-    nmax = std::max<int64_t>(nmax, d->layers[i].out_dim);
+    const lattice_linear& L = d->layers[i];
+    w.qw[i] = (uint8_t*)(base + o); o += al256((size_t)L.out_dim * fp8_ldq(L.in_dim));
+    w.sw[i] = (float*)(base + o);   o += al256((size_t)L.out_dim * 4);
   }
-  return al256((size_t)B * kmax) + al256((size_t)nmax * kmax) + al256((size_t)B * 4) + al256((size_t)nmax * 4);
+  w.bytes = o;
+  return w;
 }
+
+static size_t fp8_mlp_workspace(const lattice_mlp_desc* d, int B) { return fp8_mlp_ws(d, B, nullptr).bytes; }
 
 static hipError_t mlp_forward_fp8(const lattice_mlp_desc* d, int B, const void* in, int64_t in_stride,
                                   void* const* acts, const int64_t* strides, void* ws, int fast,
                                   hipStream_t s) {
-  int64_t kmax = 1, nmax = 1;
-  for (int i = 0; i < d->n_layers; ++i) {
-    kmax = std::max<int64_t>(kmax, fp8_ldq(d->layers[i].in_dim));
-    nmax = std::max<int64_t>(nmax, d->layers[i].out_dim);
-  }
-  char* p = (char*)ws;
-  uint8_t* qa = (uint8_t*)p; p += al256((size_t)B * kmax);
-  uint8_t* qw = (uint8_t*)p; p += al256((size_t)nmax * kmax);
-  float* sa = (float*)p; p += al256((size_t)B * 4);
-  float* sw = (float*)p;
+  const Fp8MlpWs w = fp8_mlp_ws(d, B, ws);
+  static_assert(LATTICE_MAX_LAYERS + 1 <= FP8_MAX_JOBS, "input and every weight in one launch");
+  Fp8RowJob jobs[FP8_MAX_JOBS];
+  int nj = 0;
+  jobs[nj++] = Fp8RowJob{in, in_stride, B, d->layers[0].in_dim, w.qa, fp8_ldq(d->layers[0].in_dim), w.sa};
   for (int i = 0; i < d->n_layers; ++i) {
     const lattice_linear& L = d->layers[i];
-    const void* x = i == 0 ? in : acts[i - 1];
-    const int64_t ldx = i == 0 ? in_stride : strides[i - 1];
-    const int64_t ldq = fp8_ldq(L.in_dim);
-    hipError_t e = fp8_quantize(x, DT_BF16, B, L.in_dim, ldx, 1, qa, ldq, sa, nullptr, s);
-    if (e == hipSuccess) e = fp8_quantize(L.W, DT_BF16, L.out_dim, L.in_dim, L.in_dim, 1, qw, ldq, sw, nullptr, s);
-    if (e == hipSuccess)
-      e = gemm_fp8(qa, ldq, sa, 1, qw, ldq, sw, 1, L.b, acts[i], DT_BF16, strides[i], B, L.out_dim,
-                   L.in_dim, 1, fast, s);
-    if (e != hipSuccess) return e;
+    jobs[nj++] = Fp8RowJob{L.W, L.in_dim, L.out_dim, L.in_dim, w.qw[i], fp8_ldq(L.in_dim), w.sw[i]};
   }
-  return hipSuccess;
+  hipError_t e = fp8_quantize_rows(DT_BF16, jobs, nj, s);
+  for (int i = 0; i < d->n_layers && e == hipSuccess; ++i) {
+    const lattice_linear& L = d->layers[i];
+    const int64_t ldq = fp8_ldq(L.in_dim);
+    if (i > 0) {
+      const Fp8RowJob a{acts[i - 1], strides[i - 1], B, L.in_dim, w.qa, ldq, w.sa};
+      e = fp8_quantize_rows(DT_BF16, &a, 1, s);
+      if (e != hipSuccess) break;
+    }
+    e = gemm_fp8(w.qa, ldq, w.sa, 1, w.qw[i], ldq, w.sw[i], 1, L.b, acts[i], DT_BF16, strides[i], B,
+                 L.out_dim, L.in_dim, 1, fast, s);
+  }
+  return e;
 }
 
 // Weight and bias gradients of layer i: dW = gᵀ · in (fp32), db = Σ_b g.

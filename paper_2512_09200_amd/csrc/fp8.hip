@@ -6,8 +6,15 @@
 // (row-wise) or over the whole matrix (tensor-wise), s = 1 for an all-zero
 // row / matrix, r = 1 / s, and q = e4m3(x * r) with s, r and x * r fp32
 // (correctly rounded) and the product rounded to the nearest e4m3 value, ties
-// to even, saturating at +-448.  Codes are stored row-major with a row stride of ldq bytes (a
-// multiple of 16); bytes past cols are written as zeros.
+// to even, saturating at +-448.  The rounding is the hardware conversion
+// (v_cvt_pk_fp8_f32), measured on gfx950 to give round-to-nearest-even
+// e4m3 codes for every finite fp32 value of magnitude up to 448 (1 + 2^-20)
+// (|x * r| stays below 448 (1 + 2^-22)); the product is clamped to +-448
+// first, so an overflowing reciprocal scale saturates as well.  Codes are
+// stored row-major with a row stride of ldq bytes (a multiple of 16); bytes
+// past cols are written as zeros.  Several matrices of one dtype can be
+// quantised row-wise in one launch (the forward of an FP8 MLP quantises its
+// input and every layer's weights together).
 //
 // Linear layer: Y[m, n] = act( (sum_k qa[m,k] qw[n,k]) * sa[m] * sw[n] + b[n] )
 // with the contraction on v_mfma_scale_f32_32x32x64_f8f6f4 (fp8 x fp8, unit
@@ -34,27 +41,13 @@ namespace lat {
 
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
-// fp32 -> e4m3 code, round to nearest even, saturating at the largest
-// finite value (448).  Input must be finite.
-__device__ inline uint32_t e4m3_rne(float v) {
-  const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
-  const float a = fabsf(v);
-  uint32_t code;
-  if (a >= 0.015625f) {                                  // normal e4m3: a >= 2^-6
-    const int e = (int)((__float_as_uint(a) >> 23) & 0xffu) - 127;   // floor(log2 a)
-    // q in [8, 16]: the significand scaled to 3 fraction bits, rounded
-    float q = rintf(__uint_as_float(__float_as_uint(a) - ((uint32_t)(e - 3) << 23)));
-    int ee = e;
-    if (q >= 16.f) {
-      q = 8.f;
-      ++ee;
-    }
-    code = ee > 8 ? 0x7eu : ((uint32_t)(ee + 7) << 3) | ((uint32_t)q - 8u);
-    code = code > 0x7eu ? 0x7eu : code;                  // 448
-  } else {
-    code = (uint32_t)rintf(a * 512.f);                   // subnormal steps of 2^-9 (8 -> 2^-6)
-  }
-  return sign | code;
+// Four fp32 values (already scaled) -> four e4m3 codes in one word, byte e
+// = value e: round to nearest even, saturating at +-448.
+__device__ inline uint32_t e4m3x4(float a, float b, float c, float d) {
+  auto cl = [](float v) { return __builtin_amdgcn_fmed3f(v, -448.f, 448.f); };
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(a), cl(b), 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(cl(c), cl(d), w, true);
+  return (uint32_t)w;
 }
 
 __device__ inline float wave_max(float v) {
@@ -71,19 +64,25 @@ __device__ inline float ldf(const IT* p) { return ld(p); }
 // elements), its amax reduced across the wave, then the codes written 8 per
 // lane-step.  Longer rows take the generic loop.  Tensor-wise: the same
 // kernel with a given scale (scale_in), after the two amax kernels below.
+// A launch covers the jobs of Fp8Jobs, job k taking blocks blk0[k] ..
+// blk0[k+1]-1 (four rows per block).
 template <typename IT, bool ROWWISE>
-__global__ __launch_bounds__(256) void fp8_quant_kernel(const IT* __restrict__ x, int64_t ld,
-                                                        int rows, int cols,
-                                                        uint8_t* __restrict__ q, int64_t ldq,
-                                                        float* __restrict__ scales,
-                                                        const float* __restrict__ scale_in) {
+__global__ __launch_bounds__(256) void fp8_quant_kernel(Fp8Jobs J, const float* __restrict__ scale_in) {
   constexpr int RV = 6;                      // 8-element chunks per lane kept in registers
   const int lane = threadIdx.x & 63;
-  const int row = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  int k = 0;
+#pragma unroll
+  for (int t = 1; t < FP8_MAX_JOBS; ++t)
+    if (t < J.n && (int)blockIdx.x >= J.blk0[t]) k = t;
+  const Fp8RowJob& jb = J.j[k];
+  const int rows = jb.rows, cols = jb.cols;
+  const int64_t ld = jb.ld, ldq = jb.ldq;
+  const int row = __builtin_amdgcn_readfirstlane(((int)blockIdx.x - J.blk0[k]) * 4 + (threadIdx.x >> 6));
   if (row >= rows) return;
-  const IT* xr = x + (int64_t)row * ld;
-  uint8_t* qr = q + (int64_t)row * ldq;
-  const bool vec = cols >= 8 && (cols % 8 == 0) && (ld % 8 == 0) && ((uintptr_t)x % 16 == 0) && cols <= 64 * 8 * RV;
+  const IT* xr = static_cast<const IT*>(jb.x) + (int64_t)row * ld;
+  uint8_t* qr = jb.q + (int64_t)row * ldq;
+  float* scales = jb.scales;
+  const bool vec = cols >= 8 && (cols % 8 == 0) && (ld % 8 == 0) && ((uintptr_t)jb.x % 16 == 0) && cols <= 64 * 8 * RV;
   if (vec) {
     float v[RV][8];
     float m = 0.f;
@@ -121,12 +120,9 @@ __global__ __launch_bounds__(256) void fp8_quant_kernel(const IT* __restrict__ x
     for (int i = 0; i < RV; ++i) {
       const int c0 = (lane + 64 * i) * 8;
       if (c0 < cols) {
-        uint32_t w0 = 0, w1 = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          w0 |= e4m3_rne(v[i][e] * rs) << (8 * e);
-          w1 |= e4m3_rne(v[i][4 + e] * rs) << (8 * e);
-        }
+        const float* t = v[i];
+        const uint32_t w0 = e4m3x4(t[0] * rs, t[1] * rs, t[2] * rs, t[3] * rs);
+        const uint32_t w1 = e4m3x4(t[4] * rs, t[5] * rs, t[6] * rs, t[7] * rs);
         *reinterpret_cast<u32x2*>(qr + c0) = u32x2{w0, w1};
       }
     }
@@ -145,16 +141,12 @@ __global__ __launch_bounds__(256) void fp8_quant_kernel(const IT* __restrict__ x
     s = scale_in[0];
   }
   const float rs = 1.f / s;
-  // four codes per lane and step, written as one 32-bit word
+  // four codes per lane and step, written as one 32-bit word (zeros past cols)
   for (int c0 = lane * 4; c0 < ldq; c0 += 256) {
-    uint32_t w = 0;
+    float t[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int c = c0 + e;
-      const uint32_t code = c < cols ? e4m3_rne(ldf(xr + c) * rs) : 0u;
-      w |= code << (8 * e);
-    }
-    *reinterpret_cast<uint32_t*>(qr + c0) = w;
+    for (int e = 0; e < 4; ++e) t[e] = c0 + e < cols ? ldf(xr + c0 + e) * rs : 0.f;
+    *reinterpret_cast<uint32_t*>(qr + c0) = e4m3x4(t[0], t[1], t[2], t[3]);
   }
 }
 
@@ -195,18 +187,39 @@ constexpr int FP8_AMAX_BLOCKS = 1024;
 
 size_t fp8_quantize_workspace() { return (size_t)FP8_AMAX_BLOCKS * sizeof(float); }
 
+template <bool ROWWISE>
+static void fp8_quant_launch(DType xdt, const Fp8Jobs& J, int blocks, const float* scale_in, hipStream_t s) {
+  if (xdt == DT_BF16)
+    fp8_quant_kernel<bf16_t, ROWWISE><<<blocks, 256, 0, s>>>(J, scale_in);
+  else
+    fp8_quant_kernel<float, ROWWISE><<<blocks, 256, 0, s>>>(J, scale_in);
+}
+
+hipError_t fp8_quantize_rows(DType xdt, const Fp8RowJob* jobs, int njobs, hipStream_t s) {
+  if (njobs < 1 || njobs > FP8_MAX_JOBS) {
+    set_error("fp8_quantize_rows: 1 .. %d matrices per launch", FP8_MAX_JOBS);
+    return hipErrorInvalidValue;
+  }
+  Fp8Jobs J{};
+  int blocks = 0;
+  for (int k = 0; k < njobs; ++k) {
+    J.j[J.n] = jobs[k];
+    J.blk0[J.n] = blocks;
+    if (jobs[k].rows <= 0) continue;
+    blocks += cdiv(jobs[k].rows, 4);
+    ++J.n;
+  }
+  if (blocks == 0) return hipSuccess;
+  fp8_quant_launch<true>(xdt, J, blocks, nullptr, s);
+  LAT_LAUNCH_CHECK();
+  return hipSuccess;
+}
+
 hipError_t fp8_quantize(const void* x, DType xdt, int rows, int cols, int64_t ld, int rowwise,
                         uint8_t* q, int64_t ldq, float* scales, void* ws, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  const int grid = cdiv(rows, 4);
-  if (rowwise) {
-    if (xdt == DT_BF16)
-      fp8_quant_kernel<bf16_t, true><<<grid, 256, 0, s>>>((const bf16_t*)x, ld, rows, cols, q, ldq, scales, nullptr);
-    else
-      fp8_quant_kernel<float, true><<<grid, 256, 0, s>>>((const float*)x, ld, rows, cols, q, ldq, scales, nullptr);
-    LAT_LAUNCH_CHECK();
-    return hipSuccess;
-  }
+  const Fp8RowJob job{x, ld, rows, cols, q, ldq, scales};
+  if (rowwise) return fp8_quantize_rows(xdt, &job, 1, s);
   float* part = static_cast<float*>(ws);
   const int64_t n = (int64_t)rows * cols;
   int pg = cdiv(n, 256);
@@ -218,10 +231,10 @@ hipError_t fp8_quantize(const void* x, DType xdt, int rows, int cols, int64_t ld
   LAT_LAUNCH_CHECK();
   fp8_amax_final_kernel<<<1, 256, 0, s>>>(part, pg, scales);
   LAT_LAUNCH_CHECK();
-  if (xdt == DT_BF16)
-    fp8_quant_kernel<bf16_t, false><<<grid, 256, 0, s>>>((const bf16_t*)x, ld, rows, cols, q, ldq, nullptr, scales);
-  else
-    fp8_quant_kernel<float, false><<<grid, 256, 0, s>>>((const float*)x, ld, rows, cols, q, ldq, nullptr, scales);
+  Fp8Jobs J{};
+  J.j[0] = Fp8RowJob{x, ld, rows, cols, q, ldq, nullptr};
+  J.n = 1;
+  fp8_quant_launch<false>(xdt, J, cdiv(rows, 4), scales, s);
   LAT_LAUNCH_CHECK();
   return hipSuccess;
 }
@@ -289,27 +302,47 @@ __device__ inline void mma_fp8_k128(const uint8_t* As, const uint8_t* Bs, int wm
     return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
   };
   const f32x16 zero = {};
+  if constexpr (PRECISE) {
+    // all four fragments' two chained halves from zero first, then their
+    // fp32 adds: the adds of one fragment overlap the MFMAs of the others
+    f32x16 c[2][2];
+    i32x8 a1[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const i32x8 a0 = opnd(as + i * 32 * F8LD);
+      a1[i] = opnd(as + i * 32 * F8LD + 64);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        c[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a0, opnd(bs + j * 32 * F8LD), zero,
+                                                                 0, 0, 0, 127, 0, 127);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const i32x8 b1 = opnd(bs + j * 32 * F8LD + 64);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        c[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a1[i], b1, c[i][j], 0, 0, 0, 127, 0, 127);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] += c[i][j][r];
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     // one 32-row fragment of A against both of B: the k = 0..63 and 64..127
-    // halves chained (precise: from zero, then one fp32 add per 128 k)
+    // halves chained through the accumulator
     const i32x8 a0 = opnd(as + i * 32 * F8LD), a1 = opnd(as + i * 32 * F8LD + 64);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const i32x8 b0 = opnd(bs + j * 32 * F8LD), b1 = opnd(bs + j * 32 * F8LD + 64);
       // formats 0 / 0: e4m3 operands; E8M0 block scales 127 = 2^0
-      f32x16 c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a0, b0, PRECISE ? zero : acc[i][j],
-                                                                  0, 0, 0, 127, 0, 127);
-      c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a1, b1, c, 0, 0, 0, 127, 0, 127);
-      if (PRECISE) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] += c[r];
-      } else {
-        acc[i][j] = c;
-      }
+      f32x16 c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a0, b0, acc[i][j], 0, 0, 0, 127, 0, 127);
+      acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a1, b1, c, 0, 0, 0, 127, 0, 127);
     }
-    // the precise mode keeps one fragment's operands live at a time
-    if (PRECISE) __builtin_amdgcn_sched_barrier(0);
   }
 }
 

@@ -191,6 +191,22 @@ hipError_t head_bwd(const float* z, const float* y, const uint8_t* m, int B, int
 
 // fp8.hip (OCP e4m3 linear layers, tensor- or row-wise scales)
 size_t fp8_quantize_workspace();
+// one matrix of a row-wise quantisation launch (codes q [rows, ldq], scales [rows])
+struct Fp8RowJob {
+  const void* x;
+  int64_t ld;
+  int rows, cols;
+  uint8_t* q;
+  int64_t ldq;
+  float* scales;
+};
+constexpr int FP8_MAX_JOBS = 9;
+struct Fp8Jobs {
+  Fp8RowJob j[FP8_MAX_JOBS];
+  int blk0[FP8_MAX_JOBS];
+  int n;
+};
+hipError_t fp8_quantize_rows(DType xdt, const Fp8RowJob* jobs, int njobs, hipStream_t s);
 hipError_t fp8_quantize(const void* x, DType xdt, int rows, int cols, int64_t ld, int rowwise,
                         uint8_t* q, int64_t ldq, float* scales, void* ws, hipStream_t s);
 hipError_t gemm_fp8(const uint8_t* A, int64_t lda, const float* sa, int sa_rowwise, const uint8_t* B,
