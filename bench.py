@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--lcb-n", type=int, default=0,
                     help="stacked workloads: output vectors of each fusion block's linear compression "
                          "block (full DHEN/Wukong fusion blocks; 0: FM block only)")
+    ap.add_argument("--no-skip-absent", action="store_true",
+                    help="multi-domain DOT: compute the slots of absent features too (control run)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, stream 1 GiB through a plain elementwise kernel "
                          "(torch.neg, 1 GiB read + 1 GiB written) as a counter calibration point")
@@ -151,13 +153,15 @@ def main():
                 if d[k] is not None:
                     d["d" + k] = torch.empty(tuple(d[k].shape), device=dev)
             stack.append(d)
+    # multi-domain batches leave whole features absent: the DOT forward skips them
+    skip_absent = cfg.interact == "dot" and cfg.domains is not None and not args.no_skip_absent
     model = api.StepModel(tables=E, row_base=row_base, num_features=cfg.F, dense_in=cfg.dense_in,
                           max_rows=cfg.rows,
                           bottom=bottom, top=top, interact=cfg.interact, fm_W=fm_W, fm_dW=fm_dW,
                           pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps,
                           top_act=cfg.top_act, norm_block=cfg.norm_block, norm_eps=cfg.norm_eps,
                           towers=bool(cfg.towers), n_domains=len(cfg.domains[0]) if cfg.untie else 0,
-                          untied_layers=cfg.untie)
+                          untied_layers=cfg.untie, skip_absent=skip_absent)
     nnz_max = max(b["nnz"] for b in batches)
     lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False, fp8_top=args.fp8)
     ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
@@ -326,6 +330,7 @@ def main():
                    "lcb_n": cfg.lcb_n if cfg.interact == "stack" else None,
                    "towers": cfg.towers or None,
                    "untied_top_layers": cfg.untie or None,
+                   "dot_skip_absent": skip_absent or None,
                    "norm_block": cfg.norm_block if cfg.top_act != "relu" else None,
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,

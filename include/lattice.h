@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 7
+#define LATTICE_ABI_VERSION 8
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -201,6 +201,20 @@ typedef struct {
   const lattice_stack_layer* layers;  /* host [n_layers] */
   int32_t lcb_n;         /* STACK: output vectors of each layer's linear compression
                             block (0: FM block only; < stack_n) */
+  const uint32_t* slot_mask; /* DOT, optional: device [B, 4] per-sample bitmask (16-byte
+                            aligned), bit s of word s/32 set when slot s may be
+                            non-zero (bits >= n ignored).  The caller guarantees
+                            that every slot whose bit is clear holds a zero vector
+                            (absent features are zero-padded, Section 3.2); the
+                            forward then skips those slots (their pairs are written
+                            as 0), with results equal to the full computation's;
+                            the backward computes every slot.  Needs n <= 128;
+                            NULL: every slot is computed.  lattice_step builds its
+                            own (see skip_absent): leave NULL in the model. */
+  int32_t skip_absent;   /* DOT in lattice_step: 1 when whole features may be absent from
+                            a sample (empty bags, as in multi-domain batches, Section
+                            3.2): the step builds each sample's slot mask from the
+                            batch and the forward skips the empty slots; 0: none */
 } lattice_interact_desc;
 
 /* DOT: out[b, m(i,j)] = <X[b,i], X[b,j]> for i<j, m(i,j) row-major over the

@@ -48,7 +48,8 @@ class lattice_interact_desc(Structure):
     _fields_ = [("kind", c_int), ("dtype", c_int), ("n", c_int32), ("dim", c_int32),
                 ("rank", c_int32), ("emit_slot0", c_int32), ("fm_W", c_void_p),
                 ("fm_dW", c_void_p), ("n_layers", c_int32), ("stack_n", c_int32),
-                ("ln_eps", c_float), ("layers", POINTER(lattice_stack_layer)), ("lcb_n", c_int32)]
+                ("ln_eps", c_float), ("layers", POINTER(lattice_stack_layer)), ("lcb_n", c_int32),
+                ("slot_mask", c_void_p), ("skip_absent", c_int32)]
 
 
 class lattice_linear(Structure):

@@ -157,8 +157,9 @@ def _lcb_n(stack):
 
 
 def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0, stack=None, stack_n=0,
-                  ln_eps=1e-5):
-    """stack: list of layer dicts (see stack_layers) for kind "stack"."""
+                  ln_eps=1e-5, slot_mask=None):
+    """stack: list of layer dicts (see stack_layers) for kind "stack";
+    slot_mask (DOT): int32 [B, 4] device tensor of per-sample slot bits."""
     arr = stack_layers(stack) if stack else None
     if stack:
         rank = stack[0]["W"].shape[1]
@@ -166,17 +167,19 @@ def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0, stack=None
                                 rank=(fm_W.shape[1] if fm_W is not None else rank),
                                 emit_slot0=int(emit_slot0), fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
                                 n_layers=len(stack) if stack else 0, stack_n=stack_n,
-                                ln_eps=ln_eps, layers=arr, lcb_n=_lcb_n(stack))
+                                ln_eps=ln_eps, layers=arr, lcb_n=_lcb_n(stack),
+                                slot_mask=_ptr(slot_mask))
     d._keep = arr
     return d
 
 
 def lattice_interact_fwd(kind, X, out, emit_slot0=False, fm_W=None, stream=None, stack=None,
-                         stack_n=0, ln_eps=1e-5):
+                         stack_n=0, ln_eps=1e-5, slot_mask=None):
     """Returns the workspace (saved state), which lattice_interact_bwd needs."""
-    _contig(X, fm_W)
+    _contig(X, fm_W, slot_mask)
     lib = load()
-    d = interact_desc(kind, X, emit_slot0, fm_W, stack=stack, stack_n=stack_n, ln_eps=ln_eps)
+    d = interact_desc(kind, X, emit_slot0, fm_W, stack=stack, stack_n=stack_n, ln_eps=ln_eps,
+                      slot_mask=slot_mask)
     wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
     check(lib.lattice_interact_fwd(byref(d), X.shape[0], _p(X), _p(out), _row_stride(out), _p(ws),
@@ -185,10 +188,11 @@ def lattice_interact_fwd(kind, X, out, emit_slot0=False, fm_W=None, stream=None,
 
 
 def lattice_interact_bwd(kind, X, d_out, dX, emit_slot0=False, fm_W=None, fm_dW=None, stream=None,
-                         stack=None, stack_n=0, ln_eps=1e-5, ws=None):
-    _contig(X, dX, fm_W, fm_dW)
+                         stack=None, stack_n=0, ln_eps=1e-5, ws=None, slot_mask=None):
+    _contig(X, dX, fm_W, fm_dW, slot_mask)
     lib = load()
-    d = interact_desc(kind, X, emit_slot0, fm_W, fm_dW, stack=stack, stack_n=stack_n, ln_eps=ln_eps)
+    d = interact_desc(kind, X, emit_slot0, fm_W, fm_dW, stack=stack, stack_n=stack_n, ln_eps=ln_eps,
+                      slot_mask=slot_mask)
     wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
     if ws is None:
         ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
@@ -333,12 +337,14 @@ class StepModel:
     for the top MLP's hidden layers; towers: the top MLP's last layer is the
     heads of per-objective towers (its W [T, H]); n_domains / untied_layers:
     the first untied_layers top layers hold one parameter set per domain
-    (lattice_step then takes the batch's domain_offsets)."""
+    (lattice_step then takes the batch's domain_offsets); skip_absent
+    (DOT): whole features may be absent from a sample (empty bags), so the
+    step's DOT forward skips the empty slots."""
 
     def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
                  fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5,
                  max_rows=None, top_act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6,
-                 towers=False, n_domains=0, untied_layers=0):
+                 towers=False, n_domains=0, untied_layers=0, skip_absent=False):
         _contig(tables, row_base)
         dt = _dt(tables)
         d = tables.shape[1]
@@ -353,7 +359,8 @@ class StepModel:
                                         emit_slot0=int(dense_in > 0 and interact != "stack"),
                                         fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
                                         n_layers=len(stack) if stack else 0, stack_n=stack_n,
-                                        ln_eps=ln_eps, layers=self._stack, lcb_n=_lcb_n(stack))
+                                        ln_eps=ln_eps, layers=self._stack, lcb_n=_lcb_n(stack),
+                                        skip_absent=int(bool(skip_absent)))
         self.desc = A.lattice_model_desc(dtype=dt, pool=_POOL[pool],
                                          tables=_tables(tables, row_base, max_rows),
                                          num_features=num_features, dense_in=dense_in,

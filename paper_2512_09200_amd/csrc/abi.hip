@@ -338,6 +338,13 @@ static lattice_status check_interact(const lattice_interact_desc* d, int32_t B) 
   REQUIRE(d->n >= 1 && d->dim >= 1, "bad n/dim");
   lattice_status st = check_dim(d->dim, d->dtype);
   if (st != LATTICE_OK) return st;
+  REQUIRE(d->skip_absent == 0 || d->skip_absent == 1, "skip_absent must be 0 or 1");
+  if (d->skip_absent) REQUIRE(d->kind == LATTICE_INTERACT_DOT, "skip_absent is for the DOT interaction only");
+  if (d->slot_mask) {
+    REQUIRE(d->kind == LATTICE_INTERACT_DOT, "slot_mask is for the DOT interaction only");
+    REQUIRE(d->n <= 128, "slot_mask needs n <= 128");
+    REQUIRE(((uintptr_t)d->slot_mask & 15) == 0, "slot_mask must be 16-byte aligned");
+  }
   if (d->kind == LATTICE_INTERACT_DOT) {
     if (dot_lds_bytes(d->n, d->dim) > 160 * 1024)
       FAIL(LATTICE_ERR_UNSUPPORTED, "DOT with n=%d, dim=%d exceeds LDS", d->n, d->dim);
@@ -387,6 +394,15 @@ static bool dot_uses_mfma(const lattice_interact_desc* d, const void* X) {
          ((uintptr_t)X & 3) == 0;
 }
 
+// bytes of the step's DOT slot masks (B x 4 words) when its DOT runs on MFMA
+static size_t step_dot_mask_bytes(const lattice_model_desc* m, int B) {
+  const lattice_interact_desc* d = &m->interact;
+  if (!d->skip_absent || d->kind != LATTICE_INTERACT_DOT || d->dtype != LATTICE_BF16 ||
+      !dot_mfma_supported(d->n, d->dim))
+    return 0;
+  return al256((size_t)B * 16);
+}
+
 static size_t interact_ws(const lattice_interact_desc* d, int B) {
   if (d->kind == LATTICE_INTERACT_STACK) return stack_plan(stack_shape(d), B).total_bytes;
   if (d->kind != LATTICE_INTERACT_FM) return 0;
@@ -402,7 +418,7 @@ static hipError_t interact_fwd_impl(const lattice_interact_desc* d, int B, const
   }
   if (d->kind == LATTICE_INTERACT_DOT) {
     if (dot_uses_mfma(d, X))
-      return dot_mfma(true, X, B, d->n, d->dim, out, os, d->emit_slot0, nullptr, 0, nullptr, s);
+      return dot_mfma(true, X, B, d->n, d->dim, out, os, d->emit_slot0, nullptr, 0, nullptr, d->slot_mask, s);
     return dot_fwd(dt_of(d->dtype), X, B, d->n, d->dim, out, os, d->emit_slot0, s);
   }
   if (fm_uses_mfma(d, os))
@@ -421,7 +437,7 @@ static hipError_t interact_bwd_impl(const lattice_interact_desc* d, int B, const
   }
   if (d->kind == LATTICE_INTERACT_DOT) {
     if (dot_uses_mfma(d, X))
-      return dot_mfma(false, X, B, d->n, d->dim, nullptr, 0, d->emit_slot0, dout, ds, dX, s);
+      return dot_mfma(false, X, B, d->n, d->dim, nullptr, 0, d->emit_slot0, dout, ds, dX, d->slot_mask, s);
     return dot_bwd(dt_of(d->dtype), X, B, d->n, d->dim, dout, ds, d->emit_slot0, dX, s);
   }
   if (fm_uses_mfma(d, ds))
@@ -1345,7 +1361,7 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
   sc = std::max(sc, bce_workspace((int64_t)B * P->T));
   sc = std::max(sc, head_workspace(B));
-  L.interact = take(interact_ws(&m->interact, B));
+  L.interact = take(interact_ws(&m->interact, B) + step_dot_mask_bytes(m, B));
   L.scratch = take(sc);
   L.scratch_bytes = (int64_t)sc;
   // the sparse gradient's scratch is its own: its first half may run on the
@@ -1518,7 +1534,15 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   else HIPRET(bottom_forward(s));
   // 3. interaction -> top input t = [X[:,0,:], interaction]
   HIPRET(begin(LATTICE_STAGE_INTERACT_FWD));
-  HIPRET(interact_fwd_impl(&m->interact, B, X, t, P.t_stride, at(L.interact), s));
+  lattice_interact_desc idesc = m->interact;
+  if (step_dot_mask_bytes(m, B)) {
+    // DOT with absent features: the slots whose bag is empty are zero
+    // vectors, which the forward skips
+    idesc.slot_mask = (const uint32_t*)at(L.interact);
+    HIPRET(dot_slot_mask(batch->bags.offsets, m->num_features, B, s0, m->dense_in > 0,
+                         (uint32_t*)at(L.interact), s));
+  }
+  HIPRET(interact_fwd_impl(&idesc, B, X, t, P.t_stride, at(L.interact), s));
   HIPRET(end(LATTICE_STAGE_INTERACT_FWD));
   // 4. top MLP -> logits; 5. masked BCE.  bf16 models with at most 64 heads
   // run the last layer as the fused heads: its forward with the loss
@@ -1604,7 +1628,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   // 7. interaction backward -> dX (slot 0 gets d_t[:, :d] added, then the bottom ReLU mask)
   HIPRET(begin(LATTICE_STAGE_INTERACT_BWD));
   void* dX = at(L.dX);
-  HIPRET(interact_bwd_impl(&m->interact, B, X, at(L.d_t), P.t_stride, dX, at(L.interact), s));
+  HIPRET(interact_bwd_impl(&idesc, B, X, at(L.d_t), P.t_stride, dX, at(L.interact), s));
   HIPRET(end(LATTICE_STAGE_INTERACT_BWD));
   // 8./9. The weight gradients of the top MLP and the bottom backward need
   // nothing the sparse gradient writes: on the side stream they overlap the

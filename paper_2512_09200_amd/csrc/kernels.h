@@ -140,7 +140,11 @@ hipError_t fm_mfma(bool fwd, const void* X, const void* W, int B, int n, int d, 
 // dot_mfma.hip (bf16 MFMA path of the DOT interaction)
 bool dot_mfma_supported(int n, int d);
 hipError_t dot_mfma(bool fwd, const void* X, int B, int n, int d, void* out, int64_t ostride,
-                    int emit0, const void* dout, int64_t dstride, void* dX, hipStream_t s);
+                    int emit0, const void* dout, int64_t dstride, void* dX, const uint32_t* mask,
+                    hipStream_t s);
+// per-sample DOT slot bitmasks (4 words) of a batch: the dense slot and the non-empty bags
+hipError_t dot_slot_mask(const int32_t* offsets, int F, int B, int first, int has0, uint32_t* mask,
+                         hipStream_t s);
 
 // stack.hip (stacked FM -> linear -> residual -> LayerNorm interaction)
 struct StackShape {

@@ -510,7 +510,8 @@ class Workload:
                              stack=self.stack, stack_n=c.stack_n, ln_eps=c.ln_eps,
                              top_act=c.top_act, norm_block=c.norm_block, norm_eps=c.norm_eps,
                              towers=bool(c.towers), n_domains=len(c.domains[0]) if c.untie else 0,
-                             untied_layers=c.untie)
+                             untied_layers=c.untie,
+                             skip_absent=c.interact == "dot" and c.domains is not None)
 
 
 def relu_overrides(cfg, params, table, batch, gpu_in, gpu_out, max_iter=4):

@@ -144,6 +144,21 @@ def test_interact_statuses(lib):
     # STACK layer 0 must have C when the vector count changes
     stc = interact_desc(kind=A.STACK, n=128, rank=64, layers=lay, n_layers=1, stack_n=64, emit=0, W=None)
     assert f(byref(stc), 16, FAKE, FAKE, 64 * 128, FAKE, 1 << 30, None) == INVALID_ARG
+    # the DOT slot mask: DOT only, n <= 128, 16-byte aligned
+    fm_mask = interact_desc()
+    fm_mask.slot_mask = FAKE
+    assert f(byref(fm_mask), 8, FAKE, FAKE, 1 << 20, None, 0, None) == INVALID_ARG
+    assert "slot_mask" in last_error(lib)
+    big = interact_desc(kind=A.DOT, n=129, dim=64, W=None)
+    big.slot_mask = FAKE
+    assert f(byref(big), 8, FAKE, FAKE, 1 << 20, None, 0, None) == INVALID_ARG
+    odd = interact_desc(kind=A.DOT, n=97, dim=128, W=None)
+    odd.slot_mask = FAKE + 4
+    assert f(byref(odd), 8, FAKE, FAKE, 1 << 20, None, 0, None) == INVALID_ARG
+    fm_skip = interact_desc()
+    fm_skip.skip_absent = 1
+    assert f(byref(fm_skip), 8, FAKE, FAKE, 1 << 20, None, 0, None) == INVALID_ARG
+    assert "skip_absent" in last_error(lib)
     # backward without the FM weight gradient
     nog = interact_desc()
     nog.fm_dW = None

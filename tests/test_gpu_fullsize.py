@@ -135,7 +135,8 @@ def test_fullsize_step(name):
     model = api.StepModel(tables=w.E, row_base=w.row_base, num_features=cfg.F, dense_in=cfg.dense_in,
                           bottom=w.bottom, top=w.top, interact=cfg.interact, fm_W=w.fm_W,
                           fm_dW=w.fm_dW, pool=cfg.pool, stack=w.stack, stack_n=cfg.stack_n,
-                          ln_eps=cfg.ln_eps, max_rows=cfg.rows)
+                          ln_eps=cfg.ln_eps, max_rows=cfg.rows,
+                          skip_absent=cfg.interact == "dot" and cfg.domains is not None)
     print("[fullsize-step] oracle bookkeeping", flush=True)
     bk = oe.bookkeeping(b["row_base"], b["offsets"], b["indices"], cfg.F, cfg.B)
     uniq, counts, seg = bk["unique_rows"], bk["counts"], bk["seg_offsets"]

@@ -56,9 +56,47 @@ def test_dot_unaligned_row_stride(pad):
     check_interact("dot", "bf16", 33, 97, 128, 0, True, False, pad=pad)
 
 
-def check_interact(kind, dt, B, n, d, k, emit0, zero_slots, pad=0):
+LISTED_CASES = {
+    # name: (B, n, d, emit0, fraction of zero slots, fraction of zero slots still listed, pad)
+    "n97-d128-multidomain": (600, 97, 128, True, 0.58, 0.0, 0),   # > 1 sample per block
+    "n97-d128-few-absent": (70, 97, 128, True, 0.1, 0.0, 0),      # 3 or 4 compact tiles
+    "n27-d64": (130, 27, 64, False, 0.4, 0.0, 0),
+    "n128-d64-all-listed": (40, 128, 64, True, 0.0, 0.0, 0),
+    "n97-d128-zero-rows-listed": (50, 97, 128, True, 0.5, 0.5, 0),  # mask wider than the zeros
+    "n97-d128-nothing-listed": (33, 97, 128, True, 1.0, 0.0, 0),   # every slot zero, mask empty
+    "n97-d128-stride-pad": (45, 97, 128, True, 0.58, 0.0, 3),
+    "n33-d128": (65, 33, 128, False, 0.3, 0.0, 0),
+}
+
+
+def _slot_mask(X, listed_zero, seed=6):
+    """int32 [B, 4] bitmask: bit s set where slot s is non-zero, and for a
+    fraction of the zero slots as well."""
+    B, n = X.shape[:2]
+    on = np.any(X != 0, axis=2)
+    on |= np.random.default_rng(seed).random((B, n)) < listed_zero
+    words = np.zeros((B, 4), np.uint64)
+    for s_ in range(n):
+        words[:, s_ // 32] |= on[:, s_].astype(np.uint64) << np.uint64(s_ % 32)
+    return torch.from_numpy(words.astype(np.uint32).view(np.int32).copy()).to(DEV)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(LISTED_CASES))
+def test_dot_listed_slots(name):
+    """DOT with a per-sample slot mask (the kernels skip the unlisted, zero
+    slots): equal to the oracle's full computation, pairs and every dX row."""
+    B, n, d, emit0, zf, lz, pad = LISTED_CASES[name]
+    print(f"[interact] dot listed {name}", flush=True)
+    check_interact("dot", "bf16", B, n, d, 0, emit0, zf, pad=pad, listed_zero=lz)
+
+
+def check_interact(kind, dt, B, n, d, k, emit0, zero_slots, pad=0, listed_zero=None):
     """Forward and backward of one interaction against the oracle; output
-    rows of stride `stride + pad` (a column slice of a wider buffer)."""
+    rows of stride `stride + pad` (a column slice of a wider buffer).
+    zero_slots: True (58%) or the fraction of slots zeroed; listed_zero not
+    None: DOT with a slot mask listing the non-zero slots and that fraction
+    of the zero ones."""
     from paper_2512_09200_amd import api
     rnd = rounding(dt)
     sdt = synth.torch_dtype(dt)
@@ -66,15 +104,16 @@ def check_interact(kind, dt, B, n, d, k, emit0, zero_slots, pad=0):
     X = synth.randn((B, n, d), seed=21, scale=0.05, dtype=dt)
     if zero_slots:
         r = np.random.default_rng(5)
-        X[r.random((B, n)) < 0.58] = 0.0
+        X[r.random((B, n)) < (0.58 if zero_slots is True else zero_slots)] = 0.0
     Xd = to_dev(X, sdt)
+    mask = _slot_mask(X, listed_zero) if listed_zero is not None else None
     W = synth.randn((n, k), seed=22, scale=1 / np.sqrt(n), dtype=dt) if kind == "fm" else None
     Wd = to_dev(W, sdt) if W is not None else None
     width = (n * (n - 1) // 2 if kind == "dot" else n * k)
     off = d if emit0 else 0
     stride = (off + width + 7) // 8 * 8
     out = torch.full((B, stride + pad), 7.0, dtype=sdt, device=DEV)[:, :stride]
-    api.lattice_interact_fwd(kind, Xd, out, emit_slot0=emit0, fm_W=Wd)
+    api.lattice_interact_fwd(kind, Xd, out, emit_slot0=emit0, fm_W=Wd, slot_mask=mask)
     torch.cuda.synchronize()
     if kind == "dot":
         ref = oi.dot_forward(X, rnd)
@@ -91,7 +130,7 @@ def check_interact(kind, dt, B, n, d, k, emit0, zero_slots, pad=0):
     Gd.copy_(to_dev(G, sdt))
     dX = torch.zeros((B, n, d), dtype=sdt, device=DEV)
     dW = torch.zeros((n, k), device=DEV) if kind == "fm" else None
-    api.lattice_interact_bwd(kind, Xd, Gd, dX, emit_slot0=emit0, fm_W=Wd, fm_dW=dW)
+    api.lattice_interact_bwd(kind, Xd, Gd, dX, emit_slot0=emit0, fm_W=Wd, fm_dW=dW, slot_mask=mask)
     torch.cuda.synchronize()
     if kind == "dot":
         dref = oi.dot_backward(G[:, off:off + width], X)
