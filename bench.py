@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--lcb-n", type=int, default=0,
                     help="stacked workloads: output vectors of each fusion block's linear compression "
                          "block (full DHEN/Wukong fusion blocks; 0: FM block only)")
+    ap.add_argument("--infer", action="store_true",
+                    help="time the forward alone (lattice_forward, inference); with --fp8 fast: FP8 serving")
     ap.add_argument("--no-skip-absent", action="store_true",
                     help="multi-domain DOT: compute the slots of absent features too (control run)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -177,10 +179,37 @@ def main():
                          side=None if one_stream else side, fp8_top=args.fp8,
                          domain_offsets=b["domain_offsets"])
 
+    def forward(i, events=None, one_stream=args.single_stream):
+        b = batches[i % len(batches)]
+        api.lattice_forward(model, b["offsets"], b["indices"], b["dense"], cfg.B, ws,
+                            nnz_capacity=nnz_max, side=None if one_stream else side, fp8_top=args.fp8,
+                            domain_offsets=b["domain_offsets"])
+        if events is not None:
+            raise ValueError("stage events: use the step")
+
     for i in range(args.warmup):
-        step(i)
+        (forward if args.infer else step)(i)
     torch.cuda.synchronize()
     log("[bench] warmup done")
+
+    if args.infer:
+        # inference: the forward alone (lattice_forward), no labels, no update
+        t_start = time.perf_counter()
+        for i in range(args.steps):
+            forward(args.warmup + i)
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t_start) / args.steps
+        print(json.dumps({
+            "metric": "inference samples/s (forward) at 1 GPU", "value": round(cfg.B / (ms * 1e-3), 1),
+            "unit": "samples/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": cfg.dtype if not args.fp8 else f"{cfg.dtype}+fp8-e4m3(top hidden fwd, {args.fp8} accumulation)",
+            "data": "synthetic (seeded; Zipf/Poisson jagged batches, random-init weights)",
+            "config": {"workload": cfg.name, "global_batch": cfg.B, "mode": "forward only",
+                       "fp8_top": args.fp8, "top_act": cfg.top_act, "towers": cfg.towers or None,
+                       "untied_top_layers": cfg.untie or None, "dot_skip_absent": skip_absent or None},
+            "roofline": None, "cpu_baseline": None}))
+        return
 
     nst = len(STAGES)
 

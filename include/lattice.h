@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 8
+#define LATTICE_ABI_VERSION 9
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -545,6 +545,18 @@ lattice_status lattice_step_plan(const lattice_model_desc* model, int32_t B, int
 lattice_status lattice_step(const lattice_model_desc* model, const lattice_batch_desc* batch,
                             const lattice_step_opts* opts, void* ws, size_t ws_bytes,
                             void* stream);
+
+/* The forward of lattice_step alone, for inference (Section 3.5.2 serves
+ * with FP8 and fast accumulation: opts->fp8_top = 2): pooled lookups, bottom
+ * MLP, interaction and top MLP, writing the logits ([B, T] fp32 at
+ * layout.logits) and the forward intermediates of the layout.  No loss,
+ * gradient or table update; batch->labels and batch->mask are not read (may
+ * be NULL).  Same model, plan, workspace and opts as lattice_step (a side
+ * stream, if given, runs the bottom MLP beside the pooled lookups; lr_tables
+ * and emit_grad_rows are ignored).  Errors as lattice_step. */
+lattice_status lattice_forward(const lattice_model_desc* model, const lattice_batch_desc* batch,
+                               const lattice_step_opts* opts, void* ws, size_t ws_bytes,
+                               void* stream);
 
 /* ------------------------------------------------------------------------ */
 const char* lattice_status_string(lattice_status s);

@@ -144,6 +144,8 @@ _SIGS = [
                                   POINTER(lattice_step_opts), POINTER(lattice_step_layout)]),
     ("lattice_step", c_int, [POINTER(lattice_model_desc), POINTER(lattice_batch_desc),
                              POINTER(lattice_step_opts), c_void_p, c_size_t, c_void_p]),
+    ("lattice_forward", c_int, [POINTER(lattice_model_desc), POINTER(lattice_batch_desc),
+                                POINTER(lattice_step_opts), c_void_p, c_size_t, c_void_p]),
     ("lattice_status_string", c_char_p, [c_int]),
     ("lattice_last_error", c_char_p, []),
     ("lattice_abi_version", c_int, []),

@@ -441,6 +441,25 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
                            _stream(stream)))
 
 
+def lattice_forward(model, offsets, indices, dense, B, ws, stream=None, nnz_capacity=0, side=None,
+                    fp8_top=None, domain_offsets=None):
+    """The step's forward alone (inference): logits at layout.logits of ws
+    (see step_views); no labels, gradients or table update.  The same plan
+    and workspace as lattice_step."""
+    lib = load()
+    _contig(dense, ws)
+    batch = A.lattice_batch_desc(bags=_jagged(offsets, indices, model.num_features, B),
+                                 dense=dense.data_ptr() if dense is not None and dense.numel() else None)
+    if domain_offsets is not None:
+        off = (ctypes.c_int64 * len(domain_offsets))(*[int(x) for x in domain_offsets])
+        batch.domain_offsets = ctypes.cast(off, ctypes.POINTER(ctypes.c_int64))
+    opts = A.lattice_step_opts(nnz_capacity=int(nnz_capacity or indices.numel()), fp8_top=_FP8_TOP[fp8_top])
+    if side is not None:
+        opts.side_stream, opts.side_events = side.ptrs()
+    check(lib.lattice_forward(byref(model.desc), byref(batch), byref(opts), _p(ws), ws.numel(),
+                              _stream(stream)))
+
+
 def step_views(model, ws, layout, B, T, nnz):
     """Torch views of the step's intermediates inside the workspace."""
     dt = model.tensors["tables"].dtype

@@ -1406,9 +1406,12 @@ lattice_status lattice_step_plan(const lattice_model_desc* model, int32_t B, int
   return LATTICE_OK;
 }
 
-lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_desc* batch,
-                            const lattice_step_opts* opts, void* ws, size_t ws_bytes,
-                            void* stream) {
+}  // extern "C"
+
+// The step (forward_only = false) or its forward alone (lattice_forward).
+static lattice_status step_impl(const lattice_model_desc* m, const lattice_batch_desc* batch,
+                                const lattice_step_opts* opts, void* ws, size_t ws_bytes,
+                                void* stream, bool forward_only) {
   REQUIRE(m && batch && opts, "null model/batch/opts");
   const int B = batch->bags.batch;
   REQUIRE(batch->bags.num_features == m->num_features, "batch features != model features");
@@ -1423,7 +1426,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   if (st != LATTICE_OK) return st;
   if (ws_bytes < (size_t)P.L.total_bytes || !ws)
     FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %lld", ws_bytes, (long long)P.L.total_bytes);
-  REQUIRE((batch->labels && batch->mask) || B == 0, "null labels/mask");
+  REQUIRE((batch->labels && batch->mask) || B == 0 || forward_only, "null labels/mask");
   Domains dom;
   st = check_domains(&m->top, batch->domain_offsets, B, &dom);
   if (st != LATTICE_OK) return st;
@@ -1433,6 +1436,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     for (int i = 0; i < LATTICE_STEP_SIDE_EVENTS; ++i)
       REQUIRE(opts->side_events[i], "side_events[%d] is null", i);
   }
+  if (B == 0 && forward_only) return LATTICE_OK;
   if (B == 0) {
     // sums over an empty batch: every parameter gradient, the loss and the
     // unique-row count are zero; the tables are untouched
@@ -1524,7 +1528,7 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   HIPRET(end(LATTICE_STAGE_EMBBAG_FWD));
   // fork: the sort and run bookkeeping go to the side stream, overlapping
   // the dense stages
-  if (side) {
+  if (side && !forward_only) {
     HIPRET(hipEventRecord(side->fork_fwd, s));
     HIPRET(hipStreamWaitEvent(side->s, side->fork_fwd, 0));
     HIPRET(sparse_sort(side->s));
@@ -1581,12 +1585,16 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
     else if (nt > 1)
       HIPRET(mlp_forward(&hidden, B, t, P.t_stride, tacts, tstr, &tab, s, &dom));
     HIPRET(head_fwd((const bf16_t*)head_in, head_ld, B, head.in_dim, (const bf16_t*)head.W, head.b,
-                    T, batch->labels, batch->mask, (float*)at(L.logits), scratch, s));
+                    T, forward_only ? nullptr : batch->labels, forward_only ? nullptr : batch->mask,
+                    (float*)at(L.logits), scratch, s));
   } else {
     if (opts->fp8_top) FAIL(LATTICE_ERR_UNSUPPORTED, "fp8_top needs the fused bf16 heads (<= 64 objectives)");
     HIPRET(mlp_forward(&m->top, B, t, P.t_stride, tacts, tstr, &tab, s, &dom));
   }
   HIPRET(end(LATTICE_STAGE_TOP_FWD));
+  // the forward alone ends here (a bottom MLP on the side stream was joined
+  // before the interaction)
+  if (forward_only) return LATTICE_OK;
   HIPRET(begin(LATTICE_STAGE_LOSS));
   if (fused_heads) {
     // the heads' input gradient: masked by the ReLU, or (SwishRN) the
@@ -1681,6 +1689,21 @@ lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_des
   // join: the caller's stream passes this point after all of the step's work
   if (side) HIPRET(hipStreamWaitEvent(s, side->done, 0));
   return LATTICE_OK;
+}
+
+
+extern "C" {
+
+lattice_status lattice_step(const lattice_model_desc* m, const lattice_batch_desc* batch,
+                            const lattice_step_opts* opts, void* ws, size_t ws_bytes,
+                            void* stream) {
+  return step_impl(m, batch, opts, ws, ws_bytes, stream, false);
+}
+
+lattice_status lattice_forward(const lattice_model_desc* m, const lattice_batch_desc* batch,
+                               const lattice_step_opts* opts, void* ws, size_t ws_bytes,
+                               void* stream) {
+  return step_impl(m, batch, opts, ws, ws_bytes, stream, true);
 }
 
 }  // extern "C"

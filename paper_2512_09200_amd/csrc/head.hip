@@ -61,8 +61,8 @@ __global__ __launch_bounds__(HEAD_THREADS) void head_fwd_kernel(
     const int t = tt * 32 + (ln & 31);
     const bool ok = rr < B && t < T;
     oi[j] = ok ? rr * T + t : -1;
-    yv[j] = ok ? y[(int64_t)rr * T + t] : 0.f;
-    mv[j] = ok ? m[(int64_t)rr * T + t] : 0;
+    yv[j] = (ok && y) ? y[(int64_t)rr * T + t] : 0.f;  // no labels (forward alone): no loss terms
+    mv[j] = (ok && m) ? m[(int64_t)rr * T + t] : 0;
     bv0[j] = (ok && bias) ? bias[t] : 0.f;
   }
   f32x16 acc[NT];

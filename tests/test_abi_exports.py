@@ -27,7 +27,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for required in ("lattice_embbag_fwd", "lattice_embbag_bwd", "lattice_interact_fwd",
                      "lattice_interact_bwd", "lattice_mlp_heads_fwd", "lattice_mlp_heads_bwd",
-                     "lattice_step", "lattice_step_plan", "lattice_validate_batch",
+                     "lattice_step", "lattice_forward", "lattice_step_plan", "lattice_validate_batch",
                      "lattice_status_string", "lattice_last_error", "lattice_abi_version"):
         assert required in names, required
 

@@ -235,9 +235,14 @@ def test_step_statuses(lib):
     # feature count of the batch differs from the model's
     b2 = A.lattice_batch_desc(bags=bags(F=3, B=64, nnz=1000), dense=FAKE, labels=FAKE, mask=FAKE)
     assert s(byref(m), byref(b2), byref(o), FAKE, 1 << 40, None) == INVALID_ARG
-    # null labels
+    # null labels (the forward alone reads none; an empty batch: nothing to do)
     b3 = A.lattice_batch_desc(bags=bags(F=4, B=64, nnz=1000), dense=FAKE, labels=None, mask=FAKE)
     assert s(byref(m), byref(b3), byref(o), FAKE, 1 << 40, None) == INVALID_ARG
+    fw = lib.lattice_forward
+    assert fw(None, byref(b3), byref(o), FAKE, 1 << 40, None) == INVALID_ARG
+    assert fw(byref(m), byref(b3), byref(o), FAKE, lay.total_bytes - 1, None) == WORKSPACE
+    b0 = A.lattice_batch_desc(bags=bags(F=4, B=0, nnz=0), dense=None, labels=None, mask=None)
+    assert fw(byref(m), byref(b0), byref(o), FAKE, 1 << 40, None) == OK
     # a side stream without its events
     o2 = step_opts()
     o2.side_stream = FAKE
