@@ -87,19 +87,28 @@ def layernorm_backward(dy, xhat, rstd, gamma):
     return du, dgamma
 
 
-def stack_forward(X1, layers, n_out, d, rnd, eps):
+def stack_forward(X1, layers, n_out, d, rnd, eps, fp8=False):
     """Returns (X_{L+1}, per-layer caches).  A layer with an ``L`` matrix
     ([n_lcb, n_in]) is a full fusion block: its FM block fills the first
     ``n_out - n_lcb`` output vectors and the linear compression block
     ``L X`` the last ``n_lcb`` (concatenated before the residual and the
-    LayerNorm)."""
+    LayerNorm).  fp8: the FM block's projection vec(F) A^T as an FP8 linear
+    layer (Section 3.5.2: linear layers in FP8 with row-wise scales): vec(F)
+    quantised per sample and A per output unit (oracle.fp8.quantize), the
+    product of the codes times both scales (oracle.fp8.linear_fp8)."""
+    from oracle import fp8 as ofp8
     X = np.asarray(X1, np.float64)
     B = X.shape[0]
     caches = []
     for lay in layers:
         Fm, P = fm_forward(X, lay["W"], rnd)                  # [B, n, k]
         vecF = Fm.reshape(B, -1)
-        HF = (vecF @ np.asarray(lay["A"], np.float64).T).reshape(B, -1, d)
+        if fp8:
+            qf, sf = ofp8.quantize(vecF, rowwise=True)
+            qa, sa = ofp8.quantize(np.asarray(lay["A"], np.float64), rowwise=True)
+            HF = ofp8.linear_fp8(qf, sf, qa, sa).reshape(B, -1, d)
+        else:
+            HF = (vecF @ np.asarray(lay["A"], np.float64).T).reshape(B, -1, d)
         if lay.get("L") is not None:
             HL = np.einsum("vu,bud->bvd", np.asarray(lay["L"], np.float64), X)
             H = np.concatenate([HF, HL], axis=1)

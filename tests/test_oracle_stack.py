@@ -241,3 +241,78 @@ def test_planted_fm_mistakes_fail_a_pin():
         finally:
             interact.fm_forward = orig
         assert err > 1e-6
+
+
+# ---------------------------------------------------------------------------
+# FP8 projection of the FM block (Section 3.5.2: linear layers in FP8 with
+# row-wise scales).  Pin: each quantised operand lies within half an e4m3
+# step of its value (2^-4 relative in the normal range, 2^-10 times the
+# row scale below it, plus the fp32 rounding of the scaled value), so the
+# FP8 projection lies within the propagated quantisation error of the exact
+# one; a projection that drops a scale, or quantises the wrong way round,
+# lands far outside.
+
+def _quant_err(x, s):
+    """Bound of |dequantised - x| for row-wise e4m3 quantisation with scales s."""
+    return (2.0 ** -4 + 4 * 2.0 ** -24) * np.abs(x) + 2.0 ** -10 * s[:, None]
+
+
+def _fp8_case(seed=11, B=6, n=5, k=4, d=8, nv=3):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((B, n, d)) * 0.5
+    lay = dict(W=rng.standard_normal((n, k)) / np.sqrt(n),
+               A=rng.standard_normal((nv * d, n * k)) / np.sqrt(n * k),
+               C=rng.standard_normal((nv, n)) / np.sqrt(n), gamma=1 + 0.1 * rng.standard_normal(d))
+    return X, lay, nv, d
+
+
+def _projection(X, lay, nv, d, fp8):
+    """(vec(F), A, H_F) of one layer: the exact projection, or the FP8 one
+    written out from the quantiser and the product of the codes."""
+    from oracle import fp8 as ofp8
+    Fm, _ = interact.fm_forward(X, lay["W"], identity)
+    vecF = Fm.reshape(X.shape[0], -1)
+    A = np.asarray(lay["A"], np.float64)
+    if not fp8:
+        return vecF, A, vecF @ A.T
+    qf, sf = ofp8.quantize(vecF)
+    qa, sa = ofp8.quantize(A)
+    return vecF, A, ofp8.linear_fp8(qf, sf, qa, sa)
+
+
+def test_fp8_projection_within_quantisation_error():
+    from oracle import fp8 as ofp8
+    X, lay, nv, d = _fp8_case()
+    vecF, A, exact = _projection(X, lay, nv, d, False)
+    _, _, h8 = _projection(X, lay, nv, d, True)
+    _, sf = ofp8.quantize(vecF)
+    _, sa = ofp8.quantize(A)
+    ef, ea = _quant_err(vecF, sf), _quant_err(A, sa)
+    bound = ef @ np.abs(A).T + np.abs(vecF) @ ea.T + ef @ ea.T
+    assert np.all(np.abs(h8 - exact) <= bound + 1e-300)
+    # not vacuous: the FP8 projection does differ, by far less than its size
+    assert 0 < np.max(np.abs(h8 - exact)) < 0.2 * np.max(np.abs(exact))
+    # planted mistakes: a scale dropped; the weight's scales applied per
+    # sample instead of per output unit
+    qf, sf_ = ofp8.quantize(vecF)
+    qa, sa_ = ofp8.quantize(A)
+    no_scale = ofp8.linear_fp8(qf, np.ones_like(sf_), qa, sa_)
+    assert np.any(np.abs(no_scale - exact) > bound)
+    swapped = (ofp8.e4m3_value(qf) @ ofp8.e4m3_value(qa).T) * sf_[:, None] * sa_[:X.shape[0], None]
+    assert np.any(np.abs(swapped - exact) > bound)
+
+
+def test_fp8_stack_forward_uses_the_fp8_projection():
+    """The stack's FP8 forward equals the bf16-free forward with its
+    projection replaced by the FP8 one (checked through the LayerNorm input:
+    the cached normalised values are a function of H + R alone)."""
+    X, lay, nv, d = _fp8_case()
+    Y8, c8 = interact.stack_forward(X, [lay], nv, d, identity, 0.0, fp8=True)
+    Y, c = interact.stack_forward(X, [lay], nv, d, identity, 0.0, fp8=False)
+    _, _, h8 = _projection(X, lay, nv, d, True)
+    u8 = h8.reshape(X.shape[0], nv, d) + np.einsum("vu,bud->bvd", lay["C"], X)
+    mu = u8.mean(axis=2, keepdims=True)
+    xhat = (u8 - mu) / np.sqrt(((u8 - mu) ** 2).mean(axis=2, keepdims=True))
+    np.testing.assert_allclose(c8[0]["xhat"], xhat, rtol=1e-10, atol=1e-12)
+    assert not np.allclose(Y8, Y, rtol=1e-6, atol=0)      # the FP8 path was taken
+    assert np.max(np.abs(Y8 - Y)) < 0.25 * np.max(np.abs(Y))
