@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--lcb-n", type=int, default=0,
                     help="stacked workloads: output vectors of each fusion block's linear compression "
                          "block (full DHEN/Wukong fusion blocks; 0: FM block only)")
+    ap.add_argument("--fp8-proj", choices=["precise", "fast"], default=None,
+                    help="stacked workloads: the FM blocks' projection in FP8 e4m3 (row-wise scales)")
     ap.add_argument("--infer", action="store_true",
                     help="time the forward alone (lattice_forward, inference); with --fp8 fast: FP8 serving")
     ap.add_argument("--no-skip-absent", action="store_true",
@@ -108,6 +110,11 @@ def main():
             print("--lcb-n needs a stacked workload", file=sys.stderr)
             sys.exit(2)
         cfg = cfg.scaled(lcb_n=args.lcb_n)
+    if args.fp8_proj:
+        if cfg.interact != "stack":
+            print("--fp8-proj needs a stacked workload", file=sys.stderr)
+            sys.exit(2)
+        cfg = cfg.scaled(stack_fp8=args.fp8_proj)
     if args.top_act != "relu":
         if args.fp8:
             print("--fp8 needs ReLU top layers", file=sys.stderr)
@@ -163,7 +170,7 @@ def main():
                           pool=cfg.pool, stack=stack, stack_n=cfg.stack_n, ln_eps=cfg.ln_eps,
                           top_act=cfg.top_act, norm_block=cfg.norm_block, norm_eps=cfg.norm_eps,
                           towers=bool(cfg.towers), n_domains=len(cfg.domains[0]) if cfg.untie else 0,
-                          untied_layers=cfg.untie, skip_absent=skip_absent)
+                          untied_layers=cfg.untie, skip_absent=skip_absent, fp8_proj=cfg.stack_fp8)
     nnz_max = max(b["nnz"] for b in batches)
     lay = api.lattice_step_plan(model, cfg.B, nnz_max, cfg.lr_tables, False, fp8_top=args.fp8)
     ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
@@ -360,6 +367,7 @@ def main():
                    "towers": cfg.towers or None,
                    "untied_top_layers": cfg.untie or None,
                    "dot_skip_absent": skip_absent or None,
+                   "fp8_stack_projection": cfg.stack_fp8,
                    "norm_block": cfg.norm_block if cfg.top_act != "relu" else None,
                    "sparse_sort_stream": "step" if args.single_stream else "side"},
         "roofline": roofline,

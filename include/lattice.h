@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define LATTICE_ABI_VERSION 9
+#define LATTICE_ABI_VERSION 10
 #define LATTICE_MAX_LAYERS 8
 
 typedef enum {
@@ -211,6 +211,12 @@ typedef struct {
                             the backward computes every slot.  Needs n <= 128;
                             NULL: every slot is computed.  lattice_step builds its
                             own (see skip_absent): leave NULL in the model. */
+  int32_t fp8_proj;      /* STACK: the FM blocks' projection vec(F) A^T as an FP8 linear layer
+                            (Section 3.5.2): 0 = bf16; 1 = e4m3 with row-wise scales
+                            (vec(F) per sample, A per output unit, quantised every
+                            call), fast accumulation off; 2 = the same with fast
+                            accumulation on.  The backward stays bf16 and takes the
+                            quantisation as the identity. */
   int32_t skip_absent;   /* DOT in lattice_step: 1 when whole features may be absent from
                             a sample (empty bags, as in multi-domain batches, Section
                             3.2): the step builds each sample's slot mask from the
@@ -228,6 +234,21 @@ size_t lattice_interact_workspace(const lattice_interact_desc* desc, int32_t B);
 lattice_status lattice_interact_fwd(const lattice_interact_desc* desc, int32_t B, const void* X,
                                     void* out, int64_t out_stride, void* ws, size_t ws_bytes,
                                     void* stream);
+
+/* STACK: byte offsets inside the interaction workspace of the state the
+ * forward saves for the backward, per layer l < n_layers (-1: absent):
+ * P = X_l^T W [B, dim, rank] (bf16), F = X_l P [B, n_l, rank] (bf16),
+ * H = [H_F; H_L] [B, stack_n * dim] (fp32, the LayerNorm input before the
+ * residual), mean and rstd [B, stack_n] (fp32, of the LayerNorm), and the
+ * layer's output X_{l+1} [B, stack_n, dim] (bf16; the last layer's output is
+ * the caller's out, so -1).  For inspection and tests; other kinds: all -1.
+ * Errors: INVALID_ARG, UNSUPPORTED. */
+typedef struct {
+  int64_t P[LATTICE_MAX_LAYERS], F[LATTICE_MAX_LAYERS], H[LATTICE_MAX_LAYERS];
+  int64_t mean[LATTICE_MAX_LAYERS], rstd[LATTICE_MAX_LAYERS], Xn[LATTICE_MAX_LAYERS];
+} lattice_stack_state;
+lattice_status lattice_interact_state(const lattice_interact_desc* desc, int32_t B,
+                                      lattice_stack_state* out);
 
 /* Gradient of lattice_interact_fwd: given d_out (same layout as out, storage
  * dtype), writes dX [B, n, dim] (storage dtype; with emit_slot0 the slot-0

@@ -49,7 +49,11 @@ class lattice_interact_desc(Structure):
                 ("rank", c_int32), ("emit_slot0", c_int32), ("fm_W", c_void_p),
                 ("fm_dW", c_void_p), ("n_layers", c_int32), ("stack_n", c_int32),
                 ("ln_eps", c_float), ("layers", POINTER(lattice_stack_layer)), ("lcb_n", c_int32),
-                ("slot_mask", c_void_p), ("skip_absent", c_int32)]
+                ("slot_mask", c_void_p), ("fp8_proj", c_int32), ("skip_absent", c_int32)]
+
+
+class lattice_stack_state(Structure):
+    _fields_ = [(k, c_int64 * MAX_LAYERS) for k in ("P", "F", "H", "mean", "rstd", "Xn")]
 
 
 class lattice_linear(Structure):
@@ -142,6 +146,7 @@ _SIGS = [
                                        c_int, c_int64, c_void_p]),
     ("lattice_step_plan", c_int, [POINTER(lattice_model_desc), c_int32, c_int64,
                                   POINTER(lattice_step_opts), POINTER(lattice_step_layout)]),
+    ("lattice_interact_state", c_int, [POINTER(lattice_interact_desc), c_int32, POINTER(lattice_stack_state)]),
     ("lattice_step", c_int, [POINTER(lattice_model_desc), POINTER(lattice_batch_desc),
                              POINTER(lattice_step_opts), c_void_p, c_size_t, c_void_p]),
     ("lattice_forward", c_int, [POINTER(lattice_model_desc), POINTER(lattice_batch_desc),

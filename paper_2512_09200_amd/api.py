@@ -157,9 +157,10 @@ def _lcb_n(stack):
 
 
 def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0, stack=None, stack_n=0,
-                  ln_eps=1e-5, slot_mask=None):
+                  ln_eps=1e-5, slot_mask=None, fp8_proj=None):
     """stack: list of layer dicts (see stack_layers) for kind "stack";
-    slot_mask (DOT): int32 [B, 4] device tensor of per-sample slot bits."""
+    slot_mask (DOT): int32 [B, 4] device tensor of per-sample slot bits;
+    fp8_proj (STACK): None, "precise" or "fast" (the FM projection in FP8)."""
     arr = stack_layers(stack) if stack else None
     if stack:
         rank = stack[0]["W"].shape[1]
@@ -168,18 +169,18 @@ def interact_desc(kind, X, emit_slot0, fm_W=None, fm_dW=None, rank=0, stack=None
                                 emit_slot0=int(emit_slot0), fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
                                 n_layers=len(stack) if stack else 0, stack_n=stack_n,
                                 ln_eps=ln_eps, layers=arr, lcb_n=_lcb_n(stack),
-                                slot_mask=_ptr(slot_mask))
+                                slot_mask=_ptr(slot_mask), fp8_proj=_FP8_TOP[fp8_proj])
     d._keep = arr
     return d
 
 
 def lattice_interact_fwd(kind, X, out, emit_slot0=False, fm_W=None, stream=None, stack=None,
-                         stack_n=0, ln_eps=1e-5, slot_mask=None):
+                         stack_n=0, ln_eps=1e-5, slot_mask=None, fp8_proj=None):
     """Returns the workspace (saved state), which lattice_interact_bwd needs."""
     _contig(X, fm_W, slot_mask)
     lib = load()
     d = interact_desc(kind, X, emit_slot0, fm_W, stack=stack, stack_n=stack_n, ln_eps=ln_eps,
-                      slot_mask=slot_mask)
+                      slot_mask=slot_mask, fp8_proj=fp8_proj)
     wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
     check(lib.lattice_interact_fwd(byref(d), X.shape[0], _p(X), _p(out), _row_stride(out), _p(ws),
@@ -188,11 +189,11 @@ def lattice_interact_fwd(kind, X, out, emit_slot0=False, fm_W=None, stream=None,
 
 
 def lattice_interact_bwd(kind, X, d_out, dX, emit_slot0=False, fm_W=None, fm_dW=None, stream=None,
-                         stack=None, stack_n=0, ln_eps=1e-5, ws=None, slot_mask=None):
+                         stack=None, stack_n=0, ln_eps=1e-5, ws=None, slot_mask=None, fp8_proj=None):
     _contig(X, dX, fm_W, fm_dW, slot_mask)
     lib = load()
     d = interact_desc(kind, X, emit_slot0, fm_W, fm_dW, stack=stack, stack_n=stack_n, ln_eps=ln_eps,
-                      slot_mask=slot_mask)
+                      slot_mask=slot_mask, fp8_proj=fp8_proj)
     wsb = lib.lattice_interact_workspace(byref(d), X.shape[0])
     if ws is None:
         ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
@@ -339,12 +340,13 @@ class StepModel:
     the first untied_layers top layers hold one parameter set per domain
     (lattice_step then takes the batch's domain_offsets); skip_absent
     (DOT): whole features may be absent from a sample (empty bags), so the
-    step's DOT forward skips the empty slots."""
+    step's DOT forward skips the empty slots; fp8_proj (STACK): None,
+    "precise" or "fast" -- the FM projection in FP8."""
 
     def __init__(self, *, tables, row_base, num_features, dense_in, bottom, top, interact,
                  fm_W=None, fm_dW=None, pool="sum", stack=None, stack_n=0, ln_eps=1e-5,
                  max_rows=None, top_act=None, norm_block=A.BLOCKNORM_COLS, norm_eps=1e-6,
-                 towers=False, n_domains=0, untied_layers=0, skip_absent=False):
+                 towers=False, n_domains=0, untied_layers=0, skip_absent=False, fp8_proj=None):
         _contig(tables, row_base)
         dt = _dt(tables)
         d = tables.shape[1]
@@ -360,7 +362,8 @@ class StepModel:
                                         fm_W=_ptr(fm_W), fm_dW=_ptr(fm_dW),
                                         n_layers=len(stack) if stack else 0, stack_n=stack_n,
                                         ln_eps=ln_eps, layers=self._stack, lcb_n=_lcb_n(stack),
-                                        skip_absent=int(bool(skip_absent)))
+                                        skip_absent=int(bool(skip_absent)),
+                                        fp8_proj=_FP8_TOP[fp8_proj])
         self.desc = A.lattice_model_desc(dtype=dt, pool=_POOL[pool],
                                          tables=_tables(tables, row_base, max_rows),
                                          num_features=num_features, dense_in=dense_in,
@@ -499,4 +502,53 @@ def step_views(model, ws, layout, B, T, nnz):
     v["bottom_grad"] = [view(layout.bottom_grad[i], (B, bots[i]["W"].shape[0]), dt)
                         for i in range(len(bots))] if model.dense_in > 0 else []
     _ = es
+    # the stacked interaction's saved state (per layer P, F, H, mean, rstd, X_{l+1})
+    v["stack_state"] = None
+    if model.desc.interact.kind == _KIND["stack"]:
+        st = stack_state_offsets(model.desc.interact, B)
+        base = layout.interact
+        nl, nv, k = model.desc.interact.n_layers, model.desc.interact.stack_n, model.desc.interact.rank
+        layers = []
+        for l in range(nl):
+            nin = n if l == 0 else nv
+            layers.append(dict(
+                P=view(base + st.P[l], (B, d, k), dt), F=view(base + st.F[l], (B, nin, k), dt),
+                H=view(base + st.H[l], (B, nv * d), torch.float32),
+                mean=view(base + st.mean[l], (B, nv), torch.float32),
+                rstd=view(base + st.rstd[l], (B, nv), torch.float32),
+                Xn=view(base + st.Xn[l], (B, nv, d), dt) if st.Xn[l] >= 0 else None))
+        v["stack_state"] = layers
     return v
+
+
+def stack_state_offsets(idesc, B):
+    """lattice_stack_state of an interaction descriptor (byte offsets of the
+    saved state inside its workspace)."""
+    out = A.lattice_stack_state()
+    check(load().lattice_interact_state(byref(idesc), B, byref(out)))
+    return out
+
+
+def lattice_interact_state(kind, X, stack, stack_n, ws, ln_eps=1e-5, fp8_proj=None):
+    """Views of the stacked interaction's saved state inside ws (the workspace
+    lattice_interact_fwd returned): per layer P, F, H, mean, rstd, X_{l+1}."""
+    d_ = interact_desc(kind, X, False, stack=stack, stack_n=stack_n, ln_eps=ln_eps, fp8_proj=fp8_proj)
+    st = stack_state_offsets(d_, X.shape[0])
+    B, n, dd = X.shape
+    k = stack[0]["W"].shape[1]
+
+    def view(off, shape, dtype):
+        size = 1
+        for x in shape:
+            size *= int(x)
+        size *= torch.empty((), dtype=dtype).element_size()
+        return ws[off: off + size].view(dtype).view(*shape)
+    out = []
+    for l in range(len(stack)):
+        nin = n if l == 0 else stack_n
+        out.append(dict(P=view(st.P[l], (B, dd, k), X.dtype), F=view(st.F[l], (B, nin, k), X.dtype),
+                        H=view(st.H[l], (B, stack_n * dd), torch.float32),
+                        mean=view(st.mean[l], (B, stack_n), torch.float32),
+                        rstd=view(st.rstd[l], (B, stack_n), torch.float32),
+                        Xn=view(st.Xn[l], (B, stack_n, dd), X.dtype) if st.Xn[l] >= 0 else None))
+    return out

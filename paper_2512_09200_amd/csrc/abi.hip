@@ -321,6 +321,7 @@ static StackShape stack_shape(const lattice_interact_desc* d) {
   sh.has_C0 = (d->layers && d->n_layers > 0 && d->layers[0].C) ? 1 : 0;
   sh.eps = d->ln_eps;
   sh.nL = d->lcb_n;
+  sh.fp8 = d->fp8_proj;
   return sh;
 }
 
@@ -339,6 +340,8 @@ static lattice_status check_interact(const lattice_interact_desc* d, int32_t B) 
   lattice_status st = check_dim(d->dim, d->dtype);
   if (st != LATTICE_OK) return st;
   REQUIRE(d->skip_absent == 0 || d->skip_absent == 1, "skip_absent must be 0 or 1");
+  REQUIRE(d->fp8_proj >= 0 && d->fp8_proj <= 2, "fp8_proj must be 0, 1 or 2");
+  if (d->fp8_proj) REQUIRE(d->kind == LATTICE_INTERACT_STACK, "fp8_proj is for the STACK interaction only");
   if (d->skip_absent) REQUIRE(d->kind == LATTICE_INTERACT_DOT, "skip_absent is for the DOT interaction only");
   if (d->slot_mask) {
     REQUIRE(d->kind == LATTICE_INTERACT_DOT, "slot_mask is for the DOT interaction only");
@@ -465,6 +468,27 @@ lattice_status lattice_interact_fwd(const lattice_interact_desc* desc, int32_t B
   const size_t need = desc->kind == LATTICE_INTERACT_STACK ? interact_ws(desc, B) : 0;
   if (ws_bytes < need || (need && !ws)) FAIL(LATTICE_ERR_WORKSPACE, "workspace %zu < %zu", ws_bytes, need);
   HIPRET(interact_fwd_impl(desc, B, X, out, out_stride, ws, strm(stream)));
+  return LATTICE_OK;
+}
+
+lattice_status lattice_interact_state(const lattice_interact_desc* desc, int32_t B,
+                                      lattice_stack_state* out) {
+  REQUIRE(out, "null output");
+  lattice_status st = check_interact(desc, B);
+  if (st != LATTICE_OK) return st;
+  for (int l = 0; l < LATTICE_MAX_LAYERS; ++l)
+    out->P[l] = out->F[l] = out->H[l] = out->mean[l] = out->rstd[l] = out->Xn[l] = -1;
+  if (desc->kind != LATTICE_INTERACT_STACK) return LATTICE_OK;
+  const StackShape sh = stack_shape(desc);
+  const StackPlan p = stack_plan(sh, B);
+  for (int l = 0; l < sh.L; ++l) {
+    out->P[l] = (int64_t)p.P[l];
+    out->F[l] = (int64_t)p.F[l];
+    out->H[l] = (int64_t)p.H[l];
+    out->mean[l] = (int64_t)p.mean[l];
+    out->rstd[l] = (int64_t)p.rstd[l];
+    out->Xn[l] = l + 1 < sh.L ? (int64_t)p.Xn[l] : -1;
+  }
   return LATTICE_OK;
 }
 

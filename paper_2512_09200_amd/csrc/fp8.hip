@@ -130,6 +130,46 @@ __global__ __launch_bounds__(256) void fp8_quant_kernel(Fp8Jobs J, const float* 
     for (int c0 = cols + lane * 8; c0 < ldq; c0 += 512) *reinterpret_cast<u32x2*>(qr + c0) = u32x2{0u, 0u};
     return;
   }
+  const bool vec_long = cols % 8 == 0 && ld % 8 == 0 && (uintptr_t)jb.x % 16 == 0 && cols > 64 * 8 * RV;
+  if (vec_long) {
+    // rows too long for the registers: two passes of 16-byte loads (the
+    // second re-reads the wave's row, mostly from cache)
+    auto ld8 = [&](int c0, float* v) {
+      if constexpr (sizeof(IT) == 2) {
+        Vec16<bf16_t>::unpack(ldg16(reinterpret_cast<const bf16_t*>(xr) + c0), v);
+      } else {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(xr + c0);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(xr + c0 + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { v[e] = a[e]; v[4 + e] = b[e]; }
+      }
+    };
+    float s;
+    if (ROWWISE) {
+      float m = 0.f;
+      for (int c0 = lane * 8; c0 < cols; c0 += 512) {
+        float v[8];
+        ld8(c0, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(v[e]));
+      }
+      m = wave_max(m);
+      s = m > 0.f ? m / 448.f : 1.f;
+      if (lane == 0) scales[row] = s;
+    } else {
+      s = scale_in[0];
+    }
+    const float rs = 1.f / s;
+    for (int c0 = lane * 8; c0 < cols; c0 += 512) {
+      float v[8];
+      ld8(c0, v);
+      const uint32_t w0 = e4m3x4(v[0] * rs, v[1] * rs, v[2] * rs, v[3] * rs);
+      const uint32_t w1 = e4m3x4(v[4] * rs, v[5] * rs, v[6] * rs, v[7] * rs);
+      *reinterpret_cast<u32x2*>(qr + c0) = u32x2{w0, w1};
+    }
+    for (int c0 = cols + lane * 8; c0 < ldq; c0 += 512) *reinterpret_cast<u32x2*>(qr + c0) = u32x2{0u, 0u};
+    return;
+  }
   float s;
   if (ROWWISE) {
     float m = 0.f;

@@ -152,6 +152,7 @@ struct StackShape {
   int has_C0;           // layer 0 uses a projection residual C [nv, n0]
   float eps;
   int nL;               // output vectors of the linear compression block (0: none)
+  int fp8;              // FM projection in FP8 e4m3: 0 = bf16, 1 = precise, 2 = fast accumulation
 };
 struct StackLayer {
   const void* W;        // [n, k] bf16
@@ -164,6 +165,7 @@ struct StackLayer {
 };
 struct StackPlan {       // byte offsets inside the interaction workspace
   size_t P[8], F[8], H[8], mean[8], rstd[8], Xn[8], R0, state_bytes;
+  size_t qF, sF, qA, sA;  // FP8 projection: codes and row scales of vec(F) and A (fp8 only)
   size_t du, duR, dF, dP, dXf, dgp, gemm_ws, total_bytes;
 };
 bool stack_supported(const StackShape& sh);

@@ -5,7 +5,9 @@
 //   H_L = L X                          (linear compression block, nL vectors; nL = 0: none)
 //   u = [H_F; H_L] + R,  R = C X or X  (residual; C a linear projection)
 //   X' = LayerNorm_gamma(u)            (per vector over d, gain only, fp32 math)
-// and the exact backward.  The contractions run on the bf16 MFMA GEMM
+// and the exact backward.  The contractions run on the bf16 MFMA GEMM (the
+// projection vec(F) A^T optionally in FP8 e4m3 with row-wise scales, the
+// backward then taking it as the identity of its bf16 operands)
 // (batched over samples where they are per-sample products, K-segmented
 // where they sum over samples); LayerNorm forward/backward are one wave per
 // vector.  Storage points: P = X^T W, F, X' and the GEMM operand copy of the
@@ -187,6 +189,16 @@ StackPlan stack_plan(const StackShape& sh, int B) {
     }
   }
   p.gemm_ws = take(gw);
+  if (sh.fp8) {
+    // codes of the widest vec(F) and A (layer 0 when n0 > nv), reused by every layer
+    const int nmx = sh.n0 > sh.nv ? sh.n0 : sh.nv;
+    const size_t ldq = ((size_t)nmx * sh.k + 15) / 16 * 16;
+    const size_t rowsA = (size_t)(sh.nv - sh.nL) * sh.d;
+    p.qF = take((size_t)B * ldq);
+    p.sF = take((size_t)B * 4);
+    p.qA = take(rowsA * ldq);
+    p.sA = take(rowsA * 4);
+  }
   p.total_bytes = off;
   return p;
 }
@@ -260,12 +272,27 @@ hipError_t stack_fwd(const StackShape& sh, const StackLayer* Ls, int B, const vo
     STK_CHECK(gemm(g2, nullptr, s));
     // H_F = vec(F) A^T: M = B, N = (nv - nL)*d, K = n*k (the first nv - nL vectors of H)
     const int nF = nv - sh.nL;
-    GemmArgs g3;
-    g3.A = F; g3.lda = (int64_t)n * k;
-    g3.B = Ls[l].A; g3.ldb = (int64_t)n * k;
-    g3.C = H; g3.ldc = nvd; g3.c_dt = DT_F32;
-    g3.M = B; g3.N = nF * d; g3.K = n * k;
-    STK_CHECK(gemm(g3, nullptr, s));
+    if (sh.fp8) {
+      // FP8 linear layer (Section 3.5.2): vec(F) quantised per sample and A
+      // per output unit (one launch), then the e4m3 product with both scales
+      const int64_t ldq = ((int64_t)n * k + 15) / 16 * 16;
+      uint8_t* qF = (uint8_t*)(base + p.qF);
+      uint8_t* qA = (uint8_t*)(base + p.qA);
+      float* sF = (float*)(base + p.sF);
+      float* sA = (float*)(base + p.sA);
+      const Fp8RowJob jobs[2] = {{F, (int64_t)n * k, B, n * k, qF, ldq, sF},
+                                 {Ls[l].A, (int64_t)n * k, nF * d, n * k, qA, ldq, sA}};
+      STK_CHECK(fp8_quantize_rows(DT_BF16, jobs, 2, s));
+      STK_CHECK(gemm_fp8(qF, ldq, sF, 1, qA, ldq, sA, 1, nullptr, H, DT_F32, nvd, B, nF * d, n * k, 0,
+                         sh.fp8 == 2, s));
+    } else {
+      GemmArgs g3;
+      g3.A = F; g3.lda = (int64_t)n * k;
+      g3.B = Ls[l].A; g3.ldb = (int64_t)n * k;
+      g3.C = H; g3.ldc = nvd; g3.c_dt = DT_F32;
+      g3.M = B; g3.N = nF * d; g3.K = n * k;
+      STK_CHECK(gemm(g3, nullptr, s));
+    }
     if (sh.nL > 0) {
       // H_L,b = L X_b (the last nL vectors of H): M = nL, N = d, K = n
       GemmArgs gl;

@@ -52,6 +52,7 @@ class Config:
     top_act: str = "relu"                    # hidden top layers: "relu" | "swishrn" | "hardswishrn"
     norm_block: int = 128                    # SwishRN groups: 128 (BlockNorm) or 0 (the whole row)
     norm_eps: float = 1e-6
+    stack_fp8: Optional[str] = None          # STACK: the FM projection in FP8 ("precise" / "fast")
 
     # ---- derived shapes -------------------------------------------------
     @property

@@ -361,6 +361,15 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
         assert_close_derived("interaction backward dX [stage]", dXs, rnd(full), obounds.rounded(edX, full, u_), t)
         if rows is None:
             assert_close_derived("fm.dW [stage]", grads["fm_dW"], dWr, edW, t)
+    elif cfg.stack_fp8 is not None:
+        layers = params["stack"]
+        dX1, sg, edX, eg = check_stack_fp8(layers, X, v["stack_state"], tin, gt, None, None, cfg.stack_fp8,
+                                           cfg.ln_eps, rows=rows, t=t)
+        assert_close_derived("stack backward dX [stage]", dXs, rnd(dX1), obounds.rounded(edX, dX1, u_), t)
+        if rows is None:
+            for l, (gl, el) in enumerate(zip(sg, eg)):
+                for key in gl:
+                    assert_close_derived(f"stack{l}.{key} [stage]", grads["stack"][l][key], gl[key], el[key], t)
     else:
         layers = params["stack"]
         XL, caches = ointeract.stack_forward(Xs, layers, cfg.stack_n, d, rnd, cfg.ln_eps)
@@ -375,6 +384,63 @@ def check_stages(cfg, params, batch, v, grads, rows=None, wgrad_rows=None, fp8_t
             for l, (gl, el) in enumerate(zip(sg, eg)):
                 for key in gl:
                     assert_close_derived(f"stack{l}.{key} [stage]", grads["stack"][l][key], gl[key], el[key], t)
+
+
+def check_stack_fp8(layers, X0, state, out, dY, dX, grads, mode, eps, rows=None, t=2e-2):
+    """Stage-wise parity of a stacked interaction whose FM projection ran in
+    FP8 (Section 3.5.2), from the accelerator's own saved state (per layer
+    P, F, H, X_{l+1}; see lattice_interact_state): the projection within
+    oracle.fp8.linear_fp8_bound of the exact product of the codes the oracle
+    takes from the stored vec(F) and A (the same quantiser, so the same
+    codes), the linear compression block within the fp32 sum bound, the
+    residual and LayerNorm from the stored H element-wise; then the bf16
+    backward through the oracle from those forward values, within the
+    derived deviation.  rows: the samples checked (all if None); parameter
+    gradients are compared when rows is None."""
+    from oracle import fp8 as ofp8
+    rnd = ostep.rounding("bf16")
+    R = np.arange(X0.shape[0]) if rows is None else np.asarray(rows)
+    Xl = _np64(X0)[R]
+    X_first = Xl
+    L = len(layers)
+    d = Xl.shape[2]
+    caches = []
+    for l, lay in enumerate(layers):
+        st = state[l]
+        P, F, H = _np64(st["P"])[R], _np64(st["F"])[R], _np64(st["H"])[R]
+        Bn = F.shape[0]
+        nv = H.shape[1] // d
+        vecF = F.reshape(Bn, -1)
+        A = np.asarray(lay["A"], np.float64)
+        nFd = A.shape[0]
+        qf, sf = ofp8.quantize(vecF)
+        qa, sa = ofp8.quantize(A)
+        ref = ofp8.linear_fp8(qf, sf, qa, sa)
+        bound = ofp8.linear_fp8_bound(qf, sf, qa, sa, fast_accum=(mode == "fast")) + 2.0 ** -24 * np.abs(ref)
+        ratio = float(np.max(np.abs(H[:, :nFd] - ref) / (bound + 1e-300)))
+        print(f"  stack{l} FP8 projection [stage]: worst |x-r|/bound {ratio:.3f}", flush=True)
+        assert ratio <= 1.0, f"stack{l}: FP8 projection outside its bound ({ratio})"
+        if lay.get("L") is not None:
+            Lm = np.asarray(lay["L"], np.float64)
+            HL = np.einsum("vu,bud->bvd", Lm, Xl).reshape(Bn, -1)
+            aHL = np.einsum("vu,bud->bvd", np.abs(Lm), np.abs(Xl)).reshape(Bn, -1)
+            assert_product(f"stack{l} H_L", H[:, nFd:], HL, aHL, Xl.shape[1], None, t)
+        C = lay.get("C")
+        res = np.einsum("vu,bud->bvd", np.asarray(C, np.float64), Xl) if C is not None else Xl
+        u = H.reshape(Bn, nv, d) + res
+        mu = u.mean(axis=2, keepdims=True)
+        rstd = 1.0 / np.sqrt(((u - mu) ** 2).mean(axis=2, keepdims=True) + eps)
+        xhat = (u - mu) * rstd
+        y = xhat * np.asarray(lay["gamma"], np.float64)
+        got = _np64(out)[R].reshape(Bn, nv, d) if l == L - 1 else _np64(st["Xn"])[R]
+        assert_close(f"stack{l} LayerNorm [stage]", got.reshape(Bn, -1), rnd(y).reshape(Bn, -1), t)
+        caches.append(dict(X=Xl, P=P, vecF=vecF, xhat=xhat, rstd=rstd))
+        Xl = got
+    dYr = np.asarray(dY, np.float64)[R].reshape(len(R), -1, d)
+    dX1, g = ointeract.stack_backward(dYr, layers, caches, rnd)
+    zero = lambda x: (np.zeros(x.shape), np.zeros(x.shape))
+    _, edX, eg = obounds.stack_bounds(X_first, zero(X_first), dYr, zero(dYr), layers, caches, "bf16")
+    return dX1, g, edX, eg
 
 
 def tin_grad(v, cfg):
@@ -511,7 +577,8 @@ class Workload:
                              top_act=c.top_act, norm_block=c.norm_block, norm_eps=c.norm_eps,
                              towers=bool(c.towers), n_domains=len(c.domains[0]) if c.untie else 0,
                              untied_layers=c.untie,
-                             skip_absent=c.interact == "dot" and c.domains is not None)
+                             skip_absent=c.interact == "dot" and c.domains is not None,
+                             fp8_proj=c.stack_fp8)
 
 
 def relu_overrides(cfg, params, table, batch, gpu_in, gpu_out, max_iter=4):

@@ -1,6 +1,7 @@
 """Full-size parity of the model options at the workloads' real sizes, in
 the launch configuration the benchmark times them: FP8 top layers (Section
-3.5.2), SwishRN with BlockNorm (Sections 3.3.4, 3.5.3), per-objective
+3.5.2; the top MLP's hidden layers, or the stacked interaction's FM
+projection), SwishRN with BlockNorm (Sections 3.3.4, 3.5.3), per-objective
 towers (Section 3.3.3), untied top layers (Section 3.3.4) and full fusion
 blocks (Section 3.3.2).  One step each (with the workload's SGD step); every
 stage is recomputed by the oracle from the accelerator's own stored inputs
@@ -25,6 +26,7 @@ OPTIONS = {
     "large-emb-fm-towers-32": (LARGE.scaled(top=tuple(LARGE.top[:-2]) + (T * 32, T), towers=32), None),
     "multidomain-dot-untied-2": (MD.scaled(untie=2), None),
     "deep-stack-dwfb-16": (DEEP.scaled(lcb_n=16), None),
+    "deep-stack-fp8-projection-fast": (DEEP.scaled(stack_fp8="fast"), None),
 }
 
 

@@ -192,3 +192,51 @@ def test_stack_fwd_bwd(name):
         for key in ("dW", "dA", "dgamma", "dC", "dL"):
             if key in gl:
                 assert_close_derived(f"layer{l}.{key}", dl[key], gl[key], el[key], 2e-2)
+
+
+FP8_STACK_CASES = {
+    # name: (B, n0, stack_n, d, rank, layers, lcb_n, fp8 accumulation)
+    "stack-C-d64-fp8-precise": (96, 24, 8, 64, 16, 3, 0, "precise"),
+    "stack-id-d128-fp8-fast": (40, 16, 16, 128, 32, 2, 0, "fast"),
+    "dwfb-C-d128-fp8-precise": (33, 30, 10, 128, 16, 2, 1, "precise"),
+    "stack-C-d128-fp8-fast-long-rows": (20, 64, 32, 128, 64, 2, 0, "fast"),   # vec(F) rows of 4096
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", list(FP8_STACK_CASES))
+def test_stack_fp8_projection(name):
+    """The stacked interaction with its FM projection vec(F) A^T in FP8
+    (Section 3.5.2), stage by stage from the GPU's own saved state
+    (tests._util.check_stack_fp8): the FP8 product within the accumulation
+    bound of the exact product of the codes, LayerNorm from the stored H,
+    and the bf16 backward (the quantisation taken as the identity) through
+    the oracle from the GPU's forward values."""
+    from paper_2512_09200_amd import api
+    from oracle import bounds as obounds
+    from tests._util import assert_close_derived, check_stack_fp8, stack_dev
+    B, n0, nv, d, k, L, nL, mode = FP8_STACK_CASES[name]
+    print(f"[stack-fp8] {name}", flush=True)
+    cfg = synth.DEEP_STACK.scaled(B=B, F=n0, d=d, stack_n=nv, fm_rank=k, stack_layers=L,
+                                  lcb_n=nL, top=(16, 4), seed=78)
+    params = synth.make_dense_params(cfg)
+    layers = params["stack"]
+    rnd = rounding("bf16")
+    X = synth.randn((B, n0, d), seed=33, scale=0.05, dtype="bf16")
+    Xd = to_dev(X, torch.bfloat16)
+    dev_layers = stack_dev(layers, torch.bfloat16)
+    out = torch.zeros((B, nv * d), dtype=torch.bfloat16, device=DEV)
+    ws = api.lattice_interact_fwd("stack", Xd, out, stack=dev_layers, stack_n=nv, ln_eps=cfg.ln_eps,
+                                  fp8_proj=mode)
+    G = synth.randn((B, nv * d), seed=34, scale=1e-3, dtype="bf16")
+    dX = torch.zeros((B, n0, d), dtype=torch.bfloat16, device=DEV)
+    api.lattice_interact_bwd("stack", Xd, to_dev(G, torch.bfloat16), dX, stack=dev_layers,
+                             stack_n=nv, ln_eps=cfg.ln_eps, ws=ws, fp8_proj=mode)
+    torch.cuda.synchronize()
+    state = api.lattice_interact_state("stack", Xd, dev_layers, nv, ws, ln_eps=cfg.ln_eps, fp8_proj=mode)
+    dX1, grads, edX, eg = check_stack_fp8(layers, X, state, out, G, None, None, mode, cfg.ln_eps)
+    assert_close_derived("dX", dX, rnd(dX1), obounds.rounded(edX, dX1, 2.0 ** -8), 2e-2)
+    for l, (gl, dl, el) in enumerate(zip(grads, dev_layers, eg)):
+        for key in ("dW", "dA", "dgamma", "dC", "dL"):
+            if key in gl:
+                assert_close_derived(f"layer{l}.{key}", dl[key], gl[key], el[key], 2e-2)
