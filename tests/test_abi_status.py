@@ -155,6 +155,16 @@ def test_interact_statuses(lib):
     odd = interact_desc(kind=A.DOT, n=97, dim=128, W=None)
     odd.slot_mask = FAKE + 4
     assert f(byref(odd), 8, FAKE, FAKE, 1 << 20, None, 0, None) == INVALID_ARG
+    fm_fp8 = interact_desc()
+    fm_fp8.fp8_proj = 2
+    assert f(byref(fm_fp8), 8, FAKE, FAKE, 1 << 20, None, 0, None) == INVALID_ARG
+    assert "fp8_proj" in last_error(lib)
+    # the stacked interaction's saved state: offsets per layer, the last output the caller's
+    stt = A.lattice_stack_state()
+    assert lib.lattice_interact_state(byref(st), 16, byref(stt)) == OK
+    assert stt.P[0] >= 0 and stt.F[0] > stt.P[0] and stt.H[0] > stt.F[0] and stt.Xn[0] == -1 and stt.P[1] == -1
+    assert lib.lattice_interact_state(byref(interact_desc()), 16, byref(stt)) == OK and stt.P[0] == -1
+    assert lib.lattice_interact_state(byref(st), 16, None) == INVALID_ARG
     fm_skip = interact_desc()
     fm_skip.skip_absent = 1
     assert f(byref(fm_skip), 8, FAKE, FAKE, 1 << 20, None, 0, None) == INVALID_ARG
