@@ -245,9 +245,8 @@ __device__ inline SlotMask slot_mask_of(const u32x4 raw, int n) {
   return sm;
 }
 
-// lst[r] = r-th listed slot; pos[s] = compact index of slot s or -1 (pos may
-// be null).  Thread t handles slot t (t < n).
-__device__ inline void slot_lists(const SlotMask& sm, int n, uint8_t* lst, int8_t* pos) {
+// lst[r] = r-th listed slot (r < na).  Thread t handles slot t (t < n).
+__device__ inline void slot_lists(const SlotMask& sm, int n, uint8_t* lst) {
   const int t = threadIdx.x;
   if (t >= n) return;
   const int w = t >> 5, bit = t & 31;
@@ -262,7 +261,6 @@ __device__ inline void slot_lists(const SlotMask& sm, int n, uint8_t* lst, int8_
   const bool on = (mw >> bit) & 1u;
   const int r = below + __popc(mw & ((1u << bit) - 1u));
   if (on) lst[r] = (uint8_t)t;
-  if (pos) pos[t] = on ? (int8_t)r : (int8_t)-1;
 }
 
 // Stager over the listed rows: compact row r reads slot lst[r] of the
@@ -333,7 +331,7 @@ __global__ __launch_bounds__(DOT_THREADS) void dot_fwd_listed_kernel(const bf16_
   u32x4 mraw = {0u, 0u, 0u, 0u};  // mask words of the sample after the next
   if (blockIdx.x < B) {
     const SlotMask sm = slot_mask_of(slot_mask_load(mask, blockIdx.x), n);
-    slot_lists(sm, n, lst[0], nullptr);
+    slot_lists(sm, n, lst[0]);
     na_next = sm.na;
   }
   if (blockIdx.x + G < B) mraw = slot_mask_load(mask, blockIdx.x + G);
@@ -348,7 +346,7 @@ __global__ __launch_bounds__(DOT_THREADS) void dot_fwd_listed_kernel(const bf16_
       *reinterpret_cast<u32x4*>(Zp + v * 8) = u32x4{0u, 0u, 0u, 0u};
     if (nb < B) {
       const SlotMask sm = slot_mask_of(mraw, n);
-      slot_lists(sm, n, lst[cur ^ 1], nullptr);
+      slot_lists(sm, n, lst[cur ^ 1]);
       na_next = sm.na;
     }
     __syncthreads();
