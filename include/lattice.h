@@ -474,9 +474,10 @@ typedef enum {
  * may be disabled) that it uses to fork work from `stream` onto the side
  * stream and to join it back: the bottom MLP's forward is forked at the
  * step's start and runs beside the pooled lookups; the sort is forked after
- * the pooled lookups and overlaps the dense forward and backward; the weight
- * gradients are forked after the interaction backward and overlap the
- * segmented reduction, which waits for the sort.  All work is still ordered
+ * the pooled lookups and overlaps the dense forward and backward; the bottom
+ * MLP's backward is forked after the interaction backward and overlaps the
+ * top MLP's weight gradients and the segmented reduction (which waits for
+ * the sort), both on `stream`.  All work is still ordered
  * after the caller's prior work on `stream`, and the call's work is complete
  * when `stream` reaches the end of it, as with a single stream.  The library
  * keeps no stream or event of its own.  Two calls that share a side stream
@@ -494,8 +495,8 @@ typedef struct {
   void* const* stage_events;   /* host array of 2*LATTICE_STEP_STAGES hipEvent_t or NULL:
                                   [2s] is recorded when stage s begins and [2s+1] when
                                   it ends, on the stream that runs the stage (the side
-                                  stream for BOTTOM_FWD, EMBBAG_SORT, EMBBAG_RUNS,
-                                  TOP_WGRAD and BOTTOM_BWD when a side stream is given);
+                                  stream for BOTTOM_FWD, EMBBAG_SORT, EMBBAG_RUNS and
+                                  BOTTOM_BWD when a side stream is given);
                                   NULL entries are not recorded (each record costs a
                                   few microseconds of GPU time) */
   void* side_stream;           /* hipStream_t or NULL (see above) */

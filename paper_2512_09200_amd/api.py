@@ -393,8 +393,8 @@ def lattice_step_plan(model, B, nnz, lr_tables=0.0, emit_grad_rows=False, fp8_to
 
 class SideStream:
     """A second stream of the caller's device and the fork / join events that
-    lattice_step uses to overlap the sparse gradient's sort and the dense
-    weight gradients with the rest of the step (default priority; the
+    lattice_step uses to overlap the bottom MLP and the sparse gradient's
+    sort with the rest of the step (default priority; the
     events are created here, by torch, and recorded once so they exist)."""
 
     def __init__(self, device=None):
@@ -416,7 +416,7 @@ def lattice_step(model, offsets, indices, dense, labels, mask, ws, lr_tables=0.0
     2*len(STAGES) torch.cuda.Event(enable_timing=True) or None: [2s] and
     [2s+1] are recorded when stage s begins and ends, on the stream that runs
     it (None: not recorded).
-    side: a SideStream to overlap the sort and the weight gradients on (None:
+    side: a SideStream to overlap the bottom MLP and the sort on (None:
     every stage on the step's stream).  fp8_top: None, "precise" or "fast"
     (the top MLP's hidden-layer forward in FP8; see lattice.h).
     domain_offsets: host [D + 1] offsets of the domain-grouped samples

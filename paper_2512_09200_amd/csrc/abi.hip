@@ -1129,6 +1129,29 @@ static hipError_t mlp_backward_weights(const lattice_mlp_desc* d, int B, const v
   return hipSuccess;
 }
 
+// bf16, 8 elements per thread with 16-byte accesses (N, gs and as multiples
+// of 8, pointers 16-byte aligned): the gradient masked by act > 0
+__global__ __launch_bounds__(256) void relu_mask8_kernel(const bf16_t* __restrict__ g, int64_t gs,
+                                                         const bf16_t* __restrict__ act, int64_t as,
+                                                         int B, int N, bf16_t* __restrict__ out) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (i >= (int64_t)B * N) return;
+  const int64_t r = i / N, c = i - r * N;
+  const u32x4 gv = ldg16(g + r * gs + c), av = ldg16(act + r * as + c);
+  u32x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t a = av[e], v = gv[e];
+    const uint32_t lo = __uint_as_float(a << 16) > 0.f ? (v & 0xffffu) : 0u;
+    const uint32_t hi = __uint_as_float(a & 0xffff0000u) > 0.f ? (v & 0xffff0000u) : 0u;
+    o[e] = lo | hi;
+  }
+  stg16(out + i, o);
+}
+
+static hipError_t relu_mask(const void* g, int64_t gs, const void* act, int64_t as, int B, int N,
+                            bool bf, void* out, hipStream_t s);
+
 __global__ void relu_mask_kernel(const void* g, int64_t gs, const void* act, int64_t as, int B,
                                  int N, int bf, void* out) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -1142,6 +1165,19 @@ __global__ void relu_mask_kernel(const void* g, int64_t gs, const void* act, int
     const float a = ((const float*)act)[r * as + c];
     ((float*)out)[i] = a > 0.f ? ((const float*)g)[r * gs + c] : 0.f;
   }
+}
+
+static hipError_t relu_mask(const void* g, int64_t gs, const void* act, int64_t as, int B, int N,
+                            bool bf, void* out, hipStream_t s) {
+  if (B == 0 || N == 0) return hipSuccess;
+  const bool vec = bf && N % 8 == 0 && gs % 8 == 0 && as % 8 == 0 && ((uintptr_t)g & 15) == 0 &&
+                   ((uintptr_t)act & 15) == 0 && ((uintptr_t)out & 15) == 0;
+  if (vec)
+    relu_mask8_kernel<<<cdiv((int64_t)B * N / 8, 256), 256, 0, s>>>((const bf16_t*)g, gs, (const bf16_t*)act,
+                                                                   as, B, N, (bf16_t*)out);
+  else
+    relu_mask_kernel<<<cdiv((int64_t)B * N, 256), 256, 0, s>>>(g, gs, act, as, B, N, bf, out);
+  return hipGetLastError();
 }
 
 static size_t mlp_heads_ws(const lattice_mlp_desc* d, int B) {
@@ -1252,10 +1288,9 @@ lattice_status lattice_mlp_heads_bwd(const lattice_mlp_desc* desc, int32_t B, co
     g_last = masked;
     g_ld = T;
   } else if (desc->relu_last) {
-    relu_mask_kernel<<<cdiv((int64_t)B * T, 256), 256, 0, s>>>(
-        d_out, d_out_stride, acts[L - 1], act_strides[L - 1], B, T, desc->dtype == LATTICE_BF16,
-        masked);
-    if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
+    if (relu_mask(d_out, d_out_stride, acts[L - 1], act_strides[L - 1], B, T, desc->dtype == LATTICE_BF16,
+                  masked, s) != hipSuccess)
+      FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
     g_last = masked;
     g_ld = T;
   }
@@ -1273,6 +1308,9 @@ struct Plan {
   lattice_step_layout L;
   int n, T, t_stride;
   size_t gbuf_top, gbuf_bot, scratch;
+  // offset inside the dense scratch of the bottom backward's own part (it
+  // runs on the side stream while the top weight gradients use the rest)
+  size_t scratch_bottom;
   // per hidden layer i: gradient of its output [B, out_i]; g_masked: the
   // ReLU-masked gradient of the bottom MLP's output [B, dim]
   int64_t g_top[LATTICE_MAX_LAYERS], g_bot[LATTICE_MAX_LAYERS], g_masked;
@@ -1382,9 +1420,11 @@ static lattice_status make_plan(const lattice_model_desc* m, int B, int64_t nnz,
   L.grad_rows = (o && o->emit_grad_rows) ? take((size_t)nn * d * 4) : -1;
   size_t sc = 0;
   sc = std::max(sc, mlp_bwd_ws(&m->top, B));
-  if (m->dense_in > 0) sc = std::max(sc, mlp_bwd_ws(&m->bottom, B));
   sc = std::max(sc, bce_workspace((int64_t)B * P->T));
   sc = std::max(sc, head_workspace(B));
+  // the bottom backward's part follows the top's: the two run concurrently
+  P->scratch_bottom = al256(sc);
+  sc = P->scratch_bottom + (m->dense_in > 0 ? mlp_bwd_ws(&m->bottom, B) : 0);
   L.interact = take(interact_ws(&m->interact, B) + step_dot_mask_bytes(m, B));
   L.scratch = take(sc);
   L.scratch_bytes = (int64_t)sc;
@@ -1662,9 +1702,12 @@ static lattice_status step_impl(const lattice_model_desc* m, const lattice_batch
   void* dX = at(L.dX);
   HIPRET(interact_bwd_impl(&idesc, B, X, at(L.d_t), P.t_stride, dX, at(L.interact), s));
   HIPRET(end(LATTICE_STAGE_INTERACT_BWD));
-  // 8./9. The weight gradients of the top MLP and the bottom backward need
-  // nothing the sparse gradient writes: on the side stream they overlap the
-  // segmented reduction.  (Forking them before the interaction backward
+  // 8./9. The bottom backward and the weight gradients of the top MLP need
+  // nothing the sparse gradient writes.  The top weight gradients run on the
+  // caller's stream before the segmented reduction (beside the reduction they
+  // were starved of compute units: 0.59 ms against 0.17 ms alone), the
+  // bottom backward on the side stream beside them and the reduction, with a
+  // scratch part of its own.  (Forking them before the interaction backward
   // measured no faster and costs one more cross-stream event.)
   hipStream_t ws_stream = s;
   if (side) {
@@ -1678,26 +1721,26 @@ static lattice_status step_impl(const lattice_model_desc* m, const lattice_batch
   auto wend = [&](int i) -> hipError_t {
     return ev && ev[2 * i + 1] ? hipEventRecord((hipEvent_t)ev[2 * i + 1], ws_stream) : hipSuccess;
   };
-  HIPRET(wbegin(LATTICE_STAGE_TOP_WGRAD));
-  HIPRET(mlp_backward_weights(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, gtop,
-                              &tab, scratch, ws_stream, &dom));
-  HIPRET(wend(LATTICE_STAGE_TOP_WGRAD));
   // 9. bottom backward (gradient of the post-ReLU output, masked by slot 0 > 0)
   HIPRET(wbegin(LATTICE_STAGE_BOTTOM_BWD));
   if (m->dense_in > 0) {
     void* masked = at(P.g_masked);
-    relu_mask_kernel<<<cdiv((int64_t)B * d, 256), 256, 0, ws_stream>>>(
-        dX, (int64_t)n * d, X, (int64_t)n * d, B, d, dt == DT_BF16, masked);
-    if (hipGetLastError() != hipSuccess) FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
+    if (relu_mask(dX, (int64_t)n * d, X, (int64_t)n * d, B, d, dt == DT_BF16, masked, ws_stream) != hipSuccess)
+      FAIL(LATTICE_ERR_HIP, "relu mask launch failed");
     void* gbot[LATTICE_MAX_LAYERS];
     for (int i = 0; i < LATTICE_MAX_LAYERS; ++i) gbot[i] = at(P.g_bot[i]);
     const ActBufs none;
-    HIPRET(mlp_backward_data(&m->bottom, B, bacts, bstr, masked, d, nullptr, 0, gbot, &none, scratch,
+    void* bscratch = (char*)scratch + P.scratch_bottom;
+    HIPRET(mlp_backward_data(&m->bottom, B, bacts, bstr, masked, d, nullptr, 0, gbot, &none, bscratch,
                              ws_stream));
     HIPRET(mlp_backward_weights(&m->bottom, B, batch->dense, m->dense_in, bacts, bstr, masked, d,
-                                gbot, &none, scratch, ws_stream));
+                                gbot, &none, bscratch, ws_stream));
   }
   HIPRET(wend(LATTICE_STAGE_BOTTOM_BWD));
+  HIPRET(begin(LATTICE_STAGE_TOP_WGRAD));
+  HIPRET(mlp_backward_weights(&m->top, B, t, P.t_stride, tacts, tstr, at(L.d_logits_op), T, gtop,
+                              &tab, scratch, s, &dom));
+  HIPRET(end(LATTICE_STAGE_TOP_WGRAD));
   // 10. row-coalesced embedding gradient (+ row-sparse SGD) once the sort is done
   if (side) {
     HIPRET(hipEventRecord(side->done, side->s));

@@ -379,8 +379,9 @@ def test_step_side_stream_matches_single_stream(name):
     ms = [events[2 * k].elapsed_time(events[2 * k + 1]) for k in range(len(STAGES))]
     assert all(x >= 0 for x in ms), dict(zip(STAGES, ms))
     # ordering: the sort after the pooled lookups; the reduction after the
-    # interaction backward (dX) and the run bookkeeping; the weight
-    # gradients and the bottom backward after the interaction backward
+    # interaction backward (dX), the run bookkeeping and the top weight
+    # gradients (same stream); the weight gradients and the bottom backward
+    # (side stream, beside them) after the interaction backward
     i = {s: k for k, s in enumerate(STAGES)}
 
     def before(a, b):   # stage a ends before stage b begins
@@ -389,7 +390,8 @@ def test_step_side_stream_matches_single_stream(name):
     assert before("interact_bwd", "embbag_reduce")
     assert before("embbag_runs", "embbag_reduce")
     assert before("interact_bwd", "top_wgrad")
-    assert before("top_wgrad", "bottom_bwd")
+    assert before("interact_bwd", "bottom_bwd")
+    assert before("top_wgrad", "embbag_reduce")
     # a sparse event array: only the reduction's pair is recorded
     part = [None] * (2 * len(STAGES))
     part[2 * i["embbag_reduce"]] = torch.cuda.Event(enable_timing=True)
