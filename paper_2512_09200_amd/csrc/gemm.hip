@@ -41,6 +41,7 @@
 // belong to one aligned 16-lane group per 128 columns, so the sum of squares
 // is a 16-lane butterfly.
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -475,20 +476,26 @@ struct BufMN {
   }
 };
 
-// An MN-contiguous operand staged k-major (buffer path, 128-row tiles):
-// S[k][r] with r contiguous, 128 rows per k row and no padding, copied with
-// 16-byte loads and 16-byte LDS writes (no register transpose; a load
-// instruction reads four whole 256-byte k rows).  The 16-byte units of k row
-// k are XOR-swizzled by 4 (k mod 4), so that the four consecutive k rows a
-// transposed fragment read touches fall on disjoint banks.  Thread t holds
-// unit t mod 16 of k rows t / 16 + 16 i.
-constexpr int KM_LD = GBM;
-__device__ inline int km_off(int k, int r) { return k * KM_LD + ((((r >> 3) ^ ((k & 3) << 2))) << 3) + (r & 7); }
+// An MN-contiguous operand staged k-major (buffer path): S[k][r] with r
+// contiguous, ROWS rows per k row and no padding, copied with 16-byte loads
+// and 16-byte LDS writes (no register transpose; a load instruction reads
+// whole k rows: four of 256 bytes for 128-row tiles, two of 512 for 256).
+// The 16-byte units of k row k are XOR-swizzled by 4 (k mod 4), so that the
+// four consecutive k rows a transposed fragment read touches fall on
+// disjoint banks (rows start on a 256-byte boundary, and the swizzle moves
+// a 64-byte group of units to another quarter of the bank window).  Thread
+// t holds unit t mod (ROWS / 8) of k rows t / (ROWS / 8) + (THREADS * 8 /
+// ROWS) i.
+template <int LD>
+__device__ inline int km_off(int k, int r) { return k * LD + ((((r >> 3) ^ ((k & 3) << 2))) << 3) + (r & 7); }
+template <int ROWS = GBM, int THREADS = 256>
 struct BufMNK {
-  static constexpr int NV = GBM * GBK / 8 / 256;  // 4
+  static constexpr int UNITS = ROWS / 8;              // 16-byte units per k row
+  static constexpr int KPI = THREADS / UNITS;         // k rows per load instruction round
+  static constexpr int NV = ROWS * GBK / 8 / THREADS; // vectors per thread
   struct Addr {
     __amdgpu_buffer_rsrc_t rs;
-    uint32_t voff;   // byte offset of the thread's unit in k row kbeg + t / 16
+    uint32_t voff;   // byte offset of the thread's unit in k row kbeg + t / UNITS
     uint32_t kbytes;
     int kbeg;
     __device__ inline void init(const Opnd& o, int R, int kbeg_, int kend, int r0) {
@@ -497,7 +504,7 @@ struct BufMNK {
       rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(o.p), 0, (int)(uint32_t)(last * 2),
                                              BUF_RSRC_WORD3);
       kbytes = (uint32_t)(o.ld * 2);
-      const int k = kbeg + (threadIdx.x >> 4), u = threadIdx.x & 15;
+      const int k = kbeg + threadIdx.x / UNITS, u = threadIdx.x % UNITS;
       voff = (uint32_t)(((int64_t)k * o.ld + r0 + u * 8) * 2);
     }
   };
@@ -506,15 +513,15 @@ struct BufMNK {
     const uint32_t d = (uint32_t)(k0 - a.kbeg) * a.kbytes;
 #pragma unroll
     for (int i = 0; i < NV; ++i)
-      r[i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff + d + (uint32_t)(16 * i) * a.kbytes), 0, 0);
+      r[i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff + d + (uint32_t)(KPI * i) * a.kbytes), 0, 0);
   }
   __device__ inline void store(const Addr& /*a*/, bf16_t* S) {
-    const int k = threadIdx.x >> 4, u = threadIdx.x & 15;
+    const int k = threadIdx.x / UNITS, u = threadIdx.x % UNITS;
 #pragma unroll
     for (int i = 0; i < NV; ++i)
-      *reinterpret_cast<u32x4*>(S + km_off(k + 16 * i, u * 8)) = r[i];
+      *reinterpret_cast<u32x4*>(S + km_off<ROWS>(k + KPI * i, u * 8)) = r[i];
   }
-  // row sums: the thread's 8 rows over its 4 k rows of the step (k rows past
+  // row sums: the thread's 8 rows over its k rows of the step (k rows past
   // the range read zero)
   __device__ inline void rowsum(float (&rs)[8]) const {
 #pragma unroll
@@ -525,6 +532,21 @@ struct BufMNK {
       for (int e = 0; e < 8; ++e) rs[e] += v[e];
     }
   }
+  // after the K loop: row sums added over the KPI k classes in class order
+  // (LDS scratch `red` of KPI * ROWS floats; a barrier inside); thread t < ROWS
+  // returns row t's sum
+  __device__ inline static float rowsum_combine(const float (&rs)[8], float* red) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[(threadIdx.x / UNITS) * ROWS + (threadIdx.x % UNITS) * 8 + e] = rs[e];
+    __syncthreads();
+    float s = 0.f;
+    if (threadIdx.x < ROWS) {
+#pragma unroll
+      for (int c = 0; c < KPI; ++c) s += red[c * ROWS + threadIdx.x];
+    }
+    __syncthreads();
+    return s;
+  }
 };
 
 // MFMA operand fragment (32 rows from rbase, 8 k from ks) of a k-major tile
@@ -534,13 +556,14 @@ struct BufMNK {
 // rows rbase + 16 (g % 2) + 4q .. +3 of k row ks + 8 (g / 2) + e (g = lane /
 // 16), and lane j receives row rbase + lane % 32 at four consecutive k.
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+template <int LD>
 __device__ inline bf16x8 frag_km(const bf16_t* S, int rbase, int ks, int lane) {
   const int g = lane >> 4, j = lane & 15;
   const int r = rbase + 16 * (g & 1) + 4 * (j & 3);
   const int k = ks + 8 * (g >> 1) + (j >> 2);
   typedef __attribute__((address_space(3))) i16x4 lds_v4;
-  const lds_v4* p0 = (const lds_v4*)(S + km_off(k, r));
-  const lds_v4* p1 = (const lds_v4*)(S + km_off(k + 4, r));
+  const lds_v4* p0 = (const lds_v4*)(S + km_off<LD>(k, r));
+  const lds_v4* p1 = (const lds_v4*)(S + km_off<LD>(k + 4, r));
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_v4*>(p0));
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_v4*>(p1));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -573,7 +596,7 @@ template <bool MN> struct LoaderSel<MN, false> { using T = LoadElem<MN>; };
 // the register stage of an operand: buffer loaders (BUF) or plain ones
 template <bool MN, bool VEC, bool BUF> struct StageSel { using T = PlainStage<typename LoaderSel<MN, VEC>::T>; };
 template <> struct StageSel<false, true, true> { using T = BufK<>; };
-template <> struct StageSel<true, true, true> { using T = BufMNK; };
+template <> struct StageSel<true, true, true> { using T = BufMNK<>; };
 
 // 64 k of MFMAs on the staged tiles: each wave 2x2 fragments of 32x32.
 // KA / KB: that operand's tile is k-major (transposed fragment reads).
@@ -585,10 +608,10 @@ __device__ inline void mma_k64(const bf16_t* As, const bf16_t* Bs, int wm, int w
   const bf16_t* bs = Bs + (wn * 64 + frow) * GLD + fk;
 #pragma unroll
   for (int ks = 0; ks < GBK; ks += 16) {
-    const bf16x8 a0 = KA ? frag_km(As, wm * 64, ks, lane) : *reinterpret_cast<const bf16x8*>(as + ks);
-    const bf16x8 a1 = KA ? frag_km(As, wm * 64 + 32, ks, lane) : *reinterpret_cast<const bf16x8*>(as + 32 * GLD + ks);
-    const bf16x8 b0 = KB ? frag_km(Bs, wn * 64, ks, lane) : *reinterpret_cast<const bf16x8*>(bs + ks);
-    const bf16x8 b1 = KB ? frag_km(Bs, wn * 64 + 32, ks, lane) : *reinterpret_cast<const bf16x8*>(bs + 32 * GLD + ks);
+    const bf16x8 a0 = KA ? frag_km<GBM>(As, wm * 64, ks, lane) : *reinterpret_cast<const bf16x8*>(as + ks);
+    const bf16x8 a1 = KA ? frag_km<GBM>(As, wm * 64 + 32, ks, lane) : *reinterpret_cast<const bf16x8*>(as + 32 * GLD + ks);
+    const bf16x8 b0 = KB ? frag_km<GBN>(Bs, wn * 64, ks, lane) : *reinterpret_cast<const bf16x8*>(bs + ks);
+    const bf16x8 b1 = KB ? frag_km<GBN>(Bs, wn * 64 + 32, ks, lane) : *reinterpret_cast<const bf16x8*>(bs + 32 * GLD + ks);
     acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
     acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
     acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
@@ -756,18 +779,9 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   if (rs_on) {
     int row;
     if constexpr (KA) {
-      // the 16 k classes of each row added in class order (LDS is free: the
+      // the k classes of each row added in class order (LDS is free: the
       // loop ended with a barrier)
-      float* red = reinterpret_cast<float*>(gemm_smem);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) red[(threadIdx.x >> 4) * GBM + (threadIdx.x & 15) * 8 + e] = rsv[e];
-      __syncthreads();
-      if (threadIdx.x < GBM) {
-        rs = 0.f;
-#pragma unroll
-        for (int c = 0; c < 16; ++c) rs += red[c * GBM + threadIdx.x];
-      }
-      __syncthreads();
+      rs = BufMNK<>::rowsum_combine(rsv, reinterpret_cast<float*>(gemm_smem));
       row = threadIdx.x < GBM ? m0 + threadIdx.x : M;
     } else {
       rs += __shfl_xor(rs, 1, 64);  // the two halves of the row, in a fixed order
@@ -884,9 +898,9 @@ template <bool MN, int THREADS, bool BUF> struct BigLoader;
 template <int THREADS> struct BigLoader<false, THREADS, false> { using T = PlainStage<LoadK<BBM, THREADS>>; };
 template <int THREADS> struct BigLoader<true, THREADS, false> { using T = PlainStage<LoadMN<BBM, THREADS>>; };
 template <int THREADS> struct BigLoader<false, THREADS, true> { using T = BufK<BBM, THREADS>; };
-template <int THREADS> struct BigLoader<true, THREADS, true> { using T = BufMN<BBM, THREADS>; };
+template <int THREADS> struct BigLoader<true, THREADS, true> { using T = BufMNK<BBM, THREADS>; };
 
-template <int FN>
+template <int FN, bool KA = false, bool KB = false>
 __device__ inline void mma_big_k64(const bf16_t* As, const bf16_t* Bs, int wm, int wn, int lane,
                                    f32x16 (&acc)[4][FN]) {
   const int frow = lane & 31, fk = (lane >> 5) * 8;
@@ -896,9 +910,11 @@ __device__ inline void mma_big_k64(const bf16_t* As, const bf16_t* Bs, int wm, i
   for (int ks = 0; ks < GBK; ks += 16) {
     bf16x8 a[4], b[FN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8*>(as + i * 32 * GLD + ks);
+    for (int i = 0; i < 4; ++i)
+      a[i] = KA ? frag_km<BBM>(As, wm * 128 + i * 32, ks, lane) : *reinterpret_cast<const bf16x8*>(as + i * 32 * GLD + ks);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) b[j] = *reinterpret_cast<const bf16x8*>(bs + j * 32 * GLD + ks);
+    for (int j = 0; j < FN; ++j)
+      b[j] = KB ? frag_km<BBN>(Bs, wn * FN * 32 + j * 32, ks, lane) : *reinterpret_cast<const bf16x8*>(bs + j * 32 * GLD + ks);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -935,8 +951,14 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, C
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  using SA = typename BigLoader<TA, THREADS, BUF>::T;
-  using SB = typename BigLoader<TB, THREADS, BUF>::T;
+  // k-major staging for B when M-contiguous, for A only when B is too (A
+  // k-major beside a K-contiguous B, or both k-major, costs registers in the
+  // K loop); otherwise the register transpose
+  constexpr bool KA = BUF && TA && TB, KB = BUF && TB && !TA;
+  using SA = typename std::conditional<BUF && TA && !KA, BufMN<BBM, THREADS>,
+                                       typename BigLoader<TA, THREADS, BUF>::T>::type;
+  using SB = typename std::conditional<BUF && TB && !KB, BufMN<BBM, THREADS>,
+                                       typename BigLoader<TB, THREADS, BUF>::T>::type;
   typename SA::Addr adA;
   typename SB::Addr adB;
   adA.init(A, M, 0, K, m0);
@@ -956,8 +978,17 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, C
   constexpr int TPR = THREADS / BBM;
   const bool rs_on = rowsum != nullptr && n0 == 0;
   float rs = 0.f;
+  float rsv[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) rsv[e] = 0.f;
+  auto stage_a = [&](auto& la, bf16_t* S) {
+    if constexpr (KA) {
+      if (rs_on) la.rowsum(rsv);
+    }
+    la.store(adA, S);
+  };
   auto rowsum_step = [&](const bf16_t* as) {
-    if (rs_on) {
+    if (!KA && rs_on) {
       const bf16_t* p = as + (threadIdx.x / TPR) * GLD + (threadIdx.x % TPR) * (GBK / TPR);
 #pragma unroll
       for (int v = 0; v < GBK / TPR / 8; ++v) {
@@ -973,36 +1004,42 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, C
   if (ktiles > 0) load(la0, lb0, 0);
   if (ktiles > 1) load(la1, lb1, 1);
   if (ktiles > 0) {
-    la0.store(adA, As[0]);
+    stage_a(la0, As[0]);
     lb0.store(adB, Bs[0]);
   }
   __syncthreads();
   int kt = 0;
   for (; kt + 2 <= ktiles; kt += 2) {
     if (kt + 2 < ktiles) load(la0, lb0, kt + 2);
-    mma_big_k64<FN>(As[0], Bs[0], wm, wn, lane, acc);
+    mma_big_k64<FN, KA, KB>(As[0], Bs[0], wm, wn, lane, acc);
     rowsum_step(As[0]);
-    la1.store(adA, As[1]);
+    stage_a(la1, As[1]);
     lb1.store(adB, Bs[1]);
     __syncthreads();
     if (kt + 3 < ktiles) load(la1, lb1, kt + 3);
-    mma_big_k64<FN>(As[1], Bs[1], wm, wn, lane, acc);
+    mma_big_k64<FN, KA, KB>(As[1], Bs[1], wm, wn, lane, acc);
     rowsum_step(As[1]);
     if (kt + 2 < ktiles) {
-      la0.store(adA, As[0]);
+      stage_a(la0, As[0]);
       lb0.store(adB, Bs[0]);
     }
     __syncthreads();
   }
   if (kt < ktiles) {
-    mma_big_k64<FN>(As[0], Bs[0], wm, wn, lane, acc);
+    mma_big_k64<FN, KA, KB>(As[0], Bs[0], wm, wn, lane, acc);
     rowsum_step(As[0]);
     __syncthreads();
   }
   if (rs_on) {
-    if (TPR == 2) rs += __shfl_xor(rs, 1, 64);  // the two halves of the row, fixed order
-    const int row = m0 + threadIdx.x / TPR;
-    if (threadIdx.x % TPR == 0 && row < M) rowsum[row] = rs;
+    if constexpr (KA) {
+      rs = BufMNK<BBM, THREADS>::rowsum_combine(rsv, reinterpret_cast<float*>(gemm_smem));
+      const int row = m0 + threadIdx.x;
+      if (threadIdx.x < BBM && row < M) rowsum[row] = rs;
+    } else {
+      if (TPR == 2) rs += __shfl_xor(rs, 1, 64);  // the two halves of the row, fixed order
+      const int row = m0 + threadIdx.x / TPR;
+      if (threadIdx.x % TPR == 0 && row < M) rowsum[row] = rs;
+    }
   }
 
   // epilogue in two halves of 128 rows: the waves of row half h stage their
