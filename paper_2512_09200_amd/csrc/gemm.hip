@@ -20,7 +20,15 @@
 // staged k-major (16-byte copies of whole k rows, no register transpose) and
 // its MFMA fragments are read with gfx950's transposed LDS reads
 // (ds_read_b64_tr_b16): the weight-gradient product of top layer 1 went from
-// 105 to 73 us, its input gradient from 71 to 61 us.  Global loads run two K steps ahead of the MFMAs (two
+// 105 to 73 us, its input gradient from 71 to 61 us.  On the buffer path the
+// K loop runs unchecked while four more tiles remain (no K tail, no
+// conditional load or store, one basic block), and the next tile's global
+// loads and the other LDS stage's stores are issued in four parts, each after
+// one 16-k slice of MFMAs and fenced there against the scheduler (which
+// otherwise gathers the loads at the end of the step and shortens the
+// prefetch): the 256x256 products of the deep stack went from 4.7-4.8 to
+// 3.7-3.9 ms, top layer 1 forward 52.7 -> 48 us; the last tiles finish in
+// the checked loop.  Global loads run two K steps ahead of the MFMAs (two
 // register stages, two LDS stages).  Tiles are numbered so that each XCD works
 // through whole row panels of A (one L2 keeps the panel while the XCD sweeps
 // the columns).  The finished tile is staged through LDS as fp32 so that the
@@ -426,6 +434,26 @@ struct BufK {
 #pragma unroll
     for (int i = 0; i < NV; ++i) r[i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff[i] + d), 0, 0);
   }
+  // part p of P of a load or of an LDS store (the unchecked loop, whose
+  // tiles have no K tail); the load records the tile for store()
+  __device__ inline void load_part(const Addr& a, int k0, int p, int P) {
+    if (p == 0) {
+      k0_ = k0;
+      tail_ = k0 + GBK > a.kend;
+    }
+    const uint32_t d = (uint32_t)(k0 - a.kbeg) * 2u;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (i * P / NV == p) r[i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff[i] + d), 0, 0);
+  }
+  __device__ inline void store_part(const Addr& /*a*/, bf16_t* S, int p, int P) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (i * P / NV != p) continue;
+      const int v = threadIdx.x + i * THREADS;
+      *reinterpret_cast<u32x4*>(S + (v >> 3) * GLD + (v & 7) * 8) = r[i];
+    }
+  }
   __device__ inline void store(const Addr& a, bf16_t* S) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
@@ -459,13 +487,23 @@ struct BufMN {
       for (int i = 0; i < 4; ++i)
         r[q][i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff[q] + d + (uint32_t)i * a.kbytes), 0, 0);
   }
-  __device__ inline void store(const Addr& /*a*/, bf16_t* S) {
+  __device__ inline void load_part(const Addr& a, int k0, int p, int P) {
+    const uint32_t d = (uint32_t)(k0 - a.kbeg) * a.kbytes;
+#pragma unroll
+    for (int q = 0; q < NI; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if ((q * 4 + i) * P / (4 * NI) == p)
+          r[q][i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff[q] + d + (uint32_t)i * a.kbytes), 0, 0);
+  }
+  __device__ inline void store_part(const Addr& /*a*/, bf16_t* S, int p, int P) {
 #pragma unroll
     for (int q = 0; q < NI; ++q) {
       const int it = threadIdx.x + q * THREADS;
       bf16_t* s = S + ((it >> 4) * 8) * GLD + (it & 15) * 4;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
+        if ((q * 8 + j) * P / (8 * NI) != p) continue;
         // row j of the group: (k0, k1, k2, k3) = half (j & 1) of word j/2 of the four vectors
         const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
         const uint32_t lo = __builtin_amdgcn_perm(r[q][1][j >> 1], r[q][0][j >> 1], sel);
@@ -473,6 +511,10 @@ struct BufMN {
         *reinterpret_cast<uint2*>(s + j * GLD) = uint2{lo, hi};
       }
     }
+  }
+  __device__ inline void store(const Addr& a, bf16_t* S) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) store_part(a, S, p, 4);
   }
 };
 
@@ -515,11 +557,22 @@ struct BufMNK {
     for (int i = 0; i < NV; ++i)
       r[i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff + d + (uint32_t)(KPI * i) * a.kbytes), 0, 0);
   }
-  __device__ inline void store(const Addr& /*a*/, bf16_t* S) {
+  __device__ inline void load_part(const Addr& a, int k0, int p, int P) {
+    const uint32_t d = (uint32_t)(k0 - a.kbeg) * a.kbytes;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (i * P / NV == p)
+        r[i] = __builtin_amdgcn_raw_buffer_load_b128(a.rs, (int)(a.voff + d + (uint32_t)(KPI * i) * a.kbytes), 0, 0);
+  }
+  __device__ inline void store_part(const Addr& /*a*/, bf16_t* S, int p, int P) {
     const int k = threadIdx.x / UNITS, u = threadIdx.x % UNITS;
 #pragma unroll
     for (int i = 0; i < NV; ++i)
-      *reinterpret_cast<u32x4*>(S + km_off<ROWS>(k + KPI * i, u * 8)) = r[i];
+      if (i * P / NV == p) *reinterpret_cast<u32x4*>(S + km_off<ROWS>(k + KPI * i, u * 8)) = r[i];
+  }
+  __device__ inline void store(const Addr& a, bf16_t* S) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) store_part(a, S, p, 4);
   }
   // row sums: the thread's 8 rows over its k rows of the step (k rows past
   // the range read zero)
@@ -600,9 +653,14 @@ template <> struct StageSel<true, true, true> { using T = BufMNK<>; };
 
 // 64 k of MFMAs on the staged tiles: each wave 2x2 fragments of 32x32.
 // KA / KB: that operand's tile is k-major (transposed fragment reads).
-template <bool KA = false, bool KB = false>
+struct NoSide {
+  __device__ inline void operator()(int) const {}
+};
+// side(q), q = 0..3, runs after the MFMAs of 16-k slice q (the next tile's
+// loads and the other LDS stage's stores, overlapping the matrix work)
+template <bool KA = false, bool KB = false, typename Side = NoSide>
 __device__ inline void mma_k64(const bf16_t* As, const bf16_t* Bs, int wm, int wn, int lane,
-                               f32x16 (&acc)[2][2]) {
+                               f32x16 (&acc)[2][2], Side side = Side()) {
   const int frow = lane & 31, fk = (lane >> 5) * 8;
   const bf16_t* as = As + (wm * 64 + frow) * GLD + fk;
   const bf16_t* bs = Bs + (wn * 64 + frow) * GLD + fk;
@@ -616,6 +674,8 @@ __device__ inline void mma_k64(const bf16_t* As, const bf16_t* Bs, int wm, int w
     acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
     acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
     acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+    side(ks / 16);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -755,6 +815,36 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   // The loop body is two steps with no early exit (so the accumulators keep
   // their registers); an odd last step follows the loop.
   int kt = 0;
+  if constexpr (BUF) {
+    // unchecked steady state while tiles kt .. kt + 3 exist (no K tail, no
+    // conditional load or store): the next tile's loads and the other
+    // stage's stores are issued between the MFMA slices
+    for (; kt + 4 <= ktiles; kt += 2) {
+      const int k2 = kbeg + (kt + 2) * GBK, k3 = k2 + GBK;
+      mma_k64<KA, KB>(As[0], Bs[0], wm, wn, lane, acc, [&](int q) {
+        la0.load_part(adA, k2, q, 4);
+        lb0.load_part(adB, k2, q, 4);
+        if constexpr (KA) {
+          if (q == 0 && rs_on) la1.rowsum(rsv);
+        }
+        la1.store_part(adA, As[1], q, 4);
+        lb1.store_part(adB, Bs[1], q, 4);
+      });
+      rowsum_step(As[0]);
+      __syncthreads();
+      mma_k64<KA, KB>(As[1], Bs[1], wm, wn, lane, acc, [&](int q) {
+        la1.load_part(adA, k3, q, 4);
+        lb1.load_part(adB, k3, q, 4);
+        if constexpr (KA) {
+          if (q == 0 && rs_on) la0.rowsum(rsv);
+        }
+        la0.store_part(adA, As[0], q, 4);
+        lb0.store_part(adB, Bs[0], q, 4);
+      });
+      rowsum_step(As[1]);
+      __syncthreads();
+    }
+  }
   for (; kt + 2 <= ktiles; kt += 2) {
     if (kt + 2 < ktiles) load(la0, lb0, kt + 2);
     mma_k64<KA, KB>(As[0], Bs[0], wm, wn, lane, acc);
@@ -900,9 +990,9 @@ template <int THREADS> struct BigLoader<true, THREADS, false> { using T = PlainS
 template <int THREADS> struct BigLoader<false, THREADS, true> { using T = BufK<BBM, THREADS>; };
 template <int THREADS> struct BigLoader<true, THREADS, true> { using T = BufMNK<BBM, THREADS>; };
 
-template <int FN, bool KA = false, bool KB = false>
+template <int FN, bool KA = false, bool KB = false, typename Side = NoSide>
 __device__ inline void mma_big_k64(const bf16_t* As, const bf16_t* Bs, int wm, int wn, int lane,
-                                   f32x16 (&acc)[4][FN]) {
+                                   f32x16 (&acc)[4][FN], Side side = Side()) {
   const int frow = lane & 31, fk = (lane >> 5) * 8;
   const bf16_t* as = As + (wm * 128 + frow) * GLD + fk;
   const bf16_t* bs = Bs + (wn * FN * 32 + frow) * GLD + fk;
@@ -920,6 +1010,8 @@ __device__ inline void mma_big_k64(const bf16_t* As, const bf16_t* Bs, int wm, i
 #pragma unroll
       for (int j = 0; j < FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    side(ks / 16);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -1009,6 +1101,34 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_big_kernel(Opnd A, Opnd Bm, C
   }
   __syncthreads();
   int kt = 0;
+  if constexpr (BUF) {
+    // unchecked steady state, as in the 128x128 kernel
+    for (; kt + 4 <= ktiles; kt += 2) {
+      const int k2 = (kt + 2) * GBK, k3 = k2 + GBK;
+      mma_big_k64<FN, KA, KB>(As[0], Bs[0], wm, wn, lane, acc, [&](int q) {
+        la0.load_part(adA, k2, q, 4);
+        lb0.load_part(adB, k2, q, 4);
+        if constexpr (KA) {
+          if (q == 0 && rs_on) la1.rowsum(rsv);
+        }
+        la1.store_part(adA, As[1], q, 4);
+        lb1.store_part(adB, Bs[1], q, 4);
+      });
+      rowsum_step(As[0]);
+      __syncthreads();
+      mma_big_k64<FN, KA, KB>(As[1], Bs[1], wm, wn, lane, acc, [&](int q) {
+        la1.load_part(adA, k3, q, 4);
+        lb1.load_part(adB, k3, q, 4);
+        if constexpr (KA) {
+          if (q == 0 && rs_on) la0.rowsum(rsv);
+        }
+        la0.store_part(adA, As[0], q, 4);
+        lb0.store_part(adB, Bs[0], q, 4);
+      });
+      rowsum_step(As[1]);
+      __syncthreads();
+    }
+  }
   for (; kt + 2 <= ktiles; kt += 2) {
     if (kt + 2 < ktiles) load(la0, lb0, kt + 2);
     mma_big_k64<FN, KA, KB>(As[0], Bs[0], wm, wn, lane, acc);
