@@ -1266,9 +1266,10 @@ static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 // Split-K factor by an estimated time: ceil(blocks / 512) waves (two blocks
 // per CU) of K / s each, in K steps, plus the fp32 partials each split writes
-// and the reduction reads back (2 * 4 * M * N bytes at ~5 TB/s, against
-// ~1.8 us per wave and K step), so any factor (not only powers of two) that
-// balances the waves is considered; ties keep fewer splits.
+// and the reduction reads back, M * N / 375000 K steps per split (fitted to
+// the step's weight-gradient products at K = 8192: the 512 x 1024 product
+// takes 26 us at 8 splits and 32 us at 16), so any factor (not only powers
+// of two) that balances the waves is considered; ties keep fewer splits.
 int gemm_splits(const GemmArgs& g) {
   if (g.dt != DT_BF16 || g.batch > 1 || g.max_splits <= 1) return 1;
   const int64_t tiles = (int64_t)cdiv(g.M, GBM) * cdiv(g.N, GBN);
@@ -1280,7 +1281,7 @@ int gemm_splits(const GemmArgs& g) {
     if ((int64_t)(s - 1) * kps >= g.K) continue;  // the last split would be empty
     const double waves = (double)cdiv(tiles * s, (int64_t)512);
     const double cost = waves * (double)(kps / GBK) +
-                        (s > 1 ? (double)s * g.M * g.N / 1.125e6 : 0.0);
+                        (s > 1 ? (double)s * g.M * g.N / 3.75e5 : 0.0);
     if (s == 1 || cost < 0.98 * best) {
       best = cost;
       best_s = s;
