@@ -972,7 +972,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   epi_store<CT>(C, ldc, row, col, sum_splits(partial + i, splits, (int64_t)M * N), epi, 0);
 }
 
-// --- large products: block tile 256x256, 4 waves of 128x128 (4x4 fragments) ---
+// --- large products: block tile 256x256, 4 waves of 128x128 (4x4 fragments) or 8 of 128x64 ---
 // Twice the MFMA work per byte read from LDS of the 128x128 kernel (whose
 // 64x64 wave tiles keep the LDS port as busy as the matrix cores), for
 // products with enough 256x256 tiles to fill the chip.  Same staging (two
@@ -1348,7 +1348,11 @@ static bool gemm_use_buf(const GemmArgs& g) {
 
 template <bool TA, bool TB, int NORM>
 static hipError_t gemm_big_launch(const GemmArgs& g, hipStream_t st) {
-  constexpr int NW = 4;  // 8 waves of 128x64 measured slower
+  // 8 waves of 128 x 64 (two per SIMD) where both operands load without the
+  // register transpose or one is staged k-major: 3% faster than 4 waves of
+  // 128 x 128 on the deep stack's projection products; with both operands
+  // M-contiguous the 8-wave kernel spills (51 VGPRs) and 4 waves stay
+  constexpr int NW = (TA && TB) ? 4 : 8;
   Epi epi = make_epi(g);
   Opnd a{(const bf16_t*)g.A, g.lda, g.kseg, g.ksA};
   Opnd b{(const bf16_t*)g.B, g.ldb, g.kseg, g.ksB};
