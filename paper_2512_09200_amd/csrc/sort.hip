@@ -14,6 +14,8 @@
 // implemented here from its description; tiles take their ids in the order
 // they start, so every tile looked back at is running and publishes without
 // waiting).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -226,7 +228,7 @@ __device__ inline uint32_t lb_load(const uint32_t* p) {
 // (local rows) and vals_in is unused: the keys become global rows (+ row_base
 // of the segment) and the values the bag ids, expanded from the offsets of the
 // bags the tile covers (tile_bag0: the first of them).
-template <bool FIRST>
+template <bool FIRST, int DB>
 __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
     const int* __restrict__ keys_in, const int* __restrict__ vals_in,
     const int* __restrict__ tile_bag0, const int32_t* __restrict__ offsets,
@@ -253,8 +255,8 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
   }
   __syncthreads();
   const int tix = s_tix;
-  const int radix = 1 << dbits;
-  const int shift = pass * dbits;
+  constexpr int radix = 1 << DB;  // the digit width is a template argument (dbits == DB)
+  const int shift = pass * DB;
   SegTile t;
   seg_tile(tix, tile_base, tile_seg, offsets, row_base, B, t);
   const int key0 = (int)t.key0;
@@ -299,11 +301,20 @@ __global__ __launch_bounds__(SORT_THREADS) void radix_scatter_seg_kernel(
     const int k = cbase + r * 64 + lane;
     const bool valid = k < t.cnt;
     const uint32_t d = ((uint32_t)(key[r] - key0) >> shift) & (radix - 1);
-    uint64_t peers = __ballot(valid);
-    for (int b = 0; b < dbits; ++b) {
-      const uint64_t m = __ballot((d >> b) & 1u);
-      peers &= ((d >> b) & 1u) ? m : ~m;
+    // lanes whose digit equals this lane's: for each bit, the ballot of the
+    // lanes holding it set, kept where this lane's bit is set and inverted
+    // where it is clear (sb: the bit spread over a word; unrolled over the
+    // digit's bits)
+    const uint64_t vm = __ballot(valid);
+    uint32_t plo = (uint32_t)vm, phi = (uint32_t)(vm >> 32);
+#pragma unroll
+    for (int b = 0; b < DB; ++b) {
+      const uint32_t sb = (uint32_t)((int32_t)(d << (31 - b)) >> 31);
+      const uint64_t m = __ballot(sb != 0u);
+      plo &= ~((uint32_t)m ^ sb);
+      phi &= ~((uint32_t)(m >> 32) ^ sb);
     }
+    const uint64_t peers = ((uint64_t)phi << 32) | plo;
     const int before = __popcll(peers & lt_mask);
     const int cnt = __popcll(peers);
     const int base = valid ? wcnt[w][d] : 0;
@@ -443,14 +454,25 @@ hipError_t radix_sort_segments(const int32_t* indices, int64_t n, const int32_t*
     const int remaining = passes - 1 - pass;
     int* dst_k = last ? keys_out : ((remaining % 2 == 1) ? kb : keys_out);
     int* dst_v = last ? vals_out : ((remaining % 2 == 1) ? vb : vals_out);
-    if (pass == 0)
-      radix_scatter_seg_kernel<true><<<tmax, SORT_THREADS, 0, s>>>(
+    auto launch = [&](auto first, auto db) {
+      radix_scatter_seg_kernel<decltype(first)::value, decltype(db)::value><<<tmax, SORT_THREADS, 0, s>>>(
           src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, pass, dbits, tmax,
           ghist, state, tile_ctr, dst_k, dst_v);
-    else
-      radix_scatter_seg_kernel<false><<<tmax, SORT_THREADS, 0, s>>>(
-          src_k, src_v, tile_bag0, offsets, row_base, F, B, tile_base, tile_seg, pass, dbits, tmax,
-          ghist, state, tile_ctr, dst_k, dst_v);
+    };
+    auto by_width = [&](auto first) {
+      switch (dbits) {
+        case 1: launch(first, std::integral_constant<int, 1>{}); break;
+        case 2: launch(first, std::integral_constant<int, 2>{}); break;
+        case 3: launch(first, std::integral_constant<int, 3>{}); break;
+        case 4: launch(first, std::integral_constant<int, 4>{}); break;
+        case 5: launch(first, std::integral_constant<int, 5>{}); break;
+        case 6: launch(first, std::integral_constant<int, 6>{}); break;
+        case 7: launch(first, std::integral_constant<int, 7>{}); break;
+        default: launch(first, std::integral_constant<int, 8>{}); break;
+      }
+    };
+    if (pass == 0) by_width(std::true_type{});
+    else by_width(std::false_type{});
     LAT_LAUNCH_CHECK();
     src_k = dst_k; src_v = dst_v;
   }
