@@ -1340,10 +1340,14 @@ static int64_t operand_span(int64_t ld, int R, int K, bool mn) {
   if (R <= 0 || K <= 0) return 0;
   return mn ? ((int64_t)(K - 1) * ld + (R + 7) / 8 * 8) * 2 : ((int64_t)(R - 1) * ld + (K + 7) / 8 * 8) * 2;
 }
-// Buffer loaders: no K segmentation and both operands within 2 GiB.
+// Buffer loaders: no K segmentation and both operands within 2 GiB,
+// counting the 64 k rows a last K step may address past the range (their
+// byte offsets must stay below 2^32, out of the resource's range, so that
+// they read zero rather than wrap back into it).
 static bool gemm_use_buf(const GemmArgs& g) {
   const int64_t lim = (int64_t)1 << 31;
-  return g.kseg == 0 && operand_span(g.lda, g.M, g.K, g.ta) < lim && operand_span(g.ldb, g.N, g.K, g.tb) < lim;
+  auto reach = [](int64_t ld, int R, int K, bool mn) { return operand_span(ld, R, K, mn) + (mn ? 64 * ld * 2 : 128); };
+  return g.kseg == 0 && reach(g.lda, g.M, g.K, g.ta) < lim && reach(g.ldb, g.N, g.K, g.tb) < lim;
 }
 
 template <bool TA, bool TB, int NORM>
