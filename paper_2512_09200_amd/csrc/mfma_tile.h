@@ -23,6 +23,32 @@ __device__ inline void mfma_tile(f32x16& acc, const bf16_t* A, int lda, const bf
   }
 }
 
+// acc += A[32 rows from rbase][K] * B[32 rows][K]^T with A stored k-major in
+// LDS (Akm[k * ldk + r], r contiguous), read with the transposed LDS read
+// ds_read_b64_tr_b16: within each 16-lane group it returns to lane j, as its
+// element e, element j % 4 of the 8-byte piece addressed by lane 4e + j / 4,
+// so lane 4e + q addresses rows rbase + 16 (g % 2) + 4q .. +3 of k row
+// 8 (g / 2) + e (g = lane / 16) and lane j receives row rbase + lane % 32 at
+// four consecutive k; two reads make the 8-k fragment.  ldk and rbase must
+// be multiples of 4 (8-byte aligned pieces).
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+template <int K>
+__device__ inline void mfma_tile_kmA(f32x16& acc, const bf16_t* Akm, int ldk, int rbase, const bf16_t* B,
+                                     int ldb) {
+  typedef __attribute__((address_space(3))) i16x4_t lds_v4;
+  const int lane = threadIdx.x & 63, g = lane >> 4, j = lane & 15;
+  const bf16_t* a = Akm + (8 * (g >> 1) + (j >> 2)) * ldk + rbase + 16 * (g & 1) + 4 * (j & 3);
+  const bf16_t* b = B + (lane & 31) * ldb + (lane >> 5) * 8;
+#pragma unroll
+  for (int k = 0; k < K; k += 16) {
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(a + k * ldk));
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(a + (k + 4) * ldk));
+    const bf16x8 av = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    const bf16x8 bv = *reinterpret_cast<const bf16x8*>(b + k);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
+  }
+}
+
 __device__ inline void zero16(f32x16& a) {
 #pragma unroll
   for (int r = 0; r < 16; ++r) a[r] = 0.f;
