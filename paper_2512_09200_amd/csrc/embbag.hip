@@ -720,7 +720,14 @@ __global__ __launch_bounds__(256) void seg_reduce_kernel(
 // the range where it starts, slot 0 of every later range it reaches) are
 // added in range order by S interleaved streams of dim/4 lanes each, then the
 // streams are combined in stream order; the total goes to the row gradient
-// and/or the SGD update.
+// and/or the SGD update.  A wave takes FIX_U runs per round and loads their
+// index chains (run -> its row id -> run end and table row), each stream's
+// first partial sum and the table values straight-line, all in flight
+// together (a round's positions past the last run re-read its first run, and
+// a null table reads the partials in its place; neither value is used), then
+// finishes the runs one by one: each run's arithmetic is that of a wave
+// taking it alone.
+constexpr int FIX_U = 4;
 template <typename ET>
 __global__ __launch_bounds__(256) void seg_fixup_kernel(
     const int* __restrict__ span_list, const int* __restrict__ span_count,
@@ -734,44 +741,64 @@ __global__ __launch_bounds__(256) void seg_fixup_kernel(
   const int cq = lane % CL, s = lane / CL;
   const bool act = s < S;
   const int wave = blockIdx.x * 4 + (threadIdx.x >> 6), nwaves = gridDim.x * 4;
-  for (int i = wave; i < nspan; i += nwaves) {
-    const int c0 = span_list[i];
-    const int u = part_uid[c0];
-    const int end = seg_offsets[u + 1];
-    const int Q = (end - 1) / RANGE - c0 + 1;
-    f32x4 a = {0.f, 0.f, 0.f, 0.f};
-    if (act) {
-      int q = s;
-      for (; q + 3 * S < Q; q += 4 * S) {
-        f32x4 v[4];
+  const ET* eb = E ? E : reinterpret_cast<const ET*>(part);
+  for (int i0 = wave; i0 < nspan; i0 += FIX_U * nwaves) {
+    int c0[FIX_U], u[FIX_U], Q[FIX_U];
+    int64_t erow[FIX_U];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int qq = q + t * S;
-          const int64_t slot = qq == 0 ? (int64_t)c0 * 2 + 1 : (int64_t)(c0 + qq) * 2;
-          v[t] = *reinterpret_cast<const f32x4*>(part + slot * dim + cq * 4);
+    for (int t = 0; t < FIX_U; ++t) {
+      const int i = i0 + t * nwaves;
+      c0[t] = span_list[i < nspan ? i : i0];
+    }
+#pragma unroll
+    for (int t = 0; t < FIX_U; ++t) u[t] = part_uid[c0[t]];
+#pragma unroll
+    for (int t = 0; t < FIX_U; ++t) {
+      Q[t] = (seg_offsets[u[t] + 1] - 1) / RANGE - c0[t] + 1;
+      erow[t] = E ? (int64_t)unique_rows[u[t]] * dim : 0;
+    }
+    // stream s's first partial sum (q = s; the run's first slot where the
+    // run does not reach it) and the run's table values
+    f32x4 a0[FIX_U];
+    float ev[FIX_U][4];
+#pragma unroll
+    for (int t = 0; t < FIX_U; ++t) {
+      const int q = s < Q[t] ? s : 0;
+      const int64_t slot = q == 0 ? (int64_t)c0[t] * 2 + 1 : (int64_t)(c0[t] + q) * 2;
+      a0[t] = *reinterpret_cast<const f32x4*>(part + slot * dim + cq * 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ev[t][e] = ld(eb + erow[t] + cq * 4 + e);
+    }
+#pragma unroll
+    for (int t = 0; t < FIX_U; ++t) {
+      if (i0 + t * nwaves >= nspan) break;  // wave-uniform
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+      if (act && s < Q[t]) {
+        a += a0[t];
+        int q = s + S;
+        for (; q + 3 * S < Q[t]; q += 4 * S) {
+          f32x4 v[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int64_t slot = (int64_t)(c0[t] + q + k * S) * 2;
+            v[k] = *reinterpret_cast<const f32x4*>(part + slot * dim + cq * 4);
+          }
+#pragma unroll
+          for (int k = 0; k < 4; ++k) a += v[k];
         }
-#pragma unroll
-        for (int t = 0; t < 4; ++t) a += v[t];
+        for (; q < Q[t]; q += S) a += *reinterpret_cast<const f32x4*>(part + (int64_t)(c0[t] + q) * 2 * dim + cq * 4);
       }
-      for (; q < Q; q += S) {
-        const int64_t slot = q == 0 ? (int64_t)c0 * 2 + 1 : (int64_t)(c0 + q) * 2;
-        a += *reinterpret_cast<const f32x4*>(part + slot * dim + cq * 4);
+      f32x4 t4 = {0.f, 0.f, 0.f, 0.f};
+      for (int ss = 0; ss < S; ++ss) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) t4[e] += __shfl(a[e], ss * CL + cq, 64);
       }
-    }
-    f32x4 t4 = {0.f, 0.f, 0.f, 0.f};
-    for (int ss = 0; ss < S; ++ss) {
+      if (s == 0) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) t4[e] += __shfl(a[e], ss * CL + cq, 64);
-    }
-    if (s == 0) {
-      const int row = unique_rows[u];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int c = cq * 4 + e;
-        if (grad_rows) grad_rows[(int64_t)u * dim + c] = t4[e];
-        if (E) {
-          ET* p = E + (int64_t)row * dim + c;
-          st(p, ld(p) - lr * t4[e]);
+        for (int e = 0; e < 4; ++e) {
+          const int c = cq * 4 + e;
+          if (grad_rows) grad_rows[(int64_t)u[t] * dim + c] = t4[e];
+          if (E) st(E + erow[t] + c, ev[t][e] - lr * t4[e]);
         }
       }
     }
@@ -839,7 +866,9 @@ static hipError_t embbag_bwd_reduce(const int* skeys, const int* sbags, int n, c
   LAT_LAUNCH_CHECK();
   LAT_HIP_CHECK(record(1));
   LAT_HIP_CHECK(record(2));
-  const int fix_grid = grid < 2048 ? grid : 2048;
+  // every wave resident (5 blocks of 4 waves per compute unit at the
+  // kernel's 88-96 VGPRs): each then takes its runs in rounds of FIX_U
+  const int fix_grid = grid < 1280 ? grid : 1280;
   seg_fixup_kernel<ET><<<fix_grid, 256, 0, s>>>(span_list, span_count, part_uid, seg_offsets,
                                                 unique_rows, part, dim, grad_rows, (ET*)E, lr);
   LAT_LAUNCH_CHECK();
