@@ -79,7 +79,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the path has no multi-GPU sharding in this build)", file=sys.stderr)
+              "(the training step is not sharded across GPUs)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
