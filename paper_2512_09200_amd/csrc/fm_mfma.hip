@@ -68,20 +68,19 @@ struct HeadRow {
 
 // NW waves per block; TR: X is staged once (row-major) and the X^T operand
 // of P = X^T W is read from it with transposed LDS reads, so the block's LDS
-// holds no X^T copy (with 4 waves, three blocks fit a compute unit: three
-// samples in flight instead of two).
+// holds no X^T copy, and W only as W^T, the operand of P (with 4 waves,
+// three blocks fit a compute unit: three samples in flight instead of two).
 template <int NP, int D, int K, bool HEAD, int NW = 8, bool TR = false>
 __global__ __launch_bounds__(NW * 64) void fm_fwd_mfma_kernel(const bf16_t* __restrict__ X,
                                                           const bf16_t* __restrict__ W, int B,
                                                           int n, bf16_t* __restrict__ out,
                                                           int64_t ostride, int emit0) {
-  constexpr int LX = D + 8, LT = NP + 8, LP = D + 8, LR = K + 8;
+  constexpr int LX = D + 8, LT = NP + 8, LP = D + 8;
   constexpr int H = HEAD ? 1 : 0;  // rows ahead of the MFMA rows
   constexpr int THREADS = NW * 64;
   __shared__ __attribute__((aligned(16))) bf16_t Xs[NP * LX];
   __shared__ __attribute__((aligned(16))) bf16_t XT[TR ? 8 : D * LT];
   __shared__ __attribute__((aligned(16))) bf16_t PT[K * LP];
-  __shared__ __attribute__((aligned(16))) bf16_t WR[NP * LR];
   __shared__ __attribute__((aligned(16))) bf16_t WT[K * LT];
   __shared__ float X0[HEAD ? D : 1], W0[HEAD ? K : 1];
   // per-wave 32 x 32 patch: an O tile leaves as 16-byte row segments (its
@@ -90,7 +89,7 @@ __global__ __launch_bounds__(NW * 64) void fm_fwd_mfma_kernel(const bf16_t* __re
   constexpr int LQ = 32 + 8;
   constexpr int OT = (NP / 32) * (K / 32);  // O tiles (OT <= 8), one patch per wave that has one
   constexpr int NQ = OT < NW ? OT : NW;
-  constexpr size_t BASE = 2 * ((size_t)NP * LX + (TR ? 0 : D * LT) + K * LP + NP * LR + K * LT) +
+  constexpr size_t BASE = 2 * ((size_t)NP * LX + (TR ? 0 : D * LT) + K * LP + K * LT) +
                           4 * ((HEAD ? D : 1) + (HEAD ? K : 1));
   constexpr bool VEC = BASE + (size_t)NQ * 2 * 32 * LQ <= 80 * 1024;
   __shared__ __attribute__((aligned(16))) bf16_t OQ[VEC ? NQ : 1][VEC ? 32 * LQ : 8];
@@ -100,7 +99,7 @@ __global__ __launch_bounds__(NW * 64) void fm_fwd_mfma_kernel(const bf16_t* __re
   {
     Stager<NP, K, THREADS> sw;
     sw.load(W + H * K, K, nm);
-    sw.store(WR, LR, WT, LT, nm);
+    sw.store(nullptr, 0, WT, LT, nm);  // only W^T is an operand here
     if (HEAD)
       for (int c = threadIdx.x; c < K; c += blockDim.x) W0[c] = bf2f(W[c]);
   }
@@ -827,9 +826,9 @@ static hipError_t fm_mfma_launch(bool fwd, const void* X, const void* W, int B, 
     if (B == 0) return hipSuccess;
     // 4-wave blocks without the X^T copy where three fit a compute unit's
     // LDS (three samples in flight), else 8-wave blocks, two per unit
-    constexpr int LX = D + 8, LT = NP + 8, LP = D + 8, LR = K + 8, LQ = 40;
+    constexpr int LX = D + 8, LT = NP + 8, LP = D + 8, LQ = 40;
     constexpr int NQ4 = (NP / 32) * (K / 32) < 4 ? (NP / 32) * (K / 32) : 4;
-    constexpr size_t LDS4 = 2 * ((size_t)NP * LX + K * LP + NP * LR + K * LT) + 4 * (HEAD ? D + K : 2) +
+    constexpr size_t LDS4 = 2 * ((size_t)NP * LX + K * LP + K * LT) + 4 * (HEAD ? D + K : 2) +
                             (size_t)NQ4 * 2 * 32 * LQ;
     if constexpr (3 * LDS4 <= 160 * 1024) {
       const int fblocks = B < 3 * FM_MFMA_BLOCKS ? B : 3 * FM_MFMA_BLOCKS;
